@@ -1,0 +1,422 @@
+"""Float64 NumPy oracle of ShallowStream's query-time evidence retrieval.
+
+TEST INFRASTRUCTURE ONLY: imported by the tests, the smoke check and the
+benchmark's CPU baseline, never by the library.  It shares no code with the
+HIP path.
+
+What is computed, in the paper's order (Sec. 4.1 "Query-Agnostic Shallow Index
+Construction" and Sec. 4.2 "Query-Time Answering"):
+
+* index: per shallow layer the keys of every stored unit (Eq. shallow_streaming_cache),
+  with each unit's row range; a unit descriptor per frame (Eq. memory_key);
+  optional per-frame k-means compression of the stored rows (an extension of the
+  optional compression idea of Sec. 4.1, specified by the workload: k-means with
+  farthest-point seeding, see ``kmeans``);
+* candidates: every unit except the newest ``n_recent`` (Eq. context_partition);
+* token scores: scaled Q-K logits of the question against every candidate key
+  (Sec. 4.2, "Optional Evidence Retrieval"), per (layer, query head), with the
+  text-token queries reduced by their mean (``score_lists``);
+* top-k per list (Eq. token_vote_candidates), ties to the lower row position;
+* one vote per selected token for its unit, and the selected tokens' summed
+  scores as the unit's "attention mass" tie-breaker;
+* a vote-ranked pool of ``pool_mult * K`` units, then greedy max-min diversity in
+  descriptor space (the DivTopK of Eq. selected_evidence).
+
+Readings of points the paper leaves open are listed in the module functions'
+docstrings.  Arithmetic is float64 on bfloat16-decoded inputs: products of two
+bfloat16 values are exact in float64.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+# ---------------------------------------------------------------------------
+# bfloat16 decoding (inputs are raw 16-bit patterns)
+# ---------------------------------------------------------------------------
+
+
+def decode_bf16(bits: np.ndarray) -> np.ndarray:
+    """bfloat16 bit patterns -> float64 (exact)."""
+    b = np.ascontiguousarray(bits, dtype=np.uint16)
+    out = (b.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    if not np.all(np.isfinite(out)):
+        raise ValueError("NaN or Inf in bfloat16 input")
+    return out
+
+
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    """float64 -> nearest bfloat16 (ties to even), returned as bit patterns.
+
+    The exact float64 value is rounded once: ``x = n * 2**(e-8)`` with the
+    8-bit significand ``n`` rounded half-to-even (no detour through float32).
+    """
+    x = np.asarray(x, dtype=np.float64)
+    if not np.all(np.isfinite(x)):
+        raise ValueError("NaN or Inf cannot be rounded to bfloat16")
+    a = np.abs(x)
+    _, e = np.frexp(a)                               # a = m * 2**e, m in [0.5, 1)
+    e = np.maximum(e, -125)                          # below the normal range the quantum is fixed
+    q = np.ldexp(1.0, e - 8)
+    n = a / q                                        # exact: scaling by a power of two
+    fl = np.floor(n)
+    r = n - fl
+    up = (r > 0.5) | ((r == 0.5) & (np.fmod(fl, 2.0) == 1.0))
+    y = (fl + up) * q
+    if np.any(y >= 2.0 ** 128):
+        raise OverflowError("value overflows bfloat16")
+    bits = (y.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    return np.where(np.signbit(x), bits | np.uint16(0x8000), bits).astype(np.uint16)
+
+
+# ---------------------------------------------------------------------------
+# Unit descriptor (Eq. memory_key)
+# ---------------------------------------------------------------------------
+
+
+def descriptor(last_layer_keys: np.ndarray) -> np.ndarray:
+    """Eq. memory_key: mean over the unit's raw visual tokens of the final shallow
+    layer keys, all KV heads flattened head-major, then L2-normalised.
+
+    ``last_layer_keys``: float64 ``[H_kv][T][d]``.  Returns ``[H_kv * d]``.
+    A zero mean stays zero (the normalisation is undefined there).
+    """
+    Hk, T, d = last_layer_keys.shape
+    mean = last_layer_keys.mean(axis=1)          # [H_kv][d]
+    vec = mean.reshape(Hk * d)                   # vec(): head-major flatten
+    n = np.sqrt(np.dot(vec, vec))
+    return vec / n if n > 0 else vec
+
+
+# ---------------------------------------------------------------------------
+# Per-frame k-means compression (compression at append time)
+# ---------------------------------------------------------------------------
+
+
+def kmeans(X: np.ndarray, n_centroids: int, n_iters: int):
+    """k-means of one frame's tokens at one (layer, KV head).
+
+    Readings (the paper's own compression clusters whole units over time; this
+    per-frame token rule is the workload's):
+      * squared Euclidean distance;
+      * farthest-point initialisation: the first centre is the token farthest
+        from the frame mean, each next one the not-yet-chosen token with the
+        largest distance to its nearest chosen centre; ties to the lower index;
+      * exactly ``n_iters`` rounds of (assign to nearest centre, ties to the
+        lower centre index; move each centre to the mean of its members, an
+        empty centre stays where it is);
+      * ``min(n_centroids, T)`` centres in farthest-point order;
+      * counts are the member counts of the last assignment.
+
+    Returns ``(centres [c][d] float64, counts [c] int, diag)`` where ``diag``
+    holds the smallest relative decision margins: ``init_margin`` over the
+    farthest-point argmax decisions and ``assign_margin`` over every point's
+    nearest-centre decision in every round.
+    """
+    X = np.asarray(X, dtype=np.float64)
+    T, d = X.shape
+    c = min(n_centroids, T)
+    mu = X.mean(axis=0)
+    d_mu = ((X - mu) ** 2).sum(axis=1)
+    init_margin = _argmax_margin(d_mu, np.ones(T, dtype=bool))
+    first = int(np.argmax(d_mu))                 # first index of the maximum
+    chosen = [first]
+    is_chosen = np.zeros(T, dtype=bool)
+    is_chosen[first] = True
+    mind = ((X - X[first]) ** 2).sum(axis=1)
+    while len(chosen) < c:
+        avail = ~is_chosen
+        init_margin = min(init_margin, _argmax_margin(mind, avail))
+        cand = np.where(avail, mind, -np.inf)
+        nxt = int(np.argmax(cand))
+        chosen.append(nxt)
+        is_chosen[nxt] = True
+        mind = np.minimum(mind, ((X - X[nxt]) ** 2).sum(axis=1))
+    C = X[chosen].copy()
+    assign_margin = np.inf
+    assign = np.zeros(T, dtype=np.int64)
+    sse = []
+    for _ in range(n_iters):
+        D = ((X[:, None, :] - C[None, :, :]) ** 2).sum(axis=2)   # [T][c]
+        assign = np.argmin(D, axis=1)                              # ties -> lower centre
+        if c > 1:
+            part = np.sort(D, axis=1)
+            best, second = part[:, 0], part[:, 1]
+            with np.errstate(divide="ignore", invalid="ignore"):
+                rel = np.where(second > 0, (second - best) / second, np.inf)
+            assign_margin = min(assign_margin, float(rel.min()))
+        sse.append(float(D[np.arange(T), assign].sum()))
+        for j in range(c):
+            members = assign == j
+            if members.any():
+                C[j] = X[members].mean(axis=0)
+    counts = np.bincount(assign, minlength=c)[:c] if n_iters > 0 else np.zeros(c, dtype=np.int64)
+    diag = {"init_margin": init_margin, "assign_margin": assign_margin, "sse": sse,
+            "order": chosen}
+    return C, counts, diag
+
+
+def _argmax_margin(v: np.ndarray, avail: np.ndarray) -> float:
+    vals = np.sort(v[avail])[::-1]
+    if vals.size < 2 or vals[0] <= 0:
+        return np.inf if vals.size < 2 else 0.0
+    return float((vals[0] - vals[1]) / vals[0])
+
+
+# ---------------------------------------------------------------------------
+# The index (Eq. shallow_streaming_cache, Eq. memory_key, Eq. context_partition)
+# ---------------------------------------------------------------------------
+
+
+class Index:
+    """Shallow-layer key index of one stream.
+
+    Rows of layer ``l`` and KV head ``g`` are kept as bfloat16 bit patterns in
+    append order; frame ``t`` owns rows ``[row_start[t], row_start[t] + row_count[t])``
+    in every (layer, KV head).  Frame ids are append order, from 0.
+    """
+
+    def __init__(self, n_layers: int, n_q_heads: int, n_kv_heads: int, head_dim: int,
+                 n_recent: int = 0):
+        if n_q_heads % n_kv_heads:
+            raise ValueError("query heads must be a multiple of KV heads")
+        self.L, self.Hq, self.Hk, self.d = n_layers, n_q_heads, n_kv_heads, head_dim
+        self.G = n_q_heads // n_kv_heads
+        self.n_recent = n_recent
+        self._chunks = [[] for _ in range(n_layers)]    # per layer: list of [H_kv][r][d] uint16
+        self._rows_cache = None
+        self.row_start: list[int] = []
+        self.row_count: list[int] = []
+        self.desc: list[np.ndarray] = []
+        self.counts: list[np.ndarray] = []               # per frame [L][H_kv][rows] member counts
+        self.kmeans_diag: list = []
+
+    @property
+    def n_frames(self) -> int:
+        return len(self.row_start)
+
+    @property
+    def n_rows(self) -> int:
+        return (self.row_start[-1] + self.row_count[-1]) if self.row_start else 0
+
+    def append(self, layer_keys, n_frames: int, n_tokens: int, compress=None) -> int:
+        """Append ``n_frames`` frames of ``n_tokens`` tokens.
+
+        ``layer_keys``: per layer a ``uint16 [H_kv][n_frames * n_tokens][d]`` array.
+        ``compress``: ``None`` or ``(n_centroids, n_iters)``.
+        The descriptor always uses the raw keys of the last shallow layer.
+        """
+        if len(layer_keys) != self.L:
+            raise ValueError("one key array per shallow layer expected")
+        for a in layer_keys:
+            if a.shape != (self.Hk, n_frames * n_tokens, self.d):
+                raise ValueError(f"bad key array shape {a.shape}")
+        first = self.n_frames
+        T = n_tokens
+        for f in range(n_frames):
+            sl = slice(f * T, (f + 1) * T)
+            last = decode_bf16(layer_keys[self.L - 1][:, sl, :])
+            self.desc.append(descriptor(last))
+            if compress is None:
+                rows = [layer_keys[l][:, sl, :] for l in range(self.L)]
+                cnt = np.ones((self.L, self.Hk, T), dtype=np.int64)
+                diag = None
+            else:
+                n_c, n_it = compress
+                c_eff = min(n_c, T)
+                rows, cnt, diag = [], np.zeros((self.L, self.Hk, c_eff), dtype=np.int64), []
+                for l in range(self.L):
+                    r = np.empty((self.Hk, c_eff, self.d), dtype=np.uint16)
+                    x = decode_bf16(layer_keys[l][:, sl, :])
+                    for g in range(self.Hk):
+                        C, counts, dg = kmeans(x[g], n_c, n_it)
+                        r[g] = round_bf16(C)
+                        cnt[l, g] = counts
+                        diag.append(dg)
+                    rows.append(r)
+            n_r = rows[0].shape[1]
+            self.row_start.append(self.n_rows)
+            self.row_count.append(n_r)
+            for l in range(self.L):
+                self._chunks[l].append(np.ascontiguousarray(rows[l]))
+            self.counts.append(cnt)
+            self.kmeans_diag.append(diag)
+        self._rows_cache = None
+        return first
+
+    def rows(self, layer: int) -> np.ndarray:
+        """All stored rows of a layer: ``uint16 [H_kv][N][d]``."""
+        if self._rows_cache is None:
+            self._rows_cache = [None] * self.L
+        if self._rows_cache[layer] is None:
+            ch = self._chunks[layer]
+            self._rows_cache[layer] = (np.concatenate(ch, axis=1) if ch else
+                                       np.zeros((self.Hk, 0, self.d), dtype=np.uint16))
+        return self._rows_cache[layer]
+
+    def candidate_frames(self) -> int:
+        """Eq. context_partition: the newest ``n_recent`` units are never candidates."""
+        return max(0, self.n_frames - self.n_recent)
+
+    def candidate_rows(self) -> int:
+        f = self.candidate_frames()
+        return self.row_start[f - 1] + self.row_count[f - 1] if f > 0 else 0
+
+    def frame_of_row(self) -> np.ndarray:
+        n = self.n_rows
+        out = np.empty(n, dtype=np.int64)
+        for t, (s, c) in enumerate(zip(self.row_start, self.row_count)):
+            out[s:s + c] = t
+        return out
+
+
+# ---------------------------------------------------------------------------
+# Query-time stages (Sec. 4.2, "Optional Evidence Retrieval")
+# ---------------------------------------------------------------------------
+
+
+def query_means(queries) -> list[np.ndarray]:
+    """Per layer the mean over text tokens of each head's query: ``[H_q][d]`` float64."""
+    return [decode_bf16(q).mean(axis=1) for q in queries]
+
+
+def score_lists(index: Index, queries, head_mode: int = 0, chunk_rows: int = 1 << 16):
+    """Token scores of every candidate row.
+
+    Reading: the paper scores with the final prompt token; with several text
+    tokens the score of a row is the mean over tokens of the scaled logit
+    ``q_j . K_p / sqrt(d)``, which equals ``mean_j(q_j) . K_p / sqrt(d)`` and is
+    the paper's score when there is one token.  Keys and queries are taken as
+    already rotated (RoPE upstream).  Query head ``h`` reads KV head ``h // G``.
+
+    ``head_mode == 0``: one list per (layer, query head), ordered layer-major.
+    ``head_mode == 1``: one list per layer, the scores averaged over all query
+    heads (the paper's own head reduction).
+
+    Returns a list of float64 arrays over the candidate rows.
+    """
+    N = index.candidate_rows()
+    scale = 1.0 / math.sqrt(index.d)
+    qm = query_means(queries)
+    lists = []
+    for l in range(index.L):
+        K = index.rows(l)
+        per_head = np.empty((index.Hq, N))
+        for g in range(index.Hk):
+            Qg = qm[l][g * index.G:(g + 1) * index.G]          # [G][d]
+            for r0 in range(0, N, chunk_rows):
+                r1 = min(N, r0 + chunk_rows)
+                Kc = decode_bf16(K[g, r0:r1, :])                # [r][d]
+                per_head[g * index.G:(g + 1) * index.G, r0:r1] = (Kc @ Qg.T).T * scale
+        if head_mode == 0:
+            lists.extend(per_head[h] for h in range(index.Hq))
+        elif head_mode == 1:
+            lists.append(per_head.mean(axis=0))
+        else:
+            raise ValueError("head_mode must be 0 or 1")
+    return lists
+
+
+def score_scale(index: Index, queries, layer: int, q_head: int) -> np.ndarray:
+    """Per candidate row the magnitude ``(1/sqrt d) * sum_e |qbar_e| |K_e|`` of its
+    score's terms (the natural scale for score tolerances)."""
+    N = index.candidate_rows()
+    qm = np.abs(query_means(queries)[layer][q_head])
+    K = np.abs(decode_bf16(index.rows(layer)[q_head // index.G, :N, :]))
+    return (K @ qm) / math.sqrt(index.d)
+
+
+def topk(scores: np.ndarray, k: int) -> np.ndarray:
+    """Eq. token_vote_candidates: the ``min(k, N)`` rows of largest score; equal
+    scores are ordered by the lower row position.  Returned in rank order."""
+    order = np.argsort(-scores, kind="stable")     # stable: equal scores keep position order
+    return order[:min(k, scores.size)]
+
+
+def votes_and_mass(index: Index, topk_lists, score_lists_):
+    """One vote per selected token for the unit that owns it (the vote count
+    ``v_t``), and the unit's attention mass: the sum of its selected tokens'
+    scores, accumulated in (list, rank) order.
+
+    Returns ``(votes [F] int64, mass [F] float64)`` over all frames.
+    """
+    F = index.n_frames
+    f_of = index.frame_of_row()
+    votes = np.zeros(F, dtype=np.int64)
+    mass = np.zeros(F, dtype=np.float64)
+    for pos, s in zip(topk_lists, score_lists_):
+        fr = f_of[pos]
+        np.add.at(votes, fr, 1)
+        np.add.at(mass, fr, s[pos])                 # unbuffered, in rank order
+    return votes, mass
+
+
+def vote_pool(votes: np.ndarray, mass: np.ndarray, size: int) -> np.ndarray:
+    """Vote-ranked pool: units with at least one vote, ordered by (votes desc,
+    mass desc, frame id asc), truncated to ``size``."""
+    t = np.arange(votes.size)
+    voted = votes >= 1
+    idx = t[voted]
+    order = np.lexsort((idx, -mass[voted], -votes[voted]))
+    return idx[order][:size]
+
+
+def maxmin_select(pool: np.ndarray, desc: np.ndarray, K: int):
+    """Greedy max-min diversity over descriptors, seeded by the top of the vote
+    ranking: each next unit maximises its smallest cosine distance ``1 - k_u.k_s``
+    to the already selected units; ties go to the earlier pool rank.
+
+    Returns ``(selected frame ids in selection order, margins)`` where
+    ``margins[i]`` is the gap between the best and second-best candidate value
+    at greedy step ``i`` (``inf`` when there was one candidate).
+    """
+    n = pool.size
+    want = min(K, n)
+    if want == 0:
+        return np.zeros(0, dtype=np.int64), []
+    D = desc[pool]                                   # [n][dim]
+    sel = [0]
+    taken = np.zeros(n, dtype=bool)
+    taken[0] = True
+    mind = 1.0 - D @ D[0]
+    margins = []
+    while len(sel) < want:
+        cand = np.where(taken, -np.inf, mind)
+        j = int(np.argmax(cand))                     # first maximum = earlier pool rank
+        rest = np.sort(cand[~taken])[::-1]
+        margins.append(float(rest[0] - rest[1]) if rest.size > 1 else np.inf)
+        sel.append(j)
+        taken[j] = True
+        mind = np.minimum(mind, 1.0 - D @ D[j])
+    return pool[np.array(sel)], margins
+
+
+def retrieve(index: Index, queries, top_k: int, n_select: int, pool_mult: int = 4,
+             head_mode: int = 0, debug: bool = False):
+    """Evidence retrieval for one stream and one question.
+
+    Returns ``(frame_ids, votes, mass, n_out)``: ``frame_ids`` in max-min
+    selection order, padded with -1 to ``n_select``; ``votes``/``mass`` of the
+    selected frames (0 in the padding).  With ``debug=True`` a dict of every
+    intermediate is appended.
+    """
+    if top_k < 1 or n_select < 1 or pool_mult < 1:
+        raise ValueError("top_k, n_select and pool_mult must be >= 1")
+    S = score_lists(index, queries, head_mode)
+    T = [topk(s, top_k) for s in S]
+    votes, mass = votes_and_mass(index, T, S)
+    pool = vote_pool(votes, mass, pool_mult * n_select)
+    desc = np.array(index.desc) if index.desc else np.zeros((0, index.Hk * index.d))
+    sel, margins = maxmin_select(pool, desc, n_select)
+    frame_ids = np.full(n_select, -1, dtype=np.int64)
+    v_out = np.zeros(n_select, dtype=np.int64)
+    m_out = np.zeros(n_select, dtype=np.float64)
+    frame_ids[:sel.size] = sel
+    v_out[:sel.size] = votes[sel]
+    m_out[:sel.size] = mass[sel]
+    out = (frame_ids, v_out, m_out, int(sel.size))
+    if debug:
+        return out + ({"scores": S, "topk": T, "votes": votes, "mass": mass, "pool": pool,
+                       "maxmin_margins": margins},)
+    return out
