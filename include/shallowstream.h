@@ -1,0 +1,218 @@
+/*
+ * shallowstream.h -- C ABI of the MI355X (gfx950) library for ShallowStream's
+ * query-time evidence retrieval over a shallow-layer key index.
+ *
+ * The method (Sec. 4 of the ShallowStream paper):
+ *   - index construction (Sec. 4.1): every video unit ("frame") contributes the
+ *     keys of its visual tokens at each shallow layer (Eq. shallow_streaming_cache)
+ *     and a unit descriptor (Eq. memory_key); an optional per-frame k-means
+ *     compression stores centroids instead of the raw token keys;
+ *   - retrieval (Sec. 4.2, "Optional Evidence Retrieval"): scaled Q-K scores of
+ *     the question against every stored key, top-k per list
+ *     (Eq. token_vote_candidates), one vote per selected token for its frame,
+ *     a vote-ranked pool of pool_mult*K frames (ties by attention mass) and
+ *     greedy max-min diversity in descriptor space (DivTopK, Eq. selected_evidence).
+ *
+ * Conventions for every entry point:
+ *   - bf16 arrays are raw IEEE bfloat16 bit patterns (uint16), row-major.
+ *   - "device pointer" means memory of the current HIP device; "host pointer"
+ *     means ordinary CPU memory.  `stream` is a hipStream_t (NULL = the
+ *     default stream).  Work is enqueued on `stream`; the call returns without
+ *     waiting for it.  Inputs must stay valid until that work completes.
+ *   - The library never allocates device memory: the caller provides the index
+ *     arena and every workspace and output buffer.
+ *   - Every argument is validated on the host before anything is enqueued.  On
+ *     failure the call returns a non-zero status, ss_last_error() describes it,
+ *     and the index is unchanged.  No exception crosses this boundary.
+ *   - Device faults surface at the caller's next synchronisation.
+ *   - Calls on different indices may run concurrently.  Appends and retrievals
+ *     touching one index must be ordered on one stream (or synchronised).
+ *   - Inputs must be finite; NaN or Inf keys or queries give unspecified ranks.
+ */
+#ifndef SHALLOWSTREAM_H
+#define SHALLOWSTREAM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ss_index ss_index; /* opaque, host-side handle */
+typedef int32_t ss_status;
+
+enum {
+  SS_OK = 0,
+  SS_ERR_INVALID_ARGUMENT = 1, /* a pointer, shape or parameter is wrong        */
+  SS_ERR_UNSUPPORTED = 2,      /* valid but outside what the kernels implement  */
+  SS_ERR_CAPACITY = 3,         /* the arena cannot hold the appended frames     */
+  SS_ERR_WORKSPACE = 4,        /* the workspace is smaller than required        */
+  SS_ERR_DEVICE = 5,           /* a HIP runtime call or kernel launch failed    */
+  SS_ERR_INTERNAL = 6
+};
+
+/* Shape and capacity of one stream's index.
+ *   n_layers    L_s, the shallow layers kept (the pruning boundary P).
+ *   n_q_heads   H_q query heads; n_kv_heads H_kv key heads, H_q % H_kv == 0,
+ *               G = H_q / H_kv <= 16.  Query head h reads KV head h / G.
+ *   head_dim    d, 64 or 128.
+ *   max_frames  frame capacity; max_rows row capacity per (layer, KV head),
+ *               < 2^31.
+ *   n_recent    N_r: the newest n_recent frames are never retrieval
+ *               candidates (Eq. context_partition); 0 makes every frame one. */
+typedef struct {
+  int32_t n_layers;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int64_t max_frames;
+  int64_t max_rows;
+  int32_t n_recent;
+} ss_index_desc;
+
+/* Per-frame k-means compression at append: each frame's tokens, per (layer,
+ * KV head), become min(n_centroids, n_tokens) centroids: farthest-point
+ * initialisation (first centre = the token farthest from the frame mean), then
+ * exactly n_iters Lloyd rounds on squared Euclidean distance in fp32, ties to the
+ * lower index, empty clusters keep their centre; stored as bf16 (nearest-even)
+ * in farthest-point order.  1 <= n_centroids <= 64, 0 <= n_iters <= 100,
+ * n_tokens <= 256. */
+typedef struct {
+  int32_t n_centroids;
+  int32_t n_iters;
+} ss_compress;
+
+/* Retrieval parameters.
+ *   top_k      k rows kept per list (Eq. token_vote_candidates), 1..2048; more
+ *              than the candidate rows selects them all.
+ *   n_select   K, the frame budget, 1..64.
+ *   pool_mult  the vote-ranked pool holds pool_mult*K frames (4 in the paper),
+ *              pool_mult*K <= 256; 1 makes diversity selection a no-op.
+ *   head_mode  0: one list per (layer, query head).  1: one list per layer with
+ *              the scores averaged over all query heads (the paper's reduction).
+ */
+typedef struct {
+  int32_t top_k;
+  int32_t n_select;
+  int32_t pool_mult;
+  int32_t head_mode;
+} ss_retrieve_params;
+
+/* Device bytes an index with this shape needs (0 if `desc` is invalid).
+ * Layout (each part 256-byte aligned): keys bf16 [L_s][H_kv][max_rows][d];
+ * member counts int32 [L_s][H_kv][max_rows]; descriptors fp32
+ * [max_frames][H_kv*d]; frame row offsets int32 [max_frames+1]. */
+size_t ss_index_required_bytes(const ss_index_desc* desc);
+
+/* Create an empty index over a caller-owned device arena of at least
+ * ss_index_required_bytes(desc) bytes, 256-byte aligned.  The arena must stay
+ * allocated until ss_index_destroy.  *out receives the handle. */
+ss_status ss_index_create(const ss_index_desc* desc, void* dev_arena, size_t arena_bytes,
+                          ss_index** out);
+
+/* Release the host-side handle.  The arena stays the caller's. */
+ss_status ss_index_destroy(ss_index* idx);
+
+/* Host-side counters: frames and rows per (layer, KV head) stored so far. */
+ss_status ss_index_info(const ss_index* idx, int64_t* n_frames, int64_t* n_rows);
+
+/* Append n_frames frames of n_tokens visual tokens each (Eq. shallow_streaming_cache).
+ *   layer_keys  host array of L_s device pointers; pointer l addresses bf16
+ *               [H_kv][n_frames*n_tokens][d] keys of shallow layer l (16-byte
+ *               aligned).  Frame f owns tokens [f*n_tokens, (f+1)*n_tokens).
+ *   compress    NULL stores the raw keys; otherwise see ss_compress.
+ *   first_frame_id  host out: the id of the first appended frame (frame ids are
+ *               append order from 0).
+ * The unit descriptor (Eq. memory_key) always uses the raw keys of the last
+ * shallow layer.  Fails with SS_ERR_CAPACITY (index unchanged) if the frames or
+ * rows do not fit. */
+ss_status ss_index_append(ss_index* idx, const void* const* layer_keys, int32_t n_frames,
+                          int32_t n_tokens, const ss_compress* compress, void* stream,
+                          int64_t* first_frame_id);
+
+/* Workspace bytes ss_retrieve needs for this batch in the indices' current state
+ * (0 if the arguments are invalid).  n_q: host array of n_streams token counts. */
+size_t ss_retrieve_workspace_bytes(ss_index* const* idx, int32_t n_streams, const int32_t* n_q,
+                                   const ss_retrieve_params* params);
+
+/* Evidence retrieval for n_streams independent streams with one question each.
+ *   idx        host array of n_streams handles with identical shapes.
+ *   queries    host array of n_streams*L_s device pointers, stream-major;
+ *              pointer [s*L_s + l] addresses bf16 [H_q][n_q[s]][d] query states
+ *              of layer l (post-RoPE, as cached; 16-byte aligned).  The score of
+ *              a key is the mean over query tokens of the scaled logit
+ *              q.k/sqrt(d) (the paper uses the last prompt token: n_q = 1).
+ *   n_q        host array, per stream, 1..4096.
+ *   ws         device workspace of ws_bytes >= ss_retrieve_workspace_bytes().
+ * Outputs (device, [n_streams][n_select] each, selection order):
+ *   frame_ids  int64 frame ids, -1 after the n_out[s] selected frames;
+ *   votes      int32 votes of each selected frame (0 in the padding);
+ *   mass       fp32 attention mass (sum of the frame's selected scores);
+ *   n_out      int32 [n_streams], number of frames selected. */
+ss_status ss_retrieve(ss_index* const* idx, int32_t n_streams, const void* const* queries,
+                      const int32_t* n_q, const ss_retrieve_params* params, void* ws,
+                      size_t ws_bytes, void* stream, int64_t* frame_ids, int32_t* votes,
+                      float* mass, int32_t* n_out);
+
+/* Intermediates of one retrieval, for parity checks (any pointer may be NULL).
+ * Device arrays, n_lists = L_s*H_q (head_mode 0) or L_s (head_mode 1), lists
+ * ordered layer-major, F = frames of the stream at the call:
+ *   topk_pos    int32 [n_streams][n_lists][top_k] row positions in rank order
+ *               (score desc, position asc), -1 padded;
+ *   topk_score  fp32  same shape, the scores;
+ *   vote_hist   int32 [n_streams][max_frames] votes of every frame;
+ *   mass_hist   fp32  [n_streams][max_frames] attention mass of every frame;
+ *   pool        int32 [n_streams][pool_mult*n_select] the vote-ranked pool, -1 padded;
+ *   pool_n      int32 [n_streams];
+ *   list_stats  int32 [n_streams][n_lists][2]: candidates kept by the streaming
+ *               pass, and 1 if the list took the exact fallback path. */
+typedef struct {
+  int32_t* topk_pos;
+  float* topk_score;
+  int32_t* vote_hist;
+  float* mass_hist;
+  int32_t* pool;
+  int32_t* pool_n;
+  int32_t* list_stats;
+} ss_debug_out;
+
+/* ss_retrieve plus the intermediates in `dbg`. */
+ss_status ss_retrieve_debug(ss_index* const* idx, int32_t n_streams, const void* const* queries,
+                            const int32_t* n_q, const ss_retrieve_params* params, void* ws,
+                            size_t ws_bytes, void* stream, int64_t* frame_ids, int32_t* votes,
+                            float* mass, int32_t* n_out, const ss_debug_out* dbg);
+
+/* Every score of one list over rows [row0, row0+n_rows) of one index, with the
+ * same arithmetic as ss_retrieve (parity only).  queries: host array of L_s
+ * device pointers as in ss_retrieve.  out: device fp32 [n_rows].  With
+ * head_mode 1 `q_head` is ignored and the list is the layer's head mean.
+ * ws: device workspace of ss_debug_scores_workspace_bytes() bytes. */
+size_t ss_debug_scores_workspace_bytes(const ss_index* idx);
+ss_status ss_debug_scores(const ss_index* idx, const void* const* queries, int32_t n_q,
+                          int32_t layer, int32_t q_head, int32_t head_mode, int64_t row0,
+                          int64_t n_rows, float* out, void* ws, size_t ws_bytes, void* stream);
+
+/* Copy the stored state out (parity only; any pointer may be NULL):
+ *   rows_dev     bf16 [L_s][H_kv][n_rows][d] device;
+ *   counts_dev   int32 [L_s][H_kv][n_rows] device (k-means member counts, 1 for raw rows);
+ *   desc_dev     fp32 [n_frames][H_kv*d] device descriptors;
+ *   frame_offsets_host  int64 [n_frames+1] host row offsets. */
+ss_status ss_index_export(const ss_index* idx, void* rows_dev, int32_t* counts_dev,
+                          float* desc_dev, int64_t* frame_offsets_host, void* stream);
+
+/* Optional timing hook for the streaming scoring kernel: when both are
+ * non-NULL hipEvent_t handles, later ss_retrieve calls on this thread record
+ * `ev_start` just before that kernel and `ev_stop` just after it, on the
+ * call's stream.  NULL, NULL turns it off. */
+ss_status ss_set_profile_events(void* ev_start, void* ev_stop);
+
+const char* ss_status_string(ss_status status);
+const char* ss_last_error(void); /* thread-local text of the last failure */
+int32_t ss_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SHALLOWSTREAM_H */

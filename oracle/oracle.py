@@ -245,6 +245,28 @@ class Index:
         self._rows_cache = None
         return first
 
+    def append_stored(self, layer_rows, rows_per_frame, descriptors) -> int:
+        """Append frames whose stored rows and descriptors were produced elsewhere
+        (e.g. compressed rows exported from another implementation), so retrieval
+        can be checked on identical stored data.
+
+        ``layer_rows``: per layer ``uint16 [H_kv][sum(rows_per_frame)][d]``;
+        ``descriptors``: ``[n_frames][H_kv * d]``.
+        """
+        first = self.n_frames
+        start = 0
+        for f, n_r in enumerate(rows_per_frame):
+            self.desc.append(np.asarray(descriptors[f], dtype=np.float64))
+            self.row_start.append(self.n_rows)
+            self.row_count.append(int(n_r))
+            for l in range(self.L):
+                self._chunks[l].append(np.ascontiguousarray(layer_rows[l][:, start:start + n_r, :]))
+            self.counts.append(None)
+            self.kmeans_diag.append(None)
+            start += n_r
+        self._rows_cache = None
+        return first
+
     def rows(self, layer: int) -> np.ndarray:
         """All stored rows of a layer: ``uint16 [H_kv][N][d]``."""
         if self._rows_cache is None:

@@ -1,0 +1,10 @@
+"""MI355X (gfx950) implementation of ShallowStream's query-time evidence
+retrieval over a shallow-layer key index.
+
+The work runs in ``libshallowstream.so`` (HIP kernels behind the C ABI of
+``include/shallowstream.h``); this package only marshals arguments.
+"""
+from ._lib import SSError, lib  # noqa: F401
+from .index import Retriever, ShallowIndex, set_profile_events  # noqa: F401
+
+__all__ = ["ShallowIndex", "Retriever", "SSError", "set_profile_events", "lib"]

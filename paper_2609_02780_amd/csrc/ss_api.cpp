@@ -1,0 +1,547 @@
+// C ABI of the shallow-index evidence retrieval library: argument validation,
+// per-index host bookkeeping and the retrieval planner.  Every check runs before
+// any HIP call, so invalid calls leave the index and the device untouched.
+#include "../../include/shallowstream.h"
+#include "ss_internal.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+struct ss_index {
+  ss_index_desc desc;
+  void* arena;
+  size_t arena_bytes;
+  ss::IndexDev dev;
+  int64_t n_frames;
+  int64_t n_rows;
+  std::vector<int64_t> off;  // frame row offsets, n_frames + 1 entries
+  int32_t rpf;               // common rows per frame, 0 if mixed, -1 before the first append
+};
+
+namespace {
+
+thread_local std::string g_err;
+thread_local hipEvent_t g_ev_start = nullptr;
+thread_local hipEvent_t g_ev_stop = nullptr;
+
+ss_status fail(ss_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+inline bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+struct Layout {
+  size_t keys, counts, desc, off, total;
+};
+
+// Check an index shape; fills `why` on failure.
+ss_status check_desc(const ss_index_desc* d) {
+  if (!d) return fail(SS_ERR_INVALID_ARGUMENT, "desc is NULL");
+  if (d->n_layers < 1 || d->n_layers > ss::kMaxLayers)
+    return fail(SS_ERR_UNSUPPORTED, "n_layers %d outside 1..%d", d->n_layers, ss::kMaxLayers);
+  if (d->n_q_heads < 1 || d->n_kv_heads < 1)
+    return fail(SS_ERR_INVALID_ARGUMENT, "head counts must be >= 1");
+  if (d->n_q_heads % d->n_kv_heads != 0)
+    return fail(SS_ERR_INVALID_ARGUMENT, "n_q_heads %d is not a multiple of n_kv_heads %d",
+                d->n_q_heads, d->n_kv_heads);
+  if (d->n_q_heads / d->n_kv_heads > ss::kMaxGroup)
+    return fail(SS_ERR_UNSUPPORTED, "query heads per KV head %d > %d",
+                d->n_q_heads / d->n_kv_heads, ss::kMaxGroup);
+  if (d->head_dim != 64 && d->head_dim != 128)
+    return fail(SS_ERR_UNSUPPORTED, "head_dim %d is not 64 or 128", d->head_dim);
+  if ((int64_t)d->n_kv_heads * d->head_dim > 1024)
+    return fail(SS_ERR_UNSUPPORTED, "n_kv_heads * head_dim %lld > 1024",
+                (long long)d->n_kv_heads * d->head_dim);
+  if (d->max_frames < 1 || d->max_frames > (int64_t)1 << 30)
+    return fail(SS_ERR_INVALID_ARGUMENT, "max_frames %lld outside 1..2^30", (long long)d->max_frames);
+  if (d->max_rows < 1 || d->max_rows > (int64_t)0x7FFFFFFF - 1)
+    return fail(SS_ERR_INVALID_ARGUMENT, "max_rows %lld outside 1..2^31-2", (long long)d->max_rows);
+  if (d->n_recent < 0) return fail(SS_ERR_INVALID_ARGUMENT, "n_recent must be >= 0");
+  return SS_OK;
+}
+
+Layout layout(const ss_index_desc& d) {
+  Layout L{};
+  const size_t lg = (size_t)d.n_layers * d.n_kv_heads;
+  size_t off = 0;
+  L.keys = off;
+  off = align256(off + lg * (size_t)d.max_rows * d.head_dim * 2);
+  L.counts = off;
+  off = align256(off + lg * (size_t)d.max_rows * 4);
+  L.desc = off;
+  off = align256(off + (size_t)d.max_frames * d.n_kv_heads * d.head_dim * 4);
+  L.off = off;
+  off = align256(off + ((size_t)d.max_frames + 1) * 4);
+  L.total = off;
+  return L;
+}
+
+bool same_shape(const ss_index_desc& a, const ss_index_desc& b) {
+  return a.n_layers == b.n_layers && a.n_q_heads == b.n_q_heads && a.n_kv_heads == b.n_kv_heads &&
+         a.head_dim == b.head_dim;
+}
+
+// Candidate rows and frames of an index (Eq. context_partition: the newest
+// n_recent frames are excluded).
+void candidates(const ss_index* x, int64_t& rows, int64_t& frames) {
+  frames = std::max<int64_t>(0, x->n_frames - x->desc.n_recent);
+  rows = x->off[frames];
+}
+
+constexpr int kSampleRank = 48;      // rank r of the sample cut-off
+constexpr int kFullScanRows = 4096;  // at or below this many rows the sample is the whole list
+constexpr int kChunkRows = 4096;
+constexpr int kSampleChunk = 512;
+
+struct StreamSizes {
+  int n, f, m, r, kk;
+};
+
+// Sample plan of one list.  With m sampled rows spread evenly over n rows and the
+// cut-off at the r-th largest sample score, about r n / m rows score at or above
+// it (the expected candidate count E).  r = min(k, 48) keeps the count below k
+// six standard deviations away; m = n gives an exact cut (r = k) for small lists.
+StreamSizes plan_stream(int64_t n, int64_t f, int top_k) {
+  StreamSizes z{};
+  z.n = (int)n;
+  z.f = (int)f;
+  z.kk = (int)std::min<int64_t>(top_k, n);
+  if (n == 0) return z;
+  const int64_t E = std::max<int64_t>(8 * (int64_t)z.kk, 2048);
+  int64_t r = std::min<int64_t>(z.kk, kSampleRank);
+  int64_t m = std::max<int64_t>(r, (n * r + E - 1) / E);
+  if (n <= kFullScanRows || 2 * m >= n) {
+    m = n;
+    r = z.kk;
+  }
+  z.m = (int)m;
+  z.r = (int)r;
+  return z;
+}
+
+int64_t candidate_cap(int top_k, int64_t n_max) {
+  const int64_t kk = std::min<int64_t>(top_k, std::max<int64_t>(n_max, 1));
+  const int64_t E = std::max<int64_t>(8 * kk, 2048);
+  return std::max<int64_t>(2 * E, 4096);
+}
+
+ss_status check_params(const ss_retrieve_params* p, int Hk) {
+  if (!p) return fail(SS_ERR_INVALID_ARGUMENT, "params is NULL");
+  if (p->top_k < 1 || p->top_k > ss::kMaxTopK)
+    return fail(SS_ERR_UNSUPPORTED, "top_k %d outside 1..%d", p->top_k, ss::kMaxTopK);
+  if (p->n_select < 1 || p->n_select > ss::kMaxSelect)
+    return fail(SS_ERR_UNSUPPORTED, "n_select %d outside 1..%d", p->n_select, ss::kMaxSelect);
+  if (p->pool_mult < 1) return fail(SS_ERR_INVALID_ARGUMENT, "pool_mult must be >= 1");
+  if ((int64_t)p->pool_mult * p->n_select > ss::kMaxPool)
+    return fail(SS_ERR_UNSUPPORTED, "pool_mult * n_select %lld > %d",
+                (long long)p->pool_mult * p->n_select, ss::kMaxPool);
+  if (p->head_mode != 0 && p->head_mode != 1)
+    return fail(SS_ERR_INVALID_ARGUMENT, "head_mode must be 0 or 1");
+  if (p->head_mode == 1 && Hk > 8)
+    return fail(SS_ERR_UNSUPPORTED, "head_mode 1 supports at most 8 KV heads");
+  return SS_OK;
+}
+
+// Builds the plan of streams [s0, s0 + S) of a validated batch (`queries` may be
+// NULL when only the workspace size is wanted).
+void build_plan(ss::RetrievePlan& p, ss_index* const* idx, int s0, int S, const void* const* queries,
+                const int32_t* n_q, const ss_retrieve_params* prm) {
+  std::memset(&p, 0, sizeof p);
+  const ss_index_desc& d = idx[0]->desc;
+  p.S = S;
+  p.L = d.n_layers;
+  p.Hq = d.n_q_heads;
+  p.Hk = d.n_kv_heads;
+  p.G = p.Hq / p.Hk;
+  p.D = d.head_dim;
+  p.head_mode = prm->head_mode;
+  p.NL = prm->head_mode == 0 ? p.L * p.Hq : p.L;
+  p.ncol = prm->head_mode == 0 ? p.G : 1;
+  p.ngs = prm->head_mode == 0 ? p.Hk : 1;
+  p.top_k = prm->top_k;
+  p.n_select = prm->n_select;
+  p.pool_mult = prm->pool_mult;
+  p.pool = prm->pool_mult * prm->n_select;
+  p.chunk_rows = kChunkRows;
+  p.samp_chunk = kSampleChunk;
+  int64_t n_max = 0, full = 0;
+  int hist = 1;
+  for (int i = 0; i < S; ++i) {
+    const ss_index* x = idx[s0 + i];
+    int64_t rows, frames;
+    candidates(x, rows, frames);
+    const StreamSizes z = plan_stream(rows, frames, prm->top_k);
+    ss::StreamPlan& sp = p.st[i];
+    sp.keys = x->dev.keys;
+    sp.frame_off = x->dev.frame_off;
+    sp.desc = x->dev.desc;
+    sp.row_stride = (int32_t)x->desc.max_rows;
+    sp.n = z.n;
+    sp.f = z.f;
+    sp.m = z.m;
+    sp.r = z.r;
+    sp.kk = z.kk;
+    sp.nq = n_q[s0 + i];
+    sp.rpf = x->rpf > 0 ? x->rpf : 0;
+    double sc = 1.0 / ((double)sp.nq * std::sqrt((double)p.D));
+    if (prm->head_mode == 1) sc /= (double)p.Hq;
+    sp.qscale = (float)sc;
+    for (int l = 0; l < p.L; ++l)
+      sp.q[l] = queries ? static_cast<const uint16_t*>(queries[(size_t)(s0 + i) * p.L + l]) : nullptr;
+    n_max = std::max<int64_t>(n_max, rows);
+    p.k_max = std::max(p.k_max, z.kk);
+    p.m_max = std::max(p.m_max, z.m);
+    p.f_max = std::max(p.f_max, z.f);
+    p.full_base[i] = full;
+    full += (int64_t)p.NL * rows;
+    hist = (int)std::max<int64_t>(hist, x->desc.max_frames);
+  }
+  p.f_max = std::max(p.f_max, 1);
+  p.m_max = std::max(p.m_max, 1);
+  p.cap = (int)candidate_cap(prm->top_k, n_max);
+  p.full_total = full;
+  p.dbg_hist_stride = hist;
+}
+
+ss_status check_batch(ss_index* const* idx, int32_t n_streams, const int32_t* n_q,
+                      const ss_retrieve_params* prm) {
+  if (!idx) return fail(SS_ERR_INVALID_ARGUMENT, "idx is NULL");
+  if (n_streams < 1) return fail(SS_ERR_INVALID_ARGUMENT, "n_streams must be >= 1");
+  if (!n_q) return fail(SS_ERR_INVALID_ARGUMENT, "n_q is NULL");
+  for (int s = 0; s < n_streams; ++s) {
+    if (!idx[s]) return fail(SS_ERR_INVALID_ARGUMENT, "idx[%d] is NULL", s);
+    if (!same_shape(idx[s]->desc, idx[0]->desc))
+      return fail(SS_ERR_INVALID_ARGUMENT, "idx[%d] shape differs from idx[0]", s);
+    if (n_q[s] < 1 || n_q[s] > 4096)
+      return fail(SS_ERR_INVALID_ARGUMENT, "n_q[%d] = %d outside 1..4096", s, n_q[s]);
+  }
+  return check_params(prm, idx[0]->desc.n_kv_heads);
+}
+
+size_t group_ws(ss_index* const* idx, int s0, int S, const int32_t* n_q,
+                const ss_retrieve_params* prm) {
+  ss::RetrievePlan p;
+  build_plan(p, idx, s0, S, nullptr, n_q, prm);
+  return ss::carve_workspace(p, nullptr);
+}
+
+size_t batch_ws(ss_index* const* idx, int32_t n_streams, const int32_t* n_q,
+                const ss_retrieve_params* prm) {
+  size_t need = 0;
+  for (int s0 = 0; s0 < n_streams; s0 += ss::kMaxStreams) {
+    const int S = std::min(ss::kMaxStreams, n_streams - s0);
+    need = std::max(need, group_ws(idx, s0, S, n_q, prm));
+  }
+  return need;
+}
+
+ss_status retrieve_common(ss_index* const* idx, int32_t n_streams, const void* const* queries,
+                          const int32_t* n_q, const ss_retrieve_params* prm, void* ws,
+                          size_t ws_bytes, void* stream, int64_t* frame_ids, int32_t* votes,
+                          float* mass, int32_t* n_out, const ss_debug_out* dbg) {
+  ss_status st = check_batch(idx, n_streams, n_q, prm);
+  if (st) return st;
+  if (!queries) return fail(SS_ERR_INVALID_ARGUMENT, "queries is NULL");
+  const int L = idx[0]->desc.n_layers;
+  for (int i = 0; i < n_streams * L; ++i) {
+    if (!queries[i]) return fail(SS_ERR_INVALID_ARGUMENT, "queries[%d] is NULL", i);
+    if (!aligned(queries[i], 16)) return fail(SS_ERR_INVALID_ARGUMENT, "queries[%d] not 16-byte aligned", i);
+  }
+  if (!frame_ids || !votes || !mass || !n_out)
+    return fail(SS_ERR_INVALID_ARGUMENT, "an output pointer is NULL");
+  if (!ws || !aligned(ws, 256)) return fail(SS_ERR_WORKSPACE, "workspace NULL or not 256-byte aligned");
+  const size_t need = batch_ws(idx, n_streams, n_q, prm);
+  if (ws_bytes < need)
+    return fail(SS_ERR_WORKSPACE, "workspace %zu bytes, %zu needed", ws_bytes, need);
+  if (dbg && dbg->topk_score == nullptr && dbg->topk_pos != nullptr)
+    return fail(SS_ERR_INVALID_ARGUMENT, "debug topk_pos needs topk_score");
+  if (dbg && (dbg->vote_hist == nullptr) != (dbg->mass_hist == nullptr))
+    return fail(SS_ERR_INVALID_ARGUMENT, "debug vote_hist and mass_hist go together");
+  const hipStream_t hs = static_cast<hipStream_t>(stream);
+  for (int s0 = 0; s0 < n_streams; s0 += ss::kMaxStreams) {
+    const int S = std::min(ss::kMaxStreams, n_streams - s0);
+    ss::RetrievePlan p;
+    build_plan(p, idx, s0, S, queries, n_q, prm);
+    ss::carve_workspace(p, ws);
+    p.out_ids = frame_ids + (size_t)s0 * prm->n_select;
+    p.out_votes = votes + (size_t)s0 * prm->n_select;
+    p.out_mass = mass + (size_t)s0 * prm->n_select;
+    p.out_n = n_out + s0;
+    p.out_stride = prm->n_select;
+    if (dbg) {
+      const size_t NLt = (size_t)p.NL * prm->top_k;
+      int hist = 1;
+      for (int s = 0; s < n_streams; ++s) hist = (int)std::max<int64_t>(hist, idx[s]->desc.max_frames);
+      p.dbg_hist_stride = hist;
+      p.dbg_topk_pos = dbg->topk_pos ? dbg->topk_pos + (size_t)s0 * NLt : nullptr;
+      p.dbg_topk_score = dbg->topk_score ? dbg->topk_score + (size_t)s0 * NLt : nullptr;
+      p.dbg_vote_hist = dbg->vote_hist ? dbg->vote_hist + (size_t)s0 * hist : nullptr;
+      p.dbg_mass_hist = dbg->mass_hist ? dbg->mass_hist + (size_t)s0 * hist : nullptr;
+      p.dbg_pool = dbg->pool ? dbg->pool + (size_t)s0 * p.pool : nullptr;
+      p.dbg_pool_n = dbg->pool_n ? dbg->pool_n + s0 : nullptr;
+      p.dbg_list_stats = dbg->list_stats ? dbg->list_stats + (size_t)s0 * p.NL * 2 : nullptr;
+    }
+    p.ev_start = g_ev_start;
+    p.ev_stop = g_ev_stop;
+    const hipError_t e = ss::launch_retrieve(p, hs);
+    if (e != hipSuccess) return fail(SS_ERR_DEVICE, "retrieve launch failed: %s", hipGetErrorString(e));
+  }
+  return SS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t ss_index_required_bytes(const ss_index_desc* desc) {
+  if (check_desc(desc) != SS_OK) return 0;
+  return layout(*desc).total;
+}
+
+ss_status ss_index_create(const ss_index_desc* desc, void* dev_arena, size_t arena_bytes,
+                          ss_index** out) {
+  if (!out) return fail(SS_ERR_INVALID_ARGUMENT, "out is NULL");
+  ss_status st = check_desc(desc);
+  if (st) return st;
+  if (!dev_arena) return fail(SS_ERR_INVALID_ARGUMENT, "arena is NULL");
+  if (!aligned(dev_arena, 256)) return fail(SS_ERR_INVALID_ARGUMENT, "arena not 256-byte aligned");
+  const Layout L = layout(*desc);
+  if (arena_bytes < L.total)
+    return fail(SS_ERR_CAPACITY, "arena %zu bytes, %zu needed", arena_bytes, L.total);
+  ss_index* x = new (std::nothrow) ss_index();
+  if (!x) return fail(SS_ERR_INTERNAL, "out of host memory");
+  x->desc = *desc;
+  x->arena = dev_arena;
+  x->arena_bytes = arena_bytes;
+  char* b = static_cast<char*>(dev_arena);
+  x->dev.keys = reinterpret_cast<uint16_t*>(b + L.keys);
+  x->dev.counts = reinterpret_cast<int32_t*>(b + L.counts);
+  x->dev.desc = reinterpret_cast<float*>(b + L.desc);
+  x->dev.frame_off = reinterpret_cast<int32_t*>(b + L.off);
+  x->n_frames = 0;
+  x->n_rows = 0;
+  x->off.assign(1, 0);
+  x->rpf = -1;
+  *out = x;
+  return SS_OK;
+}
+
+ss_status ss_index_destroy(ss_index* idx) {
+  if (!idx) return fail(SS_ERR_INVALID_ARGUMENT, "idx is NULL");
+  delete idx;
+  return SS_OK;
+}
+
+ss_status ss_index_info(const ss_index* idx, int64_t* n_frames, int64_t* n_rows) {
+  if (!idx) return fail(SS_ERR_INVALID_ARGUMENT, "idx is NULL");
+  if (n_frames) *n_frames = idx->n_frames;
+  if (n_rows) *n_rows = idx->n_rows;
+  return SS_OK;
+}
+
+ss_status ss_index_append(ss_index* idx, const void* const* layer_keys, int32_t n_frames,
+                          int32_t n_tokens, const ss_compress* compress, void* stream,
+                          int64_t* first_frame_id) {
+  if (!idx) return fail(SS_ERR_INVALID_ARGUMENT, "idx is NULL");
+  const ss_index_desc& d = idx->desc;
+  if (!layer_keys) return fail(SS_ERR_INVALID_ARGUMENT, "layer_keys is NULL");
+  if (n_frames < 1 || n_tokens < 1)
+    return fail(SS_ERR_INVALID_ARGUMENT, "n_frames and n_tokens must be >= 1");
+  if ((int64_t)n_frames * n_tokens > 0x7FFFFFFF)
+    return fail(SS_ERR_UNSUPPORTED, "n_frames * n_tokens exceeds 2^31-1");
+  for (int l = 0; l < d.n_layers; ++l) {
+    if (!layer_keys[l]) return fail(SS_ERR_INVALID_ARGUMENT, "layer_keys[%d] is NULL", l);
+    if (!aligned(layer_keys[l], 16))
+      return fail(SS_ERR_INVALID_ARGUMENT, "layer_keys[%d] not 16-byte aligned", l);
+  }
+  int rpf = n_tokens;
+  if (compress) {
+    if (compress->n_centroids < 1 || compress->n_centroids > ss::kMaxCentroids)
+      return fail(SS_ERR_UNSUPPORTED, "n_centroids %d outside 1..%d", compress->n_centroids,
+                  ss::kMaxCentroids);
+    if (compress->n_iters < 0 || compress->n_iters > 100)
+      return fail(SS_ERR_INVALID_ARGUMENT, "n_iters %d outside 0..100", compress->n_iters);
+    if (n_tokens > ss::kMaxTokensCompress)
+      return fail(SS_ERR_UNSUPPORTED, "compression supports at most %d tokens per frame",
+                  ss::kMaxTokensCompress);
+    rpf = std::min(compress->n_centroids, n_tokens);
+  }
+  if (idx->n_frames + n_frames > d.max_frames)
+    return fail(SS_ERR_CAPACITY, "%lld frames + %d exceeds max_frames %lld", (long long)idx->n_frames,
+                n_frames, (long long)d.max_frames);
+  const int64_t new_rows = (int64_t)n_frames * rpf;
+  if (idx->n_rows + new_rows > d.max_rows)
+    return fail(SS_ERR_CAPACITY, "%lld rows + %lld exceeds max_rows %lld", (long long)idx->n_rows,
+                (long long)new_rows, (long long)d.max_rows);
+  ss::AppendArgs a{};
+  a.L = d.n_layers;
+  a.Hk = d.n_kv_heads;
+  a.D = d.head_dim;
+  a.n_frames = n_frames;
+  a.n_tokens = n_tokens;
+  a.max_rows = d.max_rows;
+  a.row0 = idx->n_rows;
+  a.frame0 = idx->n_frames;
+  a.rows_per_frame = rpf;
+  a.n_centroids = compress ? compress->n_centroids : 0;
+  a.n_iters = compress ? compress->n_iters : 0;
+  for (int l = 0; l < d.n_layers; ++l) a.src[l] = static_cast<const uint16_t*>(layer_keys[l]);
+  a.dst = idx->dev;
+  const hipError_t e = ss::launch_append(a, compress != nullptr, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SS_ERR_DEVICE, "append launch failed: %s", hipGetErrorString(e));
+  if (first_frame_id) *first_frame_id = idx->n_frames;
+  for (int f = 1; f <= n_frames; ++f) idx->off.push_back(idx->n_rows + (int64_t)f * rpf);
+  idx->n_frames += n_frames;
+  idx->n_rows += new_rows;
+  idx->rpf = (idx->rpf == -1 || idx->rpf == rpf) ? rpf : 0;
+  return SS_OK;
+}
+
+size_t ss_retrieve_workspace_bytes(ss_index* const* idx, int32_t n_streams, const int32_t* n_q,
+                                   const ss_retrieve_params* params) {
+  if (check_batch(idx, n_streams, n_q, params) != SS_OK) return 0;
+  return batch_ws(idx, n_streams, n_q, params);
+}
+
+ss_status ss_retrieve(ss_index* const* idx, int32_t n_streams, const void* const* queries,
+                      const int32_t* n_q, const ss_retrieve_params* params, void* ws,
+                      size_t ws_bytes, void* stream, int64_t* frame_ids, int32_t* votes,
+                      float* mass, int32_t* n_out) {
+  return retrieve_common(idx, n_streams, queries, n_q, params, ws, ws_bytes, stream, frame_ids,
+                         votes, mass, n_out, nullptr);
+}
+
+ss_status ss_retrieve_debug(ss_index* const* idx, int32_t n_streams, const void* const* queries,
+                            const int32_t* n_q, const ss_retrieve_params* params, void* ws,
+                            size_t ws_bytes, void* stream, int64_t* frame_ids, int32_t* votes,
+                            float* mass, int32_t* n_out, const ss_debug_out* dbg) {
+  if (!dbg) return fail(SS_ERR_INVALID_ARGUMENT, "dbg is NULL");
+  return retrieve_common(idx, n_streams, queries, n_q, params, ws, ws_bytes, stream, frame_ids,
+                         votes, mass, n_out, dbg);
+}
+
+size_t ss_debug_scores_workspace_bytes(const ss_index* idx) {
+  if (!idx) return 0;
+  const ss_index_desc& d = idx->desc;
+  return align256((size_t)d.n_layers * d.n_kv_heads * 2 * (d.head_dim / 32) * 64 * 16);
+}
+
+ss_status ss_debug_scores(const ss_index* idx, const void* const* queries, int32_t n_q,
+                          int32_t layer, int32_t q_head, int32_t head_mode, int64_t row0,
+                          int64_t n_rows, float* out, void* ws, size_t ws_bytes, void* stream) {
+  if (!idx) return fail(SS_ERR_INVALID_ARGUMENT, "idx is NULL");
+  const ss_index_desc& d = idx->desc;
+  if (!queries) return fail(SS_ERR_INVALID_ARGUMENT, "queries is NULL");
+  for (int l = 0; l < d.n_layers; ++l)
+    if (!queries[l] || !aligned(queries[l], 16))
+      return fail(SS_ERR_INVALID_ARGUMENT, "queries[%d] NULL or not 16-byte aligned", l);
+  if (n_q < 1 || n_q > 4096) return fail(SS_ERR_INVALID_ARGUMENT, "n_q %d outside 1..4096", n_q);
+  if (head_mode != 0 && head_mode != 1) return fail(SS_ERR_INVALID_ARGUMENT, "head_mode must be 0 or 1");
+  if (head_mode == 1 && d.n_kv_heads > 8)
+    return fail(SS_ERR_UNSUPPORTED, "head_mode 1 supports at most 8 KV heads");
+  if (layer < 0 || layer >= d.n_layers) return fail(SS_ERR_INVALID_ARGUMENT, "layer out of range");
+  if (head_mode == 0 && (q_head < 0 || q_head >= d.n_q_heads))
+    return fail(SS_ERR_INVALID_ARGUMENT, "q_head out of range");
+  if (row0 < 0 || n_rows < 0 || row0 + n_rows > idx->n_rows)
+    return fail(SS_ERR_INVALID_ARGUMENT, "rows [%lld, %lld) outside the %lld stored rows",
+                (long long)row0, (long long)(row0 + n_rows), (long long)idx->n_rows);
+  if (!out && n_rows > 0) return fail(SS_ERR_INVALID_ARGUMENT, "out is NULL");
+  if (!ws || !aligned(ws, 256) || ws_bytes < ss_debug_scores_workspace_bytes(idx))
+    return fail(SS_ERR_WORKSPACE, "debug-scores workspace too small or misaligned");
+  ss::RetrievePlan p;
+  std::memset(&p, 0, sizeof p);
+  p.S = 1;
+  p.L = d.n_layers;
+  p.Hq = d.n_q_heads;
+  p.Hk = d.n_kv_heads;
+  p.G = p.Hq / p.Hk;
+  p.D = d.head_dim;
+  p.head_mode = head_mode;
+  p.NL = head_mode == 0 ? p.L * p.Hq : p.L;
+  p.ncol = head_mode == 0 ? p.G : 1;
+  p.ngs = head_mode == 0 ? p.Hk : 1;
+  p.chunk_rows = kChunkRows;
+  p.qB = static_cast<uint32_t*>(ws);
+  ss::StreamPlan& sp = p.st[0];
+  sp.keys = idx->dev.keys;
+  sp.row_stride = (int32_t)d.max_rows;
+  sp.nq = n_q;
+  double sc = 1.0 / ((double)n_q * std::sqrt((double)p.D));
+  if (head_mode == 1) sc /= (double)p.Hq;
+  sp.qscale = (float)sc;
+  for (int l = 0; l < p.L; ++l) sp.q[l] = static_cast<const uint16_t*>(queries[l]);
+  const hipError_t e =
+      ss::launch_debug_scores(p, layer, q_head, row0, n_rows, out, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SS_ERR_DEVICE, "debug scores launch failed: %s", hipGetErrorString(e));
+  return SS_OK;
+}
+
+ss_status ss_index_export(const ss_index* idx, void* rows_dev, int32_t* counts_dev, float* desc_dev,
+                          int64_t* frame_offsets_host, void* stream) {
+  if (!idx) return fail(SS_ERR_INVALID_ARGUMENT, "idx is NULL");
+  const ss_index_desc& d = idx->desc;
+  const hipStream_t hs = static_cast<hipStream_t>(stream);
+  const size_t lg = (size_t)d.n_layers * d.n_kv_heads;
+  if (frame_offsets_host)
+    std::memcpy(frame_offsets_host, idx->off.data(), idx->off.size() * sizeof(int64_t));
+  if (idx->n_rows > 0 && rows_dev) {
+    const size_t rb = (size_t)idx->n_rows * d.head_dim * 2;
+    const hipError_t e = hipMemcpy2DAsync(rows_dev, rb, idx->dev.keys, (size_t)d.max_rows * d.head_dim * 2,
+                                          rb, lg, hipMemcpyDeviceToDevice, hs);
+    if (e != hipSuccess) return fail(SS_ERR_DEVICE, "export rows: %s", hipGetErrorString(e));
+  }
+  if (idx->n_rows > 0 && counts_dev) {
+    const size_t rb = (size_t)idx->n_rows * 4;
+    const hipError_t e = hipMemcpy2DAsync(counts_dev, rb, idx->dev.counts, (size_t)d.max_rows * 4, rb, lg,
+                                          hipMemcpyDeviceToDevice, hs);
+    if (e != hipSuccess) return fail(SS_ERR_DEVICE, "export counts: %s", hipGetErrorString(e));
+  }
+  if (idx->n_frames > 0 && desc_dev) {
+    const hipError_t e = hipMemcpyAsync(desc_dev, idx->dev.desc,
+                                        (size_t)idx->n_frames * d.n_kv_heads * d.head_dim * 4,
+                                        hipMemcpyDeviceToDevice, hs);
+    if (e != hipSuccess) return fail(SS_ERR_DEVICE, "export descriptors: %s", hipGetErrorString(e));
+  }
+  return SS_OK;
+}
+
+ss_status ss_set_profile_events(void* ev_start, void* ev_stop) {
+  if ((ev_start == nullptr) != (ev_stop == nullptr))
+    return fail(SS_ERR_INVALID_ARGUMENT, "give both events or neither");
+  g_ev_start = static_cast<hipEvent_t>(ev_start);
+  g_ev_stop = static_cast<hipEvent_t>(ev_stop);
+  return SS_OK;
+}
+
+const char* ss_status_string(ss_status s) {
+  switch (s) {
+    case SS_OK: return "ok";
+    case SS_ERR_INVALID_ARGUMENT: return "invalid argument";
+    case SS_ERR_UNSUPPORTED: return "unsupported";
+    case SS_ERR_CAPACITY: return "capacity exceeded";
+    case SS_ERR_WORKSPACE: return "workspace too small";
+    case SS_ERR_DEVICE: return "device error";
+    case SS_ERR_INTERNAL: return "internal error";
+    default: return "unknown status";
+  }
+}
+
+const char* ss_last_error(void) { return g_err.c_str(); }
+
+int32_t ss_version(void) { return 1; }
+
+}  // extern "C"

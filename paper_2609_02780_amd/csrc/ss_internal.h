@@ -1,0 +1,136 @@
+// Internal declarations shared by the C-ABI layer (ss_api.cpp) and the gfx950
+// kernels (ss_kernels.hip).  Not part of the public interface.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace ss {
+
+// Streams handled by one launch of the retrieval pipeline (larger batches are
+// split by the host into groups of this size).
+constexpr int kMaxStreams = 32;
+constexpr int kMaxGroup = 16;        // G = H_q / H_kv: one 16-column MFMA B tile
+constexpr int kMaxTopK = 2048;
+constexpr int kMaxSelect = 64;
+constexpr int kMaxPool = 256;
+constexpr int kTile = 16;            // key rows per MFMA tile
+constexpr int kMaxTokensCompress = 256;
+constexpr int kMaxCentroids = 64;
+constexpr int kMaxLayers = 32;
+
+// The host-side RetrievePlan is never passed to a kernel as a whole; each
+// kernel receives a compact argument struct built from it.
+
+// Device view of one index arena.
+struct IndexDev {
+  uint16_t* keys;       // [L][H_kv][max_rows][d] bf16
+  int32_t* counts;      // [L][H_kv][max_rows]
+  float* desc;          // [max_frames][H_kv*d]
+  int32_t* frame_off;   // [max_frames+1]
+};
+
+// ---------------------------------------------------------------------------
+// Append
+// ---------------------------------------------------------------------------
+struct AppendArgs {
+  int L, Hk, D;
+  int n_frames, n_tokens;
+  int64_t max_rows;
+  int64_t row0;          // first destination row
+  int64_t frame0;        // first new frame id
+  int rows_per_frame;    // n_tokens raw, min(n_centroids, n_tokens) compressed
+  int n_centroids, n_iters;
+  const uint16_t* src[kMaxLayers];  // per layer [H_kv][n_frames*n_tokens][d]
+  IndexDev dst;
+};
+
+hipError_t launch_append(const AppendArgs& a, bool compress, hipStream_t st);
+
+// ---------------------------------------------------------------------------
+// Retrieval
+// ---------------------------------------------------------------------------
+struct StreamPlan {
+  const uint16_t* keys;
+  const int32_t* frame_off;
+  const float* desc;
+  int32_t row_stride;    // max_rows of the index
+  int32_t n;             // candidate rows
+  int32_t f;             // candidate frames
+  int32_t m;             // sampled rows
+  int32_t r;             // rank of the sample threshold
+  int32_t kk;            // min(top_k, n)
+  int32_t nq;
+  int32_t rpf;           // rows per frame when every frame has the same count, else 0
+  float qscale;          // 1 / (n_q sqrt(d)) (head_mode 0), further / H_q (head_mode 1)
+  const uint16_t* q[kMaxLayers];  // per layer query pointer [H_q][n_q][d]
+};
+
+struct RetrievePlan {
+  int S, L, Hq, Hk, G, D;
+  int head_mode;
+  int NL;                // lists per stream
+  int ncol;              // MFMA output columns used per item (G or 1)
+  int ngs;               // KV-head sets per layer: H_kv (head_mode 0) or 1
+  int top_k, n_select, pool, pool_mult;
+  int cap;               // candidate capacity per list
+  int k_max;             // max over streams of kk
+  int m_max, f_max;
+  int chunk_rows, samp_chunk;
+  int64_t full_total;    // sum over streams of NL * n
+  StreamPlan st[kMaxStreams];
+
+  // workspace carve (device pointers)
+  uint32_t* qB;          // [S][L][H_kv][2][d/32][64] uint4
+  uint32_t* tau;         // [S*NL]
+  uint32_t* cnt;         // [S*NL]
+  int32_t* flag;         // [S*NL]
+  float* samp;           // [S*NL][m_max]
+  uint64_t* cand;        // [S*NL][cap]
+  uint64_t* topk;        // [S*NL][k_max]
+  float* full;           // fallback scores, per stream base full_base[s]
+  int64_t full_base[kMaxStreams];
+  int32_t* votes;        // [S][f_max]
+  int64_t* massfx;       // [S][f_max]
+  uint64_t* rec_hi;      // [S][f_max] compacted (votes, mass, frame) records
+  uint64_t* rec_lo;
+  int32_t* pool_ids;     // [S][pool]
+  int32_t* pool_votes;   // [S][pool]
+  float* pool_mass;      // [S][pool]
+  int32_t* pool_n;       // [S]
+  float* gram;           // [S][pool][pool]
+
+  // outputs
+  int64_t* out_ids;
+  int32_t* out_votes;
+  float* out_mass;
+  int32_t* out_n;
+  int out_stride;        // n_select
+
+  // optional debug outputs
+  int32_t* dbg_topk_pos;
+  float* dbg_topk_score;
+  int32_t* dbg_vote_hist;
+  float* dbg_mass_hist;
+  int32_t* dbg_pool;
+  int32_t* dbg_pool_n;
+  int32_t* dbg_list_stats;
+  int dbg_hist_stride;   // largest max_frames of the batch
+
+  // profiling hook around the streaming kernel
+  hipEvent_t ev_start, ev_stop;
+};
+
+// Bytes of each workspace region for a plan; fills the plan's pointers when
+// `ws` is non-null.  Returns the total.
+size_t carve_workspace(RetrievePlan& p, void* ws);
+
+hipError_t launch_retrieve(RetrievePlan& p, hipStream_t st);
+
+// Scores of one list over a row range, same arithmetic as the retrieval.
+hipError_t launch_debug_scores(RetrievePlan& p, int layer, int q_head, int64_t row0,
+                               int64_t n_rows, float* out, hipStream_t st);
+
+}  // namespace ss

@@ -1,0 +1,214 @@
+"""Python binding over the C ABI.  PyTorch supplies device memory and streams only.
+
+Tensors passed in must live on the current HIP device.  bfloat16 data may be
+given as ``torch.bfloat16`` or as raw ``int16``/``uint16`` bit patterns.
+"""
+from __future__ import annotations
+
+import ctypes as C
+
+import torch
+
+from . import _lib as L
+
+_BF16_OK = (torch.bfloat16, torch.int16, torch.uint16)
+
+
+def _stream_handle(stream) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _check_bf16(t: torch.Tensor, shape, what: str) -> int:
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{what} must be a device tensor")
+    if t.dtype not in _BF16_OK:
+        raise ValueError(f"{what} must hold bfloat16 values (got {t.dtype})")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{what} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    return t.data_ptr()
+
+
+class ShallowIndex:
+    """One stream's shallow-layer key index in a device arena owned by this object."""
+
+    def __init__(self, n_layers: int, n_q_heads: int, n_kv_heads: int, head_dim: int,
+                 max_frames: int, max_rows: int, n_recent: int = 0, device=None):
+        self.desc = L.IndexDesc(n_layers, n_q_heads, n_kv_heads, head_dim, max_frames, max_rows, n_recent)
+        nbytes = L.lib().ss_index_required_bytes(C.byref(self.desc))
+        if nbytes == 0:
+            h = C.c_void_p()
+            L.check(L.lib().ss_index_create(C.byref(self.desc), None, 0, C.byref(h)))
+        dev = torch.device(device) if device is not None else torch.device("cuda", torch.cuda.current_device())
+        self.arena = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        self._h = C.c_void_p()
+        L.check(L.lib().ss_index_create(C.byref(self.desc), self.arena.data_ptr(), nbytes, C.byref(self._h)))
+        self.n_layers, self.n_q_heads, self.n_kv_heads, self.head_dim = n_layers, n_q_heads, n_kv_heads, head_dim
+
+    @property
+    def handle(self) -> C.c_void_p:
+        if self._h is None:
+            raise RuntimeError("index closed")
+        return self._h
+
+    def close(self) -> None:
+        if getattr(self, "_h", None) is not None:
+            L.check(L.lib().ss_index_destroy(self._h))
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def info(self) -> tuple[int, int]:
+        f, r = C.c_int64(), C.c_int64()
+        L.check(L.lib().ss_index_info(self.handle, C.byref(f), C.byref(r)))
+        return f.value, r.value
+
+    @property
+    def n_frames(self) -> int:
+        return self.info()[0]
+
+    @property
+    def n_rows(self) -> int:
+        return self.info()[1]
+
+    def append(self, layer_keys, n_frames: int, n_tokens: int, compress=None, stream=None) -> int:
+        """Append frames; ``layer_keys[l]`` is ``[H_kv][n_frames*n_tokens][d]`` bfloat16.
+        ``compress`` is ``None`` or ``(n_centroids, n_iters)``.  Returns the first frame id."""
+        shape = (self.n_kv_heads, n_frames * n_tokens, self.head_dim)
+        ptrs = [_check_bf16(t, shape, f"layer_keys[{l}]") for l, t in enumerate(layer_keys)]
+        if len(ptrs) != self.n_layers:
+            raise ValueError(f"expected {self.n_layers} key tensors, got {len(ptrs)}")
+        comp = L.Compress(*compress) if compress is not None else None
+        first = C.c_int64()
+        L.check(L.lib().ss_index_append(self.handle, L.ptr_array(ptrs), n_frames, n_tokens,
+                                        C.byref(comp) if comp is not None else None,
+                                        _stream_handle(stream), C.byref(first)))
+        return first.value
+
+    def export(self, stream=None) -> dict:
+        """Stored rows, member counts, descriptors and frame offsets (synchronises)."""
+        f, r = self.info()
+        dev = self.arena.device
+        rows = torch.empty((self.n_layers, self.n_kv_heads, r, self.head_dim), dtype=torch.int16, device=dev)
+        counts = torch.empty((self.n_layers, self.n_kv_heads, r), dtype=torch.int32, device=dev)
+        desc = torch.empty((f, self.n_kv_heads * self.head_dim), dtype=torch.float32, device=dev)
+        offs = (C.c_int64 * (f + 1))()
+        L.check(L.lib().ss_index_export(self.handle, rows.data_ptr(), counts.data_ptr(), desc.data_ptr(),
+                                        offs, _stream_handle(stream)))
+        torch.cuda.synchronize(dev)
+        return {"rows": rows.cpu().numpy().view("uint16"), "counts": counts.cpu().numpy(),
+                "desc": desc.cpu().numpy(), "frame_offsets": list(offs)}
+
+    def debug_scores(self, queries, layer: int, q_head: int, head_mode: int = 0, row0: int = 0,
+                     n_rows: int | None = None, stream=None) -> torch.Tensor:
+        """fp32 scores of one list over rows ``[row0, row0 + n_rows)`` (parity checks)."""
+        n_q = queries[0].shape[1]
+        qshape = (self.n_q_heads, n_q, self.head_dim)
+        qp = [_check_bf16(q, qshape, f"queries[{l}]") for l, q in enumerate(queries)]
+        if n_rows is None:
+            n_rows = self.n_rows - row0
+        out = torch.empty(max(n_rows, 1), dtype=torch.float32, device=self.arena.device)
+        wsb = L.lib().ss_debug_scores_workspace_bytes(self.handle)
+        ws = torch.empty(wsb, dtype=torch.uint8, device=self.arena.device)
+        L.check(L.lib().ss_debug_scores(self.handle, L.ptr_array(qp), n_q, layer, q_head, head_mode,
+                                        row0, n_rows, out.data_ptr(), ws.data_ptr(), wsb,
+                                        _stream_handle(stream)))
+        return out[:n_rows]
+
+
+class Retriever:
+    """Evidence retrieval over a batch of indices with identical shapes.
+
+    Holds the device workspace and output buffers, grown on demand, so repeated
+    calls allocate nothing once sizes are stable.
+    """
+
+    def __init__(self, indices, top_k: int, n_select: int, pool_mult: int = 4, head_mode: int = 0):
+        self.indices = list(indices)
+        self.params = L.RetrieveParams(top_k, n_select, pool_mult, head_mode)
+        self._ws = None
+        dev = self.indices[0].arena.device
+        S = len(self.indices)
+        self.frame_ids = torch.empty((S, n_select), dtype=torch.int64, device=dev)
+        self.votes = torch.empty((S, n_select), dtype=torch.int32, device=dev)
+        self.mass = torch.empty((S, n_select), dtype=torch.float32, device=dev)
+        self.n_out = torch.empty(S, dtype=torch.int32, device=dev)
+        self._handles = L.ptr_array([x.handle.value for x in self.indices])
+
+    def workspace_bytes(self, n_q) -> int:
+        nq = (C.c_int32 * len(self.indices))(*n_q)
+        need = L.lib().ss_retrieve_workspace_bytes(self._handles, len(self.indices), nq, C.byref(self.params))
+        if need == 0:
+            raise L.SSError(L.SS_ERR_INVALID_ARGUMENT, L.lib().ss_last_error().decode())
+        return need
+
+    def _marshal(self, queries):
+        S = len(self.indices)
+        if len(queries) != S:
+            raise ValueError(f"expected queries for {S} streams, got {len(queries)}")
+        ptrs, n_q = [], []
+        for s, (x, qs) in enumerate(zip(self.indices, queries)):
+            if len(qs) != x.n_layers:
+                raise ValueError(f"stream {s}: expected {x.n_layers} query tensors")
+            nq = qs[0].shape[1]
+            n_q.append(nq)
+            for l, q in enumerate(qs):
+                ptrs.append(_check_bf16(q, (x.n_q_heads, nq, x.head_dim), f"queries[{s}][{l}]"))
+        need = self.workspace_bytes(n_q)
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = torch.empty(need, dtype=torch.uint8, device=self.frame_ids.device)
+        return L.ptr_array(ptrs), (C.c_int32 * S)(*n_q)
+
+    def __call__(self, queries, stream=None):
+        """``queries[s][l]``: ``[H_q][n_q][d]`` bfloat16.  Returns device tensors
+        ``(frame_ids, votes, mass, n_out)`` (views of reused buffers)."""
+        qp, nq = self._marshal(queries)
+        L.check(L.lib().ss_retrieve(self._handles, len(self.indices), qp, nq, C.byref(self.params),
+                                    self._ws.data_ptr(), self._ws.numel(), _stream_handle(stream),
+                                    self.frame_ids.data_ptr(), self.votes.data_ptr(), self.mass.data_ptr(),
+                                    self.n_out.data_ptr()))
+        return self.frame_ids, self.votes, self.mass, self.n_out
+
+    def debug(self, queries, stream=None) -> dict:
+        """One retrieval with every intermediate (synchronises; parity checks only)."""
+        qp, nq = self._marshal(queries)
+        S = len(self.indices)
+        dev = self.frame_ids.device
+        p = self.params
+        NL = self.indices[0].n_layers * (self.indices[0].n_q_heads if p.head_mode == 0 else 1)
+        hist = max(x.desc.max_frames for x in self.indices)
+        pool = p.pool_mult * p.n_select
+        t = {
+            "topk_pos": torch.empty((S, NL, p.top_k), dtype=torch.int32, device=dev),
+            "topk_score": torch.empty((S, NL, p.top_k), dtype=torch.float32, device=dev),
+            "vote_hist": torch.empty((S, hist), dtype=torch.int32, device=dev),
+            "mass_hist": torch.empty((S, hist), dtype=torch.float32, device=dev),
+            "pool": torch.empty((S, pool), dtype=torch.int32, device=dev),
+            "pool_n": torch.empty(S, dtype=torch.int32, device=dev),
+            "list_stats": torch.empty((S, NL, 2), dtype=torch.int32, device=dev),
+        }
+        dbg = L.DebugOut(*(t[k].data_ptr() for k in ("topk_pos", "topk_score", "vote_hist", "mass_hist",
+                                                      "pool", "pool_n", "list_stats")))
+        L.check(L.lib().ss_retrieve_debug(self._handles, S, qp, nq, C.byref(p), self._ws.data_ptr(),
+                                          self._ws.numel(), _stream_handle(stream), self.frame_ids.data_ptr(),
+                                          self.votes.data_ptr(), self.mass.data_ptr(), self.n_out.data_ptr(),
+                                          C.byref(dbg)))
+        torch.cuda.synchronize(dev)
+        out = {k: v.cpu().numpy() for k, v in t.items()}
+        out.update(frame_ids=self.frame_ids.cpu().numpy(), votes=self.votes.cpu().numpy(),
+                   mass=self.mass.cpu().numpy(), n_out=self.n_out.cpu().numpy())
+        return out
+
+
+def set_profile_events(start, stop) -> None:
+    """Record ``start``/``stop`` (torch.cuda.Event) around the streaming scoring
+    kernel of later retrievals on this thread; ``None, None`` turns it off."""
+    a = start.cuda_event if start is not None else None
+    b = stop.cuda_event if stop is not None else None
+    L.check(L.lib().ss_set_profile_events(a, b))

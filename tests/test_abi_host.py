@@ -1,0 +1,177 @@
+"""Host-side tests of the C ABI: the library loads, exports every declared
+symbol, and rejects invalid calls before touching the device.  No GPU: every
+call here fails validation (or is a pure host query) and enqueues nothing."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "shallowstream.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2609_02780_amd import _lib
+    if not os.path.exists(_lib.LIB_PATH):
+        from paper_2609_02780_amd.build import build_library
+        build_library()
+    return _lib
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ss_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(L):
+    names = declared_functions()
+    assert len(names) >= 15
+    lib = L.lib()
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, missing
+    assert set(names) == set(L._SIGS), "binding signatures and header disagree"
+
+
+def desc(L, **kw):
+    d = dict(n_layers=4, n_q_heads=28, n_kv_heads=4, head_dim=128, max_frames=100, max_rows=19600, n_recent=0)
+    d.update(kw)
+    return L.IndexDesc(**d)
+
+
+FAKE = 0x7F0000000000     # 256-byte aligned stand-in address, never dereferenced here
+
+
+def test_required_bytes_and_layout(L):
+    lib = L.lib()
+    d = desc(L)
+    n = lib.ss_index_required_bytes(C.byref(d))
+    keys = 4 * 4 * 19600 * 128 * 2
+    counts = 4 * 4 * 19600 * 4
+    assert n >= keys + counts + 100 * 512 * 4 + 101 * 4
+    assert n % 256 == 0
+    for bad in (dict(head_dim=96), dict(n_q_heads=27), dict(n_q_heads=68, n_kv_heads=4),
+                dict(max_rows=0), dict(max_frames=0), dict(n_layers=0), dict(n_layers=33),
+                dict(n_kv_heads=16, n_q_heads=16), dict(n_recent=-1), dict(max_rows=2 ** 31)):
+        assert lib.ss_index_required_bytes(C.byref(desc(L, **bad))) == 0, bad
+
+
+def create(L, **kw):
+    lib = L.lib()
+    d = desc(L, **kw)
+    h = C.c_void_p()
+    st = lib.ss_index_create(C.byref(d), FAKE, lib.ss_index_required_bytes(C.byref(d)), C.byref(h))
+    assert st == 0, lib.ss_last_error()
+    return h
+
+
+def test_create_errors(L):
+    lib = L.lib()
+    d = desc(L)
+    n = lib.ss_index_required_bytes(C.byref(d))
+    h = C.c_void_p()
+    assert lib.ss_index_create(C.byref(d), None, n, C.byref(h)) == L.SS_ERR_INVALID_ARGUMENT
+    assert lib.ss_index_create(C.byref(d), FAKE + 8, n, C.byref(h)) == L.SS_ERR_INVALID_ARGUMENT
+    assert b"aligned" in lib.ss_last_error()
+    assert lib.ss_index_create(C.byref(d), FAKE, n - 1, C.byref(h)) == L.SS_ERR_CAPACITY
+    bad = desc(L, head_dim=80)
+    assert lib.ss_index_create(C.byref(bad), FAKE, n, C.byref(h)) == L.SS_ERR_UNSUPPORTED
+    assert lib.ss_index_create(C.byref(d), FAKE, n, None) == L.SS_ERR_INVALID_ARGUMENT
+
+
+def test_append_validation_leaves_index_unchanged(L):
+    lib = L.lib()
+    h = create(L, max_frames=4, max_rows=4 * 196)
+    ptrs = L.ptr_array([FAKE] * 4)
+    first = C.c_int64(-5)
+    # too many frames / rows
+    assert lib.ss_index_append(h, ptrs, 5, 196, None, None, C.byref(first)) == L.SS_ERR_CAPACITY
+    assert lib.ss_index_append(h, ptrs, 4, 197, None, None, C.byref(first)) == L.SS_ERR_CAPACITY
+    # misaligned and missing pointers
+    bad = L.ptr_array([FAKE, FAKE + 2, FAKE, FAKE])
+    assert lib.ss_index_append(h, bad, 1, 196, None, None, C.byref(first)) == L.SS_ERR_INVALID_ARGUMENT
+    assert b"layer_keys[1]" in lib.ss_last_error()
+    nul = L.ptr_array([FAKE, FAKE, None, FAKE])
+    assert lib.ss_index_append(h, nul, 1, 196, None, None, C.byref(first)) == L.SS_ERR_INVALID_ARGUMENT
+    assert lib.ss_index_append(h, ptrs, 0, 196, None, None, C.byref(first)) == L.SS_ERR_INVALID_ARGUMENT
+    # compression limits
+    comp = L.Compress(65, 10)
+    assert lib.ss_index_append(h, ptrs, 1, 196, C.byref(comp), None, C.byref(first)) == L.SS_ERR_UNSUPPORTED
+    comp = L.Compress(32, 101)
+    assert lib.ss_index_append(h, ptrs, 1, 196, C.byref(comp), None, C.byref(first)) == L.SS_ERR_INVALID_ARGUMENT
+    comp = L.Compress(32, 10)
+    assert lib.ss_index_append(h, ptrs, 1, 300, C.byref(comp), None, C.byref(first)) == L.SS_ERR_UNSUPPORTED
+    f, r = C.c_int64(-1), C.c_int64(-1)
+    assert lib.ss_index_info(h, C.byref(f), C.byref(r)) == 0
+    assert (f.value, r.value) == (0, 0) and first.value == -5
+    assert lib.ss_index_destroy(h) == 0
+
+
+def test_retrieve_validation(L):
+    lib = L.lib()
+    h1 = create(L)
+    h2 = create(L, n_q_heads=16, n_kv_heads=2)
+    idx = L.ptr_array([h1.value])
+    nq = (C.c_int32 * 1)(32)
+    prm = L.RetrieveParams(256, 16, 4, 0)
+    ws = lib.ss_retrieve_workspace_bytes(idx, 1, nq, C.byref(prm))
+    assert ws > 0 and ws % 256 == 0
+    q = L.ptr_array([FAKE] * 4)
+    outs = [FAKE] * 4
+
+    def call(idx_=idx, n=1, q_=q, nq_=nq, prm_=prm, w=FAKE, wb=ws):
+        return lib.ss_retrieve(idx_, n, q_, nq_, C.byref(prm_), w, wb, None, *outs)
+
+    assert call(w=None) == L.SS_ERR_WORKSPACE
+    assert call(wb=ws - 1) == L.SS_ERR_WORKSPACE
+    assert call(w=FAKE + 64) == L.SS_ERR_WORKSPACE
+    assert call(prm_=L.RetrieveParams(0, 16, 4, 0)) == L.SS_ERR_UNSUPPORTED
+    assert call(prm_=L.RetrieveParams(4096, 16, 4, 0)) == L.SS_ERR_UNSUPPORTED
+    assert call(prm_=L.RetrieveParams(256, 0, 4, 0)) == L.SS_ERR_UNSUPPORTED
+    assert call(prm_=L.RetrieveParams(256, 16, 0, 0)) == L.SS_ERR_INVALID_ARGUMENT
+    assert call(prm_=L.RetrieveParams(256, 64, 8, 0)) == L.SS_ERR_UNSUPPORTED
+    assert call(prm_=L.RetrieveParams(256, 16, 4, 2)) == L.SS_ERR_INVALID_ARGUMENT
+    assert call(nq_=(C.c_int32 * 1)(0)) == L.SS_ERR_INVALID_ARGUMENT
+    assert call(q_=L.ptr_array([FAKE, FAKE, FAKE + 4, FAKE])) == L.SS_ERR_INVALID_ARGUMENT
+    assert call(n=0) == L.SS_ERR_INVALID_ARGUMENT
+    both = L.ptr_array([h1.value, h2.value])
+    nq2 = (C.c_int32 * 2)(32, 32)
+    assert lib.ss_retrieve_workspace_bytes(both, 2, nq2, C.byref(prm)) == 0
+    assert b"shape" in lib.ss_last_error()
+    assert lib.ss_retrieve(idx, 1, q, nq, C.byref(prm), FAKE, ws, None, None, FAKE, FAKE, FAKE) == \
+        L.SS_ERR_INVALID_ARGUMENT
+    for h in (h1, h2):
+        lib.ss_index_destroy(h)
+
+
+def test_debug_scores_and_misc_validation(L):
+    lib = L.lib()
+    h = create(L)
+    q = L.ptr_array([FAKE] * 4)
+    wsb = lib.ss_debug_scores_workspace_bytes(h)
+    assert wsb == 4 * 4 * 2 * 4 * 64 * 16
+    # no rows stored yet: any non-empty range is out of bounds
+    assert lib.ss_debug_scores(h, q, 8, 0, 0, 0, 0, 1, FAKE, FAKE, wsb, None) == L.SS_ERR_INVALID_ARGUMENT
+    assert lib.ss_debug_scores(h, q, 8, 4, 0, 0, 0, 0, FAKE, FAKE, wsb, None) == L.SS_ERR_INVALID_ARGUMENT
+    assert lib.ss_debug_scores(h, q, 8, 0, 28, 0, 0, 0, FAKE, FAKE, wsb, None) == L.SS_ERR_INVALID_ARGUMENT
+    assert lib.ss_debug_scores(h, q, 8, 0, 0, 0, 0, 0, FAKE, FAKE, wsb - 1, None) == L.SS_ERR_WORKSPACE
+    assert lib.ss_set_profile_events(FAKE, None) == L.SS_ERR_INVALID_ARGUMENT
+    assert lib.ss_set_profile_events(None, None) == 0
+    assert lib.ss_status_string(0) == b"ok" and lib.ss_status_string(4) == b"workspace too small"
+    assert lib.ss_version() >= 1
+    assert lib.ss_index_destroy(None) == L.SS_ERR_INVALID_ARGUMENT
+    lib.ss_index_destroy(h)
+
+
+def test_workspace_grows_with_batch(L):
+    lib = L.lib()
+    hs = [create(L) for _ in range(3)]
+    prm = L.RetrieveParams(256, 16, 4, 0)
+    one = lib.ss_retrieve_workspace_bytes(L.ptr_array([hs[0].value]), 1, (C.c_int32 * 1)(8), C.byref(prm))
+    three = lib.ss_retrieve_workspace_bytes(L.ptr_array([h.value for h in hs]), 3, (C.c_int32 * 3)(8, 8, 8),
+                                            C.byref(prm))
+    assert three > one > 0
+    for h in hs:
+        lib.ss_index_destroy(h)

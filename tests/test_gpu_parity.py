@@ -1,0 +1,453 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Inputs come from the seeded generators in ``workloads``; expected values only
+from ``oracle``.  Tolerances: per-key scores within 1e-3 of the magnitude of
+their terms (fp32 accumulation of bf16 products); integer results (votes, row
+positions, frame ids) exact, with the boundary near-tie exemptions of
+``parity.staged_check``.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import oracle as O
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_02780_amd  # noqa: F401  (fails loudly without the built library)
+
+
+def _P():
+    import paper_2609_02780_amd as P
+    return P
+
+
+from parity import dev_bf16, score_scale, staged_check  # noqa: E402
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def make_pair(cfg, spec, keys, compress=None, n_recent=0, max_frames=None, max_rows=None):
+    P = _P()
+    T = cfg.tokens_per_frame
+    F = spec.n_frames
+    rpf = T if compress is None else min(compress[0], T)
+    gidx = P.ShallowIndex(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim,
+                          max_frames or F, max_rows or F * rpf, n_recent)
+    gidx.append([dev_bf16(k) for k in keys], F, T, compress)
+    oidx = O.Index(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, n_recent)
+    if compress is None:
+        oidx.append(keys, F, T)
+    return gidx, oidx
+
+
+def debug_run(gidxs, queries, top_k, n_select, pool_mult=4, head_mode=0):
+    P = _P()
+    r = P.Retriever(gidxs, top_k, n_select, pool_mult, head_mode)
+    qd = [[dev_bf16(q) for q in qs] for qs in queries]
+    return r.debug(qd)
+
+
+def c1():
+    cfg = W.CONFIGS["C1"]
+    spec = W.stream_specs(cfg)[0]
+    q, keys = W.make_stream(cfg, spec)
+    return cfg, spec, q, keys
+
+
+# ---------------------------------------------------------------------------
+
+
+def test_scores_c1():
+    cfg, spec, q, keys = c1()
+    log("scores C1")
+    gidx, oidx = make_pair(cfg, spec, keys)
+    S = O.score_lists(oidx, q)
+    D = score_scale(oidx, q)
+    qd = [dev_bf16(x) for x in q]
+    worst = 0.0
+    for l in range(cfg.n_layers):
+        for h in range(cfg.n_q_heads):
+            g = gidx.debug_scores(qd, l, h).cpu().numpy().astype(np.float64)
+            j = l * cfg.n_q_heads + h
+            err = np.abs(g - S[j])
+            assert np.all(err <= 1e-3 * D[j])
+            worst = max(worst, float(np.max(err / D[j])))
+    log("max |err|/D", worst)
+    assert worst < 1e-5       # the hi/lo query split keeps fp32-level accuracy
+
+
+def test_scores_ragged_row_range():
+    """A row range that starts mid-tile and ends in a ragged tail."""
+    cfg, spec, q, keys = c1()
+    gidx, oidx = make_pair(cfg, spec, keys)
+    S = O.score_lists(oidx, q)
+    qd = [dev_bf16(x) for x in q]
+    g = gidx.debug_scores(qd, 1, 3, row0=37, n_rows=501).cpu().numpy()
+    np.testing.assert_allclose(g, S[1 * 4 + 3][37:538], rtol=0, atol=1e-4)
+
+
+def test_descriptors_and_rows_c1():
+    cfg, spec, q, keys = c1()
+    gidx, oidx = make_pair(cfg, spec, keys)
+    ex = gidx.export()
+    np.testing.assert_allclose(ex["desc"], np.array(oidx.desc), rtol=0, atol=2e-6)
+    for l in range(cfg.n_layers):
+        np.testing.assert_array_equal(ex["rows"][l], keys[l])
+    assert ex["frame_offsets"] == [16 * i for i in range(65)]
+    assert np.all(ex["counts"] == 1)
+
+
+def test_retrieve_c1_staged_and_planted():
+    cfg, spec, q, keys = c1()
+    log("retrieve C1")
+    gidx, oidx = make_pair(cfg, spec, keys)
+    out = debug_run([gidx], [q], cfg.top_k, cfg.n_select)
+    rep = staged_check(oidx, q, out, 0, cfg.top_k, cfg.n_select)
+    log(rep)
+    assert rep["end_to_end_equal"]
+    planted = set(spec.planted)
+    assert out["frame_ids"][0, 0] in planted
+    assert planted <= set(out["frame_ids"][0].tolist())
+    assert out["list_stats"][0, :, 1].sum() == 0    # no list needed the fallback
+
+
+def test_zero_queries_tie_rule():
+    """All-zero queries: every score is 0, so each list keeps rows 0..k-1."""
+    cfg, spec, q, keys = c1()
+    gidx, oidx = make_pair(cfg, spec, keys)
+    zq = [np.zeros_like(x) for x in q]
+    out = debug_run([gidx], [zq], cfg.top_k, cfg.n_select)
+    for j in range(cfg.n_layers * cfg.n_q_heads):
+        np.testing.assert_array_equal(out["topk_pos"][0, j], np.arange(32))
+    assert out["vote_hist"][0, 0] == 128 and out["vote_hist"][0, 1] == 128
+    assert out["vote_hist"][0, 2:64].sum() == 0
+    assert out["n_out"][0] == 2 and out["frame_ids"][0, 0] == 0
+
+
+def test_fallback_too_many_candidates():
+    """Zero queries over 8192 rows: every row ties at the cut-off, the candidate
+    buffer overflows and the exact fallback must still return rows 0..k-1."""
+    cfg = W.Config("fb", 1, 2, 1, 64, 16, 1, 40, 3, n_frames=512)
+    spec = W.stream_specs(cfg)[0]
+    q, keys = W.make_stream(cfg, spec)
+    gidx, oidx = make_pair(cfg, spec, keys)
+    zq = [np.zeros_like(x) for x in q]
+    out = debug_run([gidx], [zq], cfg.top_k, cfg.n_select)
+    assert np.all(out["list_stats"][0, :, 1] == 1)
+    for j in range(2):
+        np.testing.assert_array_equal(out["topk_pos"][0, j], np.arange(40))
+    rep = staged_check(oidx, zq, out, 0, cfg.top_k, cfg.n_select)
+    assert rep["end_to_end_equal"]
+
+
+def test_fallback_too_few_candidates():
+    """Rows on the sample lattice score highest, so the sample cut-off keeps fewer
+    than k rows; the exact fallback must take over and match the oracle."""
+    P = _P()
+    L, Hq, Hk, d, T, F = 1, 1, 1, 64, 100, 1000
+    n = F * T
+    k = 512
+    E = max(8 * k, 2048)
+    r = min(k, 48)
+    m = max(r, -(-n * r // E))
+    rows = ((2 * np.arange(m) + 1) * n) // (2 * m)
+    rng = np.random.default_rng(11)
+    x = rng.standard_normal((1, n, d)).astype(np.float32) * 0.01
+    x[0, rows, 0] = 5.0 + rng.random(m).astype(np.float32)      # only sampled rows score high
+    keys = [W.bf16_bits(x)]
+    qv = np.zeros((Hq, 1, d), np.float32)
+    qv[0, 0, 0] = 1.0
+    q = [W.bf16_bits(qv)]
+    cfg = W.Config("few", L, Hq, Hk, d, T, 1, k, 4, n_frames=F)
+    spec = W.stream_specs(cfg)[0]
+    gidx, oidx = make_pair(cfg, spec, keys)
+    out = debug_run([gidx], [q], k, 4)
+    assert out["list_stats"][0, 0, 1] == 1
+    rep = staged_check(oidx, q, out, 0, k, 4)
+    log(rep)
+    assert rep.get("swaps", 0) == 0
+
+
+def test_head_mode_paper_reduction_c1():
+    """head_mode 1: scores averaged over all query heads, top-k per layer."""
+    cfg, spec, q, keys = c1()
+    gidx, oidx = make_pair(cfg, spec, keys)
+    qd = [dev_bf16(x) for x in q]
+    S = O.score_lists(oidx, q, 1)
+    D = score_scale(oidx, q, 1)
+    for l in range(cfg.n_layers):
+        g = gidx.debug_scores(qd, l, 0, head_mode=1).cpu().numpy()
+        assert np.all(np.abs(g - S[l]) <= 1e-3 * D[l])
+    out = debug_run([gidx], [q], 64, 4, 4, head_mode=1)
+    rep = staged_check(oidx, q, out, 0, 64, 4, 4, head_mode=1)
+    log(rep)
+    assert out["vote_hist"][0].sum() == cfg.n_layers * 64
+
+
+def test_k_beyond_rows_and_recent_window():
+    cfg = W.Config("small", 2, 4, 2, 64, 5, 3, 100, 3, n_frames=9, n_planted=1)
+    spec = W.stream_specs(cfg)[0]
+    q, keys = W.make_stream(cfg, spec)
+    gidx, oidx = make_pair(cfg, spec, keys, n_recent=2)
+    out = debug_run([gidx], [q], 100, 3)
+    n = 7 * 5
+    assert np.all(out["topk_pos"][0, :, n:] == -1)
+    assert out["vote_hist"][0].sum() == 8 * n
+    assert np.all(out["vote_hist"][0, 7:] == 0)
+    staged_check(oidx, q, out, 0, 100, 3)
+
+
+def test_no_candidates():
+    cfg = W.Config("none", 1, 2, 1, 64, 4, 2, 8, 3, n_frames=3)
+    spec = W.stream_specs(cfg)[0]
+    q, keys = W.make_stream(cfg, spec)
+    gidx, oidx = make_pair(cfg, spec, keys, n_recent=5)
+    out = debug_run([gidx], [q], 8, 3)
+    assert out["n_out"][0] == 0 and np.all(out["frame_ids"][0] == -1)
+    assert out["pool_n"][0] == 0
+
+
+def test_ragged_batch_one_call():
+    """Three streams of different lengths, token counts and recent windows, one
+    of them compressed, retrieved in one call; each checked on its own."""
+    P = _P()
+    base = W.Config("rag", 2, 8, 2, 128, 49, 6, 48, 5, n_frames=0)
+    lens, nrec, comp = [37, 120, 81], [0, 3, 0], [None, None, (8, 4)]
+    gidxs, oidxs, qs = [], [], []
+    for s, (F, nr, cp) in enumerate(zip(lens, nrec, comp)):
+        cfg = W.Config("rag", 2, 8, 2, 128, 49, 6 + 3 * s, 48, 5, n_frames=F, n_planted=2)
+        spec = W.StreamSpec(s, F, 2, cp, W.planted_frames(F, 2))
+        q, keys = W.make_stream(cfg, spec)
+        g, o = make_pair(cfg, spec, keys, compress=cp, n_recent=nr)
+        if cp is not None:
+            ex = g.export()
+            o.append_stored([ex["rows"][l] for l in range(cfg.n_layers)], [8] * F,
+                            [O.descriptor(O.decode_bf16(keys[-1][:, f * 49:(f + 1) * 49, :])) for f in range(F)])
+        gidxs.append(g)
+        oidxs.append(o)
+        qs.append(q)
+    out = debug_run(gidxs, qs, 48, 5)
+    for s in range(3):
+        rep = staged_check(oidxs[s], qs[s], out, s, 48, 5)
+        log(s, rep)
+
+
+def test_deterministic_repeat():
+    cfg, spec, q, keys = c1()
+    gidx, _ = make_pair(cfg, spec, keys)
+    a = debug_run([gidx], [q], cfg.top_k, cfg.n_select)
+    b = debug_run([gidx], [q], cfg.top_k, cfg.n_select)
+    for k in a:
+        np.testing.assert_array_equal(a[k], b[k])
+
+
+def test_append_in_pieces_equals_one_append():
+    cfg, spec, q, keys = c1()
+    P = _P()
+    g1, _ = make_pair(cfg, spec, keys)
+    g2 = P.ShallowIndex(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, 64, 1024)
+    T = cfg.tokens_per_frame
+    for f0, f1 in [(0, 10), (10, 11), (11, 64)]:
+        first = g2.append([dev_bf16(np.ascontiguousarray(k[:, f0 * T:f1 * T, :])) for k in keys], f1 - f0, T)
+        assert first == f0
+    e1, e2 = g1.export(), g2.export()
+    for k in ("rows", "counts", "desc"):
+        np.testing.assert_array_equal(e1[k], e2[k])
+    assert e1["frame_offsets"] == e2["frame_offsets"]
+
+
+def test_capacity_error_leaves_index_unchanged():
+    cfg, spec, q, keys = c1()
+    P = _P()
+    g = P.ShallowIndex(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, 10, 160)
+    T = cfg.tokens_per_frame
+    g.append([dev_bf16(np.ascontiguousarray(k[:, :8 * T, :])) for k in keys], 8, T)
+    with pytest.raises(P.SSError) as e:
+        g.append([dev_bf16(np.ascontiguousarray(k[:, :3 * T, :])) for k in keys], 3, T)
+    assert e.value.status == 3
+    assert g.info() == (8, 128)
+
+
+# ---------------------------------------------------------------------------
+# Compression (k-means at append)
+# ---------------------------------------------------------------------------
+
+
+def _kmeans_audit(ex, keys, cfg, frames, n_c, n_it):
+    """Where the oracle's decisions have a margin of at least 1e-4, the GPU's
+    bf16 centroids are within one bf16 unit and the counts are equal."""
+    T, d = cfg.tokens_per_frame, cfg.head_dim
+    checked = exempt = 0
+    for f in frames:
+        for l in range(cfg.n_layers):
+            for g in range(cfg.n_kv_heads):
+                X = O.decode_bf16(keys[l][g, f * T:(f + 1) * T, :])
+                C, cnt, dg = O.kmeans(X, n_c, n_it)
+                if min(dg["init_margin"], dg["assign_margin"]) < 1e-4:
+                    exempt += 1
+                    continue
+                want = O.round_bf16(C)
+                got = ex["rows"][l, g, f * n_c:(f + 1) * n_c, :]
+                diff = np.abs(got.astype(np.int32) - want.astype(np.int32))
+                assert diff.max() <= 1, (f, l, g)
+                np.testing.assert_array_equal(ex["counts"][l, g, f * n_c:(f + 1) * n_c], cnt)
+                checked += 1
+    return checked, exempt
+
+
+def test_compression_small_exact_cases():
+    """T <= n_centroids stores the tokens themselves in farthest-point order."""
+    cfg = W.Config("cs", 1, 2, 1, 64, 6, 2, 4, 2, n_frames=4)
+    spec = W.stream_specs(cfg)[0]
+    q, keys = W.make_stream(cfg, spec)
+    gidx, _ = make_pair(cfg, spec, keys, compress=(8, 3))
+    ex = gidx.export()
+    assert ex["frame_offsets"] == [0, 6, 12, 18, 24]
+    for f in range(4):
+        X = O.decode_bf16(keys[0][0, f * 6:(f + 1) * 6, :])
+        _, _, dg = O.kmeans(X, 8, 3)
+        np.testing.assert_array_equal(ex["rows"][0, 0, f * 6:(f + 1) * 6], keys[0][0, f * 6:(f + 1) * 6][dg["order"]])
+        assert np.all(ex["counts"][0, 0, f * 6:(f + 1) * 6] == 1)
+
+
+def test_compression_c3_shape_audit_and_retrieval():
+    """The C3 workload at 60 frames: k-means audit on every problem, then
+    retrieval parity on the GPU's stored centroids."""
+    base = W.CONFIGS["C3"]
+    cfg = W.Config("C3s", base.n_layers, base.n_q_heads, base.n_kv_heads, base.head_dim, 196, base.n_q,
+                   base.top_k, base.n_select, n_frames=60, n_planted=1, compress=(32, 10))
+    spec = W.stream_specs(cfg)[0]
+    q, keys = W.make_stream(cfg, spec)
+    log("C3-shape compressed append")
+    gidx, _ = make_pair(cfg, spec, keys, compress=(32, 10))
+    ex = gidx.export()
+    checked, exempt = _kmeans_audit(ex, keys, cfg, range(60), 32, 10)
+    log("k-means audit", checked, "checked", exempt, "exempt")
+    assert checked >= 0.5 * (checked + exempt)
+    oidx = O.Index(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim)
+    desc = [O.descriptor(O.decode_bf16(keys[-1][:, f * 196:(f + 1) * 196, :])) for f in range(60)]
+    oidx.append_stored([ex["rows"][l] for l in range(cfg.n_layers)], [32] * 60, desc)
+    np.testing.assert_allclose(ex["desc"], np.array(desc), atol=2e-6)
+    out = debug_run([gidx], [q], cfg.top_k, cfg.n_select)
+    rep = staged_check(oidx, q, out, 0, cfg.top_k, cfg.n_select)
+    log(rep)
+
+
+# ---------------------------------------------------------------------------
+# Full-size workloads
+# ---------------------------------------------------------------------------
+
+
+def _build_big(cfg, spec, q, block=600, compress=None):
+    P = _P()
+    T = cfg.tokens_per_frame
+    rpf = T if compress is None else compress[0]
+    gidx = P.ShallowIndex(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, spec.n_frames,
+                          spec.n_frames * rpf)
+    host = [[] for _ in range(cfg.n_layers)]
+    for f0 in range(0, spec.n_frames, block):
+        f1 = min(spec.n_frames, f0 + block)
+        kb = W.frame_block_keys(cfg, spec, q, f0, f1)
+        gidx.append([dev_bf16(k) for k in kb], f1 - f0, T, compress)
+        for l in range(cfg.n_layers):
+            host[l].append(kb[l])
+    torch.cuda.synchronize()
+    keys = [np.concatenate(h, axis=1) for h in host]
+    return gidx, keys
+
+
+def test_c2_full_staged():
+    cfg = W.CONFIGS["C2"]
+    spec = W.stream_specs(cfg)[0]
+    q = W.make_queries(cfg, 0, 0)
+    log("C2 build")
+    gidx, keys = _build_big(cfg, spec, q)
+    oidx = O.Index(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim)
+    oidx.append(keys, spec.n_frames, cfg.tokens_per_frame)
+    out = debug_run([gidx], [q], cfg.top_k, cfg.n_select)
+    log("C2 list stats: max candidates", out["list_stats"][0, :, 0].max(), "fallbacks",
+        out["list_stats"][0, :, 1].sum())
+    rep = staged_check(oidx, q, out, 0, cfg.top_k, cfg.n_select)
+    log(rep)
+    assert out["list_stats"][0, :, 1].sum() == 0
+    planted = set(spec.planted)
+    ranked = O.vote_pool(out["vote_hist"][0, :600].astype(np.int64), out["mass_hist"][0, :600].astype(np.float64), 600)
+    assert set(ranked[:len(planted)].tolist()) == planted            # P1
+    assert out["frame_ids"][0, 0] in planted                          # P2
+    out1 = debug_run([gidx], [q], cfg.top_k, cfg.n_select, pool_mult=1)
+    assert planted <= set(out1["frame_ids"][0].tolist())              # P3
+
+
+def test_c4_full_size_sampled():
+    """The 1-hour index at full size, in the launch configuration the benchmark
+    times: sampled lists checked against the oracle in full, every list by
+    properties, and the planted evidence."""
+    cfg = W.CONFIGS["C4"]
+    spec = W.stream_specs(cfg)[0]
+    q = W.make_queries(cfg, 0, 0)
+    log("C4 build")
+    gidx, keys = _build_big(cfg, spec, q)
+    P = _P()
+    r = P.Retriever([gidx], cfg.top_k, cfg.n_select)
+    qd = [[dev_bf16(x) for x in q]]
+    ids, v, m, n = r(qd)
+    torch.cuda.synchronize()
+    plain = ids.cpu().numpy().copy()
+    out = r.debug(qd)
+    np.testing.assert_array_equal(plain, out["frame_ids"])
+    stats = out["list_stats"][0]
+    log("C4 candidates per list: min", stats[:, 0].min(), "max", stats[:, 0].max(), "fallbacks", stats[:, 1].sum())
+    assert stats[:, 1].sum() == 0
+    NL = cfg.n_layers * cfg.n_q_heads
+    assert out["vote_hist"][0].sum() == NL * cfg.top_k
+    oidx = O.Index(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim)
+    oidx.append(keys, spec.n_frames, cfg.tokens_per_frame)
+    del keys
+    rep = {}
+    from parity import check_topk_list, check_pool, check_maxmin
+    N = oidx.candidate_rows()
+    qm = O.query_means(q)
+    for (l, h) in [(0, 0), (1, 9), (2, 17), (3, 27)]:
+        g = h // cfg.group
+        K = O.decode_bf16(oidx.rows(l)[g])
+        so = K @ qm[l][h] / math.sqrt(cfg.head_dim)
+        dsc = np.abs(K) @ np.abs(qm[l][h]) / math.sqrt(cfg.head_dim)
+        j = l * cfg.n_q_heads + h
+        check_topk_list(so, dsc, out["topk_pos"][0, j].astype(np.int64),
+                        out["topk_score"][0, j].astype(np.float64), cfg.top_k, rep, name=f"C4 list {j}")
+        del K
+    # votes from the GPU lists by the oracle's rule
+    lists = [out["topk_pos"][0, j].astype(np.int64) for j in range(NL)]
+    f_of = oidx.frame_of_row()
+    v_re = np.zeros(spec.n_frames, dtype=np.int64)
+    for p in lists:
+        np.add.at(v_re, f_of[p], 1)
+    assert np.array_equal(out["vote_hist"][0, :spec.n_frames], v_re)
+    gm = out["mass_hist"][0, :spec.n_frames].astype(np.float64)
+    m_re = np.zeros(spec.n_frames)
+    for j, p in enumerate(lists):
+        np.add.at(m_re, f_of[p], out["topk_score"][0, j].astype(np.float64))
+    np.testing.assert_allclose(gm, m_re, rtol=1e-5, atol=1e-5)
+    pn = int(out["pool_n"][0])
+    pool = out["pool"][0, :pn].astype(np.int64)
+    check_pool(pool, v_re, gm, 1e-5 * np.abs(m_re) + 1e-5, 4 * cfg.n_select, rep)
+    check_maxmin(pool, np.array(oidx.desc), cfg.n_select, out["frame_ids"][0, :int(out["n_out"][0])].astype(np.int64), rep)
+    log(rep)
+    planted = set(spec.planted)
+    assert out["frame_ids"][0, 0] in planted
+    ranked = O.vote_pool(v_re, gm, spec.n_frames)
+    assert set(ranked[:len(planted)].tolist()) == planted
