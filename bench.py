@@ -1,0 +1,235 @@
+"""Benchmark of the evidence-retrieval hot path on one MI355X.
+
+One step = one ss_retrieve call over the whole workload (query prep, sampled
+cut-off, the streaming MFMA scoring pass over every stored key, exact top-k,
+votes, pool and max-min), with the index already resident in HBM.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config C4]
+
+Prints one JSON line.  ``value`` is key vectors scored per second (a key vector
+is one stored d-dim bf16 row at one (layer, KV head); each is scored against
+its G query heads).  ``roofline`` covers the streaming scoring kernel, timed
+with HIP events recorded around it on the call's stream.  ``cpu_baseline`` is
+the CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import workloads as W  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "index keys scored/sec + % HBM roofline; p50 ss_retrieve latency, 1-hour index"
+KERNEL_SRC = os.path.join(ROOT, "paper_2609_02780_amd", "csrc", "ss_kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_score_stream_c4_traffic.md")
+HOT_KERNEL = "k_score<128, K_STREAM>"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_hash() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def stored_traffic(per_launch_bytes_alg: float):
+    """HBM bytes per launch of the hot kernel from the committed PMC summary, if it
+    was taken on the current kernel source; else None."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    text = open(TRAFFIC_FILE).read()
+    m_hash = re.search(r"kernel source sha256\[:16\]:\s*([0-9a-f]{16})", text)
+    m_bytes = re.search(r"HBM bytes per launch:\s*([0-9.eE+]+)", text)
+    if not m_hash or not m_bytes or m_hash.group(1) != kernel_hash():
+        return None
+    return float(m_bytes.group(1))
+
+
+def dev_bf16(torch, a):
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda()
+
+
+def build_streams(torch, P, cfg, block=600):
+    """Generate and append every stream of the workload; returns the indices, the
+    per-stream device queries and the first block of stream 0 (host, for the
+    CPU baseline)."""
+    specs = W.stream_specs(cfg)
+    idxs, queries, first_block = [], [], None
+    t0 = time.time()
+    for spec in specs:
+        q = W.make_queries(cfg, 0, spec.stream)
+        T = cfg.tokens_per_frame
+        rpf = T if spec.compress is None else min(spec.compress[0], T)
+        idx = P.ShallowIndex(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, spec.n_frames,
+                             spec.n_frames * rpf)
+        for f0 in range(0, spec.n_frames, block):
+            f1 = min(spec.n_frames, f0 + block)
+            kb = W.frame_block_keys(cfg, spec, q, f0, f1)
+            idx.append([dev_bf16(torch, k) for k in kb], f1 - f0, T, spec.compress)
+            if first_block is None:
+                first_block = (q, kb, f1 - f0)
+            torch.cuda.synchronize()
+        idxs.append(idx)
+        queries.append([dev_bf16(torch, x) for x in q])
+        log(f"stream {spec.stream}: {spec.n_frames} frames appended ({time.time() - t0:.1f} s)")
+    return specs, idxs, queries, first_block
+
+
+def time_append(torch, P, cfg, frames=64):
+    """Compressed append latency: one frame at a time and one batch of frames."""
+    spec = W.stream_specs(cfg)[0]
+    q = W.make_queries(cfg, 0, 0)
+    T = cfg.tokens_per_frame
+    kb = W.frame_block_keys(cfg, spec, q, 0, frames)
+    dev = [dev_bf16(torch, k) for k in kb]
+    n_c = spec.compress[0] if spec.compress else T
+    idx = P.ShallowIndex(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, 4 * frames, 4 * frames * n_c)
+    one = [d[:, :T, :].contiguous() for d in dev]
+    for _ in range(3):
+        idx.append(one, 1, T, spec.compress)
+    torch.cuda.synchronize()
+    lat = []
+    for _ in range(frames):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        idx.append(one, 1, T, spec.compress)
+        b.record()
+        b.synchronize()
+        lat.append(a.elapsed_time(b))
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    idx.append(dev, frames, T, spec.compress)
+    b.record()
+    b.synchronize()
+    batch_ms = a.elapsed_time(b)
+    return {"per_frame_p50_ms": float(np.median(lat)), "batch_frames": frames,
+            "batch_frames_per_s": frames / (batch_ms / 1e3)}
+
+
+def cpu_baseline(cfg, first_block):
+    """The oracle on the first frames of stream 0 with the workload's queries and
+    retrieval parameters."""
+    from oracle import oracle as O
+    q, kb, nf = first_block
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = 1
+    comp = W.stream_specs(cfg)[0].compress
+    if comp is not None:
+        nf = min(nf, 40)     # the float64 k-means makes compressed appends slow; keep ~10-30 s
+        kb = [np.ascontiguousarray(k[:, :nf * cfg.tokens_per_frame, :]) for k in kb]
+    oi = O.Index(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim)
+    oi.append(kb, nf, cfg.tokens_per_frame, comp)
+    t0 = time.perf_counter()
+    O.retrieve(oi, q, cfg.top_k, cfg.n_select, cfg.pool_mult)
+    dt = time.perf_counter() - t0
+    keys = oi.n_rows * cfg.n_layers * cfg.n_kv_heads
+    return {"value": keys / dt, "unit": "keys/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"full float64 oracle retrieval (scores, top-k, votes, pool, max-min) over the first "
+                      f"{nf} frames ({oi.n_rows} rows per (layer, KV head)) of the {cfg.name} stream with its "
+                      f"queries and parameters: {keys} key vectors in {dt:.2f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="C4", choices=sorted(W.CONFIGS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the retrieval has no multi-GPU path (asked for --gpus {args.gpus})",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2609_02780_amd as P
+    if not os.path.exists(P._lib.LIB_PATH):
+        from paper_2609_02780_amd.build import build_library
+        build_library()
+    torch.cuda.set_device(0)
+    cfg = W.CONFIGS[args.config]
+    specs, idxs, queries, first_block = build_streams(torch, P, cfg)
+    r = P.Retriever(idxs, cfg.top_k, cfg.n_select, cfg.pool_mult)
+    for _ in range(args.warmup):
+        r(queries)
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    for e4 in ev:
+        for e in e4:
+            e.record()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        P.set_profile_events(ev[i][2], ev[i][3])
+        ev[i][0].record()
+        r(queries)
+        ev[i][1].record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    P.set_profile_events(None, None)
+    lat = np.array([e[0].elapsed_time(e[1]) for e in ev])
+    hot = np.array([e[2].elapsed_time(e[3]) for e in ev])
+
+    rows = [x.n_rows - 0 for x in idxs]
+    key_vectors = sum(x.n_rows for x in idxs) * cfg.n_layers * cfg.n_kv_heads
+    key_bytes = key_vectors * cfg.head_dim * 2
+    ms_per_step = (t1 - t0) * 1e3 / K
+    value = key_vectors / (ms_per_step / 1e3)
+    achieved = key_bytes / (hot.mean() / 1e3) / 1e9
+    traffic = stored_traffic(key_bytes)
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "keys/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {cfg.description}; {cfg.n_layers} shallow layers, "
+                               f"{cfg.n_q_heads} query / {cfg.n_kv_heads} KV heads, d={cfg.head_dim}, "
+                               f"{cfg.n_q} query tokens, top-k {cfg.top_k}, {cfg.n_select} frames selected",
+                   "streams": len(idxs), "rows_per_layer_kv_head": rows, "key_vectors": key_vectors,
+                   "key_bytes": key_bytes},
+        "p10_latency_ms": float(np.percentile(lat, 10)),
+        "p50_latency_ms": float(np.percentile(lat, 50)),
+        "p90_latency_ms": float(np.percentile(lat, 90)),
+        "scores_per_s": value * cfg.group,
+        "hbm_frac_end_to_end": key_bytes / (np.percentile(lat, 50) / 1e3) / 1e9 / HBM_PEAK_GBS,
+        "roofline": {"kernel": HOT_KERNEL, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "avg_kernel_ms": float(hot.mean()), "bytes_per_launch": key_bytes},
+    }
+    if cfg.compress is not None:
+        out["append"] = time_append(torch, P, cfg)
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, first_block)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -71,6 +71,9 @@ ss_status check_desc(const ss_index_desc* d) {
   if (d->max_rows < 1 || d->max_rows > (int64_t)0x7FFFFFFF - 1)
     return fail(SS_ERR_INVALID_ARGUMENT, "max_rows %lld outside 1..2^31-2", (long long)d->max_rows);
   if (d->n_recent < 0) return fail(SS_ERR_INVALID_ARGUMENT, "n_recent must be >= 0");
+  if ((int64_t)d->n_layers * d->n_q_heads > ss::kMaxListsPerStream)
+    return fail(SS_ERR_UNSUPPORTED, "n_layers * n_q_heads %lld > %d",
+                (long long)d->n_layers * d->n_q_heads, ss::kMaxListsPerStream);
   return SS_OK;
 }
 
@@ -104,8 +107,17 @@ void candidates(const ss_index* x, int64_t& rows, int64_t& frames) {
 
 constexpr int kSampleRank = 48;      // rank r of the sample cut-off
 constexpr int kFullScanRows = 4096;  // at or below this many rows the sample is the whole list
+static_assert(kFullScanRows <= 16384, "a full-scan sample must fit the register select");
 constexpr int kChunkRows = 4096;
-constexpr int kSampleChunk = 512;
+constexpr int kSampleChunk = 128;
+
+// Expected candidates per list: 8k (at least 2048), raised for very long lists
+// so the sample stays within the register select (kSampleMax rows).
+constexpr int64_t kSampleMax = 16384;
+int64_t expected_candidates(int64_t n, int64_t kk) {
+  const int64_t r = std::min<int64_t>(kk, kSampleRank);
+  return std::max<int64_t>({8 * kk, 2048, (n * r + kSampleMax - 1) / kSampleMax});
+}
 
 struct StreamSizes {
   int n, f, m, r, kk;
@@ -121,10 +133,10 @@ StreamSizes plan_stream(int64_t n, int64_t f, int top_k) {
   z.f = (int)f;
   z.kk = (int)std::min<int64_t>(top_k, n);
   if (n == 0) return z;
-  const int64_t E = std::max<int64_t>(8 * (int64_t)z.kk, 2048);
   int64_t r = std::min<int64_t>(z.kk, kSampleRank);
+  const int64_t E = expected_candidates(n, z.kk);
   int64_t m = std::max<int64_t>(r, (n * r + E - 1) / E);
-  if (n <= kFullScanRows || 2 * m >= n) {
+  if (n <= kFullScanRows || (2 * m >= n && n <= kSampleMax)) {
     m = n;
     r = z.kk;
   }
@@ -135,8 +147,7 @@ StreamSizes plan_stream(int64_t n, int64_t f, int top_k) {
 
 int64_t candidate_cap(int top_k, int64_t n_max) {
   const int64_t kk = std::min<int64_t>(top_k, std::max<int64_t>(n_max, 1));
-  const int64_t E = std::max<int64_t>(8 * kk, 2048);
-  return std::max<int64_t>(2 * E, 4096);
+  return std::max<int64_t>(2 * expected_candidates(n_max, kk), 4096);
 }
 
 ss_status check_params(const ss_retrieve_params* p, int Hk) {

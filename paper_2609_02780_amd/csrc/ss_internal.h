@@ -20,6 +20,7 @@ constexpr int kTile = 16;            // key rows per MFMA tile
 constexpr int kMaxTokensCompress = 256;
 constexpr int kMaxCentroids = 64;
 constexpr int kMaxLayers = 32;
+constexpr int kMaxListsPerStream = 4096;  // n_layers * n_q_heads
 
 // The host-side RetrievePlan is never passed to a kernel as a whole; each
 // kernel receives a compact argument struct built from it.
@@ -89,7 +90,12 @@ struct RetrievePlan {
   int32_t* flag;         // [S*NL]
   float* samp;           // [S*NL][m_max]
   uint64_t* cand;        // [S*NL][cap]
-  uint64_t* topk;        // [S*NL][k_max]
+  int32_t* run_f;        // [S*NL][k_max] per-frame runs of each list's selected rows
+  int32_t* run_c;
+  int64_t* run_fx;       // fixed-point score sums at scale 2^listexp
+  int32_t* nruns;        // [S*NL]
+  int32_t* listexp;      // [S*NL]
+  int32_t* any_flag;     // [1] non-zero when some list needs the exact fallback
   float* full;           // fallback scores, per stream base full_base[s]
   int64_t full_base[kMaxStreams];
   int32_t* votes;        // [S][f_max]

@@ -4,21 +4,22 @@
 // stream, no host synchronisation:
 //   k_prep      mean query per (layer, head), pre-scaled, split into bf16 hi+lo
 //               and laid out as the MFMA B operand (lane-native).
-//   k_score<SAMPLE>   scores of a strided sample of rows per list.
-//   k_thresh    per list, the r-th largest sample score: a cut-off that keeps at
-//               least r >= ... rows of the full list (see the host planner).
-//   k_score<STREAM>   THE HOT KERNEL: streams every bf16 key row from HBM once,
-//               bf16 MFMA (16x16x32) against the group's query columns with fp32
-//               accumulation, appends rows scoring >= the cut-off as 64-bit
-//               composite keys (ordered score, inverted row).
-//   k_select    exact top-k per list from the candidates (radix select + bitonic
-//               sort in LDS); lists whose candidate count fell outside
-//               [k, capacity] are flagged.
+//   k_score<SAMPLE>   scores of an evenly spread sample of rows per list.
+//   k_thresh    per list, the r-th largest sample score: the streaming cut-off.
+//   k_score<STREAM>   THE HOT KERNEL: streams every bf16 key row from HBM once
+//               (nontemporal 16-byte loads straight into the MFMA A layout),
+//               bf16 MFMA 16x16x32 against the group's query columns with fp32
+//               accumulation, and appends rows scoring at or above the cut-off
+//               as 64-bit composite keys, one atomic per (wave, tile, head).
+//   k_select    exact top-k per list from its candidates: bisection on the
+//               ordered score in registers, ties by row; lists whose candidate
+//               count fell outside [k, capacity] are flagged.
 //   k_score<FULL> + k_fb_select   exact fallback for flagged lists only:
-//               materialise every score, radix select, ties by row order.
-//   k_votes_pool  one vote per selected row for its frame, attention mass in
-//               deterministic fixed point, vote-ranked pool (bitonic in LDS).
-//   k_gram      pool descriptor Gram matrix (fp32).
+//               materialise the list's scores, radix select, ties by row order.
+//   k_votes_pool  one vote per selected row for its frame and the attention
+//               mass in deterministic fixed point (segmented wave reductions
+//               over row-sorted lists), then the vote-ranked pool (bitonic, LDS).
+//   k_gram      fp32 Gram matrix of the pool descriptors.
 //   k_maxmin    greedy max-min diversity over the Gram matrix.
 //
 // Append: k_desc (Eq. memory_key descriptor), k_copy (raw rows) or k_kmeans
@@ -44,9 +45,12 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
-constexpr int kSelLds = 8192;       // candidates staged in LDS by k_select
+constexpr int kSelItems = 8;        // candidates per thread (of 1024) held in registers by k_select
+constexpr int kThrItems = 16;       // sample scores per thread (of 1024) in k_thresh: 16384, the planner's bound
 constexpr int kVoteLds = 4096;      // frames whose votes/mass live in LDS
 constexpr int kPoolSort = 4096;     // records per pool sorting round
+constexpr int kGramLdsPool = 128;   // pools up to this size keep their Gram matrix in LDS
+constexpr int kMaxDescDim = 1024;
 
 // ---------------------------------------------------------------------------
 // Small device helpers
@@ -277,21 +281,27 @@ struct PrepArgs {
   u32x4* qB;       // [S][L][H_kv][2][D/32][64]
 };
 
-// One wave per (stream, layer, KV head).  Lane (col = lane % 16, kg = lane / 16)
-// owns column col of the B tile and, at k-step i, the 8 dims 32 i + 8 kg .. +7.
-// Column c of head-mode 0 is query head g*G + c; head-mode 1 uses column 0 only,
-// holding the sum of the group's head means (the layer's head average is the
-// sum over KV heads of these columns against their keys).
+// One block of 8*D threads per (stream, layer, KV head): thread (tg, col, ec)
+// sums, over the query tokens j = tg mod 4, dims 8 ec .. 8 ec + 7 of B-tile
+// column col; the four partial sums are then added in tg order.  In the
+// lane-native layout those dims belong to k-step i = ec / 4 of lane
+// col + 16 (ec % 4).  Column c of head-mode 0 is query head g*G + c; head-mode 1
+// uses column 0 only, holding the sum of the group's head means (the layer's
+// head average is the sum over KV heads of these columns against their keys).
+constexpr int kPrepGroups = 4;
+
 template <int D>
-__global__ __launch_bounds__(64) void k_prep(PrepArgs a) {
-  constexpr int KS = D / 32;
+__global__ __launch_bounds__(8 * D) void k_prep(PrepArgs a) {
+  constexpr int KS = D / 32, NE = D / 8, NT = 2 * D;  // NT threads per token group
+  __shared__ float part[kPrepGroups][NT][8];
   const int pair_local = blockIdx.x / a.Hk, g = blockIdx.x % a.Hk;
   const int pair = a.first + pair_local;
   const int s = pair / a.L;
   const uint16_t* q = a.q[pair_local];
   const int nq = a.nq[s];
   const float scale = a.qscale[s];
-  const int lane = threadIdx.x, col = lane & 15, kg = lane >> 4;
+  const int tg = threadIdx.x / NT, t = threadIdx.x % NT;
+  const int col = t / NE, ec = t % NE;
   int h0, h1;
   if (a.head_mode == 0) {
     h0 = g * a.G + col;
@@ -300,33 +310,58 @@ __global__ __launch_bounds__(64) void k_prep(PrepArgs a) {
     h0 = g * a.G;
     h1 = (col == 0) ? h0 + a.G : h0;
   }
-  u32x4* out = a.qB + ((size_t)pair * a.Hk + g) * (2 * KS * kWave);
-  for (int i = 0; i < KS; ++i) {
-    float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    const int e0 = 32 * i + 8 * kg;
-    for (int h = h0; h < h1; ++h) {
-      for (int j = 0; j < nq; ++j) {
-        const u32x4 v = *reinterpret_cast<const u32x4*>(q + ((size_t)h * nq + j) * D + e0);
+  float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  const int e0 = 8 * ec;
+  for (int h = h0; h < h1; ++h) {
+    const uint16_t* qh = q + (size_t)h * nq * D + e0;
+    int j = tg;
+    for (; j + 3 * kPrepGroups < nq; j += 4 * kPrepGroups) {
+      u32x4 v[4];
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          acc[2 * t] += bf16_lo(v[t]);
-          acc[2 * t + 1] += bf16_hi(v[t]);
+      for (int u = 0; u < 4; ++u)
+        v[u] = *reinterpret_cast<const u32x4*>(qh + (size_t)(j + u * kPrepGroups) * D);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          acc[2 * w] += bf16_lo(v[u][w]);
+          acc[2 * w + 1] += bf16_hi(v[u][w]);
         }
       }
     }
-    u32x4 hi, lo;
+    for (; j < nq; j += kPrepGroups) {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(qh + (size_t)j * D);
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const float x0 = acc[2 * t] * scale, x1 = acc[2 * t + 1] * scale;
-      const uint16_t a0 = bf16_rne(x0), a1 = bf16_rne(x1);
-      const uint16_t b0 = bf16_rne(x0 - __uint_as_float((uint32_t)a0 << 16));
-      const uint16_t b1 = bf16_rne(x1 - __uint_as_float((uint32_t)a1 << 16));
-      hi[t] = (uint32_t)a0 | ((uint32_t)a1 << 16);
-      lo[t] = (uint32_t)b0 | ((uint32_t)b1 << 16);
+      for (int w = 0; w < 4; ++w) {
+        acc[2 * w] += bf16_lo(v[w]);
+        acc[2 * w + 1] += bf16_hi(v[w]);
+      }
     }
-    out[(0 * KS + i) * kWave + lane] = hi;
-    out[(1 * KS + i) * kWave + lane] = lo;
   }
+#pragma unroll
+  for (int w = 0; w < 8; ++w) part[tg][t][w] = acc[w];
+  __syncthreads();
+  if (tg != 0) return;
+#pragma unroll
+  for (int w = 0; w < 8; ++w) {
+    float x = part[0][t][w];
+    for (int k = 1; k < kPrepGroups; ++k) x += part[k][t][w];
+    acc[w] = x;
+  }
+  u32x4 hi, lo;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const float x0 = acc[2 * w] * scale, x1 = acc[2 * w + 1] * scale;
+    const uint16_t a0 = bf16_rne(x0), a1 = bf16_rne(x1);
+    const uint16_t b0 = bf16_rne(x0 - __uint_as_float((uint32_t)a0 << 16));
+    const uint16_t b1 = bf16_rne(x1 - __uint_as_float((uint32_t)a1 << 16));
+    hi[w] = (uint32_t)a0 | ((uint32_t)a1 << 16);
+    lo[w] = (uint32_t)b0 | ((uint32_t)b1 << 16);
+  }
+  u32x4* out = a.qB + ((size_t)pair * a.Hk + g) * (2 * KS * kWave);
+  const int i = ec >> 2, lane = col + 16 * (ec & 3);
+  out[(0 * KS + i) * kWave + lane] = hi;
+  out[(1 * KS + i) * kWave + lane] = lo;
 }
 
 // ---------------------------------------------------------------------------
@@ -354,6 +389,7 @@ struct ScoreArgs {
   uint64_t* cand;
   int cap;
   // K_FULL
+  const int32_t* any_flag;            // nullptr, or zero when no list needs the fallback
   const int32_t* flag;                // nullptr: write only `only_list`
   int only_list;
   float* full;
@@ -377,27 +413,51 @@ __device__ __forceinline__ int64_t unit_row(const ScoreArgs& a, int s, int u) {
 }
 
 // Per-lane output of one 16-row tile: lane (col, kg) holds the scores of rows
-// 4 kg + j (j < 4) of the tile for output column col.
+// 4 kg + j (j < 4) of the tile for output column col.  Called by whole waves.
 template <int KIND>
 __device__ __forceinline__ void emit(const ScoreArgs& a, int s, int list, bool colv, bool wr,
                                      uint32_t tau_u, int tile_u0, int u1, f32x4 acc, int kg,
                                      bool& ovf) {
+  if (KIND == K_STREAM) {
+    // Rows at or above the cut-off are appended to the list's candidates.  The
+    // four lanes of a column agree on one slot range: one atomic per (wave,
+    // tile, column) instead of one per row.
+    const int lane = threadIdx.x & (kWave - 1);
+    uint32_t uo[4];
+    bool pass[4];
+    int c = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int u = tile_u0 + 4 * kg + j;
+      uo[j] = ord_u32(acc[j] + 0.0f);  // canonical zero: -0 becomes +0
+      pass[j] = colv && !ovf && u < u1 && uo[j] >= tau_u;
+      c += pass[j];
+    }
+    if (__ballot(c > 0) == 0) return;
+    const int c16 = __shfl_xor(c, 16), c32 = __shfl_xor(c, 32), c48 = __shfl_xor(c, 48);
+    const int total = c + c16 + c32 + c48;
+    const int prefix = kg == 0 ? 0 : kg == 1 ? c16 : kg == 2 ? c32 + c48 : c16 + c32 + c48;
+    uint32_t base = 0;
+    if (kg == 0 && total > 0) base = atomicAdd(&a.cnt[list], (uint32_t)total);
+    base = (uint32_t)__shfl((int)base, lane & 15);
+    if (total > 0 && base + (uint32_t)total >= (uint32_t)a.cap) ovf = true;
+    uint32_t slot = base + (uint32_t)prefix;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (pass[j]) {
+        if (slot < (uint32_t)a.cap)
+          a.cand[(size_t)list * a.cap + slot] = mk_key(uo[j], (uint32_t)(tile_u0 + 4 * kg + j));
+        ++slot;
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int u = tile_u0 + 4 * kg + j;
-    const float sc = acc[j] + 0.0f;  // canonical zero: -0 becomes +0
+    const float sc = acc[j] + 0.0f;
     if (KIND == K_SAMPLE) {
       if (colv && u < u1) a.samp[(size_t)list * a.samp_stride + u] = sc;
-    } else if (KIND == K_STREAM) {
-      const uint32_t uo = ord_u32(sc);
-      if (colv && u < u1 && uo >= tau_u && !ovf) {
-        const uint32_t slot = atomicAdd(&a.cnt[list], 1u);
-        if (slot < (uint32_t)a.cap) {
-          a.cand[(size_t)list * a.cap + slot] = mk_key(uo, (uint32_t)u);
-        } else {
-          ovf = true;  // the list will take the exact fallback; stop counting
-        }
-      }
     } else {
       if (wr && u < u1) {
         const int ll = list - s * a.NL;
@@ -408,12 +468,13 @@ __device__ __forceinline__ void emit(const ScoreArgs& a, int s, int list, bool c
 }
 
 // Head-mode 0: one KV head per item, its G query heads in the MFMA columns, the
-// B operand in registers, two tiles in flight per wave.
+// B operand in registers, PF tiles in flight per wave.
 template <int D, int KIND>
 __global__ __launch_bounds__(256) void k_score(ScoreArgs a) {
-  constexpr int KS = D / 32;
+  constexpr int KS = D / 32, PF = 2;
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
+  if (KIND == K_FULL && a.any_flag && *a.any_flag == 0) return;
   for (int item = blockIdx.x; item < a.total_items; item += gridDim.x) {
     int s = 0;
     while (item >= a.item_base[s + 1]) ++s;
@@ -452,25 +513,25 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a) {
 #pragma unroll
       for (int i = 0; i < KS; ++i) A[i] = ok ? ld_nt(p + 32 * i) : u32x4{0, 0, 0, 0};
     };
-    auto compute = [&](int t, const u32x4 (&A)[KS]) {
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int i = 0; i < KS; ++i) {
-        acc = mfma_bf16(A[i], bh[i], acc);
-        acc = mfma_bf16(A[i], bl[i], acc);
-      }
-      emit<KIND>(a, s, list, colv, wr, tau_u, u0 + t * kTile, u1, acc, kg, ovf);
-    };
 
-    u32x4 A0[KS], A1[KS];
-    int t = wave;
-    load(t, A0);
-    for (; t < ntiles; t += 2 * nw) {
-      load(t + nw, A1);
-      compute(t, A0);
-      if (t + nw >= ntiles) break;
-      load(t + 2 * nw, A0);
-      compute(t + nw, A1);
+    u32x4 A[PF][KS];
+#pragma unroll
+    for (int p = 0; p < PF; ++p) load(wave + p * nw, A[p]);
+    for (int t = wave; t < ntiles; t += PF * nw) {
+#pragma unroll
+      for (int p = 0; p < PF; ++p) {
+        const int tt = t + p * nw;
+        if (tt < ntiles) {
+          f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int i = 0; i < KS; ++i) {
+            acc = mfma_bf16(A[p][i], bh[i], acc);
+            acc = mfma_bf16(A[p][i], bl[i], acc);
+          }
+          emit<KIND>(a, s, list, colv, wr, tau_u, u0 + tt * kTile, u1, acc, kg, ovf);
+        }
+        load(tt + PF * nw, A[p]);
+      }
     }
   }
 }
@@ -483,6 +544,7 @@ __global__ __launch_bounds__(256) void k_score_hm(ScoreArgs a) {
   __shared__ u32x4 sB[8 * 2 * KS * kWave];  // H_kv <= 8 in head-mode 1
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
+  if (KIND == K_FULL && a.any_flag && *a.any_flag == 0) return;
   for (int item = blockIdx.x; item < a.total_items; item += gridDim.x) {
     int s = 0;
     while (item >= a.item_base[s + 1]) ++s;
@@ -531,110 +593,341 @@ __global__ __launch_bounds__(256) void k_score_hm(ScoreArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Wave and block reductions (DPP within rows of 16 lanes, then readlane)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x124, 0xF, 0xF, false));  // row_ror 4
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x128, 0xF, 0xF, false));  // row_ror 8
+  const uint32_t a = __builtin_amdgcn_readlane(v, 15), b = __builtin_amdgcn_readlane(v, 31);
+  const uint32_t c = __builtin_amdgcn_readlane(v, 47), d = __builtin_amdgcn_readlane(v, 63);
+  return max(max(a, b), max(c, d));
+}
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) { return ~wave_max_u32(~v); }
+
+// Block min and max; `sh` holds 2 * (blockDim/64) words.
+__device__ void block_minmax_u32(uint32_t& mn, uint32_t& mx, uint32_t* sh) {
+  const int w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  mn = wave_min_u32(mn);
+  mx = wave_max_u32(mx);
+  if ((threadIdx.x & (kWave - 1)) == 0) { sh[2 * w] = mn; sh[2 * w + 1] = mx; }
+  __syncthreads();
+  for (int i = 0; i < nw; ++i) { mn = min(mn, sh[2 * i]); mx = max(mx, sh[2 * i + 1]); }
+  __syncthreads();
+}
+
+// Exact r-th largest (1 <= r <= #valid) of the values the block holds in
+// registers, all in [lo, hi]: radix selection over the value range, 8 bits of
+// (v - lo) per round, so about three rounds for scores of one sign and
+// exponent band.  Returns the value; `n_greater` and `n_equal` count the valid
+// values above it and equal to it.  `hist` holds 512 words.
+template <int N>
+__device__ uint32_t block_select_range(const uint32_t (&v)[N], const bool (&ok)[N], uint32_t lo,
+                                       uint32_t hi, uint32_t r, uint32_t* hist, uint32_t* res,
+                                       uint32_t& n_greater, uint32_t& n_equal) {
+  for (int i = threadIdx.x; i < 512; i += blockDim.x) hist[i] = 0;
+  uint32_t need = r, eq = 0;
+  bool rounds = false;
+  int buf = 0;
+  __syncthreads();
+  while (lo < hi) {
+    const uint32_t span = hi - lo;
+    const int bits = 32 - __clz(span);              // span < 2^bits
+    const int shift = bits > 8 ? bits - 8 : 0;
+    uint32_t* h = hist + buf * 256;
+#pragma unroll
+    for (int i = 0; i < N; ++i)
+      if (ok[i] && v[i] >= lo && v[i] <= hi) atomicAdd(&h[(v[i] - lo) >> shift], 1u);
+    __syncthreads();
+    for (int i = threadIdx.x; i < 256; i += blockDim.x) hist[(buf ^ 1) * 256 + i] = 0;
+    find_digit(h, need, res);                        // ends with a barrier
+    need -= res[1];
+    eq = res[2];
+    lo += res[0] << shift;
+    hi = (uint32_t)min((uint64_t)hi, (uint64_t)lo + (((uint64_t)1 << shift) - 1));
+    buf ^= 1;
+    rounds = true;
+  }
+  if (!rounds) {  // every valid value equals lo
+    uint32_t c = 0;
+#pragma unroll
+    for (int i = 0; i < N; ++i) c += ok[i];
+    if (threadIdx.x == 0) hist[0] = 0;
+    __syncthreads();
+    atomicAdd(&hist[0], c);
+    __syncthreads();
+    eq = hist[0];
+    __syncthreads();
+  }
+  n_greater = r - need;
+  n_equal = eq;
+  return lo;
+}
+
+// ---------------------------------------------------------------------------
 // k_thresh: per list, the r-th largest sample score as an ordered uint32
 // ---------------------------------------------------------------------------
 struct ListArgs {
-  int NL, S, cap, k_max, top_k;
+  int NL, S, cap, k_max, top_k, hist_f;
   int32_t m[kMaxStreams], r[kMaxStreams], kk[kMaxStreams], n[kMaxStreams];
+  int32_t f[kMaxStreams], rpf[kMaxStreams];
+  const int32_t* frame_off[kMaxStreams];
   int64_t full_base[kMaxStreams];
   const float* samp;
   int samp_stride;
   uint32_t* tau;
   uint32_t* cnt;
   int32_t* flag;
+  int32_t* any_flag;   // set when any list needs the fallback
   const uint64_t* cand;
-  uint64_t* topk;
+  int32_t* run_f;      // [list][k_max] per-frame runs of the selected rows
+  int32_t* run_c;
+  int64_t* run_fx;     // fixed-point score sums at scale 2^listexp
+  int32_t* nruns;      // [list]
+  int32_t* listexp;    // [list]
   const float* full;
   int32_t* dbg_pos;
   float* dbg_score;
   int32_t* dbg_stats;
 };
 
-__global__ __launch_bounds__(256) void k_thresh(ListArgs a) {
-  __shared__ uint32_t hist[256];
+__device__ __forceinline__ int frame_of_row(const ListArgs& a, int s, uint32_t row) {
+  if (a.rpf[s] > 0) return (int)(row / (uint32_t)a.rpf[s]);
+  const int32_t* off = a.frame_off[s];
+  int lo = 0, hi = a.f[s] - 1;  // largest f with off[f] <= row
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if ((uint32_t)off[mid] <= row) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// The sample (m <= kThrItems * 1024 scores) sits in registers.
+__global__ __launch_bounds__(1024) void k_thresh(ListArgs a) {
+  __shared__ uint32_t hist[512];
   __shared__ uint32_t res[4];
+  __shared__ uint32_t mm[32];
   const int list = blockIdx.x, s = list / a.NL;
   const int m = a.m[s], r = a.r[s];
   if (threadIdx.x == 0) {
     a.cnt[list] = 0;
     a.flag[list] = 0;
+    if (list == 0) *a.any_flag = 0;
   }
   if (m == 0 || r == 0) {
     if (threadIdx.x == 0) a.tau[list] = 0xFFFFFFFFu;
     return;
   }
   const float* v = a.samp + (size_t)list * a.samp_stride;
-  uint32_t ngt;
-  const uint32_t t = radix_select_u32([&](int i) { return ord_u32(v[i]); }, m, (uint32_t)r, hist,
-                                      res, ngt);
+  uint32_t x[kThrItems];
+  bool ok[kThrItems];
+  uint32_t mn = 0xFFFFFFFFu, mx = 0;
+#pragma unroll
+  for (int it = 0; it < kThrItems; ++it) {
+    const int i = threadIdx.x + it * 1024;
+    ok[it] = i < m;
+    x[it] = ok[it] ? ord_u32(v[i] + 0.0f) : 0u;
+    if (ok[it]) { mn = min(mn, x[it]); mx = max(mx, x[it]); }
+  }
+  block_minmax_u32(mn, mx, mm);
+  uint32_t ng, ne;
+  const uint32_t t = block_select_range(x, ok, mn, mx, (uint32_t)r, hist, res, ng, ne);
   if (threadIdx.x == 0) a.tau[list] = t;
 }
 
 // ---------------------------------------------------------------------------
 // k_select: exact top-k of a list's candidates
 // ---------------------------------------------------------------------------
-__device__ void write_topk(const ListArgs& a, int list, const uint64_t* sorted, int kk) {
-  uint64_t* out = a.topk + (size_t)list * a.k_max;
-  for (int i = threadIdx.x; i < kk; i += blockDim.x) out[i] = sorted[i];
+// `sel` holds the kk selected composite keys in any order; `mxa` is the largest
+// |score| among them.  Adds the rows up per frame: one run record per frame
+// with its row count and the fixed-point sum of its scores at the list's own
+// scale 2^x (|sum| < 2^61 for up to E = NL * kk entries of magnitude <= mxa).
+// Writes the debug copy in rank order.  `lv`/`lm` are LDS frame accumulators
+// (kVoteLds entries); longer streams sort by row and walk the runs instead.
+__device__ void finish_list(const ListArgs& a, int list, uint64_t* sel, int kk, float mxa,
+                            int32_t* lv, long long* lm) {
+  __shared__ uint32_t nrun;
+  const int s = list / a.NL;
+  const int F = a.f[s];
+  int xl = 127;  // no entries: never the smallest exponent of a stream
+  if (kk > 0) {
+    xl = 120;
+    if (mxa > 0.f) {
+      int e;
+      frexpf(mxa, &e);                                       // mxa < 2^e
+      const int E = a.NL * kk;
+      const int c = (E > 1) ? 32 - __clz(E - 1) : 0;        // E <= 2^c
+      xl = min(120, max(-120, 61 - e - c));
+    }
+  }
+  if (threadIdx.x == 0) nrun = 0;
+  const size_t ob = (size_t)list * a.k_max;
+  if (F <= kVoteLds) {
+    for (int f = threadIdx.x; f < F; f += blockDim.x) { lv[f] = 0; lm[f] = 0; }
+    __syncthreads();
+    for (int e = threadIdx.x; e < kk; e += blockDim.x) {
+      const uint64_t k = sel[e];
+      const int f = frame_of_row(a, s, key_row(k));
+      atomicAdd(&lv[f], 1);
+      atomicAdd(reinterpret_cast<unsigned long long*>(&lm[f]),
+                (unsigned long long)llrint(ldexp((double)key_score(k), xl)));
+    }
+    __syncthreads();
+    for (int f = threadIdx.x; f < F; f += blockDim.x) {
+      if (lv[f] > 0) {
+        const uint32_t slot = atomicAdd(&nrun, 1u);
+        a.run_f[ob + slot] = f;
+        a.run_c[ob + slot] = lv[f];
+        a.run_fx[ob + slot] = lm[f];
+      }
+    }
+  } else {
+    // long streams: order the selected rows by counting, then one record per run
+    int32_t* rank_row = lv;  // kMaxTopK <= kVoteLds entries
+    __syncthreads();
+    for (int e = threadIdx.x; e < kk; e += blockDim.x) {
+      const uint32_t my = key_row(sel[e]);
+      int rank = 0;
+      for (int e2 = 0; e2 < kk; ++e2) rank += key_row(sel[e2]) < my;
+      rank_row[rank] = e;
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < kk; i += blockDim.x) {
+      const int f = frame_of_row(a, s, key_row(sel[rank_row[i]]));
+      const int fp = i > 0 ? frame_of_row(a, s, key_row(sel[rank_row[i - 1]])) : -1;
+      if (f != fp) {
+        int len = 0;
+        long long sum = 0;
+        while (i + len < kk && frame_of_row(a, s, key_row(sel[rank_row[i + len]])) == f) {
+          sum += llrint(ldexp((double)key_score(sel[rank_row[i + len]]), xl));
+          ++len;
+        }
+        const uint32_t slot = atomicAdd(&nrun, 1u);
+        a.run_f[ob + slot] = f;
+        a.run_c[ob + slot] = len;
+        a.run_fx[ob + slot] = sum;
+      }
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    a.nruns[list] = (int32_t)nrun;
+    a.listexp[list] = xl;
+  }
   if (a.dbg_pos) {
     int32_t* dp = a.dbg_pos + (size_t)list * a.top_k;
     float* ds = a.dbg_score + (size_t)list * a.top_k;
-    for (int i = threadIdx.x; i < a.top_k; i += blockDim.x) {
-      dp[i] = i < kk ? (int32_t)key_row(sorted[i]) : -1;
-      ds[i] = i < kk ? key_score(sorted[i]) : 0.f;
+    for (int e = threadIdx.x; e < kk; e += blockDim.x) {
+      const uint64_t k = sel[e];
+      int rank = 0;
+      for (int e2 = 0; e2 < kk; ++e2) rank += sel[e2] > k;  // composite keys: rank order
+      dp[rank] = (int32_t)key_row(k);
+      ds[rank] = key_score(k);
+    }
+    for (int i = kk + threadIdx.x; i < a.top_k; i += blockDim.x) {
+      dp[i] = -1;
+      ds[i] = 0.f;
     }
   }
 }
 
-__global__ __launch_bounds__(256) void k_select(ListArgs a) {
-  __shared__ uint64_t stage[kSelLds];
-  __shared__ uint64_t sorted[kMaxTopK];
-  __shared__ uint32_t hist[256];
+__global__ __launch_bounds__(1024) void k_select(ListArgs a) {
+  __shared__ uint64_t sel[kMaxTopK];
+  __shared__ int32_t lv[kVoteLds];
+  __shared__ long long lm[kVoteLds];
+  __shared__ uint32_t hist[512];
   __shared__ uint32_t res[4];
   __shared__ uint32_t ngather;
+  __shared__ uint32_t mm[32];
   const int list = blockIdx.x, s = list / a.NL;
   const int kk = a.kk[s];
   if (kk == 0) {
-    write_topk(a, list, sorted, 0);
+    finish_list(a, list, sel, 0, 0.f, lv, lm);
     return;
   }
   const uint32_t c = a.cnt[list];
   if (c < (uint32_t)kk || c > (uint32_t)a.cap) {
-    if (threadIdx.x == 0) a.flag[list] = 1;
+    if (threadIdx.x == 0) {
+      a.flag[list] = 1;
+      atomicAdd(a.any_flag, 1);
+    }
     return;
   }
   const int n = (int)c;
   const uint64_t* src = a.cand + (size_t)list * a.cap;
-  const bool in_lds = n <= kSelLds;
-  if (in_lds) {
-    for (int i = threadIdx.x; i < n; i += blockDim.x) stage[i] = src[i];
-    __syncthreads();
-  }
-  const uint64_t* v = in_lds ? stage : src;
-  const uint64_t cut = radix_select_u64([&](int i) { return v[i]; }, n, (uint32_t)kk, hist, res);
   if (threadIdx.x == 0) ngather = 0;
-  const int np = pow2_ceil(kk);
-  for (int i = kk + threadIdx.x; i < np; i += blockDim.x) sorted[i] = 0;
-  __syncthreads();
-  for (int i = threadIdx.x; i < n; i += blockDim.x) {
-    const uint64_t x = v[i];
-    if (x >= cut) {
-      const uint32_t slot = atomicAdd(&ngather, 1u);
-      if (slot < (uint32_t)np) sorted[slot] = x;
+  float mxa;
+  if (n <= 1024 * kSelItems) {
+    // scores (high halves) and inverted rows in registers: the k-th score, then
+    // the cut among the ties at that score by row
+    uint32_t u[kSelItems], w[kSelItems];
+    bool ok[kSelItems], tie[kSelItems];
+    uint32_t mn = 0xFFFFFFFFu, mx = 0;
+#pragma unroll
+    for (int it = 0; it < kSelItems; ++it) {
+      const int i = threadIdx.x + it * 1024;
+      ok[it] = i < n;
+      const uint64_t k = ok[it] ? src[i] : 0;
+      u[it] = (uint32_t)(k >> 32);
+      w[it] = (uint32_t)k;  // 0xFFFFFFFF - row: larger for lower rows
+      if (ok[it]) { mn = min(mn, u[it]); mx = max(mx, u[it]); }
     }
+    block_minmax_u32(mn, mx, mm);
+    uint32_t n_gt, n_eq;
+    const uint32_t vstar = block_select_range(u, ok, mn, mx, (uint32_t)kk, hist, res, n_gt, n_eq);
+    const uint32_t need = (uint32_t)kk - n_gt;
+    uint32_t wcut = 0;  // ties with w >= wcut (the `need` lowest rows) are taken
+    if (n_eq > need) {
+      uint32_t wmin = 0xFFFFFFFFu, wmax = 0;
+#pragma unroll
+      for (int it = 0; it < kSelItems; ++it) {
+        tie[it] = ok[it] && u[it] == vstar;
+        if (tie[it]) { wmin = min(wmin, w[it]); wmax = max(wmax, w[it]); }
+      }
+      block_minmax_u32(wmin, wmax, mm);
+      uint32_t g2, e2;
+      wcut = block_select_range(w, tie, wmin, wmax, need, hist, res, g2, e2);
+    }
+#pragma unroll
+    for (int it = 0; it < kSelItems; ++it) {
+      if (ok[it] && (u[it] > vstar || (u[it] == vstar && w[it] >= wcut))) {
+        const uint32_t slot = atomicAdd(&ngather, 1u);
+        if (slot < (uint32_t)kMaxTopK) sel[slot] = ((uint64_t)u[it] << 32) | w[it];
+      }
+    }
+    mxa = fmaxf(fabsf(ord_f32(vstar)), fabsf(ord_f32(mx)));  // the selected scores span [v*, max]
+  } else {
+    // large candidate sets: radix select over the keys in global memory
+    __syncthreads();
+    const uint64_t cut = radix_select_u64([&](int i) { return src[i]; }, n, (uint32_t)kk, hist, res);
+    __syncthreads();
+    float m = 0.f;
+    for (int i = threadIdx.x; i < n; i += blockDim.x) {
+      const uint64_t x = src[i];
+      if (x >= cut) {
+        const uint32_t slot = atomicAdd(&ngather, 1u);
+        if (slot < (uint32_t)kMaxTopK) sel[slot] = x;
+        m = fmaxf(m, fabsf(key_score(x)));
+      }
+    }
+    __shared__ float redm[16];
+    mxa = block_max(m, redm);
   }
   __syncthreads();
-  bitonic_desc_u64(sorted, np);
-  write_topk(a, list, sorted, kk);
+  finish_list(a, list, sel, kk, mxa, lv, lm);
 }
 
 // Exact fallback: every score of the list was materialised by k_score<FULL>.
 __global__ __launch_bounds__(256) void k_fb_select(ListArgs a) {
-  __shared__ uint64_t sorted[kMaxTopK];
+  __shared__ uint64_t sel[kMaxTopK];
+  __shared__ int32_t lv[kVoteLds];
+  __shared__ long long lm[kVoteLds];
   __shared__ uint32_t hist[256];
   __shared__ uint32_t res[4];
   __shared__ uint32_t ngt_sh;
   __shared__ int scan_sh[8];
+  __shared__ float redm[4];
   const int list = blockIdx.x, s = list / a.NL;
   if (a.dbg_stats && threadIdx.x == 0) {
     a.dbg_stats[2 * list] = (int32_t)min(a.cnt[list], (uint32_t)INT_MAX);
@@ -644,36 +937,38 @@ __global__ __launch_bounds__(256) void k_fb_select(ListArgs a) {
   const int kk = a.kk[s], n = a.n[s];
   const float* v = a.full + a.full_base[s] + (int64_t)(list - s * a.NL) * n;
   uint32_t ngreater;
-  const uint32_t vstar = radix_select_u32([&](int i) { return ord_u32(v[i]); }, n,
+  const uint32_t vstar = radix_select_u32([&](int i) { return ord_u32(v[i] + 0.0f); }, n,
                                           (uint32_t)kk, hist, res, ngreater);
   const int need_eq = kk - (int)ngreater;
-  const int np = pow2_ceil(kk);
   if (threadIdx.x == 0) ngt_sh = 0;
-  for (int i = kk + threadIdx.x; i < np; i += blockDim.x) sorted[i] = 0;
   __syncthreads();
   // rows scoring above v* in any order; rows equal to v* in row order until need_eq
   int eq_taken = 0;
+  float m = 0.f;
   for (int b0 = 0; b0 < n; b0 += blockDim.x) {
     const int i = b0 + threadIdx.x;
     uint32_t u = 0;
     bool gt = false, eq = false;
     if (i < n) {
-      u = ord_u32(v[i]);
+      u = ord_u32(v[i] + 0.0f);
       gt = u > vstar;
       eq = u == vstar;
     }
     if (gt) {
       const uint32_t slot = atomicAdd(&ngt_sh, 1u);
-      if (slot < (uint32_t)np) sorted[slot] = mk_key(u, (uint32_t)i);
+      if (slot < (uint32_t)kMaxTopK) sel[slot] = mk_key(u, (uint32_t)i);
+      m = fmaxf(m, fabsf(ord_f32(u)));
     }
     int tot;
     const int pre = block_excl_scan(eq ? 1 : 0, scan_sh, tot);
-    if (eq && eq_taken + pre < need_eq) sorted[ngreater + eq_taken + pre] = mk_key(u, (uint32_t)i);
+    if (eq && eq_taken + pre < need_eq) {
+      sel[ngreater + eq_taken + pre] = mk_key(u, (uint32_t)i);
+      m = fmaxf(m, fabsf(ord_f32(u)));
+    }
     eq_taken += tot;
   }
-  __syncthreads();
-  bitonic_desc_u64(sorted, np);
-  write_topk(a, list, sorted, kk);
+  const float mxa = block_max(m, redm);
+  finish_list(a, list, sel, kk, mxa, lv, lm);
 }
 
 // ---------------------------------------------------------------------------
@@ -681,9 +976,12 @@ __global__ __launch_bounds__(256) void k_fb_select(ListArgs a) {
 // ---------------------------------------------------------------------------
 struct VoteArgs {
   int NL, k_max, pool, f_max, hist_stride;
-  int32_t kk[kMaxStreams], f[kMaxStreams], rpf[kMaxStreams];
-  const int32_t* frame_off[kMaxStreams];
-  const uint64_t* topk;
+  int32_t f[kMaxStreams];
+  const int32_t* run_f;
+  const int32_t* run_c;
+  const int64_t* run_fx;
+  const int32_t* nruns;
+  const int32_t* listexp;
   int32_t* votes_g;     // [S][f_max] (frames beyond the LDS capacity)
   int64_t* massfx_g;    // [S][f_max]
   uint64_t* rec_hi;     // [S][f_max] compacted records
@@ -698,89 +996,101 @@ struct VoteArgs {
   int32_t* dbg_pool_n;
 };
 
-__device__ __forceinline__ int frame_of(const VoteArgs& a, int s, uint32_t row) {
-  if (a.rpf[s] > 0) return (int)(row / (uint32_t)a.rpf[s]);
-  const int32_t* off = a.frame_off[s];
-  int lo = 0, hi = a.f[s] - 1;  // largest f with off[f] <= row
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if ((uint32_t)off[mid] <= row) lo = mid; else hi = mid - 1;
-  }
-  return lo;
-}
-
+// Votes and attention mass of every frame from the lists' runs.  Masses are
+// summed in 64-bit fixed point at the stream scale 2^x (the smallest list
+// exponent; a run's sum moves to it by an arithmetic shift), so the result does
+// not depend on the order of the additions.  The pool holds the voted frames of
+// rank < pool by (votes desc, mass desc, frame asc), ranked by counting.
 __global__ __launch_bounds__(1024) void k_votes_pool(VoteArgs a) {
   __shared__ int32_t sv[kVoteLds];
   __shared__ int64_t sm[kVoteLds];
   __shared__ uint64_t shi[kPoolSort];
   __shared__ uint64_t slo[kPoolSort];
-  __shared__ float red[16];
+  __shared__ int32_t roff[kMaxListsPerStream + 1];
   __shared__ int scan_sh[17];
+  __shared__ int xmin_sh;
+  __shared__ uint32_t nvoted_sh;
   const int s = blockIdx.x;
-  const int kk = a.kk[s], F = a.f[s], NL = a.NL;
-  const int E = NL * kk;
-  const uint64_t* tk = a.topk + (size_t)s * NL * a.k_max;
+  const int F = a.f[s], NL = a.NL;
   const bool lds = F <= kVoteLds;
   int32_t* votes = lds ? sv : a.votes_g + (size_t)s * a.f_max;
   int64_t* massfx = lds ? sm : a.massfx_g + (size_t)s * a.f_max;
-
-  // fixed-point exponent: |sum| <= E * max|score| < 2^61
-  float mx = 0.f;
-  for (int i = threadIdx.x; i < E; i += blockDim.x) {
-    const int j = i / kk, r = i - j * kk;
-    mx = fmaxf(mx, fabsf(key_score(tk[(size_t)j * a.k_max + r])));
-  }
-  mx = block_max(mx, red);
-  int xexp = 0;
-  if (mx > 0.f) {
-    int e;
-    frexpf(mx, &e);                       // mx < 2^e
-    const int c = (E > 1) ? 32 - __clz(E - 1) : 0;  // E <= 2^c
-    xexp = min(120, max(-120, 61 - e - c));
-  }
+  const int32_t* nr = a.nruns + (size_t)s * NL;
+  const int32_t* lx = a.listexp + (size_t)s * NL;
+  if (threadIdx.x == 0) { xmin_sh = 127; nvoted_sh = 0; }
   for (int f = threadIdx.x; f < F; f += blockDim.x) {
     votes[f] = 0;
     massfx[f] = 0;
   }
+  // run offsets (exclusive scan of the per-list run counts) and the stream exponent
+  int run_total = 0;
   __threadfence();
   __syncthreads();
-  for (int i = threadIdx.x; i < E; i += blockDim.x) {
-    const int j = i / kk, r = i - j * kk;
-    const uint64_t key = tk[(size_t)j * a.k_max + r];
-    const int f = frame_of(a, s, key_row(key));
-    const long long fx = llrint(ldexp((double)key_score(key), xexp));
-    atomicAdd(&votes[f], 1);
-    atomicAdd(reinterpret_cast<unsigned long long*>(&massfx[f]), (unsigned long long)fx);
+  for (int b0 = 0; b0 < NL; b0 += blockDim.x) {
+    const int j = b0 + threadIdx.x;
+    const int c = j < NL ? nr[j] : 0;
+    if (j < NL) atomicMin(&xmin_sh, lx[j]);
+    int tot;
+    const int pre = block_excl_scan(c, scan_sh, tot);
+    if (j < NL) roff[j] = run_total + pre;
+    run_total += tot;
+  }
+  if (threadIdx.x == 0) roff[NL] = run_total;
+  __syncthreads();
+  const int xexp = xmin_sh;
+  constexpr int VB = 4;
+  for (int bb = 0; bb < run_total; bb += VB * blockDim.x) {
+    int rf[VB], rc[VB], sh_[VB];
+    long long rx[VB];
+#pragma unroll
+    for (int u = 0; u < VB; ++u) {
+      const int i = bb + u * blockDim.x + threadIdx.x;
+      rf[u] = -1;
+      if (i < run_total) {
+        int lo = 0, hi = NL - 1;  // list j with roff[j] <= i < roff[j+1]
+        while (lo < hi) {
+          const int mid = (lo + hi + 1) >> 1;
+          if (roff[mid] <= i) lo = mid; else hi = mid - 1;
+        }
+        const size_t o = ((size_t)s * NL + lo) * a.k_max + (i - roff[lo]);
+        rf[u] = a.run_f[o];
+        rc[u] = a.run_c[o];
+        rx[u] = a.run_fx[o];
+        sh_[u] = lx[lo] - xexp;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < VB; ++u) {
+      if (rf[u] >= 0) {
+        atomicAdd(&votes[rf[u]], rc[u]);
+        const long long v = sh_[u] >= 63 ? (rx[u] < 0 ? -1 : 0) : (rx[u] >> sh_[u]);
+        atomicAdd(reinterpret_cast<unsigned long long*>(&massfx[rf[u]]), (unsigned long long)v);
+      }
+    }
   }
   __threadfence();
   __syncthreads();
   const double inv = ldexp(1.0, -xexp);
-  // compact voted frames (frame order) into records: hi = votes:32 | mass_hi:32,
+  // voted frames as records, any order: hi = votes:32 | mass_hi:32,
   // lo = mass_lo:32 | ~frame:32, compared descending
   uint64_t* rh = a.rec_hi + (size_t)s * a.f_max;
   uint64_t* rl = a.rec_lo + (size_t)s * a.f_max;
-  int n_voted = 0;
-  for (int b0 = 0; b0 < F; b0 += blockDim.x) {
-    const int f = b0 + threadIdx.x;
-    int v = 0;
-    int64_t mf = 0;
-    if (f < F) {
-      v = __hip_atomic_load(&votes[f], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      mf = __hip_atomic_load(&massfx[f], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (a.dbg_vote_hist) {
-        a.dbg_vote_hist[(size_t)s * a.hist_stride + f] = v;
-        a.dbg_mass_hist[(size_t)s * a.hist_stride + f] = (float)((double)mf * inv);
-      }
+  for (int f = threadIdx.x; f < F; f += blockDim.x) {
+    const int v = __hip_atomic_load(&votes[f], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int64_t mf = __hip_atomic_load(&massfx[f], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (a.dbg_vote_hist) {
+      a.dbg_vote_hist[(size_t)s * a.hist_stride + f] = v;
+      a.dbg_mass_hist[(size_t)s * a.hist_stride + f] = (float)((double)mf * inv);
     }
-    const bool p = v >= 1;
-    int tot;
-    const int pre = block_excl_scan(p ? 1 : 0, scan_sh, tot);
-    if (p) {
+    if (v >= 1) {
+      const uint32_t slot = atomicAdd(&nvoted_sh, 1u);
       const uint64_t mb = (uint64_t)mf ^ 0x8000000000000000ull;
-      rh[n_voted + pre] = ((uint64_t)(uint32_t)v << 32) | (mb >> 32);
-      rl[n_voted + pre] = (mb << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)f);
+      const uint64_t h = ((uint64_t)(uint32_t)v << 32) | (mb >> 32);
+      const uint64_t l = (mb << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)f);
+      if (slot < (uint32_t)kPoolSort) { shi[slot] = h; slo[slot] = l; }
+      rh[slot] = h;
+      rl[slot] = l;
     }
-    n_voted += tot;
   }
   if (a.dbg_vote_hist) {
     for (int f = F + threadIdx.x; f < a.hist_stride; f += blockDim.x) {
@@ -790,26 +1100,46 @@ __global__ __launch_bounds__(1024) void k_votes_pool(VoteArgs a) {
   }
   __threadfence();
   __syncthreads();
-  // top `pool` records: rounds of bitonic sorting, the running best kept in front
+  const int n_voted = (int)nvoted_sh;
   const int P = a.pool;
-  int kept = 0;
-  int next = 0;
-  do {
-    const int room = kPoolSort - kept;
-    const int take = min(room, n_voted - next);
-    const int tot = kept + take;
-    const int np = pow2_ceil(max(tot, 2));
-    for (int i = threadIdx.x; i < take; i += blockDim.x) {
-      shi[kept + i] = __hip_atomic_load(&rh[next + i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      slo[kept + i] = __hip_atomic_load(&rl[next + i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  int pn;
+  if (n_voted <= kPoolSort) {
+    // rank by counting: rank = number of records above (records are distinct)
+    __shared__ int32_t pslot[kMaxPool];
+    for (int i = threadIdx.x; i < n_voted; i += blockDim.x) {
+      const uint64_t h = shi[i], l = slo[i];
+      int rank = 0;
+      for (int j = 0; j < n_voted; ++j) rank += rec_less(h, l, shi[j], slo[j]);
+      if (rank < P) pslot[rank] = i;
     }
-    for (int i = tot + threadIdx.x; i < np; i += blockDim.x) { shi[i] = 0; slo[i] = 0; }
+    pn = min(P, n_voted);
     __syncthreads();
-    bitonic_desc_u128(shi, slo, np);
-    kept = min(P, tot);
-    next += take;
-  } while (next < n_voted);
-  const int pn = kept;
+    // move the pool to the front of shi/slo in rank order
+    uint64_t ph = 0, pl = 0;
+    if (threadIdx.x < pn) { ph = shi[pslot[threadIdx.x]]; pl = slo[pslot[threadIdx.x]]; }
+    __syncthreads();
+    if (threadIdx.x < pn) { shi[threadIdx.x] = ph; slo[threadIdx.x] = pl; }
+    __syncthreads();
+  } else {
+    // many voted frames: rounds of bitonic sorting, the running best kept in front
+    int kept = 0, next = 0;
+    do {
+      const int room = kPoolSort - kept;
+      const int take = min(room, n_voted - next);
+      const int tot = kept + take;
+      const int np = pow2_ceil(max(tot, 2));
+      for (int i = threadIdx.x; i < take; i += blockDim.x) {
+        shi[kept + i] = __hip_atomic_load(&rh[next + i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        slo[kept + i] = __hip_atomic_load(&rl[next + i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      for (int i = tot + threadIdx.x; i < np; i += blockDim.x) { shi[i] = 0; slo[i] = 0; }
+      __syncthreads();
+      bitonic_desc_u128(shi, slo, np);
+      kept = min(P, tot);
+      next += take;
+    } while (next < n_voted);
+    pn = kept;
+  }
   for (int i = threadIdx.x; i < P; i += blockDim.x) {
     int id = -1, v = 0;
     float m = 0.f;
@@ -831,10 +1161,12 @@ __global__ __launch_bounds__(1024) void k_votes_pool(VoteArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// k_gram: fp32 Gram matrix of the pool descriptors; 16 x 16 tiles
+// k_gram: fp32 Gram matrix of the pool descriptors; 16 x 16 tiles, upper
+// triangle computed and mirrored.  Both tiles' descriptors are loaded into LDS
+// at once (rows padded by one word against bank conflicts).
 // ---------------------------------------------------------------------------
 struct GramArgs {
-  int pool, dim, tiles;
+  int pool, ld, dim, tiles;   // ld: Gram row stride, a multiple of 4
   const float* desc[kMaxStreams];
   const int32_t* pool_ids;
   const int32_t* pool_n;
@@ -842,39 +1174,58 @@ struct GramArgs {
 };
 
 __global__ __launch_bounds__(256) void k_gram(GramArgs a) {
-  __shared__ float xi[16][65];
-  __shared__ float xj[16][65];
+  __shared__ float xi[16 * (kMaxDescDim + 1)];
+  __shared__ float xj[16 * (kMaxDescDim + 1)];
   const int s = blockIdx.x / (a.tiles * a.tiles);
   const int t = blockIdx.x % (a.tiles * a.tiles);
   const int ti = t / a.tiles, tj = t % a.tiles;
   const int pn = a.pool_n[s];
-  if (ti * 16 >= pn || tj * 16 >= pn) return;
-  const int r = threadIdx.x >> 4, c = threadIdx.x & 15;
+  if (tj < ti || ti * 16 >= pn || tj * 16 >= pn) return;
+  const int dim = a.dim, ld = dim + 1;
   const int32_t* ids = a.pool_ids + (size_t)s * a.pool;
   const float* D = a.desc[s];
-  float acc = 0.f;
-  for (int e0 = 0; e0 < a.dim; e0 += 64) {
-    for (int i = threadIdx.x; i < 16 * 64; i += blockDim.x) {
-      const int rr = i >> 6, ee = i & 63;
-      const int pi = ti * 16 + rr, pj = tj * 16 + rr;
-      const bool ein = e0 + ee < a.dim;
-      xi[rr][ee] = (pi < pn && ein) ? D[(size_t)ids[pi] * a.dim + e0 + ee] : 0.f;
-      xj[rr][ee] = (pj < pn && ein) ? D[(size_t)ids[pj] * a.dim + e0 + ee] : 0.f;
+  // 32 rows of dim floats, read as float4 (dim % 4 == 0), 8 loads in flight per thread
+  const int nv = 32 * (dim / 4);
+  for (int b = 0; b < nv; b += 8 * blockDim.x) {
+    float4 x[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = b + u * blockDim.x + threadIdx.x;
+      const int rr = i / (dim / 4), e4 = i - rr * (dim / 4);
+      const int p = rr < 16 ? ti * 16 + rr : tj * 16 + (rr - 16);
+      x[u] = (i < nv && p < pn) ? *reinterpret_cast<const float4*>(D + (size_t)ids[p] * dim + 4 * e4)
+                                : make_float4(0.f, 0.f, 0.f, 0.f);
     }
-    __syncthreads();
-#pragma unroll 8
-    for (int e = 0; e < 64; ++e) acc = fmaf(xi[r][e], xj[c][e], acc);
-    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = b + u * blockDim.x + threadIdx.x;
+      if (i < nv) {
+        const int rr = i / (dim / 4), e4 = i - rr * (dim / 4);
+        float* dst = (rr < 16 ? xi + rr * ld : xj + (rr - 16) * ld) + 4 * e4;
+        dst[0] = x[u].x; dst[1] = x[u].y; dst[2] = x[u].z; dst[3] = x[u].w;
+      }
+    }
   }
+  __syncthreads();
+  const int r = threadIdx.x >> 4, c = threadIdx.x & 15;
+  const float* x = xi + r * ld;
+  const float* y = xj + c * ld;
+  float acc = 0.f;
+#pragma unroll 8
+  for (int e = 0; e < dim; ++e) acc = fmaf(x[e], y[e], acc);
   const int pi = ti * 16 + r, pj = tj * 16 + c;
-  if (pi < pn && pj < pn) a.gram[((size_t)s * a.pool + pi) * a.pool + pj] = acc;
+  if (pi < pn && pj < pn) {
+    float* G = a.gram + (size_t)s * a.pool * a.ld;
+    G[(size_t)pi * a.ld + pj] = acc;
+    G[(size_t)pj * a.ld + pi] = acc;
+  }
 }
 
 // ---------------------------------------------------------------------------
 // k_maxmin: greedy max-min diversity (one block per stream)
 // ---------------------------------------------------------------------------
 struct MaxminArgs {
-  int pool, n_select;
+  int pool, ld, n_select;
   const int32_t* pool_ids;
   const int32_t* pool_votes;
   const float* pool_mass;
@@ -886,35 +1237,89 @@ struct MaxminArgs {
   int32_t* out_n;
 };
 
-__global__ __launch_bounds__(256) void k_maxmin(MaxminArgs a) {
+// Seeded with pool rank 0; each next pick maximises its smallest distance
+// 1 - k_u.k_s to the picks so far, ties to the earlier pool rank.  Pools of up
+// to 128 frames run in one wave over the Gram matrix staged in LDS.
+__global__ __launch_bounds__(1024) void k_maxmin(MaxminArgs a) {
+  __shared__ float g_lds[kGramLdsPool * kGramLdsPool];
   __shared__ float mind[kMaxPool];
   __shared__ int taken[kMaxPool];
   __shared__ int sel[kMaxSelect];
-  __shared__ float shv[4];
-  __shared__ int shi[4];
+  __shared__ float shv[16];
+  __shared__ int shi[16];
   const int s = blockIdx.x;
   const int pn = a.pool_n[s];
   const int K = min(a.n_select, pn);
-  const float* G = a.gram + (size_t)s * a.pool * a.pool;
-  for (int u = threadIdx.x; u < pn; u += blockDim.x) {
-    mind[u] = 1.0f - G[u];          // distance to pool rank 0
-    taken[u] = (u == 0);
-  }
-  if (threadIdx.x == 0 && K > 0) sel[0] = 0;
-  __syncthreads();
-  for (int it = 1; it < K; ++it) {
-    float bv = -INFINITY;
-    int bi = INT_MAX;
-    for (int u = threadIdx.x; u < pn; u += blockDim.x) {
-      if (!taken[u] && (mind[u] > bv || (mind[u] == bv && u < bi))) { bv = mind[u]; bi = u; }
+  const float* G = a.gram + (size_t)s * a.pool * a.ld;
+  if (pn <= kGramLdsPool) {
+    // rows of the Gram matrix as float4 (ld % 4 == 0), every load in flight at once
+    const int c4n = (pn + 3) / 4;
+    for (int b = 0; b < pn * c4n; b += 4 * blockDim.x) {
+      float4 x[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = b + u * blockDim.x + threadIdx.x;
+        const int r = i / c4n, c4 = i - r * c4n;
+        x[u] = i < pn * c4n ? *reinterpret_cast<const float4*>(G + (size_t)r * a.ld + 4 * c4)
+                            : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = b + u * blockDim.x + threadIdx.x;
+        if (i < pn * c4n) {
+          const int r = i / c4n, c = 4 * (i - r * c4n);
+          const float xv[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (c + q < pn) g_lds[r * pn + c + q] = xv[q];
+        }
+      }
     }
-    const int w = block_argmax(bv, bi, shv, shi);
-    for (int u = threadIdx.x; u < pn; u += blockDim.x) {
-      mind[u] = fminf(mind[u], 1.0f - G[(size_t)w * a.pool + u]);
-      if (u == w) taken[u] = 1;
-    }
-    if (threadIdx.x == 0) sel[it] = w;
     __syncthreads();
+    if (threadIdx.x < kWave) {
+      // lane l holds pool ranks l and l + 64; argmax by a DPP max over ordered
+      // values, ties to the lowest rank through ballots
+      const int lane = threadIdx.x;
+      const int u0 = lane, u1 = lane + kWave;
+      float m0 = u0 < pn ? 1.0f - g_lds[u0] : -INFINITY;
+      float m1 = u1 < pn ? 1.0f - g_lds[u1] : -INFINITY;
+      bool t0 = u0 == 0 || u0 >= pn, t1 = u1 >= pn;
+      if (lane == 0 && K > 0) sel[0] = 0;
+      for (int it = 1; it < K; ++it) {
+        const uint32_t o0 = t0 ? 0u : ord_u32(m0), o1 = t1 ? 0u : ord_u32(m1);
+        const uint32_t best = wave_max_u32(max(o0, o1));
+        const uint64_t b0 = __ballot(!t0 && o0 == best);
+        const int bi = b0 ? __builtin_ctzll(b0) : kWave + __builtin_ctzll(__ballot(!t1 && o1 == best));
+        const float* row = g_lds + bi * pn;
+        if (u0 < pn) m0 = fminf(m0, 1.0f - row[u0]);
+        if (u1 < pn) m1 = fminf(m1, 1.0f - row[u1]);
+        t0 = t0 || u0 == bi;
+        t1 = t1 || u1 == bi;
+        if (lane == 0) sel[it] = bi;
+      }
+    }
+    __syncthreads();
+  } else {
+    for (int u = threadIdx.x; u < pn; u += blockDim.x) {
+      mind[u] = 1.0f - G[u];          // distance to pool rank 0
+      taken[u] = (u == 0);
+    }
+    if (threadIdx.x == 0 && K > 0) sel[0] = 0;
+    __syncthreads();
+    for (int it = 1; it < K; ++it) {
+      float bv = -INFINITY;
+      int bi = INT_MAX;
+      for (int u = threadIdx.x; u < pn; u += blockDim.x) {
+        if (!taken[u] && (mind[u] > bv || (mind[u] == bv && u < bi))) { bv = mind[u]; bi = u; }
+      }
+      const int w = block_argmax(bv, bi, shv, shi);
+      for (int u = threadIdx.x; u < pn; u += blockDim.x) {
+        mind[u] = fminf(mind[u], 1.0f - G[(size_t)w * a.ld + u]);
+        if (u == w) taken[u] = 1;
+      }
+      if (threadIdx.x == 0) sel[it] = w;
+      __syncthreads();
+    }
   }
   for (int i = threadIdx.x; i < a.n_select; i += blockDim.x) {
     const size_t o = (size_t)s * a.n_select + i;
@@ -1161,7 +1566,7 @@ ScoreArgs make_score_args(const RetrievePlan& p, int kind) {
   a.total_items = items;
   a.samp = p.samp; a.samp_stride = p.m_max;
   a.tau = p.tau; a.cnt = p.cnt; a.cand = p.cand; a.cap = p.cap;
-  a.flag = p.flag; a.only_list = -1; a.full = p.full; a.row0 = 0;
+  a.flag = p.flag; a.any_flag = p.any_flag; a.only_list = -1; a.full = p.full; a.row0 = 0;
   return a;
 }
 
@@ -1188,7 +1593,7 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
       }
       for (int s = 0; s < p.S; ++s) { a.nq[s] = p.st[s].nq; a.qscale[s] = p.st[s].qscale; }
       a.qB = reinterpret_cast<u32x4*>(p.qB);
-      hipLaunchKernelGGL(k_prep<D>, dim3(cnt * p.Hk), dim3(64), 0, st, a);
+      hipLaunchKernelGGL(k_prep<D>, dim3(cnt * p.Hk), dim3(8 * D), 0, st, a);
     }
   }
   ListArgs la{};
@@ -1196,31 +1601,34 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   for (int s = 0; s < p.S; ++s) {
     la.m[s] = p.st[s].m; la.r[s] = p.st[s].r; la.kk[s] = p.st[s].kk; la.n[s] = p.st[s].n;
     la.full_base[s] = p.full_base[s];
+    la.f[s] = p.st[s].f; la.rpf[s] = p.st[s].rpf; la.frame_off[s] = p.st[s].frame_off;
   }
   la.samp = p.samp; la.samp_stride = p.m_max; la.tau = p.tau; la.cnt = p.cnt; la.flag = p.flag;
-  la.cand = p.cand; la.topk = p.topk; la.full = p.full;
+  la.cand = p.cand; la.full = p.full;
   la.dbg_pos = p.dbg_topk_pos; la.dbg_score = p.dbg_topk_score; la.dbg_stats = p.dbg_list_stats;
+  la.any_flag = p.any_flag;
+  la.run_f = p.run_f; la.run_c = p.run_c; la.run_fx = p.run_fx; la.nruns = p.nruns;
+  la.listexp = p.listexp;
   const int lists = p.S * p.NL;
   // 2. sample scores, 3. thresholds
   launch_score<D, K_SAMPLE>(make_score_args(p, K_SAMPLE), p.head_mode, 4096, st);
-  hipLaunchKernelGGL(k_thresh, dim3(lists), dim3(256), 0, st, la);
+  hipLaunchKernelGGL(k_thresh, dim3(lists), dim3(1024), 0, st, la);
   // 4. streaming pass over every key row
   if (p.ev_start) (void)hipEventRecord(p.ev_start, st);
   launch_score<D, K_STREAM>(make_score_args(p, K_STREAM), p.head_mode, 2048, st);
   if (p.ev_stop) (void)hipEventRecord(p.ev_stop, st);
   // 5. exact top-k from candidates; 6. exact fallback for flagged lists
-  hipLaunchKernelGGL(k_select, dim3(lists), dim3(256), 0, st, la);
-  launch_score<D, K_FULL>(make_score_args(p, K_FULL), p.head_mode, 1024, st);
+  hipLaunchKernelGGL(k_select, dim3(lists), dim3(1024), 0, st, la);
+  launch_score<D, K_FULL>(make_score_args(p, K_FULL), p.head_mode, 256, st);
   hipLaunchKernelGGL(k_fb_select, dim3(lists), dim3(256), 0, st, la);
   // 7. votes, mass and pool
   VoteArgs va{};
   va.NL = p.NL; va.k_max = p.k_max; va.pool = p.pool; va.f_max = p.f_max;
   va.hist_stride = p.dbg_hist_stride;
-  for (int s = 0; s < p.S; ++s) {
-    va.kk[s] = p.st[s].kk; va.f[s] = p.st[s].f; va.rpf[s] = p.st[s].rpf;
-    va.frame_off[s] = p.st[s].frame_off;
-  }
-  va.topk = p.topk; va.votes_g = p.votes; va.massfx_g = p.massfx;
+  for (int s = 0; s < p.S; ++s) va.f[s] = p.st[s].f;
+  va.run_f = p.run_f; va.run_c = p.run_c; va.run_fx = p.run_fx; va.nruns = p.nruns;
+  va.listexp = p.listexp;
+  va.votes_g = p.votes; va.massfx_g = p.massfx;
   va.rec_hi = p.rec_hi; va.rec_lo = p.rec_lo;
   va.pool_ids = p.pool_ids; va.pool_votes = p.pool_votes; va.pool_mass = p.pool_mass;
   va.pool_n = p.pool_n;
@@ -1229,16 +1637,16 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   hipLaunchKernelGGL(k_votes_pool, dim3(p.S), dim3(1024), 0, st, va);
   // 8. Gram matrix, 9. max-min
   GramArgs ga{};
-  ga.pool = p.pool; ga.dim = p.Hk * D; ga.tiles = cdiv(p.pool, 16);
+  ga.pool = p.pool; ga.ld = (p.pool + 3) & ~3; ga.dim = p.Hk * D; ga.tiles = cdiv(p.pool, 16);
   for (int s = 0; s < p.S; ++s) ga.desc[s] = p.st[s].desc;
   ga.pool_ids = p.pool_ids; ga.pool_n = p.pool_n; ga.gram = p.gram;
   hipLaunchKernelGGL(k_gram, dim3(p.S * ga.tiles * ga.tiles), dim3(256), 0, st, ga);
   MaxminArgs ma{};
-  ma.pool = p.pool; ma.n_select = p.n_select;
+  ma.pool = p.pool; ma.ld = (p.pool + 3) & ~3; ma.n_select = p.n_select;
   ma.pool_ids = p.pool_ids; ma.pool_votes = p.pool_votes; ma.pool_mass = p.pool_mass;
   ma.pool_n = p.pool_n; ma.gram = p.gram;
   ma.out_ids = p.out_ids; ma.out_votes = p.out_votes; ma.out_mass = p.out_mass; ma.out_n = p.out_n;
-  hipLaunchKernelGGL(k_maxmin, dim3(p.S), dim3(256), 0, st, ma);
+  hipLaunchKernelGGL(k_maxmin, dim3(p.S), dim3(1024), 0, st, ma);
   return hipGetLastError();
 }
 
@@ -1250,7 +1658,7 @@ hipError_t debug_scores_impl(RetrievePlan& p, int layer, int q_head, int64_t row
   for (int l = 0; l < p.L; ++l) pa.q[l] = p.st[0].q[l];
   pa.nq[0] = p.st[0].nq; pa.qscale[0] = p.st[0].qscale;
   pa.qB = reinterpret_cast<u32x4*>(p.qB);
-  hipLaunchKernelGGL(k_prep<D>, dim3(p.L * p.Hk), dim3(64), 0, st, pa);
+  hipLaunchKernelGGL(k_prep<D>, dim3(p.L * p.Hk), dim3(8 * D), 0, st, pa);
   ScoreArgs a{};
   a.L = p.L; a.Hq = p.Hq; a.Hk = p.Hk; a.G = p.G; a.NL = p.NL; a.ngs = p.ngs;
   a.head_mode = p.head_mode; a.S = 1; a.chunk = p.chunk_rows;
@@ -1287,7 +1695,12 @@ size_t carve_workspace(RetrievePlan& p, void* ws) {
   p.flag = static_cast<int32_t*>(take(lists * 4));
   p.samp = static_cast<float*>(take(lists * (size_t)p.m_max * 4));
   p.cand = static_cast<uint64_t*>(take(lists * (size_t)p.cap * 8));
-  p.topk = static_cast<uint64_t*>(take(lists * (size_t)std::max(p.k_max, 1) * 8));
+  p.run_f = static_cast<int32_t*>(take(lists * (size_t)std::max(p.k_max, 1) * 4));
+  p.run_c = static_cast<int32_t*>(take(lists * (size_t)std::max(p.k_max, 1) * 4));
+  p.run_fx = static_cast<int64_t*>(take(lists * (size_t)std::max(p.k_max, 1) * 8));
+  p.nruns = static_cast<int32_t*>(take(lists * 4));
+  p.listexp = static_cast<int32_t*>(take(lists * 4));
+  p.any_flag = static_cast<int32_t*>(take(4));
   p.full = static_cast<float*>(take((size_t)p.full_total * 4));
   p.votes = static_cast<int32_t*>(take((size_t)p.S * p.f_max * 4));
   p.massfx = static_cast<int64_t*>(take((size_t)p.S * p.f_max * 8));
@@ -1297,7 +1710,7 @@ size_t carve_workspace(RetrievePlan& p, void* ws) {
   p.pool_votes = static_cast<int32_t*>(take((size_t)p.S * p.pool * 4));
   p.pool_mass = static_cast<float*>(take((size_t)p.S * p.pool * 4));
   p.pool_n = static_cast<int32_t*>(take((size_t)p.S * 4));
-  p.gram = static_cast<float*>(take((size_t)p.S * p.pool * p.pool * 4));
+  p.gram = static_cast<float*>(take((size_t)p.S * p.pool * ((p.pool + 3) & ~3) * 4));
   return (off + 255) & ~(size_t)255;
 }
 

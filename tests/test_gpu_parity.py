@@ -120,9 +120,11 @@ def test_retrieve_c1_staged_and_planted():
     log(rep)
     assert rep["end_to_end_equal"]
     planted = set(spec.planted)
-    assert out["frame_ids"][0, 0] in planted
-    assert planted <= set(out["frame_ids"][0].tolist())
+    assert out["frame_ids"][0, 0] in planted                          # P2
     assert out["list_stats"][0, :, 1].sum() == 0    # no list needed the fallback
+    # P3: with a pool of K frames diversity cannot displace a planted frame
+    out1 = debug_run([gidx], [q], cfg.top_k, cfg.n_select, pool_mult=1)
+    assert planted <= set(out1["frame_ids"][0].tolist())
 
 
 def test_zero_queries_tie_rule():
@@ -287,9 +289,14 @@ def test_capacity_error_leaves_index_unchanged():
 # ---------------------------------------------------------------------------
 
 
+KMEANS_MARGIN = 1e-5
+
+
 def _kmeans_audit(ex, keys, cfg, frames, n_c, n_it):
-    """Where the oracle's decisions have a margin of at least 1e-4, the GPU's
-    bf16 centroids are within one bf16 unit and the counts are equal."""
+    """Where every farthest-point and assignment decision of the oracle has a
+    relative margin of at least KMEANS_MARGIN (about ten times the relative error
+    of a 128-term fp32 squared distance), the GPU's bf16 centroids are within one
+    bf16 unit of the oracle's and the member counts are equal."""
     T, d = cfg.tokens_per_frame, cfg.head_dim
     checked = exempt = 0
     for f in frames:
@@ -297,7 +304,7 @@ def _kmeans_audit(ex, keys, cfg, frames, n_c, n_it):
             for g in range(cfg.n_kv_heads):
                 X = O.decode_bf16(keys[l][g, f * T:(f + 1) * T, :])
                 C, cnt, dg = O.kmeans(X, n_c, n_it)
-                if min(dg["init_margin"], dg["assign_margin"]) < 1e-4:
+                if min(dg["init_margin"], dg["assign_margin"]) < KMEANS_MARGIN:
                     exempt += 1
                     continue
                 want = O.round_bf16(C)
@@ -337,7 +344,7 @@ def test_compression_c3_shape_audit_and_retrieval():
     ex = gidx.export()
     checked, exempt = _kmeans_audit(ex, keys, cfg, range(60), 32, 10)
     log("k-means audit", checked, "checked", exempt, "exempt")
-    assert checked >= 0.5 * (checked + exempt)
+    assert checked >= 0.5 * (checked + exempt)     # most problems have clear decisions
     oidx = O.Index(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim)
     desc = [O.descriptor(O.decode_bf16(keys[-1][:, f * 196:(f + 1) * 196, :])) for f in range(60)]
     oidx.append_stored([ex["rows"][l] for l in range(cfg.n_layers)], [32] * 60, desc)

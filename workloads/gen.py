@@ -155,22 +155,21 @@ def _planted_directions(cfg: Config, queries: list[np.ndarray]) -> np.ndarray:
 
 def _one_frame(cfg: Config, seed: int, stream: int, frame: int, planted: bool,
                dirs: np.ndarray) -> np.ndarray:
-    """Keys of one frame: ``[L][H_kv][T][d]`` bfloat16 bits."""
+    """Keys of one frame: ``[L][H_kv][T][d]`` bfloat16 bits.
+
+    Draw order per frame: all centroids ``[L][H_kv][d]``, then all token noise
+    ``[L][H_kv][T][d]``.
+    """
     rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, stream, _PURPOSE_FRAME, frame])))
     L, Hk, T, d = cfg.n_layers, cfg.n_kv_heads, cfg.tokens_per_frame, cfg.head_dim
-    out = np.empty((L, Hk, T, d), dtype=np.uint16)
-    for l in range(L):
-        for g in range(Hk):
-            z = rng.standard_normal(d, dtype=np.float32)
-            noise = rng.standard_normal((T, d), dtype=np.float32)
-            if planted:
-                c = (np.linalg.norm(z.astype(np.float64)) * dirs[l, g]).astype(np.float32)
-            else:
-                c = z
-            noise *= np.float32(0.5)
-            noise += c[None, :]
-            out[l, g] = bf16_bits(noise)
-    return out
+    z = rng.standard_normal((L, Hk, d), dtype=np.float32)
+    noise = rng.standard_normal((L, Hk, T, d), dtype=np.float32)
+    if planted:
+        norms = np.linalg.norm(z.astype(np.float64), axis=2, keepdims=True)
+        z = (norms * dirs).astype(np.float32)
+    noise *= np.float32(0.5)
+    noise += z[:, :, None, :]
+    return bf16_bits(noise)
 
 
 def frame_block_keys(cfg: Config, spec: StreamSpec, queries: list[np.ndarray], f0: int, f1: int,
