@@ -95,7 +95,6 @@ struct RetrievePlan {
   int64_t* run_fx;       // fixed-point score sums at scale 2^listexp
   int32_t* nruns;        // [S*NL]
   int32_t* listexp;      // [S*NL]
-  int32_t* any_flag;     // [1] non-zero when some list needs the exact fallback
   float* full;           // fallback scores, per stream base full_base[s]
   int64_t full_base[kMaxStreams];
   int32_t* votes;        // [S][f_max]

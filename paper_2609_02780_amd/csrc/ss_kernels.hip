@@ -11,14 +11,14 @@
 //               bf16 MFMA 16x16x32 against the group's query columns with fp32
 //               accumulation, and appends rows scoring at or above the cut-off
 //               as 64-bit composite keys, one atomic per (wave, tile, head).
-//   k_select    exact top-k per list from its candidates: bisection on the
-//               ordered score in registers, ties by row; lists whose candidate
-//               count fell outside [k, capacity] are flagged.
-//   k_score<FULL> + k_fb_select   exact fallback for flagged lists only:
-//               materialise the list's scores, radix select, ties by row order.
-//   k_votes_pool  one vote per selected row for its frame and the attention
-//               mass in deterministic fixed point (segmented wave reductions
-//               over row-sorted lists), then the vote-ranked pool (bitonic, LDS).
+//   k_select    exact top-k per list from its candidates (radix selection over
+//               the value range, items in registers, ties by row); a list whose
+//               candidate count left [k, capacity] recomputes all of its scores
+//               and selects exactly from them instead.  Each list then adds its
+//               selected rows up per frame (count, fixed-point score sum).
+//   k_votes_pool  per stream, the frames' votes and attention mass merged from
+//               the lists' per-frame sums (deterministic fixed point), then the
+//               vote-ranked pool (radix cut over 128-bit records, ranks by count).
 //   k_gram      fp32 Gram matrix of the pool descriptors.
 //   k_maxmin    greedy max-min diversity over the Gram matrix.
 //
@@ -228,6 +228,36 @@ __device__ uint64_t radix_select_u64(Get get, int n, uint32_t r, uint32_t* hist,
   return prefix;
 }
 
+// Threshold (hi, lo) such that exactly r of the n distinct 128-bit keys
+// get(i) = (hi, lo) compare >= it; same early exit as radix_select_u64.
+template <class Get>
+__device__ void radix_select_u128(Get get, int n, uint32_t r, uint32_t* hist, uint32_t* res,
+                                  uint64_t& cut_hi, uint64_t& cut_lo) {
+  uint64_t ph = 0, pl = 0, mh = 0, ml = 0;
+  uint32_t need = r;
+  for (int d = 0; d < 16; ++d) {
+    const int shift = 56 - 8 * (d & 7);
+    for (int i = threadIdx.x; i < 256; i += blockDim.x) hist[i] = 0;
+    __syncthreads();
+    for (int i = threadIdx.x; i < n; i += blockDim.x) {
+      uint64_t h, l;
+      get(i, h, l);
+      if ((h & mh) == ph && (l & ml) == pl)
+        atomicAdd(&hist[(uint32_t)((d < 8 ? h : l) >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    find_digit(hist, need, res);
+    const uint32_t b = res[0], above = res[1], inb = res[2];
+    __syncthreads();
+    if (d < 8) { ph |= (uint64_t)b << shift; mh |= 255ull << shift; }
+    else { pl |= (uint64_t)b << shift; ml |= 255ull << shift; }
+    need -= above;
+    if (inb == need) break;
+  }
+  cut_hi = ph;
+  cut_lo = pl;
+}
+
 // Descending bitonic sort of n (power of two) uint64 keys in LDS.
 __device__ void bitonic_desc_u64(uint64_t* a, int n) {
   for (int k = 2; k <= n; k <<= 1) {
@@ -389,7 +419,6 @@ struct ScoreArgs {
   uint64_t* cand;
   int cap;
   // K_FULL
-  const int32_t* any_flag;            // nullptr, or zero when no list needs the fallback
   const int32_t* flag;                // nullptr: write only `only_list`
   int only_list;
   float* full;
@@ -474,7 +503,6 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a) {
   constexpr int KS = D / 32, PF = 2;
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
-  if (KIND == K_FULL && a.any_flag && *a.any_flag == 0) return;
   for (int item = blockIdx.x; item < a.total_items; item += gridDim.x) {
     int s = 0;
     while (item >= a.item_base[s + 1]) ++s;
@@ -544,7 +572,6 @@ __global__ __launch_bounds__(256) void k_score_hm(ScoreArgs a) {
   __shared__ u32x4 sB[8 * 2 * KS * kWave];  // H_kv <= 8 in head-mode 1
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
-  if (KIND == K_FULL && a.any_flag && *a.any_flag == 0) return;
   for (int item = blockIdx.x; item < a.total_items; item += gridDim.x) {
     int s = 0;
     while (item >= a.item_base[s + 1]) ++s;
@@ -679,14 +706,18 @@ struct ListArgs {
   uint32_t* tau;
   uint32_t* cnt;
   int32_t* flag;
-  int32_t* any_flag;   // set when any list needs the fallback
   const uint64_t* cand;
   int32_t* run_f;      // [list][k_max] per-frame runs of the selected rows
   int32_t* run_c;
   int64_t* run_fx;     // fixed-point score sums at scale 2^listexp
   int32_t* nruns;      // [list]
   int32_t* listexp;    // [list]
-  const float* full;
+  // exact fallback: the list's scores are recomputed into `full`
+  float* full;
+  int L, Hq, Hk, G, head_mode;
+  const uint16_t* keys[kMaxStreams];
+  int32_t stride[kMaxStreams];
+  const u32x4* qB;
   int32_t* dbg_pos;
   float* dbg_score;
   int32_t* dbg_stats;
@@ -713,7 +744,6 @@ __global__ __launch_bounds__(1024) void k_thresh(ListArgs a) {
   if (threadIdx.x == 0) {
     a.cnt[list] = 0;
     a.flag[list] = 0;
-    if (list == 0) *a.any_flag = 0;
   }
   if (m == 0 || r == 0) {
     if (threadIdx.x == 0) a.tau[list] = 0xFFFFFFFFu;
@@ -832,6 +862,96 @@ __device__ void finish_list(const ListArgs& a, int list, uint64_t* sel, int kk, 
   }
 }
 
+// Exact fallback for a list whose candidate count left [k, capacity]: the block
+// recomputes every score of the list (same MFMA arithmetic as the streaming
+// pass) into `full`, then takes the k-th largest by radix selection, rows above
+// it in any order and rows equal to it in row order.
+template <int D>
+__device__ void fallback_list(const ListArgs& a, int list, uint64_t* sel, int32_t* lv, long long* lm,
+                              uint32_t* hist, uint32_t* res) {
+  constexpr int KS = D / 32;
+  __shared__ uint32_t ngt_sh;
+  __shared__ int scan_sh[17];
+  __shared__ float redm[16];
+  const int s = list / a.NL, ll = list - s * a.NL;
+  const int kk = a.kk[s], n = a.n[s];
+  float* full = a.full + a.full_base[s] + (int64_t)ll * n;
+  int l, g0, ng, col;
+  if (a.head_mode == 0) {
+    l = ll / a.Hq;
+    const int h = ll - l * a.Hq;
+    g0 = h / a.G;
+    col = h - g0 * a.G;
+    ng = 1;
+  } else {
+    l = ll;
+    g0 = 0;
+    col = 0;
+    ng = a.Hk;
+  }
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const int kg = lane >> 4, rl = lane & 15;
+  const size_t gstride = (size_t)a.stride[s] * D;
+  const int ntiles = (n + kTile - 1) / kTile;
+  for (int t = wave; t < ntiles; t += nw) {
+    const int row = t * kTile + rl;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int g = g0; g < g0 + ng; ++g) {
+      const u32x4* qb = a.qB + ((size_t)(s * a.L + l) * a.Hk + g) * (2 * KS * kWave);
+      const uint16_t* p = a.keys[s] + ((size_t)l * a.Hk + g) * gstride + (size_t)(row < n ? row : 0) * D + 8 * kg;
+#pragma unroll
+      for (int i = 0; i < KS; ++i) {
+        const u32x4 A = row < n ? ld_nt(p + 32 * i) : u32x4{0, 0, 0, 0};
+        acc = mfma_bf16(A, qb[i * kWave + lane], acc);
+        acc = mfma_bf16(A, qb[(KS + i) * kWave + lane], acc);
+      }
+    }
+    if ((lane & 15) == col) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = t * kTile + 4 * kg + j;
+        if (r < n) full[r] = acc[j] + 0.0f;
+      }
+    }
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __syncthreads();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  uint32_t ngreater;
+  const uint32_t vstar = radix_select_u32([&](int i) { return ord_u32(full[i]); }, n,
+                                          (uint32_t)kk, hist, res, ngreater);
+  const int need_eq = kk - (int)ngreater;
+  if (threadIdx.x == 0) ngt_sh = 0;
+  __syncthreads();
+  int eq_taken = 0;
+  float m = 0.f;
+  for (int b0 = 0; b0 < n; b0 += blockDim.x) {
+    const int i = b0 + threadIdx.x;
+    uint32_t u = 0;
+    bool gt = false, eq = false;
+    if (i < n) {
+      u = ord_u32(full[i]);
+      gt = u > vstar;
+      eq = u == vstar;
+    }
+    if (gt) {
+      const uint32_t slot = atomicAdd(&ngt_sh, 1u);
+      if (slot < (uint32_t)kMaxTopK) sel[slot] = mk_key(u, (uint32_t)i);
+      m = fmaxf(m, fabsf(ord_f32(u)));
+    }
+    int tot;
+    const int pre = block_excl_scan(eq ? 1 : 0, scan_sh, tot);
+    if (eq && eq_taken + pre < need_eq) {
+      sel[ngreater + eq_taken + pre] = mk_key(u, (uint32_t)i);
+      m = fmaxf(m, fabsf(ord_f32(u)));
+    }
+    eq_taken += tot;
+  }
+  const float mxa = block_max(m, redm);
+  finish_list(a, list, sel, kk, mxa, lv, lm);
+}
+
+template <int D>
 __global__ __launch_bounds__(1024) void k_select(ListArgs a) {
   __shared__ uint64_t sel[kMaxTopK];
   __shared__ int32_t lv[kVoteLds];
@@ -847,11 +967,14 @@ __global__ __launch_bounds__(1024) void k_select(ListArgs a) {
     return;
   }
   const uint32_t c = a.cnt[list];
-  if (c < (uint32_t)kk || c > (uint32_t)a.cap) {
-    if (threadIdx.x == 0) {
-      a.flag[list] = 1;
-      atomicAdd(a.any_flag, 1);
-    }
+  const bool fallback = c < (uint32_t)kk || c > (uint32_t)a.cap;
+  if (a.dbg_stats && threadIdx.x == 0) {
+    a.dbg_stats[2 * list] = (int32_t)min(c, (uint32_t)INT_MAX);
+    a.dbg_stats[2 * list + 1] = fallback ? 1 : 0;
+  }
+  if (fallback) {
+    if (threadIdx.x == 0) a.flag[list] = 1;
+    fallback_list<D>(a, list, sel, lv, lm, hist, res);
     return;
   }
   const int n = (int)c;
@@ -915,59 +1038,6 @@ __global__ __launch_bounds__(1024) void k_select(ListArgs a) {
     mxa = block_max(m, redm);
   }
   __syncthreads();
-  finish_list(a, list, sel, kk, mxa, lv, lm);
-}
-
-// Exact fallback: every score of the list was materialised by k_score<FULL>.
-__global__ __launch_bounds__(256) void k_fb_select(ListArgs a) {
-  __shared__ uint64_t sel[kMaxTopK];
-  __shared__ int32_t lv[kVoteLds];
-  __shared__ long long lm[kVoteLds];
-  __shared__ uint32_t hist[256];
-  __shared__ uint32_t res[4];
-  __shared__ uint32_t ngt_sh;
-  __shared__ int scan_sh[8];
-  __shared__ float redm[4];
-  const int list = blockIdx.x, s = list / a.NL;
-  if (a.dbg_stats && threadIdx.x == 0) {
-    a.dbg_stats[2 * list] = (int32_t)min(a.cnt[list], (uint32_t)INT_MAX);
-    a.dbg_stats[2 * list + 1] = a.flag[list];
-  }
-  if (!a.flag[list]) return;
-  const int kk = a.kk[s], n = a.n[s];
-  const float* v = a.full + a.full_base[s] + (int64_t)(list - s * a.NL) * n;
-  uint32_t ngreater;
-  const uint32_t vstar = radix_select_u32([&](int i) { return ord_u32(v[i] + 0.0f); }, n,
-                                          (uint32_t)kk, hist, res, ngreater);
-  const int need_eq = kk - (int)ngreater;
-  if (threadIdx.x == 0) ngt_sh = 0;
-  __syncthreads();
-  // rows scoring above v* in any order; rows equal to v* in row order until need_eq
-  int eq_taken = 0;
-  float m = 0.f;
-  for (int b0 = 0; b0 < n; b0 += blockDim.x) {
-    const int i = b0 + threadIdx.x;
-    uint32_t u = 0;
-    bool gt = false, eq = false;
-    if (i < n) {
-      u = ord_u32(v[i] + 0.0f);
-      gt = u > vstar;
-      eq = u == vstar;
-    }
-    if (gt) {
-      const uint32_t slot = atomicAdd(&ngt_sh, 1u);
-      if (slot < (uint32_t)kMaxTopK) sel[slot] = mk_key(u, (uint32_t)i);
-      m = fmaxf(m, fabsf(ord_f32(u)));
-    }
-    int tot;
-    const int pre = block_excl_scan(eq ? 1 : 0, scan_sh, tot);
-    if (eq && eq_taken + pre < need_eq) {
-      sel[ngreater + eq_taken + pre] = mk_key(u, (uint32_t)i);
-      m = fmaxf(m, fabsf(ord_f32(u)));
-    }
-    eq_taken += tot;
-  }
-  const float mxa = block_max(m, redm);
   finish_list(a, list, sel, kk, mxa, lv, lm);
 }
 
@@ -1102,44 +1172,43 @@ __global__ __launch_bounds__(1024) void k_votes_pool(VoteArgs a) {
   __syncthreads();
   const int n_voted = (int)nvoted_sh;
   const int P = a.pool;
-  int pn;
-  if (n_voted <= kPoolSort) {
-    // rank by counting: rank = number of records above (records are distinct)
-    __shared__ int32_t pslot[kMaxPool];
-    for (int i = threadIdx.x; i < n_voted; i += blockDim.x) {
-      const uint64_t h = shi[i], l = slo[i];
-      int rank = 0;
-      for (int j = 0; j < n_voted; ++j) rank += rec_less(h, l, shi[j], slo[j]);
-      if (rank < P) pslot[rank] = i;
+  __shared__ uint64_t ghi[kMaxPool];
+  __shared__ uint64_t glo[kMaxPool];
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t res[4];
+  __shared__ uint32_t ngather;
+  const int pn = min(P, n_voted);
+  // the `pool` largest records: a radix cut over the 128-bit keys (when there
+  // are more voted frames than pool slots), then ranks by counting among them
+  const bool in_lds = n_voted <= kPoolSort;
+  auto get = [&](int i, uint64_t& h, uint64_t& l) {
+    if (in_lds) { h = shi[i]; l = slo[i]; }
+    else {
+      h = __hip_atomic_load(&rh[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      l = __hip_atomic_load(&rl[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    pn = min(P, n_voted);
-    __syncthreads();
-    // move the pool to the front of shi/slo in rank order
-    uint64_t ph = 0, pl = 0;
-    if (threadIdx.x < pn) { ph = shi[pslot[threadIdx.x]]; pl = slo[pslot[threadIdx.x]]; }
-    __syncthreads();
-    if (threadIdx.x < pn) { shi[threadIdx.x] = ph; slo[threadIdx.x] = pl; }
-    __syncthreads();
-  } else {
-    // many voted frames: rounds of bitonic sorting, the running best kept in front
-    int kept = 0, next = 0;
-    do {
-      const int room = kPoolSort - kept;
-      const int take = min(room, n_voted - next);
-      const int tot = kept + take;
-      const int np = pow2_ceil(max(tot, 2));
-      for (int i = threadIdx.x; i < take; i += blockDim.x) {
-        shi[kept + i] = __hip_atomic_load(&rh[next + i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        slo[kept + i] = __hip_atomic_load(&rl[next + i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
-      for (int i = tot + threadIdx.x; i < np; i += blockDim.x) { shi[i] = 0; slo[i] = 0; }
-      __syncthreads();
-      bitonic_desc_u128(shi, slo, np);
-      kept = min(P, tot);
-      next += take;
-    } while (next < n_voted);
-    pn = kept;
+  };
+  uint64_t ch = 0, cl = 0;
+  if (n_voted > P) radix_select_u128(get, n_voted, (uint32_t)P, hist, res, ch, cl);
+  if (threadIdx.x == 0) ngather = 0;
+  __syncthreads();
+  for (int i = threadIdx.x; i < n_voted; i += blockDim.x) {
+    uint64_t h, l;
+    get(i, h, l);
+    if (h > ch || (h == ch && l >= cl)) {
+      const uint32_t slot = atomicAdd(&ngather, 1u);
+      if (slot < (uint32_t)kMaxPool) { ghi[slot] = h; glo[slot] = l; }
+    }
   }
+  __syncthreads();
+  for (int i = threadIdx.x; i < pn; i += blockDim.x) {
+    const uint64_t h = ghi[i], l = glo[i];
+    int rank = 0;
+    for (int j = 0; j < pn; ++j) rank += rec_less(h, l, ghi[j], glo[j]);
+    shi[rank] = h;   // records are distinct: ranks form a permutation
+    slo[rank] = l;
+  }
+  __syncthreads();
   for (int i = threadIdx.x; i < P; i += blockDim.x) {
     int id = -1, v = 0;
     float m = 0.f;
@@ -1566,7 +1635,7 @@ ScoreArgs make_score_args(const RetrievePlan& p, int kind) {
   a.total_items = items;
   a.samp = p.samp; a.samp_stride = p.m_max;
   a.tau = p.tau; a.cnt = p.cnt; a.cand = p.cand; a.cap = p.cap;
-  a.flag = p.flag; a.any_flag = p.any_flag; a.only_list = -1; a.full = p.full; a.row0 = 0;
+  a.flag = p.flag; a.only_list = -1; a.full = p.full; a.row0 = 0;
   return a;
 }
 
@@ -1605,8 +1674,10 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   }
   la.samp = p.samp; la.samp_stride = p.m_max; la.tau = p.tau; la.cnt = p.cnt; la.flag = p.flag;
   la.cand = p.cand; la.full = p.full;
+  la.L = p.L; la.Hq = p.Hq; la.Hk = p.Hk; la.G = p.G; la.head_mode = p.head_mode;
+  la.qB = reinterpret_cast<const u32x4*>(p.qB);
+  for (int s = 0; s < p.S; ++s) { la.keys[s] = p.st[s].keys; la.stride[s] = p.st[s].row_stride; }
   la.dbg_pos = p.dbg_topk_pos; la.dbg_score = p.dbg_topk_score; la.dbg_stats = p.dbg_list_stats;
-  la.any_flag = p.any_flag;
   la.run_f = p.run_f; la.run_c = p.run_c; la.run_fx = p.run_fx; la.nruns = p.nruns;
   la.listexp = p.listexp;
   const int lists = p.S * p.NL;
@@ -1618,9 +1689,7 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   launch_score<D, K_STREAM>(make_score_args(p, K_STREAM), p.head_mode, 2048, st);
   if (p.ev_stop) (void)hipEventRecord(p.ev_stop, st);
   // 5. exact top-k from candidates; 6. exact fallback for flagged lists
-  hipLaunchKernelGGL(k_select, dim3(lists), dim3(1024), 0, st, la);
-  launch_score<D, K_FULL>(make_score_args(p, K_FULL), p.head_mode, 256, st);
-  hipLaunchKernelGGL(k_fb_select, dim3(lists), dim3(256), 0, st, la);
+  hipLaunchKernelGGL(k_select<D>, dim3(lists), dim3(1024), 0, st, la);
   // 7. votes, mass and pool
   VoteArgs va{};
   va.NL = p.NL; va.k_max = p.k_max; va.pool = p.pool; va.f_max = p.f_max;
@@ -1700,7 +1769,6 @@ size_t carve_workspace(RetrievePlan& p, void* ws) {
   p.run_fx = static_cast<int64_t*>(take(lists * (size_t)std::max(p.k_max, 1) * 8));
   p.nruns = static_cast<int32_t*>(take(lists * 4));
   p.listexp = static_cast<int32_t*>(take(lists * 4));
-  p.any_flag = static_cast<int32_t*>(take(4));
   p.full = static_cast<float*>(take((size_t)p.full_total * 4));
   p.votes = static_cast<int32_t*>(take((size_t)p.S * p.f_max * 4));
   p.massfx = static_cast<int64_t*>(take((size_t)p.S * p.f_max * 8));
