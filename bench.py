@@ -152,6 +152,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="C4", choices=sorted(W.CONFIGS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy (calibrates the HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the retrieval has no multi-GPU path (asked for --gpus {args.gpus})",
@@ -159,6 +161,17 @@ def main():
         sys.exit(2)
 
     import torch
+
+    if args.calibrate_copy:
+        # a plain copy of known size: 2^30 bytes read and 2^30 bytes written
+        torch.cuda.set_device(0)
+        a = torch.ones(1 << 28, dtype=torch.int32, device="cuda")
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration_copy_bytes": 1 << 30}), flush=True)
+        return
 
     import paper_2609_02780_amd as P
     if not os.path.exists(P._lib.LIB_PATH):
