@@ -64,10 +64,10 @@ def dev_bf16(torch, a):
 
 def build_streams(torch, P, cfg, block=600):
     """Generate and append every stream of the workload; returns the indices, the
-    per-stream device queries and the first block of stream 0 (host, for the
+    per-stream device queries and stream 0's queries and host key blocks (for the
     CPU baseline)."""
     specs = W.stream_specs(cfg)
-    idxs, queries, first_block = [], [], None
+    idxs, queries, host0 = [], [], None
     t0 = time.time()
     for spec in specs:
         q = W.make_queries(cfg, 0, spec.stream)
@@ -75,17 +75,20 @@ def build_streams(torch, P, cfg, block=600):
         rpf = T if spec.compress is None else min(spec.compress[0], T)
         idx = P.ShallowIndex(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, spec.n_frames,
                              spec.n_frames * rpf)
+        blocks = []
         for f0 in range(0, spec.n_frames, block):
             f1 = min(spec.n_frames, f0 + block)
             kb = W.frame_block_keys(cfg, spec, q, f0, f1)
             idx.append([dev_bf16(torch, k) for k in kb], f1 - f0, T, spec.compress)
-            if first_block is None:
-                first_block = (q, kb, f1 - f0)
+            if spec.stream == 0:
+                blocks.append((kb, f1 - f0))
             torch.cuda.synchronize()
+        if spec.stream == 0:
+            host0 = (q, blocks, spec.compress)
         idxs.append(idx)
         queries.append([dev_bf16(torch, x) for x in q])
         log(f"stream {spec.stream}: {spec.n_frames} frames appended ({time.time() - t0:.1f} s)")
-    return specs, idxs, queries, first_block
+    return specs, idxs, queries, host0
 
 
 def time_append(torch, P, cfg, frames=64):
@@ -119,30 +122,47 @@ def time_append(torch, P, cfg, frames=64):
             "batch_frames_per_s": frames / (batch_ms / 1e3)}
 
 
-def cpu_baseline(cfg, first_block):
-    """The oracle on the first frames of stream 0 with the workload's queries and
-    retrieval parameters."""
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(cfg, host0):
+    """The oracle's retrieval over stream 0 of the workload, with its queries and
+    retrieval parameters.  A raw stream is taken whole; a compressed one is cut to
+    its first 40 frames, since the float64 k-means of the oracle's append is slow."""
     from oracle import oracle as O
-    q, kb, nf = first_block
+    q, blocks, comp = host0
     try:
         from threadpoolctl import threadpool_info
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:
         cores = 1
-    comp = W.stream_specs(cfg)[0].compress
-    if comp is not None:
-        nf = min(nf, 40)     # the float64 k-means makes compressed appends slow; keep ~10-30 s
-        kb = [np.ascontiguousarray(k[:, :nf * cfg.tokens_per_frame, :]) for k in kb]
     oi = O.Index(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim)
-    oi.append(kb, nf, cfg.tokens_per_frame, comp)
+    if comp is None:
+        for kb, nf in blocks:
+            oi.append(kb, nf, cfg.tokens_per_frame)
+        what = f"all {oi.n_frames} frames"
+    else:
+        kb, nf = blocks[0]
+        nf = min(nf, 40)
+        oi.append([np.ascontiguousarray(k[:, :nf * cfg.tokens_per_frame, :]) for k in kb], nf,
+                  cfg.tokens_per_frame, comp)
+        what = f"the first {nf} frames"
     t0 = time.perf_counter()
     O.retrieve(oi, q, cfg.top_k, cfg.n_select, cfg.pool_mult)
     dt = time.perf_counter() - t0
     keys = oi.n_rows * cfg.n_layers * cfg.n_kv_heads
     return {"value": keys / dt, "unit": "keys/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"full float64 oracle retrieval (scores, top-k, votes, pool, max-min) over the first "
-                      f"{nf} frames ({oi.n_rows} rows per (layer, KV head)) of the {cfg.name} stream with its "
-                      f"queries and parameters: {keys} key vectors in {dt:.2f} s"}
+            "cpu": cpu_model(),
+            "sample": f"float64 oracle retrieval (scores, top-k, votes, pool, max-min) over {what} "
+                      f"({oi.n_rows} rows per (layer, KV head)) of stream 0 of {cfg.name} with its queries "
+                      f"and parameters: {keys} key vectors in {dt:.2f} s"}
 
 
 def main():
@@ -179,7 +199,7 @@ def main():
         build_library()
     torch.cuda.set_device(0)
     cfg = W.CONFIGS[args.config]
-    specs, idxs, queries, first_block = build_streams(torch, P, cfg)
+    specs, idxs, queries, host0 = build_streams(torch, P, cfg)
     r = P.Retriever(idxs, cfg.top_k, cfg.n_select, cfg.pool_mult)
     for _ in range(args.warmup):
         r(queries)
@@ -203,7 +223,7 @@ def main():
     lat = np.array([e[0].elapsed_time(e[1]) for e in ev])
     hot = np.array([e[2].elapsed_time(e[3]) for e in ev])
 
-    rows = [x.n_rows - 0 for x in idxs]
+    rows = [x.n_rows for x in idxs]
     key_vectors = sum(x.n_rows for x in idxs) * cfg.n_layers * cfg.n_kv_heads
     key_bytes = key_vectors * cfg.head_dim * 2
     ms_per_step = (t1 - t0) * 1e3 / K
@@ -240,7 +260,7 @@ def main():
     if cfg.compress is not None:
         out["append"] = time_append(torch, P, cfg)
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, first_block)
+        out["cpu_baseline"] = cpu_baseline(cfg, host0)
     print(json.dumps(out), flush=True)
 
 

@@ -178,16 +178,17 @@ def frame_block_keys(cfg: Config, spec: StreamSpec, queries: list[np.ndarray], f
     dirs = _planted_directions(cfg, queries)
     planted = set(spec.planted)
     nthreads = threads or min(16, len(os.sched_getaffinity(0)))
-    frames = list(range(f0, f1))
-    with ThreadPoolExecutor(max(1, nthreads)) as ex:
-        per = list(ex.map(lambda f: _one_frame(cfg, seed, spec.stream, f, f in planted, dirs), frames))
     L, Hk, T, d = cfg.n_layers, cfg.n_kv_heads, cfg.tokens_per_frame, cfg.head_dim
-    out = []
-    for l in range(L):
-        arr = np.empty((Hk, (f1 - f0) * T, d), dtype=np.uint16)
-        for i, fr in enumerate(per):
-            arr[:, i * T:(i + 1) * T, :] = fr[l]
-        out.append(arr)
+    out = [np.empty((Hk, (f1 - f0) * T, d), dtype=np.uint16) for _ in range(L)]
+
+    def fill(f):
+        fr = _one_frame(cfg, seed, spec.stream, f, f in planted, dirs)
+        i = f - f0
+        for l in range(L):
+            out[l][:, i * T:(i + 1) * T, :] = fr[l]
+
+    with ThreadPoolExecutor(max(1, nthreads)) as ex:
+        list(ex.map(fill, range(f0, f1)))
     return out
 
 
