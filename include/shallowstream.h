@@ -58,7 +58,8 @@ enum {
  *               G = H_q / H_kv <= 16.  Query head h reads KV head h / G.
  *   head_dim    d, 64 or 128.
  *   max_frames  frame capacity; max_rows row capacity per (layer, KV head),
- *               < 2^31.
+ *               with max_rows * head_dim * 2 < 2^31 (one (layer, KV head) of
+ *               keys below 2 GiB: 8,388,607 rows at d = 128).
  *   n_recent    N_r: the newest n_recent frames are never retrieval
  *               candidates (Eq. context_partition); 0 makes every frame one. */
 typedef struct {

@@ -70,6 +70,10 @@ ss_status check_desc(const ss_index_desc* d) {
     return fail(SS_ERR_INVALID_ARGUMENT, "max_frames %lld outside 1..2^30", (long long)d->max_frames);
   if (d->max_rows < 1 || d->max_rows > (int64_t)0x7FFFFFFF - 1)
     return fail(SS_ERR_INVALID_ARGUMENT, "max_rows %lld outside 1..2^31-2", (long long)d->max_rows);
+  // one (layer, KV head) segment is read through a 32-bit buffer range
+  if (d->max_rows * d->head_dim * 2 > ((int64_t)1 << 31) - 1)
+    return fail(SS_ERR_UNSUPPORTED, "max_rows * head_dim * 2 = %lld bytes per (layer, KV head) >= 2^31",
+                (long long)(d->max_rows * d->head_dim * 2));
   if (d->n_recent < 0) return fail(SS_ERR_INVALID_ARGUMENT, "n_recent must be >= 0");
   if ((int64_t)d->n_layers * d->n_q_heads > ss::kMaxListsPerStream)
     return fail(SS_ERR_UNSUPPORTED, "n_layers * n_q_heads %lld > %d",

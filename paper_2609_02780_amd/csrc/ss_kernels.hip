@@ -6,11 +6,15 @@
 //               and laid out as the MFMA B operand (lane-native).
 //   k_score<SAMPLE>   scores of an evenly spread sample of rows per list.
 //   k_thresh    per list, the r-th largest sample score: the streaming cut-off.
-//   k_score<STREAM>   THE HOT KERNEL: streams every bf16 key row from HBM once
-//               (nontemporal 16-byte loads straight into the MFMA A layout),
-//               bf16 MFMA 16x16x32 against the group's query columns with fp32
-//               accumulation, and appends rows scoring at or above the cut-off
-//               as 64-bit composite keys, one atomic per (wave, tile, head).
+//   k_stream    THE HOT KERNEL: streams every bf16 key row from HBM once.
+//               The 16-row tiles of all lists form one sequence cut into one
+//               contiguous range per wave; each tile comes in as coalesced
+//               nontemporal 16-byte buffer loads, is swizzled through LDS into
+//               the MFMA A layout, is scored by bf16 MFMA 16x16x32 against the
+//               group's query columns (hi and lo parts, fp32 accumulation), and
+//               rows at or above the cut-off are staged in LDS as 64-bit
+//               composite keys and flushed with one atomic per (wave, column).
+//               (Head-mode 1 streams in k_score_hm.)
 //   k_select    exact top-k per list from its candidates (radix selection over
 //               the value range, items in registers, ties by row); a list whose
 //               candidate count left [k, capacity] recomputes all of its scores
@@ -81,6 +85,23 @@ __device__ __forceinline__ f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
+
+// The score arithmetic of every head-mode-0 path (sample, stream, exact
+// recompute): one fp32 MFMA chain over the k-steps against the hi parts of the
+// query mean, one against the lo parts, added at the end, so that each path
+// gives a row the same bits.
+template <int KS>
+__device__ __forceinline__ f32x4 score_hilo(const u32x4 (&A)[KS], const u32x4 (&bh)[KS],
+                                            const u32x4 (&bl)[KS]) {
+  f32x4 h = {0.f, 0.f, 0.f, 0.f}, l = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int i = 0; i < KS; ++i) h = mfma_bf16(A[i], bh[i], h);
+#pragma unroll
+  for (int i = 0; i < KS; ++i) l = mfma_bf16(A[i], bl[i], l);
+  return h + l;
+}
+
+constexpr int kAuxNT = 2;  // buffer-load cache policy: nontemporal
 
 __device__ __forceinline__ u32x4 ld_nt(const uint16_t* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
@@ -418,6 +439,8 @@ struct ScoreArgs {
   uint32_t* cnt;
   uint64_t* cand;
   int cap;
+  int64_t tile_base[kMaxStreams + 1];  // first tile of each stream; tiles of all streams in a row
+  int32_t ntile[kMaxStreams];          // 16-row tiles per (layer, KV head) segment
   // K_FULL
   const int32_t* flag;                // nullptr: write only `only_list`
   int only_list;
@@ -443,44 +466,10 @@ __device__ __forceinline__ int64_t unit_row(const ScoreArgs& a, int s, int u) {
 
 // Per-lane output of one 16-row tile: lane (col, kg) holds the scores of rows
 // 4 kg + j (j < 4) of the tile for output column col.  Called by whole waves.
+// K_SAMPLE writes sample scores, K_FULL whole score rows.
 template <int KIND>
 __device__ __forceinline__ void emit(const ScoreArgs& a, int s, int list, bool colv, bool wr,
-                                     uint32_t tau_u, int tile_u0, int u1, f32x4 acc, int kg,
-                                     bool& ovf) {
-  if (KIND == K_STREAM) {
-    // Rows at or above the cut-off are appended to the list's candidates.  The
-    // four lanes of a column agree on one slot range: one atomic per (wave,
-    // tile, column) instead of one per row.
-    const int lane = threadIdx.x & (kWave - 1);
-    uint32_t uo[4];
-    bool pass[4];
-    int c = 0;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int u = tile_u0 + 4 * kg + j;
-      uo[j] = ord_u32(acc[j] + 0.0f);  // canonical zero: -0 becomes +0
-      pass[j] = colv && !ovf && u < u1 && uo[j] >= tau_u;
-      c += pass[j];
-    }
-    if (__ballot(c > 0) == 0) return;
-    const int c16 = __shfl_xor(c, 16), c32 = __shfl_xor(c, 32), c48 = __shfl_xor(c, 48);
-    const int total = c + c16 + c32 + c48;
-    const int prefix = kg == 0 ? 0 : kg == 1 ? c16 : kg == 2 ? c32 + c48 : c16 + c32 + c48;
-    uint32_t base = 0;
-    if (kg == 0 && total > 0) base = atomicAdd(&a.cnt[list], (uint32_t)total);
-    base = (uint32_t)__shfl((int)base, lane & 15);
-    if (total > 0 && base + (uint32_t)total >= (uint32_t)a.cap) ovf = true;
-    uint32_t slot = base + (uint32_t)prefix;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (pass[j]) {
-        if (slot < (uint32_t)a.cap)
-          a.cand[(size_t)list * a.cap + slot] = mk_key(uo[j], (uint32_t)(tile_u0 + 4 * kg + j));
-        ++slot;
-      }
-    }
-    return;
-  }
+                                     int tile_u0, int u1, f32x4 acc, int kg) {
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int u = tile_u0 + 4 * kg + j;
@@ -496,10 +485,67 @@ __device__ __forceinline__ void emit(const ScoreArgs& a, int s, int list, bool c
   }
 }
 
+// Candidates of the streaming pass wait in LDS, kStage per (wave, column), and
+// go to the list's global buffer in one flush: one global atomic per (wave,
+// column, flush) keeps returning atomics out of the tile loop.  `lc` is the
+// staged count of the lane's column, the same in the column's four lanes.
+constexpr int kStage = 32;
+
+__device__ __forceinline__ void stage_flush(const ScoreArgs& a, int list, bool colv, int col, int kg,
+                                            const uint64_t* st, int& lc) {
+  const int lane = threadIdx.x & (kWave - 1);
+  __builtin_amdgcn_wave_barrier();
+  uint32_t base = 0;
+  if (kg == 0 && colv && lc > 0) base = atomicAdd(&a.cnt[list], (uint32_t)lc);
+  base = (uint32_t)__shfl((int)base, lane & 15);
+  for (int e = kg; e < lc; e += 4) {
+    const uint32_t slot = base + (uint32_t)e;
+    if (slot < (uint32_t)a.cap) a.cand[(size_t)list * a.cap + slot] = st[col * kStage + e];
+  }
+  __builtin_amdgcn_wave_barrier();
+  lc = 0;
+}
+
+// Rows of a tile at or above the cut-off are staged as composite keys.  Lane
+// (col, kg) holds rows 4 kg + j of the tile for column col.  Compared as
+// floats: for finite scores x >= ord_f32(tau) selects exactly the rows whose
+// canonical key ord_u32(x + 0) is at least tau (-0 and +0 compare equal and
+// share one key); invalid columns carry a NaN cut-off, which nothing passes.
+__device__ __forceinline__ void stream_emit(const ScoreArgs& a, int list, bool colv, int col,
+                                            float tau_f, int tile_u0, int u1, f32x4 acc, int kg,
+                                            uint64_t* st, int& lc) {
+  bool pass[4];
+  int c = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    pass[j] = (tile_u0 + 4 * kg + j < u1) && acc[j] >= tau_f;
+    c += pass[j];
+  }
+  if (__ballot(c > 0) == 0) return;
+  // the column's four lanes agree on a slot range, in kg order
+  const int ln = threadIdx.x & (kWave - 1);
+  const int c16 = __builtin_amdgcn_ds_bpermute((ln ^ 16) << 2, c);
+  const int c32 = __builtin_amdgcn_ds_bpermute((ln ^ 32) << 2, c);
+  const int c48 = __builtin_amdgcn_ds_bpermute((ln ^ 48) << 2, c);
+  const int total = c + c16 + c32 + c48;
+  const int prefix = kg == 0 ? 0 : kg == 1 ? c16 : kg == 2 ? c32 + c48 : c16 + c32 + c48;
+  if (__any(lc + total > kStage)) stage_flush(a, list, colv, col, kg, st, lc);
+  int slot = lc + prefix;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    if (pass[j]) {
+      st[col * kStage + slot] = mk_key(ord_u32(acc[j] + 0.0f), (uint32_t)(tile_u0 + 4 * kg + j));
+      ++slot;
+    }
+  }
+  lc += total;
+}
+
 // Head-mode 0: one KV head per item, its G query heads in the MFMA columns, the
 // B operand in registers, PF tiles in flight per wave.
 template <int D, int KIND>
 __global__ __launch_bounds__(256) void k_score(ScoreArgs a) {
+  static_assert(KIND != K_STREAM, "head-mode-0 streaming runs in k_stream");
   constexpr int KS = D / 32, PF = 2;
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
@@ -520,9 +566,6 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a) {
       wr = colv && (a.flag ? (a.flag[list] != 0) : (ll == a.only_list));
       if (!__any(wr)) continue;  // same decision in every wave of the block
     }
-    uint32_t tau_u = 0xFFFFFFFFu;
-    if (KIND == K_STREAM && colv) tau_u = a.tau[list];
-    bool ovf = false;
     const u32x4* qb = a.qB + ((size_t)(s * a.L + l) * a.Hk + g) * (2 * KS * kWave);
     u32x4 bh[KS], bl[KS];
 #pragma unroll
@@ -550,17 +593,107 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a) {
       for (int p = 0; p < PF; ++p) {
         const int tt = t + p * nw;
         if (tt < ntiles) {
-          f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int i = 0; i < KS; ++i) {
-            acc = mfma_bf16(A[p][i], bh[i], acc);
-            acc = mfma_bf16(A[p][i], bl[i], acc);
-          }
-          emit<KIND>(a, s, list, colv, wr, tau_u, u0 + tt * kTile, u1, acc, kg, ovf);
+          const f32x4 acc = score_hilo<KS>(A[p], bh, bl);
+          emit<KIND>(a, s, list, colv, wr, u0 + tt * kTile, u1, acc, kg);
         }
         load(tt + PF * nw, A[p]);
       }
     }
+  }
+}
+
+// Streaming pass, head-mode 0.  The 16-row tiles of every (stream, layer, KV
+// head) segment are numbered one after another and wave w of W takes the
+// contiguous range [w T / W, (w + 1) T / W), so the work is balanced to a tile
+// whatever the mix of list lengths.  A tile is read with coalesced 16-byte
+// loads (one instruction covers 1 KiB of consecutive rows), stored into the
+// wave's LDS tile and read back in the MFMA A layout.  LDS holds the tile as
+// 256-byte lines of 16 chunks with chunk C of line R at position C ^ (R mod 16),
+// which keeps both the row-major writes and the column reads free of bank
+// conflicts.
+template <int D>
+__global__ __launch_bounds__(256) void k_stream(ScoreArgs a) {
+  constexpr int CPR = D / 8;        // 16-byte chunks per key row
+  constexpr int TCH = 16 * CPR;     // chunks per tile
+  constexpr int NI = TCH / kWave;   // load instructions per tile
+  constexpr int KS = D / 32;        // MFMA k-steps
+  constexpr int PF = 128 / D;       // tiles in flight per wave
+  __shared__ u32x4 tiles[4][TCH];
+  __shared__ uint64_t stage[4 * kMaxGroup * kStage];
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: segment state in SGPRs
+  const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
+  u32x4* lt_ = tiles[wave];
+  uint64_t* st = stage + wave * kMaxGroup * kStage;
+  const int64_t nw = (int64_t)gridDim.x * 4, gw = (int64_t)blockIdx.x * 4 + wave;
+  const int64_t total = a.tile_base[a.S];
+  const int64_t T1 = (gw + 1) * total / nw;
+  int64_t T = gw * total / nw;
+  while (T < T1) {
+    int s = 0;
+    while (T >= a.tile_base[s + 1]) ++s;
+    const int64_t rem = T - a.tile_base[s];
+    const int nt = a.ntile[s];
+    const int lg = (int)(rem / nt);
+    const int t0 = (int)(rem - (int64_t)lg * nt);
+    const int t1 = (int)min<int64_t>(nt, t0 + (T1 - T));
+    const int g = lg % a.Hk, l = lg / a.Hk;
+    const int n = a.n[s];
+    const bool colv = col < a.G;
+    const int list = s * a.NL + l * a.Hq + g * a.G + col;
+    const float tau_f = ord_f32(colv ? a.tau[list] : 0xFFFFFFFFu);
+    const u32x4* qb = a.qB + ((size_t)(s * a.L + l) * a.Hk + g) * (2 * KS * kWave);
+    u32x4 bh[KS], bl[KS];
+#pragma unroll
+    for (int i = 0; i < KS; ++i) {
+      bh[i] = qb[i * kWave + lane];
+      bl[i] = qb[(KS + i) * kWave + lane];
+    }
+    // The segment is read through a buffer resource of exactly n rows: lanes
+    // past the last row, and the loads that run ahead of the range, fetch
+    // zeros without touching memory (the host keeps a segment below 2 GiB).
+    // Lane q of load i covers the 16-byte chunk 64 i + q of the tile.
+    const uint16_t* seg = a.keys[s] + ((size_t)l * a.Hk + g) * (size_t)a.stride[s] * D;
+    const __amdgpu_buffer_rsrc_t rsrc =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(seg), (short)0, n * D * 2, 0x00020000);
+    auto load = [&](int t, u32x4 (&V)[NI]) {
+      const uint32_t off = t < t1 ? (uint32_t)t * (TCH * 16) + lane * 16 : 0x80000000u;
+#pragma unroll
+      for (int i = 0; i < NI; ++i)
+        V[i] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off + i * kWave * 16, 0, kAuxNT);
+    };
+    // The next loads are issued as soon as a tile's registers have gone to
+    // LDS, so they overlap the MFMAs and the candidate test.  Every pass of
+    // the loop body loads and computes (a pass past the range works on zeros
+    // and emits nothing), which keeps the waits exact.
+    u32x4 V[PF][NI];
+#pragma unroll
+    for (int p = 0; p < PF; ++p) load(t0 + p, V[p]);
+    int lc = 0;
+    for (int t = t0; t < t1; t += PF) {
+#pragma unroll
+      for (int p = 0; p < PF; ++p) {
+        const int tt = t + p;
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+          const int q = i * kWave + lane, R = q >> 4, C = q & 15;
+          lt_[R * 16 + (C ^ (R & 15))] = V[p][i];
+        }
+        __builtin_amdgcn_wave_barrier();
+        load(tt + PF, V[p]);
+        u32x4 A[KS];
+#pragma unroll
+        for (int i = 0; i < KS; ++i) {
+          const int q = rl * CPR + 4 * i + kg, R = q >> 4, C = q & 15;
+          A[i] = lt_[R * 16 + (C ^ (R & 15))];
+        }
+        __builtin_amdgcn_wave_barrier();
+        const f32x4 acc = score_hilo<KS>(A, bh, bl);
+        if (tt < t1) stream_emit(a, list, colv, col, tau_f, tt * kTile, n, acc, kg, st, lc);
+      }
+    }
+    if (__any(lc > 0)) stage_flush(a, list, colv, col, kg, st, lc);
+    T += t1 - t0;
   }
 }
 
@@ -572,6 +705,8 @@ __global__ __launch_bounds__(256) void k_score_hm(ScoreArgs a) {
   __shared__ u32x4 sB[8 * 2 * KS * kWave];  // H_kv <= 8 in head-mode 1
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
+  __shared__ uint64_t stage[KIND == K_STREAM ? 4 * kStage : 1];  // column 0 only
+  uint64_t* st = stage + (KIND == K_STREAM ? wave * kStage : 0);
   for (int item = blockIdx.x; item < a.total_items; item += gridDim.x) {
     int s = 0;
     while (item >= a.item_base[s + 1]) ++s;
@@ -587,9 +722,8 @@ __global__ __launch_bounds__(256) void k_score_hm(ScoreArgs a) {
       wr = colv && (a.flag ? (a.flag[list] != 0) : (l == a.only_list));
       if (!__any(wr)) continue;
     }
-    uint32_t tau_u = 0xFFFFFFFFu;
-    if (KIND == K_STREAM && colv) tau_u = a.tau[list];
-    bool ovf = false;
+    const float tau_f = ord_f32((KIND == K_STREAM && colv) ? a.tau[list] : 0xFFFFFFFFu);
+    int lc = 0;
     __syncthreads();
     const u32x4* qb = a.qB + (size_t)(s * a.L + l) * a.Hk * (2 * KS * kWave);
     for (int i = threadIdx.x; i < a.Hk * 2 * KS * kWave; i += blockDim.x) sB[i] = qb[i];
@@ -614,8 +748,12 @@ __global__ __launch_bounds__(256) void k_score_hm(ScoreArgs a) {
           acc = mfma_bf16(A[i], b[(KS + i) * kWave + lane], acc);
         }
       }
-      emit<KIND>(a, s, list, colv, wr, tau_u, u0 + t * kTile, u1, acc, kg, ovf);
+      if (KIND == K_STREAM)
+        stream_emit(a, list, colv, col, tau_f, u0 + t * kTile, u1, acc, kg, st, lc);
+      else
+        emit<KIND>(a, s, list, colv, wr, u0 + t * kTile, u1, acc, kg);
     }
+    if (KIND == K_STREAM && __any(lc > 0)) stage_flush(a, list, colv, col, kg, st, lc);
   }
 }
 
@@ -899,11 +1037,22 @@ __device__ void fallback_list(const ListArgs& a, int list, uint64_t* sel, int32_
     for (int g = g0; g < g0 + ng; ++g) {
       const u32x4* qb = a.qB + ((size_t)(s * a.L + l) * a.Hk + g) * (2 * KS * kWave);
       const uint16_t* p = a.keys[s] + ((size_t)l * a.Hk + g) * gstride + (size_t)(row < n ? row : 0) * D + 8 * kg;
+      u32x4 A[KS], bh[KS], bl[KS];
 #pragma unroll
       for (int i = 0; i < KS; ++i) {
-        const u32x4 A = row < n ? ld_nt(p + 32 * i) : u32x4{0, 0, 0, 0};
-        acc = mfma_bf16(A, qb[i * kWave + lane], acc);
-        acc = mfma_bf16(A, qb[(KS + i) * kWave + lane], acc);
+        A[i] = row < n ? ld_nt(p + 32 * i) : u32x4{0, 0, 0, 0};
+        bh[i] = qb[i * kWave + lane];
+        bl[i] = qb[(KS + i) * kWave + lane];
+      }
+      if (a.head_mode == 0) {
+        acc = score_hilo<KS>(A, bh, bl);
+      } else {
+        // head-mode 1 order, as in k_score_hm: k-steps interleaved, KV heads in turn
+#pragma unroll
+        for (int i = 0; i < KS; ++i) {
+          acc = mfma_bf16(A[i], bh[i], acc);
+          acc = mfma_bf16(A[i], bl[i], acc);
+        }
       }
     }
     if ((lane & 15) == col) {
@@ -1633,10 +1782,34 @@ ScoreArgs make_score_args(const RetrievePlan& p, int kind) {
   }
   a.item_base[p.S] = items;
   a.total_items = items;
+  int64_t tiles = 0;
+  for (int s = 0; s < p.S; ++s) {
+    a.tile_base[s] = tiles;
+    a.ntile[s] = cdiv(p.st[s].n, kTile);
+    tiles += (int64_t)p.L * p.Hk * a.ntile[s];
+  }
+  a.tile_base[p.S] = tiles;
   a.samp = p.samp; a.samp_stride = p.m_max;
   a.tau = p.tau; a.cnt = p.cnt; a.cand = p.cand; a.cap = p.cap;
   a.flag = p.flag; a.only_list = -1; a.full = p.full; a.row0 = 0;
   return a;
+}
+
+// Blocks of the streaming pass: as many as are resident on the device at once,
+// so that every wave takes one contiguous share of the tiles.
+template <int D>
+int stream_grid() {
+  static int grid = 0;
+  if (grid == 0) {
+    int dev = 0, cus = 256, per_cu = 0;
+    if (hipGetDevice(&dev) == hipSuccess)
+      (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_stream<D>, 256, 0) != hipSuccess ||
+        per_cu < 1)
+      per_cu = 1;
+    grid = per_cu * cus;
+  }
+  return grid;
 }
 
 template <int D, int KIND>
@@ -1686,7 +1859,18 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   hipLaunchKernelGGL(k_thresh, dim3(lists), dim3(1024), 0, st, la);
   // 4. streaming pass over every key row
   if (p.ev_start) (void)hipEventRecord(p.ev_start, st);
-  launch_score<D, K_STREAM>(make_score_args(p, K_STREAM), p.head_mode, 2048, st);
+  if (p.head_mode == 0) {
+    const ScoreArgs a = make_score_args(p, K_STREAM);
+    const int64_t tiles = a.tile_base[p.S];
+    if (tiles > 0) {
+      const int grid = (int)std::min<int64_t>(stream_grid<D>(), std::max<int64_t>(1, tiles / 16));
+      hipLaunchKernelGGL(k_stream<D>, dim3(grid), dim3(256), 0, st, a);
+    }
+  } else {
+    const ScoreArgs a = make_score_args(p, K_STREAM);
+    if (a.total_items > 0)
+      hipLaunchKernelGGL((k_score_hm<D, K_STREAM>), dim3(std::min(a.total_items, 2048)), dim3(256), 0, st, a);
+  }
   if (p.ev_stop) (void)hipEventRecord(p.ev_stop, st);
   // 5. exact top-k from candidates; 6. exact fallback for flagged lists
   hipLaunchKernelGGL(k_select<D>, dim3(lists), dim3(1024), 0, st, la);

@@ -47,6 +47,8 @@ FAKE = 0x7F0000000000     # 256-byte aligned stand-in address, never dereference
 def test_required_bytes_and_layout(L):
     lib = L.lib()
     d = desc(L)
+    # one (layer, KV head) of keys must stay below 2 GiB: 2^23 - 1 rows at d = 128
+    assert lib.ss_index_required_bytes(C.byref(desc(L, max_rows=2 ** 23 - 1))) > 0
     n = lib.ss_index_required_bytes(C.byref(d))
     keys = 4 * 4 * 19600 * 128 * 2
     counts = 4 * 4 * 19600 * 4
@@ -54,7 +56,8 @@ def test_required_bytes_and_layout(L):
     assert n % 256 == 0
     for bad in (dict(head_dim=96), dict(n_q_heads=27), dict(n_q_heads=68, n_kv_heads=4),
                 dict(max_rows=0), dict(max_frames=0), dict(n_layers=0), dict(n_layers=33),
-                dict(n_kv_heads=16, n_q_heads=16), dict(n_recent=-1), dict(max_rows=2 ** 31)):
+                dict(n_kv_heads=16, n_q_heads=16), dict(n_recent=-1), dict(max_rows=2 ** 31),
+                dict(max_rows=2 ** 23)):
         assert lib.ss_index_required_bytes(C.byref(desc(L, **bad))) == 0, bad
 
 
