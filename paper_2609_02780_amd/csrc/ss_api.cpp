@@ -115,12 +115,16 @@ static_assert(kFullScanRows <= 16384, "a full-scan sample must fit the register 
 constexpr int kChunkRows = 4096;
 constexpr int kSampleChunk = 128;
 
-// Expected candidates per list: 8k (at least 2048), raised for very long lists
-// so the sample stays within the register select (kSampleMax rows).
+// Expected candidates per list: 3k (at least 1024), raised for very long lists
+// so the sample stays within the register select (kSampleMax rows).  The count
+// behaves like E Gamma(r) / r: with r = 48 it falls below k = E/3 with
+// probability 1e-10 per list and exceeds the capacity 2E with 2e-8; either case
+// takes the exact fallback.  A smaller E keeps fewer tiles on the candidate
+// path of the streaming pass.
 constexpr int64_t kSampleMax = 16384;
 int64_t expected_candidates(int64_t n, int64_t kk) {
   const int64_t r = std::min<int64_t>(kk, kSampleRank);
-  return std::max<int64_t>({8 * kk, 2048, (n * r + kSampleMax - 1) / kSampleMax});
+  return std::max<int64_t>({3 * kk, 1024, (n * r + kSampleMax - 1) / kSampleMax});
 }
 
 struct StreamSizes {
@@ -129,8 +133,8 @@ struct StreamSizes {
 
 // Sample plan of one list.  With m sampled rows spread evenly over n rows and the
 // cut-off at the r-th largest sample score, about r n / m rows score at or above
-// it (the expected candidate count E).  r = min(k, 48) keeps the count below k
-// six standard deviations away; m = n gives an exact cut (r = k) for small lists.
+// it (the expected candidate count E).  r = min(k, 48); m = n gives an exact
+// cut (r = k) for small lists.
 StreamSizes plan_stream(int64_t n, int64_t f, int top_k) {
   StreamSizes z{};
   z.n = (int)n;
