@@ -442,3 +442,36 @@ def retrieve(index: Index, queries, top_k: int, n_select: int, pool_mult: int = 
         return out + ({"scores": S, "topk": T, "votes": votes, "mass": mass, "pool": pool,
                        "maxmin_margins": margins},)
     return out
+
+
+# ---------------------------------------------------------------------------
+# Evidence assembly (Eq. selected_evidence, then deduplication and temporal
+# ordering, Sec. 4.2)
+# ---------------------------------------------------------------------------
+
+
+def evidence_units(n_frames: int, selected, n_recent: int, n_before: int = 1, n_after: int = 0,
+                   retrieved: bool = True) -> np.ndarray:
+    """The units handed to full-depth answering, ascending, without repeats.
+
+    ``R_T`` is the newest ``n_recent`` units of the ``n_frames`` stored so far
+    (Eq. context_partition).  When retrieval ran, each selected unit ``t`` is
+    expanded to its temporal neighbours ``t - n_before .. t + n_after`` (the
+    paper's setting is one preceding unit), keeping only units that exist, and
+    the evidence is ``R_T`` united with those; otherwise it is ``R_T`` alone.
+    Entries of ``selected`` below 0 are padding and are ignored.
+    """
+    if n_frames < 0 or n_recent < 0 or n_before < 0 or n_after < 0:
+        raise ValueError("sizes must be >= 0")
+    units = set(range(max(0, n_frames - n_recent), n_frames))
+    if retrieved:
+        for t in selected:
+            t = int(t)
+            if t < 0:
+                continue
+            if t >= n_frames:
+                raise ValueError(f"selected unit {t} outside the {n_frames} stored units")
+            for u in range(t - n_before, t + n_after + 1):
+                if 0 <= u < n_frames:
+                    units.add(u)
+    return np.array(sorted(units), dtype=np.int64)

@@ -492,3 +492,50 @@ def test_generator_c5_specs():
     assert all(300 <= s.n_frames <= 3600 for s in specs)
     assert all((s.compress is not None) == (s.stream % 2 == 1) for s in specs)
     assert all(s.n_planted == math.ceil(s.n_frames / 150) for s in specs)
+
+
+# ---------------------------------------------------------------------------
+# Evidence assembly (Eq. selected_evidence, deduplication, temporal order)
+# ---------------------------------------------------------------------------
+
+def _evidence_cases():
+    with open(os.path.join(GOLDEN, "evidence_hand.json")) as f:
+        return json.load(f)["cases"]
+
+
+@pytest.mark.parametrize("case", _evidence_cases(), ids=lambda c: c["name"])
+def test_evidence_hand(case):
+    got = O.evidence_units(case["n_frames"], case["selected"], case["n_recent"], case["n_before"],
+                           case["n_after"], case["retrieved"])
+    assert got.tolist() == case["units"]
+
+
+def test_evidence_invariants_random():
+    """Sorted, repeat-free, holds the recent window and every selected unit,
+    every member is recent or within the neighbourhood of a selected unit, and
+    the size stays within N_r + |sel| (1 + before + after).  Checked against a
+    per-unit membership test written from the definition."""
+    rng = np.random.default_rng(5)
+    for _ in range(300):
+        T = int(rng.integers(0, 60))
+        nr, nb, na = (int(x) for x in rng.integers(0, 5, size=3))
+        nsel = int(rng.integers(0, 8))
+        sel = rng.integers(0, max(T, 1), size=nsel) if T > 0 else np.zeros(0, np.int64)
+        sel = np.concatenate([sel, -np.ones(int(rng.integers(0, 3)), np.int64)])
+        got = O.evidence_units(T, sel, nr, nb, na, True)
+        assert np.all(np.diff(got) > 0)
+        want = [u for u in range(T)
+                if u >= T - nr or any(0 <= s and s - nb <= u <= s + na for s in sel.tolist())]
+        assert got.tolist() == want
+        assert set(range(max(0, T - nr), T)) <= set(got.tolist())
+        assert {int(s) for s in sel if s >= 0} <= set(got.tolist())
+        assert got.size <= nr + int((sel >= 0).sum()) * (1 + nb + na)
+        only = O.evidence_units(T, sel, nr, nb, na, False)
+        assert only.tolist() == list(range(max(0, T - nr), T))
+
+
+def test_evidence_rejects_bad_input():
+    with pytest.raises(ValueError):
+        O.evidence_units(5, [7], 2)
+    with pytest.raises(ValueError):
+        O.evidence_units(5, [1], -1)
