@@ -122,6 +122,24 @@ def time_append(torch, P, cfg, frames=64):
             "batch_frames_per_s": frames / (batch_ms / 1e3)}
 
 
+def time_evidence(torch, P, idxs, frame_ids, calls=20):
+    """Evidence assembly after the retrieval, with the paper's settings: 6
+    recent units and one preceding unit per selected unit."""
+    for _ in range(3):
+        P.assemble_evidence(idxs, frame_ids, 6, 1, 0, True)
+    torch.cuda.synchronize()
+    lat = []
+    for _ in range(calls):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        units, n_units = P.assemble_evidence(idxs, frame_ids, 6, 1, 0, True)
+        b.record()
+        b.synchronize()
+        lat.append(a.elapsed_time(b))
+    return {"p50_ms": float(np.median(lat)), "n_recent": 6, "n_before": 1, "n_after": 0,
+            "units_stream0": int(n_units[0].item())}
+
+
 def cpu_model() -> str:
     try:
         for line in open("/proc/cpuinfo"):
@@ -257,6 +275,7 @@ def main():
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "avg_kernel_ms": float(hot.mean()), "bytes_per_launch": key_bytes},
     }
+    out["evidence"] = time_evidence(torch, P, idxs, r.frame_ids)
     if cfg.compress is not None:
         out["append"] = time_append(torch, P, cfg)
     if not args.no_cpu_baseline:

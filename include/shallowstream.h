@@ -184,6 +184,42 @@ ss_status ss_retrieve_debug(ss_index* const* idx, int32_t n_streams, const void*
                             size_t ws_bytes, void* stream, int64_t* frame_ids, int32_t* votes,
                             float* mass, int32_t* n_out, const ss_debug_out* dbg);
 
+/* Evidence assembly parameters (Eq. selected_evidence).
+ *   n_recent   N_r, the newest frames that are always evidence (Eq.
+ *              context_partition); the paper uses 6 with retrieval, 2 without.
+ *   n_before   frames before each selected frame added as its temporal
+ *              neighbours (the paper: 1); n_after likewise after it (0).
+ *   retrieved  the gate's decision: 1 when retrieval ran, 0 for recent
+ *              context only. */
+typedef struct {
+  int32_t n_recent;
+  int32_t n_before;
+  int32_t n_after;
+  int32_t retrieved;
+} ss_evidence_params;
+
+/* Units ss_assemble_evidence can return per stream: n_recent, plus
+ * n_select*(1+n_before+n_after) when retrieved.  0 if the parameters are
+ * invalid or the count exceeds 4096. */
+int32_t ss_evidence_max_units(const ss_evidence_params* params, int32_t n_select);
+
+/* The frames handed to full-depth answering for each of n_streams streams
+ * (Eq. selected_evidence, then deduplication and temporal order): with T the
+ * frames stored in idx[s], the newest min(n_recent, T) frames, united, when
+ * retrieved, with frames t-n_before .. t+n_after (those in [0, T)) of every
+ * selected frame t; sorted ascending without repeats.
+ *   frame_ids  device int64 [n_streams][n_select] as ss_retrieve writes them
+ *              (entries < 0 are padding; ids >= T are skipped).  Not read, and
+ *              may be NULL, when params->retrieved is 0.
+ *   units      device int64 [n_streams][max_units] out, ascending, -1 padded;
+ *   n_units    device int32 [n_streams] out.
+ *   max_units  >= ss_evidence_max_units(params, n_select).
+ * Enqueued on `stream` after the retrieval that wrote frame_ids; uses the
+ * frame counts of the indices at the time of the call. */
+ss_status ss_assemble_evidence(ss_index* const* idx, int32_t n_streams, const int64_t* frame_ids,
+                               int32_t n_select, const ss_evidence_params* params, void* stream,
+                               int64_t* units, int32_t* n_units, int32_t max_units);
+
 /* Every score of one list over rows [row0, row0+n_rows) of one index, with the
  * same arithmetic as ss_retrieve (parity only).  queries: host array of L_s
  * device pointers as in ss_retrieve.  out: device fp32 [n_rows].  With

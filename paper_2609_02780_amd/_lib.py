@@ -40,6 +40,11 @@ class RetrieveParams(C.Structure):
                 ("head_mode", C.c_int32)]
 
 
+class EvidenceParams(C.Structure):
+    _fields_ = [("n_recent", C.c_int32), ("n_before", C.c_int32), ("n_after", C.c_int32),
+                ("retrieved", C.c_int32)]
+
+
 class DebugOut(C.Structure):
     _fields_ = [("topk_pos", C.c_void_p), ("topk_score", C.c_void_p), ("vote_hist", C.c_void_p),
                 ("mass_hist", C.c_void_p), ("pool", C.c_void_p), ("pool_n", C.c_void_p),
@@ -65,6 +70,9 @@ _SIGS = {
     "ss_debug_scores": (C.c_int32, [_P, C.POINTER(_P), C.c_int32, C.c_int32, C.c_int32, C.c_int32,
                                     C.c_int64, C.c_int64, _P, _P, C.c_size_t, _P]),
     "ss_index_export": (C.c_int32, [_P, _P, _P, _P, C.POINTER(C.c_int64), _P]),
+    "ss_evidence_max_units": (C.c_int32, [C.POINTER(EvidenceParams), C.c_int32]),
+    "ss_assemble_evidence": (C.c_int32, [C.POINTER(_P), C.c_int32, _P, C.c_int32, C.POINTER(EvidenceParams), _P,
+                                         _P, _P, C.c_int32]),
     "ss_set_profile_events": (C.c_int32, [_P, _P]),
     "ss_status_string": (C.c_char_p, [C.c_int32]),
     "ss_last_error": (C.c_char_p, []),

@@ -322,9 +322,64 @@ ss_status retrieve_common(ss_index* const* idx, int32_t n_streams, const void* c
   return SS_OK;
 }
 
+// Candidate units of one stream's evidence, or -1 for invalid parameters.
+int64_t evidence_units_max(const ss_evidence_params* p, int32_t n_select) {
+  if (!p || p->n_recent < 0 || p->n_before < 0 || p->n_after < 0) return -1;
+  if (p->retrieved != 0 && p->retrieved != 1) return -1;
+  int64_t n = p->n_recent;
+  if (p->retrieved) {
+    if (n_select < 1 || n_select > ss::kMaxSelect) return -1;
+    n += (int64_t)n_select * (1 + (int64_t)p->n_before + p->n_after);
+  }
+  return n;
+}
+
 }  // namespace
 
 extern "C" {
+
+int32_t ss_evidence_max_units(const ss_evidence_params* params, int32_t n_select) {
+  const int64_t n = evidence_units_max(params, n_select);
+  return (n < 0 || n > ss::kMaxEvidence) ? 0 : (int32_t)std::max<int64_t>(n, 1);
+}
+
+ss_status ss_assemble_evidence(ss_index* const* idx, int32_t n_streams, const int64_t* frame_ids,
+                               int32_t n_select, const ss_evidence_params* params, void* stream,
+                               int64_t* units, int32_t* n_units, int32_t max_units) {
+  if (!idx) return fail(SS_ERR_INVALID_ARGUMENT, "idx is NULL");
+  if (n_streams < 1) return fail(SS_ERR_INVALID_ARGUMENT, "n_streams must be >= 1");
+  for (int s = 0; s < n_streams; ++s)
+    if (!idx[s]) return fail(SS_ERR_INVALID_ARGUMENT, "idx[%d] is NULL", s);
+  const int64_t need = evidence_units_max(params, n_select);
+  if (need < 0) return fail(SS_ERR_INVALID_ARGUMENT, "invalid evidence parameters");
+  if (need > ss::kMaxEvidence)
+    return fail(SS_ERR_UNSUPPORTED, "%lld candidate units per stream > %d", (long long)need, ss::kMaxEvidence);
+  if (max_units < std::max<int64_t>(need, 1) || max_units > ss::kMaxEvidence)
+    return fail(SS_ERR_INVALID_ARGUMENT, "max_units %d outside %lld..%d", max_units,
+                (long long)std::max<int64_t>(need, 1), ss::kMaxEvidence);
+  if (params->retrieved && !frame_ids) return fail(SS_ERR_INVALID_ARGUMENT, "frame_ids is NULL");
+  if (!units || !n_units) return fail(SS_ERR_INVALID_ARGUMENT, "an output pointer is NULL");
+  if (!aligned(units, 8) || !aligned(n_units, 4) || (frame_ids && !aligned(frame_ids, 8)))
+    return fail(SS_ERR_INVALID_ARGUMENT, "misaligned device pointer");
+  const hipStream_t hs = static_cast<hipStream_t>(stream);
+  for (int s0 = 0; s0 < n_streams; s0 += ss::kMaxStreams) {
+    ss::EvidenceArgs a{};
+    a.S = std::min(ss::kMaxStreams, n_streams - s0);
+    a.n_select = params->retrieved ? n_select : 0;
+    a.n_recent = params->n_recent;
+    a.n_before = params->n_before;
+    a.n_after = params->n_after;
+    a.retrieved = params->retrieved;
+    a.max_units = max_units;
+    for (int s = 0; s < a.S; ++s) a.T[s] = idx[s0 + s]->n_frames;
+    a.frame_ids = params->retrieved ? frame_ids + (size_t)s0 * n_select : nullptr;
+    a.units = units + (size_t)s0 * max_units;
+    a.n_units = n_units + s0;
+    const hipError_t e = ss::launch_evidence(a, hs);
+    if (e != hipSuccess) return fail(SS_ERR_DEVICE, "evidence launch failed: %s", hipGetErrorString(e));
+  }
+  return SS_OK;
+}
 
 size_t ss_index_required_bytes(const ss_index_desc* desc) {
   if (check_desc(desc) != SS_OK) return 0;

@@ -134,6 +134,17 @@ size_t carve_workspace(RetrievePlan& p, void* ws);
 
 hipError_t launch_retrieve(RetrievePlan& p, hipStream_t st);
 
+// Evidence assembly of up to kMaxStreams streams, one block each.
+constexpr int kMaxEvidence = 4096;   // candidate units per stream (sorted in LDS)
+struct EvidenceArgs {
+  int S, n_select, n_recent, n_before, n_after, retrieved, max_units;
+  int64_t T[kMaxStreams];        // frames stored per stream
+  const int64_t* frame_ids;      // [S][n_select], may be null when !retrieved
+  int64_t* units;                // [S][max_units]
+  int32_t* n_units;              // [S]
+};
+hipError_t launch_evidence(const EvidenceArgs& a, hipStream_t st);
+
 // Scores of one list over a row range, same arithmetic as the retrieval.
 hipError_t launch_debug_scores(RetrievePlan& p, int layer, int q_head, int64_t row0,
                                int64_t n_rows, float* out, hipStream_t st);

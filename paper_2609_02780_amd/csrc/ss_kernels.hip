@@ -1744,6 +1744,50 @@ __global__ __launch_bounds__(256) void k_kmeans(AppendArgs a) {
   for (int c = t; c < C; c += blockDim.x) a.dst.counts[drow0 + c] = a.n_iters > 0 ? ccount[c] : 0;
 }
 
+// ---------------------------------------------------------------------------
+// k_evidence: Eq. selected_evidence plus deduplication and temporal order.
+// One block per stream: the recent window and every selected frame's
+// neighbourhood are laid out as candidate slots (missing ones as a sentinel),
+// sorted ascending in LDS, and the distinct values compacted in order.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_evidence(EvidenceArgs a) {
+  __shared__ uint64_t buf[kMaxEvidence];
+  __shared__ int scan_sh[17];
+  const int s = blockIdx.x;
+  const int64_t T = a.T[s];
+  const int64_t r0 = T > a.n_recent ? T - a.n_recent : 0;
+  const int nrec = (int)(T - r0);
+  const int span = a.n_before + 1 + a.n_after;
+  const int total = nrec + (a.retrieved ? a.n_select * span : 0);
+  const int P = pow2_ceil(max(total, 2));
+  // keys sort descending: key = INT64_MAX - unit; a missing slot is key 0
+  for (int i = threadIdx.x; i < P; i += blockDim.x) {
+    int64_t u = -1;
+    if (i < nrec) {
+      u = r0 + i;
+    } else if (i < total) {
+      const int j = i - nrec, slot = j / span, off = j % span - a.n_before;
+      const int64_t t = a.frame_ids[(size_t)s * a.n_select + slot];
+      if (t >= 0 && t < T && t + off >= 0 && t + off < T) u = t + off;
+    }
+    buf[i] = u >= 0 ? (uint64_t)(INT64_MAX - u) : 0ull;
+  }
+  __syncthreads();
+  bitonic_desc_u64(buf, P);
+  int64_t* out = a.units + (size_t)s * a.max_units;
+  int base = 0;
+  for (int b0 = 0; b0 < P; b0 += blockDim.x) {
+    const int i = b0 + threadIdx.x;
+    const bool keep = i < P && buf[i] != 0 && (i == 0 || buf[i] != buf[i - 1]);
+    int tot;
+    const int pre = block_excl_scan(keep ? 1 : 0, scan_sh, tot);
+    if (keep) out[base + pre] = INT64_MAX - (int64_t)buf[i];
+    base += tot;
+  }
+  for (int i = base + threadIdx.x; i < a.max_units; i += blockDim.x) out[i] = -1;
+  if (threadIdx.x == 0) a.n_units[s] = base;
+}
+
 inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
 template <int D>
@@ -1932,6 +1976,11 @@ hipError_t debug_scores_impl(RetrievePlan& p, int layer, int q_head, int64_t row
 }
 
 }  // namespace
+
+hipError_t launch_evidence(const EvidenceArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(k_evidence, dim3(a.S), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
 
 size_t carve_workspace(RetrievePlan& p, void* ws) {
   size_t off = 0;

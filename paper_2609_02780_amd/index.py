@@ -206,6 +206,35 @@ class Retriever:
         return out
 
 
+def assemble_evidence(indices, frame_ids, n_recent: int, n_before: int = 1, n_after: int = 0,
+                      retrieved: bool = True, stream=None):
+    """The frames handed to answering for each stream (Eq. selected_evidence,
+    deduplicated, in temporal order).  ``frame_ids``: device int64
+    ``[n_streams][n_select]`` as returned by :class:`Retriever` (ignored when
+    ``retrieved`` is false).  Returns device tensors ``(units, n_units)``:
+    ``units`` int64 ``[n_streams][max_units]`` ascending and -1 padded."""
+    indices = list(indices)
+    S = len(indices)
+    n_select = frame_ids.shape[1] if (retrieved and frame_ids is not None) else 0
+    prm = L.EvidenceParams(n_recent, n_before, n_after, 1 if retrieved else 0)
+    max_units = L.lib().ss_evidence_max_units(C.byref(prm), n_select)
+    if max_units == 0:
+        raise L.SSError(L.SS_ERR_INVALID_ARGUMENT, "invalid evidence parameters")
+    dev = indices[0].arena.device
+    fid = 0
+    if retrieved:
+        if frame_ids.dtype != torch.int64 or not frame_ids.is_cuda or tuple(frame_ids.shape) != (S, n_select) \
+                or not frame_ids.is_contiguous():
+            raise ValueError("frame_ids must be a contiguous device int64 tensor [n_streams][n_select]")
+        fid = frame_ids.data_ptr()
+    units = torch.empty((S, max_units), dtype=torch.int64, device=dev)
+    n_units = torch.empty(S, dtype=torch.int32, device=dev)
+    handles = L.ptr_array([x.handle.value for x in indices])
+    L.check(L.lib().ss_assemble_evidence(handles, S, fid, n_select, C.byref(prm), _stream_handle(stream),
+                                         units.data_ptr(), n_units.data_ptr(), max_units))
+    return units, n_units
+
+
 def set_profile_events(start, stop) -> None:
     """Record ``start``/``stop`` (torch.cuda.Event) around the streaming scoring
     kernel of later retrievals on this thread; ``None, None`` turns it off."""

@@ -178,3 +178,30 @@ def test_workspace_grows_with_batch(L):
     assert three > one > 0
     for h in hs:
         lib.ss_index_destroy(h)
+
+
+def test_evidence_validation(L):
+    """Host-side checks of ss_assemble_evidence; nothing is launched."""
+    lib = L.lib()
+    h = create(L, max_frames=4, max_rows=4 * 196)
+    idx = (C.c_void_p * 1)(h.value)
+    P = L.EvidenceParams
+    assert lib.ss_evidence_max_units(C.byref(P(6, 1, 0, 1)), 8) == 6 + 8 * 2
+    assert lib.ss_evidence_max_units(C.byref(P(2, 1, 0, 0)), 8) == 2
+    assert lib.ss_evidence_max_units(C.byref(P(0, 0, 0, 0)), 0) == 1       # room for nothing, still >= 1
+    assert lib.ss_evidence_max_units(C.byref(P(-1, 1, 0, 1)), 8) == 0
+    assert lib.ss_evidence_max_units(C.byref(P(6, 1, 0, 2)), 8) == 0
+    assert lib.ss_evidence_max_units(C.byref(P(6, 1, 0, 1)), 65) == 0
+    assert lib.ss_evidence_max_units(C.byref(P(4000, 10, 10, 1)), 64) == 0   # beyond 4096 candidates
+    ok = P(6, 1, 0, 1)
+    F = FAKE
+    assert lib.ss_assemble_evidence(idx, 1, F, 8, C.byref(ok), None, F, F, 10) == L.SS_ERR_INVALID_ARGUMENT
+    assert b"max_units" in lib.ss_last_error()
+    assert lib.ss_assemble_evidence(idx, 1, None, 8, C.byref(ok), None, F, F, 22) == L.SS_ERR_INVALID_ARGUMENT
+    assert lib.ss_assemble_evidence(idx, 1, F, 8, C.byref(ok), None, None, F, 22) == L.SS_ERR_INVALID_ARGUMENT
+    assert lib.ss_assemble_evidence(idx, 1, F + 4, 8, C.byref(ok), None, F, F, 22) == L.SS_ERR_INVALID_ARGUMENT
+    assert lib.ss_assemble_evidence(idx, 0, F, 8, C.byref(ok), None, F, F, 22) == L.SS_ERR_INVALID_ARGUMENT
+    assert lib.ss_assemble_evidence(idx, 1, F, 8, None, None, F, F, 22) == L.SS_ERR_INVALID_ARGUMENT
+    big = P(4000, 10, 10, 1)
+    assert lib.ss_assemble_evidence(idx, 1, F, 64, C.byref(big), None, F, F, 4096) == L.SS_ERR_UNSUPPORTED
+    assert lib.ss_index_destroy(h) == 0
