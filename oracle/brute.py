@@ -138,3 +138,30 @@ def retrieve(frames, queries, n_kv_heads: int, top_k: int, n_select: int, pool_m
     ma = [mass[t] for t in sel] + [0.0] * (n_select - len(sel))
     return ids, vo, ma, {"lists": lists, "votes": votes, "mass": mass, "pool": pool,
                          "desc": descs}
+
+
+def pooled_scores(frames, queries, n_kv_heads: int, n_recent: int = 0) -> list:
+    """Pooled shallow Q-K score of every candidate unit, written out as the mean,
+    over layers, query heads, query tokens and the unit's tokens, of the scaled
+    per-token logit (``frames`` and ``queries`` as in ``retrieve``)."""
+    F = len(frames)
+    L = len(queries)
+    Hq = len(queries[0])
+    G = Hq // n_kv_heads
+    d = len(queries[0][0][0])
+    out = []
+    for t in range(max(0, F - n_recent)):
+        terms = []
+        for l in range(L):
+            for h in range(Hq):
+                g = h // G
+                toks = frames[t][l][g]
+                qs = queries[l][h]
+                w = 1.0 / (L * Hq * len(qs) * len(toks))
+                for qj in qs:
+                    q = _vec(qj)
+                    for krow in toks:
+                        k = _vec(krow)
+                        terms.append(w * math.fsum(a * b for a, b in zip(q, k)) / math.sqrt(d))
+        out.append(math.fsum(terms))
+    return out

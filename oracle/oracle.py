@@ -89,6 +89,14 @@ def descriptor(last_layer_keys: np.ndarray) -> np.ndarray:
     return vec / n if n > 0 else vec
 
 
+def unit_mean_keys(frame_layer_keys) -> np.ndarray:
+    """The unit's pooled keys: per shallow layer and KV head, the mean of its raw
+    visual tokens' keys (the unnormalised means behind Eq. memory_key, at every
+    layer).  ``frame_layer_keys``: per layer ``uint16 [H_kv][T][d]``.  Returns
+    float64 ``[L][H_kv][d]``."""
+    return np.stack([decode_bf16(k).mean(axis=1) for k in frame_layer_keys])
+
+
 # ---------------------------------------------------------------------------
 # Per-frame k-means compression (compression at append time)
 # ---------------------------------------------------------------------------
@@ -189,6 +197,7 @@ class Index:
         self.row_start: list[int] = []
         self.row_count: list[int] = []
         self.desc: list[np.ndarray] = []
+        self.pooled: list[np.ndarray] = []               # per frame [L][H_kv][d] mean raw key
         self.counts: list[np.ndarray] = []               # per frame [L][H_kv][rows] member counts
         self.kmeans_diag: list = []
 
@@ -218,6 +227,7 @@ class Index:
             sl = slice(f * T, (f + 1) * T)
             last = decode_bf16(layer_keys[self.L - 1][:, sl, :])
             self.desc.append(descriptor(last))
+            self.pooled.append(unit_mean_keys([layer_keys[l][:, sl, :] for l in range(self.L)]))
             if compress is None:
                 rows = [layer_keys[l][:, sl, :] for l in range(self.L)]
                 cnt = np.ones((self.L, self.Hk, T), dtype=np.int64)
@@ -245,18 +255,20 @@ class Index:
         self._rows_cache = None
         return first
 
-    def append_stored(self, layer_rows, rows_per_frame, descriptors) -> int:
+    def append_stored(self, layer_rows, rows_per_frame, descriptors, pooled=None) -> int:
         """Append frames whose stored rows and descriptors were produced elsewhere
         (e.g. compressed rows exported from another implementation), so retrieval
         can be checked on identical stored data.
 
         ``layer_rows``: per layer ``uint16 [H_kv][sum(rows_per_frame)][d]``;
-        ``descriptors``: ``[n_frames][H_kv * d]``.
+        ``descriptors``: ``[n_frames][H_kv * d]``; ``pooled``: optional
+        ``[n_frames][L][H_kv][d]`` mean raw keys (``unit_mean_keys``).
         """
         first = self.n_frames
         start = 0
         for f, n_r in enumerate(rows_per_frame):
             self.desc.append(np.asarray(descriptors[f], dtype=np.float64))
+            self.pooled.append(None if pooled is None else np.asarray(pooled[f], dtype=np.float64))
             self.row_start.append(self.n_rows)
             self.row_count.append(int(n_r))
             for l in range(self.L):
@@ -475,3 +487,51 @@ def evidence_units(n_frames: int, selected, n_recent: int, n_before: int = 1, n_
                 if 0 <= u < n_frames:
                     units.add(u)
     return np.array(sorted(units), dtype=np.int64)
+
+
+# ---------------------------------------------------------------------------
+# Pooled shallow Q-K ranker (the baseline evidence ranker of the ablation
+# comparing rankers in Sec. 5)
+# ---------------------------------------------------------------------------
+
+
+def pooled_scores(index: Index, queries) -> np.ndarray:
+    """Score of every candidate unit under pooled shallow Q-K ranking.
+
+    Reading: keys are pooled per unit before the Q-K product, so a unit's score
+    is the scaled logit of the question's mean query against the unit's mean
+    raw key (``unit_mean_keys``), averaged over every shallow layer and query
+    head (query head ``h`` reads KV head ``h // G``):
+    ``(1 / (L H_q)) sum_{l,h} qbar_{l,h} . Kbar_{l,g(h),t} / sqrt(d)``.  For raw
+    units this is the mean of the unit's token scores over its tokens and over
+    every (layer, head) list.  Candidates are the units before the recent window
+    (Eq. context_partition).
+    """
+    F = index.candidate_frames()
+    qm = query_means(queries)
+    s = np.zeros(F)
+    if F == 0:
+        return s
+    if any(p is None for p in index.pooled[:F]):
+        raise ValueError("pooled keys missing for some units")
+    Kp = np.stack(index.pooled[:F])                         # [F][L][H_kv][d]
+    for l in range(index.L):
+        for h in range(index.Hq):
+            s += Kp[:, l, h // index.G, :] @ qm[l][h]
+    return s / (index.L * index.Hq * math.sqrt(index.d))
+
+
+def pooled_retrieve(index: Index, queries, n_select: int):
+    """The ``n_select`` best units by pooled score, ties to the earlier unit; no
+    diversity selection or temporal expansion.  Returns ``(frame_ids, scores,
+    n_out)`` padded with -1 and 0."""
+    if n_select < 1:
+        raise ValueError("n_select must be >= 1")
+    s = pooled_scores(index, queries)
+    t = np.arange(s.size)
+    order = np.lexsort((t, -s))[:n_select]
+    ids = np.full(n_select, -1, dtype=np.int64)
+    sc = np.zeros(n_select)
+    ids[:order.size] = order
+    sc[:order.size] = s[order]
+    return ids, sc, int(order.size)

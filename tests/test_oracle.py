@@ -539,3 +539,66 @@ def test_evidence_rejects_bad_input():
         O.evidence_units(5, [7], 2)
     with pytest.raises(ValueError):
         O.evidence_units(5, [1], -1)
+
+
+# ---------------------------------------------------------------------------
+# Pooled shallow Q-K ranker
+# ---------------------------------------------------------------------------
+
+def test_pooled_hand():
+    spec = _load("hand_retrieval.json")
+    pooled = _load("pooled_hand.json")
+    idx, q = hand_index(spec)
+    np.testing.assert_array_equal(O.pooled_scores(idx, q), np.array(pooled["scores"]))
+    for c in pooled["cases"]:
+        idx, q = hand_index(spec, c["n_recent"])
+        ids, sc, n = O.pooled_retrieve(idx, q, c["n_select"])
+        assert ids.tolist() == c["frame_ids"]
+        np.testing.assert_array_equal(sc, np.array(c["scores"]))
+        assert n == sum(1 for x in c["frame_ids"] if x >= 0)
+
+
+@pytest.mark.parametrize("seed,Hq,Hk,nr", [(0, 4, 2, 0), (1, 6, 2, 1), (2, 3, 3, 2)])
+def test_pooled_matches_brute_and_token_means(seed, Hq, Hk, nr):
+    """Against the per-token brute force, and (linearity of the logit) against
+    the mean of the unit's token scores over every (layer, head) list."""
+    rng = np.random.default_rng(50 + seed)
+    L, d, F, T, nq = 2, 8, 6, 5, 3
+    keys = [W.bf16_bits(rng.standard_normal((Hk, F * T, d)).astype(np.float32)) for _ in range(L)]
+    q = [W.bf16_bits(rng.standard_normal((Hq, nq, d)).astype(np.float32)) for _ in range(L)]
+    idx = O.Index(L, Hq, Hk, d, nr)
+    idx.append(keys, F, T)
+    s = O.pooled_scores(idx, q)
+    frames = _brute_frames(keys, F, T, L, Hk)
+    qs = [[[q[l][h][j] for j in range(nq)] for h in range(Hq)] for l in range(L)]
+    np.testing.assert_allclose(s, brute.pooled_scores(frames, qs, Hk, nr), rtol=1e-12, atol=1e-12)
+    lists = O.score_lists(idx, q)
+    fr = idx.frame_of_row()[:idx.candidate_rows()]
+    mean_tok = np.array([np.mean([lst[fr == t].mean() for lst in lists]) for t in range(F - nr)])
+    np.testing.assert_allclose(s, mean_tok, rtol=1e-12, atol=1e-12)
+    ids, sc, n = O.pooled_retrieve(idx, q, 4)
+    want = sorted(range(F - nr), key=lambda t: (-s[t], t))[:4]
+    assert ids[:n].tolist() == want
+
+
+def test_pooled_invariant_under_token_permutation():
+    rng = np.random.default_rng(9)
+    L, Hq, Hk, d, F, T = 2, 4, 2, 8, 4, 6
+    keys = [W.bf16_bits(rng.standard_normal((Hk, F * T, d)).astype(np.float32)) for _ in range(L)]
+    q = [W.bf16_bits(rng.standard_normal((Hq, 2, d)).astype(np.float32)) for _ in range(L)]
+    perm = np.concatenate([f * T + rng.permutation(T) for f in range(F)])
+    a, b = O.Index(L, Hq, Hk, d), O.Index(L, Hq, Hk, d)
+    a.append(keys, F, T)
+    b.append([k[:, perm, :] for k in keys], F, T)
+    np.testing.assert_allclose(O.pooled_scores(a, q), O.pooled_scores(b, q), rtol=1e-12, atol=1e-12)
+
+
+def test_pooled_uses_raw_keys_of_compressed_units():
+    rng = np.random.default_rng(4)
+    L, Hq, Hk, d, F, T = 1, 2, 1, 8, 3, 10
+    keys = [W.bf16_bits(rng.standard_normal((Hk, F * T, d)).astype(np.float32))]
+    q = [W.bf16_bits(rng.standard_normal((Hq, 1, d)).astype(np.float32))]
+    raw, comp = O.Index(L, Hq, Hk, d), O.Index(L, Hq, Hk, d)
+    raw.append(keys, F, T)
+    comp.append(keys, F, T, (3, 4))
+    np.testing.assert_array_equal(O.pooled_scores(raw, q), O.pooled_scores(comp, q))
