@@ -103,7 +103,9 @@ typedef struct {
 /* Device bytes an index with this shape needs (0 if `desc` is invalid).
  * Layout (each part 256-byte aligned): keys bf16 [L_s][H_kv][max_rows][d];
  * member counts int32 [L_s][H_kv][max_rows]; descriptors fp32
- * [max_frames][H_kv*d]; frame row offsets int32 [max_frames+1]. */
+ * [max_frames][H_kv*d]; pooled keys fp32 [max_frames][L_s][H_kv][d] (each
+ * frame's mean raw key per layer and KV head); frame row offsets int32
+ * [max_frames+1]. */
 size_t ss_index_required_bytes(const ss_index_desc* desc);
 
 /* Create an empty index over a caller-owned device arena of at least
@@ -183,6 +185,22 @@ ss_status ss_retrieve_debug(ss_index* const* idx, int32_t n_streams, const void*
                             const int32_t* n_q, const ss_retrieve_params* params, void* ws,
                             size_t ws_bytes, void* stream, int64_t* frame_ids, int32_t* votes,
                             float* mass, int32_t* n_out, const ss_debug_out* dbg);
+
+/* Pooled shallow Q-K ranking, the baseline ranker of the paper's evidence-
+ * ranker ablation: each candidate frame (all but the newest n_recent) is
+ * scored by the mean over shallow layers l and query heads h of
+ * qbar_{l,h} . Kbar_{l,h/G,t} / sqrt(d), where qbar is the mean query over the
+ * question's tokens and Kbar the frame's mean raw key of that layer and KV head
+ * (kept at append); for raw frames this is the mean of the frame's token
+ * scores.  The n_select best frames by (score desc, frame asc) are returned,
+ * with no diversity selection.  Arguments as in ss_retrieve; outputs (device,
+ * [n_streams][n_select]): frame_ids int64 (-1 padded), scores fp32 (0 in the
+ * padding), n_out int32 [n_streams].  n_select is 1..64. */
+size_t ss_pooled_workspace_bytes(ss_index* const* idx, int32_t n_streams, const int32_t* n_q,
+                                 int32_t n_select);
+ss_status ss_retrieve_pooled(ss_index* const* idx, int32_t n_streams, const void* const* queries,
+                             const int32_t* n_q, int32_t n_select, void* ws, size_t ws_bytes,
+                             void* stream, int64_t* frame_ids, float* scores, int32_t* n_out);
 
 /* Evidence assembly parameters (Eq. selected_evidence).
  *   n_recent   N_r, the newest frames that are always evidence (Eq.

@@ -70,6 +70,9 @@ _SIGS = {
     "ss_debug_scores": (C.c_int32, [_P, C.POINTER(_P), C.c_int32, C.c_int32, C.c_int32, C.c_int32,
                                     C.c_int64, C.c_int64, _P, _P, C.c_size_t, _P]),
     "ss_index_export": (C.c_int32, [_P, _P, _P, _P, C.POINTER(C.c_int64), _P]),
+    "ss_pooled_workspace_bytes": (C.c_size_t, [C.POINTER(_P), C.c_int32, C.POINTER(C.c_int32), C.c_int32]),
+    "ss_retrieve_pooled": (C.c_int32, [C.POINTER(_P), C.c_int32, C.POINTER(_P), C.POINTER(C.c_int32), C.c_int32,
+                                       _P, C.c_size_t, _P, _P, _P, _P]),
     "ss_evidence_max_units": (C.c_int32, [C.POINTER(EvidenceParams), C.c_int32]),
     "ss_assemble_evidence": (C.c_int32, [C.POINTER(_P), C.c_int32, _P, C.c_int32, C.POINTER(EvidenceParams), _P,
                                          _P, _P, C.c_int32]),

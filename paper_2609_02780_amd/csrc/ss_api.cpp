@@ -45,7 +45,7 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 inline bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 struct Layout {
-  size_t keys, counts, desc, off, total;
+  size_t keys, counts, desc, pooled, off, total;
 };
 
 // Check an index shape; fills `why` on failure.
@@ -91,6 +91,8 @@ Layout layout(const ss_index_desc& d) {
   off = align256(off + lg * (size_t)d.max_rows * 4);
   L.desc = off;
   off = align256(off + (size_t)d.max_frames * d.n_kv_heads * d.head_dim * 4);
+  L.pooled = off;
+  off = align256(off + (size_t)d.max_frames * lg * d.head_dim * 4);
   L.off = off;
   off = align256(off + ((size_t)d.max_frames + 1) * 4);
   L.total = off;
@@ -322,6 +324,52 @@ ss_status retrieve_common(ss_index* const* idx, int32_t n_streams, const void* c
   return SS_OK;
 }
 
+// Plan of one group of streams [s0, s0 + S) of a pooled-ranking batch.
+void build_pooled(ss::PooledPlan& p, ss_index* const* idx, int s0, int S, const void* const* queries,
+                  const int32_t* n_q, int n_select) {
+  std::memset(&p, 0, sizeof p);
+  const ss_index_desc& d = idx[0]->desc;
+  p.S = S; p.L = d.n_layers; p.Hq = d.n_q_heads; p.Hk = d.n_kv_heads; p.G = p.Hq / p.Hk;
+  p.D = d.head_dim; p.n_select = n_select;
+  for (int i = 0; i < S; ++i) {
+    const ss_index* x = idx[s0 + i];
+    int64_t rows, frames;
+    candidates(x, rows, frames);
+    p.F[i] = frames;
+    p.f_max = std::max<int64_t>(p.f_max, frames);
+    p.pooled[i] = x->dev.pooled;
+    p.nq[i] = n_q[s0 + i];
+    for (int l = 0; l < p.L; ++l)
+      p.q[i * p.L + l] = queries ? static_cast<const uint16_t*>(queries[(size_t)(s0 + i) * p.L + l]) : nullptr;
+  }
+}
+
+size_t pooled_ws(ss_index* const* idx, int32_t n_streams, const int32_t* n_q, int n_select) {
+  size_t need = 0;
+  for (int s0 = 0; s0 < n_streams; s0 += ss::kMaxStreams) {
+    ss::PooledPlan p;
+    build_pooled(p, idx, s0, std::min(ss::kMaxStreams, n_streams - s0), nullptr, n_q, n_select);
+    need = std::max(need, ss::pooled_workspace(p, nullptr));
+  }
+  return need;
+}
+
+ss_status check_pooled(ss_index* const* idx, int32_t n_streams, const int32_t* n_q, int32_t n_select) {
+  if (!idx) return fail(SS_ERR_INVALID_ARGUMENT, "idx is NULL");
+  if (n_streams < 1) return fail(SS_ERR_INVALID_ARGUMENT, "n_streams must be >= 1");
+  if (!n_q) return fail(SS_ERR_INVALID_ARGUMENT, "n_q is NULL");
+  for (int s = 0; s < n_streams; ++s) {
+    if (!idx[s]) return fail(SS_ERR_INVALID_ARGUMENT, "idx[%d] is NULL", s);
+    if (!same_shape(idx[s]->desc, idx[0]->desc))
+      return fail(SS_ERR_INVALID_ARGUMENT, "idx[%d] shape differs from idx[0]", s);
+    if (n_q[s] < 1 || n_q[s] > 4096)
+      return fail(SS_ERR_INVALID_ARGUMENT, "n_q[%d] = %d outside 1..4096", s, n_q[s]);
+  }
+  if (n_select < 1 || n_select > ss::kMaxSelect)
+    return fail(SS_ERR_UNSUPPORTED, "n_select %d outside 1..%d", n_select, ss::kMaxSelect);
+  return SS_OK;
+}
+
 // Candidate units of one stream's evidence, or -1 for invalid parameters.
 int64_t evidence_units_max(const ss_evidence_params* p, int32_t n_select) {
   if (!p || p->n_recent < 0 || p->n_before < 0 || p->n_after < 0) return -1;
@@ -337,6 +385,41 @@ int64_t evidence_units_max(const ss_evidence_params* p, int32_t n_select) {
 }  // namespace
 
 extern "C" {
+
+size_t ss_pooled_workspace_bytes(ss_index* const* idx, int32_t n_streams, const int32_t* n_q,
+                                  int32_t n_select) {
+  if (check_pooled(idx, n_streams, n_q, n_select) != SS_OK) return 0;
+  return pooled_ws(idx, n_streams, n_q, n_select);
+}
+
+ss_status ss_retrieve_pooled(ss_index* const* idx, int32_t n_streams, const void* const* queries,
+                             const int32_t* n_q, int32_t n_select, void* ws, size_t ws_bytes,
+                             void* stream, int64_t* frame_ids, float* scores, int32_t* n_out) {
+  ss_status st = check_pooled(idx, n_streams, n_q, n_select);
+  if (st) return st;
+  if (!queries) return fail(SS_ERR_INVALID_ARGUMENT, "queries is NULL");
+  const int L = idx[0]->desc.n_layers;
+  for (int i = 0; i < n_streams * L; ++i) {
+    if (!queries[i]) return fail(SS_ERR_INVALID_ARGUMENT, "queries[%d] is NULL", i);
+    if (!aligned(queries[i], 16)) return fail(SS_ERR_INVALID_ARGUMENT, "queries[%d] not 16-byte aligned", i);
+  }
+  if (!frame_ids || !scores || !n_out) return fail(SS_ERR_INVALID_ARGUMENT, "an output pointer is NULL");
+  if (!ws || !aligned(ws, 256)) return fail(SS_ERR_WORKSPACE, "workspace NULL or not 256-byte aligned");
+  const size_t need = pooled_ws(idx, n_streams, n_q, n_select);
+  if (ws_bytes < need) return fail(SS_ERR_WORKSPACE, "workspace %zu bytes, %zu needed", ws_bytes, need);
+  const hipStream_t hs = static_cast<hipStream_t>(stream);
+  for (int s0 = 0; s0 < n_streams; s0 += ss::kMaxStreams) {
+    ss::PooledPlan p;
+    build_pooled(p, idx, s0, std::min(ss::kMaxStreams, n_streams - s0), queries, n_q, n_select);
+    ss::pooled_workspace(p, ws);
+    p.out_ids = frame_ids + (size_t)s0 * n_select;
+    p.out_scores = scores + (size_t)s0 * n_select;
+    p.out_n = n_out + s0;
+    const hipError_t e = ss::launch_pooled(p, hs);
+    if (e != hipSuccess) return fail(SS_ERR_DEVICE, "pooled ranking launch failed: %s", hipGetErrorString(e));
+  }
+  return SS_OK;
+}
 
 int32_t ss_evidence_max_units(const ss_evidence_params* params, int32_t n_select) {
   const int64_t n = evidence_units_max(params, n_select);
@@ -405,6 +488,7 @@ ss_status ss_index_create(const ss_index_desc* desc, void* dev_arena, size_t are
   x->dev.keys = reinterpret_cast<uint16_t*>(b + L.keys);
   x->dev.counts = reinterpret_cast<int32_t*>(b + L.counts);
   x->dev.desc = reinterpret_cast<float*>(b + L.desc);
+  x->dev.pooled = reinterpret_cast<float*>(b + L.pooled);
   x->dev.frame_off = reinterpret_cast<int32_t*>(b + L.off);
   x->n_frames = 0;
   x->n_rows = 0;

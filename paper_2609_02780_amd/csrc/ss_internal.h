@@ -30,6 +30,7 @@ struct IndexDev {
   uint16_t* keys;       // [L][H_kv][max_rows][d] bf16
   int32_t* counts;      // [L][H_kv][max_rows]
   float* desc;          // [max_frames][H_kv*d]
+  float* pooled;        // [max_frames][L][H_kv][d] mean raw key per (frame, layer, KV head)
   int32_t* frame_off;   // [max_frames+1]
 };
 
@@ -133,6 +134,23 @@ struct RetrievePlan {
 size_t carve_workspace(RetrievePlan& p, void* ws);
 
 hipError_t launch_retrieve(RetrievePlan& p, hipStream_t st);
+
+// Pooled shallow Q-K ranking of up to kMaxStreams streams.
+struct PooledPlan {
+  int S, L, Hq, Hk, G, D, n_select;
+  int64_t F[kMaxStreams];               // candidate frames per stream
+  const float* pooled[kMaxStreams];     // per stream [max_frames][L][H_kv][d]
+  const uint16_t* q[kMaxStreams * kMaxLayers];  // [s * L + l] -> bf16 [H_q][n_q][d]
+  int32_t nq[kMaxStreams];
+  int64_t f_max;
+  float* w;        // workspace [S][L][H_kv][d]: pooled query weights
+  float* scores;   // workspace [S][f_max]
+  int64_t* out_ids;
+  float* out_scores;
+  int32_t* out_n;
+};
+size_t pooled_workspace(PooledPlan& p, void* ws);   // fills p.w / p.scores when ws != null
+hipError_t launch_pooled(const PooledPlan& p, hipStream_t st);
 
 // Evidence assembly of up to kMaxStreams streams, one block each.
 constexpr int kMaxEvidence = 4096;   // candidate units per stream (sorted in LDS)

@@ -26,7 +26,7 @@
 //   k_gram      fp32 Gram matrix of the pool descriptors.
 //   k_maxmin    greedy max-min diversity over the Gram matrix.
 //
-// Append: k_desc (Eq. memory_key descriptor), k_copy (raw rows) or k_kmeans
+// Append: k_unit_means (pooled keys and the Eq. memory_key descriptor), k_copy (raw rows) or k_kmeans
 // (per-frame k-means compression).
 //
 // Ordering conventions: a score s maps to an order-preserving uint32 u(s); the
@@ -1560,13 +1560,17 @@ __global__ __launch_bounds__(1024) void k_maxmin(MaxminArgs a) {
 // ---------------------------------------------------------------------------
 // Descriptor (Eq. memory_key): fp32 mean over the frame's raw last-layer tokens,
 // heads flattened head-major, L2-normalised.  Also writes the frame offsets.
+// Per (frame, layer): the mean raw key of every KV head (fp32 sums in token
+// order) becomes the frame's pooled key of that layer; the last shallow
+// layer's means, flattened head-major and L2-normalised, are the unit
+// descriptor (Eq. memory_key).  Grid: (frames, layers).
 template <int D>
-__global__ __launch_bounds__(256) void k_desc(AppendArgs a) {
+__global__ __launch_bounds__(256) void k_unit_means(AppendArgs a) {
   __shared__ float red[8];
-  const int f = blockIdx.x;
+  const int f = blockIdx.x, l = blockIdx.y;
   const int T = a.n_tokens, dim = a.Hk * D;
   const int64_t nT = (int64_t)a.n_frames * T;
-  const uint16_t* src = a.src[a.L - 1];
+  const uint16_t* src = a.src[l];
   float vals[4];
   float ss = 0.f;
   for (int k = 0; k < 4; ++k) {
@@ -1581,6 +1585,12 @@ __global__ __launch_bounds__(256) void k_desc(AppendArgs a) {
       ss = fmaf(vals[k], vals[k], ss);
     }
   }
+  float* pooled = a.dst.pooled + ((a.frame0 + f) * a.L + l) * (int64_t)dim;
+  for (int k = 0; k < 4; ++k) {
+    const int e = threadIdx.x + k * 256;
+    if (e < dim) pooled[e] = vals[k];
+  }
+  if (l != a.L - 1) return;  // the same for the whole block
   // deterministic block sum of squares
   for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
@@ -1745,6 +1755,116 @@ __global__ __launch_bounds__(256) void k_kmeans(AppendArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Pooled shallow Q-K ranking: keys pooled per unit at append (k_unit_means),
+// scored against the question's pooled query weights, top-K units.
+// ---------------------------------------------------------------------------
+struct PoolQArgs {
+  int Hq, Hk, G, L, first;
+  const uint16_t* q[128];   // (stream, layer) pairs first .. first + 127
+  int nq[kMaxStreams];
+  float* w;                 // [pairs][H_kv][D]
+};
+
+// w[pair][g][e] = (sum over the group's heads and the question's tokens of q) /
+// (n_q L H_q sqrt(D)): the weights whose dot product with a unit's pooled keys
+// is its pooled score.  Grid: pairs x H_kv, D threads.
+template <int D>
+__global__ __launch_bounds__(D) void k_pool_query(PoolQArgs a) {
+  const int pl = blockIdx.x / a.Hk, g = blockIdx.x % a.Hk;
+  const int pair = a.first + pl, s = pair / a.L;
+  const int nq = a.nq[s], e = threadIdx.x;
+  const uint16_t* q = a.q[pl];
+  float acc = 0.f;
+  for (int h = g * a.G; h < (g + 1) * a.G; ++h)
+    for (int j = 0; j < nq; ++j) acc += __uint_as_float((uint32_t)q[((size_t)h * nq + j) * D + e] << 16);
+  const float scale = 1.0f / ((float)nq * (float)a.L * (float)a.Hq * sqrtf((float)D));
+  a.w[((size_t)pair * a.Hk + g) * D + e] = acc * scale;
+}
+
+struct PoolScoreArgs {
+  int n4;                           // float4 per unit: L H_kv D / 4
+  int64_t F[kMaxStreams];
+  const float4* pooled[kMaxStreams];
+  const float4* w;                  // [S][n4]
+  float* scores;                    // [S][f_max]
+  int64_t f_max;
+};
+
+// One wave per unit: a fixed strided split over the lanes and a fixed
+// butterfly, so a unit's score does not depend on the launch.
+__global__ __launch_bounds__(256) void k_pool_score(PoolScoreArgs a) {
+  const int s = blockIdx.y, lane = threadIdx.x & (kWave - 1);
+  const int64_t f = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (f >= a.F[s]) return;   // whole waves leave together
+  const float4* k = a.pooled[s] + f * a.n4;
+  const float4* w = a.w + (size_t)s * a.n4;
+  float acc = 0.f;
+  for (int i = lane; i < a.n4; i += kWave) {
+    const float4 x = k[i], y = w[i];
+    acc = fmaf(x.x, y.x, acc);
+    acc = fmaf(x.y, y.y, acc);
+    acc = fmaf(x.z, y.z, acc);
+    acc = fmaf(x.w, y.w, acc);
+  }
+  for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
+  if (lane == 0) a.scores[(size_t)s * a.f_max + f] = acc;
+}
+
+struct PoolSelectArgs {
+  int n_select;
+  int64_t F[kMaxStreams];
+  const float* scores;              // [S][f_max]
+  int64_t f_max;
+  int64_t* out_ids;                 // [S][n_select]
+  float* out_scores;
+  int32_t* out_n;
+};
+
+// Top n_select units of a stream by (score desc, unit asc): a radix cut over
+// the composite keys, then ranks by counting.
+__global__ __launch_bounds__(1024) void k_pool_select(PoolSelectArgs a) {
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t res[4];
+  __shared__ uint64_t sel[kMaxSelect];
+  __shared__ uint32_t nsel;
+  const int s = blockIdx.x;
+  const int64_t F = a.F[s];
+  const int K = (int)min<int64_t>(a.n_select, F);
+  const float* sc = a.scores + (size_t)s * a.f_max;
+  auto key = [&](int i) -> uint64_t { return mk_key(ord_u32(sc[i] + 0.0f), (uint32_t)i); };
+  if (threadIdx.x == 0) nsel = 0;
+  uint64_t cut = 0;
+  if (K > 0 && K < F) cut = radix_select_u64(key, (int)F, (uint32_t)K, hist, res);
+  __syncthreads();
+  for (int i = threadIdx.x; i < F && K > 0; i += blockDim.x) {
+    const uint64_t k = key(i);
+    if (k >= cut) {
+      const uint32_t slot = atomicAdd(&nsel, 1u);
+      if (slot < (uint32_t)kMaxSelect) sel[slot] = k;
+    }
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < a.n_select; i += blockDim.x) {
+    int64_t id = -1;
+    float v = 0.f;
+    if (i < K) {
+      // the i-th best: the key with exactly i larger keys
+      for (int j = 0; j < K; ++j) {
+        int rank = 0;
+        for (int m = 0; m < K; ++m) rank += sel[m] > sel[j];
+        if (rank == i) {
+          id = key_row(sel[j]);
+          v = key_score(sel[j]);
+        }
+      }
+    }
+    a.out_ids[(size_t)s * a.n_select + i] = id;
+    a.out_scores[(size_t)s * a.n_select + i] = v;
+  }
+  if (threadIdx.x == 0) a.out_n[s] = K;
+}
+
+// ---------------------------------------------------------------------------
 // k_evidence: Eq. selected_evidence plus deduplication and temporal order.
 // One block per stream: the recent window and every selected frame's
 // neighbourhood are laid out as candidate slots (missing ones as a sentinel),
@@ -1792,7 +1912,7 @@ inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
 template <int D>
 hipError_t append_impl(const AppendArgs& a, bool compress, hipStream_t st) {
-  hipLaunchKernelGGL(k_desc<D>, dim3(a.n_frames), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(k_unit_means<D>, dim3(a.n_frames, a.L), dim3(256), 0, st, a);
   if (compress) {
     hipLaunchKernelGGL(k_kmeans<D>, dim3(a.n_frames * a.L * a.Hk), dim3(256), 0, st, a);
   } else {
@@ -1976,6 +2096,53 @@ hipError_t debug_scores_impl(RetrievePlan& p, int layer, int q_head, int64_t row
 }
 
 }  // namespace
+
+size_t pooled_workspace(PooledPlan& p, void* ws) {
+  size_t off = 0;
+  auto take = [&](size_t bytes) -> void* {
+    off = (off + 255) & ~(size_t)255;
+    void* r = ws ? static_cast<char*>(ws) + off : nullptr;
+    off += bytes;
+    return r;
+  };
+  p.w = static_cast<float*>(take((size_t)p.S * p.L * p.Hk * p.D * 4));
+  p.scores = static_cast<float*>(take((size_t)p.S * std::max<int64_t>(p.f_max, 1) * 4));
+  return (off + 255) & ~(size_t)255;
+}
+
+template <int D>
+hipError_t pooled_impl(const PooledPlan& p, hipStream_t st) {
+  const int pairs = p.S * p.L;
+  for (int first = 0; first < pairs; first += 128) {
+    PoolQArgs a{};
+    a.Hq = p.Hq; a.Hk = p.Hk; a.G = p.G; a.L = p.L; a.first = first; a.w = p.w;
+    const int cnt = std::min(128, pairs - first);
+    for (int i = 0; i < cnt; ++i) a.q[i] = p.q[first + i];
+    for (int s = 0; s < p.S; ++s) a.nq[s] = p.nq[s];
+    hipLaunchKernelGGL(k_pool_query<D>, dim3(cnt * p.Hk), dim3(D), 0, st, a);
+  }
+  PoolScoreArgs sa{};
+  sa.n4 = p.L * p.Hk * D / 4;
+  sa.w = reinterpret_cast<const float4*>(p.w);
+  sa.scores = p.scores;
+  sa.f_max = std::max<int64_t>(p.f_max, 1);
+  PoolSelectArgs ka{};
+  ka.n_select = p.n_select; ka.scores = p.scores; ka.f_max = sa.f_max;
+  ka.out_ids = p.out_ids; ka.out_scores = p.out_scores; ka.out_n = p.out_n;
+  for (int s = 0; s < p.S; ++s) {
+    sa.F[s] = p.F[s];
+    sa.pooled[s] = reinterpret_cast<const float4*>(p.pooled[s]);
+    ka.F[s] = p.F[s];
+  }
+  if (p.f_max > 0)
+    hipLaunchKernelGGL(k_pool_score, dim3((unsigned)cdiv(p.f_max, 4), p.S), dim3(256), 0, st, sa);
+  hipLaunchKernelGGL(k_pool_select, dim3(p.S), dim3(1024), 0, st, ka);
+  return hipGetLastError();
+}
+
+hipError_t launch_pooled(const PooledPlan& p, hipStream_t st) {
+  return p.D == 64 ? pooled_impl<64>(p, st) : pooled_impl<128>(p, st);
+}
 
 hipError_t launch_evidence(const EvidenceArgs& a, hipStream_t st) {
   hipLaunchKernelGGL(k_evidence, dim3(a.S), dim3(256), 0, st, a);

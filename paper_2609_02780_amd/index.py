@@ -206,6 +206,48 @@ class Retriever:
         return out
 
 
+class PooledRanker:
+    """Pooled shallow Q-K ranking over a batch of indices with identical shapes
+    (unit-mean keys against the question's mean query; no diversity)."""
+
+    def __init__(self, indices, n_select: int):
+        self.indices = list(indices)
+        self.n_select = n_select
+        self._ws = None
+        dev = self.indices[0].arena.device
+        S = len(self.indices)
+        self.frame_ids = torch.empty((S, n_select), dtype=torch.int64, device=dev)
+        self.scores = torch.empty((S, n_select), dtype=torch.float32, device=dev)
+        self.n_out = torch.empty(S, dtype=torch.int32, device=dev)
+        self._handles = L.ptr_array([x.handle.value for x in self.indices])
+
+    def __call__(self, queries, stream=None):
+        """``queries[s][l]``: ``[H_q][n_q][d]`` bfloat16.  Returns device tensors
+        ``(frame_ids, scores, n_out)`` (views of reused buffers)."""
+        S = len(self.indices)
+        if len(queries) != S:
+            raise ValueError(f"expected queries for {S} streams, got {len(queries)}")
+        ptrs, n_q = [], []
+        for s, (x, qs) in enumerate(zip(self.indices, queries)):
+            if len(qs) != x.n_layers:
+                raise ValueError(f"stream {s}: expected {x.n_layers} query tensors")
+            nq = qs[0].shape[1]
+            n_q.append(nq)
+            for l, q in enumerate(qs):
+                ptrs.append(_check_bf16(q, (x.n_q_heads, nq, x.head_dim), f"queries[{s}][{l}]"))
+        nqa = (C.c_int32 * S)(*n_q)
+        need = L.lib().ss_pooled_workspace_bytes(self._handles, S, nqa, self.n_select)
+        if need == 0:
+            raise L.SSError(L.SS_ERR_INVALID_ARGUMENT, L.lib().ss_last_error().decode())
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = torch.empty(need, dtype=torch.uint8, device=self.frame_ids.device)
+        L.check(L.lib().ss_retrieve_pooled(self._handles, S, L.ptr_array(ptrs), nqa, self.n_select,
+                                           self._ws.data_ptr(), self._ws.numel(), _stream_handle(stream),
+                                           self.frame_ids.data_ptr(), self.scores.data_ptr(),
+                                           self.n_out.data_ptr()))
+        return self.frame_ids, self.scores, self.n_out
+
+
 def assemble_evidence(indices, frame_ids, n_recent: int, n_before: int = 1, n_after: int = 0,
                       retrieved: bool = True, stream=None):
     """The frames handed to answering for each stream (Eq. selected_evidence,

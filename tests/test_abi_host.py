@@ -205,3 +205,24 @@ def test_evidence_validation(L):
     big = P(4000, 10, 10, 1)
     assert lib.ss_assemble_evidence(idx, 1, F, 64, C.byref(big), None, F, F, 4096) == L.SS_ERR_UNSUPPORTED
     assert lib.ss_index_destroy(h) == 0
+
+
+def test_pooled_validation(L):
+    lib = L.lib()
+    h = create(L, max_frames=4, max_rows=4 * 196)
+    idx = (C.c_void_p * 1)(h.value)
+    nq = (C.c_int32 * 1)(8)
+    assert lib.ss_pooled_workspace_bytes(idx, 1, nq, 8) > 0
+    assert lib.ss_pooled_workspace_bytes(idx, 1, nq, 0) == 0
+    assert lib.ss_pooled_workspace_bytes(idx, 1, nq, 65) == 0
+    bad = (C.c_int32 * 1)(0)
+    assert lib.ss_pooled_workspace_bytes(idx, 1, bad, 8) == 0
+    F = FAKE
+    qs = (C.c_void_p * 4)(F, F, F, F)
+    ws = lib.ss_pooled_workspace_bytes(idx, 1, nq, 8)
+    assert lib.ss_retrieve_pooled(idx, 1, qs, nq, 8, F, ws - 1, None, F, F, F) == L.SS_ERR_WORKSPACE
+    assert lib.ss_retrieve_pooled(idx, 1, qs, nq, 8, F, ws, None, None, F, F) == L.SS_ERR_INVALID_ARGUMENT
+    qs_bad = (C.c_void_p * 4)(F, F + 2, F, F)
+    assert lib.ss_retrieve_pooled(idx, 1, qs_bad, nq, 8, F, ws, None, F, F, F) == L.SS_ERR_INVALID_ARGUMENT
+    assert b"queries[1]" in lib.ss_last_error()
+    assert lib.ss_index_destroy(h) == 0
