@@ -140,6 +140,93 @@ def time_evidence(torch, P, idxs, frame_ids, calls=20):
             "units_stream0": int(n_units[0].item())}
 
 
+def sweep(torch, P, cfg, points=(64, 128, 256, 512, 1024, 2048, 3600), calls=20):
+    """History-length sweep on one growing stream of the workload's shape: at
+    each length the token-vote retrieval (with its streaming kernel), the
+    pooled Q-K ranker and the evidence assembly are timed with HIP events."""
+    spec = W.stream_specs(cfg)[0]
+    q = W.make_queries(cfg, 0, 0)
+    T = cfg.tokens_per_frame
+    F_max = max(points)
+    spec = W.StreamSpec(0, F_max, cfg.n_planted, None, W.planted_frames(F_max, cfg.n_planted))
+    idx = P.ShallowIndex(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, F_max, F_max * T)
+    qd = [[dev_bf16(torch, x) for x in q]]
+    r = P.Retriever([idx], cfg.top_k, cfg.n_select, cfg.pool_mult)
+    pr = P.PooledRanker([idx], cfg.n_select)
+
+    def timed(fn, with_kernel=False):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(calls)]
+        for e4 in ev:            # torch times only events it has recorded once itself
+            for e in e4:
+                e.record()
+        torch.cuda.synchronize()
+        for e4 in ev:
+            if with_kernel:
+                P.set_profile_events(e4[2], e4[3])
+            e4[0].record()
+            fn()
+            e4[1].record()
+        torch.cuda.synchronize()
+        P.set_profile_events(None, None)
+        lat = float(np.median([e[0].elapsed_time(e[1]) for e in ev]))
+        ker = float(np.median([e[2].elapsed_time(e[3]) for e in ev])) if with_kernel else None
+        return lat, ker
+
+    def graph_ms(fn, outs):
+        """GPU time of one call replayed from a HIP graph (no host launch
+        overhead); the replays' outputs must equal the eager call's."""
+        fn()
+        torch.cuda.synchronize()
+        want = [o.clone() for o in outs]
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fn()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            fn()
+        for _ in range(3):
+            g.replay()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(calls):
+            g.replay()
+        b.record()
+        b.synchronize()
+        for o, w in zip(outs, want):
+            if not torch.equal(o, w):
+                raise RuntimeError("graph replay differs from the eager call")
+        return a.elapsed_time(b) / calls
+
+    rows = []
+    have = 0
+    for F in points:
+        while have < F:
+            f1 = min(F, have + 600)
+            kb = W.frame_block_keys(cfg, spec, q, have, f1)
+            idx.append([dev_bf16(torch, k) for k in kb], f1 - have, T)
+            have = f1
+        torch.cuda.synchronize()
+        lat, ker = timed(lambda: r(qd), with_kernel=True)
+        plat, _ = timed(lambda: pr(qd))
+        elat, _ = timed(lambda: P.assemble_evidence([idx], r.frame_ids, 6, 1, 0, True))
+        glat = graph_ms(lambda: r(qd), [r.frame_ids, r.votes, r.n_out])
+        gplat = graph_ms(lambda: pr(qd), [pr.frame_ids, pr.n_out])
+        key_bytes = idx.n_rows * cfg.n_layers * cfg.n_kv_heads * cfg.head_dim * 2
+        rows.append({"frames": F, "key_bytes": key_bytes, "retrieve_p50_ms": lat, "retrieve_graph_ms": glat,
+                     "stream_kernel_ms": ker, "stream_kernel_gbs": key_bytes / (ker / 1e3) / 1e9,
+                     "pooled_p50_ms": plat, "pooled_graph_ms": gplat, "evidence_p50_ms": elat})
+        log(f"{F} frames: retrieve {lat:.3f} ms (graph {glat:.3f}, kernel {ker:.3f}), "
+            f"pooled {plat:.3f} ms (graph {gplat:.3f}), evidence {elat:.3f} ms")
+    return rows
+
+
 def cpu_model() -> str:
     try:
         for line in open("/proc/cpuinfo"):
@@ -190,6 +277,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="C4", choices=sorted(W.CONFIGS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sweep", action="store_true",
+                    help="history-length sweep (64..3600 frames of the workload's shape) instead of the benchmark")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (calibrates the HBM byte counters)")
     args = ap.parse_args()
@@ -217,6 +306,11 @@ def main():
         build_library()
     torch.cuda.set_device(0)
     cfg = W.CONFIGS[args.config]
+    if args.sweep:
+        rows = sweep(torch, P, cfg)
+        print(json.dumps({"sweep": "history length", "workload": cfg.name, "top_k": cfg.top_k,
+                          "n_select": cfg.n_select, "data": "synthetic", "points": rows}), flush=True)
+        return
     specs, idxs, queries, host0 = build_streams(torch, P, cfg)
     r = P.Retriever(idxs, cfg.top_k, cfg.n_select, cfg.pool_mult)
     for _ in range(args.warmup):

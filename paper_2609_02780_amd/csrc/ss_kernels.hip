@@ -1767,18 +1767,35 @@ struct PoolQArgs {
 
 // w[pair][g][e] = (sum over the group's heads and the question's tokens of q) /
 // (n_q L H_q sqrt(D)): the weights whose dot product with a unit's pooled keys
-// is its pooled score.  Grid: pairs x H_kv, D threads.
+// is its pooled score.  Grid: pairs x H_kv; 8 token groups of D threads, each
+// summing every 8th (head, token) row with four loads in flight; the groups'
+// partial sums are added in a fixed order.
+constexpr int kPoolQGroups = 8;
 template <int D>
-__global__ __launch_bounds__(D) void k_pool_query(PoolQArgs a) {
+__global__ __launch_bounds__(kPoolQGroups * D) void k_pool_query(PoolQArgs a) {
+  __shared__ float part[kPoolQGroups][D];
   const int pl = blockIdx.x / a.Hk, g = blockIdx.x % a.Hk;
   const int pair = a.first + pl, s = pair / a.L;
-  const int nq = a.nq[s], e = threadIdx.x;
-  const uint16_t* q = a.q[pl];
+  const int nq = a.nq[s], tg = threadIdx.x / D, e = threadIdx.x % D;
+  const uint16_t* q = a.q[pl] + (size_t)g * a.G * nq * D + e;   // rows of the group's heads
+  const int rows = a.G * nq;
   float acc = 0.f;
-  for (int h = g * a.G; h < (g + 1) * a.G; ++h)
-    for (int j = 0; j < nq; ++j) acc += __uint_as_float((uint32_t)q[((size_t)h * nq + j) * D + e] << 16);
+  int r = tg;
+  for (; r + 3 * kPoolQGroups < rows; r += 4 * kPoolQGroups) {
+    uint16_t v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = q[(size_t)(r + u * kPoolQGroups) * D];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acc += __uint_as_float((uint32_t)v[u] << 16);
+  }
+  for (; r < rows; r += kPoolQGroups) acc += __uint_as_float((uint32_t)q[(size_t)r * D] << 16);
+  part[tg][e] = acc;
+  __syncthreads();
+  if (tg != 0) return;
+  float x = part[0][e];
+  for (int k = 1; k < kPoolQGroups; ++k) x += part[k][e];
   const float scale = 1.0f / ((float)nq * (float)a.L * (float)a.Hq * sqrtf((float)D));
-  a.w[((size_t)pair * a.Hk + g) * D + e] = acc * scale;
+  a.w[((size_t)pair * a.Hk + g) * D + e] = x * scale;
 }
 
 struct PoolScoreArgs {
@@ -1821,7 +1838,9 @@ struct PoolSelectArgs {
 };
 
 // Top n_select units of a stream by (score desc, unit asc): a radix cut over
-// the composite keys, then ranks by counting.
+// the composite keys (scores staged in LDS when they fit), then ranks by
+// counting.
+constexpr int kPoolLds = 8192;
 __global__ __launch_bounds__(1024) void k_pool_select(PoolSelectArgs a) {
   __shared__ uint32_t hist[256];
   __shared__ uint32_t res[4];
@@ -1830,9 +1849,15 @@ __global__ __launch_bounds__(1024) void k_pool_select(PoolSelectArgs a) {
   const int s = blockIdx.x;
   const int64_t F = a.F[s];
   const int K = (int)min<int64_t>(a.n_select, F);
-  const float* sc = a.scores + (size_t)s * a.f_max;
+  __shared__ float lsc[kPoolLds];
+  const float* gsc = a.scores + (size_t)s * a.f_max;
+  const bool in_lds = F <= kPoolLds;
+  if (in_lds)
+    for (int i = threadIdx.x; i < F; i += blockDim.x) lsc[i] = gsc[i];
+  const float* sc = in_lds ? lsc : gsc;
   auto key = [&](int i) -> uint64_t { return mk_key(ord_u32(sc[i] + 0.0f), (uint32_t)i); };
   if (threadIdx.x == 0) nsel = 0;
+  __syncthreads();
   uint64_t cut = 0;
   if (K > 0 && K < F) cut = radix_select_u64(key, (int)F, (uint32_t)K, hist, res);
   __syncthreads();
@@ -1844,22 +1869,19 @@ __global__ __launch_bounds__(1024) void k_pool_select(PoolSelectArgs a) {
     }
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < a.n_select; i += blockDim.x) {
-    int64_t id = -1;
-    float v = 0.f;
-    if (i < K) {
-      // the i-th best: the key with exactly i larger keys
-      for (int j = 0; j < K; ++j) {
-        int rank = 0;
-        for (int m = 0; m < K; ++m) rank += sel[m] > sel[j];
-        if (rank == i) {
-          id = key_row(sel[j]);
-          v = key_score(sel[j]);
-        }
-      }
-    }
-    a.out_ids[(size_t)s * a.n_select + i] = id;
-    a.out_scores[(size_t)s * a.n_select + i] = v;
+  // each selected key goes to its rank (the number of larger selected keys)
+  int64_t* ids = a.out_ids + (size_t)s * a.n_select;
+  float* scs = a.out_scores + (size_t)s * a.n_select;
+  if (threadIdx.x < K) {
+    const uint64_t k = sel[threadIdx.x];
+    int rank = 0;
+    for (int m = 0; m < K; ++m) rank += sel[m] > k;
+    ids[rank] = key_row(k);
+    scs[rank] = key_score(k);
+  }
+  for (int i = K + threadIdx.x; i < a.n_select; i += blockDim.x) {
+    ids[i] = -1;
+    scs[i] = 0.f;
   }
   if (threadIdx.x == 0) a.out_n[s] = K;
 }
@@ -2119,7 +2141,7 @@ hipError_t pooled_impl(const PooledPlan& p, hipStream_t st) {
     const int cnt = std::min(128, pairs - first);
     for (int i = 0; i < cnt; ++i) a.q[i] = p.q[first + i];
     for (int s = 0; s < p.S; ++s) a.nq[s] = p.nq[s];
-    hipLaunchKernelGGL(k_pool_query<D>, dim3(cnt * p.Hk), dim3(D), 0, st, a);
+    hipLaunchKernelGGL(k_pool_query<D>, dim3(cnt * p.Hk), dim3(kPoolQGroups * D), 0, st, a);
   }
   PoolScoreArgs sa{};
   sa.n4 = p.L * p.Hk * D / 4;
