@@ -260,7 +260,7 @@ def cpu_baseline(cfg, host0):
                   cfg.tokens_per_frame, comp)
         what = f"the first {nf} frames"
     t0 = time.perf_counter()
-    O.retrieve(oi, q, cfg.top_k, cfg.n_select, cfg.pool_mult)
+    O.retrieve(oi, q, cfg.top_k, cfg.n_select, cfg.pool_mult, cfg.head_mode)
     dt = time.perf_counter() - t0
     keys = oi.n_rows * cfg.n_layers * cfg.n_kv_heads
     return {"value": keys / dt, "unit": "keys/s", "cores": int(cores), "kind": "oracle",
@@ -312,7 +312,7 @@ def main():
                           "n_select": cfg.n_select, "data": "synthetic", "points": rows}), flush=True)
         return
     specs, idxs, queries, host0 = build_streams(torch, P, cfg)
-    r = P.Retriever(idxs, cfg.top_k, cfg.n_select, cfg.pool_mult)
+    r = P.Retriever(idxs, cfg.top_k, cfg.n_select, cfg.pool_mult, cfg.head_mode)
     for _ in range(args.warmup):
         r(queries)
     torch.cuda.synchronize()
@@ -357,7 +357,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{cfg.name}: {cfg.description}; {cfg.n_layers} shallow layers, "
                                f"{cfg.n_q_heads} query / {cfg.n_kv_heads} KV heads, d={cfg.head_dim}, "
-                               f"{cfg.n_q} query tokens, top-k {cfg.top_k}, {cfg.n_select} frames selected",
+                               f"{cfg.n_q} query tokens, top-k {cfg.top_k}, {cfg.n_select} frames selected"
+                               + (", head-averaged lists" if cfg.head_mode else ""),
                    "streams": len(idxs), "rows_per_layer_kv_head": rows, "key_vectors": key_vectors,
                    "key_bytes": key_bytes},
         "p10_latency_ms": float(np.percentile(lat, 10)),
@@ -365,7 +366,7 @@ def main():
         "p90_latency_ms": float(np.percentile(lat, 90)),
         "scores_per_s": value * cfg.group,
         "hbm_frac_end_to_end": key_bytes / (np.percentile(lat, 50) / 1e3) / 1e9 / HBM_PEAK_GBS,
-        "roofline": {"kernel": HOT_KERNEL, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+        "roofline": {"kernel": HOT_KERNEL if cfg.head_mode == 0 else "k_stream_hm<128>", "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "avg_kernel_ms": float(hot.mean()), "bytes_per_launch": key_bytes},
     }

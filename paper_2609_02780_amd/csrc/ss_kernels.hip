@@ -14,7 +14,8 @@
 //               group's query columns (hi and lo parts, fp32 accumulation), and
 //               rows at or above the cut-off are staged in LDS as 64-bit
 //               composite keys and flushed with one atomic per (wave, column).
-//               (Head-mode 1 streams in k_score_hm.)
+//               k_stream_hm is the same pass for head mode 1 (one list per
+//               layer, the scores averaged over all query heads).
 //   k_select    exact top-k per list from its candidates (radix selection over
 //               the value range, items in registers, ties by row); a list whose
 //               candidate count left [k, capacity] recomputes all of its scores
@@ -106,6 +107,46 @@ constexpr int kAuxNT = 2;  // buffer-load cache policy: nontemporal
 __device__ __forceinline__ u32x4 ld_nt(const uint16_t* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
 }
+
+// Head mode 1 (the layer's head-averaged score).  One B tile holds every KV
+// head g of the layer: the hi part of its pre-scaled group query sum in column
+// g and the lo part in column g + 8 (H_kv <= 8).  A tile of head g's keys is
+// scored against it with one chain of MFMAs over the k-steps; lane (c, kg)
+// keeps the result of head c mod 8, and a row's score is the sum over the 16
+// columns in a fixed butterfly, read from column 0.  The sample, stream and
+// exact-recompute paths all take these steps, so a row gets the same bits in
+// each.
+template <int KS>
+__device__ __forceinline__ void hm_load_b(const u32x4* qb_layer, int Hk, u32x4 (&b)[KS]) {
+  const int lane = threadIdx.x & 63, c = lane & 15, kg = lane >> 4, g = c & 7;
+#pragma unroll
+  for (int i = 0; i < KS; ++i)
+    b[i] = g < Hk ? qb_layer[(size_t)g * (2 * KS * 64) + ((c < 8 ? 0 : KS) + i) * 64 + 16 * kg]
+                  : u32x4{0, 0, 0, 0};
+}
+
+template <int KS>
+__device__ __forceinline__ void hm_accumulate(const u32x4 (&A)[KS], const u32x4 (&b)[KS], int g, f32x4& v) {
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int i = 0; i < KS; ++i) acc = mfma_bf16(A[i], b[i], acc);
+  if (((threadIdx.x & 15) & 7) == g) v = acc;
+}
+
+#define SS_DPP_F(x, ctrl) __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), ctrl, 0xF, 0xF, false))
+__device__ __forceinline__ f32x4 hm_finish(f32x4 v) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    float x = v[j];
+    x += SS_DPP_F(x, 0xB1);    // quad_perm 1,0,3,2
+    x += SS_DPP_F(x, 0x4E);    // quad_perm 2,3,0,1
+    x += SS_DPP_F(x, 0x124);   // row_ror 4
+    x += SS_DPP_F(x, 0x128);   // row_ror 8
+    v[j] = x;
+  }
+  return v;
+}
+#undef SS_DPP_F
 
 // Exclusive prefix count of `p` among the lanes of a wave.
 __device__ __forceinline__ int wave_excl_count(bool p) {
@@ -697,16 +738,14 @@ __global__ __launch_bounds__(256) void k_stream(ScoreArgs a) {
   }
 }
 
-// Head-mode 1: every KV head of the layer accumulates into column 0 (the
-// layer's head-averaged score); B tiles of all KV heads staged in LDS.
+// Head mode 1, sample and exact-recompute roles: one layer per item; every
+// tile's rows are read for each KV head in the MFMA A layout.
 template <int D, int KIND>
 __global__ __launch_bounds__(256) void k_score_hm(ScoreArgs a) {
+  static_assert(KIND != K_STREAM, "head-mode-1 streaming runs in k_stream_hm");
   constexpr int KS = D / 32;
-  __shared__ u32x4 sB[8 * 2 * KS * kWave];  // H_kv <= 8 in head-mode 1
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
-  __shared__ uint64_t stage[KIND == K_STREAM ? 4 * kStage : 1];  // column 0 only
-  uint64_t* st = stage + (KIND == K_STREAM ? wave * kStage : 0);
   for (int item = blockIdx.x; item < a.total_items; item += gridDim.x) {
     int s = 0;
     while (item >= a.item_base[s + 1]) ++s;
@@ -722,12 +761,8 @@ __global__ __launch_bounds__(256) void k_score_hm(ScoreArgs a) {
       wr = colv && (a.flag ? (a.flag[list] != 0) : (l == a.only_list));
       if (!__any(wr)) continue;
     }
-    const float tau_f = ord_f32((KIND == K_STREAM && colv) ? a.tau[list] : 0xFFFFFFFFu);
-    int lc = 0;
-    __syncthreads();
-    const u32x4* qb = a.qB + (size_t)(s * a.L + l) * a.Hk * (2 * KS * kWave);
-    for (int i = threadIdx.x; i < a.Hk * 2 * KS * kWave; i += blockDim.x) sB[i] = qb[i];
-    __syncthreads();
+    u32x4 b[KS];
+    hm_load_b<KS>(a.qB + (size_t)(s * a.L + l) * a.Hk * (2 * KS * kWave), a.Hk, b);
     const size_t gstride = (size_t)a.stride[s] * D;
     const uint16_t* base = a.keys[s] + (size_t)l * a.Hk * gstride + 8 * kg;
     const int ntiles = (u1 - u0 + kTile - 1) / kTile;
@@ -735,25 +770,86 @@ __global__ __launch_bounds__(256) void k_score_hm(ScoreArgs a) {
       const int u = u0 + t * kTile + rl;
       const bool ok = u < u1;
       const int64_t row = ok ? unit_row<KIND>(a, s, u) : 0;
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      f32x4 v = {0.f, 0.f, 0.f, 0.f};
       for (int g = 0; g < a.Hk; ++g) {
         const uint16_t* p = base + g * gstride + row * D;
         u32x4 A[KS];
 #pragma unroll
         for (int i = 0; i < KS; ++i) A[i] = ok ? ld_nt(p + 32 * i) : u32x4{0, 0, 0, 0};
-        const u32x4* b = sB + g * (2 * KS * kWave);
+        hm_accumulate<KS>(A, b, g, v);
+      }
+      emit<KIND>(a, s, list, colv, wr, u0 + t * kTile, u1, hm_finish(v), kg);
+    }
+  }
+}
+
+// Head mode 1, streaming role: like k_stream, with the (stream, layer) lists
+// as segments; a tile of 16 rows is read once per KV head (coalesced, through
+// the wave's LDS tile), one sub-tile ahead.
+template <int D>
+__global__ __launch_bounds__(256) void k_stream_hm(ScoreArgs a) {
+  constexpr int CPR = D / 8, TCH = 16 * CPR, NI = TCH / kWave, KS = D / 32;
+  __shared__ u32x4 tiles[4][TCH];
+  __shared__ uint64_t stage[4 * kStage];   // column 0 only
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
+  u32x4* lt_ = tiles[wave];
+  uint64_t* st = stage + wave * kStage;
+  const int64_t nw = (int64_t)gridDim.x * 4, gw = (int64_t)blockIdx.x * 4 + wave;
+  const int64_t total = a.tile_base[a.S];
+  const int64_t T1 = (gw + 1) * total / nw;
+  int64_t T = gw * total / nw;
+  while (T < T1) {
+    int s = 0;
+    while (T >= a.tile_base[s + 1]) ++s;
+    const int64_t rem = T - a.tile_base[s];
+    const int nt = a.ntile[s];
+    const int l = (int)(rem / nt);
+    const int t0 = (int)(rem - (int64_t)l * nt);
+    const int t1 = (int)min<int64_t>(nt, t0 + (T1 - T));
+    const int n = a.n[s], Hk = a.Hk;
+    const bool colv = col == 0;
+    const int list = s * a.NL + l;
+    const float tau_f = ord_f32(colv ? a.tau[list] : 0xFFFFFFFFu);
+    u32x4 b[KS];
+    hm_load_b<KS>(a.qB + (size_t)(s * a.L + l) * Hk * (2 * KS * kWave), Hk, b);
+    const uint16_t* lay = a.keys[s] + (size_t)l * Hk * a.stride[s] * D;
+    // sub-tile (t, g): rows 16 t .. 16 t + 15 of KV head g, zeros past the list
+    auto load = [&](int t, int g, u32x4 (&V)[NI]) {
+      const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<uint16_t*>(lay + (size_t)g * a.stride[s] * D), (short)0, n * D * 2, 0x00020000);
+      const uint32_t off = t < t1 ? (uint32_t)t * (TCH * 16) + lane * 16 : 0x80000000u;
+#pragma unroll
+      for (int i = 0; i < NI; ++i) V[i] = __builtin_amdgcn_raw_buffer_load_b128(r, off + i * kWave * 16, 0, kAuxNT);
+    };
+    u32x4 V[NI];
+    load(t0, 0, V);
+    int lc = 0;
+    for (int t = t0; t < t1; ++t) {
+      f32x4 v = {0.f, 0.f, 0.f, 0.f};
+      for (int g = 0; g < Hk; ++g) {
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+          const int q = i * kWave + lane, R = q >> 4, C = q & 15;
+          lt_[R * 16 + (C ^ (R & 15))] = V[i];
+        }
+        __builtin_amdgcn_wave_barrier();
+        if (g + 1 < Hk) load(t, g + 1, V);
+        else load(t + 1, 0, V);
+        u32x4 A[KS];
 #pragma unroll
         for (int i = 0; i < KS; ++i) {
-          acc = mfma_bf16(A[i], b[i * kWave + lane], acc);
-          acc = mfma_bf16(A[i], b[(KS + i) * kWave + lane], acc);
+          const int q = rl * CPR + 4 * i + kg, R = q >> 4, C = q & 15;
+          A[i] = lt_[R * 16 + (C ^ (R & 15))];
         }
+        __builtin_amdgcn_wave_barrier();
+        hm_accumulate<KS>(A, b, g, v);
       }
-      if (KIND == K_STREAM)
-        stream_emit(a, list, colv, col, tau_f, u0 + t * kTile, u1, acc, kg, st, lc);
-      else
-        emit<KIND>(a, s, list, colv, wr, u0 + t * kTile, u1, acc, kg);
+      stream_emit(a, list, colv, col, tau_f, t * kTile, n, hm_finish(v), kg, st, lc);
     }
-    if (KIND == K_STREAM && __any(lc > 0)) stage_flush(a, list, colv, col, kg, st, lc);
+    if (__any(lc > 0)) stage_flush(a, list, colv, col, kg, st, lc);
+    T += t1 - t0;
   }
 }
 
@@ -1031,30 +1127,30 @@ __device__ void fallback_list(const ListArgs& a, int list, uint64_t* sel, int32_
   const int kg = lane >> 4, rl = lane & 15;
   const size_t gstride = (size_t)a.stride[s] * D;
   const int ntiles = (n + kTile - 1) / kTile;
+  u32x4 bhm[KS];
+  if (a.head_mode == 1) hm_load_b<KS>(a.qB + (size_t)(s * a.L + l) * a.Hk * (2 * KS * kWave), a.Hk, bhm);
   for (int t = wave; t < ntiles; t += nw) {
     const int row = t * kTile + rl;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     for (int g = g0; g < g0 + ng; ++g) {
       const u32x4* qb = a.qB + ((size_t)(s * a.L + l) * a.Hk + g) * (2 * KS * kWave);
       const uint16_t* p = a.keys[s] + ((size_t)l * a.Hk + g) * gstride + (size_t)(row < n ? row : 0) * D + 8 * kg;
-      u32x4 A[KS], bh[KS], bl[KS];
+      u32x4 A[KS];
 #pragma unroll
-      for (int i = 0; i < KS; ++i) {
-        A[i] = row < n ? ld_nt(p + 32 * i) : u32x4{0, 0, 0, 0};
-        bh[i] = qb[i * kWave + lane];
-        bl[i] = qb[(KS + i) * kWave + lane];
-      }
+      for (int i = 0; i < KS; ++i) A[i] = row < n ? ld_nt(p + 32 * i) : u32x4{0, 0, 0, 0};
       if (a.head_mode == 0) {
-        acc = score_hilo<KS>(A, bh, bl);
-      } else {
-        // head-mode 1 order, as in k_score_hm: k-steps interleaved, KV heads in turn
+        u32x4 bh[KS], bl[KS];
 #pragma unroll
         for (int i = 0; i < KS; ++i) {
-          acc = mfma_bf16(A[i], bh[i], acc);
-          acc = mfma_bf16(A[i], bl[i], acc);
+          bh[i] = qb[i * kWave + lane];
+          bl[i] = qb[(KS + i) * kWave + lane];
         }
+        acc = score_hilo<KS>(A, bh, bl);
+      } else {
+        hm_accumulate<KS>(A, bhm, g, acc);   // acc gathers the per-head results
       }
     }
+    if (a.head_mode == 1) acc = hm_finish(acc);
     if ((lane & 15) == col) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
@@ -1983,14 +2079,14 @@ ScoreArgs make_score_args(const RetrievePlan& p, int kind) {
 
 // Blocks of the streaming pass: as many as are resident on the device at once,
 // so that every wave takes one contiguous share of the tiles.
-template <int D>
+template <int D, bool HM>
 int stream_grid() {
   static int grid = 0;
   if (grid == 0) {
     int dev = 0, cus = 256, per_cu = 0;
     if (hipGetDevice(&dev) == hipSuccess)
       (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_stream<D>, 256, 0) != hipSuccess ||
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, HM ? k_stream_hm<D> : k_stream<D>, 256, 0) != hipSuccess ||
         per_cu < 1)
       per_cu = 1;
     grid = per_cu * cus;
@@ -2049,13 +2145,21 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
     const ScoreArgs a = make_score_args(p, K_STREAM);
     const int64_t tiles = a.tile_base[p.S];
     if (tiles > 0) {
-      const int grid = (int)std::min<int64_t>(stream_grid<D>(), std::max<int64_t>(1, tiles / 16));
+      const int grid = (int)std::min<int64_t>(stream_grid<D, false>(), std::max<int64_t>(1, tiles / 16));
       hipLaunchKernelGGL(k_stream<D>, dim3(grid), dim3(256), 0, st, a);
     }
   } else {
-    const ScoreArgs a = make_score_args(p, K_STREAM);
-    if (a.total_items > 0)
-      hipLaunchKernelGGL((k_score_hm<D, K_STREAM>), dim3(std::min(a.total_items, 2048)), dim3(256), 0, st, a);
+    ScoreArgs a = make_score_args(p, K_STREAM);
+    int64_t tiles = 0;   // segments are (stream, layer)
+    for (int s = 0; s < p.S; ++s) {
+      a.tile_base[s] = tiles;
+      tiles += (int64_t)p.L * a.ntile[s];
+    }
+    a.tile_base[p.S] = tiles;
+    if (tiles > 0) {
+      const int grid = (int)std::min<int64_t>(stream_grid<D, true>(), std::max<int64_t>(1, tiles / 16));
+      hipLaunchKernelGGL(k_stream_hm<D>, dim3(grid), dim3(256), 0, st, a);
+    }
   }
   if (p.ev_stop) (void)hipEventRecord(p.ev_stop, st);
   // 5. exact top-k from candidates; 6. exact fallback for flagged lists

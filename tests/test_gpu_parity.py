@@ -458,3 +458,66 @@ def test_c4_full_size_sampled():
     assert out["frame_ids"][0, 0] in planted
     ranked = O.vote_pool(v_re, gm, spec.n_frames)
     assert set(ranked[:len(planted)].tolist()) == planted
+
+
+def test_p4_paper_settings_full_size_sampled():
+    """The paper's own selection settings (one query token, head-averaged lists,
+    top 64 per layer, pool 32, 8 units) on the 1-hour stream at full size, in the
+    benchmark's launch configuration: two of the four layer lists checked
+    against the oracle in full, votes and mass from the GPU lists, pool and
+    max-min validity, and the planted evidence."""
+    cfg = W.CONFIGS["P4"]
+    spec = W.stream_specs(cfg)[0]
+    q = W.make_queries(cfg, 0, 0)
+    log("P4 build")
+    gidx, keys = _build_big(cfg, spec, q)
+    P = _P()
+    r = P.Retriever([gidx], cfg.top_k, cfg.n_select, cfg.pool_mult, 1)
+    qd = [[dev_bf16(x) for x in q]]
+    ids, v, m, n = r(qd)
+    torch.cuda.synchronize()
+    plain = ids.cpu().numpy().copy()
+    out = r.debug(qd)
+    np.testing.assert_array_equal(plain, out["frame_ids"])
+    stats = out["list_stats"][0]
+    log("P4 candidates per list", stats[:, 0].tolist(), "fallbacks", stats[:, 1].sum())
+    assert stats[:, 1].sum() == 0
+    assert out["vote_hist"][0].sum() == cfg.n_layers * cfg.top_k
+    oidx = O.Index(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim)
+    oidx.append(keys, spec.n_frames, cfg.tokens_per_frame)
+    del keys
+    rep = {}
+    from parity import check_topk_list, check_pool, check_maxmin
+    qm = O.query_means(q)
+    G = cfg.group
+    for l in (0, 3):
+        so = np.zeros(oidx.candidate_rows())
+        dsc = np.zeros_like(so)
+        for g in range(cfg.n_kv_heads):
+            K = O.decode_bf16(oidx.rows(l)[g])
+            w = qm[l][g * G:(g + 1) * G].sum(axis=0)
+            wa = np.abs(qm[l][g * G:(g + 1) * G]).sum(axis=0)
+            so += K @ w
+            dsc += np.abs(K) @ wa
+            del K
+        so /= cfg.n_q_heads * math.sqrt(cfg.head_dim)
+        dsc /= cfg.n_q_heads * math.sqrt(cfg.head_dim)
+        check_topk_list(so, dsc, out["topk_pos"][0, l].astype(np.int64),
+                        out["topk_score"][0, l].astype(np.float64), cfg.top_k, rep, name=f"P4 layer {l}")
+    lists = [out["topk_pos"][0, j].astype(np.int64) for j in range(cfg.n_layers)]
+    f_of = oidx.frame_of_row()
+    v_re = np.zeros(spec.n_frames, dtype=np.int64)
+    for p in lists:
+        np.add.at(v_re, f_of[p], 1)
+    assert np.array_equal(out["vote_hist"][0, :spec.n_frames], v_re)
+    gm = out["mass_hist"][0, :spec.n_frames].astype(np.float64)
+    m_re = np.zeros(spec.n_frames)
+    for j, p in enumerate(lists):
+        np.add.at(m_re, f_of[p], out["topk_score"][0, j].astype(np.float64))
+    np.testing.assert_allclose(gm, m_re, rtol=1e-5, atol=1e-5)
+    pn = int(out["pool_n"][0])
+    pool = out["pool"][0, :pn].astype(np.int64)
+    check_pool(pool, v_re, gm, 1e-5 * np.abs(m_re) + 1e-5, cfg.pool_mult * cfg.n_select, rep)
+    check_maxmin(pool, np.array(oidx.desc), cfg.n_select, out["frame_ids"][0, :int(out["n_out"][0])].astype(np.int64), rep)
+    log(rep)
+    assert out["frame_ids"][0, 0] in set(spec.planted)

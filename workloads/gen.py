@@ -17,6 +17,9 @@ C4   1-hour stream: 4 layers, 28/4 heads, d=128, 3600 x 196, 24 planted,
 C5   16 streams, 6 layers, 16/2 heads, d=128, lengths uniform on 300..3600
      frames x 196 tokens, odd streams compressed to 32 centroids, 32 query
      tokens, top-k 256, 16 frames per stream
+P4   C4's stream with the paper's own selection settings: one query token (the
+     last prompt token), scores averaged over heads (one list per layer),
+     top 64 per layer, pool of 32, 8 frames
 ==== ============================================================================
 
 Generator: for each (frame, layer, KV head) a centroid ``z ~ N(0, I_d)`` and
@@ -61,6 +64,7 @@ class Config:
     compress_odd_streams: bool = False
     planted_every: int = 150           # ragged batches: one planted frame per this many frames
     pool_mult: int = 4
+    head_mode: int = 0                 # 1: the paper's head-averaged lists, one per layer
     description: str = ""
 
     @property
@@ -81,6 +85,9 @@ CONFIGS: dict[str, Config] = {
     "C5": Config("C5", 6, 16, 2, 128, 196, 32, 256, 16, n_streams=16,
                  frames_range=(300, 3600), compress_odd_streams=True,
                  description="16 ragged streams (300..3600 frames), odd streams compressed"),
+    "P4": Config("P4", 4, 28, 4, 128, 196, 1, 64, 8, n_frames=3600, n_planted=24, head_mode=1,
+                 description="the paper's selection settings on the 1-hour stream: last prompt token, "
+                             "head-averaged scores, top 64 per layer, pool of 32, 8 units"),
 }
 
 
