@@ -192,6 +192,7 @@ class Index:
         self.L, self.Hq, self.Hk, self.d = n_layers, n_q_heads, n_kv_heads, head_dim
         self.G = n_q_heads // n_kv_heads
         self.n_recent = n_recent
+        self.first_detail = 0        # units before it were folded into long-term clusters
         self._chunks = [[] for _ in range(n_layers)]    # per layer: list of [H_kv][r][d] uint16
         self._rows_cache = None
         self.row_start: list[int] = []
@@ -294,8 +295,19 @@ class Index:
         return max(0, self.n_frames - self.n_recent)
 
     def candidate_rows(self) -> int:
+        """End of the candidate rows (the rows before the recent window)."""
         f = self.candidate_frames()
         return self.row_start[f - 1] + self.row_count[f - 1] if f > 0 else 0
+
+    def first_candidate_frame(self) -> int:
+        """Units before ``first_detail`` left the detailed window: with long-history
+        compression the token candidates are the detailed history S_T only
+        (Eq. optional_context_compression; Sec. 4.2 takes candidates from S_T)."""
+        return min(self.first_detail, self.candidate_frames())
+
+    def first_candidate_row(self) -> int:
+        f = self.first_candidate_frame()
+        return self.row_start[f] if f < self.n_frames else self.n_rows
 
     def frame_of_row(self) -> np.ndarray:
         n = self.n_rows
@@ -328,9 +340,11 @@ def score_lists(index: Index, queries, head_mode: int = 0, chunk_rows: int = 1 <
     ``head_mode == 1``: one list per layer, the scores averaged over all query
     heads (the paper's own head reduction).
 
-    Returns a list of float64 arrays over the candidate rows.
+    Returns a list of float64 arrays over the candidate rows; position p is
+    row ``index.first_candidate_row() + p``.
     """
-    N = index.candidate_rows()
+    lo = index.first_candidate_row()
+    N = index.candidate_rows() - lo
     scale = 1.0 / math.sqrt(index.d)
     qm = query_means(queries)
     lists = []
@@ -341,7 +355,7 @@ def score_lists(index: Index, queries, head_mode: int = 0, chunk_rows: int = 1 <
             Qg = qm[l][g * index.G:(g + 1) * index.G]          # [G][d]
             for r0 in range(0, N, chunk_rows):
                 r1 = min(N, r0 + chunk_rows)
-                Kc = decode_bf16(K[g, r0:r1, :])                # [r][d]
+                Kc = decode_bf16(K[g, lo + r0:lo + r1, :])      # [r][d]
                 per_head[g * index.G:(g + 1) * index.G, r0:r1] = (Kc @ Qg.T).T * scale
         if head_mode == 0:
             lists.extend(per_head[h] for h in range(index.Hq))
@@ -355,9 +369,9 @@ def score_lists(index: Index, queries, head_mode: int = 0, chunk_rows: int = 1 <
 def score_scale(index: Index, queries, layer: int, q_head: int) -> np.ndarray:
     """Per candidate row the magnitude ``(1/sqrt d) * sum_e |qbar_e| |K_e|`` of its
     score's terms (the natural scale for score tolerances)."""
-    N = index.candidate_rows()
+    lo, hi = index.first_candidate_row(), index.candidate_rows()
     qm = np.abs(query_means(queries)[layer][q_head])
-    K = np.abs(decode_bf16(index.rows(layer)[q_head // index.G, :N, :]))
+    K = np.abs(decode_bf16(index.rows(layer)[q_head // index.G, lo:hi, :]))
     return (K @ qm) / math.sqrt(index.d)
 
 
@@ -376,7 +390,7 @@ def votes_and_mass(index: Index, topk_lists, score_lists_):
     Returns ``(votes [F] int64, mass [F] float64)`` over all frames.
     """
     F = index.n_frames
-    f_of = index.frame_of_row()
+    f_of = index.frame_of_row()[index.first_candidate_row():index.candidate_rows()]
     votes = np.zeros(F, dtype=np.int64)
     mass = np.zeros(F, dtype=np.float64)
     for pos, s in zip(topk_lists, score_lists_):
@@ -505,16 +519,17 @@ def pooled_scores(index: Index, queries) -> np.ndarray:
     ``(1 / (L H_q)) sum_{l,h} qbar_{l,h} . Kbar_{l,g(h),t} / sqrt(d)``.  For raw
     units this is the mean of the unit's token scores over its tokens and over
     every (layer, head) list.  Candidates are the units before the recent window
-    (Eq. context_partition).
+    (Eq. context_partition) that are still in the detailed history; entry i
+    belongs to unit ``index.first_candidate_frame() + i``.
     """
-    F = index.candidate_frames()
+    f0, F = index.first_candidate_frame(), index.candidate_frames()
     qm = query_means(queries)
-    s = np.zeros(F)
-    if F == 0:
+    s = np.zeros(F - f0)
+    if F == f0:
         return s
-    if any(p is None for p in index.pooled[:F]):
+    if any(p is None for p in index.pooled[f0:F]):
         raise ValueError("pooled keys missing for some units")
-    Kp = np.stack(index.pooled[:F])                         # [F][L][H_kv][d]
+    Kp = np.stack(index.pooled[f0:F])                       # [F - f0][L][H_kv][d]
     for l in range(index.L):
         for h in range(index.Hq):
             s += Kp[:, l, h // index.G, :] @ qm[l][h]
@@ -532,6 +547,107 @@ def pooled_retrieve(index: Index, queries, n_select: int):
     order = np.lexsort((t, -s))[:n_select]
     ids = np.full(n_select, -1, dtype=np.int64)
     sc = np.zeros(n_select)
-    ids[:order.size] = order
+    ids[:order.size] = order + index.first_candidate_frame()
     sc[:order.size] = s[order]
     return ids, sc, int(order.size)
+
+
+# ---------------------------------------------------------------------------
+# Long-history compression (Sec. 4.1, "Optional Long-History Compression") and
+# cluster retrieval (Eq. selected_cluster_evidence)
+# ---------------------------------------------------------------------------
+
+
+class LongClusters:
+    """Long-term clusters of the units that left the detailed window.
+
+    Units leave in temporal order.  Eq. optional_long_memory_clustering: a
+    leaving unit ``t`` joins the latest cluster ``C_j`` when its descriptor
+    ``k_t`` (Eq. memory_key) satisfies ``k_t . c_j >= tau``, and then
+    ``c_j <- Norm((n_j c_j + k_t) / (n_j + 1))``; otherwise it starts a new
+    cluster with ``c = k_t``.  Eq. optional_long_memory_representative: the
+    cluster's representative keys are the running average
+    ``(n_j Kbar_j + K_t) / (n_j + 1)`` of the members' stored rows, position by
+    position, at every shallow layer.
+
+    Readings: the threshold and budget are parameters (the paper gives no
+    values); ``Norm`` of a zero vector stays zero; when ``max_clusters`` are in
+    use a unit that would open a new cluster joins the latest one instead and
+    ``overflow`` is set.
+    """
+
+    def __init__(self, tau: float, max_clusters: int):
+        if max_clusters < 1:
+            raise ValueError("max_clusters must be >= 1")
+        self.tau, self.max_clusters = float(tau), int(max_clusters)
+        self.centroids: list[np.ndarray] = []
+        self.sizes: list[int] = []
+        self.first: list[int] = []
+        self.last: list[int] = []
+        self.rep: list[np.ndarray] = []     # per cluster [L][H_kv][rows][d] float64
+        self.overflow = False
+
+    def absorb(self, index: Index, frame_hi: int) -> None:
+        """Units ``index.first_detail .. frame_hi - 1`` leave the detailed window."""
+        f0 = index.first_detail
+        if not f0 <= frame_hi <= index.candidate_frames():
+            raise ValueError("units leave in order and never from the recent window")
+        for t in range(f0, frame_hi):
+            k = index.desc[t]
+            r0, n_r = index.row_start[t], index.row_count[t]
+            K_t = np.stack([decode_bf16(index.rows(l)[:, r0:r0 + n_r, :]) for l in range(index.L)])
+            if self.rep and K_t.shape != self.rep[0].shape:
+                raise ValueError("every clustered unit must store the same number of rows")
+            joins = bool(self.centroids) and float(k @ self.centroids[-1]) >= self.tau
+            if not joins and self.centroids and len(self.centroids) == self.max_clusters:
+                joins = True
+                self.overflow = True
+            if joins:
+                n = self.sizes[-1]
+                c = (n * self.centroids[-1] + k) / (n + 1)
+                norm = math.sqrt(float(c @ c))
+                self.centroids[-1] = c / norm if norm > 0 else c
+                self.rep[-1] = (n * self.rep[-1] + K_t) / (n + 1)
+                self.sizes[-1] = n + 1
+                self.last[-1] = t
+            else:
+                self.centroids.append(np.array(k, dtype=np.float64))
+                self.rep.append(K_t)
+                self.sizes.append(1)
+                self.first.append(t)
+                self.last.append(t)
+        index.first_detail = frame_hi
+
+
+def cluster_scores(index: Index, clusters: LongClusters, queries) -> np.ndarray:
+    """Eq. selected_cluster_evidence scores every centroid against the final
+    shallow query state.  Reading: the centroid lives in the descriptor space of
+    Eq. memory_key (KV heads flattened head-major), so query head ``h`` of the
+    last shallow layer meets the centroid's block of KV head ``h // G``; the
+    score is the scaled logit averaged over query heads, with the question's
+    tokens reduced by their mean as for token scores."""
+    q = query_means(queries)[index.L - 1]                   # [H_q][d]
+    C = np.array(clusters.centroids).reshape(-1, index.Hk, index.d)
+    s = np.zeros(C.shape[0])
+    for h in range(index.Hq):
+        s += C[:, h // index.G, :] @ q[h]
+    return s / (index.Hq * math.sqrt(index.d))
+
+
+def cluster_retrieve(index: Index, clusters: LongClusters, queries, k_clusters: int):
+    """TopK_{K_l} of the clusters by score, ties to the older cluster.
+    Returns ``(cluster ids, scores, first frames, last frames, n_out)``, padded
+    with -1 / 0."""
+    if k_clusters < 1:
+        raise ValueError("k_clusters must be >= 1")
+    s = cluster_scores(index, clusters, queries) if clusters.centroids else np.zeros(0)
+    order = np.lexsort((np.arange(s.size), -s))[:k_clusters]
+    ids = np.full(k_clusters, -1, dtype=np.int64)
+    sc = np.zeros(k_clusters)
+    fst = np.full(k_clusters, -1, dtype=np.int64)
+    lst = np.full(k_clusters, -1, dtype=np.int64)
+    ids[:order.size] = order
+    sc[:order.size] = s[order]
+    fst[:order.size] = np.array(clusters.first)[order] if order.size else []
+    lst[:order.size] = np.array(clusters.last)[order] if order.size else []
+    return ids, sc, fst, lst, int(order.size)

@@ -602,3 +602,105 @@ def test_pooled_uses_raw_keys_of_compressed_units():
     raw.append(keys, F, T)
     comp.append(keys, F, T, (3, 4))
     np.testing.assert_array_equal(O.pooled_scores(raw, q), O.pooled_scores(comp, q))
+
+
+# ---------------------------------------------------------------------------
+# Long-history compression and cluster retrieval
+# ---------------------------------------------------------------------------
+
+def _cluster_index(tokens):
+    idx = O.Index(1, 1, 1, 2)
+    rows = bits(np.array(tokens, dtype=np.float32))[None]        # [H_kv=1][units][2]
+    idx.append([rows], len(tokens), 1)
+    return idx
+
+
+@pytest.mark.parametrize("case", [c["name"] for c in _load("clusters_hand.json")["cases"]])
+def test_clusters_hand(case):
+    spec = _load("clusters_hand.json")
+    c = next(c for c in spec["cases"] if c["name"] == case)
+    idx = _cluster_index(spec["tokens"])
+    cl = O.LongClusters(c["tau"], c["max_clusters"])
+    cl.absorb(idx, 6)
+    assert idx.first_detail == 6
+    assert [[a, b] for a, b in zip(cl.first, cl.last)] == c["members"]
+    assert cl.sizes == c["sizes"] and cl.overflow == c["overflow"]
+    if "centroids" in c:
+        np.testing.assert_allclose(np.array(cl.centroids), np.array(c["centroids"]), atol=5e-6)  # six-digit hand arithmetic
+    if "representatives" in c:
+        reps = np.array([r[0, 0, 0] for r in cl.rep])
+        np.testing.assert_allclose(reps, np.array(c["representatives"]), atol=1e-7)
+    for qc in c.get("queries", []):
+        q = [bits(np.array([[qc["q"]]], dtype=np.float32))]       # [H_q=1][n_q=1][2]
+        np.testing.assert_allclose(O.cluster_scores(idx, cl, q), qc["scores"], atol=5e-6)
+        ids, sc, fst, lst, n = O.cluster_retrieve(idx, cl, q, 5)
+        assert ids[:n].tolist() == qc["order"] and n == 3
+        assert fst[:n].tolist() == [c["members"][i][0] for i in qc["order"]]
+
+
+def test_clusters_properties_random():
+    """Clusters are contiguous runs covering the absorbed units in order; each
+    joining unit met tau against the centroid it joined (replayed from scratch);
+    representatives are the members' mean rows; absorbing in pieces equals
+    absorbing at once; tau below -1 gives one cluster, above 1 one per unit."""
+    rng = np.random.default_rng(21)
+    L, Hk, d, F, T = 2, 2, 8, 30, 3
+    scene = rng.standard_normal((5, Hk, d))           # five scenes of six units each
+    keys = []
+    for l in range(L):
+        base = scene[np.arange(F * T) // (6 * T)].transpose(1, 0, 2)   # [H_kv][F*T][d]
+        x = base + rng.standard_normal((Hk, F * T, d)) * 0.3
+        keys.append(W.bf16_bits(x.astype(np.float32)))
+    mk = lambda: (lambda i: (i.append(keys, F, T), i)[1])(O.Index(L, 4, Hk, d))
+    a = mk()
+    cl = O.LongClusters(0.8, 100)
+    cl.absorb(a, F)
+    assert cl.first[0] == 0 and cl.last[-1] == F - 1
+    assert all(cl.last[j] + 1 == cl.first[j + 1] for j in range(len(cl.first) - 1))
+    assert sum(cl.sizes) == F and 1 < len(cl.sizes) < F
+    for j in range(len(cl.first)):
+        mem = range(cl.first[j], cl.last[j] + 1)
+        rows = [np.stack([O.decode_bf16(a.rows(l)[:, t * T:(t + 1) * T, :]) for l in range(L)]) for t in mem]
+        np.testing.assert_allclose(cl.rep[j], np.mean(rows, axis=0), rtol=1e-12, atol=1e-12)
+        c = np.array(a.desc[cl.first[j]])
+        for t in list(mem)[1:]:
+            assert a.desc[t] @ c >= 0.8
+            n = t - cl.first[j]
+            c = (n * c + a.desc[t]) / (n + 1)
+            c = c / np.linalg.norm(c)
+        np.testing.assert_allclose(c, cl.centroids[j], rtol=1e-12, atol=1e-12)
+    b = mk()
+    cl2 = O.LongClusters(0.8, 100)
+    for hi in (7, 8, 19, 30):
+        cl2.absorb(b, hi)
+    assert cl2.sizes == cl.sizes
+    np.testing.assert_allclose(np.array(cl2.centroids), np.array(cl.centroids), rtol=1e-12, atol=1e-12)
+    one = O.LongClusters(-1.5, 100)
+    one.absorb(mk(), F)
+    assert one.sizes == [F]
+    every = O.LongClusters(1.5, 100)
+    every.absorb(mk(), F)
+    assert every.sizes == [1] * F
+    with pytest.raises(ValueError):
+        O.LongClusters(0.8, 100).absorb(mk(), F + 1)
+
+
+def test_detailed_window_equals_index_of_the_window():
+    """Token voting with units folded into clusters equals voting on an index
+    that holds only the detailed units (frame ids shifted)."""
+    rng = np.random.default_rng(33)
+    L, Hq, Hk, d, F, T, f0 = 2, 4, 2, 8, 12, 4, 5
+    keys = [W.bf16_bits(rng.standard_normal((Hk, F * T, d)).astype(np.float32)) for _ in range(L)]
+    q = [W.bf16_bits(rng.standard_normal((Hq, 2, d)).astype(np.float32)) for _ in range(L)]
+    full = O.Index(L, Hq, Hk, d, 2)
+    full.append(keys, F, T)
+    O.LongClusters(0.5, 10).absorb(full, f0)
+    part = O.Index(L, Hq, Hk, d, 2)
+    part.append([k[:, f0 * T:, :] for k in keys], F - f0, T)
+    a = O.retrieve(full, q, 6, 3)
+    b = O.retrieve(part, q, 6, 3)
+    assert [x + f0 if x >= 0 else -1 for x in b[0].tolist()] == a[0].tolist()
+    assert a[1].tolist() == b[1].tolist() and a[3] == b[3]
+    pa = O.pooled_retrieve(full, q, 4)
+    pb = O.pooled_retrieve(part, q, 4)
+    assert pa[0].tolist() == [x + f0 for x in pb[0].tolist()]
