@@ -202,6 +202,77 @@ ss_status ss_retrieve_pooled(ss_index* const* idx, int32_t n_streams, const void
                              const int32_t* n_q, int32_t n_select, void* ws, size_t ws_bytes,
                              void* stream, int64_t* frame_ids, float* scores, int32_t* n_out);
 
+/* Long-history compression (Sec. 4.1, "Optional Long-History Compression").
+ * When the history outgrows its budget, the oldest detailed frames leave the
+ * detailed window in temporal order (ss_clusters_absorb).  A leaving frame
+ * joins the latest long-term cluster if its descriptor (Eq. memory_key) has
+ * dot product >= tau with the cluster centroid, which becomes
+ * Norm((n c + k) / (n + 1)); otherwise it starts a new cluster (Eq.
+ * optional_long_memory_clustering).  Each cluster keeps the running average of
+ * its members' stored key rows, position by position, at every shallow layer
+ * (Eq. optional_long_memory_representative).  Frames that left the detailed
+ * window are no longer token candidates for ss_retrieve / ss_retrieve_pooled
+ * (their rows stay in the index arena); their clusters are ranked against the
+ * question by ss_clusters_retrieve (Eq. selected_cluster_evidence).
+ *   n_layers, n_kv_heads, head_dim   as the index's;
+ *   rows_per_unit  stored rows of every absorbed frame (tokens, or centroids);
+ *   max_clusters   capacity; a frame that would open a cluster beyond it joins
+ *                  the latest cluster instead and sets the overflow flag;
+ *   tau            the joining threshold (the paper gives no value). */
+typedef struct {
+  int32_t n_layers;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t rows_per_unit;
+  int64_t max_clusters;
+  float tau;
+} ss_cluster_desc;
+
+typedef struct ss_clusters ss_clusters;
+
+/* Device bytes a cluster set needs (0 if `desc` is invalid).  Layout (256-byte
+ * aligned parts): state int32 [2] (clusters in use, overflow flag); centroids
+ * fp32 [max_clusters][n_kv_heads*head_dim]; sizes int32 [max_clusters];
+ * member frame span int64 [max_clusters][2]; representatives fp32
+ * [max_clusters][n_layers][n_kv_heads][rows_per_unit][head_dim]. */
+size_t ss_clusters_required_bytes(const ss_cluster_desc* desc);
+
+/* An empty cluster set over a caller-owned device arena (256-byte aligned, at
+ * least ss_clusters_required_bytes); enqueues the zeroing of its state on
+ * `stream`. */
+ss_status ss_clusters_create(const ss_cluster_desc* desc, void* dev_arena, size_t arena_bytes,
+                             void* stream, ss_clusters** out);
+ss_status ss_clusters_destroy(ss_clusters* cl);
+
+/* Frames [first, frame_hi) of `idx` leave its detailed window, in order, and
+ * are folded into `cl`; `first` is where the previous call stopped (0 at the
+ * start).  frame_hi must not reach into the recent window (the newest n_recent
+ * frames), and every absorbed frame must store rows_per_unit rows.  ws: device
+ * workspace of ss_clusters_absorb_workspace_bytes(frame_hi - first) bytes. */
+size_t ss_clusters_absorb_workspace_bytes(int64_t n_frames);
+ss_status ss_clusters_absorb(ss_clusters* cl, ss_index* idx, int64_t frame_hi, void* ws, size_t ws_bytes,
+                             void* stream);
+
+/* The k_clusters best clusters for one question (Eq. selected_cluster_evidence):
+ * a centroid's score is the scaled logit of the mean query of the last shallow
+ * layer against it, query head h meeting the centroid's block of KV head h/G,
+ * averaged over query heads.  Ties go to the older cluster.  queries: host
+ * array of n_layers device pointers as in ss_retrieve (only the last layer is
+ * read).  Outputs (device, [k_clusters], rank order, -1 / 0 padded):
+ * cluster_ids int64, scores fp32, first_frame and last_frame int64 member
+ * span; n_out int32 [1].  k_clusters is 1..64. */
+size_t ss_clusters_retrieve_workspace_bytes(const ss_clusters* cl);
+ss_status ss_clusters_retrieve(const ss_clusters* cl, const ss_index* idx, const void* const* queries,
+                               int32_t n_q, int32_t k_clusters, void* ws, size_t ws_bytes, void* stream,
+                               int64_t* cluster_ids, float* scores, int64_t* first_frame,
+                               int64_t* last_frame, int32_t* n_out);
+
+/* Copy a cluster set out (parity only; device pointers, any may be NULL):
+ * state int32 [2], centroids, sizes, span, representatives as laid out in
+ * ss_clusters_required_bytes, for all max_clusters slots. */
+ss_status ss_clusters_export(const ss_clusters* cl, int32_t* state, float* centroids, int32_t* sizes,
+                             int64_t* span, float* reps, void* stream);
+
 /* Evidence assembly parameters (Eq. selected_evidence).
  *   n_recent   N_r, the newest frames that are always evidence (Eq.
  *              context_partition); the paper uses 6 with retrieval, 2 without.

@@ -586,6 +586,7 @@ class LongClusters:
         self.last: list[int] = []
         self.rep: list[np.ndarray] = []     # per cluster [L][H_kv][rows][d] float64
         self.overflow = False
+        self.margins: list[float] = []      # |k_t . c - tau| of every join decision
 
     def absorb(self, index: Index, frame_hi: int) -> None:
         """Units ``index.first_detail .. frame_hi - 1`` leave the detailed window."""
@@ -598,7 +599,11 @@ class LongClusters:
             K_t = np.stack([decode_bf16(index.rows(l)[:, r0:r0 + n_r, :]) for l in range(index.L)])
             if self.rep and K_t.shape != self.rep[0].shape:
                 raise ValueError("every clustered unit must store the same number of rows")
-            joins = bool(self.centroids) and float(k @ self.centroids[-1]) >= self.tau
+            joins = False
+            if self.centroids:
+                dot = float(k @ self.centroids[-1])
+                joins = dot >= self.tau
+                self.margins.append(abs(dot - self.tau))
             if not joins and self.centroids and len(self.centroids) == self.max_clusters:
                 joins = True
                 self.overflow = True

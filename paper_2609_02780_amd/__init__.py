@@ -5,6 +5,7 @@ The work runs in ``libshallowstream.so`` (HIP kernels behind the C ABI of
 ``include/shallowstream.h``); this package only marshals arguments.
 """
 from ._lib import SSError, lib  # noqa: F401
-from .index import PooledRanker, Retriever, ShallowIndex, assemble_evidence, set_profile_events  # noqa: F401
+from .index import (LongClusters, PooledRanker, Retriever, ShallowIndex, assemble_evidence,  # noqa: F401
+                    set_profile_events)
 
-__all__ = ["ShallowIndex", "Retriever", "PooledRanker", "assemble_evidence", "SSError", "set_profile_events", "lib"]
+__all__ = ["ShallowIndex", "Retriever", "PooledRanker", "LongClusters", "assemble_evidence", "SSError", "set_profile_events", "lib"]

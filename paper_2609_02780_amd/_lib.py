@@ -40,6 +40,11 @@ class RetrieveParams(C.Structure):
                 ("head_mode", C.c_int32)]
 
 
+class ClusterDesc(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32),
+                ("rows_per_unit", C.c_int32), ("max_clusters", C.c_int64), ("tau", C.c_float)]
+
+
 class EvidenceParams(C.Structure):
     _fields_ = [("n_recent", C.c_int32), ("n_before", C.c_int32), ("n_after", C.c_int32),
                 ("retrieved", C.c_int32)]
@@ -73,6 +78,15 @@ _SIGS = {
     "ss_pooled_workspace_bytes": (C.c_size_t, [C.POINTER(_P), C.c_int32, C.POINTER(C.c_int32), C.c_int32]),
     "ss_retrieve_pooled": (C.c_int32, [C.POINTER(_P), C.c_int32, C.POINTER(_P), C.POINTER(C.c_int32), C.c_int32,
                                        _P, C.c_size_t, _P, _P, _P, _P]),
+    "ss_clusters_required_bytes": (C.c_size_t, [C.POINTER(ClusterDesc)]),
+    "ss_clusters_create": (C.c_int32, [C.POINTER(ClusterDesc), _P, C.c_size_t, _P, C.POINTER(_P)]),
+    "ss_clusters_destroy": (C.c_int32, [_P]),
+    "ss_clusters_absorb_workspace_bytes": (C.c_size_t, [C.c_int64]),
+    "ss_clusters_absorb": (C.c_int32, [_P, _P, C.c_int64, _P, C.c_size_t, _P]),
+    "ss_clusters_retrieve_workspace_bytes": (C.c_size_t, [_P]),
+    "ss_clusters_retrieve": (C.c_int32, [_P, _P, C.POINTER(_P), C.c_int32, C.c_int32, _P, C.c_size_t, _P,
+                                         _P, _P, _P, _P, _P]),
+    "ss_clusters_export": (C.c_int32, [_P, _P, _P, _P, _P, _P, _P]),
     "ss_evidence_max_units": (C.c_int32, [C.POINTER(EvidenceParams), C.c_int32]),
     "ss_assemble_evidence": (C.c_int32, [C.POINTER(_P), C.c_int32, _P, C.c_int32, C.POINTER(EvidenceParams), _P,
                                          _P, _P, C.c_int32]),

@@ -11,6 +11,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -22,6 +23,7 @@ struct ss_index {
   int64_t n_frames;
   int64_t n_rows;
   std::vector<int64_t> off;  // frame row offsets, n_frames + 1 entries
+  int64_t first_detail = 0;  // frames before it were folded into long-term clusters
   int32_t rpf;               // common rows per frame, 0 if mixed, -1 before the first append
 };
 
@@ -104,11 +106,20 @@ bool same_shape(const ss_index_desc& a, const ss_index_desc& b) {
          a.head_dim == b.head_dim;
 }
 
-// Candidate rows and frames of an index (Eq. context_partition: the newest
-// n_recent frames are excluded).
-void candidates(const ss_index* x, int64_t& rows, int64_t& frames) {
-  frames = std::max<int64_t>(0, x->n_frames - x->desc.n_recent);
-  rows = x->off[frames];
+// Candidate frames [f_lo, f_hi) and rows [r_lo, r_hi) of an index: Eq.
+// context_partition excludes the newest n_recent frames, and with long-history
+// compression the frames already folded into clusters are not token candidates
+// (the detailed history S_T of Eq. optional_context_compression).
+struct Window {
+  int64_t f_lo, f_hi, r_lo, r_hi;
+};
+Window candidates(const ss_index* x) {
+  Window w;
+  w.f_hi = std::max<int64_t>(0, x->n_frames - x->desc.n_recent);
+  w.f_lo = std::min(x->first_detail, w.f_hi);
+  w.r_lo = x->off[w.f_lo];
+  w.r_hi = x->off[w.f_hi];
+  return w;
 }
 
 constexpr int kSampleRank = 48;      // rank r of the sample cut-off
@@ -203,13 +214,15 @@ void build_plan(ss::RetrievePlan& p, ss_index* const* idx, int s0, int S, const 
   int hist = 1;
   for (int i = 0; i < S; ++i) {
     const ss_index* x = idx[s0 + i];
-    int64_t rows, frames;
-    candidates(x, rows, frames);
+    const Window w = candidates(x);
+    const int64_t rows = w.r_hi - w.r_lo, frames = w.f_hi - w.f_lo;
     const StreamSizes z = plan_stream(rows, frames, prm->top_k);
     ss::StreamPlan& sp = p.st[i];
-    sp.keys = x->dev.keys;
-    sp.frame_off = x->dev.frame_off;
-    sp.desc = x->dev.desc;
+    sp.keys = x->dev.keys + w.r_lo * d.head_dim;          // each (layer, KV head) run from r_lo
+    sp.frame_off = x->dev.frame_off + w.f_lo;
+    sp.desc = x->dev.desc + w.f_lo * (int64_t)d.n_kv_heads * d.head_dim;
+    sp.frame0 = w.f_lo;
+    sp.row0 = w.r_lo;
     sp.row_stride = (int32_t)x->desc.max_rows;
     sp.n = z.n;
     sp.f = z.f;
@@ -333,11 +346,12 @@ void build_pooled(ss::PooledPlan& p, ss_index* const* idx, int s0, int S, const 
   p.D = d.head_dim; p.n_select = n_select;
   for (int i = 0; i < S; ++i) {
     const ss_index* x = idx[s0 + i];
-    int64_t rows, frames;
-    candidates(x, rows, frames);
+    const Window w = candidates(x);
+    const int64_t frames = w.f_hi - w.f_lo;
     p.F[i] = frames;
+    p.frame0[i] = w.f_lo;
     p.f_max = std::max<int64_t>(p.f_max, frames);
-    p.pooled[i] = x->dev.pooled;
+    p.pooled[i] = x->dev.pooled + w.f_lo * (int64_t)p.L * p.Hk * p.D;
     p.nq[i] = n_q[s0 + i];
     for (int l = 0; l < p.L; ++l)
       p.q[i * p.L + l] = queries ? static_cast<const uint16_t*>(queries[(size_t)(s0 + i) * p.L + l]) : nullptr;
@@ -370,6 +384,35 @@ ss_status check_pooled(ss_index* const* idx, int32_t n_streams, const int32_t* n
   return SS_OK;
 }
 
+struct ClusterLayout {
+  size_t state, centroids, sizes, span, reps, total;
+};
+
+bool cluster_desc_ok(const ss_cluster_desc* d) {
+  return d && d->n_layers >= 1 && d->n_layers <= ss::kMaxLayers && d->n_kv_heads >= 1 &&
+         (d->head_dim == 64 || d->head_dim == 128) && (int64_t)d->n_kv_heads * d->head_dim <= 1024 &&
+         d->rows_per_unit >= 1 && d->rows_per_unit <= 65536 && d->max_clusters >= 1 &&
+         d->max_clusters <= ((int64_t)1 << 30) && std::isfinite(d->tau);
+}
+
+ClusterLayout cluster_layout(const ss_cluster_desc& d) {
+  ClusterLayout L{};
+  const size_t dim = (size_t)d.n_kv_heads * d.head_dim, M = (size_t)d.max_clusters;
+  size_t off = 0;
+  L.state = off;
+  off = align256(off + 16);
+  L.centroids = off;
+  off = align256(off + M * dim * 4);
+  L.sizes = off;
+  off = align256(off + M * 4);
+  L.span = off;
+  off = align256(off + M * 16);
+  L.reps = off;
+  off = align256(off + M * d.n_layers * dim * d.rows_per_unit * 4);
+  L.total = off;
+  return L;
+}
+
 // Candidate units of one stream's evidence, or -1 for invalid parameters.
 int64_t evidence_units_max(const ss_evidence_params* p, int32_t n_select) {
   if (!p || p->n_recent < 0 || p->n_before < 0 || p->n_after < 0) return -1;
@@ -384,7 +427,142 @@ int64_t evidence_units_max(const ss_evidence_params* p, int32_t n_select) {
 
 }  // namespace
 
+struct ss_clusters {
+  ss_cluster_desc desc;
+  ss::ClusterDev dev;
+};
+
 extern "C" {
+
+size_t ss_clusters_required_bytes(const ss_cluster_desc* desc) {
+  return cluster_desc_ok(desc) ? cluster_layout(*desc).total : 0;
+}
+
+ss_status ss_clusters_create(const ss_cluster_desc* desc, void* dev_arena, size_t arena_bytes, void* stream,
+                             ss_clusters** out) {
+  if (!out) return fail(SS_ERR_INVALID_ARGUMENT, "out is NULL");
+  if (!cluster_desc_ok(desc)) return fail(SS_ERR_INVALID_ARGUMENT, "invalid cluster description");
+  if (!dev_arena || !aligned(dev_arena, 256)) return fail(SS_ERR_INVALID_ARGUMENT, "arena NULL or not 256-byte aligned");
+  const ClusterLayout L = cluster_layout(*desc);
+  if (arena_bytes < L.total) return fail(SS_ERR_CAPACITY, "arena %zu bytes, %zu needed", arena_bytes, L.total);
+  ss_clusters* c = new (std::nothrow) ss_clusters;
+  if (!c) return fail(SS_ERR_INTERNAL, "out of host memory");
+  c->desc = *desc;
+  char* b = static_cast<char*>(dev_arena);
+  c->dev.state = reinterpret_cast<int32_t*>(b + L.state);
+  c->dev.centroids = reinterpret_cast<float*>(b + L.centroids);
+  c->dev.sizes = reinterpret_cast<int32_t*>(b + L.sizes);
+  c->dev.span = reinterpret_cast<int64_t*>(b + L.span);
+  c->dev.reps = reinterpret_cast<float*>(b + L.reps);
+  const hipError_t e = ss::launch_zero32(c->dev.state, 4, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) {
+    delete c;
+    return fail(SS_ERR_DEVICE, "cluster state reset: %s", hipGetErrorString(e));
+  }
+  *out = c;
+  return SS_OK;
+}
+
+ss_status ss_clusters_destroy(ss_clusters* cl) {
+  delete cl;
+  return SS_OK;
+}
+
+size_t ss_clusters_absorb_workspace_bytes(int64_t n_frames) {
+  return n_frames < 0 ? 0 : std::max<size_t>(256, ((size_t)n_frames * 8 + 255) & ~(size_t)255);
+}
+
+ss_status ss_clusters_absorb(ss_clusters* cl, ss_index* idx, int64_t frame_hi, void* ws, size_t ws_bytes,
+                             void* stream) {
+  if (!cl || !idx) return fail(SS_ERR_INVALID_ARGUMENT, "cluster set or index is NULL");
+  const ss_cluster_desc& c = cl->desc;
+  const ss_index_desc& d = idx->desc;
+  if (c.n_layers != d.n_layers || c.n_kv_heads != d.n_kv_heads || c.head_dim != d.head_dim)
+    return fail(SS_ERR_INVALID_ARGUMENT, "cluster set and index shapes differ");
+  const int64_t f_lo = idx->first_detail;
+  const int64_t f_end = std::max<int64_t>(0, idx->n_frames - d.n_recent);
+  if (frame_hi < f_lo || frame_hi > f_end)
+    return fail(SS_ERR_INVALID_ARGUMENT, "frame_hi %lld outside %lld..%lld (frames leave in order, never from the recent window)",
+                (long long)frame_hi, (long long)f_lo, (long long)f_end);
+  for (int64_t f = f_lo; f < frame_hi; ++f)
+    if (idx->off[f + 1] - idx->off[f] != c.rows_per_unit)
+      return fail(SS_ERR_INVALID_ARGUMENT, "frame %lld stores %lld rows, the cluster set takes %d", (long long)f,
+                  (long long)(idx->off[f + 1] - idx->off[f]), c.rows_per_unit);
+  const int64_t n = frame_hi - f_lo;
+  if (n > 0x7FFFFFFF) return fail(SS_ERR_UNSUPPORTED, "too many frames in one call");
+  if (n > 0 && (!ws || !aligned(ws, 256) || ws_bytes < ss_clusters_absorb_workspace_bytes(n)))
+    return fail(SS_ERR_WORKSPACE, "absorb workspace NULL, misaligned or below %zu bytes",
+                ss_clusters_absorb_workspace_bytes(n));
+  ss::AbsorbArgs a{};
+  a.L = c.n_layers; a.Hk = c.n_kv_heads; a.D = c.head_dim; a.R = c.rows_per_unit;
+  a.max_clusters = c.max_clusters; a.max_rows = d.max_rows; a.tau = c.tau;
+  a.f_lo = f_lo; a.n_units = (int)n; a.row_lo = idx->off[f_lo];
+  a.desc = idx->dev.desc; a.keys = idx->dev.keys;
+  a.assign = static_cast<int32_t*>(ws);
+  a.cl = cl->dev;
+  const hipError_t e = ss::launch_absorb(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SS_ERR_DEVICE, "absorb launch failed: %s", hipGetErrorString(e));
+  idx->first_detail = frame_hi;
+  return SS_OK;
+}
+
+size_t ss_clusters_retrieve_workspace_bytes(const ss_clusters* cl) {
+  if (!cl) return 0;
+  ss::ClusterQueryPlan p{};
+  p.Hk = cl->desc.n_kv_heads; p.D = cl->desc.head_dim; p.max_clusters = cl->desc.max_clusters;
+  return ss::cluster_query_workspace(p, nullptr);
+}
+
+ss_status ss_clusters_retrieve(const ss_clusters* cl, const ss_index* idx, const void* const* queries,
+                               int32_t n_q, int32_t k_clusters, void* ws, size_t ws_bytes, void* stream,
+                               int64_t* cluster_ids, float* scores, int64_t* first_frame,
+                               int64_t* last_frame, int32_t* n_out) {
+  if (!cl || !idx) return fail(SS_ERR_INVALID_ARGUMENT, "cluster set or index is NULL");
+  const ss_index_desc& d = idx->desc;
+  if (cl->desc.n_layers != d.n_layers || cl->desc.n_kv_heads != d.n_kv_heads || cl->desc.head_dim != d.head_dim)
+    return fail(SS_ERR_INVALID_ARGUMENT, "cluster set and index shapes differ");
+  if (n_q < 1 || n_q > 4096) return fail(SS_ERR_INVALID_ARGUMENT, "n_q %d outside 1..4096", n_q);
+  if (k_clusters < 1 || k_clusters > ss::kMaxSelect)
+    return fail(SS_ERR_UNSUPPORTED, "k_clusters %d outside 1..%d", k_clusters, ss::kMaxSelect);
+  if (!queries || !queries[d.n_layers - 1]) return fail(SS_ERR_INVALID_ARGUMENT, "last-layer queries are NULL");
+  if (!aligned(queries[d.n_layers - 1], 16)) return fail(SS_ERR_INVALID_ARGUMENT, "queries not 16-byte aligned");
+  if (!cluster_ids || !scores || !first_frame || !last_frame || !n_out)
+    return fail(SS_ERR_INVALID_ARGUMENT, "an output pointer is NULL");
+  ss::ClusterQueryPlan p{};
+  p.L = d.n_layers; p.Hq = d.n_q_heads; p.Hk = d.n_kv_heads; p.G = p.Hq / p.Hk; p.D = d.head_dim;
+  p.nq = n_q; p.k = k_clusters; p.max_clusters = cl->desc.max_clusters;
+  p.q_last = static_cast<const uint16_t*>(queries[d.n_layers - 1]);
+  p.cl = cl->dev;
+  const size_t need = ss::cluster_query_workspace(p, nullptr);
+  if (!ws || !aligned(ws, 256) || ws_bytes < need)
+    return fail(SS_ERR_WORKSPACE, "cluster retrieval workspace NULL, misaligned or below %zu bytes", need);
+  ss::cluster_query_workspace(p, ws);
+  p.out_ids = cluster_ids; p.out_scores = scores; p.out_first = first_frame; p.out_last = last_frame;
+  p.out_n = n_out;
+  const hipError_t e = ss::launch_cluster_query(p, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SS_ERR_DEVICE, "cluster retrieval launch failed: %s", hipGetErrorString(e));
+  return SS_OK;
+}
+
+ss_status ss_clusters_export(const ss_clusters* cl, int32_t* state, float* centroids, int32_t* sizes,
+                             int64_t* span, float* reps, void* stream) {
+  if (!cl) return fail(SS_ERR_INVALID_ARGUMENT, "cluster set is NULL");
+  const ss_cluster_desc& c = cl->desc;
+  const size_t M = (size_t)c.max_clusters, dim = (size_t)c.n_kv_heads * c.head_dim;
+  const hipStream_t hs = static_cast<hipStream_t>(stream);
+  struct Part { void* dst; const void* src; size_t bytes; } parts[] = {
+      {state, cl->dev.state, 8},
+      {centroids, cl->dev.centroids, M * dim * 4},
+      {sizes, cl->dev.sizes, M * 4},
+      {span, cl->dev.span, M * 16},
+      {reps, cl->dev.reps, M * c.n_layers * dim * c.rows_per_unit * 4}};
+  for (const Part& q : parts) {
+    if (!q.dst) continue;
+    const hipError_t e = hipMemcpyAsync(q.dst, q.src, q.bytes, hipMemcpyDeviceToDevice, hs);
+    if (e != hipSuccess) return fail(SS_ERR_DEVICE, "cluster export: %s", hipGetErrorString(e));
+  }
+  return SS_OK;
+}
 
 size_t ss_pooled_workspace_bytes(ss_index* const* idx, int32_t n_streams, const int32_t* n_q,
                                   int32_t n_select) {

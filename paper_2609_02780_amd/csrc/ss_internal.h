@@ -66,6 +66,8 @@ struct StreamPlan {
   int32_t kk;            // min(top_k, n)
   int32_t nq;
   int32_t rpf;           // rows per frame when every frame has the same count, else 0
+  int64_t frame0;        // first candidate frame (earlier ones are in long-term clusters)
+  int64_t row0;          // its first row; keys, frame_off and desc above start there
   float qscale;          // 1 / (n_q sqrt(d)) (head_mode 0), further / H_q (head_mode 1)
   const uint16_t* q[kMaxLayers];  // per layer query pointer [H_q][n_q][d]
 };
@@ -139,7 +141,8 @@ hipError_t launch_retrieve(RetrievePlan& p, hipStream_t st);
 struct PooledPlan {
   int S, L, Hq, Hk, G, D, n_select;
   int64_t F[kMaxStreams];               // candidate frames per stream
-  const float* pooled[kMaxStreams];     // per stream [max_frames][L][H_kv][d]
+  int64_t frame0[kMaxStreams];          // id of the first candidate frame
+  const float* pooled[kMaxStreams];     // per stream, from the first candidate frame: [F][L][H_kv][d]
   const uint16_t* q[kMaxStreams * kMaxLayers];  // [s * L + l] -> bf16 [H_q][n_q][d]
   int32_t nq[kMaxStreams];
   int64_t f_max;
@@ -151,6 +154,46 @@ struct PooledPlan {
 };
 size_t pooled_workspace(PooledPlan& p, void* ws);   // fills p.w / p.scores when ws != null
 hipError_t launch_pooled(const PooledPlan& p, hipStream_t st);
+
+// Long-term clusters of one stream (device view of a cluster arena).
+struct ClusterDev {
+  int32_t* state;      // [0] clusters in use, [1] 1 once a unit had to join a full set
+  float* centroids;    // [max_clusters][H_kv*d]
+  int32_t* sizes;      // [max_clusters]
+  int64_t* span;       // [max_clusters][2]: first and last member frame
+  float* reps;         // [max_clusters][L][H_kv][rows][d]: running-average keys
+};
+
+struct AbsorbArgs {
+  int L, Hk, D, R;            // R: stored rows of every absorbed unit
+  int64_t max_clusters, max_rows;
+  float tau;
+  int64_t f_lo;               // first leaving frame
+  int n_units;
+  int64_t row_lo;             // its first row
+  const float* desc;          // index descriptors [max_frames][H_kv*d]
+  const uint16_t* keys;       // index keys [L][H_kv][max_rows][d]
+  int32_t* assign;            // workspace [n_units][2]: cluster, members before joining
+  ClusterDev cl;
+};
+hipError_t launch_absorb(const AbsorbArgs& a, hipStream_t st);
+hipError_t launch_zero32(int32_t* p, int n, hipStream_t st);   // a kernel, not a memset node
+
+struct ClusterQueryPlan {
+  int L, Hq, Hk, G, D, nq, k;
+  const uint16_t* q_last;     // last shallow layer's queries [H_q][n_q][d]
+  int64_t max_clusters;
+  ClusterDev cl;
+  float* w;                   // workspace [H_kv*d]
+  float* scores;              // workspace [max_clusters]
+  int64_t* out_ids;
+  float* out_scores;
+  int64_t* out_first;
+  int64_t* out_last;
+  int32_t* out_n;
+};
+size_t cluster_query_workspace(ClusterQueryPlan& p, void* ws);
+hipError_t launch_cluster_query(const ClusterQueryPlan& p, hipStream_t st);
 
 // Evidence assembly of up to kMaxStreams streams, one block each.
 constexpr int kMaxEvidence = 4096;   // candidate units per stream (sorted in LDS)

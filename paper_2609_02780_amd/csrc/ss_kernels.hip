@@ -933,7 +933,8 @@ struct ListArgs {
   int NL, S, cap, k_max, top_k, hist_f;
   int32_t m[kMaxStreams], r[kMaxStreams], kk[kMaxStreams], n[kMaxStreams];
   int32_t f[kMaxStreams], rpf[kMaxStreams];
-  const int32_t* frame_off[kMaxStreams];
+  const int32_t* frame_off[kMaxStreams];   // from the first candidate frame; values are absolute rows
+  int64_t row0[kMaxStreams];               // the first candidate row
   int64_t full_base[kMaxStreams];
   const float* samp;
   int samp_stride;
@@ -960,10 +961,11 @@ struct ListArgs {
 __device__ __forceinline__ int frame_of_row(const ListArgs& a, int s, uint32_t row) {
   if (a.rpf[s] > 0) return (int)(row / (uint32_t)a.rpf[s]);
   const int32_t* off = a.frame_off[s];
+  const int64_t r = (int64_t)row + a.row0[s];
   int lo = 0, hi = a.f[s] - 1;  // largest f with off[f] <= row
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
-    if ((uint32_t)off[mid] <= row) lo = mid; else hi = mid - 1;
+    if ((int64_t)off[mid] <= r) lo = mid; else hi = mid - 1;
   }
   return lo;
 }
@@ -1292,6 +1294,7 @@ __global__ __launch_bounds__(1024) void k_select(ListArgs a) {
 struct VoteArgs {
   int NL, k_max, pool, f_max, hist_stride;
   int32_t f[kMaxStreams];
+  int64_t frame0[kMaxStreams];   // debug outputs are indexed by absolute frame id
   const int32_t* run_f;
   const int32_t* run_c;
   const int64_t* run_fx;
@@ -1394,8 +1397,8 @@ __global__ __launch_bounds__(1024) void k_votes_pool(VoteArgs a) {
     const int v = __hip_atomic_load(&votes[f], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const int64_t mf = __hip_atomic_load(&massfx[f], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (a.dbg_vote_hist) {
-      a.dbg_vote_hist[(size_t)s * a.hist_stride + f] = v;
-      a.dbg_mass_hist[(size_t)s * a.hist_stride + f] = (float)((double)mf * inv);
+      a.dbg_vote_hist[(size_t)s * a.hist_stride + a.frame0[s] + f] = v;
+      a.dbg_mass_hist[(size_t)s * a.hist_stride + a.frame0[s] + f] = (float)((double)mf * inv);
     }
     if (v >= 1) {
       const uint32_t slot = atomicAdd(&nvoted_sh, 1u);
@@ -1408,7 +1411,8 @@ __global__ __launch_bounds__(1024) void k_votes_pool(VoteArgs a) {
     }
   }
   if (a.dbg_vote_hist) {
-    for (int f = F + threadIdx.x; f < a.hist_stride; f += blockDim.x) {
+    for (int f = threadIdx.x; f < a.hist_stride; f += blockDim.x) {
+      if (f >= a.frame0[s] && f < a.frame0[s] + F) continue;
       a.dbg_vote_hist[(size_t)s * a.hist_stride + f] = 0;
       a.dbg_mass_hist[(size_t)s * a.hist_stride + f] = 0.f;
     }
@@ -1466,7 +1470,7 @@ __global__ __launch_bounds__(1024) void k_votes_pool(VoteArgs a) {
     a.pool_ids[(size_t)s * P + i] = id;
     a.pool_votes[(size_t)s * P + i] = v;
     a.pool_mass[(size_t)s * P + i] = m;
-    if (a.dbg_pool) a.dbg_pool[(size_t)s * P + i] = id;
+    if (a.dbg_pool) a.dbg_pool[(size_t)s * P + i] = id >= 0 ? (int32_t)(id + a.frame0[s]) : -1;
   }
   if (threadIdx.x == 0) {
     a.pool_n[s] = pn;
@@ -1540,6 +1544,7 @@ __global__ __launch_bounds__(256) void k_gram(GramArgs a) {
 // ---------------------------------------------------------------------------
 struct MaxminArgs {
   int pool, ld, n_select;
+  int64_t frame0[kMaxStreams];   // added to the (window-relative) pool ids on output
   const int32_t* pool_ids;
   const int32_t* pool_votes;
   const float* pool_mass;
@@ -1639,7 +1644,7 @@ __global__ __launch_bounds__(1024) void k_maxmin(MaxminArgs a) {
     const size_t o = (size_t)s * a.n_select + i;
     if (i < K) {
       const int p = sel[i];
-      a.out_ids[o] = a.pool_ids[(size_t)s * a.pool + p];
+      a.out_ids[o] = a.pool_ids[(size_t)s * a.pool + p] + a.frame0[s];
       a.out_votes[o] = a.pool_votes[(size_t)s * a.pool + p];
       a.out_mass[o] = a.pool_mass[(size_t)s * a.pool + p];
     } else {
@@ -1896,6 +1901,7 @@ __global__ __launch_bounds__(kPoolQGroups * D) void k_pool_query(PoolQArgs a) {
 
 struct PoolScoreArgs {
   int n4;                           // float4 per unit: L H_kv D / 4
+  const int32_t* count;             // null, or a device count that caps F[0] (one stream)
   int64_t F[kMaxStreams];
   const float4* pooled[kMaxStreams];
   const float4* w;                  // [S][n4]
@@ -1908,7 +1914,8 @@ struct PoolScoreArgs {
 __global__ __launch_bounds__(256) void k_pool_score(PoolScoreArgs a) {
   const int s = blockIdx.y, lane = threadIdx.x & (kWave - 1);
   const int64_t f = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (f >= a.F[s]) return;   // whole waves leave together
+  const int64_t F = a.count ? min<int64_t>(a.F[s], *a.count) : a.F[s];
+  if (f >= F) return;   // whole waves leave together
   const float4* k = a.pooled[s] + f * a.n4;
   const float4* w = a.w + (size_t)s * a.n4;
   float acc = 0.f;
@@ -1925,7 +1932,12 @@ __global__ __launch_bounds__(256) void k_pool_score(PoolScoreArgs a) {
 
 struct PoolSelectArgs {
   int n_select;
+  const int32_t* count;             // null, or a device count that caps F[0] (one stream)
+  const int64_t* span;              // null, or [F][2] first/last frame of each unit
+  int64_t* out_first;               // with span: [S][n_select]
+  int64_t* out_last;
   int64_t F[kMaxStreams];
+  int64_t frame0[kMaxStreams];      // added to the window-relative ids
   const float* scores;              // [S][f_max]
   int64_t f_max;
   int64_t* out_ids;                 // [S][n_select]
@@ -1943,7 +1955,7 @@ __global__ __launch_bounds__(1024) void k_pool_select(PoolSelectArgs a) {
   __shared__ uint64_t sel[kMaxSelect];
   __shared__ uint32_t nsel;
   const int s = blockIdx.x;
-  const int64_t F = a.F[s];
+  const int64_t F = a.count ? min<int64_t>(a.F[s], *a.count) : a.F[s];
   const int K = (int)min<int64_t>(a.n_select, F);
   __shared__ float lsc[kPoolLds];
   const float* gsc = a.scores + (size_t)s * a.f_max;
@@ -1972,14 +1984,145 @@ __global__ __launch_bounds__(1024) void k_pool_select(PoolSelectArgs a) {
     const uint64_t k = sel[threadIdx.x];
     int rank = 0;
     for (int m = 0; m < K; ++m) rank += sel[m] > k;
-    ids[rank] = key_row(k);
+    ids[rank] = (int64_t)key_row(k) + a.frame0[s];
     scs[rank] = key_score(k);
+    if (a.span) {
+      a.out_first[(size_t)s * a.n_select + rank] = a.span[2 * (size_t)key_row(k)];
+      a.out_last[(size_t)s * a.n_select + rank] = a.span[2 * (size_t)key_row(k) + 1];
+    }
   }
   for (int i = K + threadIdx.x; i < a.n_select; i += blockDim.x) {
     ids[i] = -1;
     scs[i] = 0.f;
+    if (a.span) {
+      a.out_first[(size_t)s * a.n_select + i] = -1;
+      a.out_last[(size_t)s * a.n_select + i] = -1;
+    }
   }
   if (threadIdx.x == 0) a.out_n[s] = K;
+}
+
+// ---------------------------------------------------------------------------
+// Long-history compression (Eq. optional_long_memory_clustering and Eq.
+// optional_long_memory_representative).  k_cluster_assign walks the leaving
+// units in temporal order in one block (each decision needs the centroid the
+// previous one left); k_cluster_reps then replays the recorded assignments for
+// every element of the representative keys in parallel.
+// ---------------------------------------------------------------------------
+
+__global__ void k_zero32(int32_t* p, int n) {
+  for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = 0;
+}
+
+// Sum over a 256-thread block, the same order every time.
+__device__ float block_sum256(float v, float* red) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+__global__ __launch_bounds__(256) void k_cluster_assign(AbsorbArgs a) {
+  __shared__ float red[4];
+  const int dim = a.Hk * a.D;   // at most 1024: four elements per thread
+  int nc = a.cl.state[0], ovf = a.cl.state[1];
+  int n = nc > 0 ? a.cl.sizes[nc - 1] : 0;
+  float c[4] = {0.f, 0.f, 0.f, 0.f};
+  if (nc > 0)
+    for (int k = 0; k < 4; ++k) {
+      const int e = threadIdx.x + 256 * k;
+      if (e < dim) c[k] = a.cl.centroids[(size_t)(nc - 1) * dim + e];
+    }
+  for (int u = 0; u < a.n_units; ++u) {
+    const int64_t t = a.f_lo + u;
+    float kv[4] = {0.f, 0.f, 0.f, 0.f};
+    float part = 0.f;
+    for (int k = 0; k < 4; ++k) {
+      const int e = threadIdx.x + 256 * k;
+      if (e < dim) kv[k] = a.desc[t * dim + e];
+      part = fmaf(kv[k], c[k], part);
+    }
+    bool join = false;
+    if (nc > 0) {
+      const float dot = block_sum256(part, red);
+      join = dot >= a.tau;
+      if (!join && nc == a.max_clusters) {
+        join = true;
+        ovf = 1;
+      }
+    }
+    if (join) {
+      // c <- Norm((n c + k) / (n + 1))
+      float z[4], zz = 0.f;
+      for (int k = 0; k < 4; ++k) {
+        z[k] = ((float)n * c[k] + kv[k]) / (float)(n + 1);
+        zz = fmaf(z[k], z[k], zz);
+      }
+      const float nrm = sqrtf(block_sum256(zz, red));
+      for (int k = 0; k < 4; ++k) c[k] = nrm > 0.f ? z[k] / nrm : z[k];
+      if (threadIdx.x == 0) {
+        a.assign[2 * u] = nc - 1;
+        a.assign[2 * u + 1] = n;
+        a.cl.span[2 * (size_t)(nc - 1) + 1] = t;
+      }
+      ++n;
+    } else {
+      if (nc > 0) {
+        for (int k = 0; k < 4; ++k) {
+          const int e = threadIdx.x + 256 * k;
+          if (e < dim) a.cl.centroids[(size_t)(nc - 1) * dim + e] = c[k];
+        }
+        if (threadIdx.x == 0) a.cl.sizes[nc - 1] = n;
+      }
+      for (int k = 0; k < 4; ++k) c[k] = kv[k];
+      if (threadIdx.x == 0) {
+        a.assign[2 * u] = nc;
+        a.assign[2 * u + 1] = 0;
+        a.cl.span[2 * (size_t)nc] = t;
+        a.cl.span[2 * (size_t)nc + 1] = t;
+      }
+      n = 1;
+      ++nc;
+    }
+  }
+  if (nc > 0) {
+    for (int k = 0; k < 4; ++k) {
+      const int e = threadIdx.x + 256 * k;
+      if (e < dim) a.cl.centroids[(size_t)(nc - 1) * dim + e] = c[k];
+    }
+  }
+  if (threadIdx.x == 0) {
+    if (nc > 0) a.cl.sizes[nc - 1] = n;
+    a.cl.state[0] = nc;
+    a.cl.state[1] = ovf;
+  }
+}
+
+// One thread per element of a representative ([L][H_kv][R][D]): replays the
+// call's units in order, (n rep + K) / (n + 1) with the recorded n.
+__global__ __launch_bounds__(256) void k_cluster_reps(AbsorbArgs a) {
+  const int64_t E = (int64_t)a.L * a.Hk * a.R * a.D;
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= E) return;
+  const int d = (int)(e % a.D);
+  const int64_t lgr = e / a.D;
+  const int r = (int)(lgr % a.R);
+  const int64_t lg = lgr / a.R;   // l * H_kv + g
+  const uint16_t* src = a.keys + (lg * a.max_rows + a.row_lo + r) * a.D + d;
+  int cur = -1;
+  float v = 0.f;
+  for (int u = 0; u < a.n_units; ++u) {
+    const int j = a.assign[2 * u], nb = a.assign[2 * u + 1];
+    if (j != cur) {
+      if (cur >= 0) a.cl.reps[(size_t)cur * E + e] = v;
+      cur = j;
+      v = nb > 0 ? a.cl.reps[(size_t)j * E + e] : 0.f;
+    }
+    const float k = __uint_as_float((uint32_t)src[(int64_t)u * a.R * a.D] << 16);
+    v = nb == 0 ? k : ((float)nb * v + k) / (float)(nb + 1);
+  }
+  if (cur >= 0) a.cl.reps[(size_t)cur * E + e] = v;
 }
 
 // ---------------------------------------------------------------------------
@@ -2126,6 +2269,7 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
     la.m[s] = p.st[s].m; la.r[s] = p.st[s].r; la.kk[s] = p.st[s].kk; la.n[s] = p.st[s].n;
     la.full_base[s] = p.full_base[s];
     la.f[s] = p.st[s].f; la.rpf[s] = p.st[s].rpf; la.frame_off[s] = p.st[s].frame_off;
+    la.row0[s] = p.st[s].row0;
   }
   la.samp = p.samp; la.samp_stride = p.m_max; la.tau = p.tau; la.cnt = p.cnt; la.flag = p.flag;
   la.cand = p.cand; la.full = p.full;
@@ -2168,7 +2312,10 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   VoteArgs va{};
   va.NL = p.NL; va.k_max = p.k_max; va.pool = p.pool; va.f_max = p.f_max;
   va.hist_stride = p.dbg_hist_stride;
-  for (int s = 0; s < p.S; ++s) va.f[s] = p.st[s].f;
+  for (int s = 0; s < p.S; ++s) {
+    va.f[s] = p.st[s].f;
+    va.frame0[s] = p.st[s].frame0;
+  }
   va.run_f = p.run_f; va.run_c = p.run_c; va.run_fx = p.run_fx; va.nruns = p.nruns;
   va.listexp = p.listexp;
   va.votes_g = p.votes; va.massfx_g = p.massfx;
@@ -2188,6 +2335,7 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   ma.pool = p.pool; ma.ld = (p.pool + 3) & ~3; ma.n_select = p.n_select;
   ma.pool_ids = p.pool_ids; ma.pool_votes = p.pool_votes; ma.pool_mass = p.pool_mass;
   ma.pool_n = p.pool_n; ma.gram = p.gram;
+  for (int s = 0; s < p.S; ++s) ma.frame0[s] = p.st[s].frame0;
   ma.out_ids = p.out_ids; ma.out_votes = p.out_votes; ma.out_mass = p.out_mass; ma.out_n = p.out_n;
   hipLaunchKernelGGL(k_maxmin, dim3(p.S), dim3(1024), 0, st, ma);
   return hipGetLastError();
@@ -2259,6 +2407,7 @@ hipError_t pooled_impl(const PooledPlan& p, hipStream_t st) {
     sa.F[s] = p.F[s];
     sa.pooled[s] = reinterpret_cast<const float4*>(p.pooled[s]);
     ka.F[s] = p.F[s];
+    ka.frame0[s] = p.frame0[s];
   }
   if (p.f_max > 0)
     hipLaunchKernelGGL(k_pool_score, dim3((unsigned)cdiv(p.f_max, 4), p.S), dim3(256), 0, st, sa);
@@ -2268,6 +2417,70 @@ hipError_t pooled_impl(const PooledPlan& p, hipStream_t st) {
 
 hipError_t launch_pooled(const PooledPlan& p, hipStream_t st) {
   return p.D == 64 ? pooled_impl<64>(p, st) : pooled_impl<128>(p, st);
+}
+
+hipError_t launch_zero32(int32_t* p, int n, hipStream_t st) {
+  hipLaunchKernelGGL(k_zero32, dim3(1), dim3(64), 0, st, p, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_absorb(const AbsorbArgs& a, hipStream_t st) {
+  if (a.n_units <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_cluster_assign, dim3(1), dim3(256), 0, st, a);
+  const int64_t E = (int64_t)a.L * a.Hk * a.R * a.D;
+  hipLaunchKernelGGL(k_cluster_reps, dim3((unsigned)cdiv(E, 256)), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+size_t cluster_query_workspace(ClusterQueryPlan& p, void* ws) {
+  size_t off = 0;
+  auto take = [&](size_t bytes) -> void* {
+    off = (off + 255) & ~(size_t)255;
+    void* r = ws ? static_cast<char*>(ws) + off : nullptr;
+    off += bytes;
+    return r;
+  };
+  p.w = static_cast<float*>(take((size_t)p.Hk * p.D * 4));
+  p.scores = static_cast<float*>(take((size_t)std::max<int64_t>(p.max_clusters, 1) * 4));
+  return (off + 255) & ~(size_t)255;
+}
+
+template <int D>
+hipError_t cluster_query_impl(const ClusterQueryPlan& p, hipStream_t st) {
+  // the last layer's pooled query weights (one layer: scale 1/(n_q H_q sqrt d))
+  PoolQArgs qa{};
+  qa.Hq = p.Hq; qa.Hk = p.Hk; qa.G = p.G; qa.L = 1; qa.first = 0; qa.w = p.w;
+  qa.q[0] = p.q_last;
+  qa.nq[0] = p.nq;
+  hipLaunchKernelGGL(k_pool_query<D>, dim3(p.Hk), dim3(kPoolQGroups * D), 0, st, qa);
+  PoolScoreArgs sa{};
+  sa.n4 = p.Hk * D / 4;
+  sa.count = p.cl.state;
+  sa.F[0] = p.max_clusters;
+  sa.pooled[0] = reinterpret_cast<const float4*>(p.cl.centroids);
+  sa.w = reinterpret_cast<const float4*>(p.w);
+  sa.scores = p.scores;
+  sa.f_max = std::max<int64_t>(p.max_clusters, 1);
+  hipLaunchKernelGGL(k_pool_score, dim3((unsigned)cdiv(p.max_clusters, 4), 1), dim3(256), 0, st, sa);
+  PoolSelectArgs ka{};
+  ka.n_select = p.k;
+  ka.count = p.cl.state;
+  ka.span = p.cl.span;
+  ka.out_first = p.out_first;
+  ka.out_last = p.out_last;
+  ka.F[0] = p.max_clusters;
+  ka.frame0[0] = 0;
+  ka.scores = p.scores;
+  ka.f_max = sa.f_max;
+  ka.out_ids = p.out_ids;
+  ka.out_scores = p.out_scores;
+  ka.out_n = p.out_n;
+  hipLaunchKernelGGL(k_pool_select, dim3(1), dim3(1024), 0, st, ka);
+  return hipGetLastError();
+}
+
+hipError_t launch_cluster_query(const ClusterQueryPlan& p, hipStream_t st) {
+  return p.D == 64 ? cluster_query_impl<64>(p, st) : cluster_query_impl<128>(p, st);
 }
 
 hipError_t launch_evidence(const EvidenceArgs& a, hipStream_t st) {

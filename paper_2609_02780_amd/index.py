@@ -248,6 +248,90 @@ class PooledRanker:
         return self.frame_ids, self.scores, self.n_out
 
 
+class LongClusters:
+    """Long-term clusters of the frames that left an index's detailed window
+    (the paper's optional long-history compression), in a device arena owned by
+    this object."""
+
+    def __init__(self, index: ShallowIndex, rows_per_unit: int, max_clusters: int, tau: float, stream=None):
+        self.index = index
+        self.desc = L.ClusterDesc(index.n_layers, index.n_kv_heads, index.head_dim, rows_per_unit,
+                                  max_clusters, tau)
+        nbytes = L.lib().ss_clusters_required_bytes(C.byref(self.desc))
+        if nbytes == 0:
+            raise L.SSError(L.SS_ERR_INVALID_ARGUMENT, "invalid cluster description")
+        self.arena = torch.empty(nbytes, dtype=torch.uint8, device=index.arena.device)
+        self._h = C.c_void_p()
+        L.check(L.lib().ss_clusters_create(C.byref(self.desc), self.arena.data_ptr(), nbytes,
+                                           _stream_handle(stream), C.byref(self._h)))
+        self._ws = None
+        self._qws = None
+
+    def close(self) -> None:
+        if getattr(self, "_h", None) is not None:
+            L.check(L.lib().ss_clusters_destroy(self._h))
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def absorb(self, frame_hi: int, n_frames: int, stream=None) -> None:
+        """Frames up to ``frame_hi`` (exclusive) leave the detailed window;
+        ``n_frames`` is how many leave in this call (sizes the workspace)."""
+        need = L.lib().ss_clusters_absorb_workspace_bytes(n_frames)
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = torch.empty(need, dtype=torch.uint8, device=self.arena.device)
+        L.check(L.lib().ss_clusters_absorb(self._h, self.index.handle, frame_hi, self._ws.data_ptr(),
+                                           self._ws.numel(), _stream_handle(stream)))
+
+    def retrieve(self, queries, k_clusters: int, stream=None):
+        """``queries[l]``: ``[H_q][n_q][d]`` bfloat16 (only the last layer is
+        read).  Returns device tensors ``(cluster_ids, scores, first_frame,
+        last_frame, n_out)``."""
+        x = self.index
+        if len(queries) != x.n_layers:
+            raise ValueError(f"expected {x.n_layers} query tensors")
+        nq = queries[0].shape[1]
+        ptrs = [_check_bf16(q, (x.n_q_heads, nq, x.head_dim), f"queries[{l}]") for l, q in enumerate(queries)]
+        need = L.lib().ss_clusters_retrieve_workspace_bytes(self._h)
+        if self._qws is None or self._qws.numel() < need:
+            self._qws = torch.empty(need, dtype=torch.uint8, device=self.arena.device)
+        dev = self.arena.device
+        ids = torch.empty(k_clusters, dtype=torch.int64, device=dev)
+        sc = torch.empty(k_clusters, dtype=torch.float32, device=dev)
+        first = torch.empty(k_clusters, dtype=torch.int64, device=dev)
+        last = torch.empty(k_clusters, dtype=torch.int64, device=dev)
+        n_out = torch.empty(1, dtype=torch.int32, device=dev)
+        L.check(L.lib().ss_clusters_retrieve(self._h, x.handle, L.ptr_array(ptrs), nq, k_clusters,
+                                             self._qws.data_ptr(), self._qws.numel(), _stream_handle(stream),
+                                             ids.data_ptr(), sc.data_ptr(), first.data_ptr(), last.data_ptr(),
+                                             n_out.data_ptr()))
+        return ids, sc, first, last, n_out
+
+    def export(self, stream=None) -> dict:
+        """The cluster state on the host (synchronises; parity checks only)."""
+        d = self.desc
+        M, dim = d.max_clusters, d.n_kv_heads * d.head_dim
+        dev = self.arena.device
+        t = {"state": torch.empty(2, dtype=torch.int32, device=dev),
+             "centroids": torch.empty((M, dim), dtype=torch.float32, device=dev),
+             "sizes": torch.empty(M, dtype=torch.int32, device=dev),
+             "span": torch.empty((M, 2), dtype=torch.int64, device=dev),
+             "reps": torch.empty((M, d.n_layers, d.n_kv_heads, d.rows_per_unit, d.head_dim), dtype=torch.float32,
+                                 device=dev)}
+        L.check(L.lib().ss_clusters_export(self._h, *(t[k].data_ptr() for k in ("state", "centroids", "sizes",
+                                                                                  "span", "reps")),
+                                           _stream_handle(stream)))
+        torch.cuda.synchronize(dev)
+        out = {k: v.cpu().numpy() for k, v in t.items()}
+        n = int(out["state"][0])
+        return {"n_clusters": n, "overflow": bool(out["state"][1]), "centroids": out["centroids"][:n],
+                "sizes": out["sizes"][:n], "span": out["span"][:n], "reps": out["reps"][:n]}
+
+
 def assemble_evidence(indices, frame_ids, n_recent: int, n_before: int = 1, n_after: int = 0,
                       retrieved: bool = True, stream=None):
     """The frames handed to answering for each stream (Eq. selected_evidence,

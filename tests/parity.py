@@ -35,14 +35,15 @@ def dev_bf16(a: np.ndarray) -> torch.Tensor:
 def score_scale(oidx: O.Index, queries, head_mode: int = 0):
     """Per list, per candidate row: ``(1/sqrt d) sum_e |qbar_e| |K_e|`` (head_mode 0),
     or the head mean of those magnitudes (head_mode 1)."""
-    N = oidx.candidate_rows()
+    lo, hi = oidx.first_candidate_row(), oidx.candidate_rows()
+    N = hi - lo
     qm = O.query_means(queries)
     out = []
     for l in range(oidx.L):
         K = oidx.rows(l)
         per_head = np.empty((oidx.Hq, N))
         for g in range(oidx.Hk):
-            Ka = np.abs(O.decode_bf16(K[g, :N, :]))
+            Ka = np.abs(O.decode_bf16(K[g, lo:hi, :]))
             Qa = np.abs(qm[l][g * oidx.G:(g + 1) * oidx.G])
             per_head[g * oidx.G:(g + 1) * oidx.G] = (Ka @ Qa.T).T / math.sqrt(oidx.d)
         if head_mode == 0:
@@ -136,7 +137,7 @@ def staged_check(oidx: O.Index, queries, gpu: dict, s: int, top_k: int, n_select
     report = {}
     S_or = O.score_lists(oidx, queries, head_mode)
     Dsc = score_scale(oidx, queries, head_mode)
-    N = oidx.candidate_rows()
+    N = oidx.candidate_rows() - oidx.first_candidate_row()     # positions are window-relative
     kk = min(top_k, N)
     NL = len(S_or)
     gpu_lists, exact_lists = [], []
@@ -155,7 +156,7 @@ def staged_check(oidx: O.Index, queries, gpu: dict, s: int, top_k: int, n_select
     assert np.array_equal(gv, v_re), "votes differ from the oracle's votes of the GPU lists"
     assert gv.sum() == NL * kk
     # mass tolerance: 1e-3 of the summed magnitudes of the frame's selected scores
-    f_of = oidx.frame_of_row()
+    f_of = oidx.frame_of_row()[oidx.first_candidate_row():oidx.candidate_rows()]
     mag = np.zeros(F)
     for p, dsc in zip(gpu_lists, Dsc):
         np.add.at(mag, f_of[p], dsc[p])

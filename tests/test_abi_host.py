@@ -226,3 +226,19 @@ def test_pooled_validation(L):
     assert lib.ss_retrieve_pooled(idx, 1, qs_bad, nq, 8, F, ws, None, F, F, F) == L.SS_ERR_INVALID_ARGUMENT
     assert b"queries[1]" in lib.ss_last_error()
     assert lib.ss_index_destroy(h) == 0
+
+
+def test_clusters_validation(L):
+    lib = L.lib()
+    D = L.ClusterDesc
+    ok = D(4, 4, 128, 196, 100, 0.9)
+    n = lib.ss_clusters_required_bytes(C.byref(ok))
+    assert n >= 100 * (512 * 4 + 4 + 16 + 4 * 4 * 196 * 128 * 4)
+    for bad in (D(0, 4, 128, 196, 100, 0.9), D(4, 4, 96, 196, 100, 0.9), D(4, 4, 128, 0, 100, 0.9),
+                D(4, 4, 128, 196, 0, 0.9), D(4, 4, 128, 196, 100, float("nan")), D(4, 16, 128, 196, 100, 0.9)):
+        assert lib.ss_clusters_required_bytes(C.byref(bad)) == 0
+    h = C.c_void_p()
+    assert lib.ss_clusters_create(C.byref(ok), FAKE, n - 1, None, C.byref(h)) == L.SS_ERR_CAPACITY
+    assert lib.ss_clusters_create(C.byref(ok), FAKE + 8, n, None, C.byref(h)) == L.SS_ERR_INVALID_ARGUMENT
+    assert lib.ss_clusters_absorb_workspace_bytes(10) >= 80
+    assert lib.ss_clusters_absorb_workspace_bytes(-1) == 0
