@@ -204,6 +204,15 @@ def sweep(torch, P, cfg, points=(64, 128, 256, 512, 1024, 2048, 3600), calls=20)
                 raise RuntimeError("graph replay differs from the eager call")
         return a.elapsed_time(b) / calls
 
+    # long-history compression on: a second index keeps the newest 6 frames as
+    # recent context and the 512 before them in detail; older frames leave into
+    # long-term clusters as the stream grows
+    n_recent, n_detail, tau = 6, 512, 0.1
+    lidx = P.ShallowIndex(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, F_max, F_max * T, n_recent)
+    lcl = P.LongClusters(lidx, T, 4096, tau)
+    lr = P.Retriever([lidx], cfg.top_k, cfg.n_select, cfg.pool_mult)
+    absorbed, absorb_ms = 0, []
+
     rows = []
     have = 0
     for F in points:
@@ -211,20 +220,40 @@ def sweep(torch, P, cfg, points=(64, 128, 256, 512, 1024, 2048, 3600), calls=20)
             f1 = min(F, have + 600)
             kb = W.frame_block_keys(cfg, spec, q, have, f1)
             idx.append([dev_bf16(torch, k) for k in kb], f1 - have, T)
+            lidx.append([dev_bf16(torch, k) for k in kb], f1 - have, T)
             have = f1
         torch.cuda.synchronize()
+        hi = max(0, F - n_recent - n_detail)
+        if hi > absorbed:
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            lcl.absorb(hi, hi - absorbed)
+            b.record()
+            b.synchronize()
+            absorb_ms.append((a.elapsed_time(b), hi - absorbed))
+            absorbed = hi
         lat, ker = timed(lambda: r(qd), with_kernel=True)
         plat, _ = timed(lambda: pr(qd))
         elat, _ = timed(lambda: P.assemble_evidence([idx], r.frame_ids, 6, 1, 0, True))
+        llat, lker = timed(lambda: lr(qd), with_kernel=True)
+        clat, _ = timed(lambda: lcl.retrieve(qd[0], 4))
+        n_clusters = lcl.export()["n_clusters"] if absorbed else 0
         glat = graph_ms(lambda: r(qd), [r.frame_ids, r.votes, r.n_out])
         gplat = graph_ms(lambda: pr(qd), [pr.frame_ids, pr.n_out])
         key_bytes = idx.n_rows * cfg.n_layers * cfg.n_kv_heads * cfg.head_dim * 2
         rows.append({"frames": F, "key_bytes": key_bytes, "retrieve_p50_ms": lat, "retrieve_graph_ms": glat,
                      "stream_kernel_ms": ker, "stream_kernel_gbs": key_bytes / (ker / 1e3) / 1e9,
-                     "pooled_p50_ms": plat, "pooled_graph_ms": gplat, "evidence_p50_ms": elat})
+                     "pooled_p50_ms": plat, "pooled_graph_ms": gplat, "evidence_p50_ms": elat,
+                     "lc_detailed_frames": F - absorbed - min(F, n_recent), "lc_retrieve_p50_ms": llat,
+                     "lc_stream_kernel_ms": lker, "lc_clusters": n_clusters, "lc_cluster_retrieve_p50_ms": clat})
         log(f"{F} frames: retrieve {lat:.3f} ms (graph {glat:.3f}, kernel {ker:.3f}), "
-            f"pooled {plat:.3f} ms (graph {gplat:.3f}), evidence {elat:.3f} ms")
-    return rows
+            f"pooled {plat:.3f} ms (graph {gplat:.3f}), evidence {elat:.3f} ms; "
+            f"compression on: retrieve {llat:.3f} ms over {F - absorbed - min(F, n_recent)} detailed frames, "
+            f"{n_clusters} clusters ranked in {clat:.3f} ms")
+    per_frame = [ms / n for ms, n in absorb_ms]
+    log("absorb ms per frame", [round(x, 4) for x in per_frame])
+    return rows, {"n_recent": n_recent, "n_detail": n_detail, "tau": tau,
+                  "absorb_ms_per_frame": per_frame}
 
 
 def cpu_model() -> str:
@@ -307,9 +336,10 @@ def main():
     torch.cuda.set_device(0)
     cfg = W.CONFIGS[args.config]
     if args.sweep:
-        rows = sweep(torch, P, cfg)
+        rows, lc = sweep(torch, P, cfg)
         print(json.dumps({"sweep": "history length", "workload": cfg.name, "top_k": cfg.top_k,
-                          "n_select": cfg.n_select, "data": "synthetic", "points": rows}), flush=True)
+                          "n_select": cfg.n_select, "data": "synthetic", "points": rows,
+                          "long_history_compression": lc}), flush=True)
         return
     specs, idxs, queries, host0 = build_streams(torch, P, cfg)
     r = P.Retriever(idxs, cfg.top_k, cfg.n_select, cfg.pool_mult, cfg.head_mode)
