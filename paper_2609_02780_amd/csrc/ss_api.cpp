@@ -122,7 +122,7 @@ Window candidates(const ss_index* x) {
   return w;
 }
 
-constexpr int kSampleRank = 48;      // rank r of the sample cut-off
+constexpr int kSampleRank = 32;      // rank r of the sample cut-off
 constexpr int kFullScanRows = 4096;  // at or below this many rows the sample is the whole list
 static_assert(kFullScanRows <= 16384, "a full-scan sample must fit the register select");
 constexpr int kChunkRows = 4096;
@@ -130,10 +130,10 @@ constexpr int kSampleChunk = 128;
 
 // Expected candidates per list: 3k (at least 1024), raised for very long lists
 // so the sample stays within the register select (kSampleMax rows).  The count
-// behaves like E Gamma(r) / r: with r = 48 it falls below k = E/3 with
-// probability 1e-10 per list and exceeds the capacity 2E with 2e-8; either case
+// behaves like E Gamma(r) / r: with r = 32 it falls below k = E/3 with
+// probability 1e-7 per list and exceeds the capacity 3E with 1e-10; either case
 // takes the exact fallback.  A smaller E keeps fewer tiles on the candidate
-// path of the streaming pass.
+// path of the streaming pass; a smaller r a smaller sample.
 constexpr int64_t kSampleMax = 16384;
 int64_t expected_candidates(int64_t n, int64_t kk) {
   const int64_t r = std::min<int64_t>(kk, kSampleRank);
@@ -146,7 +146,7 @@ struct StreamSizes {
 
 // Sample plan of one list.  With m sampled rows spread evenly over n rows and the
 // cut-off at the r-th largest sample score, about r n / m rows score at or above
-// it (the expected candidate count E).  r = min(k, 48); m = n gives an exact
+// it (the expected candidate count E).  r = min(k, 32); m = n gives an exact
 // cut (r = k) for small lists.
 StreamSizes plan_stream(int64_t n, int64_t f, int top_k) {
   StreamSizes z{};
@@ -168,7 +168,7 @@ StreamSizes plan_stream(int64_t n, int64_t f, int top_k) {
 
 int64_t candidate_cap(int top_k, int64_t n_max) {
   const int64_t kk = std::min<int64_t>(top_k, std::max<int64_t>(n_max, 1));
-  return std::max<int64_t>(2 * expected_candidates(n_max, kk), 4096);
+  return std::max<int64_t>(3 * expected_candidates(n_max, kk), 4096);
 }
 
 ss_status check_params(const ss_retrieve_params* p, int Hk) {

@@ -163,7 +163,7 @@ def test_fallback_too_few_candidates():
     L, Hq, Hk, d, T, F = 1, 1, 1, 64, 100, 1000
     n = F * T
     k = 512
-    r = min(k, 48)
+    r = min(k, 32)
     E = max(3 * k, 1024, -(-n * r // 16384))   # the library's expected candidate count
     m = max(r, -(-n * r // E))
     rows = ((2 * np.arange(m) + 1) * n) // (2 * m)
