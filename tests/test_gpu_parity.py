@@ -521,3 +521,88 @@ def test_p4_paper_settings_full_size_sampled():
     check_maxmin(pool, np.array(oidx.desc), cfg.n_select, out["frame_ids"][0, :int(out["n_out"][0])].astype(np.int64), rep)
     log(rep)
     assert out["frame_ids"][0, 0] in set(spec.planted)
+
+
+def test_c5_full_size_sampled():
+    """The 16-stream ragged batch at full size (odd streams compressed to 32
+    centroids) in one call, the benchmark's launch configuration: per stream
+    the vote total and the planted evidence; streams 0 (raw) and 1 (compressed,
+    oracle on the stored centroids) in depth: two lists against the oracle,
+    votes and mass from the GPU lists, pool and max-min validity."""
+    cfg = W.CONFIGS["C5"]
+    specs = W.stream_specs(cfg)
+    P = _P()
+    from parity import check_topk_list, check_pool, check_maxmin
+    gidxs, qs, host = [], [], {}
+    for sp in specs:
+        q = W.make_queries(cfg, 0, sp.stream)
+        rpf = 196 if sp.compress is None else 32
+        g = P.ShallowIndex(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, sp.n_frames,
+                           sp.n_frames * rpf)
+        keep = sp.stream in (0, 1)
+        blocks = []
+        for f0 in range(0, sp.n_frames, 600):
+            f1 = min(sp.n_frames, f0 + 600)
+            kb = W.frame_block_keys(cfg, sp, q, f0, f1)
+            g.append([dev_bf16(k) for k in kb], f1 - f0, 196, sp.compress)
+            if keep:
+                blocks.append(kb)
+        torch.cuda.synchronize()
+        if keep:
+            host[sp.stream] = [np.concatenate([b[l] for b in blocks], axis=1) for l in range(cfg.n_layers)]
+        gidxs.append(g)
+        qs.append(q)
+        log(f"C5 stream {sp.stream}: {sp.n_frames} frames, compressed {sp.compress is not None}")
+    r = P.Retriever(gidxs, cfg.top_k, cfg.n_select)
+    qd = [[dev_bf16(x) for x in q] for q in qs]
+    ids, v, m, n = r(qd)
+    torch.cuda.synchronize()
+    plain = ids.cpu().numpy().copy()
+    out = r.debug(qd)
+    np.testing.assert_array_equal(plain, out["frame_ids"])
+    NL = cfg.n_layers * cfg.n_q_heads
+    for s, sp in enumerate(specs):
+        assert out["list_stats"][s, :, 1].sum() == 0, f"stream {s} took the fallback"
+        rows = sp.n_frames * (196 if sp.compress is None else 32)
+        assert out["vote_hist"][s].sum() == NL * min(cfg.top_k, rows)
+        assert out["frame_ids"][s, 0] in set(sp.planted), f"stream {s}: first pick not planted"
+    qm_all = [O.query_means(q) for q in qs]
+    for s in (0, 1):
+        sp = specs[s]
+        keys = host.pop(s)
+        o = O.Index(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim)
+        if sp.compress is None:
+            o.append(keys, sp.n_frames, 196)
+        else:
+            ex = gidxs[s].export()
+            desc = [O.descriptor(O.decode_bf16(keys[-1][:, f * 196:(f + 1) * 196, :])) for f in range(sp.n_frames)]
+            np.testing.assert_allclose(ex["desc"], np.array(desc), atol=2e-6)
+            o.append_stored([ex["rows"][l] for l in range(cfg.n_layers)], [32] * sp.n_frames, desc)
+        del keys
+        rep = {}
+        qm = qm_all[s]
+        for (l, h) in [(0, 3), (cfg.n_layers - 1, cfg.n_q_heads - 1)]:
+            g = h // cfg.group
+            K = O.decode_bf16(o.rows(l)[g])
+            so = K @ qm[l][h] / math.sqrt(cfg.head_dim)
+            dsc = np.abs(K) @ np.abs(qm[l][h]) / math.sqrt(cfg.head_dim)
+            j = l * cfg.n_q_heads + h
+            kk = min(cfg.top_k, so.size)
+            check_topk_list(so, dsc, out["topk_pos"][s, j, :kk].astype(np.int64),
+                            out["topk_score"][s, j, :kk].astype(np.float64), kk, rep, name=f"C5 s{s} list {j}")
+        kk = min(cfg.top_k, o.n_rows)
+        lists = [out["topk_pos"][s, j, :kk].astype(np.int64) for j in range(NL)]
+        f_of = o.frame_of_row()
+        v_re = np.zeros(sp.n_frames, dtype=np.int64)
+        m_re = np.zeros(sp.n_frames)
+        for j, p in enumerate(lists):
+            np.add.at(v_re, f_of[p], 1)
+            np.add.at(m_re, f_of[p], out["topk_score"][s, j, :kk].astype(np.float64))
+        assert np.array_equal(out["vote_hist"][s, :sp.n_frames], v_re)
+        gm = out["mass_hist"][s, :sp.n_frames].astype(np.float64)
+        np.testing.assert_allclose(gm, m_re, rtol=1e-5, atol=1e-5)
+        pn = int(out["pool_n"][s])
+        pool = out["pool"][s, :pn].astype(np.int64)
+        check_pool(pool, v_re, gm, 1e-5 * np.abs(m_re) + 1e-5, cfg.pool_mult * cfg.n_select, rep)
+        check_maxmin(pool, np.array(o.desc), cfg.n_select, out["frame_ids"][s, :int(out["n_out"][s])].astype(np.int64), rep)
+        log(f"C5 stream {s}", rep)
