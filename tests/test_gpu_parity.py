@@ -606,3 +606,29 @@ def test_c5_full_size_sampled():
         check_pool(pool, v_re, gm, 1e-5 * np.abs(m_re) + 1e-5, cfg.pool_mult * cfg.n_select, rep)
         check_maxmin(pool, np.array(o.desc), cfg.n_select, out["frame_ids"][s, :int(out["n_out"][s])].astype(np.int64), rep)
         log(f"C5 stream {s}", rep)
+
+
+def test_c3_full_size():
+    """The compressed 10-minute workload at full size: 600 frames appended with
+    per-frame k-means in the benchmark's 600-frame block, a k-means audit of 24
+    frames spread over the stream, and retrieval parity (staged, in full) on
+    the stored centroids."""
+    cfg = W.CONFIGS["C3"]
+    spec = W.stream_specs(cfg)[0]
+    q = W.make_queries(cfg, 0, 0)
+    log("C3 build")
+    gidx, keys = _build_big(cfg, spec, q, compress=cfg.compress)
+    ex = gidx.export()
+    checked, exempt = _kmeans_audit(ex, keys, cfg, range(0, spec.n_frames, 25), *cfg.compress)
+    log("C3 k-means audit", checked, "checked", exempt, "exempt")
+    assert checked >= 0.5 * (checked + exempt)
+    o = O.Index(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim)
+    desc = [O.descriptor(O.decode_bf16(keys[-1][:, f * 196:(f + 1) * 196, :])) for f in range(spec.n_frames)]
+    np.testing.assert_allclose(ex["desc"], np.array(desc), atol=2e-6)
+    o.append_stored([ex["rows"][l] for l in range(cfg.n_layers)], [32] * spec.n_frames, desc)
+    del keys
+    out = debug_run([gidx], [q], cfg.top_k, cfg.n_select)
+    assert out["list_stats"][0, :, 1].sum() == 0
+    rep = staged_check(o, q, out, 0, cfg.top_k, cfg.n_select)
+    log("C3", rep)
+    assert out["frame_ids"][0, 0] in set(spec.planted)
