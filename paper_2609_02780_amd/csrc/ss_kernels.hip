@@ -4,7 +4,8 @@
 // stream, no host synchronisation:
 //   k_prep      mean query per (layer, head), pre-scaled, split into bf16 hi+lo
 //               and laid out as the MFMA B operand (lane-native).
-//   k_score<SAMPLE>   scores of an evenly spread sample of rows per list.
+//   k_sample    scores of an evenly spread sample of rows per list group
+//               (k_score<SAMPLE> in head mode 1).
 //   k_thresh    per list, the r-th largest sample score: the streaming cut-off.
 //   k_stream    THE HOT KERNEL: streams every bf16 key row from HBM once.
 //               The 16-row tiles of all lists form one sequence cut into one
@@ -475,6 +476,7 @@ struct ScoreArgs {
   // K_SAMPLE
   float* samp;
   int samp_stride;
+  int64_t samp_step[kMaxStreams];     // n 2^32 / m: sample u sits at row (u step + step/2) >> 32
   // K_STREAM
   const uint32_t* tau;
   uint32_t* cnt;
@@ -491,14 +493,16 @@ struct ScoreArgs {
   int64_t row0;
 };
 
+// Evenly spread sample: sample u of m sits at row ((u + 1/2) n / m) rounded
+// down, in 32.32 fixed point; the identity when m == n.
+__device__ __forceinline__ int64_t sample_row(int64_t step, int u) {
+  return (int64_t)(((uint64_t)u * (uint64_t)step + ((uint64_t)step >> 1)) >> 32);
+}
+
 // Row of the key index scored for unit u of stream s.
 template <int KIND>
 __device__ __forceinline__ int64_t unit_row(const ScoreArgs& a, int s, int u) {
-  if (KIND == K_SAMPLE) {
-    // evenly spread sample: row floor((2u+1) n / (2m)), the identity when m == n
-    const int64_t n = a.n[s], m = a.units[s];
-    return ((2 * (int64_t)u + 1) * n) / (2 * m);
-  } else if (KIND == K_FULL) {
+  if (KIND == K_SAMPLE) return sample_row(a.samp_step[s], u); else if (KIND == K_FULL) {
     return a.row0 + u;
   } else {
     return u;
@@ -734,6 +738,85 @@ __global__ __launch_bounds__(256) void k_stream(ScoreArgs a) {
       }
     }
     if (__any(lc > 0)) stage_flush(a, list, colv, col, kg, st, lc);
+    T += t1 - t0;
+  }
+}
+
+// Sample pass, head-mode 0: the m sampled rows of every (stream, layer, KV
+// head) list group, 16 to a tile, numbered one after another and cut into one
+// contiguous range per wave as in k_stream; a tile's rows are gathered with
+// coalesced loads (16 lanes per 256-byte row, four rows per instruction) into
+// the wave's LDS tile and scored with the same arithmetic as k_stream.
+template <int D>
+__global__ __launch_bounds__(256) void k_sample(ScoreArgs a) {
+  constexpr int CPR = D / 8, TCH = 16 * CPR, NI = TCH / kWave, KS = D / 32;
+  __shared__ u32x4 tiles[4][TCH];
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
+  u32x4* lt_ = tiles[wave];
+  const int64_t nw = (int64_t)gridDim.x * 4, gw = (int64_t)blockIdx.x * 4 + wave;
+  const int64_t total = a.tile_base[a.S];
+  const int64_t T1 = (gw + 1) * total / nw;
+  int64_t T = gw * total / nw;
+  while (T < T1) {
+    int s = 0;
+    while (T >= a.tile_base[s + 1]) ++s;
+    const int64_t rem = T - a.tile_base[s];
+    const int nt = a.ntile[s];
+    const int lg = (int)(rem / nt);
+    const int t0 = (int)(rem - (int64_t)lg * nt);
+    const int t1 = (int)min<int64_t>(nt, t0 + (T1 - T));
+    const int g = lg % a.Hk, l = lg / a.Hk;
+    const int n = a.n[s], m = a.units[s];
+    const int64_t step = a.samp_step[s];
+    const bool colv = col < a.G;
+    const int list = s * a.NL + l * a.Hq + g * a.G + col;
+    const u32x4* qb = a.qB + ((size_t)(s * a.L + l) * a.Hk + g) * (2 * KS * kWave);
+    u32x4 bh[KS], bl[KS];
+#pragma unroll
+    for (int i = 0; i < KS; ++i) {
+      bh[i] = qb[i * kWave + lane];
+      bl[i] = qb[(KS + i) * kWave + lane];
+    }
+    const uint16_t* seg = a.keys[s] + ((size_t)l * a.Hk + g) * (size_t)a.stride[s] * D;
+    const __amdgpu_buffer_rsrc_t rsrc =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(seg), (short)0, n * D * 2, 0x00020000);
+    // chunk q = 64 i + lane of tile t: sample t 16 + q / CPR, chunk q mod CPR
+    auto load = [&](int t, u32x4 (&V)[NI]) {
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const int q = i * kWave + lane, u = t * kTile + q / CPR;
+        const uint32_t off = (t < t1 && u < m)
+                                 ? (uint32_t)sample_row(step, u) * (CPR * 16) + (q % CPR) * 16
+                                 : 0x80000000u;
+        V[i] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, kAuxNT);
+      }
+    };
+    u32x4 V[NI];
+    load(t0, V);
+    for (int t = t0; t < t1; ++t) {
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const int q = i * kWave + lane, R = q >> 4, C = q & 15;
+        lt_[R * 16 + (C ^ (R & 15))] = V[i];
+      }
+      __builtin_amdgcn_wave_barrier();
+      load(t + 1, V);
+      u32x4 A[KS];
+#pragma unroll
+      for (int i = 0; i < KS; ++i) {
+        const int q = rl * CPR + 4 * i + kg, R = q >> 4, C = q & 15;
+        A[i] = lt_[R * 16 + (C ^ (R & 15))];
+      }
+      __builtin_amdgcn_wave_barrier();
+      const f32x4 acc = score_hilo<KS>(A, bh, bl);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int u = t * kTile + 4 * kg + j;
+        if (colv && u < m) a.samp[(size_t)list * a.samp_stride + u] = acc[j] + 0.0f;
+      }
+    }
     T += t1 - t0;
   }
 }
@@ -2200,6 +2283,7 @@ ScoreArgs make_score_args(const RetrievePlan& p, int kind) {
     a.stride[s] = p.st[s].row_stride;
     a.n[s] = p.st[s].n;
     a.units[s] = kind == K_SAMPLE ? p.st[s].m : p.st[s].n;
+    a.samp_step[s] = p.st[s].m > 0 ? (int64_t)(((unsigned __int128)p.st[s].n << 32) / (unsigned)p.st[s].m) : 0;
     a.item_base[s] = items;
     items += p.L * p.ngs * cdiv(a.units[s], a.chunk);
     a.full_base[s] = p.full_base[s];
@@ -2281,7 +2365,22 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   la.listexp = p.listexp;
   const int lists = p.S * p.NL;
   // 2. sample scores, 3. thresholds
-  launch_score<D, K_SAMPLE>(make_score_args(p, K_SAMPLE), p.head_mode, 4096, st);
+  if (p.head_mode == 0) {
+    ScoreArgs a = make_score_args(p, K_SAMPLE);
+    int64_t tiles = 0;   // sample tiles of every (stream, layer, KV head)
+    for (int s = 0; s < p.S; ++s) {
+      a.tile_base[s] = tiles;
+      a.ntile[s] = cdiv(p.st[s].m, kTile);
+      tiles += (int64_t)p.L * p.Hk * a.ntile[s];
+    }
+    a.tile_base[p.S] = tiles;
+    if (tiles > 0) {
+      const int grid = (int)std::min<int64_t>(stream_grid<D, false>(), std::max<int64_t>(1, tiles / 4));
+      hipLaunchKernelGGL(k_sample<D>, dim3(grid), dim3(256), 0, st, a);
+    }
+  } else {
+    launch_score<D, K_SAMPLE>(make_score_args(p, K_SAMPLE), p.head_mode, 4096, st);
+  }
   hipLaunchKernelGGL(k_thresh, dim3(lists), dim3(1024), 0, st, la);
   // 4. streaming pass over every key row
   if (p.ev_start) (void)hipEventRecord(p.ev_start, st);

@@ -166,7 +166,9 @@ def test_fallback_too_few_candidates():
     r = min(k, 32)
     E = max(3 * k, 1024, -(-n * r // 16384))   # the library's expected candidate count
     m = max(r, -(-n * r // E))
-    rows = ((2 * np.arange(m) + 1) * n) // (2 * m)
+    step = (n << 32) // m                     # the library's sample lattice, 32.32 fixed point
+    rows = (np.arange(m, dtype=np.uint64) * np.uint64(step) + np.uint64(step >> 1)) >> np.uint64(32)
+    rows = rows.astype(np.int64)
     rng = np.random.default_rng(11)
     x = rng.standard_normal((1, n, d)).astype(np.float32) * 0.01
     x[0, rows, 0] = 5.0 + rng.random(m).astype(np.float32)      # only sampled rows score high
