@@ -105,7 +105,9 @@ typedef struct {
  * member counts int32 [L_s][H_kv][max_rows]; descriptors fp32
  * [max_frames][H_kv*d]; pooled keys fp32 [max_frames][L_s][H_kv][d] (each
  * frame's mean raw key per layer and KV head); frame row offsets int32
- * [max_frames+1]. */
+ * [max_frames+1]; a 16-byte statistics block (the largest raw key magnitude
+ * appended, which bounds every score and so fixes the fixed-point scale of
+ * the attention mass). */
 size_t ss_index_required_bytes(const ss_index_desc* desc);
 
 /* Create an empty index over a caller-owned device arena of at least

@@ -47,7 +47,7 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 inline bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 struct Layout {
-  size_t keys, counts, desc, pooled, off, total;
+  size_t keys, counts, desc, pooled, off, stats, total;
 };
 
 // Check an index shape; fills `why` on failure.
@@ -97,6 +97,8 @@ Layout layout(const ss_index_desc& d) {
   off = align256(off + (size_t)d.max_frames * lg * d.head_dim * 4);
   L.off = off;
   off = align256(off + ((size_t)d.max_frames + 1) * 4);
+  L.stats = off;
+  off = align256(off + 16);
   L.total = off;
   return L;
 }
@@ -223,6 +225,7 @@ void build_plan(ss::RetrievePlan& p, ss_index* const* idx, int s0, int S, const 
     sp.desc = x->dev.desc + w.f_lo * (int64_t)d.n_kv_heads * d.head_dim;
     sp.frame0 = w.f_lo;
     sp.row0 = w.r_lo;
+    sp.kmax = x->dev.stats;
     sp.row_stride = (int32_t)x->desc.max_rows;
     sp.n = z.n;
     sp.f = z.f;
@@ -667,6 +670,7 @@ ss_status ss_index_create(const ss_index_desc* desc, void* dev_arena, size_t are
   x->dev.counts = reinterpret_cast<int32_t*>(b + L.counts);
   x->dev.desc = reinterpret_cast<float*>(b + L.desc);
   x->dev.pooled = reinterpret_cast<float*>(b + L.pooled);
+  x->dev.stats = reinterpret_cast<uint32_t*>(b + L.stats);
   x->dev.frame_off = reinterpret_cast<int32_t*>(b + L.off);
   x->n_frames = 0;
   x->n_rows = 0;
@@ -737,7 +741,10 @@ ss_status ss_index_append(ss_index* idx, const void* const* layer_keys, int32_t 
   a.n_iters = compress ? compress->n_iters : 0;
   for (int l = 0; l < d.n_layers; ++l) a.src[l] = static_cast<const uint16_t*>(layer_keys[l]);
   a.dst = idx->dev;
-  const hipError_t e = ss::launch_append(a, compress != nullptr, static_cast<hipStream_t>(stream));
+  hipError_t e = hipSuccess;
+  if (idx->n_frames == 0)   // the key-magnitude statistic starts with the first append
+    e = ss::launch_zero32(reinterpret_cast<int32_t*>(idx->dev.stats), 1, static_cast<hipStream_t>(stream));
+  if (e == hipSuccess) e = ss::launch_append(a, compress != nullptr, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(SS_ERR_DEVICE, "append launch failed: %s", hipGetErrorString(e));
   if (first_frame_id) *first_frame_id = idx->n_frames;
   for (int f = 1; f <= n_frames; ++f) idx->off.push_back(idx->n_rows + (int64_t)f * rpf);

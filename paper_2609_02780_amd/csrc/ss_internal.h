@@ -32,6 +32,7 @@ struct IndexDev {
   float* desc;          // [max_frames][H_kv*d]
   float* pooled;        // [max_frames][L][H_kv][d] mean raw key per (frame, layer, KV head)
   int32_t* frame_off;   // [max_frames+1]
+  uint32_t* stats;      // [0]: the largest |raw key element| appended so far (float bits)
 };
 
 // ---------------------------------------------------------------------------
@@ -68,6 +69,7 @@ struct StreamPlan {
   int32_t rpf;           // rows per frame when every frame has the same count, else 0
   int64_t frame0;        // first candidate frame (earlier ones are in long-term clusters)
   int64_t row0;          // its first row; keys, frame_off and desc above start there
+  const uint32_t* kmax;  // the index's largest |key element| (float bits, device)
   float qscale;          // 1 / (n_q sqrt(d)) (head_mode 0), further / H_q (head_mode 1)
   const uint16_t* q[kMaxLayers];  // per layer query pointer [H_q][n_q][d]
 };
@@ -93,15 +95,12 @@ struct RetrievePlan {
   int32_t* flag;         // [S*NL]
   float* samp;           // [S*NL][m_max]
   uint64_t* cand;        // [S*NL][cap]
-  int32_t* run_f;        // [S*NL][k_max] per-frame runs of each list's selected rows
-  int32_t* run_c;
-  int64_t* run_fx;       // fixed-point score sums at scale 2^listexp
-  int32_t* nruns;        // [S*NL]
-  int32_t* listexp;      // [S*NL]
+  float* qcol;           // [S][L][H_kv][16] L1 norms of the scaled query columns
+  int32_t* sexp;         // [S] fixed-point exponent of each stream's attention mass
   float* full;           // fallback scores, per stream base full_base[s]
   int64_t full_base[kMaxStreams];
-  int32_t* votes;        // [S][f_max]
-  int64_t* massfx;       // [S][f_max]
+  int32_t* votes;        // [S][f_max] per-frame votes
+  int64_t* massfx;       // [S][f_max] per-frame mass at scale 2^sexp
   uint64_t* rec_hi;      // [S][f_max] compacted (votes, mass, frame) records
   uint64_t* rec_lo;
   int32_t* pool_ids;     // [S][pool]

@@ -372,6 +372,7 @@ struct PrepArgs {
   int nq[kMaxStreams];
   float qscale[kMaxStreams];
   u32x4* qB;       // [S][L][H_kv][2][D/32][64]
+  float* qcol;     // [S][L][H_kv][16] L1 norm of each scaled B column, or null
 };
 
 // One block of 8*D threads per (stream, layer, KV head): thread (tg, col, ec)
@@ -442,9 +443,11 @@ __global__ __launch_bounds__(8 * D) void k_prep(PrepArgs a) {
     acc[w] = x;
   }
   u32x4 hi, lo;
+  float l1 = 0.f;
 #pragma unroll
   for (int w = 0; w < 4; ++w) {
     const float x0 = acc[2 * w] * scale, x1 = acc[2 * w + 1] * scale;
+    l1 += fabsf(x0) + fabsf(x1);
     const uint16_t a0 = bf16_rne(x0), a1 = bf16_rne(x1);
     const uint16_t b0 = bf16_rne(x0 - __uint_as_float((uint32_t)a0 << 16));
     const uint16_t b1 = bf16_rne(x1 - __uint_as_float((uint32_t)a1 << 16));
@@ -455,6 +458,10 @@ __global__ __launch_bounds__(8 * D) void k_prep(PrepArgs a) {
   const int i = ec >> 2, lane = col + 16 * (ec & 3);
   out[(0 * KS + i) * kWave + lane] = hi;
   out[(1 * KS + i) * kWave + lane] = lo;
+  // the NE threads of a column are adjacent lanes of one wave
+#pragma unroll
+  for (int o = NE / 2; o > 0; o >>= 1) l1 += __shfl_xor(l1, o);
+  if (a.qcol && ec == 0) a.qcol[((size_t)pair * a.Hk + g) * 16 + col] = l1;
 }
 
 // ---------------------------------------------------------------------------
@@ -1025,11 +1032,13 @@ struct ListArgs {
   uint32_t* cnt;
   int32_t* flag;
   const uint64_t* cand;
-  int32_t* run_f;      // [list][k_max] per-frame runs of the selected rows
-  int32_t* run_c;
-  int64_t* run_fx;     // fixed-point score sums at scale 2^listexp
-  int32_t* nruns;      // [list]
-  int32_t* listexp;    // [list]
+  // per-frame votes and fixed-point attention mass of each stream (window-relative frames)
+  int f_max;
+  int32_t* votes_g;    // [S][f_max]
+  int64_t* massfx_g;   // [S][f_max] score sums at scale 2^sexp[s]
+  int32_t* sexp;       // [S]
+  const float* qcol;   // [S][L][H_kv][16] query column L1 norms
+  const uint32_t* kmax[kMaxStreams];   // the index's largest |key element| (float bits)
   // exact fallback: the list's scores are recomputed into `full`
   float* full;
   int L, Hq, Hk, G, head_mode;
@@ -1053,17 +1062,63 @@ __device__ __forceinline__ int frame_of_row(const ListArgs& a, int s, uint32_t r
   return lo;
 }
 
-// The sample (m <= kThrItems * 1024 scores) sits in registers.
+// Fixed-point exponent of a stream's attention mass.  A score is a dot product
+// of a scaled query column with a key row, so |score| <= |q|_1 * max|K| (head
+// mode 1 sums the KV heads' columns); with 2% headroom for fp32 rounding this
+// bounds all E = NL * kk selected scores of the stream, and at scale 2^x with
+// x = 61 - e - c (bound < 2^e, E <= 2^c) any sum of them stays below 2^61.
+__device__ void stream_exponent(const ListArgs& a, int s, float* red) {
+  const int L = a.L, Hk = a.Hk;
+  const float* qc = a.qcol + (size_t)s * L * Hk * 16;
+  float b = 0.f;
+  if (a.head_mode == 0) {
+    for (int i = threadIdx.x; i < L * Hk * 16; i += blockDim.x) b = fmaxf(b, qc[i]);
+  } else {
+    for (int l = threadIdx.x; l < L; l += blockDim.x) {
+      float t = 0.f;
+      for (int g = 0; g < Hk; ++g) t += qc[(l * Hk + g) * 16];
+      b = fmaxf(b, t);
+    }
+  }
+  b = block_max(b, red);
+  if (threadIdx.x == 0) {
+    const float bound = b * __uint_as_float(*a.kmax[s]) * 1.02f;
+    const int E = a.NL * a.kk[s];
+    int x = 120;                          // all scores are zero
+    if (!(bound <= 3.0e38f)) {
+      x = -120;                           // non-finite keys or queries
+    } else if (bound > 0.f) {
+      int e;
+      frexpf(bound, &e);                  // bound < 2^e
+      const int c = (E > 1) ? 32 - __clz(E - 1) : 0;
+      x = min(120, max(-120, 61 - e - c));
+    }
+    a.sexp[s] = x;
+  }
+}
+
+// The sample (m <= kThrItems * 1024 scores) sits in registers.  The blocks of a
+// stream also clear its frame accumulators, and its first block fixes the
+// stream's mass exponent.
 __global__ __launch_bounds__(1024) void k_thresh(ListArgs a) {
   __shared__ uint32_t hist[512];
   __shared__ uint32_t res[4];
   __shared__ uint32_t mm[32];
-  const int list = blockIdx.x, s = list / a.NL;
+  const int list = blockIdx.x, s = list / a.NL, ll = list - s * a.NL;
   const int m = a.m[s], r = a.r[s];
   if (threadIdx.x == 0) {
     a.cnt[list] = 0;
     a.flag[list] = 0;
   }
+  {
+    int32_t* vg = a.votes_g + (size_t)s * a.f_max;
+    int64_t* mg = a.massfx_g + (size_t)s * a.f_max;
+    for (int f = ll * 1024 + threadIdx.x; f < a.f[s]; f += a.NL * 1024) {
+      vg[f] = 0;
+      mg[f] = 0;
+    }
+  }
+  if (ll == 0) stream_exponent(a, s, reinterpret_cast<float*>(mm));
   if (m == 0 || r == 0) {
     if (threadIdx.x == 0) a.tau[list] = 0xFFFFFFFFu;
     return;
@@ -1088,30 +1143,19 @@ __global__ __launch_bounds__(1024) void k_thresh(ListArgs a) {
 // ---------------------------------------------------------------------------
 // k_select: exact top-k of a list's candidates
 // ---------------------------------------------------------------------------
-// `sel` holds the kk selected composite keys in any order; `mxa` is the largest
-// |score| among them.  Adds the rows up per frame: one run record per frame
-// with its row count and the fixed-point sum of its scores at the list's own
-// scale 2^x (|sum| < 2^61 for up to E = NL * kk entries of magnitude <= mxa).
-// Writes the debug copy in rank order.  `lv`/`lm` are LDS frame accumulators
-// (kVoteLds entries); longer streams sort by row and walk the runs instead.
-__device__ void finish_list(const ListArgs& a, int list, uint64_t* sel, int kk, float mxa,
+// `sel` holds the kk selected composite keys in any order.  Adds them into the
+// stream's per-frame votes and fixed-point mass (scale 2^sexp, integer sums, so
+// the totals do not depend on the order of the additions).  Streams of up to
+// kVoteLds frames first gather the list's counts in LDS (`lv`/`lm`), so each
+// (list, frame) pair costs one global atomic.  Writes the debug copy in rank
+// order.
+__device__ void finish_list(const ListArgs& a, int list, uint64_t* sel, int kk,
                             int32_t* lv, long long* lm) {
-  __shared__ uint32_t nrun;
   const int s = list / a.NL;
   const int F = a.f[s];
-  int xl = 127;  // no entries: never the smallest exponent of a stream
-  if (kk > 0) {
-    xl = 120;
-    if (mxa > 0.f) {
-      int e;
-      frexpf(mxa, &e);                                       // mxa < 2^e
-      const int E = a.NL * kk;
-      const int c = (E > 1) ? 32 - __clz(E - 1) : 0;        // E <= 2^c
-      xl = min(120, max(-120, 61 - e - c));
-    }
-  }
-  if (threadIdx.x == 0) nrun = 0;
-  const size_t ob = (size_t)list * a.k_max;
+  const int xs = a.sexp[s];
+  int32_t* vg = a.votes_g + (size_t)s * a.f_max;
+  unsigned long long* mg = reinterpret_cast<unsigned long long*>(a.massfx_g + (size_t)s * a.f_max);
   if (F <= kVoteLds) {
     for (int f = threadIdx.x; f < F; f += blockDim.x) { lv[f] = 0; lm[f] = 0; }
     __syncthreads();
@@ -1120,49 +1164,22 @@ __device__ void finish_list(const ListArgs& a, int list, uint64_t* sel, int kk, 
       const int f = frame_of_row(a, s, key_row(k));
       atomicAdd(&lv[f], 1);
       atomicAdd(reinterpret_cast<unsigned long long*>(&lm[f]),
-                (unsigned long long)llrint(ldexp((double)key_score(k), xl)));
+                (unsigned long long)llrint(ldexp((double)key_score(k), xs)));
     }
     __syncthreads();
     for (int f = threadIdx.x; f < F; f += blockDim.x) {
       if (lv[f] > 0) {
-        const uint32_t slot = atomicAdd(&nrun, 1u);
-        a.run_f[ob + slot] = f;
-        a.run_c[ob + slot] = lv[f];
-        a.run_fx[ob + slot] = lm[f];
+        atomicAdd(&vg[f], lv[f]);
+        atomicAdd(&mg[f], (unsigned long long)lm[f]);
       }
     }
   } else {
-    // long streams: order the selected rows by counting, then one record per run
-    int32_t* rank_row = lv;  // kMaxTopK <= kVoteLds entries
-    __syncthreads();
     for (int e = threadIdx.x; e < kk; e += blockDim.x) {
-      const uint32_t my = key_row(sel[e]);
-      int rank = 0;
-      for (int e2 = 0; e2 < kk; ++e2) rank += key_row(sel[e2]) < my;
-      rank_row[rank] = e;
+      const uint64_t k = sel[e];
+      const int f = frame_of_row(a, s, key_row(k));
+      atomicAdd(&vg[f], 1);
+      atomicAdd(&mg[f], (unsigned long long)llrint(ldexp((double)key_score(k), xs)));
     }
-    __syncthreads();
-    for (int i = threadIdx.x; i < kk; i += blockDim.x) {
-      const int f = frame_of_row(a, s, key_row(sel[rank_row[i]]));
-      const int fp = i > 0 ? frame_of_row(a, s, key_row(sel[rank_row[i - 1]])) : -1;
-      if (f != fp) {
-        int len = 0;
-        long long sum = 0;
-        while (i + len < kk && frame_of_row(a, s, key_row(sel[rank_row[i + len]])) == f) {
-          sum += llrint(ldexp((double)key_score(sel[rank_row[i + len]]), xl));
-          ++len;
-        }
-        const uint32_t slot = atomicAdd(&nrun, 1u);
-        a.run_f[ob + slot] = f;
-        a.run_c[ob + slot] = len;
-        a.run_fx[ob + slot] = sum;
-      }
-    }
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    a.nruns[list] = (int32_t)nrun;
-    a.listexp[list] = xl;
   }
   if (a.dbg_pos) {
     int32_t* dp = a.dbg_pos + (size_t)list * a.top_k;
@@ -1191,7 +1208,6 @@ __device__ void fallback_list(const ListArgs& a, int list, uint64_t* sel, int32_
   constexpr int KS = D / 32;
   __shared__ uint32_t ngt_sh;
   __shared__ int scan_sh[17];
-  __shared__ float redm[16];
   const int s = list / a.NL, ll = list - s * a.NL;
   const int kk = a.kk[s], n = a.n[s];
   float* full = a.full + a.full_base[s] + (int64_t)ll * n;
@@ -1254,7 +1270,6 @@ __device__ void fallback_list(const ListArgs& a, int list, uint64_t* sel, int32_
   if (threadIdx.x == 0) ngt_sh = 0;
   __syncthreads();
   int eq_taken = 0;
-  float m = 0.f;
   for (int b0 = 0; b0 < n; b0 += blockDim.x) {
     const int i = b0 + threadIdx.x;
     uint32_t u = 0;
@@ -1267,18 +1282,14 @@ __device__ void fallback_list(const ListArgs& a, int list, uint64_t* sel, int32_
     if (gt) {
       const uint32_t slot = atomicAdd(&ngt_sh, 1u);
       if (slot < (uint32_t)kMaxTopK) sel[slot] = mk_key(u, (uint32_t)i);
-      m = fmaxf(m, fabsf(ord_f32(u)));
     }
     int tot;
     const int pre = block_excl_scan(eq ? 1 : 0, scan_sh, tot);
-    if (eq && eq_taken + pre < need_eq) {
-      sel[ngreater + eq_taken + pre] = mk_key(u, (uint32_t)i);
-      m = fmaxf(m, fabsf(ord_f32(u)));
-    }
+    if (eq && eq_taken + pre < need_eq) sel[ngreater + eq_taken + pre] = mk_key(u, (uint32_t)i);
     eq_taken += tot;
   }
-  const float mxa = block_max(m, redm);
-  finish_list(a, list, sel, kk, mxa, lv, lm);
+  __syncthreads();
+  finish_list(a, list, sel, kk, lv, lm);
 }
 
 template <int D>
@@ -1293,7 +1304,7 @@ __global__ __launch_bounds__(1024) void k_select(ListArgs a) {
   const int list = blockIdx.x, s = list / a.NL;
   const int kk = a.kk[s];
   if (kk == 0) {
-    finish_list(a, list, sel, 0, 0.f, lv, lm);
+    finish_list(a, list, sel, 0, lv, lm);
     return;
   }
   const uint32_t c = a.cnt[list];
@@ -1310,7 +1321,6 @@ __global__ __launch_bounds__(1024) void k_select(ListArgs a) {
   const int n = (int)c;
   const uint64_t* src = a.cand + (size_t)list * a.cap;
   if (threadIdx.x == 0) ngather = 0;
-  float mxa;
   if (n <= 1024 * kSelItems) {
     // scores (high halves) and inverted rows in registers: the k-th score, then
     // the cut among the ties at that score by row
@@ -1349,26 +1359,21 @@ __global__ __launch_bounds__(1024) void k_select(ListArgs a) {
         if (slot < (uint32_t)kMaxTopK) sel[slot] = ((uint64_t)u[it] << 32) | w[it];
       }
     }
-    mxa = fmaxf(fabsf(ord_f32(vstar)), fabsf(ord_f32(mx)));  // the selected scores span [v*, max]
   } else {
     // large candidate sets: radix select over the keys in global memory
     __syncthreads();
     const uint64_t cut = radix_select_u64([&](int i) { return src[i]; }, n, (uint32_t)kk, hist, res);
     __syncthreads();
-    float m = 0.f;
     for (int i = threadIdx.x; i < n; i += blockDim.x) {
       const uint64_t x = src[i];
       if (x >= cut) {
         const uint32_t slot = atomicAdd(&ngather, 1u);
         if (slot < (uint32_t)kMaxTopK) sel[slot] = x;
-        m = fmaxf(m, fabsf(key_score(x)));
       }
     }
-    __shared__ float redm[16];
-    mxa = block_max(m, redm);
   }
   __syncthreads();
-  finish_list(a, list, sel, kk, mxa, lv, lm);
+  finish_list(a, list, sel, kk, lv, lm);
 }
 
 // ---------------------------------------------------------------------------
@@ -1378,13 +1383,9 @@ struct VoteArgs {
   int NL, k_max, pool, f_max, hist_stride;
   int32_t f[kMaxStreams];
   int64_t frame0[kMaxStreams];   // debug outputs are indexed by absolute frame id
-  const int32_t* run_f;
-  const int32_t* run_c;
-  const int64_t* run_fx;
-  const int32_t* nruns;
-  const int32_t* listexp;
-  int32_t* votes_g;     // [S][f_max] (frames beyond the LDS capacity)
-  int64_t* massfx_g;    // [S][f_max]
+  const int32_t* votes_g;    // [S][f_max] per-frame votes
+  const int64_t* massfx_g;   // [S][f_max] per-frame mass at scale 2^sexp[s]
+  const int32_t* sexp;       // [S]
   uint64_t* rec_hi;     // [S][f_max] compacted records
   uint64_t* rec_lo;
   int32_t* pool_ids;    // [S][pool]
@@ -1397,88 +1398,27 @@ struct VoteArgs {
   int32_t* dbg_pool_n;
 };
 
-// Votes and attention mass of every frame from the lists' runs.  Masses are
-// summed in 64-bit fixed point at the stream scale 2^x (the smallest list
-// exponent; a run's sum moves to it by an arithmetic shift), so the result does
-// not depend on the order of the additions.  The pool holds the voted frames of
-// rank < pool by (votes desc, mass desc, frame asc), ranked by counting.
+// The pool: the voted frames of rank < pool by (votes desc, mass desc, frame
+// asc) from the per-frame votes and fixed-point masses that the selection
+// blocks accumulated, ranked by counting.
 __global__ __launch_bounds__(1024) void k_votes_pool(VoteArgs a) {
-  __shared__ int32_t sv[kVoteLds];
-  __shared__ int64_t sm[kVoteLds];
   __shared__ uint64_t shi[kPoolSort];
   __shared__ uint64_t slo[kPoolSort];
-  __shared__ int32_t roff[kMaxListsPerStream + 1];
-  __shared__ int scan_sh[17];
-  __shared__ int xmin_sh;
   __shared__ uint32_t nvoted_sh;
   const int s = blockIdx.x;
-  const int F = a.f[s], NL = a.NL;
-  const bool lds = F <= kVoteLds;
-  int32_t* votes = lds ? sv : a.votes_g + (size_t)s * a.f_max;
-  int64_t* massfx = lds ? sm : a.massfx_g + (size_t)s * a.f_max;
-  const int32_t* nr = a.nruns + (size_t)s * NL;
-  const int32_t* lx = a.listexp + (size_t)s * NL;
-  if (threadIdx.x == 0) { xmin_sh = 127; nvoted_sh = 0; }
-  for (int f = threadIdx.x; f < F; f += blockDim.x) {
-    votes[f] = 0;
-    massfx[f] = 0;
-  }
-  // run offsets (exclusive scan of the per-list run counts) and the stream exponent
-  int run_total = 0;
-  __threadfence();
+  const int F = a.f[s];
+  const int32_t* votes = a.votes_g + (size_t)s * a.f_max;
+  const int64_t* massfx = a.massfx_g + (size_t)s * a.f_max;
+  if (threadIdx.x == 0) nvoted_sh = 0;
   __syncthreads();
-  for (int b0 = 0; b0 < NL; b0 += blockDim.x) {
-    const int j = b0 + threadIdx.x;
-    const int c = j < NL ? nr[j] : 0;
-    if (j < NL) atomicMin(&xmin_sh, lx[j]);
-    int tot;
-    const int pre = block_excl_scan(c, scan_sh, tot);
-    if (j < NL) roff[j] = run_total + pre;
-    run_total += tot;
-  }
-  if (threadIdx.x == 0) roff[NL] = run_total;
-  __syncthreads();
-  const int xexp = xmin_sh;
-  constexpr int VB = 4;
-  for (int bb = 0; bb < run_total; bb += VB * blockDim.x) {
-    int rf[VB], rc[VB], sh_[VB];
-    long long rx[VB];
-#pragma unroll
-    for (int u = 0; u < VB; ++u) {
-      const int i = bb + u * blockDim.x + threadIdx.x;
-      rf[u] = -1;
-      if (i < run_total) {
-        int lo = 0, hi = NL - 1;  // list j with roff[j] <= i < roff[j+1]
-        while (lo < hi) {
-          const int mid = (lo + hi + 1) >> 1;
-          if (roff[mid] <= i) lo = mid; else hi = mid - 1;
-        }
-        const size_t o = ((size_t)s * NL + lo) * a.k_max + (i - roff[lo]);
-        rf[u] = a.run_f[o];
-        rc[u] = a.run_c[o];
-        rx[u] = a.run_fx[o];
-        sh_[u] = lx[lo] - xexp;
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < VB; ++u) {
-      if (rf[u] >= 0) {
-        atomicAdd(&votes[rf[u]], rc[u]);
-        const long long v = sh_[u] >= 63 ? (rx[u] < 0 ? -1 : 0) : (rx[u] >> sh_[u]);
-        atomicAdd(reinterpret_cast<unsigned long long*>(&massfx[rf[u]]), (unsigned long long)v);
-      }
-    }
-  }
-  __threadfence();
-  __syncthreads();
-  const double inv = ldexp(1.0, -xexp);
+  const double inv = ldexp(1.0, -a.sexp[s]);
   // voted frames as records, any order: hi = votes:32 | mass_hi:32,
   // lo = mass_lo:32 | ~frame:32, compared descending
   uint64_t* rh = a.rec_hi + (size_t)s * a.f_max;
   uint64_t* rl = a.rec_lo + (size_t)s * a.f_max;
   for (int f = threadIdx.x; f < F; f += blockDim.x) {
-    const int v = __hip_atomic_load(&votes[f], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const int64_t mf = __hip_atomic_load(&massfx[f], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int v = votes[f];
+    const int64_t mf = massfx[f];
     if (a.dbg_vote_hist) {
       a.dbg_vote_hist[(size_t)s * a.hist_stride + a.frame0[s] + f] = v;
       a.dbg_mass_hist[(size_t)s * a.hist_stride + a.frame0[s] + f] = (float)((double)mf * inv);
@@ -1757,6 +1697,7 @@ __global__ __launch_bounds__(256) void k_unit_means(AppendArgs a) {
   const uint16_t* src = a.src[l];
   float vals[4];
   float ss = 0.f;
+  uint32_t amax = 0;   // largest |key element| (the bits of a non-negative float order as integers)
   for (int k = 0; k < 4; ++k) {
     const int e = threadIdx.x + k * 256;
     vals[k] = 0.f;
@@ -1764,11 +1705,17 @@ __global__ __launch_bounds__(256) void k_unit_means(AppendArgs a) {
       const int g = e / D, ee = e % D;
       const uint16_t* p = src + ((int64_t)g * nT + (int64_t)f * T) * D + ee;
       float acc = 0.f;
-      for (int t = 0; t < T; ++t) acc += __uint_as_float((uint32_t)p[(int64_t)t * D] << 16);
+      for (int t = 0; t < T; ++t) {
+        const uint32_t bits = (uint32_t)p[(int64_t)t * D] << 16;
+        acc += __uint_as_float(bits);
+        amax = max(amax, bits & 0x7FFFFFFFu);
+      }
       vals[k] = acc / (float)T;
       ss = fmaf(vals[k], vals[k], ss);
     }
   }
+  amax = wave_max_u32(amax);
+  if ((threadIdx.x & 63) == 0) atomicMax(a.dst.stats, amax);
   float* pooled = a.dst.pooled + ((a.frame0 + f) * a.L + l) * (int64_t)dim;
   for (int k = 0; k < 4; ++k) {
     const int e = threadIdx.x + k * 256;
@@ -2344,6 +2291,7 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
       }
       for (int s = 0; s < p.S; ++s) { a.nq[s] = p.st[s].nq; a.qscale[s] = p.st[s].qscale; }
       a.qB = reinterpret_cast<u32x4*>(p.qB);
+      a.qcol = p.qcol;
       hipLaunchKernelGGL(k_prep<D>, dim3(cnt * p.Hk), dim3(8 * D), 0, st, a);
     }
   }
@@ -2354,6 +2302,7 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
     la.full_base[s] = p.full_base[s];
     la.f[s] = p.st[s].f; la.rpf[s] = p.st[s].rpf; la.frame_off[s] = p.st[s].frame_off;
     la.row0[s] = p.st[s].row0;
+    la.kmax[s] = p.st[s].kmax;
   }
   la.samp = p.samp; la.samp_stride = p.m_max; la.tau = p.tau; la.cnt = p.cnt; la.flag = p.flag;
   la.cand = p.cand; la.full = p.full;
@@ -2361,8 +2310,7 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   la.qB = reinterpret_cast<const u32x4*>(p.qB);
   for (int s = 0; s < p.S; ++s) { la.keys[s] = p.st[s].keys; la.stride[s] = p.st[s].row_stride; }
   la.dbg_pos = p.dbg_topk_pos; la.dbg_score = p.dbg_topk_score; la.dbg_stats = p.dbg_list_stats;
-  la.run_f = p.run_f; la.run_c = p.run_c; la.run_fx = p.run_fx; la.nruns = p.nruns;
-  la.listexp = p.listexp;
+  la.f_max = p.f_max; la.votes_g = p.votes; la.massfx_g = p.massfx; la.sexp = p.sexp; la.qcol = p.qcol;
   const int lists = p.S * p.NL;
   // 2. sample scores, 3. thresholds
   if (p.head_mode == 0) {
@@ -2415,9 +2363,7 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
     va.f[s] = p.st[s].f;
     va.frame0[s] = p.st[s].frame0;
   }
-  va.run_f = p.run_f; va.run_c = p.run_c; va.run_fx = p.run_fx; va.nruns = p.nruns;
-  va.listexp = p.listexp;
-  va.votes_g = p.votes; va.massfx_g = p.massfx;
+  va.votes_g = p.votes; va.massfx_g = p.massfx; va.sexp = p.sexp;
   va.rec_hi = p.rec_hi; va.rec_lo = p.rec_lo;
   va.pool_ids = p.pool_ids; va.pool_votes = p.pool_votes; va.pool_mass = p.pool_mass;
   va.pool_n = p.pool_n;
@@ -2602,11 +2548,8 @@ size_t carve_workspace(RetrievePlan& p, void* ws) {
   p.flag = static_cast<int32_t*>(take(lists * 4));
   p.samp = static_cast<float*>(take(lists * (size_t)p.m_max * 4));
   p.cand = static_cast<uint64_t*>(take(lists * (size_t)p.cap * 8));
-  p.run_f = static_cast<int32_t*>(take(lists * (size_t)std::max(p.k_max, 1) * 4));
-  p.run_c = static_cast<int32_t*>(take(lists * (size_t)std::max(p.k_max, 1) * 4));
-  p.run_fx = static_cast<int64_t*>(take(lists * (size_t)std::max(p.k_max, 1) * 8));
-  p.nruns = static_cast<int32_t*>(take(lists * 4));
-  p.listexp = static_cast<int32_t*>(take(lists * 4));
+  p.qcol = static_cast<float*>(take((size_t)p.S * p.L * p.Hk * 16 * 4));
+  p.sexp = static_cast<int32_t*>(take((size_t)p.S * 4));
   p.full = static_cast<float*>(take((size_t)p.full_total * 4));
   p.votes = static_cast<int32_t*>(take((size_t)p.S * p.f_max * 4));
   p.massfx = static_cast<int64_t*>(take((size_t)p.S * p.f_max * 8));
