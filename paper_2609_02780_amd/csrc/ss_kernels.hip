@@ -654,10 +654,53 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a) {
   }
 }
 
-// Streaming pass, head-mode 0.  The 16-row tiles of every (stream, layer, KV
-// head) segment are numbered one after another and wave w of W takes the
-// contiguous range [w T / W, (w + 1) T / W), so the work is balanced to a tile
-// whatever the mix of list lengths.  A tile is read with coalesced 16-byte
+// Tiles of the streaming passes are numbered one after another over all
+// segments.  kStreamGroup blocks of one XCD (blocks are dealt to the 8 XCDs in
+// turn) share one contiguous range of that numbering, and their 4 kStreamGroup
+// waves take its tiles in turn, so that at any moment the group reads one
+// window of about 4 kStreamGroup tiles.  Measured on the 1-hour workload, a few
+// dozen such windows in flight read HBM faster than one private range per wave
+// (thousands of scattered streams) or one sweep by the whole grid.
+constexpr int kStreamGroup = 32;
+
+struct WaveRange {
+  int64_t b0, b1;   // the group's tiles
+  int sw, wg;       // waves in the group, this wave's rank among them
+};
+
+__device__ __forceinline__ WaveRange wave_range(int64_t total, int wave) {
+  const int64_t nb = gridDim.x, b = blockIdx.x;
+  int64_t ng, grp;
+  int members, rank;
+  if (nb % (8 * kStreamGroup) == 0) {
+    ng = nb / kStreamGroup;
+    const int64_t x = b % 8, r = b / 8;   // XCD, and rank among its blocks
+    grp = (r / kStreamGroup) * 8 + x;
+    members = kStreamGroup;
+    rank = (int)(r % kStreamGroup);
+  } else {
+    ng = (nb + kStreamGroup - 1) / kStreamGroup;
+    grp = b / kStreamGroup;
+    members = (int)min<int64_t>(kStreamGroup, nb - grp * kStreamGroup);
+    rank = (int)(b - grp * kStreamGroup);
+  }
+  WaveRange w;
+  w.b0 = grp * total / ng;
+  w.b1 = (grp + 1) * total / ng;
+  w.sw = 4 * members;
+  w.wg = rank * 4 + wave;
+  return w;
+}
+
+// First tile of this wave at or after segment-local tile `tb`, the piece of
+// the group's range that starts at flat tile T.
+__device__ __forceinline__ int first_tile(const WaveRange& w, int64_t T, int tb) {
+  const int d = (int)((T - w.b0) % w.sw);
+  return tb + (w.wg - d + w.sw) % w.sw;
+}
+
+// Streaming pass, head-mode 0, over the group ranges above; the segment of a
+// tile is a (stream, layer, KV head) list group.  A tile is read with coalesced 16-byte
 // loads (one instruction covers 1 KiB of consecutive rows), stored into the
 // wave's LDS tile and read back in the MFMA A layout.  LDS holds the tile as
 // 256-byte lines of 16 chunks with chunk C of line R at position C ^ (R mod 16),
@@ -677,18 +720,19 @@ __global__ __launch_bounds__(256) void k_stream(ScoreArgs a) {
   const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
   u32x4* lt_ = tiles[wave];
   uint64_t* st = stage + wave * kMaxGroup * kStage;
-  const int64_t nw = (int64_t)gridDim.x * 4, gw = (int64_t)blockIdx.x * 4 + wave;
-  const int64_t total = a.tile_base[a.S];
-  const int64_t T1 = (gw + 1) * total / nw;
-  int64_t T = gw * total / nw;
-  while (T < T1) {
+  const WaveRange wr = wave_range(a.tile_base[a.S], wave);
+  const int SW = wr.sw;
+  for (int64_t T = wr.b0; T < wr.b1;) {
     int s = 0;
     while (T >= a.tile_base[s + 1]) ++s;
     const int64_t rem = T - a.tile_base[s];
     const int nt = a.ntile[s];
     const int lg = (int)(rem / nt);
-    const int t0 = (int)(rem - (int64_t)lg * nt);
-    const int t1 = (int)min<int64_t>(nt, t0 + (T1 - T));
+    const int tb = (int)(rem - (int64_t)lg * nt);
+    const int t1 = (int)min<int64_t>(nt, tb + (wr.b1 - T));
+    const int t0 = first_tile(wr, T, tb);
+    T += t1 - tb;
+    if (t0 >= t1) continue;
     const int g = lg % a.Hk, l = lg / a.Hk;
     const int n = a.n[s];
     const bool colv = col < a.G;
@@ -720,19 +764,19 @@ __global__ __launch_bounds__(256) void k_stream(ScoreArgs a) {
     // and emits nothing), which keeps the waits exact.
     u32x4 V[PF][NI];
 #pragma unroll
-    for (int p = 0; p < PF; ++p) load(t0 + p, V[p]);
+    for (int p = 0; p < PF; ++p) load(t0 + SW * p, V[p]);
     int lc = 0;
-    for (int t = t0; t < t1; t += PF) {
+    for (int t = t0; t < t1; t += SW * PF) {
 #pragma unroll
       for (int p = 0; p < PF; ++p) {
-        const int tt = t + p;
+        const int tt = t + SW * p;
 #pragma unroll
         for (int i = 0; i < NI; ++i) {
           const int q = i * kWave + lane, R = q >> 4, C = q & 15;
           lt_[R * 16 + (C ^ (R & 15))] = V[p][i];
         }
         __builtin_amdgcn_wave_barrier();
-        load(tt + PF, V[p]);
+        load(tt + SW * PF, V[p]);
         u32x4 A[KS];
 #pragma unroll
         for (int i = 0; i < KS; ++i) {
@@ -745,13 +789,12 @@ __global__ __launch_bounds__(256) void k_stream(ScoreArgs a) {
       }
     }
     if (__any(lc > 0)) stage_flush(a, list, colv, col, kg, st, lc);
-    T += t1 - t0;
   }
 }
 
 // Sample pass, head-mode 0: the m sampled rows of every (stream, layer, KV
 // head) list group, 16 to a tile, numbered one after another and cut into one
-// contiguous range per wave as in k_stream; a tile's rows are gathered with
+// contiguous range per wave; a tile's rows are gathered with
 // coalesced loads (16 lanes per 256-byte row, four rows per instruction) into
 // the wave's LDS tile and scored with the same arithmetic as k_stream.
 template <int D>
@@ -886,18 +929,19 @@ __global__ __launch_bounds__(256) void k_stream_hm(ScoreArgs a) {
   const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
   u32x4* lt_ = tiles[wave];
   uint64_t* st = stage + wave * kStage;
-  const int64_t nw = (int64_t)gridDim.x * 4, gw = (int64_t)blockIdx.x * 4 + wave;
-  const int64_t total = a.tile_base[a.S];
-  const int64_t T1 = (gw + 1) * total / nw;
-  int64_t T = gw * total / nw;
-  while (T < T1) {
+  const WaveRange wr = wave_range(a.tile_base[a.S], wave);
+  const int SW = wr.sw;
+  for (int64_t T = wr.b0; T < wr.b1;) {
     int s = 0;
     while (T >= a.tile_base[s + 1]) ++s;
     const int64_t rem = T - a.tile_base[s];
     const int nt = a.ntile[s];
     const int l = (int)(rem / nt);
-    const int t0 = (int)(rem - (int64_t)l * nt);
-    const int t1 = (int)min<int64_t>(nt, t0 + (T1 - T));
+    const int tb = (int)(rem - (int64_t)l * nt);
+    const int t1 = (int)min<int64_t>(nt, tb + (wr.b1 - T));
+    const int t0 = first_tile(wr, T, tb);
+    T += t1 - tb;
+    if (t0 >= t1) continue;
     const int n = a.n[s], Hk = a.Hk;
     const bool colv = col == 0;
     const int list = s * a.NL + l;
@@ -916,7 +960,7 @@ __global__ __launch_bounds__(256) void k_stream_hm(ScoreArgs a) {
     u32x4 V[NI];
     load(t0, 0, V);
     int lc = 0;
-    for (int t = t0; t < t1; ++t) {
+    for (int t = t0; t < t1; t += SW) {
       f32x4 v = {0.f, 0.f, 0.f, 0.f};
       for (int g = 0; g < Hk; ++g) {
 #pragma unroll
@@ -926,7 +970,7 @@ __global__ __launch_bounds__(256) void k_stream_hm(ScoreArgs a) {
         }
         __builtin_amdgcn_wave_barrier();
         if (g + 1 < Hk) load(t, g + 1, V);
-        else load(t + 1, 0, V);
+        else load(t + SW, 0, V);
         u32x4 A[KS];
 #pragma unroll
         for (int i = 0; i < KS; ++i) {
@@ -939,7 +983,6 @@ __global__ __launch_bounds__(256) void k_stream_hm(ScoreArgs a) {
       stream_emit(a, list, colv, col, tau_f, t * kTile, n, hm_finish(v), kg, st, lc);
     }
     if (__any(lc > 0)) stage_flush(a, list, colv, col, kg, st, lc);
-    T += t1 - t0;
   }
 }
 
