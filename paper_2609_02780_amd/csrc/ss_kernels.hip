@@ -1803,129 +1803,535 @@ __global__ __launch_bounds__(256) void k_copy(AppendArgs a) {
 }
 
 // Per (frame, layer, KV head) k-means: farthest-point seeding from the frame
-// mean, then n_iters Lloyd rounds on squared Euclidean distance in fp32.
-// One thread per token; centroids in LDS (read as broadcasts).
+// mean, then n_iters Lloyd rounds on squared Euclidean distance in fp32.  One
+// block of 16 waves per problem; wave w holds tokens 16w..16w+15 as an MFMA
+// operand tile (bf16 16x16x32, fp32 accumulation).
+//
+// Exact products, bounded sums: the tokens are exact bf16, and every fp32
+// centre is split exactly into three bf16 parts (c = c1 + c2 + c3), so every
+// product in a dot product is exact and only the fp32 sums round (each addition
+// off by at most 2^-23 relative, whatever the rounding mode of the matrix
+// core).  An expanded distance |x|^2 + |y|^2 - 2 x.y then lies within a bound
+// eps of the exact one (below), and wherever two candidates are closer than
+// 2.5 eps the decision is taken again in the direct form sum_e (x_e - y_e)^2
+// (fmaf in dimension order).  Every decision is therefore the exact one or the
+// direct form's.
+//
+// Seeding: pick 0 is the token farthest from the frame mean (direct form).
+// Each later pick is the token whose running minimum of expanded distances to
+// the picks so far is largest (ties to the lower token); eps = 2^-24 max|x|^2
+// (6D + 16).  Candidates near the maximum get their exact minimum over every
+// pick so far.
+//
+// Assignment: per token the two smallest keys (ordered expanded distance, low 6
+// bits = centre) over the centres, reduced over the 16 lanes of an MFMA row by
+// DPP; eps = 2^-24 ((D + 8)(|x|^2 + max|c|^2) + 4 (D + 9) |x| max|c| + d) plus
+// the key truncation.  Near ties are re-decided by one wave, one lane per centre.
+//
+// Update: the member sums are an MFMA contraction over the tokens (one-hot
+// membership x tokens; exact products, a fixed summation order); a centre moves
+// to sum / count, an empty centre stays.  The new centres are published as
+// fp32 rows, squared norms and split MFMA operands.
+// DPP move of a float / the two smallest of (k1, k2) and the partner's pair
+template <int ctrl>
+__device__ __forceinline__ float km_dpp_f(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), ctrl, 0xF, 0xF, false));
+}
+template <int ctrl>
+__device__ __forceinline__ void km_pair_min(uint32_t& k1, uint32_t& k2) {
+  const uint32_t o1 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)k1, ctrl, 0xF, 0xF, false);
+  const uint32_t o2 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)k2, ctrl, 0xF, 0xF, false);
+  k2 = min(max(k1, o1), min(k2, o2));
+  k1 = min(k1, o1);
+}
+
+constexpr int kKmThreads = 1024;      // 16 waves: one 16-token tile per wave (T <= kMaxTokensCompress = 256)
+constexpr int kKmMeanThreads = 256;   // threads of the frame-mean partial sums
+
 template <int D>
-__global__ __launch_bounds__(256) void k_kmeans(AppendArgs a) {
-  constexpr int XS = D / 2 + 1;  // padded row stride in 32-bit words (bank-conflict free)
-  __shared__ uint32_t xs[kMaxTokensCompress * XS];
-  __shared__ float cen[kMaxCentroids * D];
-  __shared__ float mu[D];
-  __shared__ float mind[kMaxTokensCompress];
-  __shared__ int assign_[kMaxTokensCompress];
-  __shared__ int members[kMaxTokensCompress];
+struct KmLayout {
+  static constexpr int KS = D / 32;        // k-steps of 32 dims
+  static constexpr int Q = D / 8;          // 8-dim groups per row
+  static constexpr int XW = D / 2 + 4;     // token row stride in 32-bit words (padded by 16 B)
+  static constexpr int CS = D + 1;         // fp32 centre row stride in floats (conflict-free columns)
+  // token rows, padded to whole 32-token MFMA k-steps
+  __host__ __device__ static int rows(int T) { return (T + 31) / 32 * 32; }
+  __host__ __device__ static size_t op_bytes(int C) { return (size_t)((C + 15) / 16) * 3 * KS * 64 * 16; }
+  __host__ __device__ static size_t x_bytes(int T) { return (size_t)rows(T) * XW * 4; }
+  // the centre rows also hold the frame mean's partial sums (kKmMeanThreads / Q slices of D)
+  __host__ __device__ static size_t c_bytes(int C) {
+    const size_t n = (size_t)C * CS, m = (size_t)8 * kKmMeanThreads;
+    return (n > m ? n : m) * 4;
+  }
+  __host__ __device__ static size_t bytes(int T, int C) { return op_bytes(C) + x_bytes(T) + c_bytes(C); }
+};
+
+__device__ __forceinline__ float bf16f(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+// Publishes the 8 dims 8q..8q+7 of centre c: the fp32 row (c < C), its exact
+// three-part bf16 split as MFMA A operands, and (lane q == 0) the squared norm
+// summed over the Q lanes of the centre in a fixed butterfly.  Every lane of
+// the wave calls it (inactive items pass zeros and c >= C).
+template <int D>
+__device__ __forceinline__ void km_publish(int c, int q, int C, const float (&v)[8], float* cenf,
+                                           u32x4* opA, float* cn) {
+  using Lay = KmLayout<D>;
+  float ss = 0.f;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) ss = fmaf(v[k], v[k], ss);
+  uint32_t w1[4], w2[4], w3[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    uint16_t p1[2], p2[2], p3[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const float x = v[2 * k + h];
+      p1[h] = bf16_rne(x);
+      const float r1 = x - bf16f(p1[h]);
+      p2[h] = bf16_rne(r1);
+      p3[h] = bf16_rne(r1 - bf16f(p2[h]));
+    }
+    w1[k] = (uint32_t)p1[0] | ((uint32_t)p1[1] << 16);
+    w2[k] = (uint32_t)p2[0] | ((uint32_t)p2[1] << 16);
+    w3[k] = (uint32_t)p3[0] | ((uint32_t)p3[1] << 16);
+  }
+  if (c < (C + 15) / 16 * 16) {
+    const int ct = c >> 4, ln = (c & 15) + 16 * (q & 3), ks = q >> 2;
+    opA[((ct * 3 + 0) * Lay::KS + ks) * 64 + ln] = u32x4{w1[0], w1[1], w1[2], w1[3]};
+    opA[((ct * 3 + 1) * Lay::KS + ks) * 64 + ln] = u32x4{w2[0], w2[1], w2[2], w2[3]};
+    opA[((ct * 3 + 2) * Lay::KS + ks) * 64 + ln] = u32x4{w3[0], w3[1], w3[2], w3[3]};
+  }
+  if (c < C) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) cenf[c * Lay::CS + 8 * q + k] = v[k];
+  }
+  if (Lay::Q == 16) {   // the 16 lanes of the centre are one DPP row; lane q == 0 keeps its sum
+    ss += km_dpp_f<0xB1>(ss);
+    ss += km_dpp_f<0x4E>(ss);
+    ss += km_dpp_f<0x124>(ss);
+    ss += km_dpp_f<0x128>(ss);
+  } else {
+    ss += __shfl_xor(ss, 1);
+    ss += __shfl_xor(ss, 2);
+    ss += __shfl_xor(ss, 4);
+  }
+  if (q == 0 && c < C) cn[c] = ss;
+}
+
+// Direct squared distance sum_e (x_e - y_e)^2 (fmaf in dimension order) of a
+// bf16 token row in LDS against another bf16 row, or against fp32 values read
+// by `yv(e)`; 16 dims at a time are loaded ahead of the chain.
+template <int D>
+__device__ __forceinline__ float km_dist_rows(const uint32_t* xr, const uint32_t* yr) {
+  float acc = 0.f;
+#pragma unroll
+  for (int c0 = 0; c0 < D / 8; c0 += 2) {
+    u32x4 xa[2], ya[2];
+#pragma unroll
+    for (int v = 0; v < 2; ++v) {
+      xa[v] = *reinterpret_cast<const u32x4*>(xr + 4 * (c0 + v));
+      ya[v] = *reinterpret_cast<const u32x4*>(yr + 4 * (c0 + v));
+    }
+#pragma unroll
+    for (int v = 0; v < 2; ++v)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const float d0 = bf16_lo(xa[v][k]) - bf16_lo(ya[v][k]);
+        acc = fmaf(d0, d0, acc);
+        const float d1 = bf16_hi(xa[v][k]) - bf16_hi(ya[v][k]);
+        acc = fmaf(d1, d1, acc);
+      }
+  }
+  return acc;
+}
+template <int D, class YV>
+__device__ __forceinline__ float km_dist_row_f32(const uint32_t* xr, YV yv) {
+  float acc = 0.f;
+#pragma unroll
+  for (int c0 = 0; c0 < D / 8; c0 += 2) {
+    u32x4 xa[2];
+    float y[16];
+#pragma unroll
+    for (int v = 0; v < 2; ++v) xa[v] = *reinterpret_cast<const u32x4*>(xr + 4 * (c0 + v));
+#pragma unroll
+    for (int e = 0; e < 16; ++e) y[e] = yv(8 * c0 + e);
+#pragma unroll
+    for (int v = 0; v < 2; ++v)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const float d0 = bf16_lo(xa[v][k]) - y[8 * v + 2 * k];
+        acc = fmaf(d0, d0, acc);
+        const float d1 = bf16_hi(xa[v][k]) - y[8 * v + 2 * k + 1];
+        acc = fmaf(d1, d1, acc);
+      }
+  }
+  return acc;
+}
+
+// Exact (direct-form) minimum squared distance of token `tok` to the picks
+// chosen[0..c-1], one lane per pick (c <= 64), reduced over the wave.  Kept out
+// of line: it runs only near ties and would otherwise hold registers in the
+// seeding loop.
+template <int D>
+__device__ __noinline__ float km_exact_min(const uint32_t* xs, int xw, const int* chosen, int tok, int c) {
+  const int lane = threadIdx.x & 63;
+  float m = lane < c ? km_dist_rows<D>(xs + tok * xw, xs + chosen[lane] * xw) : INFINITY;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) m = fminf(m, __shfl_xor(m, o));
+  return m;
+}
+
+template <int D>
+__global__ __launch_bounds__(kKmThreads) void k_kmeans(AppendArgs a) {
+  using Lay = KmLayout<D>;
+  constexpr int KS = Lay::KS, Q = Lay::Q, XW = Lay::XW, CS = Lay::CS;
+  constexpr int NW = kKmThreads / 64;      // one 16-token tile per wave
+  constexpr int SL = kKmMeanThreads / Q;   // token slices of the frame-mean partial sums
+  constexpr int NDT = D / 16;              // dim tiles of the update
+  constexpr int MAXS = kMaxTokensCompress / 32;
+  extern __shared__ __align__(16) unsigned char km_dyn[];
+  __shared__ float xn[kMaxTokensCompress];
+  __shared__ __align__(16) int assign_[kMaxTokensCompress];
+  __shared__ int rlist[kMaxTokensCompress];
+  __shared__ float cn[kMaxCentroids];
   __shared__ int ccount[kMaxCentroids];
-  __shared__ int coff[kMaxCentroids];
   __shared__ int chosen[kMaxCentroids];
-  __shared__ float shv[4];
-  __shared__ int shi[4];
+  __shared__ float mu[D];
+  __shared__ uint32_t shk[2][NW], shk2[2][NW];
+  __shared__ int shi[2][NW];
+  __shared__ float cval[kMaxTokensCompress];   // exact minima of near-tie candidates
+  __shared__ float xnmax_sh;
+  __shared__ int rcount, pick_sh;
+
   const int b = blockIdx.x;
   const int g = b % a.Hk, fl = b / a.Hk, l = fl % a.L, f = fl / a.L;
   const int T = a.n_tokens, C = min(a.n_centroids, T);
+  const int nct = (C + 15) / 16, Tp = Lay::rows(T), ntt = (T + 15) / 16, nsteps = Tp / 32;
   const int64_t nT = (int64_t)a.n_frames * T;
   const uint16_t* src = a.src[l] + ((int64_t)g * nT + (int64_t)f * T) * D;
-  const int t = threadIdx.x;
-  for (int i = t; i < T * (D / 2); i += blockDim.x) {
-    const int r = i / (D / 2), w = i % (D / 2);
-    xs[r * XS + w] = reinterpret_cast<const uint32_t*>(src + (int64_t)r * D)[w];
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+
+  u32x4* opA = reinterpret_cast<u32x4*>(km_dyn);
+  uint32_t* xs = reinterpret_cast<uint32_t*>(km_dyn + Lay::op_bytes(C));
+  float* cenf = reinterpret_cast<float*>(km_dyn + Lay::op_bytes(C) + Lay::x_bytes(T));
+
+  // tokens -> LDS (bf16 rows, padded stride; rows T..Tp-1 zero); padded rows have no centre
+  for (int i = t; i < Tp * Q; i += kKmThreads) {
+    const int r = i / Q, v = i - r * Q;
+    u32x4 x = {0u, 0u, 0u, 0u};
+    if (r < T) x = *reinterpret_cast<const u32x4*>(src + (int64_t)r * D + 8 * v);
+    *reinterpret_cast<u32x4*>(xs + r * XW + 4 * v) = x;
   }
+  for (int r = t; r < kMaxTokensCompress; r += kKmThreads) assign_[r] = -1;
+  if (t == 0) rcount = 0;
   __syncthreads();
-  auto xval = [&](int r, int e) -> float {
-    const uint32_t w = xs[r * XS + (e >> 1)];
-    return (e & 1) ? bf16_hi(w) : bf16_lo(w);
-  };
-  // frame mean (token order)
-  for (int e = t; e < D; e += blockDim.x) {
-    float acc = 0.f;
-    for (int r = 0; r < T; ++r) acc += xval(r, e);
-    mu[e] = acc / (float)T;
-  }
-  __syncthreads();
-  float dm = -INFINITY;
-  if (t < T) {
-    float acc = 0.f;
-    for (int e = 0; e < D; ++e) { const float d = xval(t, e) - mu[e]; acc = fmaf(d, d, acc); }
-    dm = acc;
-  }
-  int pick = block_argmax(dm, t < T ? t : INT_MAX, shv, shi);
-  bool is_taken = (t == pick);
-  if (t == 0) chosen[0] = pick;
-  float my_min = INFINITY;
-  for (int c = 0; c < C; ++c) {
-    if (c > 0) {
-      pick = block_argmax((t < T && !is_taken) ? my_min : -INFINITY, (t < T && !is_taken) ? t : INT_MAX,
-                          shv, shi);
-      if (t == pick) is_taken = true;
-      if (t == 0) chosen[c] = pick;
-    }
-    if (t < T) {
-      float acc = 0.f;
-      for (int e = 0; e < D; ++e) { const float d = xval(t, e) - xval(pick, e); acc = fmaf(d, d, acc); }
-      my_min = fminf(my_min, acc);
-    }
-  }
-  __syncthreads();
-  for (int i = t; i < C * D; i += blockDim.x) cen[i] = xval(chosen[i / D], i % D);
-  __syncthreads();
-  for (int it = 0; it < a.n_iters; ++it) {
-    // assignment: nearest centre, ties to the lower index
-    if (t < T) {
-      float acc[kMaxCentroids];
+  // frame mean: thread (slice s, group q) sums dims 8q..8q+7 over tokens s, s + SL, ...;
+  // the slices' partial sums (staged in the centre rows, unused until seeding ends) are
+  // then added in slice order.  Squared norms |x|^2 in dimension order (fmaf).
+  if (t < kKmMeanThreads) {
+    const int q = t % Q, s = t / Q;
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int r = s; r < T; r += SL) {
+      const u32x4 x = *reinterpret_cast<const u32x4*>(xs + r * XW + 4 * q);
+      const uint32_t ws[4] = {x[0], x[1], x[2], x[3]};
 #pragma unroll
-      for (int c = 0; c < kMaxCentroids; ++c) acc[c] = 0.f;
-      for (int e = 0; e < D; e += 2) {
-        const uint32_t w = xs[t * XS + (e >> 1)];
-        const float x0 = bf16_lo(w), x1 = bf16_hi(w);
+      for (int k = 0; k < 4; ++k) { acc[2 * k] += bf16_lo(ws[k]); acc[2 * k + 1] += bf16_hi(ws[k]); }
+    }
 #pragma unroll
-        for (int c = 0; c < kMaxCentroids; ++c) {
-          if (c < C) {
-            const float d0 = x0 - cen[c * D + e], d1 = x1 - cen[c * D + e + 1];
-            acc[c] = fmaf(d1, d1, fmaf(d0, d0, acc[c]));
-          }
+    for (int k = 0; k < 8; ++k) cenf[s * D + 8 * q + k] = acc[k];
+  } else if (t < kKmMeanThreads + kMaxTokensCompress) {
+    const int r = t - kKmMeanThreads;
+    float s2 = 0.f;
+    if (r < T) {
+#pragma unroll
+      for (int v = 0; v < Q; ++v) {
+        const u32x4 x = *reinterpret_cast<const u32x4*>(xs + r * XW + 4 * v);
+        const uint32_t ws[4] = {x[0], x[1], x[2], x[3]};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          s2 = fmaf(bf16_lo(ws[k]), bf16_lo(ws[k]), s2);
+          s2 = fmaf(bf16_hi(ws[k]), bf16_hi(ws[k]), s2);
         }
       }
-      int bi = 0;
-      float bv = acc[0];
+    }
+    xn[r] = s2;
+  }
+  __syncthreads();
+  if (t < D) {
+    float acc = 0.f;
+    for (int s = 0; s < SL; ++s) acc += cenf[s * D + t];
+    mu[t] = acc / (float)T;
+  } else if (t >= 64 * 4 && t < 64 * 5) {   // wave 4: the largest squared norm
+    float m = 0.f;
+    for (int r = lane; r < T; r += 64) m = fmaxf(m, xn[r]);
+    const uint32_t mm = wave_max_u32(__float_as_uint(m));   // non-negative floats order as uint
+    if (lane == 0) xnmax_sh = __uint_as_float(mm);
+  }
+  __syncthreads();
+
+  // The wave's token tile (tokens 16w..16w+15) as MFMA A operands, kept for seeding
+  // and assignment.  Output lane l holds tokens 16w + 4(l>>4) + j, j = 0..3; lane l
+  // owns token tok_l = 16w + 4(l>>4) + (l&3) (four lanes per token, identical values).
+  const bool has_tile = w < ntt;
+  u32x4 A[KS];
 #pragma unroll
-      for (int c = 1; c < kMaxCentroids; ++c) {
-        if (c < C && acc[c] < bv) { bv = acc[c]; bi = c; }
+  for (int ks = 0; ks < KS; ++ks)
+    A[ks] = has_tile ? *reinterpret_cast<const u32x4*>(xs + (16 * w + (lane & 15)) * XW + 16 * ks + 4 * (lane >> 4))
+                     : u32x4{0u, 0u, 0u, 0u};
+  const int my_tok = 16 * w + 4 * (lane >> 4) + (lane & 3);
+  const bool tok_ok = has_tile && my_tok < T;
+  const float my_xn = tok_ok ? xn[my_tok] : 0.f;
+  const float xnmax = xnmax_sh;
+
+  // ---- farthest-point seeding (pick 0 in the direct form, later picks from
+  // MFMA dot products with the exact re-decision near ties)
+  if (t < T) cval[t] = km_dist_row_f32<D>(xs + t * XW, [&](int e) { return mu[e]; });
+  __syncthreads();
+  float val = tok_ok ? cval[my_tok] : -INFINITY;
+  bool avail = tok_ok;
+  float my_min = INFINITY;
+  const float band = 2.5f * 5.9604645e-8f * xnmax * (float)(6 * D + 16);
+  for (int c = 0; c < C; ++c) {
+    const int pb = c & 1;
+    {
+      // wave: largest value, its lowest token, the largest value of any other token
+      const uint32_t o = avail ? ord_u32(val) : 0u;
+      const uint32_t m1 = wave_max_u32(o);
+      const uint64_t bm = __ballot(avail && o == m1);
+      const int blane = bm ? __builtin_ctzll(bm) : 0;
+      const int btok = 16 * w + 4 * (blane >> 4) + (blane & 3);
+      const uint32_t m2 = wave_max_u32(avail && my_tok != btok ? o : 0u);
+      if (lane == 0) {
+        shk[pb][w] = m1;
+        shk2[pb][w] = m2;
+        shi[pb][w] = bm ? btok : INT_MAX;
       }
-      assign_[t] = bi;
+    }
+    __syncthreads();
+    // the waves' winners, lane i holding wave i's: the largest, its lowest token,
+    // the largest of everything else (waves without a candidate hold zeros)
+    uint32_t k1, k2;
+    int pick;
+    {
+      const uint32_t a1 = lane < NW ? shk[pb][lane] : 0u, a2 = lane < NW ? shk2[pb][lane] : 0u;
+      const int i1 = lane < NW ? shi[pb][lane] : INT_MAX;
+      k1 = wave_max_u32(a1);
+      pick = (int)wave_min_u32(a1 == k1 ? (uint32_t)i1 : (uint32_t)INT_MAX);
+      k2 = wave_max_u32(max(i1 != pick ? a1 : 0u, a2));
+    }
+    if (c > 0 && k2 != 0u && ord_f32(k2) >= ord_f32(k1) - band) {
+      // near tie: exact minima of the candidates over picks 0..c-1, one wave each
+      if (t == 0) rcount = 0;
+      __syncthreads();
+      const float v1 = ord_f32(k1);
+      if (avail && (lane >> 2 & 3) == 0 && val >= v1 - band) rlist[atomicAdd(&rcount, 1)] = my_tok;
+      __syncthreads();
+      const int ncand = rcount;
+      for (int i = w; i < ncand; i += NW) {
+        const float m = km_exact_min<D>(xs, XW, chosen, rlist[i], c);
+        if (lane == 0) cval[i] = m;
+      }
+      __syncthreads();
+      if (t == 0) {
+        float bv = -INFINITY;
+        int bt = INT_MAX;
+        for (int i = 0; i < ncand; ++i) {
+          const float m = cval[i];
+          const int tok = rlist[i];
+          if (m > bv || (m == bv && tok < bt)) { bv = m; bt = tok; }
+        }
+        pick_sh = bt;
+      }
+      __syncthreads();
+      pick = pick_sh;
+    }
+    if (my_tok == pick) avail = false;
+    if (t == 0) chosen[c] = pick;
+    if (c == C - 1) break;
+    if (has_tile) {   // wave-uniform: dot products with the pick
+      u32x4 B[KS];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        B[ks] = *reinterpret_cast<const u32x4*>(xs + pick * XW + 16 * ks + 4 * (lane >> 4));
+      f32x4 h = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) h = mfma_bf16(A[ks], B[ks], h);
+      const float xp = xn[pick];
+      const int j = lane & 3;
+      const float dot = j == 0 ? h[0] : j == 1 ? h[1] : j == 2 ? h[2] : h[3];
+      my_min = fminf(my_min, fmaf(-2.f, dot, my_xn + xp));
+    }
+    val = my_min;
+  }
+  __syncthreads();
+  // initial centres: the chosen tokens
+  for (int i = t; i < nct * 16 * Q; i += kKmThreads) {
+    const int c = i / Q, q = i - c * Q;
+    float v[8];
+    if (c < C) {
+      const u32x4 x = *reinterpret_cast<const u32x4*>(xs + chosen[c] * XW + 4 * q);
+      const uint32_t ws[4] = {x[0], x[1], x[2], x[3]};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) { v[2 * k] = bf16_lo(ws[k]); v[2 * k + 1] = bf16_hi(ws[k]); }
+    } else {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) v[k] = 0.f;
+    }
+    km_publish<D>(c, q, C, v, cenf, opA, cn);
+  }
+  if (t == 0) rcount = 0;
+  __syncthreads();
+
+  const int dt = w % NDT;
+  for (int it = 0; it < a.n_iters; ++it) {
+    // ---- assignment: MFMA dot products (A = the wave's 16 tokens, B = 16 centres),
+    // expanded distances as keys (ordered distance, low 6 bits = centre), per token
+    // the two smallest keys over the 16 lanes of an MFMA row (DPP), exact
+    // re-decision near ties
+    if (has_tile) {   // wave-uniform
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        A[ks] = *reinterpret_cast<const u32x4*>(xs + (16 * w + (lane & 15)) * XW + 16 * ks + 4 * (lane >> 4));
+      float cmax = 0.f;
+      for (int ct = 0; ct < nct; ++ct) {
+        const int c = ct * 16 + (lane & 15);
+        if (c < C) cmax = fmaxf(cmax, cn[c]);
+      }
+      cmax = fmaxf(cmax, km_dpp_f<0xB1>(cmax));
+      cmax = fmaxf(cmax, km_dpp_f<0x4E>(cmax));
+      cmax = fmaxf(cmax, km_dpp_f<0x124>(cmax));
+      cmax = fmaxf(cmax, km_dpp_f<0x128>(cmax));
+      float xv[4];
+      uint32_t k1[4], k2[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        xv[j] = xn[16 * w + 4 * (lane >> 4) + j];
+        k1[j] = 0xFFFFFFFFu;
+        k2[j] = 0xFFFFFFFFu;
+      }
+      for (int ct = 0; ct < nct; ++ct) {
+        const int c = ct * 16 + (lane & 15);
+        const float cc = c < C ? cn[c] : 0.f;
+        f32x4 h = {0.f, 0.f, 0.f, 0.f}, m = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) h = mfma_bf16(A[ks], opA[((ct * 3 + 0) * KS + ks) * 64 + lane], h);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) m = mfma_bf16(A[ks], opA[((ct * 3 + 2) * KS + ks) * 64 + lane], m);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) m = mfma_bf16(A[ks], opA[((ct * 3 + 1) * KS + ks) * 64 + lane], m);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float d = fmaf(-2.f, h[j] + m[j], xv[j] + cc);
+          const uint32_t kn = c < C ? ((ord_u32(d) & ~63u) | (uint32_t)c) : 0xFFFFFFFFu;
+          if (kn < k1[j]) { k2[j] = k1[j]; k1[j] = kn; }
+          else k2[j] = min(k2[j], kn);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        km_pair_min<0xB1>(k1[j], k2[j]);
+        km_pair_min<0x4E>(k1[j], k2[j]);
+        km_pair_min<0x124>(k1[j], k2[j]);
+        km_pair_min<0x128>(k1[j], k2[j]);
+      }
+      // lane (row r, j < 4) decides token 16w + 4r + j
+      const int j = lane & 15, tok = 16 * w + 4 * (lane >> 4) + j;
+      if (j < 4 && tok < T) {
+        const uint32_t b1 = j == 0 ? k1[0] : j == 1 ? k1[1] : j == 2 ? k1[2] : k1[3];
+        const uint32_t b2 = j == 0 ? k2[0] : j == 1 ? k2[1] : j == 2 ? k2[2] : k2[3];
+        const float xx = j == 0 ? xv[0] : j == 1 ? xv[1] : j == 2 ? xv[2] : xv[3];
+        assign_[tok] = b1 != 0xFFFFFFFFu ? (int)(b1 & 63u) : 0;
+        if (b2 != 0xFFFFFFFFu) {
+          const float d1 = ord_f32(b1 & ~63u), d2 = ord_f32(b2 & ~63u);
+          const float eps = 5.9604645e-8f * ((float)(D + 8) * (xx + cmax) +
+                                             (float)(4 * (D + 9)) * sqrtf(xx * cmax) + fabsf(d1));
+          if (!(d2 - d1 > 2.5f * eps + 3.0517578e-5f * fabsf(d2))) rlist[atomicAdd(&rcount, 1)] = tok;
+        }
+      }
     }
     if (t < kMaxCentroids) ccount[t] = 0;
     __syncthreads();
-    // stable counting sort of tokens by centre
-    int rank = 0;
-    if (t < T) {
-      const int me = assign_[t];
-      for (int r = 0; r < t; ++r) rank += (assign_[r] == me);
-      atomicAdd(&ccount[me], 1);
-    }
-    __syncthreads();
-    if (t == 0) {
-      int run = 0;
-      for (int c = 0; c < C; ++c) { coff[c] = run; run += ccount[c]; }
-    }
-    __syncthreads();
-    if (t < T) members[coff[assign_[t]] + rank] = t;
-    __syncthreads();
-    // update: mean of members in token order; empty centres stay
-    for (int i = t; i < C * D; i += blockDim.x) {
-      const int c = i / D, e = i % D;
-      const int n = ccount[c];
-      if (n > 0) {
-        float acc = 0.f;
-        for (int q = 0; q < n; ++q) acc += xval(members[coff[c] + q], e);
-        cen[i] = acc / (float)n;
+    const int nref = rcount;
+    for (int i = w; i < nref; i += NW) {   // direct form, lane = centre
+      const int tok = rlist[i];
+      float acc = INFINITY;
+      if (lane < C) acc = km_dist_row_f32<D>(xs + tok * XW, [&](int e) { return cenf[lane * CS + e]; });
+      int bi = lane < C ? lane : INT_MAX;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const float v2 = __shfl_xor(acc, o);
+        const int i2 = __shfl_xor(bi, o);
+        if (v2 < acc || (v2 == acc && i2 < bi)) { acc = v2; bi = i2; }
       }
+      if (lane == 0) assign_[tok] = bi;
+    }
+    __syncthreads();
+    if (t < T) atomicAdd(&ccount[assign_[t]], 1);
+    if (t == 0) rcount = 0;
+    __syncthreads();
+    // ---- update: member sums as an MFMA contraction over the tokens (A = one-hot
+    // membership of 16 centres, B = the wave's 16 dims of the tokens; exact products,
+    // fixed summation order); mean = sum / count, an empty centre stays
+      // the wave's dim tile of the tokens as MFMA B operands for the update (k = 32
+      // tokens per step, column = dim); the tokens never change
+      u32x4 xT[MAXS];
+    #pragma unroll
+      for (int st = 0; st < MAXS; ++st) {
+        xT[st] = u32x4{0u, 0u, 0u, 0u};
+        if (st >= nsteps) continue;   // wave-uniform
+        const int dcol = dt * 16 + (lane & 15), t0 = 32 * st + 8 * (lane >> 4);
+        uint32_t xb[4];
+    #pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const uint32_t w0 = xs[(t0 + 2 * k) * XW + (dcol >> 1)];
+          const uint32_t w1 = xs[(t0 + 2 * k + 1) * XW + (dcol >> 1)];
+          const uint32_t v0 = (dcol & 1) ? (w0 >> 16) : (w0 & 0xFFFFu);
+          const uint32_t v1 = (dcol & 1) ? (w1 >> 16) : (w1 & 0xFFFFu);
+          xb[k] = v0 | (v1 << 16);
+        }
+        xT[st] = u32x4{xb[0], xb[1], xb[2], xb[3]};
+      }
+    for (int ct = w / NDT; ct < nct; ct += NW / NDT) {   // wave-uniform
+      const int crow = ct * 16 + (lane & 15);
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < MAXS; ++st) {
+        if (st >= nsteps) continue;   // wave-uniform
+        const int t0 = 32 * st + 8 * (lane >> 4);
+        const int4 a0 = *reinterpret_cast<const int4*>(assign_ + t0);
+        const int4 a1 = *reinterpret_cast<const int4*>(assign_ + t0 + 4);
+        const u32x4 oh = {(a0.x == crow ? 0x3F80u : 0u) | (a0.y == crow ? 0x3F800000u : 0u),
+                          (a0.z == crow ? 0x3F80u : 0u) | (a0.w == crow ? 0x3F800000u : 0u),
+                          (a1.x == crow ? 0x3F80u : 0u) | (a1.y == crow ? 0x3F800000u : 0u),
+                          (a1.z == crow ? 0x3F80u : 0u) | (a1.w == crow ? 0x3F800000u : 0u)};
+        acc = mfma_bf16(oh, xT[st], acc);
+      }
+      const int dcol = dt * 16 + (lane & 15);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int c = ct * 16 + 4 * (lane >> 4) + j;
+        if (c < C) {
+          const int n = ccount[c];
+          if (n > 0) cenf[c * CS + dcol] = acc[j] / (float)n;
+        }
+      }
+    }
+    __syncthreads();
+    for (int i = t; i < nct * 16 * Q; i += kKmThreads) {
+      const int c = i / Q, q = i - c * Q;
+      float v[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) v[k] = c < C ? cenf[c * CS + 8 * q + k] : 0.f;
+      km_publish<D>(c, q, C, v, cenf, opA, cn);
     }
     __syncthreads();
   }
   const int64_t drow0 = ((int64_t)l * a.Hk + g) * a.max_rows + a.row0 + (int64_t)f * C;
-  for (int i = t; i < C * D; i += blockDim.x) {
-    a.dst.keys[(drow0 + i / D) * D + (i % D)] = bf16_rne(cen[i]);
+  for (int i = t; i < C * D; i += kKmThreads) {
+    const int c = i / D, e = i - c * D;
+    a.dst.keys[(drow0 + c) * D + e] = bf16_rne(cenf[c * CS + e]);
   }
-  for (int c = t; c < C; c += blockDim.x) a.dst.counts[drow0 + c] = a.n_iters > 0 ? ccount[c] : 0;
+  for (int c = t; c < C; c += kKmThreads) a.dst.counts[drow0 + c] = a.n_iters > 0 ? ccount[c] : 0;
 }
 
 // ---------------------------------------------------------------------------
@@ -2248,7 +2654,14 @@ template <int D>
 hipError_t append_impl(const AppendArgs& a, bool compress, hipStream_t st) {
   hipLaunchKernelGGL(k_unit_means<D>, dim3(a.n_frames, a.L), dim3(256), 0, st, a);
   if (compress) {
-    hipLaunchKernelGGL(k_kmeans<D>, dim3(a.n_frames * a.L * a.Hk), dim3(256), 0, st, a);
+    const int C = std::min(a.n_centroids, a.n_tokens);
+    const size_t lds = KmLayout<D>::bytes(a.n_tokens, C);
+    // the largest layout the API admits (n_tokens <= 256, n_centroids <= 64) fits in 160 KB
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_kmeans<D>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize,
+                                             (int)KmLayout<D>::bytes(kMaxTokensCompress, kMaxCentroids));
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_kmeans<D>, dim3(a.n_frames * a.L * a.Hk), dim3(kKmThreads), lds, st, a);
   } else {
     const int64_t total = (int64_t)a.L * a.Hk * a.n_frames * a.n_tokens * (D / 8);
     const int grid = (int)std::min<int64_t>(cdiv(total, 256), 8192);

@@ -333,6 +333,36 @@ def test_compression_small_exact_cases():
         assert np.all(ex["counts"][0, 0, f * 6:(f + 1) * 6] == 1)
 
 
+def test_compression_exact_ties():
+    """Exact ties, which the oracle and the GPU must break the same way (lower
+    token, lower centre): frame 0 holds 24 random tokens twice, so every
+    farthest-point pick has an equal twin; frame 1 is symmetric (+-2 e_i and
+    zero rows), so a zero row is equidistant from the first two centres.  Both
+    frames are checked exactly: bf16 centres within one unit, equal counts."""
+    P = _P()
+    rng = np.random.default_rng(7)
+    T, d = 48, 128
+    base = rng.standard_normal((T // 2, d)).astype(np.float32)
+    f0 = np.concatenate([base, base])
+    f1 = np.zeros((T, d), dtype=np.float32)
+    for i in range(8):
+        f1[2 * i, i] = 2.0
+        f1[2 * i + 1, i] = -2.0
+    keys_f = np.concatenate([f0, f1])[None]                  # [H_kv = 1][2T][d]
+    bits = W.bf16_bits(keys_f)
+    for n_c, n_it in ((8, 3), (2, 2), (20, 4)):
+        g = P.ShallowIndex(1, 1, 1, d, 2, 2 * n_c)
+        g.append([dev_bf16(bits)], 2, T, (n_c, n_it))
+        ex = g.export()
+        for f in range(2):
+            X = O.decode_bf16(bits[0, f * T:(f + 1) * T])
+            C, cnt, _ = O.kmeans(X, n_c, n_it)
+            got = ex["rows"][0, 0, f * n_c:(f + 1) * n_c]
+            diff = np.abs(got.astype(np.int32) - O.round_bf16(C).astype(np.int32))
+            assert diff.max() <= 1, (n_c, n_it, f)
+            np.testing.assert_array_equal(ex["counts"][0, 0, f * n_c:(f + 1) * n_c], cnt)
+
+
 def test_compression_c3_shape_audit_and_retrieval():
     """The C3 workload at 60 frames: k-means audit on every problem, then
     retrieval parity on the GPU's stored centroids."""
