@@ -1727,38 +1727,68 @@ __global__ __launch_bounds__(1024) void k_maxmin(MaxminArgs a) {
 // ---------------------------------------------------------------------------
 // Descriptor (Eq. memory_key): fp32 mean over the frame's raw last-layer tokens,
 // heads flattened head-major, L2-normalised.  Also writes the frame offsets.
-// Per (frame, layer): the mean raw key of every KV head (fp32 sums in token
-// order) becomes the frame's pooled key of that layer; the last shallow
-// layer's means, flattened head-major and L2-normalised, are the unit
-// descriptor (Eq. memory_key).  Grid: (frames, layers).
+// Per (frame, layer): the mean raw key of every KV head becomes the frame's
+// pooled key of that layer; the last shallow layer's means, flattened
+// head-major and L2-normalised, are the unit descriptor (Eq. memory_key).
+// Grid: (frames, layers).  Thread (slice s, 8-dim group v) sums tokens s, s + S,
+// ... of its group with 16-byte loads (fp32, token order within the slice); the
+// S slices are then added in slice order, so the sums are deterministic.
 template <int D>
 __global__ __launch_bounds__(256) void k_unit_means(AppendArgs a) {
+  __shared__ float part[256 * 8];   // [slice][dim] partial sums (S * dim = 2048 floats)
   __shared__ float red[8];
   const int f = blockIdx.x, l = blockIdx.y;
-  const int T = a.n_tokens, dim = a.Hk * D;
+  const int T = a.n_tokens, dim = a.Hk * D, G8 = dim / 8;
+  const int S = 256 / G8;           // dim <= kMaxDescDim: G8 <= 128, S >= 2
   const int64_t nT = (int64_t)a.n_frames * T;
   const uint16_t* src = a.src[l];
+  uint32_t amax = 0;   // largest |key element| (the bits of a non-negative float order as integers)
+  if (threadIdx.x < S * G8) {
+    const int v = threadIdx.x % G8, sl = threadIdx.x / G8;
+    const int g = (8 * v) / D, e0 = (8 * v) % D;
+    const uint16_t* p = src + ((int64_t)g * nT + (int64_t)f * T) * D + e0;
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    int t = sl;
+    for (; t + 3 * S < T; t += 4 * S) {
+      u32x4 x[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) x[u] = *reinterpret_cast<const u32x4*>(p + (int64_t)(t + u * S) * D);
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          acc[2 * k] += bf16_lo(x[u][k]);
+          acc[2 * k + 1] += bf16_hi(x[u][k]);
+          amax = max(amax, max((x[u][k] << 16) & 0x7FFFFFFFu, x[u][k] & 0x7FFF0000u));
+        }
+    }
+    for (; t < T; t += S) {
+      const u32x4 x = *reinterpret_cast<const u32x4*>(p + (int64_t)t * D);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        acc[2 * k] += bf16_lo(x[k]);
+        acc[2 * k + 1] += bf16_hi(x[k]);
+        amax = max(amax, max((x[k] << 16) & 0x7FFFFFFFu, x[k] & 0x7FFF0000u));
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) part[sl * dim + 8 * v + k] = acc[k];
+  }
+  amax = wave_max_u32(amax);
+  if ((threadIdx.x & 63) == 0) atomicMax(a.dst.stats, amax);
+  __syncthreads();
   float vals[4];
   float ss = 0.f;
-  uint32_t amax = 0;   // largest |key element| (the bits of a non-negative float order as integers)
   for (int k = 0; k < 4; ++k) {
     const int e = threadIdx.x + k * 256;
     vals[k] = 0.f;
     if (e < dim) {
-      const int g = e / D, ee = e % D;
-      const uint16_t* p = src + ((int64_t)g * nT + (int64_t)f * T) * D + ee;
       float acc = 0.f;
-      for (int t = 0; t < T; ++t) {
-        const uint32_t bits = (uint32_t)p[(int64_t)t * D] << 16;
-        acc += __uint_as_float(bits);
-        amax = max(amax, bits & 0x7FFFFFFFu);
-      }
+      for (int sl = 0; sl < S; ++sl) acc += part[sl * dim + e];
       vals[k] = acc / (float)T;
       ss = fmaf(vals[k], vals[k], ss);
     }
   }
-  amax = wave_max_u32(amax);
-  if ((threadIdx.x & 63) == 0) atomicMax(a.dst.stats, amax);
   float* pooled = a.dst.pooled + ((a.frame0 + f) * a.L + l) * (int64_t)dim;
   for (int k = 0; k < 4; ++k) {
     const int e = threadIdx.x + k * 256;
