@@ -22,9 +22,10 @@
 //               candidate count left [k, capacity] recomputes all of its scores
 //               and selects exactly from them instead.  Each list then adds its
 //               selected rows up per frame (count, fixed-point score sum).
-//   k_votes_pool  per stream, the frames' votes and attention mass merged from
-//               the lists' per-frame sums (deterministic fixed point), then the
-//               vote-ranked pool (radix cut over 128-bit records, ranks by count).
+//   k_votes_pool  per stream, the vote-ranked pool from the frames' votes and
+//               fixed-point attention mass: a vote histogram fixes the cut,
+//               frames tied at it are ranked by counting (a radix cut over the
+//               128-bit records when many tie), the pool is ranked by counting.
 //   k_gram      fp32 Gram matrix of the pool descriptors.
 //   k_maxmin    greedy max-min diversity over the Gram matrix.
 //
@@ -1335,16 +1336,20 @@ __device__ void fallback_list(const ListArgs& a, int list, uint64_t* sel, int32_
   finish_list(a, list, sel, kk, lv, lm);
 }
 
+// LDS of one list's selection.
+struct SelectShared {
+  uint64_t sel[kMaxTopK];
+  int32_t lv[kVoteLds];
+  long long lm[kVoteLds];
+};
+
 template <int D>
-__global__ __launch_bounds__(1024) void k_select(ListArgs a) {
-  __shared__ uint64_t sel[kMaxTopK];
-  __shared__ int32_t lv[kVoteLds];
-  __shared__ long long lm[kVoteLds];
-  __shared__ uint32_t hist[512];
-  __shared__ uint32_t res[4];
-  __shared__ uint32_t ngather;
-  __shared__ uint32_t mm[32];
-  const int list = blockIdx.x, s = list / a.NL;
+__device__ void select_list(const ListArgs& a, int list, SelectShared& sh, uint32_t* hist, uint32_t* res,
+                            uint32_t& ngather, uint32_t* mm) {
+  uint64_t* sel = sh.sel;
+  int32_t* lv = sh.lv;
+  long long* lm = sh.lm;
+  const int s = list / a.NL;
   const int kk = a.kk[s];
   if (kk == 0) {
     finish_list(a, list, sel, 0, lv, lm);
@@ -1444,19 +1449,39 @@ struct VoteArgs {
 // The pool: the voted frames of rank < pool by (votes desc, mass desc, frame
 // asc) from the per-frame votes and fixed-point masses that the selection
 // blocks accumulated, ranked by counting.
-__global__ __launch_bounds__(1024) void k_votes_pool(VoteArgs a) {
-  __shared__ uint64_t shi[kPoolSort];
-  __shared__ uint64_t slo[kPoolSort];
-  __shared__ uint32_t nvoted_sh;
-  const int s = blockIdx.x;
+//
+// Records: hi = votes:32 | mass_hi:32, lo = mass_lo:32 | ~frame:32, compared
+// descending (mass as offset binary).  The cut between the pool and the rest:
+// a histogram of the votes gives the vote count v* of the last pool slot; the
+// frames with exactly v* votes are ranked by counting among themselves (when
+// there are at most kTieRank of them, the usual case); otherwise a radix cut
+// over the 128-bit records.  Leaves the ordered pool in shi/slo[0 .. pn) and
+// returns pn.  One block of 1024 threads per stream.
+constexpr int kVoteBins = 2048;   // vote histogram bins (the last one collects larger counts)
+constexpr int kTieRank = 128;     // frames tied at the cut ranked by counting
+
+struct PoolShared {
+  uint64_t shi[kPoolSort];
+  uint64_t slo[kPoolSort];
+  uint64_t ghi[kMaxPool];
+  uint64_t glo[kMaxPool];
+  uint32_t vh[kVoteBins];
+  int tl[kTieRank];
+  int scan[17];
+  uint32_t hist[256];
+  uint32_t res[4];
+  uint32_t nvoted, ngather, ntie;
+  uint64_t cut_hi, cut_lo;
+  int vstar, above, inb;
+};
+
+__device__ int pool_select(const VoteArgs& a, int s, PoolShared& sh) {
   const int F = a.f[s];
   const int32_t* votes = a.votes_g + (size_t)s * a.f_max;
   const int64_t* massfx = a.massfx_g + (size_t)s * a.f_max;
-  if (threadIdx.x == 0) nvoted_sh = 0;
+  if (threadIdx.x == 0) { sh.nvoted = 0; sh.ngather = 0; sh.ntie = 0; sh.vstar = -1; }
   __syncthreads();
   const double inv = ldexp(1.0, -a.sexp[s]);
-  // voted frames as records, any order: hi = votes:32 | mass_hi:32,
-  // lo = mass_lo:32 | ~frame:32, compared descending
   uint64_t* rh = a.rec_hi + (size_t)s * a.f_max;
   uint64_t* rl = a.rec_lo + (size_t)s * a.f_max;
   for (int f = threadIdx.x; f < F; f += blockDim.x) {
@@ -1467,13 +1492,12 @@ __global__ __launch_bounds__(1024) void k_votes_pool(VoteArgs a) {
       a.dbg_mass_hist[(size_t)s * a.hist_stride + a.frame0[s] + f] = (float)((double)mf * inv);
     }
     if (v >= 1) {
-      const uint32_t slot = atomicAdd(&nvoted_sh, 1u);
+      const uint32_t slot = atomicAdd(&sh.nvoted, 1u);
       const uint64_t mb = (uint64_t)mf ^ 0x8000000000000000ull;
       const uint64_t h = ((uint64_t)(uint32_t)v << 32) | (mb >> 32);
       const uint64_t l = (mb << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)f);
-      if (slot < (uint32_t)kPoolSort) { shi[slot] = h; slo[slot] = l; }
-      rh[slot] = h;
-      rl[slot] = l;
+      if (slot < (uint32_t)kPoolSort) { sh.shi[slot] = h; sh.slo[slot] = l; }
+      else { rh[slot] = h; rl[slot] = l; }
     }
   }
   if (a.dbg_vote_hist) {
@@ -1485,52 +1509,92 @@ __global__ __launch_bounds__(1024) void k_votes_pool(VoteArgs a) {
   }
   __threadfence();
   __syncthreads();
-  const int n_voted = (int)nvoted_sh;
+  const int n_voted = (int)sh.nvoted;
   const int P = a.pool;
-  __shared__ uint64_t ghi[kMaxPool];
-  __shared__ uint64_t glo[kMaxPool];
-  __shared__ uint32_t hist[256];
-  __shared__ uint32_t res[4];
-  __shared__ uint32_t ngather;
   const int pn = min(P, n_voted);
-  // the `pool` largest records: a radix cut over the 128-bit keys (when there
-  // are more voted frames than pool slots), then ranks by counting among them
   const bool in_lds = n_voted <= kPoolSort;
+  if (!in_lds) {   // the records beyond the LDS part live in global memory only
+    for (int i = threadIdx.x; i < kPoolSort; i += blockDim.x) { rh[i] = sh.shi[i]; rl[i] = sh.slo[i]; }
+    __threadfence();
+    __syncthreads();
+  }
   auto get = [&](int i, uint64_t& h, uint64_t& l) {
-    if (in_lds) { h = shi[i]; l = slo[i]; }
+    if (in_lds) { h = sh.shi[i]; l = sh.slo[i]; }
     else {
       h = __hip_atomic_load(&rh[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       l = __hip_atomic_load(&rl[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   };
   uint64_t ch = 0, cl = 0;
-  if (n_voted > P) radix_select_u128(get, n_voted, (uint32_t)P, hist, res, ch, cl);
-  if (threadIdx.x == 0) ngather = 0;
+  if (n_voted > P) {
+    bool cut = false;
+    if (in_lds) {
+      // vote histogram; pair of bins (2q, 2q + 1) per thread, q from the top
+      for (int i = threadIdx.x; i < kVoteBins; i += blockDim.x) sh.vh[i] = 0;
+      __syncthreads();
+      for (int i = threadIdx.x; i < n_voted; i += blockDim.x)
+        atomicAdd(&sh.vh[min((uint32_t)(sh.shi[i] >> 32), (uint32_t)(kVoteBins - 1))], 1u);
+      __syncthreads();
+      const int q = kVoteBins / 2 - 1 - (int)threadIdx.x;   // blockDim == kVoteBins / 2
+      const int hb = (int)sh.vh[2 * q + 1], lb = (int)sh.vh[2 * q];
+      int tot;
+      const int above = block_excl_scan(hb + lb, sh.scan, tot);   // records in higher bin pairs
+      if (above < P && P <= above + hb) { sh.vstar = 2 * q + 1; sh.above = above; sh.inb = hb; }
+      else if (above + hb < P && P <= above + hb + lb) { sh.vstar = 2 * q; sh.above = above + hb; sh.inb = lb; }
+      __syncthreads();
+      const int vstar = sh.vstar, need = P - sh.above, inb = sh.inb;
+      if (vstar >= 1 && vstar < kVoteBins - 1 && inb <= kTieRank) {
+        if (inb == need) {
+          ch = (uint64_t)(uint32_t)vstar << 32;   // every frame with >= v* votes
+          cl = 0;
+        } else {
+          for (int i = threadIdx.x; i < n_voted; i += blockDim.x)
+            if ((int)(sh.shi[i] >> 32) == vstar) sh.tl[atomicAdd(&sh.ntie, 1u)] = i;
+          __syncthreads();
+          if ((int)threadIdx.x < inb) {
+            const int me = sh.tl[threadIdx.x];
+            const uint64_t h = sh.shi[me], l = sh.slo[me];
+            int rank = 0;
+            for (int k = 0; k < inb; ++k) {
+              const int o = sh.tl[k];
+              rank += rec_less(h, l, sh.shi[o], sh.slo[o]);
+            }
+            if (rank == need - 1) { sh.cut_hi = h; sh.cut_lo = l; }   // records are distinct
+          }
+          __syncthreads();
+          ch = sh.cut_hi;
+          cl = sh.cut_lo;
+        }
+        cut = true;
+      }
+    }
+    if (!cut) radix_select_u128(get, n_voted, (uint32_t)P, sh.hist, sh.res, ch, cl);
+  }
   __syncthreads();
   for (int i = threadIdx.x; i < n_voted; i += blockDim.x) {
     uint64_t h, l;
     get(i, h, l);
     if (h > ch || (h == ch && l >= cl)) {
-      const uint32_t slot = atomicAdd(&ngather, 1u);
-      if (slot < (uint32_t)kMaxPool) { ghi[slot] = h; glo[slot] = l; }
+      const uint32_t slot = atomicAdd(&sh.ngather, 1u);
+      if (slot < (uint32_t)kMaxPool) { sh.ghi[slot] = h; sh.glo[slot] = l; }
     }
   }
   __syncthreads();
   for (int i = threadIdx.x; i < pn; i += blockDim.x) {
-    const uint64_t h = ghi[i], l = glo[i];
+    const uint64_t h = sh.ghi[i], l = sh.glo[i];
     int rank = 0;
-    for (int j = 0; j < pn; ++j) rank += rec_less(h, l, ghi[j], glo[j]);
-    shi[rank] = h;   // records are distinct: ranks form a permutation
-    slo[rank] = l;
+    for (int j = 0; j < pn; ++j) rank += rec_less(h, l, sh.ghi[j], sh.glo[j]);
+    sh.shi[rank] = h;   // records are distinct: ranks form a permutation
+    sh.slo[rank] = l;
   }
   __syncthreads();
   for (int i = threadIdx.x; i < P; i += blockDim.x) {
     int id = -1, v = 0;
     float m = 0.f;
     if (i < pn) {
-      id = (int)(0xFFFFFFFFu - (uint32_t)slo[i]);
-      v = (int)(shi[i] >> 32);
-      const uint64_t mb = (shi[i] << 32) | (slo[i] >> 32);
+      id = (int)(0xFFFFFFFFu - (uint32_t)sh.slo[i]);
+      v = (int)(sh.shi[i] >> 32);
+      const uint64_t mb = (sh.shi[i] << 32) | (sh.slo[i] >> 32);
       m = (float)((double)(int64_t)(mb ^ 0x8000000000000000ull) * inv);
     }
     a.pool_ids[(size_t)s * P + i] = id;
@@ -1542,71 +1606,30 @@ __global__ __launch_bounds__(1024) void k_votes_pool(VoteArgs a) {
     a.pool_n[s] = pn;
     if (a.dbg_pool_n) a.dbg_pool_n[s] = pn;
   }
+  return pn;
+}
+
+
+// One block per list: exact top-k and the list's votes and mass.
+template <int D>
+__global__ __launch_bounds__(1024) void k_select(ListArgs a) {
+  __shared__ SelectShared sh;
+  __shared__ uint32_t hist[512];
+  __shared__ uint32_t res[4];
+  __shared__ uint32_t ngather;
+  __shared__ uint32_t mm[32];
+  select_list<D>(a, blockIdx.x, sh, hist, res, ngather, mm);
+}
+
+// One block per stream: the pool.
+__global__ __launch_bounds__(1024) void k_votes_pool(VoteArgs a) {
+  __shared__ PoolShared sh;
+  pool_select(a, blockIdx.x, sh);
 }
 
 // ---------------------------------------------------------------------------
-// k_gram: fp32 Gram matrix of the pool descriptors; 16 x 16 tiles, upper
-// triangle computed and mirrored.  Both tiles' descriptors are loaded into LDS
-// at once (rows padded by one word against bank conflicts).
-// ---------------------------------------------------------------------------
-struct GramArgs {
-  int pool, ld, dim, tiles;   // ld: Gram row stride, a multiple of 4
-  const float* desc[kMaxStreams];
-  const int32_t* pool_ids;
-  const int32_t* pool_n;
-  float* gram;          // [S][pool][pool]
-};
-
-__global__ __launch_bounds__(256) void k_gram(GramArgs a) {
-  __shared__ float xi[16 * (kMaxDescDim + 1)];
-  __shared__ float xj[16 * (kMaxDescDim + 1)];
-  const int s = blockIdx.x / (a.tiles * a.tiles);
-  const int t = blockIdx.x % (a.tiles * a.tiles);
-  const int ti = t / a.tiles, tj = t % a.tiles;
-  const int pn = a.pool_n[s];
-  if (tj < ti || ti * 16 >= pn || tj * 16 >= pn) return;
-  const int dim = a.dim, ld = dim + 1;
-  const int32_t* ids = a.pool_ids + (size_t)s * a.pool;
-  const float* D = a.desc[s];
-  // 32 rows of dim floats, read as float4 (dim % 4 == 0), 8 loads in flight per thread
-  const int nv = 32 * (dim / 4);
-  for (int b = 0; b < nv; b += 8 * blockDim.x) {
-    float4 x[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int i = b + u * blockDim.x + threadIdx.x;
-      const int rr = i / (dim / 4), e4 = i - rr * (dim / 4);
-      const int p = rr < 16 ? ti * 16 + rr : tj * 16 + (rr - 16);
-      x[u] = (i < nv && p < pn) ? *reinterpret_cast<const float4*>(D + (size_t)ids[p] * dim + 4 * e4)
-                                : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int i = b + u * blockDim.x + threadIdx.x;
-      if (i < nv) {
-        const int rr = i / (dim / 4), e4 = i - rr * (dim / 4);
-        float* dst = (rr < 16 ? xi + rr * ld : xj + (rr - 16) * ld) + 4 * e4;
-        dst[0] = x[u].x; dst[1] = x[u].y; dst[2] = x[u].z; dst[3] = x[u].w;
-      }
-    }
-  }
-  __syncthreads();
-  const int r = threadIdx.x >> 4, c = threadIdx.x & 15;
-  const float* x = xi + r * ld;
-  const float* y = xj + c * ld;
-  float acc = 0.f;
-#pragma unroll 8
-  for (int e = 0; e < dim; ++e) acc = fmaf(x[e], y[e], acc);
-  const int pi = ti * 16 + r, pj = tj * 16 + c;
-  if (pi < pn && pj < pn) {
-    float* G = a.gram + (size_t)s * a.pool * a.ld;
-    G[(size_t)pi * a.ld + pj] = acc;
-    G[(size_t)pj * a.ld + pi] = acc;
-  }
-}
-
-// ---------------------------------------------------------------------------
-// k_maxmin: greedy max-min diversity (one block per stream)
+// Max-min diversity over the pool (greedy, on the Gram matrix of the pool's
+// descriptors)
 // ---------------------------------------------------------------------------
 struct MaxminArgs {
   int pool, ld, n_select;
@@ -1625,14 +1648,22 @@ struct MaxminArgs {
 // Seeded with pool rank 0; each next pick maximises its smallest distance
 // 1 - k_u.k_s to the picks so far, ties to the earlier pool rank.  Pools of up
 // to 128 frames run in one wave over the Gram matrix staged in LDS.
-__global__ __launch_bounds__(1024) void k_maxmin(MaxminArgs a) {
-  __shared__ float g_lds[kGramLdsPool * kGramLdsPool];
-  __shared__ float mind[kMaxPool];
-  __shared__ int taken[kMaxPool];
-  __shared__ int sel[kMaxSelect];
-  __shared__ float shv[16];
-  __shared__ int shi[16];
-  const int s = blockIdx.x;
+struct MaxminShared {
+  float g_lds[kGramLdsPool * kGramLdsPool];
+  float mind[kMaxPool];
+  int taken[kMaxPool];
+  int sel[kMaxSelect];
+  float shv[16];
+  int shi[16];
+};
+
+__device__ void maxmin_block(const MaxminArgs& a, int s, MaxminShared& sh) {
+  float* g_lds = sh.g_lds;
+  float* mind = sh.mind;
+  int* taken = sh.taken;
+  int* sel = sh.sel;
+  float* shv = sh.shv;
+  int* shi = sh.shi;
   const int pn = a.pool_n[s];
   const int K = min(a.n_select, pn);
   const float* G = a.gram + (size_t)s * a.pool * a.ld;
@@ -1720,6 +1751,80 @@ __global__ __launch_bounds__(1024) void k_maxmin(MaxminArgs a) {
     }
   }
   if (threadIdx.x == 0) a.out_n[s] = K;
+}
+
+__global__ __launch_bounds__(1024) void k_maxmin(MaxminArgs a) {
+  __shared__ MaxminShared sh;
+  maxmin_block(a, blockIdx.x, sh);
+}
+
+// ---------------------------------------------------------------------------
+// k_gram: fp32 Gram matrix of the pool descriptors; 16 x 16 tiles, upper
+// triangle computed and mirrored.  Both tiles' descriptors are loaded into LDS
+// at once (rows padded by one word against bank conflicts).
+// ---------------------------------------------------------------------------
+struct GramArgs {
+  int pool, ld, dim, tiles;   // ld: Gram row stride, a multiple of 4
+  const float* desc[kMaxStreams];
+  const int32_t* pool_ids;
+  const int32_t* pool_n;
+  float* gram;          // [S][pool][pool]
+};
+
+struct GramTiles {
+  float xi[16 * (kMaxDescDim + 1)];
+  float xj[16 * (kMaxDescDim + 1)];
+};
+
+__global__ __launch_bounds__(256) void k_gram(GramArgs a) {
+  __shared__ GramTiles sh;
+  float* xi = sh.xi;
+  float* xj = sh.xj;
+  const int s = blockIdx.x / (a.tiles * a.tiles);
+  const int t = blockIdx.x % (a.tiles * a.tiles);
+  const int ti = t / a.tiles, tj = t % a.tiles;
+  const int pn = a.pool_n[s];
+  if (tj < ti || ti * 16 >= pn || tj * 16 >= pn) return;
+  {
+    const int dim = a.dim, ld = dim + 1;
+    const int32_t* ids = a.pool_ids + (size_t)s * a.pool;
+    const float* D = a.desc[s];
+    // 32 rows of dim floats, read as float4 (dim % 4 == 0), 8 loads in flight per thread
+    const int nv = 32 * (dim / 4);
+    for (int b = 0; b < nv; b += 8 * blockDim.x) {
+      float4 x[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int i = b + u * blockDim.x + threadIdx.x;
+        const int rr = i / (dim / 4), e4 = i - rr * (dim / 4);
+        const int p = rr < 16 ? ti * 16 + rr : tj * 16 + (rr - 16);
+        x[u] = (i < nv && p < pn) ? *reinterpret_cast<const float4*>(D + (size_t)ids[p] * dim + 4 * e4)
+                                  : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int i = b + u * blockDim.x + threadIdx.x;
+        if (i < nv) {
+          const int rr = i / (dim / 4), e4 = i - rr * (dim / 4);
+          float* dst = (rr < 16 ? xi + rr * ld : xj + (rr - 16) * ld) + 4 * e4;
+          dst[0] = x[u].x; dst[1] = x[u].y; dst[2] = x[u].z; dst[3] = x[u].w;
+        }
+      }
+    }
+    __syncthreads();
+    const int r = threadIdx.x >> 4, c = threadIdx.x & 15;
+    const float* x = xi + r * ld;
+    const float* y = xj + c * ld;
+    float acc = 0.f;
+#pragma unroll 8
+    for (int e = 0; e < dim; ++e) acc = fmaf(x[e], y[e], acc);
+    const int pi = ti * 16 + r, pj = tj * 16 + c;
+    if (pi < pn && pj < pn) {
+      float* G = a.gram + (size_t)s * a.pool * a.ld;
+      G[(size_t)pi * a.ld + pj] = acc;
+      G[(size_t)pj * a.ld + pi] = acc;
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -2839,9 +2944,8 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
     }
   }
   if (p.ev_stop) (void)hipEventRecord(p.ev_stop, st);
-  // 5. exact top-k from candidates; 6. exact fallback for flagged lists
-  hipLaunchKernelGGL(k_select<D>, dim3(lists), dim3(1024), 0, st, la);
-  // 7. votes, mass and pool
+  // 5. exact top-k from candidates (6. exact fallback for flagged lists), each
+  // list adding its votes and mass per frame; 7. the pool
   VoteArgs va{};
   va.NL = p.NL; va.k_max = p.k_max; va.pool = p.pool; va.f_max = p.f_max;
   va.hist_stride = p.dbg_hist_stride;
@@ -2855,19 +2959,20 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   va.pool_n = p.pool_n;
   va.dbg_vote_hist = p.dbg_vote_hist; va.dbg_mass_hist = p.dbg_mass_hist;
   va.dbg_pool = p.dbg_pool; va.dbg_pool_n = p.dbg_pool_n;
+  hipLaunchKernelGGL(k_select<D>, dim3(lists), dim3(1024), 0, st, la);
   hipLaunchKernelGGL(k_votes_pool, dim3(p.S), dim3(1024), 0, st, va);
   // 8. Gram matrix, 9. max-min
   GramArgs ga{};
   ga.pool = p.pool; ga.ld = (p.pool + 3) & ~3; ga.dim = p.Hk * D; ga.tiles = cdiv(p.pool, 16);
   for (int s = 0; s < p.S; ++s) ga.desc[s] = p.st[s].desc;
   ga.pool_ids = p.pool_ids; ga.pool_n = p.pool_n; ga.gram = p.gram;
-  hipLaunchKernelGGL(k_gram, dim3(p.S * ga.tiles * ga.tiles), dim3(256), 0, st, ga);
   MaxminArgs ma{};
-  ma.pool = p.pool; ma.ld = (p.pool + 3) & ~3; ma.n_select = p.n_select;
+  ma.pool = p.pool; ma.ld = ga.ld; ma.n_select = p.n_select;
   ma.pool_ids = p.pool_ids; ma.pool_votes = p.pool_votes; ma.pool_mass = p.pool_mass;
   ma.pool_n = p.pool_n; ma.gram = p.gram;
   for (int s = 0; s < p.S; ++s) ma.frame0[s] = p.st[s].frame0;
   ma.out_ids = p.out_ids; ma.out_votes = p.out_votes; ma.out_mass = p.out_mass; ma.out_n = p.out_n;
+  hipLaunchKernelGGL(k_gram, dim3(p.S * ga.tiles * ga.tiles), dim3(256), 0, st, ga);
   hipLaunchKernelGGL(k_maxmin, dim3(p.S), dim3(1024), 0, st, ma);
   return hipGetLastError();
 }
