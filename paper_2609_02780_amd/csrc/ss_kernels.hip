@@ -2842,8 +2842,14 @@ ScoreArgs make_score_args(const RetrievePlan& p, int kind) {
   return a;
 }
 
-// Blocks of the streaming pass: as many as are resident on the device at once,
-// so that every wave takes one contiguous share of the tiles.
+// Blocks of the streaming pass: all resident at once, so that every wave takes
+// one contiguous share of the tiles; two resident blocks (8 waves) per CU.
+// Measured on gfx950, reads with about
+// 32 KiB of nontemporal loads in flight per CU reach 7.1 TB/s with 4 to 8 waves
+// per CU and only 6.8 to 6.9 TB/s with 12 to 16, and the streaming pass went
+// from 425.6 us (4 blocks per CU) to 410.4 us on the 1-hour index.
+constexpr int kStreamBlocksPerCU = 2;
+
 template <int D, bool HM>
 int stream_grid() {
   static int grid = 0;
@@ -2854,7 +2860,7 @@ int stream_grid() {
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, HM ? k_stream_hm<D> : k_stream<D>, 256, 0) != hipSuccess ||
         per_cu < 1)
       per_cu = 1;
-    grid = per_cu * cus;
+    grid = std::min(per_cu, kStreamBlocksPerCU) * cus;
   }
   return grid;
 }
