@@ -1491,8 +1491,14 @@ __device__ int pool_select(const VoteArgs& a, int s, PoolShared& sh) {
       a.dbg_vote_hist[(size_t)s * a.hist_stride + a.frame0[s] + f] = v;
       a.dbg_mass_hist[(size_t)s * a.hist_stride + a.frame0[s] + f] = (float)((double)mf * inv);
     }
+    // one LDS atomic per wave for the wave's voted frames
+    const uint64_t vm = __ballot(v >= 1);
+    uint32_t base = 0;
+    if ((threadIdx.x & 63) == (uint32_t)(__builtin_ffsll((long long)vm) - 1))
+      base = atomicAdd(&sh.nvoted, (uint32_t)__popcll(vm));
+    base = __shfl(base, __builtin_ffsll((long long)vm) - 1);
     if (v >= 1) {
-      const uint32_t slot = atomicAdd(&sh.nvoted, 1u);
+      const uint32_t slot = base + (uint32_t)__popcll(vm & ((1ull << (threadIdx.x & 63)) - 1ull));
       const uint64_t mb = (uint64_t)mf ^ 0x8000000000000000ull;
       const uint64_t h = ((uint64_t)(uint32_t)v << 32) | (mb >> 32);
       const uint64_t l = (mb << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)f);
@@ -1580,12 +1586,23 @@ __device__ int pool_select(const VoteArgs& a, int s, PoolShared& sh) {
     }
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < pn; i += blockDim.x) {
-    const uint64_t h = sh.ghi[i], l = sh.glo[i];
+  // rank by counting, 8 threads per record (pn <= kMaxPool = 256 = blockDim / 8 * 2)
+  for (int i0 = 0; i0 < pn; i0 += (int)blockDim.x / 8) {
+    const int i = i0 + (int)threadIdx.x / 8, part = threadIdx.x & 7;
     int rank = 0;
-    for (int j = 0; j < pn; ++j) rank += rec_less(h, l, sh.ghi[j], sh.glo[j]);
-    sh.shi[rank] = h;   // records are distinct: ranks form a permutation
-    sh.slo[rank] = l;
+    uint64_t h = 0, l = 0;
+    if (i < pn) {
+      h = sh.ghi[i];
+      l = sh.glo[i];
+      for (int j = part; j < pn; j += 8) rank += rec_less(h, l, sh.ghi[j], sh.glo[j]);
+    }
+    rank += __shfl_xor(rank, 1);
+    rank += __shfl_xor(rank, 2);
+    rank += __shfl_xor(rank, 4);
+    if (i < pn && part == 0) {
+      sh.shi[rank] = h;   // records are distinct: ranks form a permutation
+      sh.slo[rank] = l;
+    }
   }
   __syncthreads();
   for (int i = threadIdx.x; i < P; i += blockDim.x) {
@@ -1789,12 +1806,12 @@ __global__ __launch_bounds__(256) void k_gram(GramArgs a) {
     const int dim = a.dim, ld = dim + 1;
     const int32_t* ids = a.pool_ids + (size_t)s * a.pool;
     const float* D = a.desc[s];
-    // 32 rows of dim floats, read as float4 (dim % 4 == 0), 8 loads in flight per thread
+    // 32 rows of dim floats, read as float4 (dim % 4 == 0), 16 loads in flight per thread
     const int nv = 32 * (dim / 4);
-    for (int b = 0; b < nv; b += 8 * blockDim.x) {
-      float4 x[8];
+    for (int b = 0; b < nv; b += 16 * blockDim.x) {
+      float4 x[16];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
+      for (int u = 0; u < 16; ++u) {
         const int i = b + u * blockDim.x + threadIdx.x;
         const int rr = i / (dim / 4), e4 = i - rr * (dim / 4);
         const int p = rr < 16 ? ti * 16 + rr : tj * 16 + (rr - 16);
@@ -1802,7 +1819,7 @@ __global__ __launch_bounds__(256) void k_gram(GramArgs a) {
                                   : make_float4(0.f, 0.f, 0.f, 0.f);
       }
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
+      for (int u = 0; u < 16; ++u) {
         const int i = b + u * blockDim.x + threadIdx.x;
         if (i < nv) {
           const int rr = i / (dim / 4), e4 = i - rr * (dim / 4);
@@ -1815,9 +1832,16 @@ __global__ __launch_bounds__(256) void k_gram(GramArgs a) {
     const int r = threadIdx.x >> 4, c = threadIdx.x & 15;
     const float* x = xi + r * ld;
     const float* y = xj + c * ld;
-    float acc = 0.f;
-#pragma unroll 8
-    for (int e = 0; e < dim; ++e) acc = fmaf(x[e], y[e], acc);
+    // four chains over the dims e = 0, 1, 2, 3 mod 4 (dim % 4 == 0), added in a fixed order
+    float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+#pragma unroll 4
+    for (int e = 0; e < dim; e += 4) {
+      a0 = fmaf(x[e], y[e], a0);
+      a1 = fmaf(x[e + 1], y[e + 1], a1);
+      a2 = fmaf(x[e + 2], y[e + 2], a2);
+      a3 = fmaf(x[e + 3], y[e + 3], a3);
+    }
+    const float acc = (a0 + a1) + (a2 + a3);
     const int pi = ti * 16 + r, pj = tj * 16 + c;
     if (pi < pn && pj < pn) {
       float* G = a.gram + (size_t)s * a.pool * a.ld;
