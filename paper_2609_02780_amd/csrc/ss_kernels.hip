@@ -243,6 +243,38 @@ __device__ void find_digit(const uint32_t* hist, uint32_t need, uint32_t* res) {
   __syncthreads();
 }
 
+// Wave 0 finds, in an NB-bin histogram (NB = 64 * BPL) scanned from the top
+// bin down, the bin holding the `need`-th element: res[0..2] = bin, count
+// above it, bin count.  Ends with a barrier.
+template <int BPL>
+__device__ void find_digit_wide(const uint32_t* hist, uint32_t need, uint32_t* res) {
+  if (threadIdx.x < kWave) {
+    const int lane = threadIdx.x;
+    uint32_t hs[BPL], mine = 0;
+#pragma unroll
+    for (int j = 0; j < BPL; ++j) { hs[j] = hist[BPL * lane + j]; mine += hs[j]; }
+    uint32_t x = mine;  // inclusive suffix sum over lanes >= lane
+    for (int o = 1; o < kWave; o <<= 1) {
+      const uint32_t y = __shfl_down(x, o);
+      if (lane + o < kWave) x += y;
+    }
+    const uint32_t above = x - mine;
+    if (above < need && need <= above + mine) {
+      uint32_t a = above;
+      for (int j = BPL - 1; j >= 0; --j) {
+        if (need <= a + hs[j]) {
+          res[0] = BPL * lane + j;
+          res[1] = a;
+          res[2] = hs[j];
+          break;
+        }
+        a += hs[j];
+      }
+    }
+  }
+  __syncthreads();
+}
+
 // r-th largest (1-based) of n uint32 values given by get(i).  Returns it and the
 // number of values strictly greater.  hist: LDS [256]; res: LDS [4].
 template <class Get>
@@ -1014,18 +1046,37 @@ __device__ void block_minmax_u32(uint32_t& mn, uint32_t& mx, uint32_t* sh) {
 
 // Exact r-th largest (1 <= r <= #valid) of the values the block holds in
 // registers, all in [lo, hi]: radix selection over the value range, 8 bits of
-// (v - lo) per round, so about three rounds for scores of one sign and
-// exponent band.  Returns the value; `n_greater` and `n_equal` count the valid
-// values above it and equal to it.  `hist` holds 512 words.
-template <int N>
+// (v - lo) per round, so about three rounds for scores of one sign and exponent
+// band.  WIDE: the first round takes 11 bits (2048 bins spread the bulk of many
+// values, which keeps same-bin LDS atomics rare, and saves a round).  Returns
+// the value; `n_greater` and `n_equal` count the valid values above it and
+// equal to it.  `hist` holds 512 words, kSelHist when WIDE.
+constexpr int kSelHist = 2048 + 512;
+template <int N, bool WIDE>
 __device__ uint32_t block_select_range(const uint32_t (&v)[N], const bool (&ok)[N], uint32_t lo,
                                        uint32_t hi, uint32_t r, uint32_t* hist, uint32_t* res,
                                        uint32_t& n_greater, uint32_t& n_equal) {
-  for (int i = threadIdx.x; i < 512; i += blockDim.x) hist[i] = 0;
+  uint32_t* wide = hist + 512;
+  for (int i = threadIdx.x; i < (WIDE ? kSelHist : 512); i += blockDim.x) hist[i] = 0;
   uint32_t need = r, eq = 0;
   bool rounds = false;
   int buf = 0;
   __syncthreads();
+  if (WIDE && lo < hi) {   // first round: 11 bits
+    const uint32_t span = hi - lo;
+    const int bits = 32 - __clz(span);
+    const int shift = bits > 11 ? bits - 11 : 0;
+#pragma unroll
+    for (int i = 0; i < N; ++i)
+      if (ok[i] && v[i] >= lo && v[i] <= hi) atomicAdd(&wide[(v[i] - lo) >> shift], 1u);
+    __syncthreads();
+    find_digit_wide<32>(wide, need, res);
+    need -= res[1];
+    eq = res[2];
+    lo += res[0] << shift;
+    hi = (uint32_t)min((uint64_t)hi, (uint64_t)lo + (((uint64_t)1 << shift) - 1));
+    rounds = true;
+  }
   while (lo < hi) {
     const uint32_t span = hi - lo;
     const int bits = 32 - __clz(span);              // span < 2^bits
@@ -1111,20 +1162,22 @@ __device__ __forceinline__ int frame_of_row(const ListArgs& a, int s, uint32_t r
 // mode 1 sums the KV heads' columns); with 2% headroom for fp32 rounding this
 // bounds all E = NL * kk selected scores of the stream, and at scale 2^x with
 // x = 61 - e - c (bound < 2^e, E <= 2^c) any sum of them stays below 2^61.
-__device__ void stream_exponent(const ListArgs& a, int s, float* red) {
+// Run by wave 0 of the block alone (no block barrier).
+__device__ void stream_exponent(const ListArgs& a, int s) {
+  if (threadIdx.x >= kWave) return;
   const int L = a.L, Hk = a.Hk;
   const float* qc = a.qcol + (size_t)s * L * Hk * 16;
   float b = 0.f;
   if (a.head_mode == 0) {
-    for (int i = threadIdx.x; i < L * Hk * 16; i += blockDim.x) b = fmaxf(b, qc[i]);
+    for (int i = threadIdx.x; i < L * Hk * 16; i += kWave) b = fmaxf(b, qc[i]);
   } else {
-    for (int l = threadIdx.x; l < L; l += blockDim.x) {
+    for (int l = threadIdx.x; l < L; l += kWave) {
       float t = 0.f;
       for (int g = 0; g < Hk; ++g) t += qc[(l * Hk + g) * 16];
       b = fmaxf(b, t);
     }
   }
-  b = block_max(b, red);
+  b = __uint_as_float(wave_max_u32(__float_as_uint(b)));   // non-negative: ordered as integers
   if (threadIdx.x == 0) {
     const float bound = b * __uint_as_float(*a.kmax[s]) * 1.02f;
     const int E = a.NL * a.kk[s];
@@ -1145,7 +1198,7 @@ __device__ void stream_exponent(const ListArgs& a, int s, float* red) {
 // stream also clear its frame accumulators, and its first block fixes the
 // stream's mass exponent.
 __global__ __launch_bounds__(1024) void k_thresh(ListArgs a) {
-  __shared__ uint32_t hist[512];
+  __shared__ uint32_t hist[kSelHist];
   __shared__ uint32_t res[4];
   __shared__ uint32_t mm[32];
   const int list = blockIdx.x, s = list / a.NL, ll = list - s * a.NL;
@@ -1162,7 +1215,7 @@ __global__ __launch_bounds__(1024) void k_thresh(ListArgs a) {
       mg[f] = 0;
     }
   }
-  if (ll == 0) stream_exponent(a, s, reinterpret_cast<float*>(mm));
+  if (ll == 0) stream_exponent(a, s);
   if (m == 0 || r == 0) {
     if (threadIdx.x == 0) a.tau[list] = 0xFFFFFFFFu;
     return;
@@ -1180,7 +1233,7 @@ __global__ __launch_bounds__(1024) void k_thresh(ListArgs a) {
   }
   block_minmax_u32(mn, mx, mm);
   uint32_t ng, ne;
-  const uint32_t t = block_select_range(x, ok, mn, mx, (uint32_t)r, hist, res, ng, ne);
+  const uint32_t t = block_select_range<kThrItems, true>(x, ok, mn, mx, (uint32_t)r, hist, res, ng, ne);
   if (threadIdx.x == 0) a.tau[list] = t;
 }
 
@@ -1386,7 +1439,7 @@ __device__ void select_list(const ListArgs& a, int list, SelectShared& sh, uint3
     }
     block_minmax_u32(mn, mx, mm);
     uint32_t n_gt, n_eq;
-    const uint32_t vstar = block_select_range(u, ok, mn, mx, (uint32_t)kk, hist, res, n_gt, n_eq);
+    const uint32_t vstar = block_select_range<kSelItems, false>(u, ok, mn, mx, (uint32_t)kk, hist, res, n_gt, n_eq);
     const uint32_t need = (uint32_t)kk - n_gt;
     uint32_t wcut = 0;  // ties with w >= wcut (the `need` lowest rows) are taken
     if (n_eq > need) {
@@ -1398,7 +1451,7 @@ __device__ void select_list(const ListArgs& a, int list, SelectShared& sh, uint3
       }
       block_minmax_u32(wmin, wmax, mm);
       uint32_t g2, e2;
-      wcut = block_select_range(w, tie, wmin, wmax, need, hist, res, g2, e2);
+      wcut = block_select_range<kSelItems, false>(w, tie, wmin, wmax, need, hist, res, g2, e2);
     }
 #pragma unroll
     for (int it = 0; it < kSelItems; ++it) {
