@@ -250,6 +250,24 @@ def test_ragged_batch_one_call():
         log(s, rep)
 
 
+def test_pool_cut_many_ties():
+    """One selected row per list over 256 lists of an 800-frame stream: almost
+    every voted frame has a single vote, so more than 128 frames tie at the
+    pool's cut and the pool falls back to the radix cut over the (votes, mass,
+    frame) records; checked against the oracle stage by stage."""
+    cfg = W.Config("ties", 8, 32, 8, 64, 4, 2, 1, 16, n_frames=800, n_planted=0)
+    spec = W.stream_specs(cfg)[0]
+    q, keys = W.make_stream(cfg, spec)
+    g, o = make_pair(cfg, spec, keys)
+    out = debug_run([g], [q], cfg.top_k, cfg.n_select)
+    v = out["vote_hist"][0, :spec.n_frames]
+    P = 4 * cfg.n_select
+    vstar = np.sort(v)[::-1][P - 1]
+    assert vstar >= 1 and np.count_nonzero(v == vstar) > 128   # the radix cut ran
+    rep = staged_check(o, q, out, 0, cfg.top_k, cfg.n_select)
+    log(rep)
+
+
 def test_deterministic_repeat():
     cfg, spec, q, keys = c1()
     gidx, _ = make_pair(cfg, spec, keys)
