@@ -132,14 +132,50 @@ constexpr int kSampleChunk = 128;
 
 // Expected candidates per list: 3k (at least 1024), raised for very long lists
 // so the sample stays within the register select (kSampleMax rows).  The count
-// behaves like E Gamma(r) / r: with r = 32 it falls below k = E/3 with
-// probability 1e-7 per list and exceeds the capacity 3E with 1e-10; either case
-// takes the exact fallback.  A smaller E keeps fewer tiles on the candidate
-// path of the streaming pass; a smaller r a smaller sample.
+// behaves like E Gamma(r) / r; it falls below k with probability
+// P(Poisson(r k / E) >= r) (about 1e-7 per list for r = 32, E = 3k) and exceeds
+// the capacity 3E with far less; either case takes the exact fallback.  A
+// smaller E keeps fewer tiles on the candidate path of the streaming pass; a
+// smaller r a smaller sample.
 constexpr int64_t kSampleMax = 16384;
 int64_t expected_candidates(int64_t n, int64_t kk) {
   const int64_t r = std::min<int64_t>(kk, kSampleRank);
   return std::max<int64_t>({3 * kk, 1024, (n * r + kSampleMax - 1) / kSampleMax});
+}
+
+// P(X >= r) for X ~ Poisson(lam): the terms from r upward, in log space.
+double poisson_tail(double lam, int r) {
+  if (lam <= 0.0) return r <= 0 ? 1.0 : 0.0;
+  double term = std::exp(-lam + r * std::log(lam) - std::lgamma(r + 1.0)), sum = 0.0;
+  for (int i = r; i < r + 2000 && term > 1e-300; ++i) {
+    sum += term;
+    term *= lam / (i + 1);
+  }
+  return sum;
+}
+
+// P(X <= r) for X ~ Poisson(lam).
+double poisson_cdf(double lam, int r) {
+  if (r < 0) return 0.0;
+  double term = std::exp(-lam), sum = 0.0;
+  for (int i = 0; i <= r; ++i) {
+    sum += term;
+    term *= lam / (i + 1);
+  }
+  return std::min(sum, 1.0);
+}
+
+// The smallest sample rank r <= min(k, 32) whose chances of too few candidates,
+// P(Poisson(r k / E) >= r), and of more than the capacity (at least 3E),
+// P(Poisson(3 r) <= r - 1), are both at most kFallbackOdds per list.
+constexpr double kFallbackOdds = 2e-7;
+int64_t sample_rank(int64_t kk, int64_t E) {
+  const int64_t rmax = std::min<int64_t>(kk, kSampleRank);
+  for (int64_t r = 1; r < rmax; ++r)
+    if (poisson_tail((double)r * (double)kk / (double)E, (int)r) <= kFallbackOdds &&
+        poisson_cdf(3.0 * (double)r, (int)r - 1) <= kFallbackOdds)
+      return r;
+  return rmax;
 }
 
 struct StreamSizes {
@@ -148,16 +184,17 @@ struct StreamSizes {
 
 // Sample plan of one list.  With m sampled rows spread evenly over n rows and the
 // cut-off at the r-th largest sample score, about r n / m rows score at or above
-// it (the expected candidate count E).  r = min(k, 32); m = n gives an exact
-// cut (r = k) for small lists.
+// it (the expected candidate count E).  r from sample_rank (32 when E = 3k,
+// fewer when E is a larger multiple of k); m = n gives an exact cut (r = k)
+// for small lists.
 StreamSizes plan_stream(int64_t n, int64_t f, int top_k) {
   StreamSizes z{};
   z.n = (int)n;
   z.f = (int)f;
   z.kk = (int)std::min<int64_t>(top_k, n);
   if (n == 0) return z;
-  int64_t r = std::min<int64_t>(z.kk, kSampleRank);
   const int64_t E = expected_candidates(n, z.kk);
+  int64_t r = sample_rank(z.kk, E);
   int64_t m = std::max<int64_t>(r, (n * r + E - 1) / E);
   if (n <= kFullScanRows || (2 * m >= n && n <= kSampleMax)) {
     m = n;

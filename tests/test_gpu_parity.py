@@ -156,6 +156,38 @@ def test_fallback_too_many_candidates():
     assert rep["end_to_end_equal"]
 
 
+def _poisson_tail(lam, r):
+    """P(X >= r), X ~ Poisson(lam)."""
+    term = math.exp(-lam + r * math.log(lam) - math.lgamma(r + 1))
+    tot, i = 0.0, r
+    while term > 1e-300 and i < r + 2000:
+        tot += term
+        term *= lam / (i + 1)
+        i += 1
+    return tot
+
+
+def _poisson_cdf(lam, r):
+    """P(X <= r), X ~ Poisson(lam)."""
+    term, tot = math.exp(-lam), 0.0
+    for i in range(r + 1):
+        tot += term
+        term *= lam / (i + 1)
+    return min(tot, 1.0)
+
+
+def _sample_plan(n, k):
+    """The library's sample plan of one list of n rows (rank r, expected
+    candidates E, sampled rows m), mirrored here to plant scores on its lattice."""
+    E = max(3 * k, 1024, -(-n * min(k, 32) // 16384))
+    r = min(k, 32)
+    for rr in range(1, min(k, 32)):
+        if _poisson_tail(rr * k / E, rr) <= 2e-7 and _poisson_cdf(3.0 * rr, rr - 1) <= 2e-7:
+            r = rr
+            break
+    return r, E, max(r, -(-n * r // E))
+
+
 def test_fallback_too_few_candidates():
     """Rows on the sample lattice score highest, so the sample cut-off keeps fewer
     than k rows; the exact fallback must take over and match the oracle."""
@@ -163,9 +195,7 @@ def test_fallback_too_few_candidates():
     L, Hq, Hk, d, T, F = 1, 1, 1, 64, 100, 1000
     n = F * T
     k = 512
-    r = min(k, 32)
-    E = max(3 * k, 1024, -(-n * r // 16384))   # the library's expected candidate count
-    m = max(r, -(-n * r // E))
+    r, E, m = _sample_plan(n, k)
     step = (n << 32) // m                     # the library's sample lattice, 32.32 fixed point
     rows = (np.arange(m, dtype=np.uint64) * np.uint64(step) + np.uint64(step >> 1)) >> np.uint64(32)
     rows = rows.astype(np.int64)
