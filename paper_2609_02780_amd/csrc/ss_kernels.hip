@@ -570,6 +570,17 @@ __device__ __forceinline__ void emit(const ScoreArgs& a, int s, int list, bool c
   }
 }
 
+// The value of lane ^ 16 / lane ^ 32 (whole wave active): gfx950's row swaps
+// exchange rows of 16 lanes in registers.
+__device__ __forceinline__ int lane_xor16(int x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  return ((threadIdx.x >> 4) & 1) ? (int)r[0] : (int)r[1];
+}
+__device__ __forceinline__ int lane_xor32(int x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+  return ((threadIdx.x >> 5) & 1) ? (int)r[0] : (int)r[1];
+}
+
 // Candidates of the streaming pass wait in LDS, kStage per (wave, column), and
 // go to the list's global buffer in one flush: one global atomic per (wave,
 // column, flush) keeps returning atomics out of the tile loop.  `lc` is the
@@ -578,13 +589,13 @@ constexpr int kStage = 32;
 
 __device__ __forceinline__ void stage_flush(const ScoreArgs& a, int list, bool colv, int col, int kg,
                                             const uint64_t* st, int& lc) {
-  const int lane = threadIdx.x & (kWave - 1);
   __builtin_amdgcn_wave_barrier();
-  uint32_t base = 0;
-  if (kg == 0 && colv && lc > 0) base = atomicAdd(&a.cnt[list], (uint32_t)lc);
-  base = (uint32_t)__shfl((int)base, lane & 15);
+  int base = 0;   // set in the column's kg = 0 lane only, then summed over its four lanes
+  if (kg == 0 && colv && lc > 0) base = (int)atomicAdd(&a.cnt[list], (uint32_t)lc);
+  base += lane_xor16(base);
+  base += lane_xor32(base);
   for (int e = kg; e < lc; e += 4) {
-    const uint32_t slot = base + (uint32_t)e;
+    const uint32_t slot = (uint32_t)base + (uint32_t)e;
     if (slot < (uint32_t)a.cap) a.cand[(size_t)list * a.cap + slot] = st[col * kStage + e];
   }
   __builtin_amdgcn_wave_barrier();
@@ -607,11 +618,11 @@ __device__ __forceinline__ void stream_emit(const ScoreArgs& a, int list, bool c
     c += pass[j];
   }
   if (__ballot(c > 0) == 0) return;
-  // the column's four lanes agree on a slot range, in kg order
-  const int ln = threadIdx.x & (kWave - 1);
-  const int c16 = __builtin_amdgcn_ds_bpermute((ln ^ 16) << 2, c);
-  const int c32 = __builtin_amdgcn_ds_bpermute((ln ^ 32) << 2, c);
-  const int c48 = __builtin_amdgcn_ds_bpermute((ln ^ 48) << 2, c);
+  // the column's four lanes (lanes col + 16 kg) agree on a slot range, in kg
+  // order; their counts travel by row swaps in registers
+  const int c16 = lane_xor16(c);
+  const int c32 = lane_xor32(c);
+  const int c48 = lane_xor32(c16);
   const int total = c + c16 + c32 + c48;
   const int prefix = kg == 0 ? 0 : kg == 1 ? c16 : kg == 2 ? c32 + c48 : c16 + c32 + c48;
   if (__any(lc + total > kStage)) stage_flush(a, list, colv, col, kg, st, lc);
