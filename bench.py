@@ -122,6 +122,34 @@ def time_append(torch, P, cfg, frames=64):
             "batch_frames_per_s": frames / (batch_ms / 1e3)}
 
 
+def time_cold(torch, P, r, queries, key_bytes, calls=20, scratch_bytes=512 << 20):
+    """Cold-cache retrieval: before each call a 512 MB scratch buffer is written,
+    which evicts the index from L2 and the 256 MB Infinity Cache; the call and its
+    streaming kernel are timed with HIP events (the scratch writes are outside)."""
+    scratch = torch.empty(scratch_bytes // 4, dtype=torch.int32, device="cuda")
+    lat, hot = [], []
+    for i in range(calls + 2):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        for x in e:   # torch reads elapsed times only of events it has recorded once
+            x.record()
+        scratch.fill_(i)
+        P.set_profile_events(e[2], e[3])
+        e[0].record()
+        r(queries)
+        e[1].record()
+        P.set_profile_events(None, None)
+        torch.cuda.synchronize()
+        if i >= 2:
+            lat.append(e[0].elapsed_time(e[1]))
+            hot.append(e[2].elapsed_time(e[3]))
+    del scratch
+    hot_ms = float(np.mean(hot))
+    return {"p50_latency_ms": float(np.percentile(lat, 50)), "p10_latency_ms": float(np.percentile(lat, 10)),
+            "p90_latency_ms": float(np.percentile(lat, 90)), "avg_kernel_ms": hot_ms,
+            "kernel_gbs": key_bytes / (hot_ms / 1e3) / 1e9, "calls": calls,
+            "scratch_bytes": scratch_bytes}
+
+
 def time_evidence(torch, P, idxs, frame_ids, calls=20):
     """Evidence assembly after the retrieval, with the paper's settings: 6
     recent units and one preceding unit per selected unit."""
@@ -308,6 +336,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="C4", choices=sorted(W.CONFIGS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cold", action="store_true",
+                    help="also time cold-cache calls (on by default for indices of at most 1 GiB)")
     ap.add_argument("--sweep", action="store_true",
                     help="history-length sweep (64..3600 frames of the workload's shape) instead of the benchmark")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -412,6 +442,8 @@ def main():
                      "event_samples": len(hot)},
     }
     out["evidence"] = time_evidence(torch, P, idxs, r.frame_ids)
+    if args.cold or key_bytes <= (1 << 30):   # indices that a warm Infinity Cache could hold
+        out["cold"] = time_cold(torch, P, r, queries, key_bytes)
     if cfg.compress is not None:
         out["append"] = time_append(torch, P, cfg)
     if not args.no_cpu_baseline:
