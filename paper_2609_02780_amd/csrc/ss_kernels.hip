@@ -43,6 +43,7 @@
 #include <climits>
 #include <cmath>
 #include <cstdint>
+#include <utility>
 
 namespace ss {
 namespace {
@@ -1548,26 +1549,41 @@ __device__ int pool_select(const VoteArgs& a, int s, PoolShared& sh) {
   const double inv = ldexp(1.0, -a.sexp[s]);
   uint64_t* rh = a.rec_hi + (size_t)s * a.f_max;
   uint64_t* rl = a.rec_lo + (size_t)s * a.f_max;
-  for (int f = threadIdx.x; f < F; f += blockDim.x) {
-    const int v = votes[f];
-    const int64_t mf = massfx[f];
-    if (a.dbg_vote_hist) {
-      a.dbg_vote_hist[(size_t)s * a.hist_stride + a.frame0[s] + f] = v;
-      a.dbg_mass_hist[(size_t)s * a.hist_stride + a.frame0[s] + f] = (float)((double)mf * inv);
+  // four frames per thread per pass, their loads issued together; every lane of a
+  // wave takes part in the ballots (frames past F count as unvoted)
+  for (int f0 = 0; f0 < F; f0 += 4 * (int)blockDim.x) {
+    int vv[4];
+    int64_t mm[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int f = f0 + u * (int)blockDim.x + (int)threadIdx.x;
+      vv[u] = f < F ? votes[f] : 0;
+      mm[u] = f < F ? massfx[f] : 0;
     }
-    // one LDS atomic per wave for the wave's voted frames
-    const uint64_t vm = __ballot(v >= 1);
-    uint32_t base = 0;
-    if ((threadIdx.x & 63) == (uint32_t)(__builtin_ffsll((long long)vm) - 1))
-      base = atomicAdd(&sh.nvoted, (uint32_t)__popcll(vm));
-    base = __shfl(base, __builtin_ffsll((long long)vm) - 1);
-    if (v >= 1) {
-      const uint32_t slot = base + (uint32_t)__popcll(vm & ((1ull << (threadIdx.x & 63)) - 1ull));
-      const uint64_t mb = (uint64_t)mf ^ 0x8000000000000000ull;
-      const uint64_t h = ((uint64_t)(uint32_t)v << 32) | (mb >> 32);
-      const uint64_t l = (mb << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)f);
-      if (slot < (uint32_t)kPoolSort) { sh.shi[slot] = h; sh.slo[slot] = l; }
-      else { rh[slot] = h; rl[slot] = l; }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int f = f0 + u * (int)blockDim.x + (int)threadIdx.x;
+      const int v = vv[u];
+      const int64_t mf = mm[u];
+      if (a.dbg_vote_hist && f < F) {
+        a.dbg_vote_hist[(size_t)s * a.hist_stride + a.frame0[s] + f] = v;
+        a.dbg_mass_hist[(size_t)s * a.hist_stride + a.frame0[s] + f] = (float)((double)mf * inv);
+      }
+      // one LDS atomic per wave for the wave's voted frames
+      const uint64_t vm = __ballot(v >= 1);
+      if (vm == 0) continue;
+      const int first = __builtin_ffsll((long long)vm) - 1;
+      uint32_t base = 0;
+      if ((threadIdx.x & 63) == (uint32_t)first) base = atomicAdd(&sh.nvoted, (uint32_t)__popcll(vm));
+      base = __shfl(base, first);
+      if (v >= 1) {
+        const uint32_t slot = base + (uint32_t)__popcll(vm & ((1ull << (threadIdx.x & 63)) - 1ull));
+        const uint64_t mb = (uint64_t)mf ^ 0x8000000000000000ull;
+        const uint64_t h = ((uint64_t)(uint32_t)v << 32) | (mb >> 32);
+        const uint64_t l = (mb << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)f);
+        if (slot < (uint32_t)kPoolSort) { sh.shi[slot] = h; sh.slo[slot] = l; }
+        else { rh[slot] = h; rl[slot] = l; }
+      }
     }
   }
   if (a.dbg_vote_hist) {
@@ -1577,7 +1593,6 @@ __device__ int pool_select(const VoteArgs& a, int s, PoolShared& sh) {
       a.dbg_mass_hist[(size_t)s * a.hist_stride + f] = 0.f;
     }
   }
-  __threadfence();
   __syncthreads();
   const int n_voted = (int)sh.nvoted;
   const int P = a.pool;
@@ -1585,7 +1600,7 @@ __device__ int pool_select(const VoteArgs& a, int s, PoolShared& sh) {
   const bool in_lds = n_voted <= kPoolSort;
   if (!in_lds) {   // the records beyond the LDS part live in global memory only
     for (int i = threadIdx.x; i < kPoolSort; i += blockDim.x) { rh[i] = sh.shi[i]; rl[i] = sh.slo[i]; }
-    __threadfence();
+    __threadfence();   // every record, from any thread, visible to the reads below
     __syncthreads();
   }
   auto get = [&](int i, uint64_t& h, uint64_t& l) {
@@ -1728,9 +1743,11 @@ struct MaxminArgs {
 
 // Seeded with pool rank 0; each next pick maximises its smallest distance
 // 1 - k_u.k_s to the picks so far, ties to the earlier pool rank.  Pools of up
-// to 128 frames run in one wave over the Gram matrix staged in LDS.
+// to 128 frames run in one wave over the distances staged in LDS as
+// order-preserving words (so the running minimum and the argmax are integer
+// operations on the same fp32 values).
 struct MaxminShared {
-  float g_lds[kGramLdsPool * kGramLdsPool];
+  uint32_t d_lds[kGramLdsPool * kGramLdsPool];
   float mind[kMaxPool];
   int taken[kMaxPool];
   int sel[kMaxSelect];
@@ -1739,7 +1756,7 @@ struct MaxminShared {
 };
 
 __device__ void maxmin_block(const MaxminArgs& a, int s, MaxminShared& sh) {
-  float* g_lds = sh.g_lds;
+  uint32_t* d_lds = sh.d_lds;
   float* mind = sh.mind;
   int* taken = sh.taken;
   int* sel = sh.sel;
@@ -1749,49 +1766,52 @@ __device__ void maxmin_block(const MaxminArgs& a, int s, MaxminShared& sh) {
   const int K = min(a.n_select, pn);
   const float* G = a.gram + (size_t)s * a.pool * a.ld;
   if (pn <= kGramLdsPool) {
-    // rows of the Gram matrix as float4 (ld % 4 == 0), every load in flight at once
-    const int c4n = (pn + 3) / 4;
-    for (int b = 0; b < pn * c4n; b += 4 * blockDim.x) {
+    // row r, column c < 128: ord(1 - g_rc) for c < pn, else 0 (below every
+    // distance word, like a frame already picked).  Rows are read as float4 from
+    // clamped in-bounds addresses (ld % 4 == 0 and ld >= pool >= pn); what a
+    // clamped read returns is never used.
+    constexpr int C4 = kGramLdsPool / 4;
+    for (int b = 0; b < pn * C4; b += 4 * blockDim.x) {
       float4 x[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const int i = b + u * blockDim.x + threadIdx.x;
-        const int r = i / c4n, c4 = i - r * c4n;
-        x[u] = i < pn * c4n ? *reinterpret_cast<const float4*>(G + (size_t)r * a.ld + 4 * c4)
-                            : make_float4(0.f, 0.f, 0.f, 0.f);
+        const int i = min(b + u * (int)blockDim.x + (int)threadIdx.x, pn * C4 - 1);
+        const int r = i / C4, c = min(4 * (i - r * C4), a.ld - 4);
+        x[u] = *reinterpret_cast<const float4*>(G + (size_t)r * a.ld + c);
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int i = b + u * blockDim.x + threadIdx.x;
-        if (i < pn * c4n) {
-          const int r = i / c4n, c = 4 * (i - r * c4n);
+        if (i < pn * C4) {
+          const int r = i / C4, c = 4 * (i - r * C4);
           const float xv[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
+          uint4 o;
+          uint32_t* ov = reinterpret_cast<uint32_t*>(&o);
 #pragma unroll
-          for (int q = 0; q < 4; ++q)
-            if (c + q < pn) g_lds[r * pn + c + q] = xv[q];
+          for (int q = 0; q < 4; ++q) ov[q] = c + q < pn ? ord_u32(1.0f - xv[q]) : 0u;
+          *reinterpret_cast<uint4*>(d_lds + r * kGramLdsPool + c) = o;
         }
       }
     }
     __syncthreads();
     if (threadIdx.x < kWave) {
-      // lane l holds pool ranks l and l + 64; argmax by a DPP max over ordered
-      // values, ties to the lowest rank through ballots
+      // lane l holds pool ranks l and l + 64; picked and absent ranks hold 0, so
+      // min() keeps them out of every later argmax; argmax by a DPP max, ties
+      // to the lowest rank through ballots
       const int lane = threadIdx.x;
-      const int u0 = lane, u1 = lane + kWave;
-      float m0 = u0 < pn ? 1.0f - g_lds[u0] : -INFINITY;
-      float m1 = u1 < pn ? 1.0f - g_lds[u1] : -INFINITY;
-      bool t0 = u0 == 0 || u0 >= pn, t1 = u1 >= pn;
+      uint32_t m0 = lane == 0 ? 0u : d_lds[lane];
+      uint32_t m1 = d_lds[lane + kWave];
       if (lane == 0 && K > 0) sel[0] = 0;
       for (int it = 1; it < K; ++it) {
-        const uint32_t o0 = t0 ? 0u : ord_u32(m0), o1 = t1 ? 0u : ord_u32(m1);
-        const uint32_t best = wave_max_u32(max(o0, o1));
-        const uint64_t b0 = __ballot(!t0 && o0 == best);
-        const int bi = b0 ? __builtin_ctzll(b0) : kWave + __builtin_ctzll(__ballot(!t1 && o1 == best));
-        const float* row = g_lds + bi * pn;
-        if (u0 < pn) m0 = fminf(m0, 1.0f - row[u0]);
-        if (u1 < pn) m1 = fminf(m1, 1.0f - row[u1]);
-        t0 = t0 || u0 == bi;
-        t1 = t1 || u1 == bi;
+        const uint32_t best = wave_max_u32(max(m0, m1));
+        const uint64_t b0 = __ballot(m0 == best), b1 = __ballot(m1 == best);
+        const int bi = b0 ? __builtin_ctzll(b0) : kWave + __builtin_ctzll(b1);
+        const uint32_t* row = d_lds + bi * kGramLdsPool;
+        const uint32_t r0 = row[lane], r1 = row[lane + kWave];
+        m0 = min(m0, r0);
+        m1 = min(m1, r1);
+        m0 = lane == bi ? 0u : m0;
+        m1 = lane + kWave == bi ? 0u : m1;
         if (lane == 0) sel[it] = bi;
       }
     }
@@ -1840,80 +1860,77 @@ __global__ __launch_bounds__(1024) void k_maxmin(MaxminArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// k_gram: fp32 Gram matrix of the pool descriptors; 16 x 16 tiles, upper
-// triangle computed and mirrored.  Both tiles' descriptors are loaded into LDS
-// at once (rows padded by one word against bank conflicts).
+// k_gram: fp32 Gram matrix of the pool descriptors, one 16 x 16 tile of the
+// upper triangle per block (mirrored on store), on the fp32 MFMA 16x16x4.  Lane l
+// feeds row l & 15 of either operand with dimensions 4 (l >> 4) + j of each
+// 16-dimension step (j = 0..3, one MFMA each); each of the four waves covers a
+// quarter of the dimensions and the four partial tiles are added in wave order.
 // ---------------------------------------------------------------------------
 struct GramArgs {
-  int pool, ld, dim, tiles;   // ld: Gram row stride, a multiple of 4
+  int pool, ld, dim, tiles;   // ld: Gram row stride, a multiple of 4; dim in {64, 128, ..., 1024}
   const float* desc[kMaxStreams];
   const int32_t* pool_ids;
   const int32_t* pool_n;
-  float* gram;          // [S][pool][pool]
+  float* gram;          // [S][pool][ld]
 };
 
-struct GramTiles {
-  float xi[16 * (kMaxDescDim + 1)];
-  float xj[16 * (kMaxDescDim + 1)];
-};
-
+template <int NST>   // 16-dimension steps per wave: dim / 64
 __global__ __launch_bounds__(256) void k_gram(GramArgs a) {
-  __shared__ GramTiles sh;
-  float* xi = sh.xi;
-  float* xj = sh.xj;
+  __shared__ float part[4][256];
   const int s = blockIdx.x / (a.tiles * a.tiles);
   const int t = blockIdx.x % (a.tiles * a.tiles);
   const int ti = t / a.tiles, tj = t % a.tiles;
   const int pn = a.pool_n[s];
   if (tj < ti || ti * 16 >= pn || tj * 16 >= pn) return;
-  {
-    const int dim = a.dim, ld = dim + 1;
-    const int32_t* ids = a.pool_ids + (size_t)s * a.pool;
-    const float* D = a.desc[s];
-    // 32 rows of dim floats, read as float4 (dim % 4 == 0), 16 loads in flight per thread
-    const int nv = 32 * (dim / 4);
-    for (int b = 0; b < nv; b += 16 * blockDim.x) {
-      float4 x[16];
+  const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x >> 6;
+  constexpr int dim = 64 * NST;
+  const int32_t* ids = a.pool_ids + (size_t)s * a.pool;
+  // rows past the pool repeat its last row: they only feed tile entries that
+  // are never stored
+  const int ri = min(ti * 16 + (lane & 15), pn - 1), rj = min(tj * 16 + (lane & 15), pn - 1);
+  const float* xi = a.desc[s] + (size_t)ids[ri] * dim + w * (dim / 4) + 4 * (lane >> 4);
+  const float* xj = a.desc[s] + (size_t)ids[rj] * dim + w * (dim / 4) + 4 * (lane >> 4);
+  float4 va[NST], vb[NST];
 #pragma unroll
-      for (int u = 0; u < 16; ++u) {
-        const int i = b + u * blockDim.x + threadIdx.x;
-        const int rr = i / (dim / 4), e4 = i - rr * (dim / 4);
-        const int p = rr < 16 ? ti * 16 + rr : tj * 16 + (rr - 16);
-        x[u] = (i < nv && p < pn) ? *reinterpret_cast<const float4*>(D + (size_t)ids[p] * dim + 4 * e4)
-                                  : make_float4(0.f, 0.f, 0.f, 0.f);
-      }
+  for (int u = 0; u < NST; ++u) {
+    va[u] = *reinterpret_cast<const float4*>(xi + 16 * u);
+    vb[u] = *reinterpret_cast<const float4*>(xj + 16 * u);
+  }
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int u = 0; u < 16; ++u) {
-        const int i = b + u * blockDim.x + threadIdx.x;
-        if (i < nv) {
-          const int rr = i / (dim / 4), e4 = i - rr * (dim / 4);
-          float* dst = (rr < 16 ? xi + rr * ld : xj + (rr - 16) * ld) + 4 * e4;
-          dst[0] = x[u].x; dst[1] = x[u].y; dst[2] = x[u].z; dst[3] = x[u].w;
-        }
-      }
-    }
-    __syncthreads();
-    const int r = threadIdx.x >> 4, c = threadIdx.x & 15;
-    const float* x = xi + r * ld;
-    const float* y = xj + c * ld;
-    // four chains over the dims e = 0, 1, 2, 3 mod 4 (dim % 4 == 0), added in a fixed order
-    float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
-#pragma unroll 4
-    for (int e = 0; e < dim; e += 4) {
-      a0 = fmaf(x[e], y[e], a0);
-      a1 = fmaf(x[e + 1], y[e + 1], a1);
-      a2 = fmaf(x[e + 2], y[e + 2], a2);
-      a3 = fmaf(x[e + 3], y[e + 3], a3);
-    }
-    const float acc = (a0 + a1) + (a2 + a3);
-    const int pi = ti * 16 + r, pj = tj * 16 + c;
-    if (pi < pn && pj < pn) {
-      float* G = a.gram + (size_t)s * a.pool * a.ld;
-      G[(size_t)pi * a.ld + pj] = acc;
-      G[(size_t)pj * a.ld + pi] = acc;
-    }
+  for (int u = 0; u < NST; ++u) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(va[u].x, vb[u].x, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(va[u].y, vb[u].y, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(va[u].z, vb[u].z, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(va[u].w, vb[u].w, acc, 0, 0, 0);
+  }
+  // lane l holds tile rows 4 (l >> 4) + j, column l & 15
+#pragma unroll
+  for (int j = 0; j < 4; ++j) part[w][(4 * (lane >> 4) + j) * 16 + (lane & 15)] = acc[j];
+  __syncthreads();
+  const int r = threadIdx.x >> 4, c = threadIdx.x & 15;
+  const float v = ((part[0][threadIdx.x] + part[1][threadIdx.x]) + part[2][threadIdx.x]) + part[3][threadIdx.x];
+  const int pi = ti * 16 + r, pj = tj * 16 + c;
+  if (pi < pn && pj < pn) {
+    float* G = a.gram + (size_t)s * a.pool * a.ld;
+    G[(size_t)pi * a.ld + pj] = v;
+    G[(size_t)pj * a.ld + pi] = v;
   }
 }
+
+// k_gram<1..N> launchers indexed by dim / 64 - 1
+using GramLaunch = void (*)(dim3, const GramArgs&, hipStream_t);
+template <int NST>
+void launch_gram_n(dim3 g, const GramArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(k_gram<NST>, g, dim3(256), 0, st, a);
+}
+template <int... I>
+const GramLaunch* gram_table(std::integer_sequence<int, I...>) {
+  static const GramLaunch t[] = {&launch_gram_n<I + 1>...};
+  return t;
+}
+template <int N>
+const GramLaunch* gram_launchers() { return gram_table(std::make_integer_sequence<int, N>{}); }
 
 // ---------------------------------------------------------------------------
 // Append kernels
@@ -3066,7 +3083,8 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   ma.pool_n = p.pool_n; ma.gram = p.gram;
   for (int s = 0; s < p.S; ++s) ma.frame0[s] = p.st[s].frame0;
   ma.out_ids = p.out_ids; ma.out_votes = p.out_votes; ma.out_mass = p.out_mass; ma.out_n = p.out_n;
-  hipLaunchKernelGGL(k_gram, dim3(p.S * ga.tiles * ga.tiles), dim3(256), 0, st, ga);
+  if (ga.dim % 64 != 0 || ga.dim < 64 || ga.dim > kMaxDescDim) return hipErrorInvalidValue;
+  gram_launchers<kMaxDescDim / 64>()[ga.dim / 64 - 1](dim3(p.S * ga.tiles * ga.tiles), ga, st);
   hipLaunchKernelGGL(k_maxmin, dim3(p.S), dim3(1024), 0, st, ma);
   return hipGetLastError();
 }
