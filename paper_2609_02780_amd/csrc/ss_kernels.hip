@@ -442,27 +442,22 @@ __global__ __launch_bounds__(8 * D) void k_prep(PrepArgs a) {
   const int e0 = 8 * ec;
   for (int h = h0; h < h1; ++h) {
     const uint16_t* qh = q + (size_t)h * nq * D + e0;
-    int j = tg;
-    for (; j + 3 * kPrepGroups < nq; j += 4 * kPrepGroups) {
-      u32x4 v[4];
+    // tokens tg, tg + 4, ... in increasing order; 16 loads in flight per pass,
+    // from clamped in-bounds token indices (only tokens below nq are added)
+    for (int j0 = tg; j0 < nq; j0 += 16 * kPrepGroups) {
+      u32x4 v[16];
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-        v[u] = *reinterpret_cast<const u32x4*>(qh + (size_t)(j + u * kPrepGroups) * D);
+      for (int u = 0; u < 16; ++u)
+        v[u] = *reinterpret_cast<const u32x4*>(qh + (size_t)min(j0 + u * kPrepGroups, nq - 1) * D);
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < 16; ++u) {
+        if (j0 + u * kPrepGroups < nq) {
 #pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          acc[2 * w] += bf16_lo(v[u][w]);
-          acc[2 * w + 1] += bf16_hi(v[u][w]);
+          for (int w = 0; w < 4; ++w) {
+            acc[2 * w] += bf16_lo(v[u][w]);
+            acc[2 * w + 1] += bf16_hi(v[u][w]);
+          }
         }
-      }
-    }
-    for (; j < nq; j += kPrepGroups) {
-      const u32x4 v = *reinterpret_cast<const u32x4*>(qh + (size_t)j * D);
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        acc[2 * w] += bf16_lo(v[w]);
-        acc[2 * w + 1] += bf16_hi(v[w]);
       }
     }
   }
@@ -1088,6 +1083,35 @@ __device__ uint32_t block_select_range(const uint32_t (&v)[N], const bool (&ok)[
     lo += res[0] << shift;
     hi = (uint32_t)min((uint64_t)hi, (uint64_t)lo + (((uint64_t)1 << shift) - 1));
     rounds = true;
+    if (lo < hi && eq <= (uint32_t)kWave) {
+      // a bin of at most 64 values (the usual case for a cut in the tail of a
+      // sample) is finished by ranking its values by counting in one wave,
+      // instead of further radix rounds; the wide histogram's words hold them
+      uint32_t* vals = wide;
+      if (threadIdx.x == 0) res[3] = 0;
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < N; ++i)
+        if (ok[i] && v[i] >= lo && v[i] <= hi) vals[atomicAdd(&res[3], 1u)] = v[i];
+      __syncthreads();
+      if (threadIdx.x < kWave) {
+        const int lane = threadIdx.x;
+        const uint32_t mine = lane < (int)eq ? vals[lane] : 0u;
+        uint32_t gt = 0, ge = 0;
+        for (uint32_t j = 0; j < eq; ++j) {
+          const uint32_t o = vals[j];
+          gt += o > mine;
+          ge += o >= mine;
+        }
+        // the need-th largest t: fewer than need values above it, at least need at or above it
+        const uint64_t hit = __ballot(lane < (int)eq && gt < need && need <= ge);
+        if (lane == __builtin_ctzll(hit)) { res[0] = mine; res[1] = gt; res[2] = ge - gt; }
+      }
+      __syncthreads();
+      lo = hi = res[0];
+      need -= res[1];
+      eq = res[2];
+    }
   }
   while (lo < hi) {
     const uint32_t span = hi - lo;
@@ -1236,11 +1260,13 @@ __global__ __launch_bounds__(1024) void k_thresh(ListArgs a) {
   uint32_t x[kThrItems];
   bool ok[kThrItems];
   uint32_t mn = 0xFFFFFFFFu, mx = 0;
+  // every load issued at once, from clamped in-bounds indices (m >= 1)
+#pragma unroll
+  for (int it = 0; it < kThrItems; ++it) x[it] = __float_as_uint(v[min((int)threadIdx.x + it * 1024, m - 1)]);
 #pragma unroll
   for (int it = 0; it < kThrItems; ++it) {
-    const int i = threadIdx.x + it * 1024;
-    ok[it] = i < m;
-    x[it] = ok[it] ? ord_u32(v[i] + 0.0f) : 0u;
+    ok[it] = (int)threadIdx.x + it * 1024 < m;
+    x[it] = ok[it] ? ord_u32(__uint_as_float(x[it]) + 0.0f) : 0u;
     if (ok[it]) { mn = min(mn, x[it]); mx = max(mx, x[it]); }
   }
   block_minmax_u32(mn, mx, mm);
