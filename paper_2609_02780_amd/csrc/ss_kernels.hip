@@ -1059,6 +1059,41 @@ __device__ void block_minmax_u32(uint32_t& mn, uint32_t& mx, uint32_t* sh) {
 // the value; `n_greater` and `n_equal` count the valid values above it and
 // equal to it.  `hist` holds 512 words, kSelHist when WIDE.
 constexpr int kSelHist = 2048 + 512;
+
+// Ends a radix selection whose current bin [lo, hi] holds eq <= 64 values: they
+// are gathered into `vals` (64 words, no longer read as a histogram) and wave 0
+// ranks them by counting; the need-th largest t of the bin gives lo = hi = t,
+// need = its rank among the values equal to t, eq = their count.  res[3] is the
+// gather counter; res[0..2] carry the result.  Called by the whole block.
+template <int N>
+__device__ void finish_bin_by_counting(const uint32_t (&v)[N], const bool (&ok)[N], uint32_t& lo,
+                                       uint32_t& hi, uint32_t& need, uint32_t& eq, uint32_t* vals,
+                                       uint32_t* res) {
+  if (threadIdx.x == 0) res[3] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < N; ++i)
+    if (ok[i] && v[i] >= lo && v[i] <= hi) vals[atomicAdd(&res[3], 1u)] = v[i];
+  __syncthreads();
+  if (threadIdx.x < kWave) {
+    const int lane = threadIdx.x;
+    const uint32_t mine = lane < (int)eq ? vals[lane] : 0u;
+    uint32_t gt = 0, ge = 0;
+    for (uint32_t j = 0; j < eq; ++j) {
+      const uint32_t o = vals[j];
+      gt += o > mine;
+      ge += o >= mine;
+    }
+    // t: fewer than need values of the bin above it, at least need at or above it
+    const uint64_t hit = __ballot(lane < (int)eq && gt < need && need <= ge);
+    if (lane == __builtin_ctzll(hit)) { res[0] = mine; res[1] = gt; res[2] = ge - gt; }
+  }
+  __syncthreads();
+  lo = hi = res[0];
+  need -= res[1];
+  eq = res[2];
+}
+
 template <int N, bool WIDE>
 __device__ uint32_t block_select_range(const uint32_t (&v)[N], const bool (&ok)[N], uint32_t lo,
                                        uint32_t hi, uint32_t r, uint32_t* hist, uint32_t* res,
@@ -1083,35 +1118,9 @@ __device__ uint32_t block_select_range(const uint32_t (&v)[N], const bool (&ok)[
     lo += res[0] << shift;
     hi = (uint32_t)min((uint64_t)hi, (uint64_t)lo + (((uint64_t)1 << shift) - 1));
     rounds = true;
-    if (lo < hi && eq <= (uint32_t)kWave) {
-      // a bin of at most 64 values (the usual case for a cut in the tail of a
-      // sample) is finished by ranking its values by counting in one wave,
-      // instead of further radix rounds; the wide histogram's words hold them
-      uint32_t* vals = wide;
-      if (threadIdx.x == 0) res[3] = 0;
-      __syncthreads();
-#pragma unroll
-      for (int i = 0; i < N; ++i)
-        if (ok[i] && v[i] >= lo && v[i] <= hi) vals[atomicAdd(&res[3], 1u)] = v[i];
-      __syncthreads();
-      if (threadIdx.x < kWave) {
-        const int lane = threadIdx.x;
-        const uint32_t mine = lane < (int)eq ? vals[lane] : 0u;
-        uint32_t gt = 0, ge = 0;
-        for (uint32_t j = 0; j < eq; ++j) {
-          const uint32_t o = vals[j];
-          gt += o > mine;
-          ge += o >= mine;
-        }
-        // the need-th largest t: fewer than need values above it, at least need at or above it
-        const uint64_t hit = __ballot(lane < (int)eq && gt < need && need <= ge);
-        if (lane == __builtin_ctzll(hit)) { res[0] = mine; res[1] = gt; res[2] = ge - gt; }
-      }
-      __syncthreads();
-      lo = hi = res[0];
-      need -= res[1];
-      eq = res[2];
-    }
+    // a bin of at most 64 values (the usual case for a cut in the tail of a
+    // sample) is ranked by counting instead of further radix rounds
+    if (lo < hi && eq <= (uint32_t)kWave) finish_bin_by_counting<N>(v, ok, lo, hi, need, eq, wide, res);
   }
   while (lo < hi) {
     const uint32_t span = hi - lo;
@@ -1128,8 +1137,10 @@ __device__ uint32_t block_select_range(const uint32_t (&v)[N], const bool (&ok)[
     eq = res[2];
     lo += res[0] << shift;
     hi = (uint32_t)min((uint64_t)hi, (uint64_t)lo + (((uint64_t)1 << shift) - 1));
-    buf ^= 1;
     rounds = true;
+    // this round's histogram is read no more: it takes the values of a small bin
+    if (lo < hi && eq <= (uint32_t)kWave) finish_bin_by_counting<N>(v, ok, lo, hi, need, eq, h, res);
+    buf ^= 1;
   }
   if (!rounds) {  // every valid value equals lo
     uint32_t c = 0;
