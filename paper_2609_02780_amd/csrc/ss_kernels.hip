@@ -520,6 +520,7 @@ struct ScoreArgs {
   int cap;
   int64_t tile_base[kMaxStreams + 1];  // first tile of each stream; tiles of all streams in a row
   int32_t ntile[kMaxStreams];          // 16-row tiles per (layer, KV head) segment
+  int sgroup;                          // blocks per XCD group of the streaming pass
   // K_FULL
   const int32_t* flag;                // nullptr: write only `only_list`
   int only_list;
@@ -699,34 +700,43 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a) {
 }
 
 // Tiles of the streaming passes are numbered one after another over all
-// segments.  kStreamGroup blocks of one XCD (blocks are dealt to the 8 XCDs in
-// turn) share one contiguous range of that numbering, and their 4 kStreamGroup
-// waves take its tiles in turn, so that at any moment the group reads one
-// window of about 4 kStreamGroup tiles.  Measured on the 1-hour workload, a few
-// dozen such windows in flight read HBM faster than one private range per wave
-// (thousands of scattered streams) or one sweep by the whole grid.
-constexpr int kStreamGroup = 32;
+// segments.  `sgroup` blocks of one XCD (blocks are dealt to the 8 XCDs in
+// turn) share one contiguous range of that numbering, and their 4 sgroup waves
+// take its tiles in turn, so that at any moment the group reads one window of
+// about 4 sgroup tiles.  Measured on the 1-hour workload, a few dozen such
+// windows in flight read HBM faster than one private range per wave
+// (thousands of scattered streams) or one sweep by the whole grid: 32 blocks
+// per group (16 windows) beat 8 (64 windows) by 2%.  But every wave visits
+// every segment of its group's range, and at the end of each visit it flushes
+// its staged candidates with a returning atomic on the list's counter that all
+// the group's waves hit at about the same moment.  Where segments are short
+// against the range (the 16-stream ragged batch: 192 segments, 12 per range at
+// 32 blocks) those stalls cost 10% of the pass, and 8 blocks per group (3
+// segments per range) took it from 2,060 to 1,964 us.  The host therefore
+// takes the largest group of at most kStreamGroupMax blocks whose range spans
+// at most three average segments.
+constexpr int kStreamGroupMax = 32;
 
 struct WaveRange {
   int64_t b0, b1;   // the group's tiles
   int sw, wg;       // waves in the group, this wave's rank among them
 };
 
-__device__ __forceinline__ WaveRange wave_range(int64_t total, int wave) {
+__device__ __forceinline__ WaveRange wave_range(int64_t total, int wave, int sgroup) {
   const int64_t nb = gridDim.x, b = blockIdx.x;
   int64_t ng, grp;
   int members, rank;
-  if (nb % (8 * kStreamGroup) == 0) {
-    ng = nb / kStreamGroup;
+  if (nb % (8 * sgroup) == 0) {
+    ng = nb / sgroup;
     const int64_t x = b % 8, r = b / 8;   // XCD, and rank among its blocks
-    grp = (r / kStreamGroup) * 8 + x;
-    members = kStreamGroup;
-    rank = (int)(r % kStreamGroup);
+    grp = (r / sgroup) * 8 + x;
+    members = sgroup;
+    rank = (int)(r % sgroup);
   } else {
-    ng = (nb + kStreamGroup - 1) / kStreamGroup;
-    grp = b / kStreamGroup;
-    members = (int)min<int64_t>(kStreamGroup, nb - grp * kStreamGroup);
-    rank = (int)(b - grp * kStreamGroup);
+    ng = (nb + sgroup - 1) / sgroup;
+    grp = b / sgroup;
+    members = (int)min<int64_t>(sgroup, nb - grp * sgroup);
+    rank = (int)(b - grp * sgroup);
   }
   WaveRange w;
   w.b0 = grp * total / ng;
@@ -764,7 +774,7 @@ __global__ __launch_bounds__(256) void k_stream(ScoreArgs a) {
   const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
   u32x4* lt_ = tiles[wave];
   uint64_t* st = stage + wave * kMaxGroup * kStage;
-  const WaveRange wr = wave_range(a.tile_base[a.S], wave);
+  const WaveRange wr = wave_range(a.tile_base[a.S], wave, a.sgroup);
   const int SW = wr.sw;
   for (int64_t T = wr.b0; T < wr.b1;) {
     int s = 0;
@@ -973,7 +983,7 @@ __global__ __launch_bounds__(256) void k_stream_hm(ScoreArgs a) {
   const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
   u32x4* lt_ = tiles[wave];
   uint64_t* st = stage + wave * kStage;
-  const WaveRange wr = wave_range(a.tile_base[a.S], wave);
+  const WaveRange wr = wave_range(a.tile_base[a.S], wave, a.sgroup);
   const int SW = wr.sw;
   for (int64_t T = wr.b0; T < wr.b1;) {
     int s = 0;
@@ -2985,6 +2995,7 @@ ScoreArgs make_score_args(const RetrievePlan& p, int kind) {
   a.samp = p.samp; a.samp_stride = p.m_max;
   a.tau = p.tau; a.cnt = p.cnt; a.cand = p.cand; a.cap = p.cap;
   a.flag = p.flag; a.only_list = -1; a.full = p.full; a.row0 = 0;
+  a.sgroup = kStreamGroupMax;
   return a;
 }
 
@@ -3009,6 +3020,14 @@ int stream_grid() {
     grid = std::min(per_cu, kStreamBlocksPerCU) * cus;
   }
   return grid;
+}
+
+// Blocks per XCD group of the streaming pass: the largest power of two up to
+// kStreamGroupMax whose group range spans at most three average segments.
+int stream_group(int grid, int nseg) {
+  int g = kStreamGroupMax;
+  while (g > 1 && (int64_t)g * nseg > 3 * (int64_t)grid) g >>= 1;
+  return g;
 }
 
 template <int D, int KIND>
@@ -3076,10 +3095,13 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   // 4. streaming pass over every key row
   if (p.ev_start) (void)hipEventRecord(p.ev_start, st);
   if (p.head_mode == 0) {
-    const ScoreArgs a = make_score_args(p, K_STREAM);
+    ScoreArgs a = make_score_args(p, K_STREAM);
     const int64_t tiles = a.tile_base[p.S];
     if (tiles > 0) {
       const int grid = (int)std::min<int64_t>(stream_grid<D, false>(), std::max<int64_t>(1, tiles / 16));
+      int nseg = 0;   // (stream, layer, KV head) segments with rows
+      for (int s = 0; s < p.S; ++s) nseg += a.ntile[s] > 0 ? p.L * p.Hk : 0;
+      a.sgroup = stream_group(grid, nseg);
       hipLaunchKernelGGL(k_stream<D>, dim3(grid), dim3(256), 0, st, a);
     }
   } else {
@@ -3092,6 +3114,9 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
     a.tile_base[p.S] = tiles;
     if (tiles > 0) {
       const int grid = (int)std::min<int64_t>(stream_grid<D, true>(), std::max<int64_t>(1, tiles / 16));
+      int nseg = 0;   // (stream, layer) segments with rows
+      for (int s = 0; s < p.S; ++s) nseg += a.ntile[s] > 0 ? p.L : 0;
+      a.sgroup = stream_group(grid, nseg);
       hipLaunchKernelGGL(k_stream_hm<D>, dim3(grid), dim3(256), 0, st, a);
     }
   }
