@@ -130,19 +130,21 @@ static_assert(kFullScanRows <= 16384, "a full-scan sample must fit the register 
 constexpr int kChunkRows = 4096;
 constexpr int kSampleChunk = 128;
 
-// Expected candidates per list: 4k (at least 1024), raised for very long lists
+// Expected candidates per list: 6k (at least 1024), raised for very long lists
 // so the sample stays within the register select (kSampleMax rows).  The count
 // behaves like E Gamma(r) / r; it falls below k with probability
 // P(Poisson(r k / E) >= r) and exceeds the capacity 3E with probability
 // P(Poisson(3 r) <= r - 1); either case takes the exact fallback.  A smaller E
 // keeps fewer tiles on the candidate path of the streaming pass and fewer
 // candidates for the selection; a larger E allows a smaller r, hence a smaller
-// sample (m = r n / E).  E = 4k gives r = 21 and measured best on the 1-hour
-// index (against 3k, 6k and 8k).
+// sample (m = r n / E).  E = 6k gives r = 14, where the capacity tail binds
+// (m = 3,216 of 705,600 rows per list group on the 1-hour index); against 4k
+// (r = 21) it took 2 to 7 us off a call on the 1-hour, paper-settings, 10-minute
+// and 16-stream workloads, and 8k was slower on all four.
 constexpr int64_t kSampleMax = 16384;
 int64_t expected_candidates(int64_t n, int64_t kk) {
   const int64_t r = std::min<int64_t>(kk, kSampleRank);
-  return std::max<int64_t>({4 * kk, 1024, (n * r + kSampleMax - 1) / kSampleMax});
+  return std::max<int64_t>({6 * kk, 1024, (n * r + kSampleMax - 1) / kSampleMax});
 }
 
 // P(X >= r) for X ~ Poisson(lam): the terms from r upward, in log space.
@@ -186,9 +188,8 @@ struct StreamSizes {
 
 // Sample plan of one list.  With m sampled rows spread evenly over n rows and the
 // cut-off at the r-th largest sample score, about r n / m rows score at or above
-// it (the expected candidate count E).  r from sample_rank (21 when E = 4k,
-// fewer when E is a larger multiple of k); m = n gives an exact cut (r = k)
-// for small lists.
+// it (the expected candidate count E).  r from sample_rank (14 when E = 6k);
+// m = n gives an exact cut (r = k) for small lists.
 StreamSizes plan_stream(int64_t n, int64_t f, int top_k) {
   StreamSizes z{};
   z.n = (int)n;

@@ -179,7 +179,7 @@ def _poisson_cdf(lam, r):
 def _sample_plan(n, k):
     """The library's sample plan of one list of n rows (rank r, expected
     candidates E, sampled rows m), mirrored here to plant scores on its lattice."""
-    E = max(4 * k, 1024, -(-n * min(k, 32) // 16384))
+    E = max(6 * k, 1024, -(-n * min(k, 32) // 16384))
     r = min(k, 32)
     for rr in range(1, min(k, 32)):
         if _poisson_tail(rr * k / E, rr) <= 2e-7 and _poisson_cdf(3.0 * rr, rr - 1) <= 2e-7:
