@@ -210,7 +210,9 @@ def test_fallback_too_few_candidates():
     spec = W.stream_specs(cfg)[0]
     gidx, oidx = make_pair(cfg, spec, keys)
     out = debug_run([gidx], [q], k, 4)
-    assert out["list_stats"][0, 0, 1] == 1
+    assert out["list_stats"][0, 0, 1] == 1, (
+        "no fallback: the planted rows no longer sit on the library's sample lattice; "
+        "_sample_plan must mirror expected_candidates and sample_rank in ss_api.cpp")
     rep = staged_check(oidx, q, out, 0, k, 4)
     log(rep)
     assert rep.get("swaps", 0) == 0
