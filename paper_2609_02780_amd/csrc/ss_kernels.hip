@@ -717,6 +717,20 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a) {
 // at most three average segments.
 constexpr int kStreamGroupMax = 32;
 
+// Share of the tiles per group by XCD parity.  On this part the odd XCDs read
+// HBM about 9% slower than the even ones while all eight stream (the same
+// pattern on every box measured: with equal shares the even XCDs finish the
+// 1-hour pass at 350-380 us and the odd ones at 386-417 us), so a group on an
+// even XCD takes kXcdEvenWeight / kXcdOddWeight times the tiles of one on an odd
+// XCD.  Measured: 1-hour pass 409 -> 403 us, 16-stream batch 1,954 -> 1,932 us;
+// the XCD end times then no longer split by parity but still spread by about
+// 20 us.  Handing the last 10-20% of the tiles out in chunks through atomic
+// counters balanced the batch better (-55 us) but cost the 1-hour pass 7-35 us:
+// single-wave chunks lose the DRAM locality of the group windows.  Only the
+// split of the tiles between waves depends on these weights.
+constexpr int64_t kXcdEvenWeight = 1090;
+constexpr int64_t kXcdOddWeight = 1000;
+
 struct WaveRange {
   int64_t b0, b1;   // the group's tiles
   int sw, wg;       // waves in the group, this wave's rank among them
@@ -732,6 +746,17 @@ __device__ __forceinline__ WaveRange wave_range(int64_t total, int wave, int sgr
     grp = (r / sgroup) * 8 + x;
     members = sgroup;
     rank = (int)(r % sgroup);
+    // groups alternate even and odd XCDs; ng is a multiple of 8
+    const int64_t pair = kXcdEvenWeight + kXcdOddWeight;
+    const int64_t w0 = (grp / 2) * pair + (grp % 2) * kXcdEvenWeight;
+    const int64_t w1 = w0 + ((grp % 2) ? kXcdOddWeight : kXcdEvenWeight);
+    const int64_t wt = (ng / 2) * pair;
+    WaveRange w;
+    w.b0 = total * w0 / wt;
+    w.b1 = total * w1 / wt;
+    w.sw = 4 * members;
+    w.wg = rank * 4 + wave;
+    return w;
   } else {
     ng = (nb + sgroup - 1) / sgroup;
     grp = b / sgroup;
