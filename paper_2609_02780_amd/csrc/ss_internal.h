@@ -97,6 +97,7 @@ struct RetrievePlan {
   uint64_t* cand;        // [S*NL][cap]
   float* qcol;           // [S][L][H_kv][16] L1 norms of the scaled query columns
   int32_t* sexp;         // [S] fixed-point exponent of each stream's attention mass
+  uint32_t* dyn_ctr;     // chunk counters of the streaming pass
   float* full;           // fallback scores, per stream base full_base[s]
   int64_t full_base[kMaxStreams];
   int32_t* votes;        // [S][f_max] per-frame votes

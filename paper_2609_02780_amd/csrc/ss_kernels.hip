@@ -521,6 +521,9 @@ struct ScoreArgs {
   int64_t tile_base[kMaxStreams + 1];  // first tile of each stream; tiles of all streams in a row
   int32_t ntile[kMaxStreams];          // 16-row tiles per (layer, KV head) segment
   int sgroup;                          // blocks per XCD group of the streaming pass
+  int64_t dyn_tiles;                   // the last tiles, handed out in chunks (0: all static)
+  int dyn_chunk;                       // tiles per handed-out chunk
+  uint32_t* dyn_ctr;                   // kDynCtr chunk counters, kDynStride words apart
   // K_FULL
   const int32_t* flag;                // nullptr: write only `only_list`
   int only_list;
@@ -725,11 +728,22 @@ constexpr int kStreamGroupMax = 32;
 // XCD.  Measured: 1-hour pass 409 -> 403 us, 16-stream batch 1,954 -> 1,932 us;
 // the XCD end times then no longer split by parity but still spread by about
 // 20 us.  Handing the last 10-20% of the tiles out in chunks through atomic
-// counters balanced the batch better (-55 us) but cost the 1-hour pass 7-35 us:
-// single-wave chunks lose the DRAM locality of the group windows.  Only the
-// split of the tiles between waves depends on these weights.
+// counters (below) cost the 1-hour pass 7-35 us, since single-wave chunks lose
+// the DRAM locality of the group windows, so it is kept for the segment-rich
+// batches only.  Only the split of the tiles between waves depends on these
+// weights.
 constexpr int64_t kXcdEvenWeight = 1090;
 constexpr int64_t kXcdOddWeight = 1000;
+
+// The handed-out tail of the streaming pass on batches of many short segments
+// (where the group size rule picks fewer than kStreamGroupMax blocks): kDynCtr
+// chunk counters, each in its own 256-byte line; kDynPermille of the tiles in
+// chunks of kDynChunk.  On the 16-stream batch it took the pass from 1,950 to
+// 1,895 us (the waves that visit many segments no longer finish last).
+constexpr int kDynCtr = 32;
+constexpr int kDynStride = 64;
+constexpr int kDynPermille = 150;
+constexpr int kDynChunk = 16;
 
 struct WaveRange {
   int64_t b0, b1;   // the group's tiles
@@ -799,75 +813,102 @@ __global__ __launch_bounds__(256) void k_stream(ScoreArgs a) {
   const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
   u32x4* lt_ = tiles[wave];
   uint64_t* st = stage + wave * kMaxGroup * kStage;
-  const WaveRange wr = wave_range(a.tile_base[a.S], wave, a.sgroup);
-  const int SW = wr.sw;
-  for (int64_t T = wr.b0; T < wr.b1;) {
-    int s = 0;
-    while (T >= a.tile_base[s + 1]) ++s;
-    const int64_t rem = T - a.tile_base[s];
-    const int nt = a.ntile[s];
-    const int lg = (int)(rem / nt);
-    const int tb = (int)(rem - (int64_t)lg * nt);
-    const int t1 = (int)min<int64_t>(nt, tb + (wr.b1 - T));
-    const int t0 = first_tile(wr, T, tb);
-    T += t1 - tb;
-    if (t0 >= t1) continue;
-    const int g = lg % a.Hk, l = lg / a.Hk;
-    const int n = a.n[s];
-    const bool colv = col < a.G;
-    const int list = s * a.NL + l * a.Hq + g * a.G + col;
-    const float tau_f = ord_f32(colv ? a.tau[list] : 0xFFFFFFFFu);
-    const u32x4* qb = a.qB + ((size_t)(s * a.L + l) * a.Hk + g) * (2 * KS * kWave);
-    u32x4 bh[KS], bl[KS];
+  // Tiles [0, total - dyn_tiles) in the wave's static share of its group's
+  // range (see wave_range); then, on batches of many short segments, chunks of
+  // the last dyn_tiles handed out by the chunk counters to whichever waves are
+  // free (the waves that visit many segments flush more and fall behind).
+  const int64_t total = a.tile_base[a.S], static_end = total - a.dyn_tiles;
+  auto run_range = [&](const WaveRange& wr) {
+    const int SW = wr.sw;
+    for (int64_t T = wr.b0; T < wr.b1;) {
+      int s = 0;
+      while (T >= a.tile_base[s + 1]) ++s;
+      const int64_t rem = T - a.tile_base[s];
+      const int nt = a.ntile[s];
+      const int lg = (int)(rem / nt);
+      const int tb = (int)(rem - (int64_t)lg * nt);
+      const int t1 = (int)min<int64_t>(nt, tb + (wr.b1 - T));
+      const int t0 = first_tile(wr, T, tb);
+      T += t1 - tb;
+      if (t0 >= t1) continue;
+      const int g = lg % a.Hk, l = lg / a.Hk;
+      const int n = a.n[s];
+      const bool colv = col < a.G;
+      const int list = s * a.NL + l * a.Hq + g * a.G + col;
+      const float tau_f = ord_f32(colv ? a.tau[list] : 0xFFFFFFFFu);
+      const u32x4* qb = a.qB + ((size_t)(s * a.L + l) * a.Hk + g) * (2 * KS * kWave);
+      u32x4 bh[KS], bl[KS];
 #pragma unroll
-    for (int i = 0; i < KS; ++i) {
-      bh[i] = qb[i * kWave + lane];
-      bl[i] = qb[(KS + i) * kWave + lane];
-    }
-    // The segment is read through a buffer resource of exactly n rows: lanes
-    // past the last row, and the loads that run ahead of the range, fetch
-    // zeros without touching memory (the host keeps a segment below 2 GiB).
-    // Lane q of load i covers the 16-byte chunk 64 i + q of the tile.
-    const uint16_t* seg = a.keys[s] + ((size_t)l * a.Hk + g) * (size_t)a.stride[s] * D;
-    const __amdgpu_buffer_rsrc_t rsrc =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(seg), (short)0, n * D * 2, 0x00020000);
-    auto load = [&](int t, u32x4 (&V)[NI]) {
-      const uint32_t off = t < t1 ? (uint32_t)t * (TCH * 16) + lane * 16 : 0x80000000u;
-#pragma unroll
-      for (int i = 0; i < NI; ++i)
-        V[i] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off + i * kWave * 16, 0, kAuxNT);
-    };
-    // The next loads are issued as soon as a tile's registers have gone to
-    // LDS, so they overlap the MFMAs and the candidate test.  Every pass of
-    // the loop body loads and computes (a pass past the range works on zeros
-    // and emits nothing), which keeps the waits exact.
-    u32x4 V[PF][NI];
-#pragma unroll
-    for (int p = 0; p < PF; ++p) load(t0 + SW * p, V[p]);
-    int lc = 0;
-    for (int t = t0; t < t1; t += SW * PF) {
-#pragma unroll
-      for (int p = 0; p < PF; ++p) {
-        const int tt = t + SW * p;
-#pragma unroll
-        for (int i = 0; i < NI; ++i) {
-          const int q = i * kWave + lane, R = q >> 4, C = q & 15;
-          lt_[R * 16 + (C ^ (R & 15))] = V[p][i];
-        }
-        __builtin_amdgcn_wave_barrier();
-        load(tt + SW * PF, V[p]);
-        u32x4 A[KS];
-#pragma unroll
-        for (int i = 0; i < KS; ++i) {
-          const int q = rl * CPR + 4 * i + kg, R = q >> 4, C = q & 15;
-          A[i] = lt_[R * 16 + (C ^ (R & 15))];
-        }
-        __builtin_amdgcn_wave_barrier();
-        const f32x4 acc = score_hilo<KS>(A, bh, bl);
-        if (tt < t1) stream_emit(a, list, colv, col, tau_f, tt * kTile, n, acc, kg, st, lc);
+      for (int i = 0; i < KS; ++i) {
+        bh[i] = qb[i * kWave + lane];
+        bl[i] = qb[(KS + i) * kWave + lane];
       }
+      // The segment is read through a buffer resource of exactly n rows: lanes
+      // past the last row, and the loads that run ahead of the range, fetch
+      // zeros without touching memory (the host keeps a segment below 2 GiB).
+      // Lane q of load i covers the 16-byte chunk 64 i + q of the tile.
+      const uint16_t* seg = a.keys[s] + ((size_t)l * a.Hk + g) * (size_t)a.stride[s] * D;
+      const __amdgpu_buffer_rsrc_t rsrc =
+          __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(seg), (short)0, n * D * 2, 0x00020000);
+      auto load = [&](int t, u32x4 (&V)[NI]) {
+        const uint32_t off = t < t1 ? (uint32_t)t * (TCH * 16) + lane * 16 : 0x80000000u;
+#pragma unroll
+        for (int i = 0; i < NI; ++i)
+          V[i] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off + i * kWave * 16, 0, kAuxNT);
+      };
+      // The next loads are issued as soon as a tile's registers have gone to
+      // LDS, so they overlap the MFMAs and the candidate test.  Every pass of
+      // the loop body loads and computes (a pass past the range works on zeros
+      // and emits nothing), which keeps the waits exact.
+      u32x4 V[PF][NI];
+#pragma unroll
+      for (int p = 0; p < PF; ++p) load(t0 + SW * p, V[p]);
+      int lc = 0;
+      for (int t = t0; t < t1; t += SW * PF) {
+#pragma unroll
+        for (int p = 0; p < PF; ++p) {
+          const int tt = t + SW * p;
+#pragma unroll
+          for (int i = 0; i < NI; ++i) {
+            const int q = i * kWave + lane, R = q >> 4, C = q & 15;
+            lt_[R * 16 + (C ^ (R & 15))] = V[p][i];
+          }
+          __builtin_amdgcn_wave_barrier();
+          load(tt + SW * PF, V[p]);
+          u32x4 A[KS];
+#pragma unroll
+          for (int i = 0; i < KS; ++i) {
+            const int q = rl * CPR + 4 * i + kg, R = q >> 4, C = q & 15;
+            A[i] = lt_[R * 16 + (C ^ (R & 15))];
+          }
+          __builtin_amdgcn_wave_barrier();
+          const f32x4 acc = score_hilo<KS>(A, bh, bl);
+          if (tt < t1) stream_emit(a, list, colv, col, tau_f, tt * kTile, n, acc, kg, st, lc);
+        }
+      }
+      if (__any(lc > 0)) stage_flush(a, list, colv, col, kg, st, lc);
     }
-    if (__any(lc > 0)) stage_flush(a, list, colv, col, kg, st, lc);
+  };
+  run_range(wave_range(static_end, wave, a.sgroup));
+  if (a.dyn_tiles > 0) {
+    // counter k serves the chunks k, k + kDynCtr, ...; the blocks that share a
+    // counter span all XCDs (block b sits on XCD b mod 8)
+    const int k0 = (int)((blockIdx.x >> 3) % kDynCtr);
+    uint32_t* ctr = a.dyn_ctr + k0 * kDynStride;
+    const int64_t nch = (a.dyn_tiles + a.dyn_chunk - 1) / a.dyn_chunk;
+    for (;;) {
+      uint32_t q = 0;
+      if (lane == 0) q = atomicAdd(ctr, 1u);
+      q = __builtin_amdgcn_readfirstlane(q);
+      const int64_t c = k0 + (int64_t)kDynCtr * q;
+      if (c >= nch) break;
+      WaveRange d;
+      d.b0 = static_end + c * a.dyn_chunk;
+      d.b1 = min<int64_t>(d.b0 + a.dyn_chunk, total);
+      d.sw = 1;
+      d.wg = 0;
+      run_range(d);
+    }
   }
 }
 
@@ -1229,6 +1270,7 @@ struct ListArgs {
   int32_t* dbg_pos;
   float* dbg_score;
   int32_t* dbg_stats;
+  uint32_t* dyn_ctr;   // the streaming pass's chunk counters (zeroed by k_thresh)
 };
 
 __device__ __forceinline__ int frame_of_row(const ListArgs& a, int s, uint32_t row) {
@@ -1293,6 +1335,7 @@ __global__ __launch_bounds__(1024) void k_thresh(ListArgs a) {
     a.cnt[list] = 0;
     a.flag[list] = 0;
   }
+  if (list == 0 && threadIdx.x < kDynCtr) a.dyn_ctr[threadIdx.x * kDynStride] = 0;
   {
     int32_t* vg = a.votes_g + (size_t)s * a.f_max;
     int64_t* mg = a.massfx_g + (size_t)s * a.f_max;
@@ -3021,6 +3064,9 @@ ScoreArgs make_score_args(const RetrievePlan& p, int kind) {
   a.tau = p.tau; a.cnt = p.cnt; a.cand = p.cand; a.cap = p.cap;
   a.flag = p.flag; a.only_list = -1; a.full = p.full; a.row0 = 0;
   a.sgroup = kStreamGroupMax;
+  a.dyn_tiles = 0;
+  a.dyn_chunk = kDynChunk;
+  a.dyn_ctr = p.dyn_ctr;
   return a;
 }
 
@@ -3098,6 +3144,7 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   for (int s = 0; s < p.S; ++s) { la.keys[s] = p.st[s].keys; la.stride[s] = p.st[s].row_stride; }
   la.dbg_pos = p.dbg_topk_pos; la.dbg_score = p.dbg_topk_score; la.dbg_stats = p.dbg_list_stats;
   la.f_max = p.f_max; la.votes_g = p.votes; la.massfx_g = p.massfx; la.sexp = p.sexp; la.qcol = p.qcol;
+  la.dyn_ctr = p.dyn_ctr;
   const int lists = p.S * p.NL;
   // 2. sample scores, 3. thresholds
   if (p.head_mode == 0) {
@@ -3127,6 +3174,7 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
       int nseg = 0;   // (stream, layer, KV head) segments with rows
       for (int s = 0; s < p.S; ++s) nseg += a.ntile[s] > 0 ? p.L * p.Hk : 0;
       a.sgroup = stream_group(grid, nseg);
+      if (a.sgroup < kStreamGroupMax) a.dyn_tiles = tiles * kDynPermille / 1000;
       hipLaunchKernelGGL(k_stream<D>, dim3(grid), dim3(256), 0, st, a);
     }
   } else {
@@ -3344,6 +3392,7 @@ size_t carve_workspace(RetrievePlan& p, void* ws) {
   p.cand = static_cast<uint64_t*>(take(lists * (size_t)p.cap * 8));
   p.qcol = static_cast<float*>(take((size_t)p.S * p.L * p.Hk * 16 * 4));
   p.sexp = static_cast<int32_t*>(take((size_t)p.S * 4));
+  p.dyn_ctr = static_cast<uint32_t*>(take((size_t)kDynCtr * kDynStride * 4));
   p.full = static_cast<float*>(take((size_t)p.full_total * 4));
   p.votes = static_cast<int32_t*>(take((size_t)p.S * p.f_max * 4));
   p.massfx = static_cast<int64_t*>(take((size_t)p.S * p.f_max * 8));
