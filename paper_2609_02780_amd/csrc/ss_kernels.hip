@@ -1325,7 +1325,7 @@ __device__ void stream_exponent(const ListArgs& a, int s) {
 // The sample (m <= kThrItems * 1024 scores) sits in registers.  The blocks of a
 // stream also clear its frame accumulators, and its first block fixes the
 // stream's mass exponent.
-__global__ __launch_bounds__(1024) void k_thresh(ListArgs a) {
+__device__ __forceinline__ void thresh_list(const ListArgs& a) {
   __shared__ uint32_t hist[kSelHist];
   __shared__ uint32_t res[4];
   __shared__ uint32_t mm[32];
@@ -1366,6 +1366,18 @@ __global__ __launch_bounds__(1024) void k_thresh(ListArgs a) {
   uint32_t ng, ne;
   const uint32_t t = block_select_range<kThrItems, true>(x, ok, mn, mx, (uint32_t)r, hist, res, ng, ne);
   if (threadIdx.x == 0) a.tau[list] = t;
+}
+
+// One block per list.  With up to two lists per CU the kernel takes the
+// registers it wants (90 VGPRs: one block per CU); with more lists (the
+// 16-stream batch: 1,536) the dense variant fits two blocks per CU in 64 VGPRs
+// with a few spills, three rounds of blocks instead of six (41 -> 32 us on that
+// batch).
+__global__ __launch_bounds__(1024) void k_thresh(ListArgs a) {
+  thresh_list(a);
+}
+__global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(8, 8))) void k_thresh_dense(ListArgs a) {
+  thresh_list(a);
 }
 
 // ---------------------------------------------------------------------------
@@ -3163,7 +3175,14 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   } else {
     launch_score<D, K_SAMPLE>(make_score_args(p, K_SAMPLE), p.head_mode, 4096, st);
   }
-  hipLaunchKernelGGL(k_thresh, dim3(lists), dim3(1024), 0, st, la);
+  {
+    int dev = 0, cus = 256;
+    if (hipGetDevice(&dev) == hipSuccess) (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (lists > 2 * cus)
+      hipLaunchKernelGGL(k_thresh_dense, dim3(lists), dim3(1024), 0, st, la);
+    else
+      hipLaunchKernelGGL(k_thresh, dim3(lists), dim3(1024), 0, st, la);
+  }
   // 4. streaming pass over every key row
   if (p.ev_start) (void)hipEventRecord(p.ev_start, st);
   if (p.head_mode == 0) {
