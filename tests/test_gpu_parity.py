@@ -282,6 +282,29 @@ def test_ragged_batch_one_call():
         log(s, rep)
 
 
+def test_segment_rich_batch_weighted_split_and_handed_out_tail():
+    """Sixteen ragged streams of 2 layers x 2 KV heads (64 segments of 60-75
+    frames x 32 rows) in one call: the streaming pass takes groups of 16 blocks
+    with XCD-weighted ranges and hands the last 15% of its tiles out in chunks
+    through the chunk counters, so segments are cut at arbitrary tiles between
+    waves.  Every stream checked stage by stage against the oracle."""
+    gidxs, oidxs, qs = [], [], []
+    for s in range(16):
+        F = 60 + s
+        cfg = W.Config("segrich", 2, 4, 2, 64, 32, 8, 32, 4, n_frames=F, n_planted=1)
+        spec = W.stream_specs(cfg)[0]
+        q, keys = W.make_stream(cfg, spec, seed=100 + s)
+        g, o = make_pair(cfg, spec, keys)
+        gidxs.append(g)
+        oidxs.append(o)
+        qs.append(q)
+    out = debug_run(gidxs, qs, 32, 4)
+    assert out["list_stats"][:, :, 1].sum() == 0    # no list needed the fallback
+    for s in range(16):
+        rep = staged_check(oidxs[s], qs[s], out, s, 32, 4)
+        log(s, rep)
+
+
 def test_pool_cut_many_ties():
     """One selected row per list over 256 lists of an 800-frame stream: almost
     every voted frame has a single vote, so more than 128 frames tie at the
