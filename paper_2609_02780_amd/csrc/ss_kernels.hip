@@ -5,11 +5,13 @@
 //   k_prep      mean query per (layer, head), pre-scaled, split into bf16 hi+lo
 //               and laid out as the MFMA B operand (lane-native).
 //   k_sample    scores of an evenly spread sample of rows per list group
-//               (k_score<SAMPLE> in head mode 1).
+//               (k_score<SAMPLE> in head mode 1).  k_prep_sample does both
+//               steps in one launch when its blocks fit one round.
 //   k_thresh    per list, the r-th largest sample score: the streaming cut-off.
 //   k_stream    THE HOT KERNEL: streams every bf16 key row from HBM once.
-//               The 16-row tiles of all lists form one sequence cut into one
-//               contiguous range per wave; each tile comes in as coalesced
+//               The 16-row tiles of all lists form one sequence, cut into
+//               XCD-weighted group ranges (plus a handed-out tail on
+//               segment-rich batches); each tile comes in as coalesced
 //               nontemporal 16-byte buffer loads, is swizzled through LDS into
 //               the MFMA A layout, is scored by bf16 MFMA 16x16x32 against the
 //               group's query columns (hi and lo parts, fp32 accumulation), and
@@ -409,20 +411,19 @@ struct PrepArgs {
   float* qcol;     // [S][L][H_kv][16] L1 norm of each scaled B column, or null
 };
 
-// One block of 8*D threads per (stream, layer, KV head): thread (tg, col, ec)
-// sums, over the query tokens j = tg mod 4, dims 8 ec .. 8 ec + 7 of B-tile
-// column col; the four partial sums are then added in tg order.  In the
-// lane-native layout those dims belong to k-step i = ec / 4 of lane
-// col + 16 (ec % 4).  Column c of head-mode 0 is query head g*G + c; head-mode 1
-// uses column 0 only, holding the sum of the group's head means (the layer's
-// head average is the sum over KV heads of these columns against their keys).
+// Query token groups of the B-tile prep (the partial sums of each are added in
+// group order).
 constexpr int kPrepGroups = 4;
 
+// Forms the B tile of (pair, KV head g) with the block's 8 D threads; `part`
+// is the block's LDS scratch for the token-group partial sums.  The threads of
+// token group 0 (the first 2 D threads, whole waves) hold the result: they
+// write it to `out_lds` if given, and to the global B tile and the column L1
+// norms if `global` is set.
 template <int D>
-__global__ __launch_bounds__(8 * D) void k_prep(PrepArgs a) {
+__device__ __forceinline__ void prep_b(const PrepArgs& a, int pair_local, int g,
+                                       float (*part)[2 * D][8], u32x4* out_lds, bool global) {
   constexpr int KS = D / 32, NE = D / 8, NT = 2 * D;  // NT threads per token group
-  __shared__ float part[kPrepGroups][NT][8];
-  const int pair_local = blockIdx.x / a.Hk, g = blockIdx.x % a.Hk;
   const int pair = a.first + pair_local;
   const int s = pair / a.L;
   const uint16_t* q = a.q[pair_local];
@@ -464,33 +465,53 @@ __global__ __launch_bounds__(8 * D) void k_prep(PrepArgs a) {
 #pragma unroll
   for (int w = 0; w < 8; ++w) part[tg][t][w] = acc[w];
   __syncthreads();
-  if (tg != 0) return;
+  if (tg == 0) {
 #pragma unroll
-  for (int w = 0; w < 8; ++w) {
-    float x = part[0][t][w];
-    for (int k = 1; k < kPrepGroups; ++k) x += part[k][t][w];
-    acc[w] = x;
+    for (int w = 0; w < 8; ++w) {
+      float x = part[0][t][w];
+      for (int k = 1; k < kPrepGroups; ++k) x += part[k][t][w];
+      acc[w] = x;
+    }
+    u32x4 hi, lo;
+    float l1 = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float x0 = acc[2 * w] * scale, x1 = acc[2 * w + 1] * scale;
+      l1 += fabsf(x0) + fabsf(x1);
+      const uint16_t a0 = bf16_rne(x0), a1 = bf16_rne(x1);
+      const uint16_t b0 = bf16_rne(x0 - __uint_as_float((uint32_t)a0 << 16));
+      const uint16_t b1 = bf16_rne(x1 - __uint_as_float((uint32_t)a1 << 16));
+      hi[w] = (uint32_t)a0 | ((uint32_t)a1 << 16);
+      lo[w] = (uint32_t)b0 | ((uint32_t)b1 << 16);
+    }
+    const int i = ec >> 2, lane = col + 16 * (ec & 3);
+    if (out_lds) {
+      out_lds[(0 * KS + i) * kWave + lane] = hi;
+      out_lds[(1 * KS + i) * kWave + lane] = lo;
+    }
+    if (global) {
+      u32x4* out = a.qB + ((size_t)pair * a.Hk + g) * (2 * KS * kWave);
+      out[(0 * KS + i) * kWave + lane] = hi;
+      out[(1 * KS + i) * kWave + lane] = lo;
+    }
+    // the NE threads of a column are adjacent lanes of one wave
+#pragma unroll
+    for (int o = NE / 2; o > 0; o >>= 1) l1 += __shfl_xor(l1, o);
+    if (global && a.qcol && ec == 0) a.qcol[((size_t)pair * a.Hk + g) * 16 + col] = l1;
   }
-  u32x4 hi, lo;
-  float l1 = 0.f;
-#pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    const float x0 = acc[2 * w] * scale, x1 = acc[2 * w + 1] * scale;
-    l1 += fabsf(x0) + fabsf(x1);
-    const uint16_t a0 = bf16_rne(x0), a1 = bf16_rne(x1);
-    const uint16_t b0 = bf16_rne(x0 - __uint_as_float((uint32_t)a0 << 16));
-    const uint16_t b1 = bf16_rne(x1 - __uint_as_float((uint32_t)a1 << 16));
-    hi[w] = (uint32_t)a0 | ((uint32_t)a1 << 16);
-    lo[w] = (uint32_t)b0 | ((uint32_t)b1 << 16);
-  }
-  u32x4* out = a.qB + ((size_t)pair * a.Hk + g) * (2 * KS * kWave);
-  const int i = ec >> 2, lane = col + 16 * (ec & 3);
-  out[(0 * KS + i) * kWave + lane] = hi;
-  out[(1 * KS + i) * kWave + lane] = lo;
-  // the NE threads of a column are adjacent lanes of one wave
-#pragma unroll
-  for (int o = NE / 2; o > 0; o >>= 1) l1 += __shfl_xor(l1, o);
-  if (a.qcol && ec == 0) a.qcol[((size_t)pair * a.Hk + g) * 16 + col] = l1;
+}
+
+// One block of 8*D threads per (stream, layer, KV head): thread (tg, col, ec)
+// sums, over the query tokens j = tg mod 4, dims 8 ec .. 8 ec + 7 of B-tile
+// column col; the four partial sums are then added in tg order.  In the
+// lane-native layout those dims belong to k-step i = ec / 4 of lane
+// col + 16 (ec % 4).  Column c of head-mode 0 is query head g*G + c; head-mode 1
+// uses column 0 only, holding the sum of the group's head means (the layer's
+// head average is the sum over KV heads of these columns against their keys).
+template <int D>
+__global__ __launch_bounds__(8 * D) void k_prep(PrepArgs a) {
+  __shared__ float part[kPrepGroups][2 * D][8];
+  prep_b<D>(a, blockIdx.x / a.Hk, blockIdx.x % a.Hk, part, nullptr, true);
 }
 
 // ---------------------------------------------------------------------------
@@ -988,6 +1009,96 @@ __global__ __launch_bounds__(256) void k_sample(ScoreArgs a) {
       }
     }
     T += t1 - t0;
+  }
+}
+
+// Query prep and the sample pass in one launch (head-mode 0).  Block b works on
+// one (stream, layer, KV head) group and kPsTiles of its sample tiles: it first
+// forms the group's B tile exactly as k_prep does (the same sums in the same
+// order, so every block of the group holds the same bits; the group's first
+// block also writes them, and the column norms, for the streaming pass), keeps
+// it in LDS, and then each wave gathers and scores its tiles as k_sample does.
+// One launch instead of two: the sample no longer waits for a separate prep
+// kernel to drain.
+constexpr int kPsTiles = 32;   // sample tiles per block
+
+struct PsArgs {
+  int blk_base[kMaxStreams + 1];   // first block of each stream
+  int spg[kMaxStreams];            // blocks per (layer, KV head) group of each stream
+};
+
+template <int D>
+__global__ __launch_bounds__(8 * D) void k_prep_sample(PrepArgs pa, ScoreArgs a, PsArgs ps) {
+  constexpr int CPR = D / 8, TCH = 16 * CPR, NI = TCH / kWave, KS = D / 32;
+  constexpr int NW = 8 * D / kWave;   // waves per block
+  constexpr int PF = kPsTiles / NW;   // tiles per wave, all in flight
+  union PsShared {
+    float part[kPrepGroups][2 * D][8];
+    u32x4 tiles[NW][TCH];
+  };
+  __shared__ PsShared sh;
+  __shared__ u32x4 bsh[2 * KS * kWave];
+  int s = 0;
+  while ((int)blockIdx.x >= ps.blk_base[s + 1]) ++s;
+  const int rem = (int)blockIdx.x - ps.blk_base[s];
+  const int lg = rem / ps.spg[s], slice = rem - lg * ps.spg[s];
+  const int l = lg / a.Hk, g = lg - l * a.Hk;
+  prep_b<D>(pa, s * a.L + l, g, sh.part, bsh, slice == 0);
+  __syncthreads();   // the B tile is in LDS and the partial sums are read no more
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
+  u32x4* lt_ = sh.tiles[wave];
+  const int n = a.n[s], m = a.units[s], nt = a.ntile[s];
+  const int64_t step = a.samp_step[s];
+  const bool colv = col < a.G;
+  const int list = s * a.NL + l * a.Hq + g * a.G + col;
+  u32x4 bh[KS], bl[KS];
+#pragma unroll
+  for (int i = 0; i < KS; ++i) {
+    bh[i] = bsh[i * kWave + lane];
+    bl[i] = bsh[(KS + i) * kWave + lane];
+  }
+  const uint16_t* seg = a.keys[s] + ((size_t)l * a.Hk + g) * (size_t)a.stride[s] * D;
+  const __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(seg), (short)0, n * D * 2, 0x00020000);
+  // wave w scores tiles slice kPsTiles + w + NW p (p < PF); chunk q = 64 i +
+  // lane of tile t is chunk q mod CPR of sample t 16 + q / CPR; past the
+  // group's tiles or samples the loads read zeros without touching memory
+  u32x4 V[PF][NI];
+#pragma unroll
+  for (int p = 0; p < PF; ++p) {
+    const int t = slice * kPsTiles + wave + NW * p;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int q = i * kWave + lane, u = t * kTile + q / CPR;
+      const uint32_t off = (t < nt && u < m) ? (uint32_t)sample_row(step, u) * (CPR * 16) + (q % CPR) * 16
+                                             : 0x80000000u;
+      V[p][i] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, kAuxNT);
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < PF; ++p) {
+    const int t = slice * kPsTiles + wave + NW * p;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int q = i * kWave + lane, R = q >> 4, C = q & 15;
+      lt_[R * 16 + (C ^ (R & 15))] = V[p][i];
+    }
+    __builtin_amdgcn_wave_barrier();
+    u32x4 A[KS];
+#pragma unroll
+    for (int i = 0; i < KS; ++i) {
+      const int q = rl * CPR + 4 * i + kg, R = q >> 4, C = q & 15;
+      A[i] = lt_[R * 16 + (C ^ (R & 15))];
+    }
+    __builtin_amdgcn_wave_barrier();
+    const f32x4 acc = score_hilo<KS>(A, bh, bl);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int u = t * kTile + 4 * kg + j;
+      if (colv && t < nt && u < m) a.samp[(size_t)list * a.samp_stride + u] = acc[j] + 0.0f;
+    }
   }
 }
 
@@ -3123,22 +3234,39 @@ void launch_score(const ScoreArgs& a, int head_mode, int max_grid, hipStream_t s
 
 template <int D>
 hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
-  // 1. query prep
-  {
-    const int pairs = p.S * p.L;
-    for (int first = 0; first < pairs; first += 128) {
-      PrepArgs a{};
-      a.Hq = p.Hq; a.Hk = p.Hk; a.G = p.G; a.L = p.L; a.head_mode = p.head_mode; a.first = first;
-      const int cnt = std::min(128, pairs - first);
-      for (int i = 0; i < cnt; ++i) {
-        const int pr = first + i;
-        a.q[i] = p.st[pr / p.L].q[pr % p.L];
-      }
-      for (int s = 0; s < p.S; ++s) { a.nq[s] = p.st[s].nq; a.qscale[s] = p.st[s].qscale; }
-      a.qB = reinterpret_cast<u32x4*>(p.qB);
-      a.qcol = p.qcol;
-      hipLaunchKernelGGL(k_prep<D>, dim3(cnt * p.Hk), dim3(8 * D), 0, st, a);
+  // 1. query prep, fused with 2., the sample scores, in k_prep_sample (head
+  // mode 0) when its blocks fit one round: at most one per CU (104 VGPRs at
+  // d = 128).  Measured: 1-hour index -3 us, 10-minute -2 us, compressed
+  // -1 us per call; on the 16-stream batch (about 800 blocks) the two kernels
+  // are faster.
+  const int pairs = p.S * p.L;
+  PsArgs ps{};
+  int ps_blocks = 0;
+  for (int s = 0; s < p.S; ++s) {
+    ps.blk_base[s] = ps_blocks;
+    ps.spg[s] = std::max(1, cdiv(cdiv(p.st[s].m, kTile), kPsTiles));   // every group forms its B tile
+    ps_blocks += p.L * p.Hk * ps.spg[s];
+  }
+  ps.blk_base[p.S] = ps_blocks;
+  int cus = 256, dev = 0;
+  if (hipGetDevice(&dev) == hipSuccess) (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  const bool fused = p.head_mode == 0 && pairs <= 128 && ps_blocks <= cus;
+  PrepArgs pa_fused{};
+  for (int first = 0; first < pairs; first += 128) {
+    PrepArgs a{};
+    a.Hq = p.Hq; a.Hk = p.Hk; a.G = p.G; a.L = p.L; a.head_mode = p.head_mode; a.first = first;
+    const int cnt = std::min(128, pairs - first);
+    for (int i = 0; i < cnt; ++i) {
+      const int pr = first + i;
+      a.q[i] = p.st[pr / p.L].q[pr % p.L];
     }
+    for (int s = 0; s < p.S; ++s) { a.nq[s] = p.st[s].nq; a.qscale[s] = p.st[s].qscale; }
+    a.qB = reinterpret_cast<u32x4*>(p.qB);
+    a.qcol = p.qcol;
+    if (fused)
+      pa_fused = a;
+    else
+      hipLaunchKernelGGL(k_prep<D>, dim3(cnt * p.Hk), dim3(8 * D), 0, st, a);
   }
   ListArgs la{};
   la.NL = p.NL; la.S = p.S; la.cap = p.cap; la.k_max = p.k_max; la.top_k = p.top_k;
@@ -3168,21 +3296,19 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
       tiles += (int64_t)p.L * p.Hk * a.ntile[s];
     }
     a.tile_base[p.S] = tiles;
-    if (tiles > 0) {
+    if (fused) {
+      hipLaunchKernelGGL(k_prep_sample<D>, dim3(ps_blocks), dim3(8 * D), 0, st, pa_fused, a, ps);
+    } else if (tiles > 0) {
       const int grid = (int)std::min<int64_t>(stream_grid<D, false>(), std::max<int64_t>(1, tiles / 4));
       hipLaunchKernelGGL(k_sample<D>, dim3(grid), dim3(256), 0, st, a);
     }
   } else {
     launch_score<D, K_SAMPLE>(make_score_args(p, K_SAMPLE), p.head_mode, 4096, st);
   }
-  {
-    int dev = 0, cus = 256;
-    if (hipGetDevice(&dev) == hipSuccess) (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    if (lists > 2 * cus)
-      hipLaunchKernelGGL(k_thresh_dense, dim3(lists), dim3(1024), 0, st, la);
-    else
-      hipLaunchKernelGGL(k_thresh, dim3(lists), dim3(1024), 0, st, la);
-  }
+  if (lists > 2 * cus)
+    hipLaunchKernelGGL(k_thresh_dense, dim3(lists), dim3(1024), 0, st, la);
+  else
+    hipLaunchKernelGGL(k_thresh, dim3(lists), dim3(1024), 0, st, la);
   // 4. streaming pass over every key row
   if (p.ev_start) (void)hipEventRecord(p.ev_start, st);
   if (p.head_mode == 0) {
