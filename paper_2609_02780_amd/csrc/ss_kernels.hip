@@ -912,16 +912,19 @@ __global__ __launch_bounds__(256) void k_stream(ScoreArgs a) {
   };
   run_range(wave_range(static_end, wave, a.sgroup));
   if (a.dyn_tiles > 0) {
-    // counter k serves the chunks k, k + kDynCtr, ...; the blocks that share a
-    // counter span all XCDs (block b sits on XCD b mod 8)
-    const int k0 = (int)((blockIdx.x >> 3) % kDynCtr);
+    // K = min(kDynCtr, grid / 8) counters (at least one); counter k serves the
+    // chunks k, k + K, ..., and block b uses counter (b / 8) mod K, so every
+    // counter has blocks and the blocks that share one span all XCDs (block b
+    // sits on XCD b mod 8)
+    const int K = (int)min<int64_t>(kDynCtr, max<int64_t>(1, (int64_t)gridDim.x / 8));
+    const int k0 = (int)((blockIdx.x >> 3) % K);
     uint32_t* ctr = a.dyn_ctr + k0 * kDynStride;
     const int64_t nch = (a.dyn_tiles + a.dyn_chunk - 1) / a.dyn_chunk;
     for (;;) {
       uint32_t q = 0;
       if (lane == 0) q = atomicAdd(ctr, 1u);
       q = __builtin_amdgcn_readfirstlane(q);
-      const int64_t c = k0 + (int64_t)kDynCtr * q;
+      const int64_t c = k0 + (int64_t)K * q;
       if (c >= nch) break;
       WaveRange d;
       d.b0 = static_end + c * a.dyn_chunk;

@@ -127,6 +127,27 @@ def test_retrieve_c1_staged_and_planted():
     assert planted <= set(out1["frame_ids"][0].tolist())
 
 
+def test_small_grid_handed_out_tail_covers_last_tiles():
+    """The tiny workload runs the streaming pass on 16 blocks with the handed-out
+    tail on (4 segments against a 16-block grid).  The last frame gets twice the
+    keys of a planted frame, so the top rows of the last segment's lists sit in
+    its last tile, inside the last handed-out chunk: every chunk counter must
+    have waves, or those rows are never scored and the lists fall back."""
+    cfg, spec, q, keys = c1()
+    F, T = spec.n_frames, cfg.tokens_per_frame
+    src = spec.planted[-1]
+    for l in range(cfg.n_layers):
+        x = O.decode_bf16(keys[l])
+        x[:, (F - 1) * T:F * T, :] = 2.0 * x[:, src * T:(src + 1) * T, :]   # exact in bf16
+        keys[l] = W.bf16_bits(x.astype(np.float32))
+    gidx, oidx = make_pair(cfg, spec, keys)
+    out = debug_run([gidx], [q], cfg.top_k, cfg.n_select)
+    assert out["list_stats"][0, :, 1].sum() == 0    # no list needed the fallback
+    rep = staged_check(oidx, q, out, 0, cfg.top_k, cfg.n_select)
+    log(rep)
+    assert F - 1 in out["frame_ids"][0].tolist()
+
+
 def test_zero_queries_tie_rule():
     """All-zero queries: every score is 0, so each list keeps rows 0..k-1."""
     cfg, spec, q, keys = c1()
