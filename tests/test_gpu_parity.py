@@ -148,6 +148,24 @@ def test_small_grid_handed_out_tail_covers_last_tiles():
     assert F - 1 in out["frame_ids"][0].tolist()
 
 
+def test_selected_scores_have_the_recompute_bits():
+    """Every path scores a row with the same arithmetic: the scores the retrieval
+    selects (query prep fused with the sample pass, then the streaming pass) are
+    bit-equal to the standalone prep and recompute kernels' scores of the same
+    rows, in both head modes."""
+    cfg, spec, q, keys = c1()
+    gidx, _ = make_pair(cfg, spec, keys)
+    qd = [dev_bf16(x) for x in q]
+    for head_mode, n_lists in ((0, cfg.n_layers * cfg.n_q_heads), (1, cfg.n_layers)):
+        out = debug_run([gidx], [q], cfg.top_k, cfg.n_select, head_mode=head_mode)
+        for j in range(n_lists):
+            l, h = (j // cfg.n_q_heads, j % cfg.n_q_heads) if head_mode == 0 else (j, 0)
+            full = gidx.debug_scores(qd, l, h, head_mode=head_mode).cpu().numpy()
+            pos = out["topk_pos"][0, j]
+            got = out["topk_score"][0, j]
+            assert np.array_equal(got.view(np.uint32), full[pos].view(np.uint32)), (head_mode, j)
+
+
 def test_zero_queries_tie_rule():
     """All-zero queries: every score is 0, so each list keeps rows 0..k-1."""
     cfg, spec, q, keys = c1()
