@@ -542,6 +542,7 @@ struct ScoreArgs {
   int64_t tile_base[kMaxStreams + 1];  // first tile of each stream; tiles of all streams in a row
   int32_t ntile[kMaxStreams];          // 16-row tiles per (layer, KV head) segment
   int sgroup;                          // blocks per XCD group of the streaming pass
+  int xcd_weights;                     // weight the group ranges by XCD parity (MI355X with all 256 CUs)
   int64_t dyn_tiles;                   // the last tiles, handed out in chunks (0: all static)
   int dyn_chunk;                       // tiles per handed-out chunk
   uint32_t* dyn_ctr;                   // kDynCtr chunk counters, kDynStride words apart
@@ -746,7 +747,8 @@ constexpr int kStreamGroupMax = 32;
 // pattern on every box measured: with equal shares the even XCDs finish the
 // 1-hour pass at 350-380 us and the odd ones at 386-417 us), so a group on an
 // even XCD takes kXcdEvenWeight / kXcdOddWeight times the tiles of one on an odd
-// XCD.  Measured: 1-hour pass 409 -> 403 us, 16-stream batch 1,954 -> 1,932 us;
+// XCD (on a device of 256 CUs, the whole MI355X, where block b runs on XCD
+// b mod 8).  Measured: 1-hour pass 409 -> 403 us, 16-stream batch 1,954 -> 1,932 us;
 // the XCD end times then no longer split by parity but still spread by about
 // 20 us.  Handing the last 10-20% of the tiles out in chunks through atomic
 // counters (below) cost the 1-hour pass 7-35 us, since single-wave chunks lose
@@ -771,7 +773,7 @@ struct WaveRange {
   int sw, wg;       // waves in the group, this wave's rank among them
 };
 
-__device__ __forceinline__ WaveRange wave_range(int64_t total, int wave, int sgroup) {
+__device__ __forceinline__ WaveRange wave_range(int64_t total, int wave, int sgroup, bool xcd_weights) {
   const int64_t nb = gridDim.x, b = blockIdx.x;
   int64_t ng, grp;
   int members, rank;
@@ -782,9 +784,10 @@ __device__ __forceinline__ WaveRange wave_range(int64_t total, int wave, int sgr
     members = sgroup;
     rank = (int)(r % sgroup);
     // groups alternate even and odd XCDs; ng is a multiple of 8
-    const int64_t pair = kXcdEvenWeight + kXcdOddWeight;
-    const int64_t w0 = (grp / 2) * pair + (grp % 2) * kXcdEvenWeight;
-    const int64_t w1 = w0 + ((grp % 2) ? kXcdOddWeight : kXcdEvenWeight);
+    const int64_t even = xcd_weights ? kXcdEvenWeight : kXcdOddWeight;
+    const int64_t pair = even + kXcdOddWeight;
+    const int64_t w0 = (grp / 2) * pair + (grp % 2) * even;
+    const int64_t w1 = w0 + ((grp % 2) ? kXcdOddWeight : even);
     const int64_t wt = (ng / 2) * pair;
     WaveRange w;
     w.b0 = total * w0 / wt;
@@ -910,7 +913,7 @@ __global__ __launch_bounds__(256) void k_stream(ScoreArgs a) {
       if (__any(lc > 0)) stage_flush(a, list, colv, col, kg, st, lc);
     }
   };
-  run_range(wave_range(static_end, wave, a.sgroup));
+  run_range(wave_range(static_end, wave, a.sgroup, a.xcd_weights != 0));
   if (a.dyn_tiles > 0) {
     // K = min(kDynCtr, grid / 8) counters (at least one); counter k serves the
     // chunks k, k + K, ..., and block b uses counter (b / 8) mod K, so every
@@ -1163,7 +1166,7 @@ __global__ __launch_bounds__(256) void k_stream_hm(ScoreArgs a) {
   const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
   u32x4* lt_ = tiles[wave];
   uint64_t* st = stage + wave * kStage;
-  const WaveRange wr = wave_range(a.tile_base[a.S], wave, a.sgroup);
+  const WaveRange wr = wave_range(a.tile_base[a.S], wave, a.sgroup, a.xcd_weights != 0);
   const int SW = wr.sw;
   for (int64_t T = wr.b0; T < wr.b1;) {
     int s = 0;
@@ -3190,6 +3193,7 @@ ScoreArgs make_score_args(const RetrievePlan& p, int kind) {
   a.tau = p.tau; a.cnt = p.cnt; a.cand = p.cand; a.cap = p.cap;
   a.flag = p.flag; a.only_list = -1; a.full = p.full; a.row0 = 0;
   a.sgroup = kStreamGroupMax;
+  a.xcd_weights = 0;
   a.dyn_tiles = 0;
   a.dyn_chunk = kDynChunk;
   a.dyn_ctr = p.dyn_ctr;
@@ -3322,6 +3326,7 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
       int nseg = 0;   // (stream, layer, KV head) segments with rows
       for (int s = 0; s < p.S; ++s) nseg += a.ntile[s] > 0 ? p.L * p.Hk : 0;
       a.sgroup = stream_group(grid, nseg);
+      a.xcd_weights = cus == 256;
       if (a.sgroup < kStreamGroupMax) a.dyn_tiles = tiles * kDynPermille / 1000;
       hipLaunchKernelGGL(k_stream<D>, dim3(grid), dim3(256), 0, st, a);
     }
@@ -3338,6 +3343,7 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
       int nseg = 0;   // (stream, layer) segments with rows
       for (int s = 0; s < p.S; ++s) nseg += a.ntile[s] > 0 ? p.L : 0;
       a.sgroup = stream_group(grid, nseg);
+      a.xcd_weights = cus == 256;
       hipLaunchKernelGGL(k_stream_hm<D>, dim3(grid), dim3(256), 0, st, a);
     }
   }
