@@ -111,8 +111,15 @@ typedef struct {
 size_t ss_index_required_bytes(const ss_index_desc* desc);
 
 /* Create an empty index over a caller-owned device arena of at least
- * ss_index_required_bytes(desc) bytes, 256-byte aligned.  The arena must stay
- * allocated until ss_index_destroy.  *out receives the handle. */
+ * ss_index_required_bytes(desc) bytes, 256-byte aligned: the full-history
+ * shallow cache of Sec. 4.1 ("Full-History Shallow Cache", Eq.
+ * shallow_streaming_cache) for L_s = P shallow layers, with room for each
+ * unit's descriptor (Eq. memory_key).  Only keys are kept: the values of the
+ * cache are not read by retrieval.  The arena must stay allocated until
+ * ss_index_destroy; the library writes it only through ss_index_append.
+ * *out receives the handle (host memory owned by the library).  Errors:
+ * SS_ERR_INVALID_ARGUMENT / SS_ERR_UNSUPPORTED for a bad shape, SS_ERR_CAPACITY
+ * when arena_bytes is too small; nothing is created then. */
 ss_status ss_index_create(const ss_index_desc* desc, void* dev_arena, size_t arena_bytes,
                           ss_index** out);
 
@@ -122,7 +129,10 @@ ss_status ss_index_destroy(ss_index* idx);
 /* Host-side counters: frames and rows per (layer, KV head) stored so far. */
 ss_status ss_index_info(const ss_index* idx, int64_t* n_frames, int64_t* n_rows);
 
-/* Append n_frames frames of n_tokens visual tokens each (Eq. shallow_streaming_cache).
+/* Append n_frames frames of n_tokens visual tokens each: each unit's keys at
+ * every shallow layer join the cache in temporal order (Sec. 4.1, Eq.
+ * shallow_streaming_cache; frame t of the paper's stream is frame id t - 1
+ * here), and its descriptor (Eq. memory_key) is computed on the device.
  *   layer_keys  host array of L_s device pointers; pointer l addresses bf16
  *               [H_kv][n_frames*n_tokens][d] keys of shallow layer l (16-byte
  *               aligned).  Frame f owns tokens [f*n_tokens, (f+1)*n_tokens).
@@ -131,7 +141,9 @@ ss_status ss_index_info(const ss_index* idx, int64_t* n_frames, int64_t* n_rows)
  *               append order from 0).
  * The unit descriptor (Eq. memory_key) always uses the raw keys of the last
  * shallow layer.  Fails with SS_ERR_CAPACITY (index unchanged) if the frames or
- * rows do not fit. */
+ * rows do not fit; the host bookkeeping is reserved before any work is
+ * enqueued, so an error return never leaves work behind on `stream`.  The
+ * keys are read by the enqueued kernels: keep them valid until they finish. */
 ss_status ss_index_append(ss_index* idx, const void* const* layer_keys, int32_t n_frames,
                           int32_t n_tokens, const ss_compress* compress, void* stream,
                           int64_t* first_frame_id);
@@ -141,7 +153,15 @@ ss_status ss_index_append(ss_index* idx, const void* const* layer_keys, int32_t 
 size_t ss_retrieve_workspace_bytes(ss_index* const* idx, int32_t n_streams, const int32_t* n_q,
                                    const ss_retrieve_params* params);
 
-/* Evidence retrieval for n_streams independent streams with one question each.
+/* Evidence retrieval for n_streams independent streams with one question each
+ * (Sec. 4.2, "Optional Evidence Retrieval"): the candidate tokens are those of
+ * every frame except the newest n_recent (Eq. context_partition) and, after
+ * long-history compression, those of the detailed window only; each list
+ * keeps its top_k tokens (Eq. token_vote_candidates), every selected token
+ * votes for its frame, the pool_mult*n_select frames with the most votes
+ * (ties by attention mass, then the lower frame id) form the pool, and greedy
+ * max-min diversity over the descriptors of Eq. memory_key picks n_select of
+ * them (DivTopK of Eq. selected_evidence).
  *   idx        host array of n_streams handles with identical shapes.
  *   queries    host array of n_streams*L_s device pointers, stream-major;
  *              pointer [s*L_s + l] addresses bf16 [H_q][n_q[s]][d] query states
@@ -328,6 +348,16 @@ ss_status ss_debug_scores(const ss_index* idx, const void* const* queries, int32
  *   frame_offsets_host  int64 [n_frames+1] host row offsets. */
 ss_status ss_index_export(const ss_index* idx, void* rows_dev, int32_t* counts_dev,
                           float* desc_dev, int64_t* frame_offsets_host, void* stream);
+
+/* The sample plan ss_retrieve uses for one list of n_rows candidate rows and
+ * top_k (parity only; host work only).  The streaming cut-off of the list is
+ * the r-th largest score among m evenly spread sampled rows: sample u < m is
+ * row (u * step + step / 2) >> 32 with step = floor(n_rows * 2^32 / m), in
+ * unsigned 64-bit arithmetic.  out (host int32 [4]): m, r, the list's
+ * candidate capacity (a batch uses the capacity of its longest list), and
+ * the expected candidate count the plan aims at (0 when n_rows is 0).  With
+ * m = n_rows every row is sampled and r = min(top_k, n_rows). */
+ss_status ss_debug_sample_plan(int64_t n_rows, int32_t top_k, int32_t* out);
 
 /* Optional timing hook for the streaming scoring kernel: when both are
  * non-NULL hipEvent_t handles, later ss_retrieve calls on this thread record

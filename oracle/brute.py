@@ -4,7 +4,8 @@ TEST INFRASTRUCTURE ONLY (see the package docstring).  Written independently of
 ``oracle.oracle``: plain loops, ``math.fsum`` for every sum, Python's ``sorted``
 with explicit tuple keys, and token scores taken as the mean of the per-token
 scaled logits (Sec. 4.2, "Optional Evidence Retrieval"), not a pre-averaged
-query.  It exists to cross-check the vectorised oracle.
+query; attention probabilities from explicit exponentials of each list.  It
+exists to cross-check the vectorised oracle.
 """
 from __future__ import annotations
 
@@ -74,12 +75,17 @@ def kmeans(X, n_centroids: int, n_iters: int):
 
 
 def retrieve(frames, queries, n_kv_heads: int, top_k: int, n_select: int, pool_mult: int = 4,
-             n_recent: int = 0):
+             n_recent: int = 0, head_mode: int = 0, score_mode: int = 0):
     """Brute-force retrieval over raw (uncompressed) frames.
 
     ``frames[t][l][g][p]`` : list of bfloat16 bit rows (length d) of frame ``t``;
     ``queries[l][h][j]``   : bfloat16 bit rows of query token ``j`` of head ``h``.
-    Returns ``(frame_ids, votes, mass, debug)`` with the padding of the oracle.
+    ``score_mode`` 1 turns each (layer, head)'s logits into attention
+    probabilities over the candidate rows (``exp(s - lse)``, ``lse`` from the
+    largest logit plus the log of an ``fsum`` of exponentials); ``head_mode`` 1
+    averages the per-head values of a row over the layer's heads (one list per
+    layer).  Returns ``(frame_ids, votes, mass, debug)`` with the padding of the
+    oracle.
     """
     F = len(frames)
     L = len(queries)
@@ -87,25 +93,33 @@ def retrieve(frames, queries, n_kv_heads: int, top_k: int, n_select: int, pool_m
     G = Hq // n_kv_heads
     d = len(queries[0][0][0])
     F_c = max(0, F - n_recent)
-    # row positions are append order within each (layer, KV head)
-    rows = []                      # (frame, position)
-    pos = 0
+    owner = []                     # frame of each candidate row, in append order
     for t in range(F_c):
-        for _ in range(len(frames[t][0][0])):
-            rows.append((t, pos))
-            pos += 1
+        owner.extend([t] * len(frames[t][0][0]))
     lists = []
     for l in range(L):
+        per_head = []
         for h in range(Hq):
             g = h // G
             qs = [_vec(qj) for qj in queries[l][h]]
-            scored = []
+            vals = []
             for t in range(F_c):
-                for p_local, krow in enumerate(frames[t][l][g]):
+                for krow in frames[t][l][g]:
                     k = _vec(krow)
                     logits = [math.fsum(a * b for a, b in zip(q, k)) / math.sqrt(d) for q in qs]
-                    s = math.fsum(logits) / len(logits)
-                    scored.append((s, t, len(scored)))
+                    vals.append(math.fsum(logits) / len(logits))
+            if score_mode == 1 and vals:
+                top = max(vals)
+                lse = top + math.log(math.fsum(math.exp(v - top) for v in vals))
+                vals = [math.exp(v - lse) for v in vals]
+            per_head.append(vals)
+        if head_mode == 0:
+            row_lists = per_head
+        else:
+            n = len(owner)
+            row_lists = [[math.fsum(per_head[h][p] for h in range(Hq)) / Hq for p in range(n)]]
+        for vals in row_lists:
+            scored = [(v, owner[p], p) for p, v in enumerate(vals)]
             ranked = sorted(scored, key=lambda x: (-x[0], x[2]))
             lists.append(ranked[:min(top_k, len(ranked))])
     votes = [0] * F

@@ -13,12 +13,14 @@ Construction" and Sec. 4.2 "Query-Time Answering"):
   optional compression idea of Sec. 4.1, specified by the workload: k-means with
   farthest-point seeding, see ``kmeans``);
 * candidates: every unit except the newest ``n_recent`` (Eq. context_partition);
-* token scores: scaled Q-K logits of the question against every candidate key
-  (Sec. 4.2, "Optional Evidence Retrieval"), per (layer, query head), with the
-  text-token queries reduced by their mean (``score_lists``);
+* token scores (Sec. 4.2, "Optional Evidence Retrieval"), per (layer, query
+  head), with the text-token queries reduced by their mean: either the scaled
+  Q-K logit of the question against every candidate key, or the attention
+  probability (the softmax of those logits over the candidate rows); per head
+  or averaged over heads (``score_lists``);
 * top-k per list (Eq. token_vote_candidates), ties to the lower row position;
 * one vote per selected token for its unit, and the selected tokens' summed
-  scores as the unit's "attention mass" tie-breaker;
+  list values as the unit's "attention mass" tie-breaker;
 * a vote-ranked pool of ``pool_mult * K`` units, then greedy max-min diversity in
   descriptor space (the DivTopK of Eq. selected_evidence).
 
@@ -327,22 +329,36 @@ def query_means(queries) -> list[np.ndarray]:
     return [decode_bf16(q).mean(axis=1) for q in queries]
 
 
-def score_lists(index: Index, queries, head_mode: int = 0, chunk_rows: int = 1 << 16):
+def score_lists(index: Index, queries, head_mode: int = 0, score_mode: int = 0,
+                chunk_rows: int = 1 << 16):
     """Token scores of every candidate row.
 
-    Reading: the paper scores with the final prompt token; with several text
-    tokens the score of a row is the mean over tokens of the scaled logit
-    ``q_j . K_p / sqrt(d)``, which equals ``mean_j(q_j) . K_p / sqrt(d)`` and is
-    the paper's score when there is one token.  Keys and queries are taken as
-    already rotated (RoPE upstream).  Query head ``h`` reads KV head ``h // G``.
+    Reading of multi-token questions: the paper scores with the final prompt
+    token; with several text tokens the logit of a row is the mean over tokens
+    of the scaled logit ``q_j . K_p / sqrt(d)``, which equals
+    ``mean_j(q_j) . K_p / sqrt(d)`` and is the paper's logit when there is one
+    token.  Keys and queries are taken as already rotated (RoPE upstream).
+    Query head ``h`` reads KV head ``h // G``.
+
+    ``score_mode == 0``: the value of a row in list (l, h) is that scaled logit.
+    ``score_mode == 1``: the attention the question pays to the row (Sec. 4.2
+    scores candidates by Q-K attention): the softmax of the list's logits over
+    the candidate rows, ``exp(s_p - lse)`` with ``lse = log sum_p' exp(s_p')``
+    over every candidate row ``p'`` of that (layer, query head).
 
     ``head_mode == 0``: one list per (layer, query head), ordered layer-major.
-    ``head_mode == 1``: one list per layer, the scores averaged over all query
-    heads (the paper's own head reduction).
+    ``head_mode == 1``: one list per layer, the values averaged over all query
+    heads (Eq. token_vote_candidates averages over attention heads).  Under
+    ``score_mode == 1`` each head is normalised by its own softmax before the
+    average, so the two score modes rank rows differently in this head mode.
 
     Returns a list of float64 arrays over the candidate rows; position p is
     row ``index.first_candidate_row() + p``.
     """
+    if head_mode not in (0, 1):
+        raise ValueError("head_mode must be 0 or 1")
+    if score_mode not in (0, 1):
+        raise ValueError("score_mode must be 0 or 1")
     lo = index.first_candidate_row()
     N = index.candidate_rows() - lo
     scale = 1.0 / math.sqrt(index.d)
@@ -357,13 +373,21 @@ def score_lists(index: Index, queries, head_mode: int = 0, chunk_rows: int = 1 <
                 r1 = min(N, r0 + chunk_rows)
                 Kc = decode_bf16(K[g, lo + r0:lo + r1, :])      # [r][d]
                 per_head[g * index.G:(g + 1) * index.G, r0:r1] = (Kc @ Qg.T).T * scale
+        if score_mode == 1 and N > 0:
+            per_head = softmax_rows(per_head)
         if head_mode == 0:
             lists.extend(per_head[h] for h in range(index.Hq))
-        elif head_mode == 1:
-            lists.append(per_head.mean(axis=0))
         else:
-            raise ValueError("head_mode must be 0 or 1")
+            lists.append(per_head.mean(axis=0))
     return lists
+
+
+def softmax_rows(x: np.ndarray) -> np.ndarray:
+    """Softmax of each row of ``x`` (shifted by the row maximum, which leaves the
+    value unchanged and keeps ``exp`` finite)."""
+    m = x.max(axis=1, keepdims=True)
+    e = np.exp(x - m)
+    return e / e.sum(axis=1, keepdims=True)
 
 
 def score_scale(index: Index, queries, layer: int, q_head: int) -> np.ndarray:
@@ -385,7 +409,8 @@ def topk(scores: np.ndarray, k: int) -> np.ndarray:
 def votes_and_mass(index: Index, topk_lists, score_lists_):
     """One vote per selected token for the unit that owns it (the vote count
     ``v_t``), and the unit's attention mass: the sum of its selected tokens'
-    scores, accumulated in (list, rank) order.
+    list values (scaled logits, or attention probabilities under
+    ``score_mode == 1``), accumulated in (list, rank) order.
 
     Returns ``(votes [F] int64, mass [F] float64)`` over all frames.
     """
@@ -441,7 +466,7 @@ def maxmin_select(pool: np.ndarray, desc: np.ndarray, K: int):
 
 
 def retrieve(index: Index, queries, top_k: int, n_select: int, pool_mult: int = 4,
-             head_mode: int = 0, debug: bool = False):
+             head_mode: int = 0, debug: bool = False, score_mode: int = 0):
     """Evidence retrieval for one stream and one question.
 
     Returns ``(frame_ids, votes, mass, n_out)``: ``frame_ids`` in max-min
@@ -451,7 +476,7 @@ def retrieve(index: Index, queries, top_k: int, n_select: int, pool_mult: int = 
     """
     if top_k < 1 or n_select < 1 or pool_mult < 1:
         raise ValueError("top_k, n_select and pool_mult must be >= 1")
-    S = score_lists(index, queries, head_mode)
+    S = score_lists(index, queries, head_mode, score_mode)
     T = [topk(s, top_k) for s in S]
     votes, mass = votes_and_mass(index, T, S)
     pool = vote_pool(votes, mass, pool_mult * n_select)

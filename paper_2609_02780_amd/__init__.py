@@ -6,6 +6,7 @@ The work runs in ``libshallowstream.so`` (HIP kernels behind the C ABI of
 """
 from ._lib import SSError, lib  # noqa: F401
 from .index import (LongClusters, PooledRanker, Retriever, ShallowIndex, assemble_evidence,  # noqa: F401
-                    set_profile_events)
+                    sample_plan, set_profile_events)
 
-__all__ = ["ShallowIndex", "Retriever", "PooledRanker", "LongClusters", "assemble_evidence", "SSError", "set_profile_events", "lib"]
+__all__ = ["ShallowIndex", "Retriever", "PooledRanker", "LongClusters", "assemble_evidence", "SSError", "sample_plan",
+           "set_profile_events", "lib"]

@@ -90,6 +90,7 @@ _SIGS = {
     "ss_evidence_max_units": (C.c_int32, [C.POINTER(EvidenceParams), C.c_int32]),
     "ss_assemble_evidence": (C.c_int32, [C.POINTER(_P), C.c_int32, _P, C.c_int32, C.POINTER(EvidenceParams), _P,
                                          _P, _P, C.c_int32]),
+    "ss_debug_sample_plan": (C.c_int32, [C.c_int64, C.c_int32, C.POINTER(C.c_int32)]),
     "ss_set_profile_events": (C.c_int32, [_P, _P]),
     "ss_status_string": (C.c_char_p, [C.c_int32]),
     "ss_last_error": (C.c_char_p, []),

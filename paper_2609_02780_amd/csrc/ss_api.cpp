@@ -29,18 +29,30 @@ struct ss_index {
 
 namespace {
 
-thread_local std::string g_err;
+// The last failure's text: a fixed buffer, so recording an error never allocates.
+thread_local char g_err[512] = "";
 thread_local hipEvent_t g_ev_start = nullptr;
 thread_local hipEvent_t g_ev_stop = nullptr;
 
 ss_status fail(ss_status st, const char* fmt, ...) {
-  char buf[512];
   va_list ap;
   va_start(ap, fmt);
-  std::vsnprintf(buf, sizeof buf, fmt, ap);
+  std::vsnprintf(g_err, sizeof g_err, fmt, ap);
   va_end(ap);
-  g_err = buf;
   return st;
+}
+
+// Runs the body of an entry point; no C++ exception crosses the C ABI (host
+// allocations can throw std::bad_alloc).
+template <class F>
+ss_status guarded(F&& body) noexcept {
+  try {
+    return body();
+  } catch (const std::bad_alloc&) {
+    return fail(SS_ERR_INTERNAL, "out of host memory");
+  } catch (...) {
+    return fail(SS_ERR_INTERNAL, "unexpected C++ exception");
+  }
 }
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -252,7 +264,7 @@ void build_plan(ss::RetrievePlan& p, ss_index* const* idx, int s0, int S, const 
   p.pool = prm->pool_mult * prm->n_select;
   p.chunk_rows = kChunkRows;
   p.samp_chunk = kSampleChunk;
-  int64_t n_max = 0, full = 0;
+  int64_t n_max = 0;
   int hist = 1;
   for (int i = 0; i < S; ++i) {
     const ss_index* x = idx[s0 + i];
@@ -283,14 +295,11 @@ void build_plan(ss::RetrievePlan& p, ss_index* const* idx, int s0, int S, const 
     p.k_max = std::max(p.k_max, z.kk);
     p.m_max = std::max(p.m_max, z.m);
     p.f_max = std::max(p.f_max, z.f);
-    p.full_base[i] = full;
-    full += (int64_t)p.NL * rows;
     hist = (int)std::max<int64_t>(hist, x->desc.max_frames);
   }
   p.f_max = std::max(p.f_max, 1);
   p.m_max = std::max(p.m_max, 1);
   p.cap = (int)candidate_cap(prm->top_k, n_max);
-  p.full_total = full;
   p.dbg_hist_stride = hist;
 }
 
@@ -483,32 +492,36 @@ size_t ss_clusters_required_bytes(const ss_cluster_desc* desc) {
 
 ss_status ss_clusters_create(const ss_cluster_desc* desc, void* dev_arena, size_t arena_bytes, void* stream,
                              ss_clusters** out) {
-  if (!out) return fail(SS_ERR_INVALID_ARGUMENT, "out is NULL");
-  if (!cluster_desc_ok(desc)) return fail(SS_ERR_INVALID_ARGUMENT, "invalid cluster description");
-  if (!dev_arena || !aligned(dev_arena, 256)) return fail(SS_ERR_INVALID_ARGUMENT, "arena NULL or not 256-byte aligned");
-  const ClusterLayout L = cluster_layout(*desc);
-  if (arena_bytes < L.total) return fail(SS_ERR_CAPACITY, "arena %zu bytes, %zu needed", arena_bytes, L.total);
-  ss_clusters* c = new (std::nothrow) ss_clusters;
-  if (!c) return fail(SS_ERR_INTERNAL, "out of host memory");
-  c->desc = *desc;
-  char* b = static_cast<char*>(dev_arena);
-  c->dev.state = reinterpret_cast<int32_t*>(b + L.state);
-  c->dev.centroids = reinterpret_cast<float*>(b + L.centroids);
-  c->dev.sizes = reinterpret_cast<int32_t*>(b + L.sizes);
-  c->dev.span = reinterpret_cast<int64_t*>(b + L.span);
-  c->dev.reps = reinterpret_cast<float*>(b + L.reps);
-  const hipError_t e = ss::launch_zero32(c->dev.state, 4, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) {
-    delete c;
-    return fail(SS_ERR_DEVICE, "cluster state reset: %s", hipGetErrorString(e));
-  }
-  *out = c;
-  return SS_OK;
+  return guarded([&]() -> ss_status {
+    if (!out) return fail(SS_ERR_INVALID_ARGUMENT, "out is NULL");
+    if (!cluster_desc_ok(desc)) return fail(SS_ERR_INVALID_ARGUMENT, "invalid cluster description");
+    if (!dev_arena || !aligned(dev_arena, 256)) return fail(SS_ERR_INVALID_ARGUMENT, "arena NULL or not 256-byte aligned");
+    const ClusterLayout L = cluster_layout(*desc);
+    if (arena_bytes < L.total) return fail(SS_ERR_CAPACITY, "arena %zu bytes, %zu needed", arena_bytes, L.total);
+    ss_clusters* c = new (std::nothrow) ss_clusters;
+    if (!c) return fail(SS_ERR_INTERNAL, "out of host memory");
+    c->desc = *desc;
+    char* b = static_cast<char*>(dev_arena);
+    c->dev.state = reinterpret_cast<int32_t*>(b + L.state);
+    c->dev.centroids = reinterpret_cast<float*>(b + L.centroids);
+    c->dev.sizes = reinterpret_cast<int32_t*>(b + L.sizes);
+    c->dev.span = reinterpret_cast<int64_t*>(b + L.span);
+    c->dev.reps = reinterpret_cast<float*>(b + L.reps);
+    const hipError_t e = ss::launch_zero32(c->dev.state, 4, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) {
+      delete c;
+      return fail(SS_ERR_DEVICE, "cluster state reset: %s", hipGetErrorString(e));
+    }
+    *out = c;
+    return SS_OK;
+  });
 }
 
 ss_status ss_clusters_destroy(ss_clusters* cl) {
-  delete cl;
-  return SS_OK;
+  return guarded([&]() -> ss_status {
+    delete cl;
+    return SS_OK;
+  });
 }
 
 size_t ss_clusters_absorb_workspace_bytes(int64_t n_frames) {
@@ -517,36 +530,38 @@ size_t ss_clusters_absorb_workspace_bytes(int64_t n_frames) {
 
 ss_status ss_clusters_absorb(ss_clusters* cl, ss_index* idx, int64_t frame_hi, void* ws, size_t ws_bytes,
                              void* stream) {
-  if (!cl || !idx) return fail(SS_ERR_INVALID_ARGUMENT, "cluster set or index is NULL");
-  const ss_cluster_desc& c = cl->desc;
-  const ss_index_desc& d = idx->desc;
-  if (c.n_layers != d.n_layers || c.n_kv_heads != d.n_kv_heads || c.head_dim != d.head_dim)
-    return fail(SS_ERR_INVALID_ARGUMENT, "cluster set and index shapes differ");
-  const int64_t f_lo = idx->first_detail;
-  const int64_t f_end = std::max<int64_t>(0, idx->n_frames - d.n_recent);
-  if (frame_hi < f_lo || frame_hi > f_end)
-    return fail(SS_ERR_INVALID_ARGUMENT, "frame_hi %lld outside %lld..%lld (frames leave in order, never from the recent window)",
-                (long long)frame_hi, (long long)f_lo, (long long)f_end);
-  for (int64_t f = f_lo; f < frame_hi; ++f)
-    if (idx->off[f + 1] - idx->off[f] != c.rows_per_unit)
-      return fail(SS_ERR_INVALID_ARGUMENT, "frame %lld stores %lld rows, the cluster set takes %d", (long long)f,
-                  (long long)(idx->off[f + 1] - idx->off[f]), c.rows_per_unit);
-  const int64_t n = frame_hi - f_lo;
-  if (n > 0x7FFFFFFF) return fail(SS_ERR_UNSUPPORTED, "too many frames in one call");
-  if (n > 0 && (!ws || !aligned(ws, 256) || ws_bytes < ss_clusters_absorb_workspace_bytes(n)))
-    return fail(SS_ERR_WORKSPACE, "absorb workspace NULL, misaligned or below %zu bytes",
-                ss_clusters_absorb_workspace_bytes(n));
-  ss::AbsorbArgs a{};
-  a.L = c.n_layers; a.Hk = c.n_kv_heads; a.D = c.head_dim; a.R = c.rows_per_unit;
-  a.max_clusters = c.max_clusters; a.max_rows = d.max_rows; a.tau = c.tau;
-  a.f_lo = f_lo; a.n_units = (int)n; a.row_lo = idx->off[f_lo];
-  a.desc = idx->dev.desc; a.keys = idx->dev.keys;
-  a.assign = static_cast<int32_t*>(ws);
-  a.cl = cl->dev;
-  const hipError_t e = ss::launch_absorb(a, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(SS_ERR_DEVICE, "absorb launch failed: %s", hipGetErrorString(e));
-  idx->first_detail = frame_hi;
-  return SS_OK;
+  return guarded([&]() -> ss_status {
+    if (!cl || !idx) return fail(SS_ERR_INVALID_ARGUMENT, "cluster set or index is NULL");
+    const ss_cluster_desc& c = cl->desc;
+    const ss_index_desc& d = idx->desc;
+    if (c.n_layers != d.n_layers || c.n_kv_heads != d.n_kv_heads || c.head_dim != d.head_dim)
+      return fail(SS_ERR_INVALID_ARGUMENT, "cluster set and index shapes differ");
+    const int64_t f_lo = idx->first_detail;
+    const int64_t f_end = std::max<int64_t>(0, idx->n_frames - d.n_recent);
+    if (frame_hi < f_lo || frame_hi > f_end)
+      return fail(SS_ERR_INVALID_ARGUMENT, "frame_hi %lld outside %lld..%lld (frames leave in order, never from the recent window)",
+                  (long long)frame_hi, (long long)f_lo, (long long)f_end);
+    for (int64_t f = f_lo; f < frame_hi; ++f)
+      if (idx->off[f + 1] - idx->off[f] != c.rows_per_unit)
+        return fail(SS_ERR_INVALID_ARGUMENT, "frame %lld stores %lld rows, the cluster set takes %d", (long long)f,
+                    (long long)(idx->off[f + 1] - idx->off[f]), c.rows_per_unit);
+    const int64_t n = frame_hi - f_lo;
+    if (n > 0x7FFFFFFF) return fail(SS_ERR_UNSUPPORTED, "too many frames in one call");
+    if (n > 0 && (!ws || !aligned(ws, 256) || ws_bytes < ss_clusters_absorb_workspace_bytes(n)))
+      return fail(SS_ERR_WORKSPACE, "absorb workspace NULL, misaligned or below %zu bytes",
+                  ss_clusters_absorb_workspace_bytes(n));
+    ss::AbsorbArgs a{};
+    a.L = c.n_layers; a.Hk = c.n_kv_heads; a.D = c.head_dim; a.R = c.rows_per_unit;
+    a.max_clusters = c.max_clusters; a.max_rows = d.max_rows; a.tau = c.tau;
+    a.f_lo = f_lo; a.n_units = (int)n; a.row_lo = idx->off[f_lo];
+    a.desc = idx->dev.desc; a.keys = idx->dev.keys;
+    a.assign = static_cast<int32_t*>(ws);
+    a.cl = cl->dev;
+    const hipError_t e = ss::launch_absorb(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(SS_ERR_DEVICE, "absorb launch failed: %s", hipGetErrorString(e));
+    idx->first_detail = frame_hi;
+    return SS_OK;
+  });
 }
 
 size_t ss_clusters_retrieve_workspace_bytes(const ss_clusters* cl) {
@@ -560,51 +575,55 @@ ss_status ss_clusters_retrieve(const ss_clusters* cl, const ss_index* idx, const
                                int32_t n_q, int32_t k_clusters, void* ws, size_t ws_bytes, void* stream,
                                int64_t* cluster_ids, float* scores, int64_t* first_frame,
                                int64_t* last_frame, int32_t* n_out) {
-  if (!cl || !idx) return fail(SS_ERR_INVALID_ARGUMENT, "cluster set or index is NULL");
-  const ss_index_desc& d = idx->desc;
-  if (cl->desc.n_layers != d.n_layers || cl->desc.n_kv_heads != d.n_kv_heads || cl->desc.head_dim != d.head_dim)
-    return fail(SS_ERR_INVALID_ARGUMENT, "cluster set and index shapes differ");
-  if (n_q < 1 || n_q > 4096) return fail(SS_ERR_INVALID_ARGUMENT, "n_q %d outside 1..4096", n_q);
-  if (k_clusters < 1 || k_clusters > ss::kMaxSelect)
-    return fail(SS_ERR_UNSUPPORTED, "k_clusters %d outside 1..%d", k_clusters, ss::kMaxSelect);
-  if (!queries || !queries[d.n_layers - 1]) return fail(SS_ERR_INVALID_ARGUMENT, "last-layer queries are NULL");
-  if (!aligned(queries[d.n_layers - 1], 16)) return fail(SS_ERR_INVALID_ARGUMENT, "queries not 16-byte aligned");
-  if (!cluster_ids || !scores || !first_frame || !last_frame || !n_out)
-    return fail(SS_ERR_INVALID_ARGUMENT, "an output pointer is NULL");
-  ss::ClusterQueryPlan p{};
-  p.L = d.n_layers; p.Hq = d.n_q_heads; p.Hk = d.n_kv_heads; p.G = p.Hq / p.Hk; p.D = d.head_dim;
-  p.nq = n_q; p.k = k_clusters; p.max_clusters = cl->desc.max_clusters;
-  p.q_last = static_cast<const uint16_t*>(queries[d.n_layers - 1]);
-  p.cl = cl->dev;
-  const size_t need = ss::cluster_query_workspace(p, nullptr);
-  if (!ws || !aligned(ws, 256) || ws_bytes < need)
-    return fail(SS_ERR_WORKSPACE, "cluster retrieval workspace NULL, misaligned or below %zu bytes", need);
-  ss::cluster_query_workspace(p, ws);
-  p.out_ids = cluster_ids; p.out_scores = scores; p.out_first = first_frame; p.out_last = last_frame;
-  p.out_n = n_out;
-  const hipError_t e = ss::launch_cluster_query(p, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(SS_ERR_DEVICE, "cluster retrieval launch failed: %s", hipGetErrorString(e));
-  return SS_OK;
+  return guarded([&]() -> ss_status {
+    if (!cl || !idx) return fail(SS_ERR_INVALID_ARGUMENT, "cluster set or index is NULL");
+    const ss_index_desc& d = idx->desc;
+    if (cl->desc.n_layers != d.n_layers || cl->desc.n_kv_heads != d.n_kv_heads || cl->desc.head_dim != d.head_dim)
+      return fail(SS_ERR_INVALID_ARGUMENT, "cluster set and index shapes differ");
+    if (n_q < 1 || n_q > 4096) return fail(SS_ERR_INVALID_ARGUMENT, "n_q %d outside 1..4096", n_q);
+    if (k_clusters < 1 || k_clusters > ss::kMaxSelect)
+      return fail(SS_ERR_UNSUPPORTED, "k_clusters %d outside 1..%d", k_clusters, ss::kMaxSelect);
+    if (!queries || !queries[d.n_layers - 1]) return fail(SS_ERR_INVALID_ARGUMENT, "last-layer queries are NULL");
+    if (!aligned(queries[d.n_layers - 1], 16)) return fail(SS_ERR_INVALID_ARGUMENT, "queries not 16-byte aligned");
+    if (!cluster_ids || !scores || !first_frame || !last_frame || !n_out)
+      return fail(SS_ERR_INVALID_ARGUMENT, "an output pointer is NULL");
+    ss::ClusterQueryPlan p{};
+    p.L = d.n_layers; p.Hq = d.n_q_heads; p.Hk = d.n_kv_heads; p.G = p.Hq / p.Hk; p.D = d.head_dim;
+    p.nq = n_q; p.k = k_clusters; p.max_clusters = cl->desc.max_clusters;
+    p.q_last = static_cast<const uint16_t*>(queries[d.n_layers - 1]);
+    p.cl = cl->dev;
+    const size_t need = ss::cluster_query_workspace(p, nullptr);
+    if (!ws || !aligned(ws, 256) || ws_bytes < need)
+      return fail(SS_ERR_WORKSPACE, "cluster retrieval workspace NULL, misaligned or below %zu bytes", need);
+    ss::cluster_query_workspace(p, ws);
+    p.out_ids = cluster_ids; p.out_scores = scores; p.out_first = first_frame; p.out_last = last_frame;
+    p.out_n = n_out;
+    const hipError_t e = ss::launch_cluster_query(p, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(SS_ERR_DEVICE, "cluster retrieval launch failed: %s", hipGetErrorString(e));
+    return SS_OK;
+  });
 }
 
 ss_status ss_clusters_export(const ss_clusters* cl, int32_t* state, float* centroids, int32_t* sizes,
                              int64_t* span, float* reps, void* stream) {
-  if (!cl) return fail(SS_ERR_INVALID_ARGUMENT, "cluster set is NULL");
-  const ss_cluster_desc& c = cl->desc;
-  const size_t M = (size_t)c.max_clusters, dim = (size_t)c.n_kv_heads * c.head_dim;
-  const hipStream_t hs = static_cast<hipStream_t>(stream);
-  struct Part { void* dst; const void* src; size_t bytes; } parts[] = {
-      {state, cl->dev.state, 8},
-      {centroids, cl->dev.centroids, M * dim * 4},
-      {sizes, cl->dev.sizes, M * 4},
-      {span, cl->dev.span, M * 16},
-      {reps, cl->dev.reps, M * c.n_layers * dim * c.rows_per_unit * 4}};
-  for (const Part& q : parts) {
-    if (!q.dst) continue;
-    const hipError_t e = hipMemcpyAsync(q.dst, q.src, q.bytes, hipMemcpyDeviceToDevice, hs);
-    if (e != hipSuccess) return fail(SS_ERR_DEVICE, "cluster export: %s", hipGetErrorString(e));
-  }
-  return SS_OK;
+  return guarded([&]() -> ss_status {
+    if (!cl) return fail(SS_ERR_INVALID_ARGUMENT, "cluster set is NULL");
+    const ss_cluster_desc& c = cl->desc;
+    const size_t M = (size_t)c.max_clusters, dim = (size_t)c.n_kv_heads * c.head_dim;
+    const hipStream_t hs = static_cast<hipStream_t>(stream);
+    struct Part { void* dst; const void* src; size_t bytes; } parts[] = {
+        {state, cl->dev.state, 8},
+        {centroids, cl->dev.centroids, M * dim * 4},
+        {sizes, cl->dev.sizes, M * 4},
+        {span, cl->dev.span, M * 16},
+        {reps, cl->dev.reps, M * c.n_layers * dim * c.rows_per_unit * 4}};
+    for (const Part& q : parts) {
+      if (!q.dst) continue;
+      const hipError_t e = hipMemcpyAsync(q.dst, q.src, q.bytes, hipMemcpyDeviceToDevice, hs);
+      if (e != hipSuccess) return fail(SS_ERR_DEVICE, "cluster export: %s", hipGetErrorString(e));
+    }
+    return SS_OK;
+  });
 }
 
 size_t ss_pooled_workspace_bytes(ss_index* const* idx, int32_t n_streams, const int32_t* n_q,
@@ -616,30 +635,32 @@ size_t ss_pooled_workspace_bytes(ss_index* const* idx, int32_t n_streams, const 
 ss_status ss_retrieve_pooled(ss_index* const* idx, int32_t n_streams, const void* const* queries,
                              const int32_t* n_q, int32_t n_select, void* ws, size_t ws_bytes,
                              void* stream, int64_t* frame_ids, float* scores, int32_t* n_out) {
-  ss_status st = check_pooled(idx, n_streams, n_q, n_select);
-  if (st) return st;
-  if (!queries) return fail(SS_ERR_INVALID_ARGUMENT, "queries is NULL");
-  const int L = idx[0]->desc.n_layers;
-  for (int i = 0; i < n_streams * L; ++i) {
-    if (!queries[i]) return fail(SS_ERR_INVALID_ARGUMENT, "queries[%d] is NULL", i);
-    if (!aligned(queries[i], 16)) return fail(SS_ERR_INVALID_ARGUMENT, "queries[%d] not 16-byte aligned", i);
-  }
-  if (!frame_ids || !scores || !n_out) return fail(SS_ERR_INVALID_ARGUMENT, "an output pointer is NULL");
-  if (!ws || !aligned(ws, 256)) return fail(SS_ERR_WORKSPACE, "workspace NULL or not 256-byte aligned");
-  const size_t need = pooled_ws(idx, n_streams, n_q, n_select);
-  if (ws_bytes < need) return fail(SS_ERR_WORKSPACE, "workspace %zu bytes, %zu needed", ws_bytes, need);
-  const hipStream_t hs = static_cast<hipStream_t>(stream);
-  for (int s0 = 0; s0 < n_streams; s0 += ss::kMaxStreams) {
-    ss::PooledPlan p;
-    build_pooled(p, idx, s0, std::min(ss::kMaxStreams, n_streams - s0), queries, n_q, n_select);
-    ss::pooled_workspace(p, ws);
-    p.out_ids = frame_ids + (size_t)s0 * n_select;
-    p.out_scores = scores + (size_t)s0 * n_select;
-    p.out_n = n_out + s0;
-    const hipError_t e = ss::launch_pooled(p, hs);
-    if (e != hipSuccess) return fail(SS_ERR_DEVICE, "pooled ranking launch failed: %s", hipGetErrorString(e));
-  }
-  return SS_OK;
+  return guarded([&]() -> ss_status {
+    ss_status st = check_pooled(idx, n_streams, n_q, n_select);
+    if (st) return st;
+    if (!queries) return fail(SS_ERR_INVALID_ARGUMENT, "queries is NULL");
+    const int L = idx[0]->desc.n_layers;
+    for (int i = 0; i < n_streams * L; ++i) {
+      if (!queries[i]) return fail(SS_ERR_INVALID_ARGUMENT, "queries[%d] is NULL", i);
+      if (!aligned(queries[i], 16)) return fail(SS_ERR_INVALID_ARGUMENT, "queries[%d] not 16-byte aligned", i);
+    }
+    if (!frame_ids || !scores || !n_out) return fail(SS_ERR_INVALID_ARGUMENT, "an output pointer is NULL");
+    if (!ws || !aligned(ws, 256)) return fail(SS_ERR_WORKSPACE, "workspace NULL or not 256-byte aligned");
+    const size_t need = pooled_ws(idx, n_streams, n_q, n_select);
+    if (ws_bytes < need) return fail(SS_ERR_WORKSPACE, "workspace %zu bytes, %zu needed", ws_bytes, need);
+    const hipStream_t hs = static_cast<hipStream_t>(stream);
+    for (int s0 = 0; s0 < n_streams; s0 += ss::kMaxStreams) {
+      ss::PooledPlan p;
+      build_pooled(p, idx, s0, std::min(ss::kMaxStreams, n_streams - s0), queries, n_q, n_select);
+      ss::pooled_workspace(p, ws);
+      p.out_ids = frame_ids + (size_t)s0 * n_select;
+      p.out_scores = scores + (size_t)s0 * n_select;
+      p.out_n = n_out + s0;
+      const hipError_t e = ss::launch_pooled(p, hs);
+      if (e != hipSuccess) return fail(SS_ERR_DEVICE, "pooled ranking launch failed: %s", hipGetErrorString(e));
+    }
+    return SS_OK;
+  });
 }
 
 int32_t ss_evidence_max_units(const ss_evidence_params* params, int32_t n_select) {
@@ -650,39 +671,41 @@ int32_t ss_evidence_max_units(const ss_evidence_params* params, int32_t n_select
 ss_status ss_assemble_evidence(ss_index* const* idx, int32_t n_streams, const int64_t* frame_ids,
                                int32_t n_select, const ss_evidence_params* params, void* stream,
                                int64_t* units, int32_t* n_units, int32_t max_units) {
-  if (!idx) return fail(SS_ERR_INVALID_ARGUMENT, "idx is NULL");
-  if (n_streams < 1) return fail(SS_ERR_INVALID_ARGUMENT, "n_streams must be >= 1");
-  for (int s = 0; s < n_streams; ++s)
-    if (!idx[s]) return fail(SS_ERR_INVALID_ARGUMENT, "idx[%d] is NULL", s);
-  const int64_t need = evidence_units_max(params, n_select);
-  if (need < 0) return fail(SS_ERR_INVALID_ARGUMENT, "invalid evidence parameters");
-  if (need > ss::kMaxEvidence)
-    return fail(SS_ERR_UNSUPPORTED, "%lld candidate units per stream > %d", (long long)need, ss::kMaxEvidence);
-  if (max_units < std::max<int64_t>(need, 1) || max_units > ss::kMaxEvidence)
-    return fail(SS_ERR_INVALID_ARGUMENT, "max_units %d outside %lld..%d", max_units,
-                (long long)std::max<int64_t>(need, 1), ss::kMaxEvidence);
-  if (params->retrieved && !frame_ids) return fail(SS_ERR_INVALID_ARGUMENT, "frame_ids is NULL");
-  if (!units || !n_units) return fail(SS_ERR_INVALID_ARGUMENT, "an output pointer is NULL");
-  if (!aligned(units, 8) || !aligned(n_units, 4) || (frame_ids && !aligned(frame_ids, 8)))
-    return fail(SS_ERR_INVALID_ARGUMENT, "misaligned device pointer");
-  const hipStream_t hs = static_cast<hipStream_t>(stream);
-  for (int s0 = 0; s0 < n_streams; s0 += ss::kMaxStreams) {
-    ss::EvidenceArgs a{};
-    a.S = std::min(ss::kMaxStreams, n_streams - s0);
-    a.n_select = params->retrieved ? n_select : 0;
-    a.n_recent = params->n_recent;
-    a.n_before = params->n_before;
-    a.n_after = params->n_after;
-    a.retrieved = params->retrieved;
-    a.max_units = max_units;
-    for (int s = 0; s < a.S; ++s) a.T[s] = idx[s0 + s]->n_frames;
-    a.frame_ids = params->retrieved ? frame_ids + (size_t)s0 * n_select : nullptr;
-    a.units = units + (size_t)s0 * max_units;
-    a.n_units = n_units + s0;
-    const hipError_t e = ss::launch_evidence(a, hs);
-    if (e != hipSuccess) return fail(SS_ERR_DEVICE, "evidence launch failed: %s", hipGetErrorString(e));
-  }
-  return SS_OK;
+  return guarded([&]() -> ss_status {
+    if (!idx) return fail(SS_ERR_INVALID_ARGUMENT, "idx is NULL");
+    if (n_streams < 1) return fail(SS_ERR_INVALID_ARGUMENT, "n_streams must be >= 1");
+    for (int s = 0; s < n_streams; ++s)
+      if (!idx[s]) return fail(SS_ERR_INVALID_ARGUMENT, "idx[%d] is NULL", s);
+    const int64_t need = evidence_units_max(params, n_select);
+    if (need < 0) return fail(SS_ERR_INVALID_ARGUMENT, "invalid evidence parameters");
+    if (need > ss::kMaxEvidence)
+      return fail(SS_ERR_UNSUPPORTED, "%lld candidate units per stream > %d", (long long)need, ss::kMaxEvidence);
+    if (max_units < std::max<int64_t>(need, 1) || max_units > ss::kMaxEvidence)
+      return fail(SS_ERR_INVALID_ARGUMENT, "max_units %d outside %lld..%d", max_units,
+                  (long long)std::max<int64_t>(need, 1), ss::kMaxEvidence);
+    if (params->retrieved && !frame_ids) return fail(SS_ERR_INVALID_ARGUMENT, "frame_ids is NULL");
+    if (!units || !n_units) return fail(SS_ERR_INVALID_ARGUMENT, "an output pointer is NULL");
+    if (!aligned(units, 8) || !aligned(n_units, 4) || (frame_ids && !aligned(frame_ids, 8)))
+      return fail(SS_ERR_INVALID_ARGUMENT, "misaligned device pointer");
+    const hipStream_t hs = static_cast<hipStream_t>(stream);
+    for (int s0 = 0; s0 < n_streams; s0 += ss::kMaxStreams) {
+      ss::EvidenceArgs a{};
+      a.S = std::min(ss::kMaxStreams, n_streams - s0);
+      a.n_select = params->retrieved ? n_select : 0;
+      a.n_recent = params->n_recent;
+      a.n_before = params->n_before;
+      a.n_after = params->n_after;
+      a.retrieved = params->retrieved;
+      a.max_units = max_units;
+      for (int s = 0; s < a.S; ++s) a.T[s] = idx[s0 + s]->n_frames;
+      a.frame_ids = params->retrieved ? frame_ids + (size_t)s0 * n_select : nullptr;
+      a.units = units + (size_t)s0 * max_units;
+      a.n_units = n_units + s0;
+      const hipError_t e = ss::launch_evidence(a, hs);
+      if (e != hipSuccess) return fail(SS_ERR_DEVICE, "evidence launch failed: %s", hipGetErrorString(e));
+    }
+    return SS_OK;
+  });
 }
 
 size_t ss_index_required_bytes(const ss_index_desc* desc) {
@@ -692,106 +715,118 @@ size_t ss_index_required_bytes(const ss_index_desc* desc) {
 
 ss_status ss_index_create(const ss_index_desc* desc, void* dev_arena, size_t arena_bytes,
                           ss_index** out) {
-  if (!out) return fail(SS_ERR_INVALID_ARGUMENT, "out is NULL");
-  ss_status st = check_desc(desc);
-  if (st) return st;
-  if (!dev_arena) return fail(SS_ERR_INVALID_ARGUMENT, "arena is NULL");
-  if (!aligned(dev_arena, 256)) return fail(SS_ERR_INVALID_ARGUMENT, "arena not 256-byte aligned");
-  const Layout L = layout(*desc);
-  if (arena_bytes < L.total)
-    return fail(SS_ERR_CAPACITY, "arena %zu bytes, %zu needed", arena_bytes, L.total);
-  ss_index* x = new (std::nothrow) ss_index();
-  if (!x) return fail(SS_ERR_INTERNAL, "out of host memory");
-  x->desc = *desc;
-  x->arena = dev_arena;
-  x->arena_bytes = arena_bytes;
-  char* b = static_cast<char*>(dev_arena);
-  x->dev.keys = reinterpret_cast<uint16_t*>(b + L.keys);
-  x->dev.counts = reinterpret_cast<int32_t*>(b + L.counts);
-  x->dev.desc = reinterpret_cast<float*>(b + L.desc);
-  x->dev.pooled = reinterpret_cast<float*>(b + L.pooled);
-  x->dev.stats = reinterpret_cast<uint32_t*>(b + L.stats);
-  x->dev.frame_off = reinterpret_cast<int32_t*>(b + L.off);
-  x->n_frames = 0;
-  x->n_rows = 0;
-  x->off.assign(1, 0);
-  x->rpf = -1;
-  *out = x;
-  return SS_OK;
+  return guarded([&]() -> ss_status {
+    if (!out) return fail(SS_ERR_INVALID_ARGUMENT, "out is NULL");
+    ss_status st = check_desc(desc);
+    if (st) return st;
+    if (!dev_arena) return fail(SS_ERR_INVALID_ARGUMENT, "arena is NULL");
+    if (!aligned(dev_arena, 256)) return fail(SS_ERR_INVALID_ARGUMENT, "arena not 256-byte aligned");
+    const Layout L = layout(*desc);
+    if (arena_bytes < L.total)
+      return fail(SS_ERR_CAPACITY, "arena %zu bytes, %zu needed", arena_bytes, L.total);
+    ss_index* x = new (std::nothrow) ss_index();
+    if (!x) return fail(SS_ERR_INTERNAL, "out of host memory");
+    x->desc = *desc;
+    x->arena = dev_arena;
+    x->arena_bytes = arena_bytes;
+    char* b = static_cast<char*>(dev_arena);
+    x->dev.keys = reinterpret_cast<uint16_t*>(b + L.keys);
+    x->dev.counts = reinterpret_cast<int32_t*>(b + L.counts);
+    x->dev.desc = reinterpret_cast<float*>(b + L.desc);
+    x->dev.pooled = reinterpret_cast<float*>(b + L.pooled);
+    x->dev.stats = reinterpret_cast<uint32_t*>(b + L.stats);
+    x->dev.frame_off = reinterpret_cast<int32_t*>(b + L.off);
+    x->n_frames = 0;
+    x->n_rows = 0;
+    x->off.assign(1, 0);
+    x->rpf = -1;
+    *out = x;
+    return SS_OK;
+  });
 }
 
 ss_status ss_index_destroy(ss_index* idx) {
-  if (!idx) return fail(SS_ERR_INVALID_ARGUMENT, "idx is NULL");
-  delete idx;
-  return SS_OK;
+  return guarded([&]() -> ss_status {
+    if (!idx) return fail(SS_ERR_INVALID_ARGUMENT, "idx is NULL");
+    delete idx;
+    return SS_OK;
+  });
 }
 
 ss_status ss_index_info(const ss_index* idx, int64_t* n_frames, int64_t* n_rows) {
-  if (!idx) return fail(SS_ERR_INVALID_ARGUMENT, "idx is NULL");
-  if (n_frames) *n_frames = idx->n_frames;
-  if (n_rows) *n_rows = idx->n_rows;
-  return SS_OK;
+  return guarded([&]() -> ss_status {
+    if (!idx) return fail(SS_ERR_INVALID_ARGUMENT, "idx is NULL");
+    if (n_frames) *n_frames = idx->n_frames;
+    if (n_rows) *n_rows = idx->n_rows;
+    return SS_OK;
+  });
 }
 
 ss_status ss_index_append(ss_index* idx, const void* const* layer_keys, int32_t n_frames,
                           int32_t n_tokens, const ss_compress* compress, void* stream,
                           int64_t* first_frame_id) {
-  if (!idx) return fail(SS_ERR_INVALID_ARGUMENT, "idx is NULL");
-  const ss_index_desc& d = idx->desc;
-  if (!layer_keys) return fail(SS_ERR_INVALID_ARGUMENT, "layer_keys is NULL");
-  if (n_frames < 1 || n_tokens < 1)
-    return fail(SS_ERR_INVALID_ARGUMENT, "n_frames and n_tokens must be >= 1");
-  if ((int64_t)n_frames * n_tokens > 0x7FFFFFFF)
-    return fail(SS_ERR_UNSUPPORTED, "n_frames * n_tokens exceeds 2^31-1");
-  for (int l = 0; l < d.n_layers; ++l) {
-    if (!layer_keys[l]) return fail(SS_ERR_INVALID_ARGUMENT, "layer_keys[%d] is NULL", l);
-    if (!aligned(layer_keys[l], 16))
-      return fail(SS_ERR_INVALID_ARGUMENT, "layer_keys[%d] not 16-byte aligned", l);
-  }
-  int rpf = n_tokens;
-  if (compress) {
-    if (compress->n_centroids < 1 || compress->n_centroids > ss::kMaxCentroids)
-      return fail(SS_ERR_UNSUPPORTED, "n_centroids %d outside 1..%d", compress->n_centroids,
-                  ss::kMaxCentroids);
-    if (compress->n_iters < 0 || compress->n_iters > 100)
-      return fail(SS_ERR_INVALID_ARGUMENT, "n_iters %d outside 0..100", compress->n_iters);
-    if (n_tokens > ss::kMaxTokensCompress)
-      return fail(SS_ERR_UNSUPPORTED, "compression supports at most %d tokens per frame",
-                  ss::kMaxTokensCompress);
-    rpf = std::min(compress->n_centroids, n_tokens);
-  }
-  if (idx->n_frames + n_frames > d.max_frames)
-    return fail(SS_ERR_CAPACITY, "%lld frames + %d exceeds max_frames %lld", (long long)idx->n_frames,
-                n_frames, (long long)d.max_frames);
-  const int64_t new_rows = (int64_t)n_frames * rpf;
-  if (idx->n_rows + new_rows > d.max_rows)
-    return fail(SS_ERR_CAPACITY, "%lld rows + %lld exceeds max_rows %lld", (long long)idx->n_rows,
-                (long long)new_rows, (long long)d.max_rows);
-  ss::AppendArgs a{};
-  a.L = d.n_layers;
-  a.Hk = d.n_kv_heads;
-  a.D = d.head_dim;
-  a.n_frames = n_frames;
-  a.n_tokens = n_tokens;
-  a.max_rows = d.max_rows;
-  a.row0 = idx->n_rows;
-  a.frame0 = idx->n_frames;
-  a.rows_per_frame = rpf;
-  a.n_centroids = compress ? compress->n_centroids : 0;
-  a.n_iters = compress ? compress->n_iters : 0;
-  for (int l = 0; l < d.n_layers; ++l) a.src[l] = static_cast<const uint16_t*>(layer_keys[l]);
-  a.dst = idx->dev;
-  hipError_t e = hipSuccess;
-  if (idx->n_frames == 0)   // the key-magnitude statistic starts with the first append
-    e = ss::launch_zero32(reinterpret_cast<int32_t*>(idx->dev.stats), 1, static_cast<hipStream_t>(stream));
-  if (e == hipSuccess) e = ss::launch_append(a, compress != nullptr, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(SS_ERR_DEVICE, "append launch failed: %s", hipGetErrorString(e));
-  if (first_frame_id) *first_frame_id = idx->n_frames;
-  for (int f = 1; f <= n_frames; ++f) idx->off.push_back(idx->n_rows + (int64_t)f * rpf);
-  idx->n_frames += n_frames;
-  idx->n_rows += new_rows;
-  idx->rpf = (idx->rpf == -1 || idx->rpf == rpf) ? rpf : 0;
-  return SS_OK;
+  return guarded([&]() -> ss_status {
+    if (!idx) return fail(SS_ERR_INVALID_ARGUMENT, "idx is NULL");
+    const ss_index_desc& d = idx->desc;
+    if (!layer_keys) return fail(SS_ERR_INVALID_ARGUMENT, "layer_keys is NULL");
+    if (n_frames < 1 || n_tokens < 1)
+      return fail(SS_ERR_INVALID_ARGUMENT, "n_frames and n_tokens must be >= 1");
+    if ((int64_t)n_frames * n_tokens > 0x7FFFFFFF)
+      return fail(SS_ERR_UNSUPPORTED, "n_frames * n_tokens exceeds 2^31-1");
+    for (int l = 0; l < d.n_layers; ++l) {
+      if (!layer_keys[l]) return fail(SS_ERR_INVALID_ARGUMENT, "layer_keys[%d] is NULL", l);
+      if (!aligned(layer_keys[l], 16))
+        return fail(SS_ERR_INVALID_ARGUMENT, "layer_keys[%d] not 16-byte aligned", l);
+    }
+    int rpf = n_tokens;
+    if (compress) {
+      if (compress->n_centroids < 1 || compress->n_centroids > ss::kMaxCentroids)
+        return fail(SS_ERR_UNSUPPORTED, "n_centroids %d outside 1..%d", compress->n_centroids,
+                    ss::kMaxCentroids);
+      if (compress->n_iters < 0 || compress->n_iters > 100)
+        return fail(SS_ERR_INVALID_ARGUMENT, "n_iters %d outside 0..100", compress->n_iters);
+      if (n_tokens > ss::kMaxTokensCompress)
+        return fail(SS_ERR_UNSUPPORTED, "compression supports at most %d tokens per frame",
+                    ss::kMaxTokensCompress);
+      rpf = std::min(compress->n_centroids, n_tokens);
+    }
+    if (idx->n_frames + n_frames > d.max_frames)
+      return fail(SS_ERR_CAPACITY, "%lld frames + %d exceeds max_frames %lld", (long long)idx->n_frames,
+                  n_frames, (long long)d.max_frames);
+    const int64_t new_rows = (int64_t)n_frames * rpf;
+    if (idx->n_rows + new_rows > d.max_rows)
+      return fail(SS_ERR_CAPACITY, "%lld rows + %lld exceeds max_rows %lld", (long long)idx->n_rows,
+                  (long long)new_rows, (long long)d.max_rows);
+    // the host offsets are reserved before anything is enqueued, so that the
+    // bookkeeping after the launch cannot fail and leave the index behind the
+    // device state
+    idx->off.reserve(idx->off.size() + (size_t)n_frames);
+    ss::AppendArgs a{};
+    a.L = d.n_layers;
+    a.Hk = d.n_kv_heads;
+    a.D = d.head_dim;
+    a.n_frames = n_frames;
+    a.n_tokens = n_tokens;
+    a.max_rows = d.max_rows;
+    a.row0 = idx->n_rows;
+    a.frame0 = idx->n_frames;
+    a.rows_per_frame = rpf;
+    a.n_centroids = compress ? compress->n_centroids : 0;
+    a.n_iters = compress ? compress->n_iters : 0;
+    for (int l = 0; l < d.n_layers; ++l) a.src[l] = static_cast<const uint16_t*>(layer_keys[l]);
+    a.dst = idx->dev;
+    hipError_t e = hipSuccess;
+    if (idx->n_frames == 0)   // the key-magnitude statistic starts with the first append
+      e = ss::launch_zero32(reinterpret_cast<int32_t*>(idx->dev.stats), 1, static_cast<hipStream_t>(stream));
+    if (e == hipSuccess) e = ss::launch_append(a, compress != nullptr, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(SS_ERR_DEVICE, "append launch failed: %s", hipGetErrorString(e));
+    if (first_frame_id) *first_frame_id = idx->n_frames;
+    for (int f = 1; f <= n_frames; ++f) idx->off.push_back(idx->n_rows + (int64_t)f * rpf);   // reserved
+    idx->n_frames += n_frames;
+    idx->n_rows += new_rows;
+    idx->rpf = (idx->rpf == -1 || idx->rpf == rpf) ? rpf : 0;
+    return SS_OK;
+  });
 }
 
 size_t ss_retrieve_workspace_bytes(ss_index* const* idx, int32_t n_streams, const int32_t* n_q,
@@ -804,17 +839,21 @@ ss_status ss_retrieve(ss_index* const* idx, int32_t n_streams, const void* const
                       const int32_t* n_q, const ss_retrieve_params* params, void* ws,
                       size_t ws_bytes, void* stream, int64_t* frame_ids, int32_t* votes,
                       float* mass, int32_t* n_out) {
-  return retrieve_common(idx, n_streams, queries, n_q, params, ws, ws_bytes, stream, frame_ids,
-                         votes, mass, n_out, nullptr);
+  return guarded([&]() -> ss_status {
+    return retrieve_common(idx, n_streams, queries, n_q, params, ws, ws_bytes, stream, frame_ids,
+                           votes, mass, n_out, nullptr);
+  });
 }
 
 ss_status ss_retrieve_debug(ss_index* const* idx, int32_t n_streams, const void* const* queries,
                             const int32_t* n_q, const ss_retrieve_params* params, void* ws,
                             size_t ws_bytes, void* stream, int64_t* frame_ids, int32_t* votes,
                             float* mass, int32_t* n_out, const ss_debug_out* dbg) {
-  if (!dbg) return fail(SS_ERR_INVALID_ARGUMENT, "dbg is NULL");
-  return retrieve_common(idx, n_streams, queries, n_q, params, ws, ws_bytes, stream, frame_ids,
-                         votes, mass, n_out, dbg);
+  return guarded([&]() -> ss_status {
+    if (!dbg) return fail(SS_ERR_INVALID_ARGUMENT, "dbg is NULL");
+    return retrieve_common(idx, n_streams, queries, n_q, params, ws, ws_bytes, stream, frame_ids,
+                           votes, mass, n_out, dbg);
+  });
 }
 
 size_t ss_debug_scores_workspace_bytes(const ss_index* idx) {
@@ -826,88 +865,110 @@ size_t ss_debug_scores_workspace_bytes(const ss_index* idx) {
 ss_status ss_debug_scores(const ss_index* idx, const void* const* queries, int32_t n_q,
                           int32_t layer, int32_t q_head, int32_t head_mode, int64_t row0,
                           int64_t n_rows, float* out, void* ws, size_t ws_bytes, void* stream) {
-  if (!idx) return fail(SS_ERR_INVALID_ARGUMENT, "idx is NULL");
-  const ss_index_desc& d = idx->desc;
-  if (!queries) return fail(SS_ERR_INVALID_ARGUMENT, "queries is NULL");
-  for (int l = 0; l < d.n_layers; ++l)
-    if (!queries[l] || !aligned(queries[l], 16))
-      return fail(SS_ERR_INVALID_ARGUMENT, "queries[%d] NULL or not 16-byte aligned", l);
-  if (n_q < 1 || n_q > 4096) return fail(SS_ERR_INVALID_ARGUMENT, "n_q %d outside 1..4096", n_q);
-  if (head_mode != 0 && head_mode != 1) return fail(SS_ERR_INVALID_ARGUMENT, "head_mode must be 0 or 1");
-  if (head_mode == 1 && d.n_kv_heads > 8)
-    return fail(SS_ERR_UNSUPPORTED, "head_mode 1 supports at most 8 KV heads");
-  if (layer < 0 || layer >= d.n_layers) return fail(SS_ERR_INVALID_ARGUMENT, "layer out of range");
-  if (head_mode == 0 && (q_head < 0 || q_head >= d.n_q_heads))
-    return fail(SS_ERR_INVALID_ARGUMENT, "q_head out of range");
-  if (row0 < 0 || n_rows < 0 || row0 + n_rows > idx->n_rows)
-    return fail(SS_ERR_INVALID_ARGUMENT, "rows [%lld, %lld) outside the %lld stored rows",
-                (long long)row0, (long long)(row0 + n_rows), (long long)idx->n_rows);
-  if (!out && n_rows > 0) return fail(SS_ERR_INVALID_ARGUMENT, "out is NULL");
-  if (!ws || !aligned(ws, 256) || ws_bytes < ss_debug_scores_workspace_bytes(idx))
-    return fail(SS_ERR_WORKSPACE, "debug-scores workspace too small or misaligned");
-  ss::RetrievePlan p;
-  std::memset(&p, 0, sizeof p);
-  p.S = 1;
-  p.L = d.n_layers;
-  p.Hq = d.n_q_heads;
-  p.Hk = d.n_kv_heads;
-  p.G = p.Hq / p.Hk;
-  p.D = d.head_dim;
-  p.head_mode = head_mode;
-  p.NL = head_mode == 0 ? p.L * p.Hq : p.L;
-  p.ncol = head_mode == 0 ? p.G : 1;
-  p.ngs = head_mode == 0 ? p.Hk : 1;
-  p.chunk_rows = kChunkRows;
-  p.qB = static_cast<uint32_t*>(ws);
-  ss::StreamPlan& sp = p.st[0];
-  sp.keys = idx->dev.keys;
-  sp.row_stride = (int32_t)d.max_rows;
-  sp.nq = n_q;
-  double sc = 1.0 / ((double)n_q * std::sqrt((double)p.D));
-  if (head_mode == 1) sc /= (double)p.Hq;
-  sp.qscale = (float)sc;
-  for (int l = 0; l < p.L; ++l) sp.q[l] = static_cast<const uint16_t*>(queries[l]);
-  const hipError_t e =
-      ss::launch_debug_scores(p, layer, q_head, row0, n_rows, out, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(SS_ERR_DEVICE, "debug scores launch failed: %s", hipGetErrorString(e));
-  return SS_OK;
+  return guarded([&]() -> ss_status {
+    if (!idx) return fail(SS_ERR_INVALID_ARGUMENT, "idx is NULL");
+    const ss_index_desc& d = idx->desc;
+    if (!queries) return fail(SS_ERR_INVALID_ARGUMENT, "queries is NULL");
+    for (int l = 0; l < d.n_layers; ++l)
+      if (!queries[l] || !aligned(queries[l], 16))
+        return fail(SS_ERR_INVALID_ARGUMENT, "queries[%d] NULL or not 16-byte aligned", l);
+    if (n_q < 1 || n_q > 4096) return fail(SS_ERR_INVALID_ARGUMENT, "n_q %d outside 1..4096", n_q);
+    if (head_mode != 0 && head_mode != 1) return fail(SS_ERR_INVALID_ARGUMENT, "head_mode must be 0 or 1");
+    if (head_mode == 1 && d.n_kv_heads > 8)
+      return fail(SS_ERR_UNSUPPORTED, "head_mode 1 supports at most 8 KV heads");
+    if (layer < 0 || layer >= d.n_layers) return fail(SS_ERR_INVALID_ARGUMENT, "layer out of range");
+    if (head_mode == 0 && (q_head < 0 || q_head >= d.n_q_heads))
+      return fail(SS_ERR_INVALID_ARGUMENT, "q_head out of range");
+    if (row0 < 0 || n_rows < 0 || row0 + n_rows > idx->n_rows)
+      return fail(SS_ERR_INVALID_ARGUMENT, "rows [%lld, %lld) outside the %lld stored rows",
+                  (long long)row0, (long long)(row0 + n_rows), (long long)idx->n_rows);
+    if (!out && n_rows > 0) return fail(SS_ERR_INVALID_ARGUMENT, "out is NULL");
+    if (!ws || !aligned(ws, 256) || ws_bytes < ss_debug_scores_workspace_bytes(idx))
+      return fail(SS_ERR_WORKSPACE, "debug-scores workspace too small or misaligned");
+    ss::RetrievePlan p;
+    std::memset(&p, 0, sizeof p);
+    p.S = 1;
+    p.L = d.n_layers;
+    p.Hq = d.n_q_heads;
+    p.Hk = d.n_kv_heads;
+    p.G = p.Hq / p.Hk;
+    p.D = d.head_dim;
+    p.head_mode = head_mode;
+    p.NL = head_mode == 0 ? p.L * p.Hq : p.L;
+    p.ncol = head_mode == 0 ? p.G : 1;
+    p.ngs = head_mode == 0 ? p.Hk : 1;
+    p.chunk_rows = kChunkRows;
+    p.qB = static_cast<uint32_t*>(ws);
+    ss::StreamPlan& sp = p.st[0];
+    sp.keys = idx->dev.keys;
+    sp.row_stride = (int32_t)d.max_rows;
+    sp.nq = n_q;
+    double sc = 1.0 / ((double)n_q * std::sqrt((double)p.D));
+    if (head_mode == 1) sc /= (double)p.Hq;
+    sp.qscale = (float)sc;
+    for (int l = 0; l < p.L; ++l) sp.q[l] = static_cast<const uint16_t*>(queries[l]);
+    const hipError_t e =
+        ss::launch_debug_scores(p, layer, q_head, row0, n_rows, out, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(SS_ERR_DEVICE, "debug scores launch failed: %s", hipGetErrorString(e));
+    return SS_OK;
+  });
 }
 
 ss_status ss_index_export(const ss_index* idx, void* rows_dev, int32_t* counts_dev, float* desc_dev,
                           int64_t* frame_offsets_host, void* stream) {
-  if (!idx) return fail(SS_ERR_INVALID_ARGUMENT, "idx is NULL");
-  const ss_index_desc& d = idx->desc;
-  const hipStream_t hs = static_cast<hipStream_t>(stream);
-  const size_t lg = (size_t)d.n_layers * d.n_kv_heads;
-  if (frame_offsets_host)
-    std::memcpy(frame_offsets_host, idx->off.data(), idx->off.size() * sizeof(int64_t));
-  if (idx->n_rows > 0 && rows_dev) {
-    const size_t rb = (size_t)idx->n_rows * d.head_dim * 2;
-    const hipError_t e = hipMemcpy2DAsync(rows_dev, rb, idx->dev.keys, (size_t)d.max_rows * d.head_dim * 2,
-                                          rb, lg, hipMemcpyDeviceToDevice, hs);
-    if (e != hipSuccess) return fail(SS_ERR_DEVICE, "export rows: %s", hipGetErrorString(e));
-  }
-  if (idx->n_rows > 0 && counts_dev) {
-    const size_t rb = (size_t)idx->n_rows * 4;
-    const hipError_t e = hipMemcpy2DAsync(counts_dev, rb, idx->dev.counts, (size_t)d.max_rows * 4, rb, lg,
+  return guarded([&]() -> ss_status {
+    if (!idx) return fail(SS_ERR_INVALID_ARGUMENT, "idx is NULL");
+    const ss_index_desc& d = idx->desc;
+    const hipStream_t hs = static_cast<hipStream_t>(stream);
+    const size_t lg = (size_t)d.n_layers * d.n_kv_heads;
+    if (frame_offsets_host)
+      std::memcpy(frame_offsets_host, idx->off.data(), idx->off.size() * sizeof(int64_t));
+    if (idx->n_rows > 0 && rows_dev) {
+      const size_t rb = (size_t)idx->n_rows * d.head_dim * 2;
+      const hipError_t e = hipMemcpy2DAsync(rows_dev, rb, idx->dev.keys, (size_t)d.max_rows * d.head_dim * 2,
+                                            rb, lg, hipMemcpyDeviceToDevice, hs);
+      if (e != hipSuccess) return fail(SS_ERR_DEVICE, "export rows: %s", hipGetErrorString(e));
+    }
+    if (idx->n_rows > 0 && counts_dev) {
+      const size_t rb = (size_t)idx->n_rows * 4;
+      const hipError_t e = hipMemcpy2DAsync(counts_dev, rb, idx->dev.counts, (size_t)d.max_rows * 4, rb, lg,
+                                            hipMemcpyDeviceToDevice, hs);
+      if (e != hipSuccess) return fail(SS_ERR_DEVICE, "export counts: %s", hipGetErrorString(e));
+    }
+    if (idx->n_frames > 0 && desc_dev) {
+      const hipError_t e = hipMemcpyAsync(desc_dev, idx->dev.desc,
+                                          (size_t)idx->n_frames * d.n_kv_heads * d.head_dim * 4,
                                           hipMemcpyDeviceToDevice, hs);
-    if (e != hipSuccess) return fail(SS_ERR_DEVICE, "export counts: %s", hipGetErrorString(e));
-  }
-  if (idx->n_frames > 0 && desc_dev) {
-    const hipError_t e = hipMemcpyAsync(desc_dev, idx->dev.desc,
-                                        (size_t)idx->n_frames * d.n_kv_heads * d.head_dim * 4,
-                                        hipMemcpyDeviceToDevice, hs);
-    if (e != hipSuccess) return fail(SS_ERR_DEVICE, "export descriptors: %s", hipGetErrorString(e));
-  }
-  return SS_OK;
+      if (e != hipSuccess) return fail(SS_ERR_DEVICE, "export descriptors: %s", hipGetErrorString(e));
+    }
+    return SS_OK;
+  });
+}
+
+ss_status ss_debug_sample_plan(int64_t n_rows, int32_t top_k, int32_t* out) {
+  return guarded([&]() -> ss_status {
+    if (!out) return fail(SS_ERR_INVALID_ARGUMENT, "out is NULL");
+    if (n_rows < 0 || n_rows > (int64_t)0x7FFFFFFF - 1)
+      return fail(SS_ERR_INVALID_ARGUMENT, "n_rows %lld outside 0..2^31-2", (long long)n_rows);
+    if (top_k < 1 || top_k > ss::kMaxTopK)
+      return fail(SS_ERR_UNSUPPORTED, "top_k %d outside 1..%d", top_k, ss::kMaxTopK);
+    const StreamSizes z = plan_stream(n_rows, 0, top_k);
+    out[0] = z.m;
+    out[1] = z.r;
+    out[2] = (int32_t)candidate_cap(top_k, n_rows);
+    out[3] = z.kk > 0 ? (int32_t)expected_candidates(n_rows, z.kk) : 0;
+    return SS_OK;
+  });
 }
 
 ss_status ss_set_profile_events(void* ev_start, void* ev_stop) {
-  if ((ev_start == nullptr) != (ev_stop == nullptr))
-    return fail(SS_ERR_INVALID_ARGUMENT, "give both events or neither");
-  g_ev_start = static_cast<hipEvent_t>(ev_start);
-  g_ev_stop = static_cast<hipEvent_t>(ev_stop);
-  return SS_OK;
+  return guarded([&]() -> ss_status {
+    if ((ev_start == nullptr) != (ev_stop == nullptr))
+      return fail(SS_ERR_INVALID_ARGUMENT, "give both events or neither");
+    g_ev_start = static_cast<hipEvent_t>(ev_start);
+    g_ev_stop = static_cast<hipEvent_t>(ev_stop);
+    return SS_OK;
+  });
 }
 
 const char* ss_status_string(ss_status s) {
@@ -923,7 +984,7 @@ const char* ss_status_string(ss_status s) {
   }
 }
 
-const char* ss_last_error(void) { return g_err.c_str(); }
+const char* ss_last_error(void) { return g_err; }
 
 int32_t ss_version(void) { return 1; }
 

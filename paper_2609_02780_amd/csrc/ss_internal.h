@@ -85,21 +85,17 @@ struct RetrievePlan {
   int k_max;             // max over streams of kk
   int m_max, f_max;
   int chunk_rows, samp_chunk;
-  int64_t full_total;    // sum over streams of NL * n
   StreamPlan st[kMaxStreams];
 
   // workspace carve (device pointers)
   uint32_t* qB;          // [S][L][H_kv][2][d/32][64] uint4
   uint32_t* tau;         // [S*NL]
   uint32_t* cnt;         // [S*NL]
-  int32_t* flag;         // [S*NL]
   float* samp;           // [S*NL][m_max]
   uint64_t* cand;        // [S*NL][cap]
   float* qcol;           // [S][L][H_kv][16] L1 norms of the scaled query columns
   int32_t* sexp;         // [S] fixed-point exponent of each stream's attention mass
   uint32_t* dyn_ctr;     // chunk counters of the streaming pass
-  float* full;           // fallback scores, per stream base full_base[s]
-  int64_t full_base[kMaxStreams];
   int32_t* votes;        // [S][f_max] per-frame votes
   int64_t* massfx;       // [S][f_max] per-frame mass at scale 2^sexp
   uint64_t* rec_hi;      // [S][f_max] compacted (votes, mass, frame) records

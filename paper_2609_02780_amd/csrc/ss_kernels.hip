@@ -42,6 +42,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <climits>
 #include <cmath>
 #include <cstdint>
@@ -546,8 +547,7 @@ struct ScoreArgs {
   int64_t dyn_tiles;                   // the last tiles, handed out in chunks (0: all static)
   int dyn_chunk;                       // tiles per handed-out chunk
   uint32_t* dyn_ctr;                   // kDynCtr chunk counters, kDynStride words apart
-  // K_FULL
-  const int32_t* flag;                // nullptr: write only `only_list`
+  // K_FULL (parity scores of one list)
   int only_list;
   float* full;
   int64_t full_base[kMaxStreams];
@@ -685,7 +685,7 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a) {
     bool wr = false;
     if (KIND == K_FULL) {
       const int ll = l * a.Hq + g * a.G + col;
-      wr = colv && (a.flag ? (a.flag[list] != 0) : (ll == a.only_list));
+      wr = colv && ll == a.only_list;
       if (!__any(wr)) continue;  // same decision in every wave of the block
     }
     const u32x4* qb = a.qB + ((size_t)(s * a.L + l) * a.Hk + g) * (2 * KS * kWave);
@@ -1128,7 +1128,7 @@ __global__ __launch_bounds__(256) void k_score_hm(ScoreArgs a) {
     const int list = s * a.NL + l;
     bool wr = false;
     if (KIND == K_FULL) {
-      wr = colv && (a.flag ? (a.flag[list] != 0) : (l == a.only_list));
+      wr = colv && l == a.only_list;
       if (!__any(wr)) continue;
     }
     u32x4 b[KS];
@@ -1364,12 +1364,10 @@ struct ListArgs {
   int32_t f[kMaxStreams], rpf[kMaxStreams];
   const int32_t* frame_off[kMaxStreams];   // from the first candidate frame; values are absolute rows
   int64_t row0[kMaxStreams];               // the first candidate row
-  int64_t full_base[kMaxStreams];
   const float* samp;
   int samp_stride;
   uint32_t* tau;
   uint32_t* cnt;
-  int32_t* flag;
   const uint64_t* cand;
   // per-frame votes and fixed-point attention mass of each stream (window-relative frames)
   int f_max;
@@ -1378,8 +1376,7 @@ struct ListArgs {
   int32_t* sexp;       // [S]
   const float* qcol;   // [S][L][H_kv][16] query column L1 norms
   const uint32_t* kmax[kMaxStreams];   // the index's largest |key element| (float bits)
-  // exact fallback: the list's scores are recomputed into `full`
-  float* full;
+  // exact fallback: the list's scores are recomputed from the keys
   int L, Hq, Hk, G, head_mode;
   const uint16_t* keys[kMaxStreams];
   int32_t stride[kMaxStreams];
@@ -1448,10 +1445,7 @@ __device__ __forceinline__ void thresh_list(const ListArgs& a) {
   __shared__ uint32_t mm[32];
   const int list = blockIdx.x, s = list / a.NL, ll = list - s * a.NL;
   const int m = a.m[s], r = a.r[s];
-  if (threadIdx.x == 0) {
-    a.cnt[list] = 0;
-    a.flag[list] = 0;
-  }
+  if (threadIdx.x == 0) a.cnt[list] = 0;
   if (list == 0 && threadIdx.x < kDynCtr) a.dyn_ctr[threadIdx.x * kDynStride] = 0;
   {
     int32_t* vg = a.votes_g + (size_t)s * a.f_max;
@@ -1555,19 +1549,26 @@ __device__ void finish_list(const ListArgs& a, int list, uint64_t* sel, int kk,
   }
 }
 
-// Exact fallback for a list whose candidate count left [k, capacity]: the block
-// recomputes every score of the list (same MFMA arithmetic as the streaming
-// pass) into `full`, then takes the k-th largest by radix selection, rows above
-// it in any order and rows equal to it in row order.
+// Exact fallback for a list whose candidate count left [k, capacity]: the
+// block selects from every score of the list, recomputed in each of its passes
+// with the streaming pass's arithmetic (the same bits), so nothing is stored
+// per row.  A pass scores 1,024 rows at a time (four tiles per wave) into LDS.
+// Three radix rounds of 11, 11 and 10 bits over the ordered scores find the
+// k-th largest value v* (a round whose bin is taken whole ends the search
+// early: every row at or above that bin is selected); a last pass takes the
+// rows above v* and, in row order, the rows equal to it that are still needed.
+constexpr int kFbTilesPerWave = 4;
+constexpr int kFbRows = 16 * kFbTilesPerWave * kTile;   // rows per pass of a 1024-thread block
+
 template <int D>
 __device__ void fallback_list(const ListArgs& a, int list, uint64_t* sel, int32_t* lv, long long* lm,
-                              uint32_t* hist, uint32_t* res) {
+                              uint32_t* res) {
   constexpr int KS = D / 32;
+  __shared__ float chunk[kFbRows];
   __shared__ uint32_t ngt_sh;
   __shared__ int scan_sh[17];
   const int s = list / a.NL, ll = list - s * a.NL;
   const int kk = a.kk[s], n = a.n[s];
-  float* full = a.full + a.full_base[s] + (int64_t)ll * n;
   int l, g0, ng, col;
   if (a.head_mode == 0) {
     l = ll / a.Hq;
@@ -1581,68 +1582,93 @@ __device__ void fallback_list(const ListArgs& a, int list, uint64_t* sel, int32_
     col = 0;
     ng = a.Hk;
   }
-  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
   const int kg = lane >> 4, rl = lane & 15;
   const size_t gstride = (size_t)a.stride[s] * D;
-  const int ntiles = (n + kTile - 1) / kTile;
-  u32x4 bhm[KS];
-  if (a.head_mode == 1) hm_load_b<KS>(a.qB + (size_t)(s * a.L + l) * a.Hk * (2 * KS * kWave), a.Hk, bhm);
-  for (int t = wave; t < ntiles; t += nw) {
-    const int row = t * kTile + rl;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int g = g0; g < g0 + ng; ++g) {
-      const u32x4* qb = a.qB + ((size_t)(s * a.L + l) * a.Hk + g) * (2 * KS * kWave);
-      const uint16_t* p = a.keys[s] + ((size_t)l * a.Hk + g) * gstride + (size_t)(row < n ? row : 0) * D + 8 * kg;
-      u32x4 A[KS];
+  u32x4 bh[KS], bl[KS];
+  if (a.head_mode == 0) {
+    const u32x4* qb = a.qB + ((size_t)(s * a.L + l) * a.Hk + g0) * (2 * KS * kWave);
 #pragma unroll
-      for (int i = 0; i < KS; ++i) A[i] = row < n ? ld_nt(p + 32 * i) : u32x4{0, 0, 0, 0};
-      if (a.head_mode == 0) {
-        u32x4 bh[KS], bl[KS];
-#pragma unroll
-        for (int i = 0; i < KS; ++i) {
-          bh[i] = qb[i * kWave + lane];
-          bl[i] = qb[(KS + i) * kWave + lane];
-        }
-        acc = score_hilo<KS>(A, bh, bl);
-      } else {
-        hm_accumulate<KS>(A, bhm, g, acc);   // acc gathers the per-head results
-      }
+    for (int i = 0; i < KS; ++i) {
+      bh[i] = qb[i * kWave + lane];
+      bl[i] = qb[(KS + i) * kWave + lane];
     }
-    if (a.head_mode == 1) acc = hm_finish(acc);
-    if ((lane & 15) == col) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r = t * kTile + 4 * kg + j;
-        if (r < n) full[r] = acc[j] + 0.0f;
-      }
-    }
+  } else {
+    hm_load_b<KS>(a.qB + (size_t)(s * a.L + l) * a.Hk * (2 * KS * kWave), a.Hk, bh);
   }
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-  __syncthreads();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-  uint32_t ngreater;
-  const uint32_t vstar = radix_select_u32([&](int i) { return ord_u32(full[i]); }, n,
-                                          (uint32_t)kk, hist, res, ngreater);
-  const int need_eq = kk - (int)ngreater;
+  // chunk[r - c0] = score of row r for rows [c0, c0 + kFbRows) below n
+  auto score_chunk = [&](int c0) {
+#pragma unroll
+    for (int q = 0; q < kFbTilesPerWave; ++q) {
+      const int tl = wave * kFbTilesPerWave + q;        // tile of the chunk
+      const int row = c0 + tl * kTile + rl;
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      for (int g = g0; g < g0 + ng; ++g) {
+        const uint16_t* p = a.keys[s] + ((size_t)l * a.Hk + g) * gstride + (size_t)(row < n ? row : 0) * D + 8 * kg;
+        u32x4 A[KS];
+#pragma unroll
+        for (int i = 0; i < KS; ++i) A[i] = row < n ? ld_nt(p + 32 * i) : u32x4{0, 0, 0, 0};
+        if (a.head_mode == 0) acc = score_hilo<KS>(A, bh, bl);
+        else hm_accumulate<KS>(A, bh, g, acc);   // acc gathers the per-head results
+      }
+      if (a.head_mode == 1) acc = hm_finish(acc);
+      if ((lane & 15) == col) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) chunk[tl * kTile + 4 * kg + j] = acc[j] + 0.0f;
+      }
+    }
+  };
+  uint32_t* hist = reinterpret_cast<uint32_t*>(lv);   // 2048 bins; lv is free until finish_list
+  uint32_t prefix = 0, mask = 0, need = (uint32_t)kk;
+  bool whole = false;
+  for (int rd = 0; rd < 3 && !whole; ++rd) {
+    const int shift = rd == 0 ? 21 : rd == 1 ? 10 : 0;
+    const uint32_t nb = rd == 2 ? 1024u : 2048u;
+    for (int i = threadIdx.x; i < 2048; i += blockDim.x) hist[i] = 0;
+    __syncthreads();
+    for (int c0 = 0; c0 < n; c0 += kFbRows) {
+      score_chunk(c0);
+      __syncthreads();
+      const int r = c0 + (int)threadIdx.x;
+      if (r < n) {
+        const uint32_t u = ord_u32(chunk[threadIdx.x]);
+        if ((u & mask) == prefix) atomicAdd(&hist[(u >> shift) & (nb - 1)], 1u);
+      }
+      __syncthreads();
+    }
+    if (nb == 2048u) find_digit_wide<32>(hist, need, res);
+    else find_digit_wide<16>(hist, need, res);
+    const uint32_t b = res[0], above = res[1], inb = res[2];
+    __syncthreads();
+    prefix |= b << shift;
+    mask |= (nb - 1) << shift;
+    need -= above;
+    whole = inb == need;   // the bin is taken whole: every row >= prefix is selected
+  }
+  const uint32_t vstar = prefix;
+  const int need_eq = whole ? 0 : (int)need;
   if (threadIdx.x == 0) ngt_sh = 0;
   __syncthreads();
   int eq_taken = 0;
-  for (int b0 = 0; b0 < n; b0 += blockDim.x) {
-    const int i = b0 + threadIdx.x;
+  for (int c0 = 0; c0 < n; c0 += kFbRows) {
+    score_chunk(c0);
+    __syncthreads();
+    const int r = c0 + (int)threadIdx.x;
     uint32_t u = 0;
     bool gt = false, eq = false;
-    if (i < n) {
-      u = ord_u32(full[i]);
-      gt = u > vstar;
-      eq = u == vstar;
+    if (r < n) {
+      u = ord_u32(chunk[threadIdx.x]);
+      gt = whole ? u >= vstar : u > vstar;
+      eq = !whole && u == vstar;
     }
     if (gt) {
       const uint32_t slot = atomicAdd(&ngt_sh, 1u);
-      if (slot < (uint32_t)kMaxTopK) sel[slot] = mk_key(u, (uint32_t)i);
+      if (slot < (uint32_t)kMaxTopK) sel[slot] = mk_key(u, (uint32_t)r);
     }
     int tot;
+    // ends with a barrier, after every thread has read its chunk entry
     const int pre = block_excl_scan(eq ? 1 : 0, scan_sh, tot);
-    if (eq && eq_taken + pre < need_eq) sel[ngreater + eq_taken + pre] = mk_key(u, (uint32_t)i);
+    if (eq && eq_taken + pre < need_eq) sel[kk - need_eq + eq_taken + pre] = mk_key(u, (uint32_t)r);
     eq_taken += tot;
   }
   __syncthreads();
@@ -1675,8 +1701,7 @@ __device__ void select_list(const ListArgs& a, int list, SelectShared& sh, uint3
     a.dbg_stats[2 * list + 1] = fallback ? 1 : 0;
   }
   if (fallback) {
-    if (threadIdx.x == 0) a.flag[list] = 1;
-    fallback_list<D>(a, list, sel, lv, lm, hist, res);
+    fallback_list<D>(a, list, sel, lv, lm, res);
     return;
   }
   const int n = (int)c;
@@ -3177,8 +3202,6 @@ ScoreArgs make_score_args(const RetrievePlan& p, int kind) {
     a.samp_step[s] = p.st[s].m > 0 ? (int64_t)(((unsigned __int128)p.st[s].n << 32) / (unsigned)p.st[s].m) : 0;
     a.item_base[s] = items;
     items += p.L * p.ngs * cdiv(a.units[s], a.chunk);
-    a.full_base[s] = p.full_base[s];
-    a.full_stride[s] = p.st[s].n;
   }
   a.item_base[p.S] = items;
   a.total_items = items;
@@ -3191,7 +3214,7 @@ ScoreArgs make_score_args(const RetrievePlan& p, int kind) {
   a.tile_base[p.S] = tiles;
   a.samp = p.samp; a.samp_stride = p.m_max;
   a.tau = p.tau; a.cnt = p.cnt; a.cand = p.cand; a.cap = p.cap;
-  a.flag = p.flag; a.only_list = -1; a.full = p.full; a.row0 = 0;
+  a.only_list = -1; a.full = nullptr; a.row0 = 0;
   a.sgroup = kStreamGroupMax;
   a.xcd_weights = 0;
   a.dyn_tiles = 0;
@@ -3208,17 +3231,25 @@ ScoreArgs make_score_args(const RetrievePlan& p, int kind) {
 // from 425.6 us (4 blocks per CU) to 410.4 us on the 1-hour index.
 constexpr int kStreamBlocksPerCU = 2;
 
+// Cached per device (one atomic slot each: concurrent first calls compute the
+// same value, and no call reads a half-written one).
+constexpr int kMaxDevices = 64;
+
 template <int D, bool HM>
 int stream_grid() {
-  static int grid = 0;
+  static std::atomic<int> cache[kMaxDevices];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) dev = 0;
+  std::atomic<int>& slot = cache[dev % kMaxDevices];
+  int grid = slot.load(std::memory_order_relaxed);
   if (grid == 0) {
-    int dev = 0, cus = 256, per_cu = 0;
-    if (hipGetDevice(&dev) == hipSuccess)
-      (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    int cus = 256, per_cu = 0;
+    (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, HM ? k_stream_hm<D> : k_stream<D>, 256, 0) != hipSuccess ||
         per_cu < 1)
       per_cu = 1;
-    grid = std::min(per_cu, kStreamBlocksPerCU) * cus;
+    grid = std::min(per_cu, kStreamBlocksPerCU) * std::max(cus, 1);
+    slot.store(grid, std::memory_order_relaxed);
   }
   return grid;
 }
@@ -3279,13 +3310,12 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   la.NL = p.NL; la.S = p.S; la.cap = p.cap; la.k_max = p.k_max; la.top_k = p.top_k;
   for (int s = 0; s < p.S; ++s) {
     la.m[s] = p.st[s].m; la.r[s] = p.st[s].r; la.kk[s] = p.st[s].kk; la.n[s] = p.st[s].n;
-    la.full_base[s] = p.full_base[s];
     la.f[s] = p.st[s].f; la.rpf[s] = p.st[s].rpf; la.frame_off[s] = p.st[s].frame_off;
     la.row0[s] = p.st[s].row0;
     la.kmax[s] = p.st[s].kmax;
   }
-  la.samp = p.samp; la.samp_stride = p.m_max; la.tau = p.tau; la.cnt = p.cnt; la.flag = p.flag;
-  la.cand = p.cand; la.full = p.full;
+  la.samp = p.samp; la.samp_stride = p.m_max; la.tau = p.tau; la.cnt = p.cnt;
+  la.cand = p.cand;
   la.L = p.L; la.Hq = p.Hq; la.Hk = p.Hk; la.G = p.G; la.head_mode = p.head_mode;
   la.qB = reinterpret_cast<const u32x4*>(p.qB);
   for (int s = 0; s < p.S; ++s) { la.keys[s] = p.st[s].keys; la.stride[s] = p.st[s].row_stride; }
@@ -3402,7 +3432,6 @@ hipError_t debug_scores_impl(RetrievePlan& p, int layer, int q_head, int64_t row
   a.item_base[0] = 0;
   a.item_base[1] = p.L * p.ngs * nch;
   a.total_items = a.item_base[1];
-  a.flag = nullptr;
   a.only_list = p.head_mode == 0 ? layer * p.Hq + q_head : layer;
   a.full = out; a.full_base[0] = -(int64_t)a.only_list * n_rows; a.full_stride[0] = (int32_t)n_rows;
   a.row0 = row0;
@@ -3541,13 +3570,11 @@ size_t carve_workspace(RetrievePlan& p, void* ws) {
   p.qB = static_cast<uint32_t*>(take((size_t)p.S * p.L * p.Hk * 2 * (p.D / 32) * 64 * 16));
   p.tau = static_cast<uint32_t*>(take(lists * 4));
   p.cnt = static_cast<uint32_t*>(take(lists * 4));
-  p.flag = static_cast<int32_t*>(take(lists * 4));
   p.samp = static_cast<float*>(take(lists * (size_t)p.m_max * 4));
   p.cand = static_cast<uint64_t*>(take(lists * (size_t)p.cap * 8));
   p.qcol = static_cast<float*>(take((size_t)p.S * p.L * p.Hk * 16 * 4));
   p.sexp = static_cast<int32_t*>(take((size_t)p.S * 4));
   p.dyn_ctr = static_cast<uint32_t*>(take((size_t)kDynCtr * kDynStride * 4));
-  p.full = static_cast<float*>(take((size_t)p.full_total * 4));
   p.votes = static_cast<int32_t*>(take((size_t)p.S * p.f_max * 4));
   p.massfx = static_cast<int64_t*>(take((size_t)p.S * p.f_max * 8));
   p.rec_hi = static_cast<uint64_t*>(take((size_t)p.S * p.f_max * 8));

@@ -19,6 +19,26 @@ def _stream_handle(stream) -> int:
     return s.cuda_stream
 
 
+def _used_on(stream, *tensors) -> None:
+    """Tell torch's caching allocator that work enqueued on a caller-given
+    stream reads or writes these buffers, so that their memory is not handed
+    out again before that work is done (buffers used on the current stream
+    need nothing)."""
+    if stream is None:
+        return
+    for t in tensors:
+        if t is not None:
+            t.record_stream(stream)
+
+
+def sample_plan(n_rows: int, top_k: int) -> tuple[int, int, int, int]:
+    """The library's sample plan of one list: ``(m, r, capacity, expected)``
+    (see ``ss_debug_sample_plan``)."""
+    out = (C.c_int32 * 4)()
+    L.check(L.lib().ss_debug_sample_plan(n_rows, top_k, out))
+    return tuple(out)
+
+
 def _check_bf16(t: torch.Tensor, shape, what: str) -> int:
     if not isinstance(t, torch.Tensor) or not t.is_cuda:
         raise ValueError(f"{what} must be a device tensor")
@@ -119,6 +139,7 @@ class ShallowIndex:
         L.check(L.lib().ss_debug_scores(self.handle, L.ptr_array(qp), n_q, layer, q_head, head_mode,
                                         row0, n_rows, out.data_ptr(), ws.data_ptr(), wsb,
                                         _stream_handle(stream)))
+        _used_on(stream, ws, out)
         return out[:n_rows]
 
 
@@ -173,6 +194,7 @@ class Retriever:
                                     self._ws.data_ptr(), self._ws.numel(), _stream_handle(stream),
                                     self.frame_ids.data_ptr(), self.votes.data_ptr(), self.mass.data_ptr(),
                                     self.n_out.data_ptr()))
+        _used_on(stream, self._ws)
         return self.frame_ids, self.votes, self.mass, self.n_out
 
     def debug(self, queries, stream=None) -> dict:
@@ -199,6 +221,7 @@ class Retriever:
                                           self._ws.numel(), _stream_handle(stream), self.frame_ids.data_ptr(),
                                           self.votes.data_ptr(), self.mass.data_ptr(), self.n_out.data_ptr(),
                                           C.byref(dbg)))
+        _used_on(stream, self._ws)
         torch.cuda.synchronize(dev)
         out = {k: v.cpu().numpy() for k, v in t.items()}
         out.update(frame_ids=self.frame_ids.cpu().numpy(), votes=self.votes.cpu().numpy(),
@@ -245,6 +268,7 @@ class PooledRanker:
                                            self._ws.data_ptr(), self._ws.numel(), _stream_handle(stream),
                                            self.frame_ids.data_ptr(), self.scores.data_ptr(),
                                            self.n_out.data_ptr()))
+        _used_on(stream, self._ws)
         return self.frame_ids, self.scores, self.n_out
 
 
@@ -286,6 +310,7 @@ class LongClusters:
             self._ws = torch.empty(need, dtype=torch.uint8, device=self.arena.device)
         L.check(L.lib().ss_clusters_absorb(self._h, self.index.handle, frame_hi, self._ws.data_ptr(),
                                            self._ws.numel(), _stream_handle(stream)))
+        _used_on(stream, self._ws)
 
     def retrieve(self, queries, k_clusters: int, stream=None):
         """``queries[l]``: ``[H_q][n_q][d]`` bfloat16 (only the last layer is
@@ -309,6 +334,7 @@ class LongClusters:
                                              self._qws.data_ptr(), self._qws.numel(), _stream_handle(stream),
                                              ids.data_ptr(), sc.data_ptr(), first.data_ptr(), last.data_ptr(),
                                              n_out.data_ptr()))
+        _used_on(stream, self._qws, ids, sc, first, last, n_out)
         return ids, sc, first, last, n_out
 
     def export(self, stream=None) -> dict:
@@ -358,6 +384,7 @@ def assemble_evidence(indices, frame_ids, n_recent: int, n_before: int = 1, n_af
     handles = L.ptr_array([x.handle.value for x in indices])
     L.check(L.lib().ss_assemble_evidence(handles, S, fid, n_select, C.byref(prm), _stream_handle(stream),
                                          units.data_ptr(), n_units.data_ptr(), max_units))
+    _used_on(stream, units, n_units)
     return units, n_units
 
 

@@ -34,7 +34,8 @@ def dev_bf16(a: np.ndarray) -> torch.Tensor:
 
 def score_scale(oidx: O.Index, queries, head_mode: int = 0):
     """Per list, per candidate row: ``(1/sqrt d) sum_e |qbar_e| |K_e|`` (head_mode 0),
-    or the head mean of those magnitudes (head_mode 1)."""
+    or the head mean of those magnitudes (head_mode 1): the scale of the scaled
+    logits' terms."""
     lo, hi = oidx.first_candidate_row(), oidx.candidate_rows()
     N = hi - lo
     qm = O.query_means(queries)
@@ -66,6 +67,8 @@ def check_topk_list(so, dscale, pos, gscore, kk, report, name=""):
                                       float(np.max(err / np.maximum(dscale[pos], 1e-300))))
     # rank order of the GPU list: scores non-increasing, equal scores by row
     assert np.all(np.diff(gscore) <= 0), f"{name}: GPU list not sorted"
+    tied = np.diff(gscore) == 0
+    assert np.all(np.diff(pos)[tied] > 0), f"{name}: equal scores not in row order"
     if kk == 0:
         return np.zeros(0, dtype=np.int64)
     exact = O.topk(so, kk)
@@ -132,8 +135,9 @@ def check_maxmin(pool, desc, K, selected, report):
 
 
 def staged_check(oidx: O.Index, queries, gpu: dict, s: int, top_k: int, n_select: int,
-                 pool_mult: int = 4, head_mode: int = 0, lists=None):
-    """Run stages 2-5 for stream ``s`` of a ``Retriever.debug`` result; returns a report."""
+                 pool_mult: int = 4, head_mode: int = 0):
+    """Run stages 2-5 for stream ``s`` of a ``Retriever.debug`` result; returns a
+    report with the swap and exemption counts."""
     report = {}
     S_or = O.score_lists(oidx, queries, head_mode)
     Dsc = score_scale(oidx, queries, head_mode)
@@ -176,6 +180,7 @@ def staged_check(oidx: O.Index, queries, gpu: dict, s: int, top_k: int, n_select
     np.testing.assert_allclose(gpu["mass"][s, :n_out], gm[sel], rtol=1e-6, atol=1e-6)
     # end to end against the pure oracle
     ids, v, m, n = O.retrieve(oidx, queries, top_k, n_select, pool_mult, head_mode)
+    report["lists"] = NL
     report["end_to_end_equal"] = bool(np.array_equal(ids[:n], sel) and n == n_out)
     clean = not any(report.get(k, 0) for k in ("swaps", "pool_exempt", "pool_differs", "maxmin_exempt"))
     if clean:

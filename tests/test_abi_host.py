@@ -2,6 +2,7 @@
 symbol, and rejects invalid calls before touching the device.  No GPU: every
 call here fails validation (or is a pure host query) and enqueues nothing."""
 import ctypes as C
+import math
 import os
 import re
 
@@ -242,3 +243,57 @@ def test_clusters_validation(L):
     assert lib.ss_clusters_create(C.byref(ok), FAKE + 8, n, None, C.byref(h)) == L.SS_ERR_INVALID_ARGUMENT
     assert lib.ss_clusters_absorb_workspace_bytes(10) >= 80
     assert lib.ss_clusters_absorb_workspace_bytes(-1) == 0
+
+
+def _poisson_tail(lam, r):
+    """P(X >= r) for X ~ Poisson(lam), summed from the terms upward."""
+    if lam <= 0:
+        return 1.0 if r <= 0 else 0.0
+    term = math.exp(-lam + r * math.log(lam) - math.lgamma(r + 1))
+    tot, i = 0.0, r
+    while term > 1e-300 and i < r + 4000:
+        tot += term
+        term *= lam / (i + 1)
+        i += 1
+    return tot
+
+
+def _poisson_cdf(lam, r):
+    """P(X <= r) for X ~ Poisson(lam)."""
+    return sum(math.exp(-lam + i * math.log(lam) - math.lgamma(i + 1)) for i in range(r + 1)) if r >= 0 else 0.0
+
+
+def test_sample_plan(L):
+    """The streaming cut-off's sample plan (a host query, no GPU): small lists
+    are sampled whole with r = k; otherwise the plan keeps both ways into the
+    exact fallback (too few candidates, more than the capacity) at odds of at
+    most 2e-7 per list, with the smallest rank that does so."""
+    lib = L.lib()
+    out = (C.c_int32 * 4)()
+    assert lib.ss_debug_sample_plan(100, 8, None) == L.SS_ERR_INVALID_ARGUMENT
+    assert lib.ss_debug_sample_plan(-1, 8, out) == L.SS_ERR_INVALID_ARGUMENT
+    assert lib.ss_debug_sample_plan(100, 0, out) == L.SS_ERR_UNSUPPORTED
+    assert lib.ss_debug_sample_plan(100, 2049, out) == L.SS_ERR_UNSUPPORTED
+    for n, k in [(0, 8), (1, 8), (1000, 32), (4096, 512), (4096, 5000 // 3)]:
+        assert lib.ss_debug_sample_plan(n, k, out) == 0
+        m, r, cap, E = out
+        assert m == n and r == min(k, n) and cap >= 4096
+    for n, k in [(117600, 256), (705600, 512), (705600, 64), (19200, 64), (24000, 2048), (8388606, 2048),
+                 (5000, 1), (200000, 1)]:
+        assert lib.ss_debug_sample_plan(n, k, out) == 0
+        m, r, cap, E = out
+        kk = min(k, n)
+        if m == n:
+            assert r == kk
+            continue
+        assert 1 <= r <= min(kk, 32) and r <= m < n
+        assert m == max(r, -(-n * r // E)) and E >= 6 * kk and cap >= 3 * E
+        assert m <= 16384
+        if r < min(kk, 32):
+            assert _poisson_tail(r * kk / E, r) <= 2e-7 * (1 + 1e-9)
+            assert _poisson_cdf(3.0 * r, r - 1) <= 2e-7 * (1 + 1e-9)
+        if r > 1:
+            worse = _poisson_tail((r - 1) * kk / E, r - 1) > 2e-7 or _poisson_cdf(3.0 * (r - 1), r - 2) > 2e-7
+            assert worse, (n, k, r)
+    lib.ss_debug_sample_plan(705600, 512, out)
+    assert tuple(out)[:2] == (3216, 14)       # the 1-hour index: 3,216 sampled rows, rank 14

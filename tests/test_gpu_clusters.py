@@ -115,9 +115,13 @@ def test_clusters_streaming_against_oracle(seed, tau, max_clusters, compress):
             else:
                 o.first_detail = hi
     if compress is not None:
-        # the oracle's own k-means is not the object here: use the stored rows
+        # the oracle's own k-means is not the object here: the stored centroid
+        # rows are the GPU's (k-means parity is audited elsewhere); the
+        # descriptors, which drive every joining decision, are the oracle's own
+        # from the raw last-layer keys
         ex = g.export()
-        o.append_stored([ex["rows"][l] for l in range(L)], [R] * F, list(ex["desc"]))
+        desc = [O.descriptor(O.decode_bf16(keys[L - 1][:, f * T:(f + 1) * T, :])) for f in range(F)]
+        o.append_stored([ex["rows"][l] for l in range(L)], [R] * F, desc)
         o.first_detail = 0
         ocl = O.LongClusters(tau, max_clusters)
         ocl.absorb(o, F - nr - keep)

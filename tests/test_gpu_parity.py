@@ -195,38 +195,6 @@ def test_fallback_too_many_candidates():
     assert rep["end_to_end_equal"]
 
 
-def _poisson_tail(lam, r):
-    """P(X >= r), X ~ Poisson(lam)."""
-    term = math.exp(-lam + r * math.log(lam) - math.lgamma(r + 1))
-    tot, i = 0.0, r
-    while term > 1e-300 and i < r + 2000:
-        tot += term
-        term *= lam / (i + 1)
-        i += 1
-    return tot
-
-
-def _poisson_cdf(lam, r):
-    """P(X <= r), X ~ Poisson(lam)."""
-    term, tot = math.exp(-lam), 0.0
-    for i in range(r + 1):
-        tot += term
-        term *= lam / (i + 1)
-    return min(tot, 1.0)
-
-
-def _sample_plan(n, k):
-    """The library's sample plan of one list of n rows (rank r, expected
-    candidates E, sampled rows m), mirrored here to plant scores on its lattice."""
-    E = max(6 * k, 1024, -(-n * min(k, 32) // 16384))
-    r = min(k, 32)
-    for rr in range(1, min(k, 32)):
-        if _poisson_tail(rr * k / E, rr) <= 2e-7 and _poisson_cdf(3.0 * rr, rr - 1) <= 2e-7:
-            r = rr
-            break
-    return r, E, max(r, -(-n * r // E))
-
-
 def test_fallback_too_few_candidates():
     """Rows on the sample lattice score highest, so the sample cut-off keeps fewer
     than k rows; the exact fallback must take over and match the oracle."""
@@ -234,8 +202,9 @@ def test_fallback_too_few_candidates():
     L, Hq, Hk, d, T, F = 1, 1, 1, 64, 100, 1000
     n = F * T
     k = 512
-    r, E, m = _sample_plan(n, k)
-    step = (n << 32) // m                     # the library's sample lattice, 32.32 fixed point
+    m, r, cap, E = P.sample_plan(n, k)        # the library's own plan of this list
+    assert m < n
+    step = (n << 32) // m                     # the documented sample lattice, 32.32 fixed point
     rows = (np.arange(m, dtype=np.uint64) * np.uint64(step) + np.uint64(step >> 1)) >> np.uint64(32)
     rows = rows.astype(np.int64)
     rng = np.random.default_rng(11)
@@ -249,9 +218,7 @@ def test_fallback_too_few_candidates():
     spec = W.stream_specs(cfg)[0]
     gidx, oidx = make_pair(cfg, spec, keys)
     out = debug_run([gidx], [q], k, 4)
-    assert out["list_stats"][0, 0, 1] == 1, (
-        "no fallback: the planted rows no longer sit on the library's sample lattice; "
-        "_sample_plan must mirror expected_candidates and sample_rank in ss_api.cpp")
+    assert out["list_stats"][0, 0, 1] == 1, "no fallback: the planted rows are not the library's sample"
     rep = staged_check(oidx, q, out, 0, k, 4)
     log(rep)
     assert rep.get("swaps", 0) == 0
@@ -362,6 +329,67 @@ def test_pool_cut_many_ties():
     log(rep)
 
 
+def test_long_stream_global_paths():
+    """A 6,000-frame stream with k = 2048 per list: more than 4,096 frames, so
+    the selection adds votes and mass with global atomics; more than 4,096
+    voted frames, so the pool keeps its records in global memory and cuts them
+    by the 128-bit radix selection; and about 12,000 candidates per list on
+    average, above the 8,192 that the selection holds in registers, so lists
+    select by radix over their candidates in global memory.  Staged against
+    the oracle."""
+    cfg = W.Config("long", 2, 8, 2, 64, 4, 3, 2048, 16, n_frames=6000, n_planted=4)
+    spec = W.stream_specs(cfg)[0]
+    q, keys = W.make_stream(cfg, spec)
+    g, o = make_pair(cfg, spec, keys)
+    out = debug_run([g], [q], cfg.top_k, cfg.n_select)
+    stats = out["list_stats"][0]
+    voted = int(np.count_nonzero(out["vote_hist"][0, :spec.n_frames]))
+    log("long stream: candidates per list", stats[:, 0].min(), stats[:, 0].max(), "fallbacks",
+        stats[:, 1].sum(), "voted frames", voted)
+    assert stats[:, 0].max() > 8192 and stats[:, 1].sum() == 0
+    assert voted > 4096
+    rep = staged_check(o, q, out, 0, cfg.top_k, cfg.n_select)
+    log("long stream", rep)
+
+
+def test_group_of_16_query_heads():
+    """G = 16 query heads per KV head (the largest group: 16 MFMA columns for
+    the hi chain and 16 for the lo chain), d = 64 and d = 128."""
+    for d in (64, 128):
+        cfg = W.Config(f"g16-{d}", 2, 16, 1, d, 16, 5, 40, 6, n_frames=150, n_planted=2)
+        spec = W.stream_specs(cfg)[0]
+        q, keys = W.make_stream(cfg, spec)
+        g, o = make_pair(cfg, spec, keys)
+        worst = _all_row_scores(g, o, q, [(l, h) for l in range(2) for h in range(16)])
+        log(f"G=16 d={d}: max |err|/D", worst)
+        assert worst < 1e-5
+        out = debug_run([g], [q], cfg.top_k, cfg.n_select)
+        rep = staged_check(o, q, out, 0, cfg.top_k, cfg.n_select)
+        log(f"G=16 d={d}", rep)
+        out1 = debug_run([g], [q], cfg.top_k, cfg.n_select, head_mode=1)
+        rep1 = staged_check(o, q, out1, 0, cfg.top_k, cfg.n_select, head_mode=1)
+        log(f"G=16 d={d} head mode 1", rep1)
+
+
+def test_more_streams_than_one_launch():
+    """40 streams in one call: the host runs them as a group of 32 and a group
+    of 8 over one workspace; every stream staged against the oracle."""
+    gidxs, oidxs, qs = [], [], []
+    for s in range(40):
+        F = 20 + (7 * s) % 23
+        cfg = W.Config("many", 2, 4, 2, 64, 8, 2 + s % 3, 12, 3, n_frames=F, n_planted=1)
+        spec = W.stream_specs(cfg)[0]
+        q, keys = W.make_stream(cfg, spec, seed=300 + s)
+        g, o = make_pair(cfg, spec, keys)
+        gidxs.append(g)
+        oidxs.append(o)
+        qs.append(q)
+    out = debug_run(gidxs, qs, 12, 3)
+    for s in range(40):
+        staged_check(oidxs[s], qs[s], out, s, 12, 3)
+    log("40 streams staged")
+
+
 def test_deterministic_repeat():
     cfg, spec, q, keys = c1()
     gidx, _ = make_pair(cfg, spec, keys)
@@ -406,28 +434,50 @@ def test_capacity_error_leaves_index_unchanged():
 KMEANS_MARGIN = 1e-5
 
 
+KMEANS_SSE_BAND = 0.02
+
+
+def _nearest_sse(X, C):
+    """Sum over tokens of the squared distance to the nearest centre (float64)."""
+    d2 = ((X[:, None, :] - C[None, :, :]) ** 2).sum(axis=2)
+    return float(d2.min(axis=1).sum())
+
+
 def _kmeans_audit(ex, keys, cfg, frames, n_c, n_it):
     """Where every farthest-point and assignment decision of the oracle has a
     relative margin of at least KMEANS_MARGIN (about ten times the relative error
     of a 128-term fp32 squared distance), the GPU's bf16 centroids are within one
-    bf16 unit of the oracle's and the member counts are equal."""
+    bf16 unit of the oracle's and the member counts are equal.  The other
+    problems, where an fp32 near-tie may legitimately flip a decision, are
+    checked by tolerance: their counts add up to the tokens, and the tokens'
+    squared distance to their nearest stored centroid (the clustering's SSE)
+    is within KMEANS_SSE_BAND of the same figure for the oracle's centroids.
+    Returns (checked, exempt, largest relative SSE gap over all problems)."""
     T, d = cfg.tokens_per_frame, cfg.head_dim
     checked = exempt = 0
+    sse_gap = 0.0
     for f in frames:
         for l in range(cfg.n_layers):
             for g in range(cfg.n_kv_heads):
                 X = O.decode_bf16(keys[l][g, f * T:(f + 1) * T, :])
                 C, cnt, dg = O.kmeans(X, n_c, n_it)
+                got = ex["rows"][l, g, f * n_c:(f + 1) * n_c, :]
+                got_cnt = ex["counts"][l, g, f * n_c:(f + 1) * n_c]
+                want = O.round_bf16(C)
+                s_gpu = _nearest_sse(X, O.decode_bf16(got))
+                s_ora = _nearest_sse(X, O.decode_bf16(want))
+                gap = abs(s_gpu - s_ora) / max(s_ora, 1e-300)
+                sse_gap = max(sse_gap, gap)
                 if min(dg["init_margin"], dg["assign_margin"]) < KMEANS_MARGIN:
                     exempt += 1
+                    assert int(got_cnt.sum()) == T and np.all(got_cnt >= 0), (f, l, g)
+                    assert gap <= KMEANS_SSE_BAND, (f, l, g, gap)
                     continue
-                want = O.round_bf16(C)
-                got = ex["rows"][l, g, f * n_c:(f + 1) * n_c, :]
                 diff = np.abs(got.astype(np.int32) - want.astype(np.int32))
                 assert diff.max() <= 1, (f, l, g)
-                np.testing.assert_array_equal(ex["counts"][l, g, f * n_c:(f + 1) * n_c], cnt)
+                np.testing.assert_array_equal(got_cnt, cnt)
                 checked += 1
-    return checked, exempt
+    return checked, exempt, sse_gap
 
 
 def test_compression_small_exact_cases():
@@ -486,9 +536,9 @@ def test_compression_c3_shape_audit_and_retrieval():
     log("C3-shape compressed append")
     gidx, _ = make_pair(cfg, spec, keys, compress=(32, 10))
     ex = gidx.export()
-    checked, exempt = _kmeans_audit(ex, keys, cfg, range(60), 32, 10)
-    log("k-means audit", checked, "checked", exempt, "exempt")
-    assert checked >= 0.5 * (checked + exempt)     # most problems have clear decisions
+    checked, exempt, gap = _kmeans_audit(ex, keys, cfg, range(60), 32, 10)
+    log("k-means audit", checked, "checked exactly,", exempt, "by tolerance; largest relative SSE gap", gap)
+    assert checked >= 0.9 * (checked + exempt)
     oidx = O.Index(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim)
     desc = [O.descriptor(O.decode_bf16(keys[-1][:, f * 196:(f + 1) * 196, :])) for f in range(60)]
     oidx.append_stored([ex["rows"][l] for l in range(cfg.n_layers)], [32] * 60, desc)
@@ -521,7 +571,42 @@ def _build_big(cfg, spec, q, block=600, compress=None):
     return gidx, keys
 
 
+def _all_row_scores(gidx, oidx, q, lists, head_mode=0):
+    """Per-key scores of every row of the given lists (layer, query head)
+    against the oracle's: within 1e-3 D each, and the largest |err|/D."""
+    qd = [dev_bf16(x) for x in q]
+    S = O.score_lists(oidx, q, head_mode)
+    D = score_scale(oidx, q, head_mode)
+    Hq = oidx.Hq if head_mode == 0 else 1
+    worst = 0.0
+    for l, h in lists:
+        g = gidx.debug_scores(qd, l, h, head_mode=head_mode).cpu().numpy().astype(np.float64)
+        j = l * Hq + (h if head_mode == 0 else 0)
+        assert g.shape == S[j].shape
+        err = np.abs(g - S[j])
+        assert np.all(err <= 1e-3 * D[j]), (l, h)
+        worst = max(worst, float(np.max(err / D[j])))
+    return worst
+
+
+def _planted_checks(out, s, spec, F):
+    planted = set(spec.planted)
+    ranked = O.vote_pool(out["vote_hist"][s, :F].astype(np.int64), out["mass_hist"][s, :F].astype(np.float64), F)
+    assert set(ranked[:len(planted)].tolist()) == planted            # P1
+    assert out["frame_ids"][s, 0] in planted                          # P2
+
+
+def _tally(total, rep):
+    for k in ("swaps", "lists_with_swaps", "pool_exempt", "pool_differs", "maxmin_exempt"):
+        total[k] = total.get(k, 0) + rep.get(k, 0)
+    total["end_to_end_equal"] = total.get("end_to_end_equal", 0) + int(rep["end_to_end_equal"])
+    total["max_rel_score_err"] = max(total.get("max_rel_score_err", 0.0), rep.get("max_rel_score_err", 0.0))
+
+
 def test_c2_full_staged():
+    """The 10-minute workload: staged in full, the planted evidence (P1-P3), and
+    the per-key scores of every row of every list of layers 0 and 3 (all four
+    KV-head groups, G = 7) and of every head-mean list."""
     cfg = W.CONFIGS["C2"]
     spec = W.stream_specs(cfg)[0]
     q = W.make_queries(cfg, 0, 0)
@@ -533,20 +618,46 @@ def test_c2_full_staged():
     log("C2 list stats: max candidates", out["list_stats"][0, :, 0].max(), "fallbacks",
         out["list_stats"][0, :, 1].sum())
     rep = staged_check(oidx, q, out, 0, cfg.top_k, cfg.n_select)
-    log(rep)
+    log("C2", rep)
     assert out["list_stats"][0, :, 1].sum() == 0
-    planted = set(spec.planted)
-    ranked = O.vote_pool(out["vote_hist"][0, :600].astype(np.int64), out["mass_hist"][0, :600].astype(np.float64), 600)
-    assert set(ranked[:len(planted)].tolist()) == planted            # P1
-    assert out["frame_ids"][0, 0] in planted                          # P2
+    _planted_checks(out, 0, spec, spec.n_frames)
     out1 = debug_run([gidx], [q], cfg.top_k, cfg.n_select, pool_mult=1)
-    assert planted <= set(out1["frame_ids"][0].tolist())              # P3
+    assert set(spec.planted) <= set(out1["frame_ids"][0].tolist())   # P3
+    worst = _all_row_scores(gidx, oidx, q, [(l, h) for l in (0, 3) for h in range(cfg.n_q_heads)])
+    log("C2 all rows, layers 0 and 3, every query head: max |err|/D", worst)
+    assert worst < 1e-5
+    worst1 = _all_row_scores(gidx, oidx, q, [(l, 0) for l in range(cfg.n_layers)], head_mode=1)
+    log("C2 all rows, head-mean lists of every layer: max |err|/D", worst1)
+    assert worst1 < 1e-5
 
 
-def test_c4_full_size_sampled():
+def test_scores_all_rows_group_of_8():
+    """The 16-stream workload's head shape (6 layers, 16 query / 2 KV heads,
+    G = 8: the whole 16-column MFMA tile) at 400 frames: every row of every
+    list of layers 0 and 5, and every head-mean list."""
+    base = W.CONFIGS["C5"]
+    cfg = W.Config("C5-shape", base.n_layers, base.n_q_heads, base.n_kv_heads, base.head_dim, 196, base.n_q,
+                   base.top_k, base.n_select, n_frames=400, n_planted=3)
+    spec = W.stream_specs(cfg)[0]
+    q, keys = W.make_stream(cfg, spec)
+    gidx, oidx = make_pair(cfg, spec, keys)
+    worst = _all_row_scores(gidx, oidx, q, [(l, h) for l in (0, 5) for h in range(cfg.n_q_heads)])
+    log("G=8 all rows, layers 0 and 5, every query head: max |err|/D", worst)
+    assert worst < 1e-5
+    worst1 = _all_row_scores(gidx, oidx, q, [(l, 0) for l in range(cfg.n_layers)], head_mode=1)
+    log("G=8 all rows, head-mean lists: max |err|/D", worst1)
+    assert worst1 < 1e-5
+    out = debug_run([gidx], [q], cfg.top_k, cfg.n_select)
+    rep = staged_check(oidx, q, out, 0, cfg.top_k, cfg.n_select)
+    log("G=8 staged", rep)
+
+
+def test_c4_full_size_staged():
     """The 1-hour index at full size, in the launch configuration the benchmark
-    times: sampled lists checked against the oracle in full, every list by
-    properties, and the planted evidence."""
+    times: every one of the 112 lists staged against the oracle (the scores of
+    the selected rows, a tolerance-valid top-k, votes exactly, mass against the
+    oracle's scores, pool and max-min), the frame ids end to end against the
+    pure oracle, and the planted evidence."""
     cfg = W.CONFIGS["C4"]
     spec = W.stream_specs(cfg)[0]
     q = W.make_queries(cfg, 0, 0)
@@ -563,53 +674,21 @@ def test_c4_full_size_sampled():
     stats = out["list_stats"][0]
     log("C4 candidates per list: min", stats[:, 0].min(), "max", stats[:, 0].max(), "fallbacks", stats[:, 1].sum())
     assert stats[:, 1].sum() == 0
-    NL = cfg.n_layers * cfg.n_q_heads
-    assert out["vote_hist"][0].sum() == NL * cfg.top_k
     oidx = O.Index(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim)
     oidx.append(keys, spec.n_frames, cfg.tokens_per_frame)
     del keys
-    rep = {}
-    from parity import check_topk_list, check_pool, check_maxmin
-    N = oidx.candidate_rows()
-    qm = O.query_means(q)
-    for (l, h) in [(0, 0), (1, 9), (2, 17), (3, 27)]:
-        g = h // cfg.group
-        K = O.decode_bf16(oidx.rows(l)[g])
-        so = K @ qm[l][h] / math.sqrt(cfg.head_dim)
-        dsc = np.abs(K) @ np.abs(qm[l][h]) / math.sqrt(cfg.head_dim)
-        j = l * cfg.n_q_heads + h
-        check_topk_list(so, dsc, out["topk_pos"][0, j].astype(np.int64),
-                        out["topk_score"][0, j].astype(np.float64), cfg.top_k, rep, name=f"C4 list {j}")
-        del K
-    # votes from the GPU lists by the oracle's rule
-    lists = [out["topk_pos"][0, j].astype(np.int64) for j in range(NL)]
-    f_of = oidx.frame_of_row()
-    v_re = np.zeros(spec.n_frames, dtype=np.int64)
-    for p in lists:
-        np.add.at(v_re, f_of[p], 1)
-    assert np.array_equal(out["vote_hist"][0, :spec.n_frames], v_re)
-    gm = out["mass_hist"][0, :spec.n_frames].astype(np.float64)
-    m_re = np.zeros(spec.n_frames)
-    for j, p in enumerate(lists):
-        np.add.at(m_re, f_of[p], out["topk_score"][0, j].astype(np.float64))
-    np.testing.assert_allclose(gm, m_re, rtol=1e-5, atol=1e-5)
-    pn = int(out["pool_n"][0])
-    pool = out["pool"][0, :pn].astype(np.int64)
-    check_pool(pool, v_re, gm, 1e-5 * np.abs(m_re) + 1e-5, 4 * cfg.n_select, rep)
-    check_maxmin(pool, np.array(oidx.desc), cfg.n_select, out["frame_ids"][0, :int(out["n_out"][0])].astype(np.int64), rep)
-    log(rep)
-    planted = set(spec.planted)
-    assert out["frame_ids"][0, 0] in planted
-    ranked = O.vote_pool(v_re, gm, spec.n_frames)
-    assert set(ranked[:len(planted)].tolist()) == planted
+    log("C4 oracle, 112 lists")
+    rep = staged_check(oidx, q, out, 0, cfg.top_k, cfg.n_select)
+    log("C4", rep)
+    assert rep["lists"] == cfg.n_layers * cfg.n_q_heads
+    _planted_checks(out, 0, spec, spec.n_frames)
 
 
-def test_p4_paper_settings_full_size_sampled():
+def test_p4_paper_settings_full_size_staged():
     """The paper's own selection settings (one query token, head-averaged lists,
-    top 64 per layer, pool 32, 8 units) on the 1-hour stream at full size, in the
-    benchmark's launch configuration: two of the four layer lists checked
-    against the oracle in full, votes and mass from the GPU lists, pool and
-    max-min validity, and the planted evidence."""
+    top 64 per layer, pool 32, 8 units) on the 1-hour stream at full size, in
+    the benchmark's launch configuration: all four layer lists staged against
+    the oracle, the frame ids end to end, and the planted evidence."""
     cfg = W.CONFIGS["P4"]
     spec = W.stream_specs(cfg)[0]
     q = W.make_queries(cfg, 0, 0)
@@ -626,74 +705,36 @@ def test_p4_paper_settings_full_size_sampled():
     stats = out["list_stats"][0]
     log("P4 candidates per list", stats[:, 0].tolist(), "fallbacks", stats[:, 1].sum())
     assert stats[:, 1].sum() == 0
-    assert out["vote_hist"][0].sum() == cfg.n_layers * cfg.top_k
     oidx = O.Index(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim)
     oidx.append(keys, spec.n_frames, cfg.tokens_per_frame)
     del keys
-    rep = {}
-    from parity import check_topk_list, check_pool, check_maxmin
-    qm = O.query_means(q)
-    G = cfg.group
-    for l in (0, 3):
-        so = np.zeros(oidx.candidate_rows())
-        dsc = np.zeros_like(so)
-        for g in range(cfg.n_kv_heads):
-            K = O.decode_bf16(oidx.rows(l)[g])
-            w = qm[l][g * G:(g + 1) * G].sum(axis=0)
-            wa = np.abs(qm[l][g * G:(g + 1) * G]).sum(axis=0)
-            so += K @ w
-            dsc += np.abs(K) @ wa
-            del K
-        so /= cfg.n_q_heads * math.sqrt(cfg.head_dim)
-        dsc /= cfg.n_q_heads * math.sqrt(cfg.head_dim)
-        check_topk_list(so, dsc, out["topk_pos"][0, l].astype(np.int64),
-                        out["topk_score"][0, l].astype(np.float64), cfg.top_k, rep, name=f"P4 layer {l}")
-    lists = [out["topk_pos"][0, j].astype(np.int64) for j in range(cfg.n_layers)]
-    f_of = oidx.frame_of_row()
-    v_re = np.zeros(spec.n_frames, dtype=np.int64)
-    for p in lists:
-        np.add.at(v_re, f_of[p], 1)
-    assert np.array_equal(out["vote_hist"][0, :spec.n_frames], v_re)
-    gm = out["mass_hist"][0, :spec.n_frames].astype(np.float64)
-    m_re = np.zeros(spec.n_frames)
-    for j, p in enumerate(lists):
-        np.add.at(m_re, f_of[p], out["topk_score"][0, j].astype(np.float64))
-    np.testing.assert_allclose(gm, m_re, rtol=1e-5, atol=1e-5)
-    pn = int(out["pool_n"][0])
-    pool = out["pool"][0, :pn].astype(np.int64)
-    check_pool(pool, v_re, gm, 1e-5 * np.abs(m_re) + 1e-5, cfg.pool_mult * cfg.n_select, rep)
-    check_maxmin(pool, np.array(oidx.desc), cfg.n_select, out["frame_ids"][0, :int(out["n_out"][0])].astype(np.int64), rep)
-    log(rep)
+    log("P4 oracle, 4 layer lists")
+    rep = staged_check(oidx, q, out, 0, cfg.top_k, cfg.n_select, cfg.pool_mult, head_mode=1)
+    log("P4", rep)
+    assert rep["lists"] == cfg.n_layers
     assert out["frame_ids"][0, 0] in set(spec.planted)
 
 
-def test_c5_full_size_sampled():
+def test_c5_full_size_staged():
     """The 16-stream ragged batch at full size (odd streams compressed to 32
-    centroids) in one call, the benchmark's launch configuration: per stream
-    the vote total and the planted evidence; streams 0 (raw) and 1 (compressed,
-    oracle on the stored centroids) in depth: two lists against the oracle,
-    votes and mass from the GPU lists, pool and max-min validity."""
+    centroids) in one call, the benchmark's launch configuration: every stream
+    staged against the oracle in full (compressed streams on the GPU's stored
+    centroids with the oracle's own descriptors from the raw keys), frame ids
+    end to end, and the planted evidence."""
     cfg = W.CONFIGS["C5"]
     specs = W.stream_specs(cfg)
     P = _P()
-    from parity import check_topk_list, check_pool, check_maxmin
-    gidxs, qs, host = [], [], {}
+    gidxs, qs = [], []
     for sp in specs:
         q = W.make_queries(cfg, 0, sp.stream)
         rpf = 196 if sp.compress is None else 32
         g = P.ShallowIndex(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, sp.n_frames,
                            sp.n_frames * rpf)
-        keep = sp.stream in (0, 1)
-        blocks = []
         for f0 in range(0, sp.n_frames, 600):
             f1 = min(sp.n_frames, f0 + 600)
             kb = W.frame_block_keys(cfg, sp, q, f0, f1)
             g.append([dev_bf16(k) for k in kb], f1 - f0, 196, sp.compress)
-            if keep:
-                blocks.append(kb)
         torch.cuda.synchronize()
-        if keep:
-            host[sp.stream] = [np.concatenate([b[l] for b in blocks], axis=1) for l in range(cfg.n_layers)]
         gidxs.append(g)
         qs.append(q)
         log(f"C5 stream {sp.stream}: {sp.n_frames} frames, compressed {sp.compress is not None}")
@@ -704,16 +745,10 @@ def test_c5_full_size_sampled():
     plain = ids.cpu().numpy().copy()
     out = r.debug(qd)
     np.testing.assert_array_equal(plain, out["frame_ids"])
-    NL = cfg.n_layers * cfg.n_q_heads
+    total = {}
     for s, sp in enumerate(specs):
         assert out["list_stats"][s, :, 1].sum() == 0, f"stream {s} took the fallback"
-        rows = sp.n_frames * (196 if sp.compress is None else 32)
-        assert out["vote_hist"][s].sum() == NL * min(cfg.top_k, rows)
-        assert out["frame_ids"][s, 0] in set(sp.planted), f"stream {s}: first pick not planted"
-    qm_all = [O.query_means(q) for q in qs]
-    for s in (0, 1):
-        sp = specs[s]
-        keys = host.pop(s)
+        keys = W.frame_block_keys(cfg, sp, qs[s], 0, sp.n_frames)     # the same bytes again
         o = O.Index(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim)
         if sp.compress is None:
             o.append(keys, sp.n_frames, 196)
@@ -722,34 +757,15 @@ def test_c5_full_size_sampled():
             desc = [O.descriptor(O.decode_bf16(keys[-1][:, f * 196:(f + 1) * 196, :])) for f in range(sp.n_frames)]
             np.testing.assert_allclose(ex["desc"], np.array(desc), atol=2e-6)
             o.append_stored([ex["rows"][l] for l in range(cfg.n_layers)], [32] * sp.n_frames, desc)
+            del ex
         del keys
-        rep = {}
-        qm = qm_all[s]
-        for (l, h) in [(0, 3), (cfg.n_layers - 1, cfg.n_q_heads - 1)]:
-            g = h // cfg.group
-            K = O.decode_bf16(o.rows(l)[g])
-            so = K @ qm[l][h] / math.sqrt(cfg.head_dim)
-            dsc = np.abs(K) @ np.abs(qm[l][h]) / math.sqrt(cfg.head_dim)
-            j = l * cfg.n_q_heads + h
-            kk = min(cfg.top_k, so.size)
-            check_topk_list(so, dsc, out["topk_pos"][s, j, :kk].astype(np.int64),
-                            out["topk_score"][s, j, :kk].astype(np.float64), kk, rep, name=f"C5 s{s} list {j}")
-        kk = min(cfg.top_k, o.n_rows)
-        lists = [out["topk_pos"][s, j, :kk].astype(np.int64) for j in range(NL)]
-        f_of = o.frame_of_row()
-        v_re = np.zeros(sp.n_frames, dtype=np.int64)
-        m_re = np.zeros(sp.n_frames)
-        for j, p in enumerate(lists):
-            np.add.at(v_re, f_of[p], 1)
-            np.add.at(m_re, f_of[p], out["topk_score"][s, j, :kk].astype(np.float64))
-        assert np.array_equal(out["vote_hist"][s, :sp.n_frames], v_re)
-        gm = out["mass_hist"][s, :sp.n_frames].astype(np.float64)
-        np.testing.assert_allclose(gm, m_re, rtol=1e-5, atol=1e-5)
-        pn = int(out["pool_n"][s])
-        pool = out["pool"][s, :pn].astype(np.int64)
-        check_pool(pool, v_re, gm, 1e-5 * np.abs(m_re) + 1e-5, cfg.pool_mult * cfg.n_select, rep)
-        check_maxmin(pool, np.array(o.desc), cfg.n_select, out["frame_ids"][s, :int(out["n_out"][s])].astype(np.int64), rep)
-        log(f"C5 stream {s}", rep)
+        rep = staged_check(o, qs[s], out, s, cfg.top_k, cfg.n_select)
+        log(f"C5 stream {s} ({sp.n_frames} frames)", rep)
+        assert out["frame_ids"][s, 0] in set(sp.planted), f"stream {s}: first pick not planted"
+        _tally(total, rep)
+        del o
+    log("C5 all streams", total)
+    assert total["end_to_end_equal"] >= 1
 
 
 def test_c3_full_size():
@@ -763,9 +779,9 @@ def test_c3_full_size():
     log("C3 build")
     gidx, keys = _build_big(cfg, spec, q, compress=cfg.compress)
     ex = gidx.export()
-    checked, exempt = _kmeans_audit(ex, keys, cfg, range(0, spec.n_frames, 25), *cfg.compress)
-    log("C3 k-means audit", checked, "checked", exempt, "exempt")
-    assert checked >= 0.5 * (checked + exempt)
+    checked, exempt, gap = _kmeans_audit(ex, keys, cfg, range(0, spec.n_frames, 25), *cfg.compress)
+    log("C3 k-means audit", checked, "checked exactly,", exempt, "by tolerance; largest relative SSE gap", gap)
+    assert checked >= 0.9 * (checked + exempt)
     o = O.Index(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim)
     desc = [O.descriptor(O.decode_bf16(keys[-1][:, f * 196:(f + 1) * 196, :])) for f in range(spec.n_frames)]
     np.testing.assert_allclose(ex["desc"], np.array(desc), atol=2e-6)

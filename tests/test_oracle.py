@@ -74,6 +74,8 @@ def test_hand_scores():
     S = O.score_lists(idx, q)
     for got, want in zip(S, spec["scores"]):
         np.testing.assert_array_equal(got, np.array(want, dtype=np.float64))
+    (hm,) = O.score_lists(idx, q, head_mode=1)
+    np.testing.assert_array_equal(hm, np.array(spec["scores_head_mean"], dtype=np.float64))
 
 
 @pytest.mark.parametrize("case", [c["name"] for c in _load("hand_retrieval.json")["cases"]])
@@ -81,13 +83,70 @@ def test_hand_retrieval(case):
     spec = _load("hand_retrieval.json")
     c = next(c for c in spec["cases"] if c["name"] == case)
     idx, q = hand_index(spec, c["n_recent"])
-    ids, v, m, n, dbg = O.retrieve(idx, q, c["top_k"], c["n_select"], c["pool_mult"], debug=True)
+    ids, v, m, n, dbg = O.retrieve(idx, q, c["top_k"], c["n_select"], c["pool_mult"],
+                                   head_mode=c.get("head_mode", 0), debug=True)
     assert [list(t) for t in dbg["topk"]] == c["topk"]
     assert list(dbg["votes"]) == c["votes"]
     np.testing.assert_allclose(dbg["mass"], c["mass"], rtol=0, atol=1e-12)
     assert list(dbg["pool"]) == c["pool"]
     assert list(ids) == c["frame_ids"] and list(v) == c["sel_votes"] and n == c["n_out"]
     np.testing.assert_allclose(m, c["sel_mass"], rtol=0, atol=1e-12)
+
+
+def _closed_form(expr, defs):
+    """Evaluates a fixture's hand-derived closed form (exp, sqrt, + - * / and the
+    fixture's named normalisers only)."""
+    env = {"exp": math.exp, "sqrt": math.sqrt}
+    for k, e in defs.items():
+        env[k] = eval(e, {"__builtins__": {}}, dict(env))
+    return float(eval(expr, {"__builtins__": {}}, env))
+
+
+@pytest.mark.parametrize("case", [c["name"] for c in _load("hand_attention.json")["cases"]])
+def test_hand_attention(case):
+    """The logit and the attention-probability readings on a hand-worked index
+    where they select different rows (head mode 1) and rank the pool
+    differently (head mode 0)."""
+    spec = _load("hand_attention.json")
+    c = next(c for c in spec["cases"] if c["name"] == case)
+    cf = lambda e: _closed_form(e, spec["defs"])
+    idx, q = hand_index(spec, c["n_recent"])
+    hm, sm = c["head_mode"], c["score_mode"]
+    if "values" in c:
+        S = O.score_lists(idx, q, hm, sm)
+        assert len(S) == len(c["values"])
+        for got, want in zip(S, c["values"]):
+            np.testing.assert_allclose(got, [cf(e) for e in want], rtol=1e-13, atol=1e-15)
+    ids, v, m, n, dbg = O.retrieve(idx, q, c["top_k"], c["n_select"], c["pool_mult"],
+                                   head_mode=hm, score_mode=sm, debug=True)
+    assert [list(t) for t in dbg["topk"]] == c["topk"]
+    assert list(dbg["votes"]) == c["votes"]
+    np.testing.assert_allclose(dbg["mass"], [cf(e) for e in c["mass"]], rtol=1e-13, atol=1e-15)
+    assert list(dbg["pool"]) == c["pool"]
+    assert list(ids) == c["frame_ids"] and list(v) == c["sel_votes"] and n == c["n_out"]
+    np.testing.assert_allclose(m, [cf(e) for e in c["sel_mass"]], rtol=1e-13, atol=1e-15)
+
+
+def test_hand_attention_descriptor_distances():
+    spec = _load("hand_attention.json")
+    idx, _ = hand_index(spec)
+    D = np.array(idx.desc)
+    dist = {k: _closed_form(e, {}) for k, e in spec["distances"].items()}
+    assert math.isclose(1 - D[0] @ D[1], dist["f0_f1"], abs_tol=1e-14)
+    assert math.isclose(1 - D[0] @ D[2], dist["f0_f2"], abs_tol=1e-14)
+    assert math.isclose(1 - D[1] @ D[2], dist["f1_f2"], abs_tol=1e-14)
+
+
+def test_readings_disagree_only_where_expected():
+    """On the attention fixture the two readings give different head-mode-1
+    lists and different head-mode-0 pools, but the same head-mode-0 lists."""
+    spec = _load("hand_attention.json")
+    idx, q = hand_index(spec)
+    r = {sm: O.retrieve(idx, q, 2, 2, 1, head_mode=0, score_mode=sm, debug=True)[4] for sm in (0, 1)}
+    assert [list(t) for t in r[0]["topk"]] == [list(t) for t in r[1]["topk"]]
+    assert list(r[0]["pool"]) != list(r[1]["pool"])
+    h = {sm: O.retrieve(idx, q, 2, 2, 4, head_mode=1, score_mode=sm, debug=True)[4] for sm in (0, 1)}
+    assert list(h[0]["topk"][0]) != list(h[1]["topk"][0])
 
 
 def test_hand_descriptor_distances():
@@ -157,16 +216,58 @@ def test_gqa_mapping():
         np.testing.assert_array_equal(S[h], want)
 
 
-def test_head_mean_mode():
+def test_head_mean_equal_heads_reduce_to_one_head():
+    """Special case: when every query head of a layer carries the same query and
+    every KV head the same keys, the head average of either reading is the
+    single head's value, a textbook dot product (or its softmax)."""
     rng = np.random.default_rng(2)
-    idx, _ = _random_index(rng)
+    L, Hq, Hk, d, F, T = 2, 4, 2, 8, 5, 3
+    k1 = [np.round(rng.standard_normal((1, F * T, d)) * 8) / 8 for _ in range(L)]
+    keys = [bits(np.repeat(k, Hk, axis=0)) for k in k1]
+    q1 = [np.round(rng.standard_normal((1, 1, d)) * 8) / 8 for _ in range(L)]
+    q = [bits(np.repeat(x, Hq, axis=0)) for x in q1]
+    idx = O.Index(L, Hq, Hk, d)
+    idx.append(keys, F, T)
+    for l in range(L):
+        K = O.decode_bf16(keys[l][0])
+        qv = O.decode_bf16(q[l][0, 0])
+        logit = np.array([math.fsum(K[p] * qv) for p in range(F * T)]) / math.sqrt(d)
+        m = logit.max()
+        prob = np.exp(logit - m) / math.fsum(np.exp(logit - m))
+        np.testing.assert_allclose(O.score_lists(idx, q, 1, 0)[l], logit, rtol=1e-14, atol=1e-14)
+        np.testing.assert_allclose(O.score_lists(idx, q, 1, 1)[l], prob, rtol=1e-13, atol=1e-16)
+
+
+def test_attention_probabilities_are_distributions():
+    """Each (layer, head)'s probabilities are positive and sum to one over the
+    candidates, keep the order of its logits (so head-mode-0 lists are the same
+    in both readings), and their head mean sums to one as well."""
+    rng = np.random.default_rng(12)
+    idx, _ = _random_index(rng, F=7, T=4, n_recent=2)
     q = _random_queries(rng)
-    per_head = O.score_lists(idx, q, 0)
-    per_layer = O.score_lists(idx, q, 1)
-    assert len(per_layer) == idx.L
-    for l in range(idx.L):
-        np.testing.assert_allclose(per_layer[l], np.mean(per_head[l * idx.Hq:(l + 1) * idx.Hq], axis=0),
-                                   rtol=1e-14, atol=1e-14)
+    lg = O.score_lists(idx, q, 0, 0)
+    pr = O.score_lists(idx, q, 0, 1)
+    for a, b in zip(lg, pr):
+        assert np.all(b > 0) and math.isclose(math.fsum(b), 1.0, rel_tol=1e-13)
+        np.testing.assert_array_equal(O.topk(a, a.size), O.topk(b, b.size))
+    for hm in O.score_lists(idx, q, 1, 1):
+        assert math.isclose(math.fsum(hm), 1.0, rel_tol=1e-13)
+    # shifting every logit of a list by a constant leaves its probabilities unchanged:
+    # doubling a query is not a shift, but a zero query gives the uniform distribution
+    zq = [np.zeros_like(x) for x in q]
+    for b in O.score_lists(idx, zq, 0, 1):
+        np.testing.assert_allclose(b, 1.0 / b.size, rtol=1e-15)
+
+
+def test_attention_probabilities_of_huge_logits():
+    """Logits 1024, 1020 and 0 (exp(1024) overflows float64): the probabilities
+    are 1/(1+e^-4), e^-4/(1+e^-4) and 0 in closed form."""
+    idx = O.Index(1, 1, 1, 4)
+    idx.append([bits(np.array([[[1024, 0, 0, 0], [1020, 0, 0, 0], [0, 0, 0, 0]]], np.float32))], 3, 1)
+    q = [bits(np.array([[[2, 0, 0, 0]]], np.float32))]
+    (b,) = O.score_lists(idx, q, 0, 1)
+    e4 = math.exp(-4.0)
+    np.testing.assert_allclose(b, [1 / (1 + e4), e4 / (1 + e4), 0.0], rtol=1e-15, atol=0)
 
 
 # ---------------------------------------------------------------------------
@@ -213,8 +314,13 @@ def test_vote_sum_invariant(seed):
     idx, _ = _random_index(rng, F=7, T=4)
     q = _random_queries(rng)
     for k in (1, 5, 28, 100):
-        _, _, _, _, dbg = O.retrieve(idx, q, k, 3, debug=True)
-        assert dbg["votes"].sum() == idx.L * idx.Hq * min(k, idx.candidate_rows())
+        for sm in (0, 1):
+            _, _, _, _, dbg = O.retrieve(idx, q, k, 3, debug=True, score_mode=sm)
+            assert dbg["votes"].sum() == idx.L * idx.Hq * min(k, idx.candidate_rows())
+            # head mode 1: one list per layer, so sum v = L min(k, N)
+            _, _, _, _, dbg = O.retrieve(idx, q, k, 3, head_mode=1, debug=True, score_mode=sm)
+            assert dbg["votes"].sum() == idx.L * min(k, idx.candidate_rows())
+            assert all(len(t) == min(k, idx.candidate_rows()) for t in dbg["topk"])
 
 
 def test_votes_invariant_under_row_permutation_within_frame():
@@ -401,20 +507,23 @@ def _brute_frames(keys, F, T, L, Hk):
     return [[[[keys[l][g][t * T + p] for p in range(T)] for g in range(Hk)] for l in range(L)] for t in range(F)]
 
 
-@pytest.mark.parametrize("seed,k,K,pm,nr,Hq,Hk", [
-    (0, 4, 3, 4, 0, 4, 2), (1, 9, 2, 1, 0, 4, 4), (2, 200, 4, 4, 0, 2, 1),
-    (3, 3, 5, 2, 2, 6, 2), (4, 1, 1, 4, 0, 4, 2), (5, 6, 4, 4, 6, 4, 2)])
-def test_oracle_matches_brute(seed, k, K, pm, nr, Hq, Hk):
+@pytest.mark.parametrize("seed,k,K,pm,nr,Hq,Hk,hm,sm", [
+    (0, 4, 3, 4, 0, 4, 2, 0, 0), (1, 9, 2, 1, 0, 4, 4, 0, 0), (2, 200, 4, 4, 0, 2, 1, 0, 0),
+    (3, 3, 5, 2, 2, 6, 2, 0, 0), (4, 1, 1, 4, 0, 4, 2, 0, 0), (5, 6, 4, 4, 6, 4, 2, 0, 0),
+    (6, 4, 3, 4, 0, 4, 2, 1, 0), (7, 9, 2, 4, 1, 6, 2, 1, 0), (8, 200, 4, 4, 0, 2, 1, 1, 0),
+    (9, 4, 3, 4, 0, 4, 2, 0, 1), (10, 3, 5, 2, 2, 6, 2, 0, 1), (11, 4, 3, 4, 0, 4, 2, 1, 1),
+    (12, 7, 2, 4, 1, 6, 3, 1, 1), (13, 200, 4, 4, 0, 2, 1, 1, 1)])
+def test_oracle_matches_brute(seed, k, K, pm, nr, Hq, Hk, hm, sm):
     rng = np.random.default_rng(seed)
     L, d, F, T, nq = 2, 8, 6, 5, 3
     keys = [W.bf16_bits(rng.standard_normal((Hk, F * T, d)).astype(np.float32)) for _ in range(L)]
     q = [W.bf16_bits(rng.standard_normal((Hq, nq, d)).astype(np.float32)) for _ in range(L)]
     idx = O.Index(L, Hq, Hk, d, nr)
     idx.append(keys, F, T)
-    ids, v, m, n, dbg = O.retrieve(idx, q, k, K, pm, debug=True)
+    ids, v, m, n, dbg = O.retrieve(idx, q, k, K, pm, head_mode=hm, score_mode=sm, debug=True)
     frames = _brute_frames(keys, F, T, L, Hk)
     qs = [[[q[l][h][j] for j in range(nq)] for h in range(Hq)] for l in range(L)]
-    bi, bv, bm, bd = brute.retrieve(frames, qs, Hk, k, K, pm, nr)
+    bi, bv, bm, bd = brute.retrieve(frames, qs, Hk, k, K, pm, nr, head_mode=hm, score_mode=sm)
     assert list(ids) == bi and list(v) == bv and n == sum(1 for x in bi if x >= 0)
     np.testing.assert_allclose(m, bm, rtol=1e-12, atol=1e-12)
     assert [list(t) for t in dbg["topk"]] == [[r[2] for r in lst] for lst in bd["lists"]]
