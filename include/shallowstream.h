@@ -180,6 +180,25 @@ ss_status ss_retrieve(ss_index* const* idx, int32_t n_streams, const void* const
                       size_t ws_bytes, void* stream, int64_t* frame_ids, int32_t* votes,
                       float* mass, int32_t* n_out);
 
+/* ss_retrieve for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * workspace is a library-owned device buffer of SS_NOALLOC_WORKSPACE_BYTES
+ * (64 MiB) on each device, which the runtime places when the library's code is
+ * loaded on that device and keeps until the process ends; its address is
+ * looked up on the first such call on a device.  The call allocates nothing
+ * and frees nothing.  Arguments and outputs as in ss_retrieve, without ws.
+ * Fails with SS_ERR_WORKSPACE, before enqueueing anything, when
+ * ss_retrieve_workspace_bytes() of the batch exceeds SS_NOALLOC_WORKSPACE_BYTES
+ * (a single one-hour stream of the 28/4-head, d = 128 shape needs about 10 MB;
+ * a batch of 16 such streams does not fit).  Every call on one device shares
+ * that buffer and leaves its contents behind (each call initialises what it
+ * reads): calls that overlap on one device (unordered streams, or several host
+ * threads) race and give undefined results, so order them on one stream. */
+#define SS_NOALLOC_WORKSPACE_BYTES ((size_t)64 << 20)
+ss_status ss_retrieve_noalloc(ss_index* const* idx, int32_t n_streams, const void* const* queries,
+                              const int32_t* n_q, const ss_retrieve_params* params, void* stream,
+                              int64_t* frame_ids, int32_t* votes, float* mass, int32_t* n_out);
+
 /* Intermediates of one retrieval, for parity checks (any pointer may be NULL).
  * Device arrays, n_lists = L_s*H_q (head_mode 0) or L_s (head_mode 1), lists
  * ordered layer-major, F = frames of the stream at the call:

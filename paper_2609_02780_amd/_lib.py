@@ -17,6 +17,7 @@ SS_ERR_CAPACITY = 3
 SS_ERR_WORKSPACE = 4
 SS_ERR_DEVICE = 5
 SS_ERR_INTERNAL = 6
+NOALLOC_WORKSPACE_BYTES = 64 << 20
 
 
 class SSError(RuntimeError):
@@ -68,6 +69,8 @@ _SIGS = {
                                                  C.POINTER(RetrieveParams)]),
     "ss_retrieve": (C.c_int32, [C.POINTER(_P), C.c_int32, C.POINTER(_P), C.POINTER(C.c_int32),
                                 C.POINTER(RetrieveParams), _P, C.c_size_t, _P, _P, _P, _P, _P]),
+    "ss_retrieve_noalloc": (C.c_int32, [C.POINTER(_P), C.c_int32, C.POINTER(_P), C.POINTER(C.c_int32),
+                                        C.POINTER(RetrieveParams), _P, _P, _P, _P, _P]),
     "ss_retrieve_debug": (C.c_int32, [C.POINTER(_P), C.c_int32, C.POINTER(_P), C.POINTER(C.c_int32),
                                       C.POINTER(RetrieveParams), _P, C.c_size_t, _P, _P, _P, _P, _P,
                                       C.POINTER(DebugOut)]),

@@ -845,6 +845,26 @@ ss_status ss_retrieve(ss_index* const* idx, int32_t n_streams, const void* const
   });
 }
 
+ss_status ss_retrieve_noalloc(ss_index* const* idx, int32_t n_streams, const void* const* queries,
+                              const int32_t* n_q, const ss_retrieve_params* params, void* stream,
+                              int64_t* frame_ids, int32_t* votes, float* mass, int32_t* n_out) {
+  return guarded([&]() -> ss_status {
+    ss_status st = check_batch(idx, n_streams, n_q, params);
+    if (st) return st;
+    const size_t need = batch_ws(idx, n_streams, n_q, params);
+    if (need > ss::kNoAllocBytes)
+      return fail(SS_ERR_WORKSPACE,
+                  "this batch needs a %zu-byte workspace, above the %zu bytes of the library-owned one: "
+                  "call ss_retrieve with a caller workspace, or split the batch",
+                  need, ss::kNoAllocBytes);
+    void* ws = nullptr;
+    const hipError_t e = ss::noalloc_workspace(&ws);
+    if (e != hipSuccess) return fail(SS_ERR_DEVICE, "library workspace lookup failed: %s", hipGetErrorString(e));
+    return retrieve_common(idx, n_streams, queries, n_q, params, ws, ss::kNoAllocBytes, stream, frame_ids,
+                           votes, mass, n_out, nullptr);
+  });
+}
+
 ss_status ss_retrieve_debug(ss_index* const* idx, int32_t n_streams, const void* const* queries,
                             const int32_t* n_q, const ss_retrieve_params* params, void* ws,
                             size_t ws_bytes, void* stream, int64_t* frame_ids, int32_t* votes,

@@ -133,6 +133,13 @@ size_t carve_workspace(RetrievePlan& p, void* ws);
 
 hipError_t launch_retrieve(RetrievePlan& p, hipStream_t st);
 
+// The library-owned retrieval workspace of the no-alloc entry point: a
+// file-scope device array of kNoAllocBytes on every device the library runs
+// on.  noalloc_workspace() returns its device address on the current device
+// (looked up once per device with hipGetSymbolAddress).
+constexpr size_t kNoAllocBytes = (size_t)64 << 20;
+hipError_t noalloc_workspace(void** ptr);
+
 // Pooled shallow Q-K ranking of up to kMaxStreams streams.
 struct PooledPlan {
   int S, L, Hq, Hk, G, D, n_select;

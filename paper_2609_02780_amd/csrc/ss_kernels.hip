@@ -3591,6 +3591,31 @@ hipError_t launch_append(const AppendArgs& a, bool compress, hipStream_t st) {
   return a.D == 128 ? append_impl<128>(a, compress, st) : append_impl<64>(a, compress, st);
 }
 
+// The no-alloc retrieval's workspace.  In host code `scratch` names a host-side
+// stand-in, not device memory: only the address that hipGetSymbolAddress
+// returns for the current device is ever passed to a kernel.  The runtime
+// places one copy on each device when the library's code object is loaded
+// there; it lives until the process ends.
+static __device__ __align__(256) unsigned char scratch[kNoAllocBytes];
+
+hipError_t noalloc_workspace(void** ptr) {
+  static std::atomic<void*> cache[kMaxDevices];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  void* p = cache[dev].load(std::memory_order_acquire);
+  if (p == nullptr) {
+    // concurrent first calls on one device look up the same address
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    cache[dev].store(p, std::memory_order_release);
+  }
+  *ptr = p;
+  return hipSuccess;
+}
+
 hipError_t launch_retrieve(RetrievePlan& p, hipStream_t st) {
   return p.D == 128 ? retrieve_impl<128>(p, st) : retrieve_impl<64>(p, st);
 }

@@ -197,6 +197,27 @@ class Retriever:
         _used_on(stream, self._ws)
         return self.frame_ids, self.votes, self.mass, self.n_out
 
+    def noalloc(self, queries, stream=None):
+        """The same retrieval through ``ss_retrieve_noalloc``: the library's own
+        device workspace instead of this object's (no device allocation by the
+        library or here).  Returns the same reused output buffers."""
+        S = len(self.indices)
+        if len(queries) != S:
+            raise ValueError(f"expected queries for {S} streams, got {len(queries)}")
+        ptrs, n_q = [], []
+        for s, (x, qs) in enumerate(zip(self.indices, queries)):
+            if len(qs) != x.n_layers:
+                raise ValueError(f"stream {s}: expected {x.n_layers} query tensors")
+            nq = qs[0].shape[1]
+            n_q.append(nq)
+            for l, q in enumerate(qs):
+                ptrs.append(_check_bf16(q, (x.n_q_heads, nq, x.head_dim), f"queries[{s}][{l}]"))
+        L.check(L.lib().ss_retrieve_noalloc(self._handles, S, L.ptr_array(ptrs), (C.c_int32 * S)(*n_q),
+                                            C.byref(self.params), _stream_handle(stream),
+                                            self.frame_ids.data_ptr(), self.votes.data_ptr(),
+                                            self.mass.data_ptr(), self.n_out.data_ptr()))
+        return self.frame_ids, self.votes, self.mass, self.n_out
+
     def debug(self, queries, stream=None) -> dict:
         """One retrieval with every intermediate (synchronises; parity checks only)."""
         qp, nq = self._marshal(queries)
