@@ -160,7 +160,7 @@ def time_evidence(torch, P, idxs, frame_ids, calls=20):
     for _ in range(calls):
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record()
-        units, n_units = P.assemble_evidence(idxs, frame_ids, 6, 1, 0, True)
+        units, _, n_units = P.assemble_evidence(idxs, frame_ids, 6, 1, 0, True)
         b.record()
         b.synchronize()
         lat.append(a.elapsed_time(b))

@@ -328,27 +328,53 @@ typedef struct {
   int32_t retrieved;
 } ss_evidence_params;
 
-/* Units ss_assemble_evidence can return per stream: n_recent, plus
- * n_select*(1+n_before+n_after) when retrieved.  0 if the parameters are
- * invalid or the count exceeds 4096. */
-int32_t ss_evidence_max_units(const ss_evidence_params* params, int32_t n_select);
+/* Long-term clusters retrieved for each stream (Eq. selected_cluster_evidence),
+ * to unite with the detailed evidence.
+ *   sets         host array of n_streams cluster sets (an entry may be NULL:
+ *                that stream has no long-term memory);
+ *   cluster_ids  device int64 [n_streams][k_clusters] cluster ids in any order,
+ *                as ss_clusters_retrieve writes them (entries < 0, or of
+ *                clusters not in use, are padding);
+ *   k_clusters   1..64. */
+typedef struct {
+  const ss_clusters* const* sets;
+  const int64_t* cluster_ids;
+  int32_t k_clusters;
+} ss_evidence_clusters;
 
-/* The frames handed to full-depth answering for each of n_streams streams
- * (Eq. selected_evidence, then deduplication and temporal order): with T the
- * frames stored in idx[s], the newest min(n_recent, T) frames, united, when
- * retrieved, with frames t-n_before .. t+n_after (those in [0, T)) of every
- * selected frame t; sorted ascending without repeats.
+/* Items ss_assemble_evidence can return per stream: n_recent, plus, when
+ * retrieved, n_select*(1+n_before+n_after) + k_clusters (k_clusters = 0 without
+ * clusters).  0 if the parameters are invalid or the count exceeds 4096. */
+int32_t ss_evidence_max_units(const ss_evidence_params* params, int32_t n_select, int32_t k_clusters);
+
+/* The evidence handed to full-depth answering for each of n_streams streams:
+ * E_det(q) of Eq. selected_evidence united with E_cl(q) of Eq.
+ * selected_cluster_evidence, deduplicated and in temporal order.  With T the
+ * frames stored in idx[s] and D = [first_detail, T) its detailed window (all
+ * of [0, T) unless frames left it through ss_clusters_absorb): the newest
+ * min(n_recent, T) frames and, when retrieved, frames t-n_before .. t+n_after
+ * of every selected frame t, each kept only if it lies in D (a frame that
+ * left D exists only inside its cluster's representative); then, when
+ * retrieved and clusters is given, every distinct retrieved cluster of the
+ * stream, placed in the temporal order at its first member frame (clusters
+ * cover disjoint runs of frames before D).
  *   frame_ids  device int64 [n_streams][n_select] as ss_retrieve writes them
  *              (entries < 0 are padding; ids >= T are skipped).  Not read, and
  *              may be NULL, when params->retrieved is 0.
- *   units      device int64 [n_streams][max_units] out, ascending, -1 padded;
+ *   clusters   NULL for detailed evidence only; not read when not retrieved.
+ *   units      device int64 [n_streams][max_units] out: frame ids (kind 0) or
+ *              cluster ids (kind 1) in temporal order, -1 padded;
+ *   kinds      device int32 [n_streams][max_units] out: 0 frame, 1 cluster,
+ *              -1 padding; may be NULL when clusters is NULL;
  *   n_units    device int32 [n_streams] out.
- *   max_units  >= ss_evidence_max_units(params, n_select).
- * Enqueued on `stream` after the retrieval that wrote frame_ids; uses the
- * frame counts of the indices at the time of the call. */
+ *   max_units  >= ss_evidence_max_units(params, n_select, k_clusters).
+ * Enqueued on `stream` after the retrievals that wrote frame_ids and
+ * cluster_ids; uses the frame counts and detailed windows of the indices at
+ * the time of the call. */
 ss_status ss_assemble_evidence(ss_index* const* idx, int32_t n_streams, const int64_t* frame_ids,
-                               int32_t n_select, const ss_evidence_params* params, void* stream,
-                               int64_t* units, int32_t* n_units, int32_t max_units);
+                               int32_t n_select, const ss_evidence_clusters* clusters,
+                               const ss_evidence_params* params, void* stream, int64_t* units, int32_t* kinds,
+                               int32_t* n_units, int32_t max_units);
 
 /* Every score of one list over rows [row0, row0+n_rows) of one index, with the
  * same arithmetic as ss_retrieve (parity only).  queries: host array of L_s

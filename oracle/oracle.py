@@ -502,19 +502,27 @@ def retrieve(index: Index, queries, top_k: int, n_select: int, pool_mult: int = 
 
 
 def evidence_units(n_frames: int, selected, n_recent: int, n_before: int = 1, n_after: int = 0,
-                   retrieved: bool = True) -> np.ndarray:
-    """The units handed to full-depth answering, ascending, without repeats.
+                   retrieved: bool = True, first_detail: int = 0) -> np.ndarray:
+    """The detailed units handed to full-depth answering, ascending, without
+    repeats (Eq. selected_evidence, then deduplication and temporal ordering).
 
     ``R_T`` is the newest ``n_recent`` units of the ``n_frames`` stored so far
     (Eq. context_partition).  When retrieval ran, each selected unit ``t`` is
     expanded to its temporal neighbours ``t - n_before .. t + n_after`` (the
-    paper's setting is one preceding unit), keeping only units that exist, and
-    the evidence is ``R_T`` united with those; otherwise it is ``R_T`` alone.
-    Entries of ``selected`` below 0 are padding and are ignored.
+    paper's setting is one preceding unit), and the evidence is ``R_T`` united
+    with those; otherwise it is ``R_T`` alone.  Entries of ``selected`` below 0
+    are padding and are ignored.
+
+    Reading: every detailed unit lies in the detailed window ``[first_detail,
+    n_frames)``: units that left it for long-term clusters (Eq.
+    optional_context_compression) no longer exist on their own, only inside
+    their cluster's representative, so neighbours and recent units below it
+    are dropped (``first_detail`` is 0 without compression).
     """
-    if n_frames < 0 or n_recent < 0 or n_before < 0 or n_after < 0:
+    if n_frames < 0 or n_recent < 0 or n_before < 0 or n_after < 0 or first_detail < 0:
         raise ValueError("sizes must be >= 0")
-    units = set(range(max(0, n_frames - n_recent), n_frames))
+    lo = min(first_detail, n_frames)
+    units = set(range(max(lo, n_frames - n_recent), n_frames))
     if retrieved:
         for t in selected:
             t = int(t)
@@ -523,9 +531,41 @@ def evidence_units(n_frames: int, selected, n_recent: int, n_before: int = 1, n_
             if t >= n_frames:
                 raise ValueError(f"selected unit {t} outside the {n_frames} stored units")
             for u in range(t - n_before, t + n_after + 1):
-                if 0 <= u < n_frames:
+                if lo <= u < n_frames:
                     units.add(u)
     return np.array(sorted(units), dtype=np.int64)
+
+
+def evidence_items(n_frames: int, selected, n_recent: int, n_before: int = 1, n_after: int = 0,
+                   retrieved: bool = True, first_detail: int = 0, cluster_first=(),
+                   selected_clusters=()):
+    """``E_det(q)`` united with ``E_cl(q)`` after deduplication and temporal
+    ordering (Eq. selected_evidence, Eq. selected_cluster_evidence and the
+    sentence after it).
+
+    ``cluster_first[j]`` is the first member unit of long-term cluster ``j``;
+    ``selected_clusters`` the retrieved cluster ids (entries below 0, or not
+    below ``len(cluster_first)``, are padding).  Reading: a cluster stands in
+    the temporal order at its first member unit; the clusters cover disjoint
+    runs of units before the detailed window, so no cluster and detailed unit
+    share a position.  Without retrieval ``E_cl`` is empty.
+
+    Returns ``(ids, kinds)``: int64 arrays in temporal order, kind 0 for a
+    detailed unit (id = unit), kind 1 for a cluster (id = cluster).
+    """
+    det = evidence_units(n_frames, selected, n_recent, n_before, n_after, retrieved, first_detail)
+    items = [(int(t), 0, int(t)) for t in det]
+    if retrieved:
+        seen = set()
+        for j in selected_clusters:
+            j = int(j)
+            if j < 0 or j >= len(cluster_first) or j in seen:
+                continue
+            seen.add(j)
+            items.append((int(cluster_first[j]), 1, j))
+    items.sort()
+    return (np.array([i for _, _, i in items], dtype=np.int64),
+            np.array([k for _, k, _ in items], dtype=np.int64))
 
 
 # ---------------------------------------------------------------------------

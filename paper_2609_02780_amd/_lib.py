@@ -51,6 +51,10 @@ class EvidenceParams(C.Structure):
                 ("retrieved", C.c_int32)]
 
 
+class EvidenceClusters(C.Structure):
+    _fields_ = [("sets", C.c_void_p), ("cluster_ids", C.c_void_p), ("k_clusters", C.c_int32)]
+
+
 class DebugOut(C.Structure):
     _fields_ = [("topk_pos", C.c_void_p), ("topk_score", C.c_void_p), ("vote_hist", C.c_void_p),
                 ("mass_hist", C.c_void_p), ("pool", C.c_void_p), ("pool_n", C.c_void_p),
@@ -90,9 +94,9 @@ _SIGS = {
     "ss_clusters_retrieve": (C.c_int32, [_P, _P, C.POINTER(_P), C.c_int32, C.c_int32, _P, C.c_size_t, _P,
                                          _P, _P, _P, _P, _P]),
     "ss_clusters_export": (C.c_int32, [_P, _P, _P, _P, _P, _P, _P]),
-    "ss_evidence_max_units": (C.c_int32, [C.POINTER(EvidenceParams), C.c_int32]),
-    "ss_assemble_evidence": (C.c_int32, [C.POINTER(_P), C.c_int32, _P, C.c_int32, C.POINTER(EvidenceParams), _P,
-                                         _P, _P, C.c_int32]),
+    "ss_evidence_max_units": (C.c_int32, [C.POINTER(EvidenceParams), C.c_int32, C.c_int32]),
+    "ss_assemble_evidence": (C.c_int32, [C.POINTER(_P), C.c_int32, _P, C.c_int32, C.POINTER(EvidenceClusters),
+                                         C.POINTER(EvidenceParams), _P, _P, _P, _P, C.c_int32]),
     "ss_debug_sample_plan": (C.c_int32, [C.c_int64, C.c_int32, C.POINTER(C.c_int32)]),
     "ss_set_profile_events": (C.c_int32, [_P, _P]),
     "ss_status_string": (C.c_char_p, [C.c_int32]),

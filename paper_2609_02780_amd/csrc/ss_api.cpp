@@ -465,14 +465,15 @@ ClusterLayout cluster_layout(const ss_cluster_desc& d) {
   return L;
 }
 
-// Candidate units of one stream's evidence, or -1 for invalid parameters.
-int64_t evidence_units_max(const ss_evidence_params* p, int32_t n_select) {
+// Candidate items of one stream's evidence, or -1 for invalid parameters.
+int64_t evidence_units_max(const ss_evidence_params* p, int32_t n_select, int32_t k_clusters) {
   if (!p || p->n_recent < 0 || p->n_before < 0 || p->n_after < 0) return -1;
   if (p->retrieved != 0 && p->retrieved != 1) return -1;
+  if (k_clusters < 0 || k_clusters > ss::kMaxSelect) return -1;
   int64_t n = p->n_recent;
   if (p->retrieved) {
     if (n_select < 1 || n_select > ss::kMaxSelect) return -1;
-    n += (int64_t)n_select * (1 + (int64_t)p->n_before + p->n_after);
+    n += (int64_t)n_select * (1 + (int64_t)p->n_before + p->n_after) + k_clusters;
   }
   return n;
 }
@@ -663,30 +664,49 @@ ss_status ss_retrieve_pooled(ss_index* const* idx, int32_t n_streams, const void
   });
 }
 
-int32_t ss_evidence_max_units(const ss_evidence_params* params, int32_t n_select) {
-  const int64_t n = evidence_units_max(params, n_select);
+int32_t ss_evidence_max_units(const ss_evidence_params* params, int32_t n_select, int32_t k_clusters) {
+  const int64_t n = evidence_units_max(params, n_select, k_clusters);
   return (n < 0 || n > ss::kMaxEvidence) ? 0 : (int32_t)std::max<int64_t>(n, 1);
 }
 
 ss_status ss_assemble_evidence(ss_index* const* idx, int32_t n_streams, const int64_t* frame_ids,
-                               int32_t n_select, const ss_evidence_params* params, void* stream,
-                               int64_t* units, int32_t* n_units, int32_t max_units) {
+                               int32_t n_select, const ss_evidence_clusters* clusters,
+                               const ss_evidence_params* params, void* stream, int64_t* units, int32_t* kinds,
+                               int32_t* n_units, int32_t max_units) {
   return guarded([&]() -> ss_status {
     if (!idx) return fail(SS_ERR_INVALID_ARGUMENT, "idx is NULL");
     if (n_streams < 1) return fail(SS_ERR_INVALID_ARGUMENT, "n_streams must be >= 1");
     for (int s = 0; s < n_streams; ++s)
       if (!idx[s]) return fail(SS_ERR_INVALID_ARGUMENT, "idx[%d] is NULL", s);
-    const int64_t need = evidence_units_max(params, n_select);
+    const int kc = clusters ? clusters->k_clusters : 0;
+    if (clusters && (kc < 1 || kc > ss::kMaxSelect))
+      return fail(SS_ERR_UNSUPPORTED, "k_clusters %d outside 1..%d", kc, ss::kMaxSelect);
+    const int64_t need = evidence_units_max(params, n_select, kc);
     if (need < 0) return fail(SS_ERR_INVALID_ARGUMENT, "invalid evidence parameters");
     if (need > ss::kMaxEvidence)
-      return fail(SS_ERR_UNSUPPORTED, "%lld candidate units per stream > %d", (long long)need, ss::kMaxEvidence);
+      return fail(SS_ERR_UNSUPPORTED, "%lld candidate items per stream > %d", (long long)need, ss::kMaxEvidence);
     if (max_units < std::max<int64_t>(need, 1) || max_units > ss::kMaxEvidence)
       return fail(SS_ERR_INVALID_ARGUMENT, "max_units %d outside %lld..%d", max_units,
                   (long long)std::max<int64_t>(need, 1), ss::kMaxEvidence);
     if (params->retrieved && !frame_ids) return fail(SS_ERR_INVALID_ARGUMENT, "frame_ids is NULL");
     if (!units || !n_units) return fail(SS_ERR_INVALID_ARGUMENT, "an output pointer is NULL");
-    if (!aligned(units, 8) || !aligned(n_units, 4) || (frame_ids && !aligned(frame_ids, 8)))
+    if (clusters && !kinds) return fail(SS_ERR_INVALID_ARGUMENT, "kinds is NULL (needed with clusters)");
+    if (!aligned(units, 8) || !aligned(n_units, 4) || (kinds && !aligned(kinds, 4)) ||
+        (frame_ids && !aligned(frame_ids, 8)))
       return fail(SS_ERR_INVALID_ARGUMENT, "misaligned device pointer");
+    if (clusters) {
+      if (!clusters->sets) return fail(SS_ERR_INVALID_ARGUMENT, "clusters->sets is NULL");
+      if (params->retrieved && !clusters->cluster_ids)
+        return fail(SS_ERR_INVALID_ARGUMENT, "clusters->cluster_ids is NULL");
+      if (clusters->cluster_ids && !aligned(clusters->cluster_ids, 8))
+        return fail(SS_ERR_INVALID_ARGUMENT, "misaligned device pointer");
+      for (int s = 0; s < n_streams; ++s) {
+        const ss_clusters* c = clusters->sets[s];
+        if (c && (c->desc.n_layers != idx[s]->desc.n_layers || c->desc.n_kv_heads != idx[s]->desc.n_kv_heads ||
+                  c->desc.head_dim != idx[s]->desc.head_dim))
+          return fail(SS_ERR_INVALID_ARGUMENT, "cluster set %d and index %d shapes differ", s, s);
+      }
+    }
     const hipStream_t hs = static_cast<hipStream_t>(stream);
     for (int s0 = 0; s0 < n_streams; s0 += ss::kMaxStreams) {
       ss::EvidenceArgs a{};
@@ -697,9 +717,23 @@ ss_status ss_assemble_evidence(ss_index* const* idx, int32_t n_streams, const in
       a.n_after = params->n_after;
       a.retrieved = params->retrieved;
       a.max_units = max_units;
-      for (int s = 0; s < a.S; ++s) a.T[s] = idx[s0 + s]->n_frames;
+      for (int s = 0; s < a.S; ++s) {
+        const ss_index* x = idx[s0 + s];
+        a.T[s] = x->n_frames;
+        a.lo[s] = std::min(x->first_detail, x->n_frames);
+      }
       a.frame_ids = params->retrieved ? frame_ids + (size_t)s0 * n_select : nullptr;
+      if (clusters && params->retrieved) {
+        a.k_clusters = kc;
+        a.cluster_ids = clusters->cluster_ids + (size_t)s0 * kc;
+        for (int s = 0; s < a.S; ++s) {
+          const ss_clusters* c = clusters->sets[s0 + s];
+          a.cl_span[s] = c ? c->dev.span : nullptr;
+          a.cl_count[s] = c ? c->dev.state : nullptr;
+        }
+      }
       a.units = units + (size_t)s0 * max_units;
+      a.kinds = kinds ? kinds + (size_t)s0 * max_units : nullptr;
       a.n_units = n_units + s0;
       const hipError_t e = ss::launch_evidence(a, hs);
       if (e != hipSuccess) return fail(SS_ERR_DEVICE, "evidence launch failed: %s", hipGetErrorString(e));

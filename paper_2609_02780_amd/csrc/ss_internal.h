@@ -203,8 +203,15 @@ constexpr int kMaxEvidence = 4096;   // candidate units per stream (sorted in LD
 struct EvidenceArgs {
   int S, n_select, n_recent, n_before, n_after, retrieved, max_units;
   int64_t T[kMaxStreams];        // frames stored per stream
+  int64_t lo[kMaxStreams];       // first frame of each stream's detailed window
   const int64_t* frame_ids;      // [S][n_select], may be null when !retrieved
+  // retrieved long-term clusters (k_clusters == 0: none)
+  int k_clusters;
+  const int64_t* cluster_ids;        // [S][k_clusters], -1 padded
+  const int64_t* cl_span[kMaxStreams];   // per stream [max_clusters][2], null: no cluster set
+  const int32_t* cl_count[kMaxStreams];  // per stream: clusters in use (device)
   int64_t* units;                // [S][max_units]
+  int32_t* kinds;                // [S][max_units] 0 unit, 1 cluster, -1 padding; may be null
   int32_t* n_units;              // [S]
 };
 hipError_t launch_evidence(const EvidenceArgs& a, hipStream_t st);

@@ -3123,41 +3123,63 @@ __global__ __launch_bounds__(256) void k_cluster_reps(AbsorbArgs a) {
 // neighbourhood are laid out as candidate slots (missing ones as a sentinel),
 // sorted ascending in LDS, and the distinct values compacted in order.
 // ---------------------------------------------------------------------------
+// Items sort by their position in the stream: a detailed unit t at t, a
+// long-term cluster at its first member unit.  Key = position << 32 | kind << 31
+// | id (a position below 2^31, ids below 2^31); stored inverted (~key) so that
+// a descending sort gives temporal order and an empty slot (0) sorts last.
+__device__ __forceinline__ uint64_t evidence_key(int64_t pos, int kind, int64_t id) {
+  return ~(((uint64_t)pos << 32) | ((uint64_t)kind << 31) | (uint64_t)id);
+}
+
 __global__ __launch_bounds__(256) void k_evidence(EvidenceArgs a) {
   __shared__ uint64_t buf[kMaxEvidence];
   __shared__ int scan_sh[17];
   const int s = blockIdx.x;
-  const int64_t T = a.T[s];
-  const int64_t r0 = T > a.n_recent ? T - a.n_recent : 0;
-  const int nrec = (int)(T - r0);
+  const int64_t T = a.T[s], lo = a.lo[s];
+  const int64_t r0 = max(lo, T > a.n_recent ? T - a.n_recent : (int64_t)0);
+  const int nrec = (int)max((int64_t)0, T - r0);
   const int span = a.n_before + 1 + a.n_after;
-  const int total = nrec + (a.retrieved ? a.n_select * span : 0);
+  const int ndet = nrec + (a.retrieved ? a.n_select * span : 0);
+  const int ncl = (a.retrieved && a.cl_span[s]) ? a.k_clusters : 0;
+  const int total = ndet + ncl;
   const int P = pow2_ceil(max(total, 2));
-  // keys sort descending: key = INT64_MAX - unit; a missing slot is key 0
+  const int32_t n_cl = ncl > 0 ? *a.cl_count[s] : 0;
   for (int i = threadIdx.x; i < P; i += blockDim.x) {
-    int64_t u = -1;
+    uint64_t key = 0;
     if (i < nrec) {
-      u = r0 + i;
-    } else if (i < total) {
+      key = evidence_key(r0 + i, 0, r0 + i);
+    } else if (i < ndet) {
       const int j = i - nrec, slot = j / span, off = j % span - a.n_before;
       const int64_t t = a.frame_ids[(size_t)s * a.n_select + slot];
-      if (t >= 0 && t < T && t + off >= 0 && t + off < T) u = t + off;
+      // detailed units only: neighbours inside long-term clusters are not units any more
+      if (t >= 0 && t < T && t + off >= lo && t + off < T) key = evidence_key(t + off, 0, t + off);
+    } else if (i < total) {
+      const int64_t c = a.cluster_ids[(size_t)s * a.k_clusters + (i - ndet)];
+      if (c >= 0 && c < n_cl) key = evidence_key(a.cl_span[s][2 * c], 1, c);
     }
-    buf[i] = u >= 0 ? (uint64_t)(INT64_MAX - u) : 0ull;
+    buf[i] = key;
   }
   __syncthreads();
   bitonic_desc_u64(buf, P);
   int64_t* out = a.units + (size_t)s * a.max_units;
+  int32_t* kinds = a.kinds ? a.kinds + (size_t)s * a.max_units : nullptr;
   int base = 0;
   for (int b0 = 0; b0 < P; b0 += blockDim.x) {
     const int i = b0 + threadIdx.x;
     const bool keep = i < P && buf[i] != 0 && (i == 0 || buf[i] != buf[i - 1]);
     int tot;
     const int pre = block_excl_scan(keep ? 1 : 0, scan_sh, tot);
-    if (keep) out[base + pre] = INT64_MAX - (int64_t)buf[i];
+    if (keep) {
+      const uint64_t key = ~buf[i];
+      out[base + pre] = (int64_t)(key & 0x7FFFFFFFu);
+      if (kinds) kinds[base + pre] = (int32_t)((key >> 31) & 1u);
+    }
     base += tot;
   }
-  for (int i = base + threadIdx.x; i < a.max_units; i += blockDim.x) out[i] = -1;
+  for (int i = base + threadIdx.x; i < a.max_units; i += blockDim.x) {
+    out[i] = -1;
+    if (kinds) kinds[i] = -1;
+  }
   if (threadIdx.x == 0) a.n_units[s] = base;
 }
 

@@ -380,20 +380,37 @@ class LongClusters:
 
 
 def assemble_evidence(indices, frame_ids, n_recent: int, n_before: int = 1, n_after: int = 0,
-                      retrieved: bool = True, stream=None):
-    """The frames handed to answering for each stream (Eq. selected_evidence,
-    deduplicated, in temporal order).  ``frame_ids``: device int64
-    ``[n_streams][n_select]`` as returned by :class:`Retriever` (ignored when
-    ``retrieved`` is false).  Returns device tensors ``(units, n_units)``:
-    ``units`` int64 ``[n_streams][max_units]`` ascending and -1 padded."""
+                      retrieved: bool = True, clusters=None, cluster_ids=None, stream=None):
+    """The evidence handed to answering for each stream (Eq. selected_evidence,
+    united with the retrieved long-term clusters of Eq.
+    selected_cluster_evidence when ``clusters`` is given; deduplicated, in
+    temporal order).  ``frame_ids``: device int64 ``[n_streams][n_select]`` as
+    returned by :class:`Retriever` (ignored when ``retrieved`` is false).
+    ``clusters``: a list of :class:`LongClusters` (or None) per stream, with
+    ``cluster_ids`` device int64 ``[n_streams][k_clusters]``.  Returns device
+    tensors ``(units, kinds, n_units)``: ``units`` int64 and ``kinds`` int32
+    ``[n_streams][max_units]`` (kind 0 a frame id, 1 a cluster id; -1 padded)."""
     indices = list(indices)
     S = len(indices)
     n_select = frame_ids.shape[1] if (retrieved and frame_ids is not None) else 0
     prm = L.EvidenceParams(n_recent, n_before, n_after, 1 if retrieved else 0)
-    max_units = L.lib().ss_evidence_max_units(C.byref(prm), n_select)
+    dev = indices[0].arena.device
+    ec = None
+    k_clusters = 0
+    keep = []
+    if clusters is not None:
+        if len(clusters) != S:
+            raise ValueError(f"expected {S} cluster sets (or None entries)")
+        if cluster_ids is None or cluster_ids.dtype != torch.int64 or not cluster_ids.is_cuda \
+                or cluster_ids.dim() != 2 or cluster_ids.shape[0] != S or not cluster_ids.is_contiguous():
+            raise ValueError("cluster_ids must be a contiguous device int64 tensor [n_streams][k_clusters]")
+        k_clusters = cluster_ids.shape[1]
+        sets = L.ptr_array([c._h.value if c is not None else None for c in clusters])
+        keep.append(sets)
+        ec = L.EvidenceClusters(C.cast(sets, C.c_void_p), cluster_ids.data_ptr(), k_clusters)
+    max_units = L.lib().ss_evidence_max_units(C.byref(prm), n_select, k_clusters)
     if max_units == 0:
         raise L.SSError(L.SS_ERR_INVALID_ARGUMENT, "invalid evidence parameters")
-    dev = indices[0].arena.device
     fid = 0
     if retrieved:
         if frame_ids.dtype != torch.int64 or not frame_ids.is_cuda or tuple(frame_ids.shape) != (S, n_select) \
@@ -401,12 +418,14 @@ def assemble_evidence(indices, frame_ids, n_recent: int, n_before: int = 1, n_af
             raise ValueError("frame_ids must be a contiguous device int64 tensor [n_streams][n_select]")
         fid = frame_ids.data_ptr()
     units = torch.empty((S, max_units), dtype=torch.int64, device=dev)
+    kinds = torch.empty((S, max_units), dtype=torch.int32, device=dev)
     n_units = torch.empty(S, dtype=torch.int32, device=dev)
     handles = L.ptr_array([x.handle.value for x in indices])
-    L.check(L.lib().ss_assemble_evidence(handles, S, fid, n_select, C.byref(prm), _stream_handle(stream),
-                                         units.data_ptr(), n_units.data_ptr(), max_units))
-    _used_on(stream, units, n_units)
-    return units, n_units
+    L.check(L.lib().ss_assemble_evidence(handles, S, fid, n_select, C.byref(ec) if ec is not None else None,
+                                         C.byref(prm), _stream_handle(stream), units.data_ptr(), kinds.data_ptr(),
+                                         n_units.data_ptr(), max_units))
+    _used_on(stream, units, kinds, n_units)
+    return units, kinds, n_units
 
 
 def set_profile_events(start, stop) -> None:

@@ -187,24 +187,39 @@ def test_evidence_validation(L):
     h = create(L, max_frames=4, max_rows=4 * 196)
     idx = (C.c_void_p * 1)(h.value)
     P = L.EvidenceParams
-    assert lib.ss_evidence_max_units(C.byref(P(6, 1, 0, 1)), 8) == 6 + 8 * 2
-    assert lib.ss_evidence_max_units(C.byref(P(2, 1, 0, 0)), 8) == 2
-    assert lib.ss_evidence_max_units(C.byref(P(0, 0, 0, 0)), 0) == 1       # room for nothing, still >= 1
-    assert lib.ss_evidence_max_units(C.byref(P(-1, 1, 0, 1)), 8) == 0
-    assert lib.ss_evidence_max_units(C.byref(P(6, 1, 0, 2)), 8) == 0
-    assert lib.ss_evidence_max_units(C.byref(P(6, 1, 0, 1)), 65) == 0
-    assert lib.ss_evidence_max_units(C.byref(P(4000, 10, 10, 1)), 64) == 0   # beyond 4096 candidates
+    assert lib.ss_evidence_max_units(C.byref(P(6, 1, 0, 1)), 8, 0) == 6 + 8 * 2
+    assert lib.ss_evidence_max_units(C.byref(P(6, 1, 0, 1)), 8, 5) == 6 + 8 * 2 + 5
+    assert lib.ss_evidence_max_units(C.byref(P(2, 1, 0, 0)), 8, 5) == 2          # no retrieval, no clusters
+    assert lib.ss_evidence_max_units(C.byref(P(0, 0, 0, 0)), 0, 0) == 1       # room for nothing, still >= 1
+    assert lib.ss_evidence_max_units(C.byref(P(-1, 1, 0, 1)), 8, 0) == 0
+    assert lib.ss_evidence_max_units(C.byref(P(6, 1, 0, 2)), 8, 0) == 0
+    assert lib.ss_evidence_max_units(C.byref(P(6, 1, 0, 1)), 65, 0) == 0
+    assert lib.ss_evidence_max_units(C.byref(P(6, 1, 0, 1)), 8, 65) == 0
+    assert lib.ss_evidence_max_units(C.byref(P(4000, 10, 10, 1)), 64, 0) == 0   # beyond 4096 candidates
     ok = P(6, 1, 0, 1)
     F = FAKE
-    assert lib.ss_assemble_evidence(idx, 1, F, 8, C.byref(ok), None, F, F, 10) == L.SS_ERR_INVALID_ARGUMENT
+    ev = lambda n, fid, ns, cl, prm, units, kinds, nu, mx: lib.ss_assemble_evidence(  # noqa: E731
+        idx, n, fid, ns, cl, prm, None, units, kinds, nu, mx)
+    assert ev(1, F, 8, None, C.byref(ok), F, F, F, 10) == L.SS_ERR_INVALID_ARGUMENT
     assert b"max_units" in lib.ss_last_error()
-    assert lib.ss_assemble_evidence(idx, 1, None, 8, C.byref(ok), None, F, F, 22) == L.SS_ERR_INVALID_ARGUMENT
-    assert lib.ss_assemble_evidence(idx, 1, F, 8, C.byref(ok), None, None, F, 22) == L.SS_ERR_INVALID_ARGUMENT
-    assert lib.ss_assemble_evidence(idx, 1, F + 4, 8, C.byref(ok), None, F, F, 22) == L.SS_ERR_INVALID_ARGUMENT
-    assert lib.ss_assemble_evidence(idx, 0, F, 8, C.byref(ok), None, F, F, 22) == L.SS_ERR_INVALID_ARGUMENT
-    assert lib.ss_assemble_evidence(idx, 1, F, 8, None, None, F, F, 22) == L.SS_ERR_INVALID_ARGUMENT
+    assert ev(1, None, 8, None, C.byref(ok), F, F, F, 22) == L.SS_ERR_INVALID_ARGUMENT
+    assert ev(1, F, 8, None, C.byref(ok), None, F, F, 22) == L.SS_ERR_INVALID_ARGUMENT
+    assert ev(1, F + 4, 8, None, C.byref(ok), F, F, F, 22) == L.SS_ERR_INVALID_ARGUMENT
+    assert ev(0, F, 8, None, C.byref(ok), F, F, F, 22) == L.SS_ERR_INVALID_ARGUMENT
+    assert ev(1, F, 8, None, None, F, F, F, 22) == L.SS_ERR_INVALID_ARGUMENT
     big = P(4000, 10, 10, 1)
-    assert lib.ss_assemble_evidence(idx, 1, F, 64, C.byref(big), None, F, F, 4096) == L.SS_ERR_UNSUPPORTED
+    assert ev(1, F, 64, None, C.byref(big), F, F, F, 4096) == L.SS_ERR_UNSUPPORTED
+    # with clusters: k_clusters range, the cluster ids and the kinds output are required
+    sets = (C.c_void_p * 1)(None)
+    EC = L.EvidenceClusters
+    assert ev(1, F, 8, C.byref(EC(C.cast(sets, C.c_void_p), F, 0)), C.byref(ok), F, F, F, 22) == L.SS_ERR_UNSUPPORTED
+    assert ev(1, F, 8, C.byref(EC(C.cast(sets, C.c_void_p), F, 4)), C.byref(ok), F, F, F, 22) == \
+        L.SS_ERR_INVALID_ARGUMENT                                                 # 26 items need max_units 26
+    assert ev(1, F, 8, C.byref(EC(C.cast(sets, C.c_void_p), None, 4)), C.byref(ok), F, F, F, 26) == \
+        L.SS_ERR_INVALID_ARGUMENT
+    assert ev(1, F, 8, C.byref(EC(C.cast(sets, C.c_void_p), F, 4)), C.byref(ok), F, None, F, 26) == \
+        L.SS_ERR_INVALID_ARGUMENT
+    assert ev(1, F, 8, C.byref(EC(None, F, 4)), C.byref(ok), F, F, F, 26) == L.SS_ERR_INVALID_ARGUMENT
     assert lib.ss_index_destroy(h) == 0
 
 

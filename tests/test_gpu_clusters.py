@@ -154,6 +154,18 @@ def test_clusters_streaming_against_oracle(seed, tau, max_clusters, compress):
         return   # near tie at the cut: the set may differ
     assert sorted(ids.cpu().numpy()[:k].tolist()) == sorted(w_ids[:k].tolist())
     np.testing.assert_allclose(sc.cpu().numpy()[:k], s_all[ids.cpu().numpy()[:k]], atol=2e-6)
+    # the evidence handed to answering: detailed units and retrieved clusters in
+    # temporal order, from the GPU's selections (checked above), against the
+    # oracle's assembly with the oracle's cluster spans
+    ev_ids, ev_kinds, ev_n = P.assemble_evidence([g], r.frame_ids, nr, 1, 0, True, clusters=[cl],
+                                                 cluster_ids=ids[None, :].contiguous())
+    torch.cuda.synchronize()
+    m = int(ev_n.cpu()[0])
+    wi, wk = O.evidence_items(F, out["frame_ids"][0], nr, 1, 0, True, o.first_detail, ocl.first,
+                              ids.cpu().numpy())
+    assert ev_ids.cpu().numpy()[0, :m].tolist() == wi.tolist()
+    assert ev_kinds.cpu().numpy()[0, :m].tolist() == wk.tolist()
+    assert int(wk.sum()) == k
 
 
 def g_first(g, o):

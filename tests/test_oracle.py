@@ -643,6 +643,40 @@ def test_evidence_invariants_random():
         assert only.tolist() == list(range(max(0, T - nr), T))
 
 
+@pytest.mark.parametrize("case", _load("evidence_hand.json")["cluster_cases"], ids=lambda c: c["name"])
+def test_evidence_with_clusters_hand(case):
+    ids, kinds = O.evidence_items(case["n_frames"], case["selected"], case["n_recent"], case["n_before"],
+                                  case["n_after"], case["retrieved"], case["first_detail"], case["cluster_first"],
+                                  case["selected_clusters"])
+    assert ids.tolist() == case["ids"] and kinds.tolist() == case["kinds"]
+
+
+def test_evidence_with_clusters_invariants_random():
+    """Against a membership test written from the definition: the detailed part
+    is every unit of [first_detail, T) that is recent or a neighbour of a
+    selected unit, each retrieved cluster appears once, and the items run in
+    the order of their positions (a cluster at its first member unit)."""
+    rng = np.random.default_rng(6)
+    for _ in range(300):
+        T = int(rng.integers(1, 60))
+        fd = int(rng.integers(0, T + 1))
+        cuts = sorted(set(rng.integers(1, fd + 1, size=int(rng.integers(0, 5))).tolist())) if fd > 0 else []
+        firsts = [0] + [c for c in cuts if c < fd] if fd > 0 else []
+        nr, nb, na = (int(x) for x in rng.integers(0, 5, size=3))
+        sel = rng.integers(fd, T, size=int(rng.integers(0, 6))) if fd < T else np.zeros(0, np.int64)
+        sc = rng.integers(-1, len(firsts) + 2, size=int(rng.integers(0, 6)))
+        ids, kinds = O.evidence_items(T, sel, nr, nb, na, True, fd, firsts, sc)
+        det = [u for u in range(fd, T)
+               if u >= T - nr or any(s - nb <= u <= s + na for s in sel.tolist())]
+        cl = sorted({int(j) for j in sc if 0 <= j < len(firsts)})
+        assert ids[kinds == 0].tolist() == det
+        assert sorted(ids[kinds == 1].tolist()) == cl
+        pos = [int(i) if k == 0 else firsts[int(i)] for i, k in zip(ids, kinds)]
+        assert pos == sorted(pos) and len(set(pos)) == len(pos)
+        only_ids, only_kinds = O.evidence_items(T, sel, nr, nb, na, False, fd, firsts, sc)
+        assert only_ids.tolist() == list(range(max(fd, T - nr), T)) and not only_kinds.any()
+
+
 def test_evidence_rejects_bad_input():
     with pytest.raises(ValueError):
         O.evidence_units(5, [7], 2)
