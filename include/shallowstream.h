@@ -126,8 +126,44 @@ ss_status ss_index_create(const ss_index_desc* desc, void* dev_arena, size_t are
 /* Release the host-side handle.  The arena stays the caller's. */
 ss_status ss_index_destroy(ss_index* idx);
 
-/* Host-side counters: frames and rows per (layer, KV head) stored so far. */
+/* Host-side counters: frames appended so far (frame ids run 0 .. n_frames-1)
+ * and rows per (layer, KV head) the arena holds now. */
 ss_status ss_index_info(const ss_index* idx, int64_t* n_frames, int64_t* n_rows);
+
+/* The frames the index holds: the arena stores frames [first_stored,
+ * n_frames) (frames below were dropped by ss_index_compact), and frames below
+ * first_detail have left the detailed window for long-term clusters
+ * (ss_clusters_absorb); first_stored <= first_detail.  Either pointer may be
+ * NULL. */
+ss_status ss_index_window(const ss_index* idx, int64_t* first_stored, int64_t* first_detail);
+
+/* The memory side of long-history compression (Eq.
+ * optional_context_compression): the frames that left the detailed window
+ * leave the arena too.  Their rows, member counts, descriptors, pooled keys and
+ * row offsets are dropped; the stored rows of the detailed frames move to the
+ * start of every (layer, KV head) run of the arena (in passes of at most the
+ * dropped rows, each a copy kernel on `stream`), so that later appends reuse
+ * the space: max_frames and max_rows then bound the frames and rows kept in
+ * detail, not the stream's length.  Frame ids stay as they were.  Retrieval,
+ * pooled ranking, absorption and evidence are unchanged by it.  No-op when no
+ * frame has left the detailed window since the last compaction.  Its cost is a
+ * copy of the kept rows, so compact after absorbing many frames at once.
+ * Ordered on `stream` with the index's other work like an append; on
+ * SS_ERR_DEVICE the index must be discarded. */
+ss_status ss_index_compact(ss_index* idx, void* stream);
+
+/* Where the detailed window must start to fit a byte budget B (Eq.
+ * optional_context_compression: once Mem(M_T) > B, older history leaves for
+ * long-term clusters while the recent units and the near history stay in
+ * detail).  Mem counts the arena bytes of the frames in the detailed window:
+ * a frame of r stored rows takes r*L_s*H_kv*(2d + 4) + (1 + L_s)*H_kv*d*4 + 4
+ * bytes (keys, member counts, descriptor, pooled keys, row offset).
+ * *frame_hi (host) receives the smallest frame_hi in [first_detail,
+ * max(first_detail, n_frames - n_recent)] whose frames [frame_hi, n_frames) fit
+ * in budget_bytes, or the end of that range when none does (the recent window
+ * always stays detailed); first_detail when the window already fits.  Pass it
+ * to ss_clusters_absorb, then ss_index_compact.  Host work only. */
+ss_status ss_index_budget_split(const ss_index* idx, uint64_t budget_bytes, int64_t* frame_hi);
 
 /* Append n_frames frames of n_tokens visual tokens each: each unit's keys at
  * every shallow layer join the cache in temporal order (Sec. 4.1, Eq.
@@ -205,8 +241,9 @@ ss_status ss_retrieve_noalloc(ss_index* const* idx, int32_t n_streams, const voi
  *   topk_pos    int32 [n_streams][n_lists][top_k] row positions in rank order
  *               (score desc, position asc), -1 padded;
  *   topk_score  fp32  same shape, the scores;
- *   vote_hist   int32 [n_streams][max_frames] votes of every frame;
- *   mass_hist   fp32  [n_streams][max_frames] attention mass of every frame;
+ *   vote_hist   int32 [n_streams][max_frames] votes of every stored frame,
+ *               at frame id - first_stored (ss_index_window);
+ *   mass_hist   fp32  [n_streams][max_frames] attention mass, likewise;
  *   pool        int32 [n_streams][pool_mult*n_select] the vote-ranked pool, -1 padded;
  *   pool_n      int32 [n_streams];
  *   list_stats  int32 [n_streams][n_lists][2]: candidates kept by the streaming
@@ -386,11 +423,13 @@ ss_status ss_debug_scores(const ss_index* idx, const void* const* queries, int32
                           int32_t layer, int32_t q_head, int32_t head_mode, int64_t row0,
                           int64_t n_rows, float* out, void* ws, size_t ws_bytes, void* stream);
 
-/* Copy the stored state out (parity only; any pointer may be NULL):
+/* Copy the stored state out (parity only; any pointer may be NULL), for the
+ * frames the arena stores, first_stored .. n_frames-1 (ss_index_window):
  *   rows_dev     bf16 [L_s][H_kv][n_rows][d] device;
  *   counts_dev   int32 [L_s][H_kv][n_rows] device (k-means member counts, 1 for raw rows);
- *   desc_dev     fp32 [n_frames][H_kv*d] device descriptors;
- *   frame_offsets_host  int64 [n_frames+1] host row offsets. */
+ *   desc_dev     fp32 [n_frames - first_stored][H_kv*d] device descriptors;
+ *   frame_offsets_host  int64 [n_frames - first_stored + 1] host row offsets
+ *                in the arena. */
 ss_status ss_index_export(const ss_index* idx, void* rows_dev, int32_t* counts_dev,
                           float* desc_dev, int64_t* frame_offsets_host, void* stream);
 

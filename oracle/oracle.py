@@ -689,6 +689,32 @@ class LongClusters:
         index.first_detail = frame_hi
 
 
+def frame_bytes(n_rows: int, n_layers: int, n_kv_heads: int, head_dim: int) -> int:
+    """Index bytes one stored unit takes: its keys (bfloat16) and member counts
+    (int32) at every shallow layer and KV head, its descriptor (Eq. memory_key)
+    and pooled keys (float32), and its row offset (int32)."""
+    return (n_rows * n_layers * n_kv_heads * (2 * head_dim + 4)
+            + (1 + n_layers) * n_kv_heads * head_dim * 4 + 4)
+
+
+def budget_split(row_counts, first_detail: int, n_recent: int, n_layers: int, n_kv_heads: int,
+                 head_dim: int, budget: int) -> int:
+    """Eq. optional_context_compression: once the memory of the detailed history
+    exceeds the budget B, the oldest detailed units leave for long-term
+    clusters while the recent context stays detailed.  Reading: Mem is the
+    index bytes (``frame_bytes``) of the units in the detailed window
+    ``[first_detail, T)``; the result is the smallest ``h`` in
+    ``[first_detail, max(first_detail, T - n_recent)]`` whose units ``[h, T)``
+    fit in ``budget``, or the end of that range when none does."""
+    T = len(row_counts)
+    hi = max(first_detail, T - n_recent)
+    for h in range(first_detail, hi + 1):
+        mem = sum(frame_bytes(int(row_counts[f]), n_layers, n_kv_heads, head_dim) for f in range(h, T))
+        if mem <= budget:
+            return h
+    return hi
+
+
 def cluster_scores(index: Index, clusters: LongClusters, queries) -> np.ndarray:
     """Eq. selected_cluster_evidence scores every centroid against the final
     shallow query state.  Reading: the centroid lives in the descriptor space of

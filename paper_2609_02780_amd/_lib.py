@@ -67,6 +67,9 @@ _SIGS = {
     "ss_index_create": (C.c_int32, [C.POINTER(IndexDesc), _P, C.c_size_t, C.POINTER(_P)]),
     "ss_index_destroy": (C.c_int32, [_P]),
     "ss_index_info": (C.c_int32, [_P, C.POINTER(C.c_int64), C.POINTER(C.c_int64)]),
+    "ss_index_window": (C.c_int32, [_P, C.POINTER(C.c_int64), C.POINTER(C.c_int64)]),
+    "ss_index_compact": (C.c_int32, [_P, _P]),
+    "ss_index_budget_split": (C.c_int32, [_P, C.c_uint64, C.POINTER(C.c_int64)]),
     "ss_index_append": (C.c_int32, [_P, C.POINTER(_P), C.c_int32, C.c_int32, C.POINTER(Compress), _P,
                                     C.POINTER(C.c_int64)]),
     "ss_retrieve_workspace_bytes": (C.c_size_t, [C.POINTER(_P), C.c_int32, C.POINTER(C.c_int32),

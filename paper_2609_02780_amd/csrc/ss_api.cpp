@@ -20,9 +20,11 @@ struct ss_index {
   void* arena;
   size_t arena_bytes;
   ss::IndexDev dev;
-  int64_t n_frames;
-  int64_t n_rows;
-  std::vector<int64_t> off;  // frame row offsets, n_frames + 1 entries
+  int64_t n_frames;          // frames appended so far: ids 0 .. n_frames - 1
+  int64_t frame_base = 0;    // frames below it were dropped from the arena (ss_index_compact);
+                             // per-frame arena entries are indexed by id - frame_base
+  int64_t n_rows;            // rows the arena holds per (layer, KV head)
+  std::vector<int64_t> off;  // arena row offsets of frames frame_base .. n_frames
   int64_t first_detail = 0;  // frames before it were folded into long-term clusters
   int32_t rpf;               // common rows per frame, 0 if mixed, -1 before the first append
 };
@@ -127,12 +129,17 @@ bool same_shape(const ss_index_desc& a, const ss_index_desc& b) {
 struct Window {
   int64_t f_lo, f_hi, r_lo, r_hi;
 };
+// Arena row where frame f's rows start (frame_base <= f <= n_frames).
+inline int64_t row_of(const ss_index* x, int64_t f) { return x->off[(size_t)(f - x->frame_base)]; }
+
 Window candidates(const ss_index* x) {
   Window w;
-  w.f_hi = std::max<int64_t>(0, x->n_frames - x->desc.n_recent);
+  // frames leave the arena only after they left the detailed window, which
+  // never reaches into the recent window: frame_base <= f_lo <= f_hi
+  w.f_hi = std::max(x->frame_base, x->n_frames - x->desc.n_recent);
   w.f_lo = std::min(x->first_detail, w.f_hi);
-  w.r_lo = x->off[w.f_lo];
-  w.r_hi = x->off[w.f_hi];
+  w.r_lo = row_of(x, w.f_lo);
+  w.r_hi = row_of(x, w.f_hi);
   return w;
 }
 
@@ -273,9 +280,10 @@ void build_plan(ss::RetrievePlan& p, ss_index* const* idx, int s0, int S, const 
     const StreamSizes z = plan_stream(rows, frames, prm->top_k);
     ss::StreamPlan& sp = p.st[i];
     sp.keys = x->dev.keys + w.r_lo * d.head_dim;          // each (layer, KV head) run from r_lo
-    sp.frame_off = x->dev.frame_off + w.f_lo;
-    sp.desc = x->dev.desc + w.f_lo * (int64_t)d.n_kv_heads * d.head_dim;
+    sp.frame_off = x->dev.frame_off + (w.f_lo - x->frame_base);
+    sp.desc = x->dev.desc + (w.f_lo - x->frame_base) * (int64_t)d.n_kv_heads * d.head_dim;
     sp.frame0 = w.f_lo;
+    sp.hist0 = w.f_lo - x->frame_base;
     sp.row0 = w.r_lo;
     sp.kmax = x->dev.stats;
     sp.row_stride = (int32_t)x->desc.max_rows;
@@ -403,7 +411,7 @@ void build_pooled(ss::PooledPlan& p, ss_index* const* idx, int s0, int S, const 
     p.F[i] = frames;
     p.frame0[i] = w.f_lo;
     p.f_max = std::max<int64_t>(p.f_max, frames);
-    p.pooled[i] = x->dev.pooled + w.f_lo * (int64_t)p.L * p.Hk * p.D;
+    p.pooled[i] = x->dev.pooled + (w.f_lo - x->frame_base) * (int64_t)p.L * p.Hk * p.D;
     p.nq[i] = n_q[s0 + i];
     for (int l = 0; l < p.L; ++l)
       p.q[i * p.L + l] = queries ? static_cast<const uint16_t*>(queries[(size_t)(s0 + i) * p.L + l]) : nullptr;
@@ -543,9 +551,9 @@ ss_status ss_clusters_absorb(ss_clusters* cl, ss_index* idx, int64_t frame_hi, v
       return fail(SS_ERR_INVALID_ARGUMENT, "frame_hi %lld outside %lld..%lld (frames leave in order, never from the recent window)",
                   (long long)frame_hi, (long long)f_lo, (long long)f_end);
     for (int64_t f = f_lo; f < frame_hi; ++f)
-      if (idx->off[f + 1] - idx->off[f] != c.rows_per_unit)
+      if (row_of(idx, f + 1) - row_of(idx, f) != c.rows_per_unit)
         return fail(SS_ERR_INVALID_ARGUMENT, "frame %lld stores %lld rows, the cluster set takes %d", (long long)f,
-                    (long long)(idx->off[f + 1] - idx->off[f]), c.rows_per_unit);
+                    (long long)(row_of(idx, f + 1) - row_of(idx, f)), c.rows_per_unit);
     const int64_t n = frame_hi - f_lo;
     if (n > 0x7FFFFFFF) return fail(SS_ERR_UNSUPPORTED, "too many frames in one call");
     if (n > 0 && (!ws || !aligned(ws, 256) || ws_bytes < ss_clusters_absorb_workspace_bytes(n)))
@@ -554,8 +562,9 @@ ss_status ss_clusters_absorb(ss_clusters* cl, ss_index* idx, int64_t frame_hi, v
     ss::AbsorbArgs a{};
     a.L = c.n_layers; a.Hk = c.n_kv_heads; a.D = c.head_dim; a.R = c.rows_per_unit;
     a.max_clusters = c.max_clusters; a.max_rows = d.max_rows; a.tau = c.tau;
-    a.f_lo = f_lo; a.n_units = (int)n; a.row_lo = idx->off[f_lo];
-    a.desc = idx->dev.desc; a.keys = idx->dev.keys;
+    a.f_lo = f_lo; a.n_units = (int)n; a.row_lo = row_of(idx, f_lo);
+    a.desc = idx->dev.desc + (f_lo - idx->frame_base) * (int64_t)d.n_kv_heads * d.head_dim;
+    a.keys = idx->dev.keys;
     a.assign = static_cast<int32_t*>(ws);
     a.cl = cl->dev;
     const hipError_t e = ss::launch_absorb(a, static_cast<hipStream_t>(stream));
@@ -796,6 +805,61 @@ ss_status ss_index_info(const ss_index* idx, int64_t* n_frames, int64_t* n_rows)
   });
 }
 
+ss_status ss_index_window(const ss_index* idx, int64_t* first_stored, int64_t* first_detail) {
+  return guarded([&]() -> ss_status {
+    if (!idx) return fail(SS_ERR_INVALID_ARGUMENT, "idx is NULL");
+    if (first_stored) *first_stored = idx->frame_base;
+    if (first_detail) *first_detail = idx->first_detail;
+    return SS_OK;
+  });
+}
+
+ss_status ss_index_compact(ss_index* idx, void* stream) {
+  return guarded([&]() -> ss_status {
+    if (!idx) return fail(SS_ERR_INVALID_ARGUMENT, "idx is NULL");
+    const int64_t fs = idx->first_detail - idx->frame_base;
+    if (fs <= 0) return SS_OK;
+    const int64_t rs = row_of(idx, idx->first_detail);
+    // the new host offsets first, so that nothing after the launch can fail
+    std::vector<int64_t> off(idx->off.begin() + fs, idx->off.end());
+    for (int64_t& v : off) v -= rs;
+    ss::CompactArgs a{};
+    const ss_index_desc& d = idx->desc;
+    a.dev = idx->dev;
+    a.L = d.n_layers; a.Hk = d.n_kv_heads; a.D = d.head_dim; a.max_rows = d.max_rows;
+    a.row_shift = rs;
+    a.keep_rows = idx->n_rows - rs;
+    a.frame_shift = fs;
+    a.keep_frames = idx->n_frames - idx->first_detail;
+    const hipError_t e = ss::launch_compact(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(SS_ERR_DEVICE, "compaction launch failed: %s", hipGetErrorString(e));
+    idx->off.swap(off);
+    idx->frame_base = idx->first_detail;
+    idx->n_rows = a.keep_rows;
+    return SS_OK;
+  });
+}
+
+ss_status ss_index_budget_split(const ss_index* idx, uint64_t budget_bytes, int64_t* frame_hi) {
+  return guarded([&]() -> ss_status {
+    if (!idx || !frame_hi) return fail(SS_ERR_INVALID_ARGUMENT, "idx or frame_hi is NULL");
+    const ss_index_desc& d = idx->desc;
+    const uint64_t L = (uint64_t)d.n_layers, Hk = (uint64_t)d.n_kv_heads, D = (uint64_t)d.head_dim;
+    auto bytes = [&](int64_t f) {
+      const uint64_t rows = (uint64_t)(row_of(idx, f + 1) - row_of(idx, f));
+      return rows * L * Hk * (2 * D + 4) + (Hk * D + L * Hk * D) * 4 + 4;
+    };
+    const int64_t T = idx->n_frames, lo = idx->first_detail;
+    const int64_t hi = std::max(lo, T - (int64_t)d.n_recent);   // the recent window stays detailed
+    uint64_t mem = 0;
+    for (int64_t f = lo; f < T; ++f) mem += bytes(f);
+    int64_t h = lo;
+    while (h < hi && mem > budget_bytes) mem -= bytes(h++);
+    *frame_hi = h;
+    return SS_OK;
+  });
+}
+
 ss_status ss_index_append(ss_index* idx, const void* const* layer_keys, int32_t n_frames,
                           int32_t n_tokens, const ss_compress* compress, void* stream,
                           int64_t* first_frame_id) {
@@ -824,8 +888,9 @@ ss_status ss_index_append(ss_index* idx, const void* const* layer_keys, int32_t 
                     ss::kMaxTokensCompress);
       rpf = std::min(compress->n_centroids, n_tokens);
     }
-    if (idx->n_frames + n_frames > d.max_frames)
-      return fail(SS_ERR_CAPACITY, "%lld frames + %d exceeds max_frames %lld", (long long)idx->n_frames,
+    const int64_t stored = idx->n_frames - idx->frame_base;
+    if (stored + n_frames > d.max_frames)
+      return fail(SS_ERR_CAPACITY, "%lld stored frames + %d exceeds max_frames %lld", (long long)stored,
                   n_frames, (long long)d.max_frames);
     const int64_t new_rows = (int64_t)n_frames * rpf;
     if (idx->n_rows + new_rows > d.max_rows)
@@ -843,7 +908,7 @@ ss_status ss_index_append(ss_index* idx, const void* const* layer_keys, int32_t 
     a.n_tokens = n_tokens;
     a.max_rows = d.max_rows;
     a.row0 = idx->n_rows;
-    a.frame0 = idx->n_frames;
+    a.frame0 = stored;        // per-frame arena entries sit at id - frame_base
     a.rows_per_frame = rpf;
     a.n_centroids = compress ? compress->n_centroids : 0;
     a.n_iters = compress ? compress->n_iters : 0;
@@ -989,9 +1054,10 @@ ss_status ss_index_export(const ss_index* idx, void* rows_dev, int32_t* counts_d
                                             hipMemcpyDeviceToDevice, hs);
       if (e != hipSuccess) return fail(SS_ERR_DEVICE, "export counts: %s", hipGetErrorString(e));
     }
-    if (idx->n_frames > 0 && desc_dev) {
+    const int64_t stored = idx->n_frames - idx->frame_base;
+    if (stored > 0 && desc_dev) {
       const hipError_t e = hipMemcpyAsync(desc_dev, idx->dev.desc,
-                                          (size_t)idx->n_frames * d.n_kv_heads * d.head_dim * 4,
+                                          (size_t)stored * d.n_kv_heads * d.head_dim * 4,
                                           hipMemcpyDeviceToDevice, hs);
       if (e != hipSuccess) return fail(SS_ERR_DEVICE, "export descriptors: %s", hipGetErrorString(e));
     }

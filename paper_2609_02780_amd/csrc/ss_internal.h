@@ -68,6 +68,7 @@ struct StreamPlan {
   int32_t nq;
   int32_t rpf;           // rows per frame when every frame has the same count, else 0
   int64_t frame0;        // first candidate frame (earlier ones are in long-term clusters)
+  int64_t hist0;         // its place among the frames the arena stores (frame0 - the first stored frame)
   int64_t row0;          // its first row; keys, frame_off and desc above start there
   const uint32_t* kmax;  // the index's largest |key element| (float bits, device)
   float qscale;          // 1 / (n_q sqrt(d)) (head_mode 0), further / H_q (head_mode 1)
@@ -174,7 +175,7 @@ struct AbsorbArgs {
   int64_t f_lo;               // first leaving frame
   int n_units;
   int64_t row_lo;             // its first row
-  const float* desc;          // index descriptors [max_frames][H_kv*d]
+  const float* desc;          // descriptors of the leaving frames [n_units][H_kv*d]
   const uint16_t* keys;       // index keys [L][H_kv][max_rows][d]
   int32_t* assign;            // workspace [n_units][2]: cluster, members before joining
   ClusterDev cl;
@@ -215,6 +216,21 @@ struct EvidenceArgs {
   int32_t* n_units;              // [S]
 };
 hipError_t launch_evidence(const EvidenceArgs& a, hipStream_t st);
+
+// Compaction of an index arena: the stored frames from the first detailed one
+// on move to the arena's start.  Rows [row_shift, row_shift + keep_rows) of
+// every (layer, KV head) go to [0, keep_rows); the per-frame entries of the
+// stored frames [frame_shift, frame_shift + keep_frames) go to [0,
+// keep_frames), and the row offsets (keep_frames + 1 of them) are rebased by
+// row_shift.
+struct CompactArgs {
+  IndexDev dev;
+  int L, Hk, D;
+  int64_t max_rows;
+  int64_t row_shift, keep_rows;
+  int64_t frame_shift, keep_frames;
+};
+hipError_t launch_compact(const CompactArgs& a, hipStream_t st);
 
 // Scores of one list over a row range, same arithmetic as the retrieval.
 hipError_t launch_debug_scores(RetrievePlan& p, int layer, int q_head, int64_t row0,

@@ -1768,7 +1768,8 @@ __device__ void select_list(const ListArgs& a, int list, SelectShared& sh, uint3
 struct VoteArgs {
   int NL, k_max, pool, f_max, hist_stride;
   int32_t f[kMaxStreams];
-  int64_t frame0[kMaxStreams];   // debug outputs are indexed by absolute frame id
+  int64_t frame0[kMaxStreams];   // id of the first candidate frame (pool ids are reported as absolute ids)
+  int64_t hist0[kMaxStreams];    // its place among the stored frames (index of the debug histograms)
   const int32_t* votes_g;    // [S][f_max] per-frame votes
   const int64_t* massfx_g;   // [S][f_max] per-frame mass at scale 2^sexp[s]
   const int32_t* sexp;       // [S]
@@ -1839,8 +1840,8 @@ __device__ int pool_select(const VoteArgs& a, int s, PoolShared& sh) {
       const int v = vv[u];
       const int64_t mf = mm[u];
       if (a.dbg_vote_hist && f < F) {
-        a.dbg_vote_hist[(size_t)s * a.hist_stride + a.frame0[s] + f] = v;
-        a.dbg_mass_hist[(size_t)s * a.hist_stride + a.frame0[s] + f] = (float)((double)mf * inv);
+        a.dbg_vote_hist[(size_t)s * a.hist_stride + a.hist0[s] + f] = v;
+        a.dbg_mass_hist[(size_t)s * a.hist_stride + a.hist0[s] + f] = (float)((double)mf * inv);
       }
       // one LDS atomic per wave for the wave's voted frames
       const uint64_t vm = __ballot(v >= 1);
@@ -1861,7 +1862,7 @@ __device__ int pool_select(const VoteArgs& a, int s, PoolShared& sh) {
   }
   if (a.dbg_vote_hist) {
     for (int f = threadIdx.x; f < a.hist_stride; f += blockDim.x) {
-      if (f >= a.frame0[s] && f < a.frame0[s] + F) continue;
+      if (f >= a.hist0[s] && f < a.hist0[s] + F) continue;
       a.dbg_vote_hist[(size_t)s * a.hist_stride + f] = 0;
       a.dbg_mass_hist[(size_t)s * a.hist_stride + f] = 0.f;
     }
@@ -3032,7 +3033,7 @@ __global__ __launch_bounds__(256) void k_cluster_assign(AbsorbArgs a) {
     float part = 0.f;
     for (int k = 0; k < 4; ++k) {
       const int e = threadIdx.x + 256 * k;
-      if (e < dim) kv[k] = a.desc[t * dim + e];
+      if (e < dim) kv[k] = a.desc[(int64_t)u * dim + e];
       part = fmaf(kv[k], c[k], part);
     }
     bool join = false;
@@ -3115,6 +3116,35 @@ __global__ __launch_bounds__(256) void k_cluster_reps(AbsorbArgs a) {
     v = nb == 0 ? k : ((float)nb * v + k) / (float)(nb + 1);
   }
   if (cur >= 0) a.cl.reps[(size_t)cur * E + e] = v;
+}
+
+// ---------------------------------------------------------------------------
+// Index compaction (the memory side of long-history compression)
+// ---------------------------------------------------------------------------
+// Copies len units from unit src to unit dst in each of n_seg segments
+// (seg_stride units apart).  The host cuts a move into passes of at most the
+// shift, so a launch's source and destination ranges never overlap and its
+// copies may run in any order; the passes follow one another on the stream.
+__global__ __launch_bounds__(256) void k_move16(u32x4* base, int64_t seg_stride, int n_seg, int64_t src,
+                                                int64_t dst, int64_t len) {
+  const int64_t total = len * n_seg;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+    const int64_t sg = i / len, e = i - sg * len;
+    u32x4* b = base + sg * seg_stride;
+    b[dst + e] = b[src + e];
+  }
+}
+
+// The same for 4-byte words, subtracting `sub` from each (row offsets are
+// rebased as they move; 0 for data).
+__global__ __launch_bounds__(256) void k_move4(uint32_t* base, int64_t seg_stride, int n_seg, int64_t src,
+                                               int64_t dst, int64_t len, uint32_t sub) {
+  const int64_t total = len * n_seg;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+    const int64_t sg = i / len, e = i - sg * len;
+    uint32_t* b = base + sg * seg_stride;
+    b[dst + e] = b[src + e] - sub;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -3408,6 +3438,7 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   for (int s = 0; s < p.S; ++s) {
     va.f[s] = p.st[s].f;
     va.frame0[s] = p.st[s].frame0;
+    va.hist0[s] = p.st[s].hist0;
   }
   va.votes_g = p.votes; va.massfx_g = p.massfx; va.sexp = p.sexp;
   va.rec_hi = p.rec_hi; va.rec_lo = p.rec_lo;
@@ -3573,6 +3604,38 @@ hipError_t cluster_query_impl(const ClusterQueryPlan& p, hipStream_t st) {
 
 hipError_t launch_cluster_query(const ClusterQueryPlan& p, hipStream_t st) {
   return p.D == 64 ? cluster_query_impl<64>(p, st) : cluster_query_impl<128>(p, st);
+}
+
+hipError_t launch_compact(const CompactArgs& a, hipStream_t st) {
+  auto grid = [](int64_t n) { return dim3((unsigned)std::max<int64_t>(1, std::min<int64_t>((n + 255) / 256, 8192))); };
+  // items [shift, shift + keep) -> [0, keep) of `unit` units each, in passes of at most `shift` items
+  auto move16 = [&](void* base, int64_t seg_stride, int n_seg, int64_t unit, int64_t shift, int64_t keep) {
+    for (int64_t done = 0; done < keep; done += shift) {
+      const int64_t len = std::min(shift, keep - done) * unit;
+      hipLaunchKernelGGL(k_move16, grid(len * n_seg), dim3(256), 0, st, static_cast<u32x4*>(base), seg_stride,
+                         n_seg, (shift + done) * unit, done * unit, len);
+    }
+  };
+  auto move4 = [&](void* base, int64_t seg_stride, int n_seg, int64_t shift, int64_t keep, uint32_t sub) {
+    for (int64_t done = 0; done < keep; done += shift) {
+      const int64_t len = std::min(shift, keep - done);
+      hipLaunchKernelGGL(k_move4, grid(len * n_seg), dim3(256), 0, st, static_cast<uint32_t*>(base), seg_stride,
+                         n_seg, shift + done, done, len, sub);
+    }
+  };
+  const int lg = a.L * a.Hk;
+  if (a.row_shift > 0 && a.keep_rows > 0) {
+    move16(a.dev.keys, a.max_rows * a.D / 8, lg, a.D / 8, a.row_shift, a.keep_rows);   // 16-byte units of bf16 rows
+    move4(a.dev.counts, a.max_rows, lg, a.row_shift, a.keep_rows, 0u);
+  }
+  if (a.frame_shift > 0) {
+    if (a.keep_frames > 0) {
+      move16(a.dev.desc, 0, 1, (int64_t)a.Hk * a.D / 4, a.frame_shift, a.keep_frames);
+      move16(a.dev.pooled, 0, 1, (int64_t)a.L * a.Hk * a.D / 4, a.frame_shift, a.keep_frames);
+    }
+    move4(a.dev.frame_off, 0, 1, a.frame_shift, a.keep_frames + 1, (uint32_t)a.row_shift);
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_evidence(const EvidenceArgs& a, hipStream_t st) {

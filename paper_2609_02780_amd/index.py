@@ -89,6 +89,25 @@ class ShallowIndex:
         L.check(L.lib().ss_index_info(self.handle, C.byref(f), C.byref(r)))
         return f.value, r.value
 
+    def window(self) -> tuple[int, int]:
+        """``(first_stored, first_detail)``: the first frame the arena still
+        stores, and the first frame of the detailed window."""
+        a, b = C.c_int64(), C.c_int64()
+        L.check(L.lib().ss_index_window(self.handle, C.byref(a), C.byref(b)))
+        return a.value, b.value
+
+    def compact(self, stream=None) -> None:
+        """Drop the frames that left the detailed window from the arena (their
+        space is reused by later appends)."""
+        L.check(L.lib().ss_index_compact(self.handle, _stream_handle(stream)))
+
+    def budget_split(self, budget_bytes: int) -> int:
+        """The frame where the detailed window must start to fit ``budget_bytes``
+        (pass it to :meth:`LongClusters.absorb`, then :meth:`compact`)."""
+        h = C.c_int64()
+        L.check(L.lib().ss_index_budget_split(self.handle, budget_bytes, C.byref(h)))
+        return h.value
+
     @property
     def n_frames(self) -> int:
         return self.info()[0]
@@ -112,8 +131,10 @@ class ShallowIndex:
         return first.value
 
     def export(self, stream=None) -> dict:
-        """Stored rows, member counts, descriptors and frame offsets (synchronises)."""
+        """Stored rows, member counts, descriptors and frame offsets of the frames
+        the arena stores (synchronises)."""
         f, r = self.info()
+        f -= self.window()[0]          # stored frames
         dev = self.arena.device
         rows = torch.empty((self.n_layers, self.n_kv_heads, r, self.head_dim), dtype=torch.int16, device=dev)
         counts = torch.empty((self.n_layers, self.n_kv_heads, r), dtype=torch.int32, device=dev)

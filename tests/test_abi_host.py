@@ -312,3 +312,18 @@ def test_sample_plan(L):
             assert worse, (n, k, r)
     lib.ss_debug_sample_plan(705600, 512, out)
     assert tuple(out)[:2] == (3216, 14)       # the 1-hour index: 3,216 sampled rows, rank 14
+
+
+def test_window_compact_budget_on_empty_index(L):
+    """Host paths of the compaction calls: an empty index stores nothing, has
+    nothing to compact (no work is enqueued) and fits any budget."""
+    lib = L.lib()
+    h = create(L, max_frames=8, max_rows=8 * 196)
+    a, b, fh = C.c_int64(-1), C.c_int64(-1), C.c_int64(-1)
+    assert lib.ss_index_window(h, C.byref(a), C.byref(b)) == 0 and (a.value, b.value) == (0, 0)
+    assert lib.ss_index_window(None, C.byref(a), C.byref(b)) == L.SS_ERR_INVALID_ARGUMENT
+    assert lib.ss_index_compact(h, None) == 0
+    assert lib.ss_index_compact(None, None) == L.SS_ERR_INVALID_ARGUMENT
+    assert lib.ss_index_budget_split(h, 0, C.byref(fh)) == 0 and fh.value == 0
+    assert lib.ss_index_budget_split(h, 0, None) == L.SS_ERR_INVALID_ARGUMENT
+    assert lib.ss_index_destroy(h) == 0

@@ -847,3 +847,14 @@ def test_detailed_window_equals_index_of_the_window():
     pa = O.pooled_retrieve(full, q, 4)
     pb = O.pooled_retrieve(part, q, 4)
     assert pa[0].tolist() == [x + f0 for x in pb[0].tolist()]
+
+
+def test_budget_split_hand():
+    spec = _load("budget_hand.json")
+    sh = spec["shape"]
+    assert [O.frame_bytes(r, sh["n_layers"], sh["n_kv_heads"], sh["head_dim"]) for r in spec["rows"]] == \
+        spec["frame_bytes"]
+    for c in spec["cases"]:
+        got = O.budget_split(spec["rows"], c["first_detail"], c["n_recent"], sh["n_layers"], sh["n_kv_heads"],
+                             sh["head_dim"], c["budget"])
+        assert got == c["frame_hi"], c
