@@ -294,7 +294,16 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def cpu_baseline(cfg, host0):
+def hot_kernel(cfg, score_mode: int) -> str:
+    """The streaming scoring kernel of the workload's mode."""
+    if cfg.head_mode == 0:
+        return HOT_KERNEL
+    if score_mode == 1:
+        return f"k_stream_hp<{cfg.head_dim}, {cfg.n_kv_heads}>"
+    return f"k_stream_hm<{cfg.head_dim}>"
+
+
+def cpu_baseline(cfg, host0, score_mode: int = 0):
     """The oracle's retrieval over stream 0 of the workload, with its queries and
     retrieval parameters.  A raw stream is taken whole; a compressed one is cut to
     its first 40 frames, since the float64 k-means of the oracle's append is slow."""
@@ -317,7 +326,7 @@ def cpu_baseline(cfg, host0):
                   cfg.tokens_per_frame, comp)
         what = f"the first {nf} frames"
     t0 = time.perf_counter()
-    O.retrieve(oi, q, cfg.top_k, cfg.n_select, cfg.pool_mult, cfg.head_mode)
+    O.retrieve(oi, q, cfg.top_k, cfg.n_select, cfg.pool_mult, cfg.head_mode, score_mode=score_mode)
     dt = time.perf_counter() - t0
     keys = oi.n_rows * cfg.n_layers * cfg.n_kv_heads
     return {"value": keys / dt, "unit": "keys/s", "cores": int(cores), "kind": "oracle",
@@ -335,6 +344,8 @@ def main():
                     help="record the latency and streaming-kernel events on every N-th timed step")
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="C4", choices=sorted(W.CONFIGS))
+    ap.add_argument("--score-mode", type=int, default=0, choices=(0, 1),
+                    help="list values: 0 scaled logits (the workloads' default), 1 attention probabilities")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cold", action="store_true",
                     help="also time cold-cache calls (on by default for indices of at most 1 GiB)")
@@ -374,7 +385,7 @@ def main():
                           "long_history_compression": lc}), flush=True)
         return
     specs, idxs, queries, host0 = build_streams(torch, P, cfg)
-    r = P.Retriever(idxs, cfg.top_k, cfg.n_select, cfg.pool_mult, cfg.head_mode)
+    r = P.Retriever(idxs, cfg.top_k, cfg.n_select, cfg.pool_mult, cfg.head_mode, args.score_mode)
     for _ in range(args.warmup):
         r(queries)
     torch.cuda.synchronize()
@@ -428,7 +439,8 @@ def main():
         "config": {"workload": f"{cfg.name}: {cfg.description}; {cfg.n_layers} shallow layers, "
                                f"{cfg.n_q_heads} query / {cfg.n_kv_heads} KV heads, d={cfg.head_dim}, "
                                f"{cfg.n_q} query tokens, top-k {cfg.top_k}, {cfg.n_select} frames selected"
-                               + (", head-averaged lists" if cfg.head_mode else ""),
+                               + (", head-averaged lists" if cfg.head_mode else "")
+                               + (", attention probabilities" if args.score_mode else ""),
                    "streams": len(idxs), "rows_per_layer_kv_head": rows, "key_vectors": key_vectors,
                    "key_bytes": key_bytes},
         "p10_latency_ms": float(np.percentile(lat, 10)),
@@ -436,7 +448,8 @@ def main():
         "p90_latency_ms": float(np.percentile(lat, 90)),
         "scores_per_s": value * cfg.group,
         "hbm_frac_end_to_end": key_bytes / (np.percentile(lat, 50) / 1e3) / 1e9 / HBM_PEAK_GBS,
-        "roofline": {"kernel": HOT_KERNEL if cfg.head_mode == 0 else "k_stream_hm<128>", "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+        "roofline": {"kernel": hot_kernel(cfg, args.score_mode), "bound": "hbm", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "avg_kernel_ms": float(hot.mean()), "bytes_per_launch": key_bytes,
                      "event_samples": len(hot)},
@@ -447,7 +460,7 @@ def main():
     if cfg.compress is not None:
         out["append"] = time_append(torch, P, cfg)
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, host0)
+        out["cpu_baseline"] = cpu_baseline(cfg, host0, args.score_mode)
     print(json.dumps(out), flush=True)
 
 

@@ -91,13 +91,24 @@ typedef struct {
  *   pool_mult  the vote-ranked pool holds pool_mult*K frames (4 in the paper),
  *              pool_mult*K <= 256; 1 makes diversity selection a no-op.
  *   head_mode  0: one list per (layer, query head).  1: one list per layer with
- *              the scores averaged over all query heads (the paper's reduction).
+ *              the values averaged over all query heads (Sec. 4.2 averages the
+ *              attention over heads).
+ *   score_mode the value of a candidate row in a list.  0: the scaled logit
+ *              q.k/sqrt(d) (mean over query tokens).  1: the Q-K attention
+ *              probability, the softmax of one (layer, query head)'s logits
+ *              over all candidate rows, so a head-mode-1 list averages
+ *              per-head probabilities.  The attention mass of a frame is the
+ *              sum of its selected rows' values.  In head mode 0 the lists and
+ *              votes are the same in both modes (only the mass differs); in
+ *              head mode 1 they differ.  Head mode 1 with score_mode 1 needs
+ *              n_kv_heads in {1, 2, 4, 8} and n_kv_heads * head_dim <= 512.
  */
 typedef struct {
   int32_t top_k;
   int32_t n_select;
   int32_t pool_mult;
   int32_t head_mode;
+  int32_t score_mode;
 } ss_retrieve_params;
 
 /* Device bytes an index with this shape needs (0 if `desc` is invalid).

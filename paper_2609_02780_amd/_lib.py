@@ -38,7 +38,7 @@ class Compress(C.Structure):
 
 class RetrieveParams(C.Structure):
     _fields_ = [("top_k", C.c_int32), ("n_select", C.c_int32), ("pool_mult", C.c_int32),
-                ("head_mode", C.c_int32)]
+                ("head_mode", C.c_int32), ("score_mode", C.c_int32)]
 
 
 class ClusterDesc(C.Structure):

@@ -232,7 +232,7 @@ int64_t candidate_cap(int top_k, int64_t n_max) {
   return std::max<int64_t>(3 * expected_candidates(n_max, kk), 4096);
 }
 
-ss_status check_params(const ss_retrieve_params* p, int Hk) {
+ss_status check_params(const ss_retrieve_params* p, int Hk, int D) {
   if (!p) return fail(SS_ERR_INVALID_ARGUMENT, "params is NULL");
   if (p->top_k < 1 || p->top_k > ss::kMaxTopK)
     return fail(SS_ERR_UNSUPPORTED, "top_k %d outside 1..%d", p->top_k, ss::kMaxTopK);
@@ -246,6 +246,13 @@ ss_status check_params(const ss_retrieve_params* p, int Hk) {
     return fail(SS_ERR_INVALID_ARGUMENT, "head_mode must be 0 or 1");
   if (p->head_mode == 1 && Hk > 8)
     return fail(SS_ERR_UNSUPPORTED, "head_mode 1 supports at most 8 KV heads");
+  if (p->score_mode != 0 && p->score_mode != 1)
+    return fail(SS_ERR_INVALID_ARGUMENT, "score_mode must be 0 or 1");
+  if (p->head_mode == 1 && p->score_mode == 1 &&
+      ((int64_t)Hk * D > 512 || (Hk != 1 && Hk != 2 && Hk != 4 && Hk != 8)))
+    return fail(SS_ERR_UNSUPPORTED,
+                "head_mode 1 with attention probabilities needs n_kv_heads in {1, 2, 4, 8} and "
+                "n_kv_heads * head_dim <= 512");
   return SS_OK;
 }
 
@@ -262,7 +269,10 @@ void build_plan(ss::RetrievePlan& p, ss_index* const* idx, int s0, int S, const 
   p.G = p.Hq / p.Hk;
   p.D = d.head_dim;
   p.head_mode = prm->head_mode;
+  p.score_mode = prm->score_mode;
+  p.hm_prob = prm->head_mode == 1 && prm->score_mode == 1;
   p.NL = prm->head_mode == 0 ? p.L * p.Hq : p.L;
+  p.NLs = p.hm_prob ? p.L * p.Hq : p.NL;
   p.ncol = prm->head_mode == 0 ? p.G : 1;
   p.ngs = prm->head_mode == 0 ? p.Hk : 1;
   p.top_k = prm->top_k;
@@ -295,7 +305,7 @@ void build_plan(ss::RetrievePlan& p, ss_index* const* idx, int s0, int S, const 
     sp.nq = n_q[s0 + i];
     sp.rpf = x->rpf > 0 ? x->rpf : 0;
     double sc = 1.0 / ((double)sp.nq * std::sqrt((double)p.D));
-    if (prm->head_mode == 1) sc /= (double)p.Hq;
+    if (prm->head_mode == 1 && !p.hm_prob) sc /= (double)p.Hq;   // the logit mean folds 1/H_q into the query
     sp.qscale = (float)sc;
     for (int l = 0; l < p.L; ++l)
       sp.q[l] = queries ? static_cast<const uint16_t*>(queries[(size_t)(s0 + i) * p.L + l]) : nullptr;
@@ -323,7 +333,7 @@ ss_status check_batch(ss_index* const* idx, int32_t n_streams, const int32_t* n_
     if (n_q[s] < 1 || n_q[s] > 4096)
       return fail(SS_ERR_INVALID_ARGUMENT, "n_q[%d] = %d outside 1..4096", s, n_q[s]);
   }
-  return check_params(prm, idx[0]->desc.n_kv_heads);
+  return check_params(prm, idx[0]->desc.n_kv_heads, idx[0]->desc.head_dim);
 }
 
 size_t group_ws(ss_index* const* idx, int s0, int S, const int32_t* n_q,

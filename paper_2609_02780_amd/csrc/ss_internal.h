@@ -78,7 +78,10 @@ struct StreamPlan {
 struct RetrievePlan {
   int S, L, Hq, Hk, G, D;
   int head_mode;
+  int score_mode;        // 0 scaled logits, 1 attention probabilities
+  bool hm_prob;          // head_mode 1 with attention probabilities: per-head scores throughout
   int NL;                // lists per stream
+  int NLs;               // sampled lists per stream: NL, or L * H_q when hm_prob (one per head)
   int ncol;              // MFMA output columns used per item (G or 1)
   int ngs;               // KV-head sets per layer: H_kv (head_mode 0) or 1
   int top_k, n_select, pool, pool_mult;
@@ -92,7 +95,12 @@ struct RetrievePlan {
   uint32_t* qB;          // [S][L][H_kv][2][d/32][64] uint4
   uint32_t* tau;         // [S*NL]
   uint32_t* cnt;         // [S*NL]
-  float* samp;           // [S*NL][m_max]
+  float* samp;           // [S*NLs][m_max]
+  uint64_t* below;       // score_mode 1: fixed-point sums of exp over the rows below each cut-off,
+                         // [S*NL] (head mode 0) or [S*L*H_q] (hm_prob)
+  float* lhat;           // hm_prob: [S*L*H_q] sample estimates of each head's log-sum-exp
+  float* cand_sc;        // hm_prob: [S*NL][cap][H_q] per-head scores of the candidates
+  uint32_t* left_max;    // hm_prob: [S*NL] largest estimate among the rows the streaming pass left out
   uint64_t* cand;        // [S*NL][cap]
   float* qcol;           // [S][L][H_kv][16] L1 norms of the scaled query columns
   int32_t* sexp;         // [S] fixed-point exponent of each stream's attention mass

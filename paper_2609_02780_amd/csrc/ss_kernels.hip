@@ -62,6 +62,8 @@ constexpr int kVoteLds = 4096;      // frames whose votes/mass live in LDS
 constexpr int kPoolSort = 4096;     // records per pool sorting round
 constexpr int kGramLdsPool = 128;   // pools up to this size keep their Gram matrix in LDS
 constexpr int kMaxDescDim = 1024;
+constexpr int kProbMassExp = 50;    // fixed-point exponent of attention-probability masses
+constexpr int kBelowExp = 40;       // fixed-point exponent of the exp sums below a cut-off
 
 // ---------------------------------------------------------------------------
 // Small device helpers
@@ -536,6 +538,10 @@ struct ScoreArgs {
   int samp_stride;
   int64_t samp_step[kMaxStreams];     // n 2^32 / m: sample u sits at row (u step + step/2) >> 32
   // K_STREAM
+  int score_mode;                      // 1: attention probabilities (exp sums below each cut-off)
+  uint64_t* below;                     // fixed-point sums of exp below each cut-off
+  const float* lhat;                   // hm_prob: log-sum-exp estimate of each (stream, layer, head)
+  uint32_t* left_max;                  // hm_prob: largest alpha_hat per list among the rows left out
   const uint32_t* tau;
   uint32_t* cnt;
   uint64_t* cand;
@@ -635,13 +641,17 @@ __device__ __forceinline__ void stage_flush(const ScoreArgs& a, int list, bool c
 // share one key); invalid columns carry a NaN cut-off, which nothing passes.
 __device__ __forceinline__ void stream_emit(const ScoreArgs& a, int list, bool colv, int col,
                                             float tau_f, int tile_u0, int u1, f32x4 acc, int kg,
-                                            uint64_t* st, int& lc) {
+                                            uint64_t* st, int& lc, double& below, bool prob) {
   bool pass[4];
   int c = 0;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    pass[j] = (tile_u0 + 4 * kg + j < u1) && acc[j] >= tau_f;
+    const bool valid = tile_u0 + 4 * kg + j < u1;
+    pass[j] = valid && acc[j] >= tau_f;
     c += pass[j];
+    // attention probabilities: every row below the cut-off adds exp(s - tau),
+    // in (0, 1), to its list's normaliser
+    if (prob && colv && valid && !pass[j]) below += (double)__expf(acc[j] - tau_f);
   }
   if (__ballot(c > 0) == 0) return;
   // the column's four lanes (lanes col + 16 kg) agree on a slot range, in kg
@@ -661,6 +671,19 @@ __device__ __forceinline__ void stream_emit(const ScoreArgs& a, int list, bool c
     }
   }
   lc += total;
+}
+
+// Adds a (wave, column)'s sum of exp below the cut-off to the list's fixed-point
+// total at the end of a segment visit: the column's four lanes are added in a
+// fixed order, scaled by 2^kBelowExp and rounded, and integer atomics keep the
+// total independent of the order of the visits.  Called by the whole wave.
+__device__ __forceinline__ void below_flush(uint64_t* dst, bool colv, int kg, double& v, double scale) {
+  double x = v;
+  x += __shfl_xor(x, 16);
+  x += __shfl_xor(x, 32);
+  if (kg == 0 && colv && x > 0.0)
+    atomicAdd(reinterpret_cast<unsigned long long*>(dst), (unsigned long long)llrint(ldexp(x * scale, kBelowExp)));
+  v = 0.0;
 }
 
 // Head-mode 0: one KV head per item, its G query heads in the MFMA columns, the
@@ -888,6 +911,8 @@ __global__ __launch_bounds__(256) void k_stream(ScoreArgs a) {
 #pragma unroll
       for (int p = 0; p < PF; ++p) load(t0 + SW * p, V[p]);
       int lc = 0;
+      double bsum = 0.0;
+      const bool prob = a.score_mode != 0;
       for (int t = t0; t < t1; t += SW * PF) {
 #pragma unroll
         for (int p = 0; p < PF; ++p) {
@@ -907,10 +932,11 @@ __global__ __launch_bounds__(256) void k_stream(ScoreArgs a) {
           }
           __builtin_amdgcn_wave_barrier();
           const f32x4 acc = score_hilo<KS>(A, bh, bl);
-          if (tt < t1) stream_emit(a, list, colv, col, tau_f, tt * kTile, n, acc, kg, st, lc);
+          if (tt < t1) stream_emit(a, list, colv, col, tau_f, tt * kTile, n, acc, kg, st, lc, bsum, prob);
         }
       }
       if (__any(lc > 0)) stage_flush(a, list, colv, col, kg, st, lc);
+      if (prob) below_flush(&a.below[list], colv, kg, bsum, 1.0);
     }
   };
   run_range(wave_range(static_end, wave, a.sgroup, a.xcd_weights != 0));
@@ -1217,9 +1243,129 @@ __global__ __launch_bounds__(256) void k_stream_hm(ScoreArgs a) {
         __builtin_amdgcn_wave_barrier();
         hm_accumulate<KS>(A, b, g, v);
       }
-      stream_emit(a, list, colv, col, tau_f, t * kTile, n, hm_finish(v), kg, st, lc);
+      double unused = 0.0;
+      stream_emit(a, list, colv, col, tau_f, t * kTile, n, hm_finish(v), kg, st, lc, unused, false);
     }
     if (__any(lc > 0)) stage_flush(a, list, colv, col, kg, st, lc);
+  }
+}
+
+// Streaming pass, head mode 1 with attention probabilities.  Like k_stream_hm,
+// the segments are (stream, layer) lists and a 16-row tile is read once per KV
+// head; but each head keeps its own logits: the B tiles are head mode 0's (hi
+// and lo, the G query heads of a KV head in the columns), all HK of them in
+// registers for the visit.  Lane (c, kg) turns the logits of head g G + c into
+// e = exp(s - Lhat) (the sample estimate of the head's log-sum-exp), the
+// row's 16 columns and HK heads are summed in a fixed butterfly, and
+// alpha_hat = that sum / H_q.  Rows with alpha_hat >= tau_hat are staged as
+// candidates; every other row adds e / (H_q tau_hat), below 1 for it, to its
+// head's fixed-point sum.  MFMA work per key vector is that of head mode 0.
+template <int D, int HK>
+__global__ __launch_bounds__(256) void k_stream_hp(ScoreArgs a) {
+  constexpr int CPR = D / 8, TCH = 16 * CPR, NI = TCH / kWave, KS = D / 32;
+  __shared__ u32x4 tiles[4][TCH];
+  __shared__ uint64_t stage[4 * kStage];   // column 0 only
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
+  u32x4* lt_ = tiles[wave];
+  uint64_t* st = stage + wave * kStage;
+  const WaveRange wr = wave_range(a.tile_base[a.S], wave, a.sgroup, a.xcd_weights != 0);
+  const int SW = wr.sw;
+  const float inv_h = 1.0f / (float)a.Hq;
+  for (int64_t T = wr.b0; T < wr.b1;) {
+    int s = 0;
+    while (T >= a.tile_base[s + 1]) ++s;
+    const int64_t rem = T - a.tile_base[s];
+    const int nt = a.ntile[s];
+    const int l = (int)(rem / nt);
+    const int tb = (int)(rem - (int64_t)l * nt);
+    const int t1 = (int)min<int64_t>(nt, tb + (wr.b1 - T));
+    const int t0 = first_tile(wr, T, tb);
+    T += t1 - tb;
+    if (t0 >= t1) continue;
+    const int n = a.n[s];
+    const bool colv = col == 0;
+    const int list = s * a.NL + l;
+    const float tau_all = ord_f32(a.tau[list]);
+    const float tau_f = colv ? tau_all : __uint_as_float(0x7FC00000u);   // staging lanes only
+    const double bscale = tau_all > 0.f ? 1.0 / ((double)a.Hq * (double)tau_all) : 0.0;
+    const size_t hb = (size_t)(s * a.L + l) * a.Hq;   // head 0 of the layer
+    u32x4 bh[HK][KS], bl[HK][KS];
+    float lh[HK];
+#pragma unroll
+    for (int g = 0; g < HK; ++g) {
+      const u32x4* qb = a.qB + ((size_t)(s * a.L + l) * HK + g) * (2 * KS * kWave);
+#pragma unroll
+      for (int i = 0; i < KS; ++i) {
+        bh[g][i] = qb[i * kWave + lane];
+        bl[g][i] = qb[(KS + i) * kWave + lane];
+      }
+      lh[g] = col < a.G ? a.lhat[hb + g * a.G + col] : INFINITY;   // exp(s - inf) = 0 in padding columns
+    }
+    const uint16_t* lay = a.keys[s] + (size_t)l * HK * a.stride[s] * D;
+    auto load = [&](int t, int g, u32x4 (&V)[NI]) {
+      const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<uint16_t*>(lay + (size_t)g * a.stride[s] * D), (short)0, n * D * 2, 0x00020000);
+      const uint32_t off = t < t1 ? (uint32_t)t * (TCH * 16) + lane * 16 : 0x80000000u;
+#pragma unroll
+      for (int i = 0; i < NI; ++i) V[i] = __builtin_amdgcn_raw_buffer_load_b128(r, off + i * kWave * 16, 0, kAuxNT);
+    };
+    u32x4 V[NI];
+    load(t0, 0, V);
+    int lc = 0;
+    uint32_t lmax = 0;   // largest alpha_hat left out (ordered bits; 0 below every value)
+    double bsum[HK];
+#pragma unroll
+    for (int g = 0; g < HK; ++g) bsum[g] = 0.0;
+    for (int t = t0; t < t1; t += SW) {
+      float e[HK][4];
+      f32x4 rs = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int g = 0; g < HK; ++g) {
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+          const int q = i * kWave + lane, R = q >> 4, C = q & 15;
+          lt_[R * 16 + (C ^ (R & 15))] = V[i];
+        }
+        __builtin_amdgcn_wave_barrier();
+        if (g + 1 < HK) load(t, g + 1, V);
+        else load(t + SW, 0, V);
+        u32x4 A[KS];
+#pragma unroll
+        for (int i = 0; i < KS; ++i) {
+          const int q = rl * CPR + 4 * i + kg, R = q >> 4, C = q & 15;
+          A[i] = lt_[R * 16 + (C ^ (R & 15))];
+        }
+        __builtin_amdgcn_wave_barrier();
+        const f32x4 acc = score_hilo<KS>(A, bh[g], bl[g]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          e[g][j] = __expf(acc[j] - lh[g]);
+          rs[j] += e[g][j];
+        }
+      }
+      rs = hm_finish(rs);   // every lane of a 16-lane row: the sum over its 16 columns
+      f32x4 al;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) al[j] = rs[j] * inv_h + 0.0f;
+      double unused = 0.0;
+      stream_emit(a, list, colv, col, tau_f, t * kTile, n, al, kg, st, lc, unused, false);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (t * kTile + 4 * kg + j < n && !(al[j] >= tau_all)) {
+          lmax = max(lmax, ord_u32(al[j]));
+#pragma unroll
+          for (int g = 0; g < HK; ++g) bsum[g] += (double)e[g][j];
+        }
+      }
+    }
+    if (__any(lc > 0)) stage_flush(a, list, colv, col, kg, st, lc);
+#pragma unroll
+    for (int g = 0; g < HK; ++g)
+      below_flush(&a.below[hb + min(g * a.G + col, a.Hq - 1)], col < a.G, kg, bsum[g], bscale);
+    for (int o = 32; o > 0; o >>= 1) lmax = max(lmax, (uint32_t)__shfl_xor((int)lmax, o));
+    if (lane == 0 && lmax > 0) atomicMax(&a.left_max[list], lmax);
   }
 }
 
@@ -1360,6 +1506,13 @@ __device__ uint32_t block_select_range(const uint32_t (&v)[N], const bool (&ok)[
 // ---------------------------------------------------------------------------
 struct ListArgs {
   int NL, S, cap, k_max, top_k, hist_f;
+  int score_mode;                          // 1: attention probabilities
+  int hm_prob;                             // head mode 1 with attention probabilities
+  int NLs;                                 // sampled lists per stream (L * H_q when hm_prob)
+  uint64_t* below;                         // score_mode 1: fixed-point exp sums below each cut-off
+  float* lhat;                             // hm_prob: sample log-sum-exp estimate of each (layer, head)
+  float* cand_sc;                          // hm_prob: [S*NL][cap][H_q] per-head candidate scores
+  uint32_t* left_max;                      // hm_prob: [S*NL] largest alpha_hat left out (ordered bits)
   int32_t m[kMaxStreams], r[kMaxStreams], kk[kMaxStreams], n[kMaxStreams];
   int32_t f[kMaxStreams], rpf[kMaxStreams];
   const int32_t* frame_off[kMaxStreams];   // from the first candidate frame; values are absolute rows
@@ -1368,7 +1521,7 @@ struct ListArgs {
   int samp_stride;
   uint32_t* tau;
   uint32_t* cnt;
-  const uint64_t* cand;
+  uint64_t* cand;                          // candidate keys (rewritten with exact values in hm_prob)
   // per-frame votes and fixed-point attention mass of each stream (window-relative frames)
   int f_max;
   int32_t* votes_g;    // [S][f_max]
@@ -1407,6 +1560,12 @@ __device__ __forceinline__ int frame_of_row(const ListArgs& a, int s, uint32_t r
 // Run by wave 0 of the block alone (no block barrier).
 __device__ void stream_exponent(const ListArgs& a, int s) {
   if (threadIdx.x >= kWave) return;
+  if (a.score_mode == 1) {
+    // attention probabilities: a list's selected values add up to at most 1,
+    // so a frame's mass is below NL <= 2^12 and 2^50 keeps every sum below 2^62
+    if (threadIdx.x == 0) a.sexp[s] = kProbMassExp;
+    return;
+  }
   const int L = a.L, Hk = a.Hk;
   const float* qc = a.qcol + (size_t)s * L * Hk * 16;
   float b = 0.f;
@@ -1446,6 +1605,7 @@ __device__ __forceinline__ void thresh_list(const ListArgs& a) {
   const int list = blockIdx.x, s = list / a.NL, ll = list - s * a.NL;
   const int m = a.m[s], r = a.r[s];
   if (threadIdx.x == 0) a.cnt[list] = 0;
+  if (a.below && threadIdx.x == 0) a.below[list] = 0;
   if (list == 0 && threadIdx.x < kDynCtr) a.dyn_ctr[threadIdx.x * kDynStride] = 0;
   {
     int32_t* vg = a.votes_g + (size_t)s * a.f_max;
@@ -1489,6 +1649,99 @@ __global__ __launch_bounds__(1024) void k_thresh(ListArgs a) {
 }
 __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(8, 8))) void k_thresh_dense(ListArgs a) {
   thresh_list(a);
+}
+
+// Sum of a wave's doubles in a fixed butterfly (every lane gets the total).
+__device__ __forceinline__ double wave_sum_f64(double v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ float wave_max_f32(float v) {
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+constexpr int kMaxHeadsHp = 128;   // query heads of a layer in head mode 1 (H_kv <= 8, G <= 16)
+
+// Head mode 1 with attention probabilities: the cut-off of a layer's list from
+// its sample.  Each head h gets an estimate of its log-sum-exp over the list,
+// Lhat_h = log((n / m) sum over the sample of exp(s_h)) (one wave per head:
+// the sample maximum first, then the shifted sum in a fixed order); then each
+// sampled row's estimated attention alpha_hat = mean_h exp(s_h - Lhat_h) and
+// the cut-off tau_hat = the r-th largest alpha_hat.  The streaming pass keeps
+// the rows with alpha_hat >= tau_hat, and k_select proves from the exact
+// normalisers that no other row can reach its top k (else it recomputes the
+// list).  The block also clears the list's exp sums and the stream's frame
+// accumulators.
+__global__ __launch_bounds__(1024) void k_thresh_hp(ListArgs a) {
+  __shared__ uint32_t hist[kSelHist];
+  __shared__ uint32_t res[4];
+  __shared__ uint32_t mm[32];
+  __shared__ float lh[kMaxHeadsHp];
+  const int list = blockIdx.x, s = list / a.NL, l = list - s * a.NL;
+  const int m = a.m[s], r = a.r[s], Hq = a.Hq;
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const size_t hbase = (size_t)s * a.NLs + (size_t)l * Hq;   // sampled list of head 0 of the layer
+  if (threadIdx.x == 0) {
+    a.cnt[list] = 0;
+    a.left_max[list] = 0;
+  }
+  for (int h = threadIdx.x; h < Hq; h += blockDim.x) a.below[hbase + h] = 0;
+  if (list == 0 && threadIdx.x < kDynCtr) a.dyn_ctr[threadIdx.x * kDynStride] = 0;
+  {
+    int32_t* vg = a.votes_g + (size_t)s * a.f_max;
+    int64_t* mg = a.massfx_g + (size_t)s * a.f_max;
+    for (int f = l * 1024 + threadIdx.x; f < a.f[s]; f += a.NL * 1024) {
+      vg[f] = 0;
+      mg[f] = 0;
+    }
+  }
+  if (l == 0) stream_exponent(a, s);
+  if (m == 0 || r == 0) {
+    if (threadIdx.x == 0) a.tau[list] = 0xFFFFFFFFu;
+    return;
+  }
+  const float log_nm = logf((float)a.n[s] / (float)m);
+  for (int h = wave; h < Hq; h += nw) {
+    const float* v = a.samp + (hbase + h) * a.samp_stride;
+    float mx = -INFINITY;
+    for (int u = lane; u < m; u += kWave) mx = fmaxf(mx, v[u]);
+    mx = wave_max_f32(mx);
+    double sm = 0.0;
+    for (int u = lane; u < m; u += kWave) sm += (double)__expf(v[u] - mx);
+    sm = wave_sum_f64(sm);
+    if (lane == 0) {
+      lh[h] = mx + (float)log(sm) + log_nm;
+      a.lhat[hbase + h] = lh[h];
+    }
+  }
+  __syncthreads();
+  float al[kThrItems];
+#pragma unroll
+  for (int it = 0; it < kThrItems; ++it) al[it] = 0.f;
+  for (int h = 0; h < Hq; ++h) {
+    const float* v = a.samp + (hbase + h) * a.samp_stride;
+    const float L = lh[h];
+#pragma unroll
+    for (int it = 0; it < kThrItems; ++it) {
+      const int u = (int)threadIdx.x + it * 1024;
+      if (u < m) al[it] += __expf(v[u] - L);
+    }
+  }
+  uint32_t x[kThrItems];
+  bool ok[kThrItems];
+  uint32_t mn = 0xFFFFFFFFu, mx = 0;
+  const float inv_h = 1.0f / (float)Hq;
+#pragma unroll
+  for (int it = 0; it < kThrItems; ++it) {
+    ok[it] = (int)threadIdx.x + it * 1024 < m;
+    x[it] = ok[it] ? ord_u32(al[it] * inv_h + 0.0f) : 0u;
+    if (ok[it]) { mn = min(mn, x[it]); mx = max(mx, x[it]); }
+  }
+  block_minmax_u32(mn, mx, mm);
+  uint32_t ng, ne;
+  const uint32_t t = block_select_range<kThrItems, true>(x, ok, mn, mx, (uint32_t)r, hist, res, ng, ne);
+  if (threadIdx.x == 0) a.tau[list] = t;
 }
 
 // ---------------------------------------------------------------------------
@@ -1550,75 +1803,21 @@ __device__ void finish_list(const ListArgs& a, int list, uint64_t* sel, int kk,
 }
 
 // Exact fallback for a list whose candidate count left [k, capacity]: the
-// block selects from every score of the list, recomputed in each of its passes
+// block selects from every value of the list, recomputed in each of its passes
 // with the streaming pass's arithmetic (the same bits), so nothing is stored
-// per row.  A pass scores 1,024 rows at a time (four tiles per wave) into LDS.
-// Three radix rounds of 11, 11 and 10 bits over the ordered scores find the
-// k-th largest value v* (a round whose bin is taken whole ends the search
+// per row.  A pass fills `chunk` with the values of 1,024 rows (four tiles per
+// wave).  Three radix rounds of 11, 11 and 10 bits over the ordered values find
+// the k-th largest value v* (a round whose bin is taken whole ends the search
 // early: every row at or above that bin is selected); a last pass takes the
 // rows above v* and, in row order, the rows equal to it that are still needed.
 constexpr int kFbTilesPerWave = 4;
 constexpr int kFbRows = 16 * kFbTilesPerWave * kTile;   // rows per pass of a 1024-thread block
 
-template <int D>
-__device__ void fallback_list(const ListArgs& a, int list, uint64_t* sel, int32_t* lv, long long* lm,
-                              uint32_t* res) {
-  constexpr int KS = D / 32;
-  __shared__ float chunk[kFbRows];
+template <class Chunk>
+__device__ void fallback_select_rows(int n, int kk, Chunk score_chunk, const float* chunk, uint64_t* sel,
+                                     uint32_t* hist, uint32_t* res) {
   __shared__ uint32_t ngt_sh;
   __shared__ int scan_sh[17];
-  const int s = list / a.NL, ll = list - s * a.NL;
-  const int kk = a.kk[s], n = a.n[s];
-  int l, g0, ng, col;
-  if (a.head_mode == 0) {
-    l = ll / a.Hq;
-    const int h = ll - l * a.Hq;
-    g0 = h / a.G;
-    col = h - g0 * a.G;
-    ng = 1;
-  } else {
-    l = ll;
-    g0 = 0;
-    col = 0;
-    ng = a.Hk;
-  }
-  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
-  const int kg = lane >> 4, rl = lane & 15;
-  const size_t gstride = (size_t)a.stride[s] * D;
-  u32x4 bh[KS], bl[KS];
-  if (a.head_mode == 0) {
-    const u32x4* qb = a.qB + ((size_t)(s * a.L + l) * a.Hk + g0) * (2 * KS * kWave);
-#pragma unroll
-    for (int i = 0; i < KS; ++i) {
-      bh[i] = qb[i * kWave + lane];
-      bl[i] = qb[(KS + i) * kWave + lane];
-    }
-  } else {
-    hm_load_b<KS>(a.qB + (size_t)(s * a.L + l) * a.Hk * (2 * KS * kWave), a.Hk, bh);
-  }
-  // chunk[r - c0] = score of row r for rows [c0, c0 + kFbRows) below n
-  auto score_chunk = [&](int c0) {
-#pragma unroll
-    for (int q = 0; q < kFbTilesPerWave; ++q) {
-      const int tl = wave * kFbTilesPerWave + q;        // tile of the chunk
-      const int row = c0 + tl * kTile + rl;
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-      for (int g = g0; g < g0 + ng; ++g) {
-        const uint16_t* p = a.keys[s] + ((size_t)l * a.Hk + g) * gstride + (size_t)(row < n ? row : 0) * D + 8 * kg;
-        u32x4 A[KS];
-#pragma unroll
-        for (int i = 0; i < KS; ++i) A[i] = row < n ? ld_nt(p + 32 * i) : u32x4{0, 0, 0, 0};
-        if (a.head_mode == 0) acc = score_hilo<KS>(A, bh, bl);
-        else hm_accumulate<KS>(A, bh, g, acc);   // acc gathers the per-head results
-      }
-      if (a.head_mode == 1) acc = hm_finish(acc);
-      if ((lane & 15) == col) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) chunk[tl * kTile + 4 * kg + j] = acc[j] + 0.0f;
-      }
-    }
-  };
-  uint32_t* hist = reinterpret_cast<uint32_t*>(lv);   // 2048 bins; lv is free until finish_list
   uint32_t prefix = 0, mask = 0, need = (uint32_t)kk;
   bool whole = false;
   for (int rd = 0; rd < 3 && !whole; ++rd) {
@@ -1672,6 +1871,335 @@ __device__ void fallback_list(const ListArgs& a, int list, uint64_t* sel, int32_
     eq_taken += tot;
   }
   __syncthreads();
+}
+
+// Rewrites selected composite keys from logits to attention probabilities
+// exp(s - lse) (a list keeps its order).  Ends with a barrier.
+__device__ void to_probabilities(uint64_t* sel, int kk, float lse) {
+  __syncthreads();
+  for (int e = threadIdx.x; e < kk; e += blockDim.x) {
+    const uint64_t k = sel[e];
+    sel[e] = mk_key(ord_u32(__expf(key_score(k) - lse) + 0.0f), key_row(k));
+  }
+  __syncthreads();
+}
+
+__device__ __forceinline__ unsigned long long wave_sum_u64(unsigned long long v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+template <int D>
+__device__ void fallback_list(const ListArgs& a, int list, uint64_t* sel, int32_t* lv, long long* lm,
+                              uint32_t* res) {
+  constexpr int KS = D / 32;
+  __shared__ float chunk[kFbRows];
+  __shared__ uint32_t max_sh;
+  __shared__ unsigned long long sum_sh;
+  const int s = list / a.NL, ll = list - s * a.NL;
+  const int kk = a.kk[s], n = a.n[s];
+  int l, g0, ng, col;
+  if (a.head_mode == 0) {
+    l = ll / a.Hq;
+    const int h = ll - l * a.Hq;
+    g0 = h / a.G;
+    col = h - g0 * a.G;
+    ng = 1;
+  } else {
+    l = ll;
+    g0 = 0;
+    col = 0;
+    ng = a.Hk;
+  }
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
+  const int kg = lane >> 4, rl = lane & 15;
+  const size_t gstride = (size_t)a.stride[s] * D;
+  u32x4 bh[KS], bl[KS];
+  if (a.head_mode == 0) {
+    const u32x4* qb = a.qB + ((size_t)(s * a.L + l) * a.Hk + g0) * (2 * KS * kWave);
+#pragma unroll
+    for (int i = 0; i < KS; ++i) {
+      bh[i] = qb[i * kWave + lane];
+      bl[i] = qb[(KS + i) * kWave + lane];
+    }
+  } else {
+    hm_load_b<KS>(a.qB + (size_t)(s * a.L + l) * a.Hk * (2 * KS * kWave), a.Hk, bh);
+  }
+  // chunk[r - c0] = score of row r for rows [c0, c0 + kFbRows) below n
+  auto score_chunk = [&](int c0) {
+#pragma unroll
+    for (int q = 0; q < kFbTilesPerWave; ++q) {
+      const int tl = wave * kFbTilesPerWave + q;        // tile of the chunk
+      const int row = c0 + tl * kTile + rl;
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      for (int g = g0; g < g0 + ng; ++g) {
+        const uint16_t* p = a.keys[s] + ((size_t)l * a.Hk + g) * gstride + (size_t)(row < n ? row : 0) * D + 8 * kg;
+        u32x4 A[KS];
+#pragma unroll
+        for (int i = 0; i < KS; ++i) A[i] = row < n ? ld_nt(p + 32 * i) : u32x4{0, 0, 0, 0};
+        if (a.head_mode == 0) acc = score_hilo<KS>(A, bh, bl);
+        else hm_accumulate<KS>(A, bh, g, acc);   // acc gathers the per-head results
+      }
+      if (a.head_mode == 1) acc = hm_finish(acc);
+      if ((lane & 15) == col) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) chunk[tl * kTile + 4 * kg + j] = acc[j] + 0.0f;
+      }
+    }
+  };
+  uint32_t* hist = reinterpret_cast<uint32_t*>(lv);   // 2048 bins; lv is free until finish_list
+  fallback_select_rows(n, kk, score_chunk, chunk, sel, hist, res);
+  if (a.score_mode == 1) {
+    // head mode 0, attention probabilities: the list's exact log-sum-exp over
+    // all its rows (the maximum, then the exp sum in fixed point), then the
+    // selected rows' probabilities
+    if (threadIdx.x == 0) { max_sh = 0; sum_sh = 0; }
+    __syncthreads();
+    uint32_t mx = 0;
+    for (int c0 = 0; c0 < n; c0 += kFbRows) {
+      score_chunk(c0);
+      __syncthreads();
+      if (c0 + (int)threadIdx.x < n) mx = max(mx, ord_u32(chunk[threadIdx.x]));
+      __syncthreads();
+    }
+    atomicMax(&max_sh, mx);
+    __syncthreads();
+    const float M = ord_f32(max_sh);
+    double sm = 0.0;
+    for (int c0 = 0; c0 < n; c0 += kFbRows) {
+      score_chunk(c0);
+      __syncthreads();
+      if (c0 + (int)threadIdx.x < n) sm += (double)__expf(chunk[threadIdx.x] - M);
+      __syncthreads();
+    }
+    atomicAdd(&sum_sh, (unsigned long long)llrint(ldexp(sm, kBelowExp)));
+    __syncthreads();
+    to_probabilities(sel, kk, M + (float)log(ldexp((double)sum_sh, -kBelowExp)));
+  }
+  finish_list(a, list, sel, kk, lv, lm);
+}
+
+// Head mode 0, attention probabilities: the log-sum-exp of a list over all its
+// candidate rows.  The candidates (every row at or above the cut-off tau) are
+// summed here in fixed point against M = max(tau, their largest logit); the
+// streaming pass summed exp(s - tau) over the rows below tau.
+__device__ float lse_from_candidates(const ListArgs& a, int list, const uint64_t* src, int n, uint32_t* mm) {
+  __shared__ unsigned long long fx_sh;
+  const float tau = ord_f32(a.tau[list]);
+  uint32_t mn = 0xFFFFFFFFu, mx = ord_u32(tau + 0.0f);
+  for (int i = threadIdx.x; i < n; i += blockDim.x) mx = max(mx, (uint32_t)(src[i] >> 32));
+  block_minmax_u32(mn, mx, mm);
+  const float M = ord_f32(mx);
+  if (threadIdx.x == 0) fx_sh = 0;
+  __syncthreads();
+  unsigned long long part = 0;
+  for (int i = threadIdx.x; i < n; i += blockDim.x)
+    part += (unsigned long long)llrint(ldexp((double)__expf(key_score(src[i]) - M), kBelowExp));
+  if (part) atomicAdd(&fx_sh, part);
+  __syncthreads();
+  const double z = ldexp((double)fx_sh, -kBelowExp) +
+                   ldexp((double)a.below[list], -kBelowExp) * exp((double)tau - (double)M);
+  return M + (float)log(z);
+}
+
+// Head mode 1, attention probabilities.  Every candidate's per-head logits,
+// recomputed with the streaming pass's arithmetic (16 candidate rows per wave
+// step, each KV head's rows against the head-mode-0 B tiles), into cand_sc;
+// each head's exact log-sum-exp lse_h over the list: the candidates summed
+// here in fixed point against M_h = max(Lhat_h, their largest logit), plus the
+// streaming pass's sum over the rows it left out (each of those added
+// exp(s - Lhat_h) / (H_q tau_hat)); then each candidate's exact alpha =
+// mean_h exp(s_h - lse_h), written into its composite key.  Returns rho =
+// max_h exp(Lhat_h - lse_h): a left-out row's alpha is at most rho times its
+// estimate.  Ends with a barrier.
+template <int D>
+__device__ float hp_candidate_values(const ListArgs& a, int list, int n) {
+  constexpr int KS = D / 32;
+  __shared__ float lse_sh[kMaxHeadsHp];
+  __shared__ uint32_t rho_sh;
+  const int s = list / a.NL, l = list - s * a.NL;
+  const int Hq = a.Hq, G = a.G, Hk = a.Hk;
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const int kg = lane >> 4, rl = lane & 15, col = lane & 15;
+  uint64_t* src = a.cand + (size_t)list * a.cap;
+  float* cs = a.cand_sc + (size_t)list * a.cap * Hq;
+  const size_t gstride = (size_t)a.stride[s] * D;
+  const size_t hb = (size_t)(s * a.L + l) * Hq;
+  for (int i0 = wave * kTile; i0 < n; i0 += nw * kTile) {
+    const int i = i0 + rl;
+    const uint32_t row = i < n ? key_row(src[i]) : 0u;
+    for (int g = 0; g < Hk; ++g) {
+      const u32x4* qb = a.qB + ((size_t)(s * a.L + l) * Hk + g) * (2 * KS * kWave);
+      const uint16_t* p = a.keys[s] + ((size_t)l * Hk + g) * gstride + (size_t)row * D + 8 * kg;
+      u32x4 bh[KS], bl[KS], A[KS];
+#pragma unroll
+      for (int ii = 0; ii < KS; ++ii) {
+        bh[ii] = qb[ii * kWave + lane];
+        bl[ii] = qb[(KS + ii) * kWave + lane];
+        A[ii] = i < n ? ld_nt(p + 32 * ii) : u32x4{0, 0, 0, 0};
+      }
+      const f32x4 acc = score_hilo<KS>(A, bh, bl);
+      if (col < G) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int ic = i0 + 4 * kg + j;
+          if (ic < n) cs[(size_t)ic * Hq + g * G + col] = acc[j] + 0.0f;
+        }
+      }
+    }
+  }
+  if (threadIdx.x == 0) rho_sh = 0;
+  __threadfence_block();
+  __syncthreads();
+  const float tau = ord_f32(a.tau[list]);
+  for (int h = wave; h < Hq; h += nw) {
+    const float Lh = a.lhat[hb + h];
+    float mx = -INFINITY;
+    for (int i = lane; i < n; i += kWave) mx = fmaxf(mx, cs[(size_t)i * Hq + h]);
+    const float M = fmaxf(wave_max_f32(mx), Lh);
+    unsigned long long fx = 0;
+    for (int i = lane; i < n; i += kWave)
+      fx += (unsigned long long)llrint(ldexp((double)__expf(cs[(size_t)i * Hq + h] - M), kBelowExp));
+    fx = wave_sum_u64(fx);
+    if (lane == 0) {
+      const double left_out = ldexp((double)a.below[hb + h], -kBelowExp) * (double)Hq * (double)tau;
+      const double z = ldexp((double)fx, -kBelowExp) + left_out * exp((double)Lh - (double)M);
+      const float lse = M + (float)log(z);
+      lse_sh[h] = lse;
+      atomicMax(&rho_sh, ord_u32(expf(Lh - lse)));   // positive values: the order of the floats
+    }
+  }
+  __syncthreads();
+  const float inv_h = 1.0f / (float)Hq;
+  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+    float al = 0.f;
+    for (int h = 0; h < Hq; ++h) al += __expf(cs[(size_t)i * Hq + h] - lse_sh[h]);
+    src[i] = mk_key(ord_u32(al * inv_h + 0.0f), key_row(src[i]));
+  }
+  __threadfence_block();
+  __syncthreads();
+  return ord_f32(rho_sh);
+}
+
+// The head-mode-1 probability selection is exact when its k-th largest value
+// exceeds rho times the largest estimate alpha_hat among the rows the streaming
+// pass left out (with 1e-4 of margin for the fp32 error of alpha and of its
+// estimate): such a row's exact alpha is at most rho alpha_hat.  Trivially so
+// when no row was left out.
+__device__ bool hp_selection_proven(const ListArgs& a, int list, const uint64_t* sel, int kk, float rho,
+                                    uint32_t* mm) {
+  uint32_t mn = 0xFFFFFFFFu, mx = 0;
+  for (int e = threadIdx.x; e < kk; e += blockDim.x) mn = min(mn, (uint32_t)(sel[e] >> 32));
+  block_minmax_u32(mn, mx, mm);
+  const uint32_t lm = a.left_max[list];
+  if (lm == 0) return true;
+  return ord_f32(mn) > ord_f32(lm) * rho * 1.0001f;
+}
+
+// Head mode 1 with attention probabilities, exact over every row of the list
+// (when the candidate count left [k, capacity] or the selection could not be
+// proven).  Pass 1 takes each head's largest logit, pass 2 its exp sum against
+// it (fixed point, so the order of the additions does not matter): the exact
+// lse_h.  The rows are then selected by alpha = mean_h exp(s_h - lse_h) with
+// the radix rounds above, every pass recomputing the logits with the streaming
+// pass's arithmetic.
+template <int D>
+__device__ void fallback_list_hp(const ListArgs& a, int list, uint64_t* sel, int32_t* lv, long long* lm,
+                                 uint32_t* res) {
+  constexpr int KS = D / 32;
+  constexpr int kHkMax = 8;
+  __shared__ float chunk[kFbRows];
+  __shared__ uint32_t hmax[kMaxHeadsHp];
+  __shared__ unsigned long long hsum[kMaxHeadsHp];
+  __shared__ float lse_sh[kMaxHeadsHp];
+  const int s = list / a.NL, l = list - s * a.NL;
+  const int kk = a.kk[s], n = a.n[s], Hq = a.Hq, G = a.G, Hk = a.Hk;
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
+  const int kg = lane >> 4, rl = lane & 15, col = lane & 15;
+  const size_t gstride = (size_t)a.stride[s] * D;
+  // logits of KV head g for tile t: lane (c, kg) gets head g G + c, rows 16 t + 4 kg + j
+  auto tile_logits = [&](int t, int g) -> f32x4 {
+    const int row = t * kTile + rl;
+    const u32x4* qb = a.qB + ((size_t)(s * a.L + l) * Hk + g) * (2 * KS * kWave);
+    const uint16_t* p = a.keys[s] + ((size_t)l * Hk + g) * gstride + (size_t)(row < n ? row : 0) * D + 8 * kg;
+    u32x4 bh[KS], bl[KS], A[KS];
+#pragma unroll
+    for (int i = 0; i < KS; ++i) {
+      bh[i] = qb[i * kWave + lane];
+      bl[i] = qb[(KS + i) * kWave + lane];
+      A[i] = row < n ? ld_nt(p + 32 * i) : u32x4{0, 0, 0, 0};
+    }
+    return score_hilo<KS>(A, bh, bl);
+  };
+  for (int h = threadIdx.x; h < Hq; h += blockDim.x) { hmax[h] = 0; hsum[h] = 0; }
+  __syncthreads();
+  // pass 1: every head's largest logit
+  float mx[kHkMax];
+  double sm[kHkMax];
+#pragma unroll
+  for (int g = 0; g < kHkMax; ++g) { mx[g] = -INFINITY; sm[g] = 0.0; }
+  const int ntile = (n + kTile - 1) / kTile;
+  for (int t = wave; t < ntile; t += blockDim.x / kWave) {
+#pragma unroll
+    for (int g = 0; g < kHkMax; ++g) {
+      if (g < Hk) {
+        const f32x4 acc = tile_logits(t, g);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (t * kTile + 4 * kg + j < n) mx[g] = fmaxf(mx[g], acc[j]);
+      }
+    }
+  }
+#pragma unroll
+  for (int g = 0; g < kHkMax; ++g)
+    if (g < Hk && col < G && mx[g] > -INFINITY) atomicMax(&hmax[g * G + col], ord_u32(mx[g]));
+  __syncthreads();
+  // pass 2: every head's exp sum against its maximum
+  for (int t = wave; t < ntile; t += blockDim.x / kWave) {
+#pragma unroll
+    for (int g = 0; g < kHkMax; ++g) {
+      if (g < Hk) {   // uniform: the whole wave issues the loads and MFMAs
+        const f32x4 acc = tile_logits(t, g);
+        if (col < G) {
+          const float M = ord_f32(hmax[g * G + col]);
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            if (t * kTile + 4 * kg + j < n) sm[g] += (double)__expf(acc[j] - M);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int g = 0; g < kHkMax; ++g)
+    if (g < Hk && col < G && sm[g] > 0.0)
+      atomicAdd(&hsum[g * G + col], (unsigned long long)llrint(ldexp(sm[g], kBelowExp)));
+  __syncthreads();
+  for (int h = threadIdx.x; h < Hq; h += blockDim.x)
+    lse_sh[h] = ord_f32(hmax[h]) + (float)log(ldexp((double)hsum[h], -kBelowExp));
+  __syncthreads();
+  const float inv_h = 1.0f / (float)Hq;
+  // chunk[r - c0] = alpha of row r for rows [c0, c0 + kFbRows) below n
+  auto alpha_chunk = [&](int c0) {
+#pragma unroll
+    for (int q = 0; q < kFbTilesPerWave; ++q) {
+      const int tl = wave * kFbTilesPerWave + q;
+      const int t = c0 / kTile + tl;
+      f32x4 rs = {0.f, 0.f, 0.f, 0.f};
+      for (int g = 0; g < Hk; ++g) {
+        const f32x4 acc = tile_logits(t, g);
+        const float L = col < G ? lse_sh[g * G + col] : INFINITY;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) rs[j] += __expf(acc[j] - L);
+      }
+      rs = hm_finish(rs);
+      if (col == 0) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) chunk[tl * kTile + 4 * kg + j] = rs[j] * inv_h + 0.0f;
+      }
+    }
+  };
+  uint32_t* hist = reinterpret_cast<uint32_t*>(lv);
+  fallback_select_rows(n, kk, alpha_chunk, chunk, sel, hist, res);
   finish_list(a, list, sel, kk, lv, lm);
 }
 
@@ -1682,30 +2210,12 @@ struct SelectShared {
   long long lm[kVoteLds];
 };
 
-template <int D>
-__device__ void select_list(const ListArgs& a, int list, SelectShared& sh, uint32_t* hist, uint32_t* res,
-                            uint32_t& ngather, uint32_t* mm) {
-  uint64_t* sel = sh.sel;
-  int32_t* lv = sh.lv;
-  long long* lm = sh.lm;
-  const int s = list / a.NL;
-  const int kk = a.kk[s];
-  if (kk == 0) {
-    finish_list(a, list, sel, 0, lv, lm);
-    return;
-  }
-  const uint32_t c = a.cnt[list];
-  const bool fallback = c < (uint32_t)kk || c > (uint32_t)a.cap;
-  if (a.dbg_stats && threadIdx.x == 0) {
-    a.dbg_stats[2 * list] = (int32_t)min(c, (uint32_t)INT_MAX);
-    a.dbg_stats[2 * list + 1] = fallback ? 1 : 0;
-  }
-  if (fallback) {
-    fallback_list<D>(a, list, sel, lv, lm, res);
-    return;
-  }
-  const int n = (int)c;
-  const uint64_t* src = a.cand + (size_t)list * a.cap;
+// Exact top-kk of a list's n candidate keys (composite: value, then row) into
+// `sel`, in any order: the values (high halves) and inverted rows in
+// registers for up to 8,192 candidates, else a radix selection over the keys
+// in global memory.  Ends with a barrier.
+__device__ void select_candidates(const uint64_t* src, int n, int kk, uint64_t* sel, uint32_t* hist,
+                                  uint32_t* res, uint32_t& ngather, uint32_t* mm) {
   if (threadIdx.x == 0) ngather = 0;
   if (n <= 1024 * kSelItems) {
     // scores (high halves) and inverted rows in registers: the k-th score, then
@@ -1759,6 +2269,49 @@ __device__ void select_list(const ListArgs& a, int list, SelectShared& sh, uint3
     }
   }
   __syncthreads();
+}
+
+// HP: head mode 1 with attention probabilities (its own kernel, so that the
+// registers and LDS of its paths stay out of the other modes' selection).
+template <int D, bool HP>
+__device__ void select_list(const ListArgs& a, int list, SelectShared& sh, uint32_t* hist, uint32_t* res,
+                            uint32_t& ngather, uint32_t* mm) {
+  uint64_t* sel = sh.sel;
+  int32_t* lv = sh.lv;
+  long long* lm = sh.lm;
+  const int s = list / a.NL;
+  const int kk = a.kk[s];
+  if (kk == 0) {
+    finish_list(a, list, sel, 0, lv, lm);
+    return;
+  }
+  const uint32_t c = a.cnt[list];
+  int fallback = (c < (uint32_t)kk || c > (uint32_t)a.cap) ? 1 : 0;
+  uint64_t* src = a.cand + (size_t)list * a.cap;
+  float rho = 0.f;
+  if (HP && !fallback) rho = hp_candidate_values<D>(a, list, (int)c);
+  if (!fallback) {
+    select_candidates(src, (int)c, kk, sel, hist, res, ngather, mm);
+    // head mode 1, attention probabilities: the selection is exact when its
+    // k-th value beats every row the streaming pass left out (fallback 2)
+    if (HP && !hp_selection_proven(a, list, sel, kk, rho, mm)) fallback = 2;
+  }
+  if (a.dbg_stats && threadIdx.x == 0) {
+    a.dbg_stats[2 * list] = (int32_t)min(c, (uint32_t)INT_MAX);
+    a.dbg_stats[2 * list + 1] = fallback;
+  }
+  if (fallback) {
+    if (HP) fallback_list_hp<D>(a, list, sel, lv, lm, res);
+    else fallback_list<D>(a, list, sel, lv, lm, res);
+    return;
+  }
+  if (!HP && a.score_mode == 1) {
+    // head mode 0: the lists are those of the logits; the normaliser of the
+    // list is the candidates' exp sum plus the streaming pass's sum below the
+    // cut-off, and the selected rows carry their probabilities from here on
+    const float lse = lse_from_candidates(a, list, src, (int)c, mm);
+    to_probabilities(sel, kk, lse);
+  }
   finish_list(a, list, sel, kk, lv, lm);
 }
 
@@ -1988,7 +2541,18 @@ __global__ __launch_bounds__(1024) void k_select(ListArgs a) {
   __shared__ uint32_t res[4];
   __shared__ uint32_t ngather;
   __shared__ uint32_t mm[32];
-  select_list<D>(a, blockIdx.x, sh, hist, res, ngather, mm);
+  select_list<D, false>(a, blockIdx.x, sh, hist, res, ngather, mm);
+}
+
+// The same for head mode 1 with attention probabilities.
+template <int D>
+__global__ __launch_bounds__(1024) void k_select_hp(ListArgs a) {
+  __shared__ SelectShared sh;
+  __shared__ uint32_t hist[512];
+  __shared__ uint32_t res[4];
+  __shared__ uint32_t ngather;
+  __shared__ uint32_t mm[32];
+  select_list<D, true>(a, blockIdx.x, sh, hist, res, ngather, mm);
 }
 
 // One block per stream: the pool.
@@ -3287,7 +3851,8 @@ constexpr int kStreamBlocksPerCU = 2;
 // same value, and no call reads a half-written one).
 constexpr int kMaxDevices = 64;
 
-template <int D, bool HM>
+// KIND 0: k_stream, 1: k_stream_hm, 2: k_stream_hp<D, HK>.
+template <int D, int KIND, int HK = 1>
 int stream_grid() {
   static std::atomic<int> cache[kMaxDevices];
   int dev = 0;
@@ -3297,8 +3862,10 @@ int stream_grid() {
   if (grid == 0) {
     int cus = 256, per_cu = 0;
     (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, HM ? k_stream_hm<D> : k_stream<D>, 256, 0) != hipSuccess ||
-        per_cu < 1)
+    const void* fn = KIND == 0 ? reinterpret_cast<const void*>(k_stream<D>)
+                     : KIND == 1 ? reinterpret_cast<const void*>(k_stream_hm<D>)
+                                 : reinterpret_cast<const void*>(k_stream_hp<D, HK>);
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 256, 0) != hipSuccess || per_cu < 1)
       per_cu = 1;
     grid = std::min(per_cu, kStreamBlocksPerCU) * std::max(cus, 1);
     slot.store(grid, std::memory_order_relaxed);
@@ -3322,6 +3889,31 @@ void launch_score(const ScoreArgs& a, int head_mode, int max_grid, hipStream_t s
   else hipLaunchKernelGGL((k_score_hm<D, KIND>), dim3(grid), dim3(256), 0, st, a);
 }
 
+// The head-mode-1 probability streaming pass for the layer's KV-head count
+// (H_kv * d <= 512: every B tile stays in registers).
+template <int D, int HK>
+void launch_stream_hp_hk(ScoreArgs a, const RetrievePlan& p, int64_t tiles, int cus, hipStream_t st) {
+  const int grid = (int)std::min<int64_t>(stream_grid<D, 2, HK>(), std::max<int64_t>(1, tiles / 16));
+  int nseg = 0;   // (stream, layer) segments with rows
+  for (int s = 0; s < p.S; ++s) nseg += a.ntile[s] > 0 ? p.L : 0;
+  a.sgroup = stream_group(grid, nseg);
+  a.xcd_weights = cus == 256;
+  hipLaunchKernelGGL((k_stream_hp<D, HK>), dim3(grid), dim3(256), 0, st, a);
+}
+
+template <int D>
+hipError_t launch_stream_hp(const ScoreArgs& a, const RetrievePlan& p, int64_t tiles, int cus, hipStream_t st) {
+  switch (p.Hk) {
+    case 1: launch_stream_hp_hk<D, 1>(a, p, tiles, cus, st); return hipSuccess;
+    case 2: launch_stream_hp_hk<D, 2>(a, p, tiles, cus, st); return hipSuccess;
+    case 4: launch_stream_hp_hk<D, 4>(a, p, tiles, cus, st); return hipSuccess;
+    case 8:
+      if (D * 8 <= 512) { launch_stream_hp_hk<D, (D * 8 <= 512 ? 8 : 4)>(a, p, tiles, cus, st); return hipSuccess; }
+      return hipErrorInvalidValue;
+    default: return hipErrorInvalidValue;
+  }
+}
+
 template <int D>
 hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   // 1. query prep, fused with 2., the sample scores, in k_prep_sample (head
@@ -3340,11 +3932,14 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   ps.blk_base[p.S] = ps_blocks;
   int cus = 256, dev = 0;
   if (hipGetDevice(&dev) == hipSuccess) (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-  const bool fused = p.head_mode == 0 && pairs <= 128 && ps_blocks <= cus;
+  // head mode 1 with attention probabilities keeps every head's logits: its
+  // prep and sample are head mode 0's (one sampled list per head)
+  const int prep_hm = p.hm_prob ? 0 : p.head_mode;
+  const bool fused = prep_hm == 0 && pairs <= 128 && ps_blocks <= cus;
   PrepArgs pa_fused{};
   for (int first = 0; first < pairs; first += 128) {
     PrepArgs a{};
-    a.Hq = p.Hq; a.Hk = p.Hk; a.G = p.G; a.L = p.L; a.head_mode = p.head_mode; a.first = first;
+    a.Hq = p.Hq; a.Hk = p.Hk; a.G = p.G; a.L = p.L; a.head_mode = prep_hm; a.first = first;
     const int cnt = std::min(128, pairs - first);
     for (int i = 0; i < cnt; ++i) {
       const int pr = first + i;
@@ -3374,10 +3969,14 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   la.dbg_pos = p.dbg_topk_pos; la.dbg_score = p.dbg_topk_score; la.dbg_stats = p.dbg_list_stats;
   la.f_max = p.f_max; la.votes_g = p.votes; la.massfx_g = p.massfx; la.sexp = p.sexp; la.qcol = p.qcol;
   la.dyn_ctr = p.dyn_ctr;
+  la.score_mode = p.score_mode; la.hm_prob = p.hm_prob ? 1 : 0; la.NLs = p.NLs;
+  la.below = p.below; la.lhat = p.lhat; la.cand_sc = p.cand_sc; la.left_max = p.left_max;
   const int lists = p.S * p.NL;
   // 2. sample scores, 3. thresholds
-  if (p.head_mode == 0) {
+  if (prep_hm == 0) {
     ScoreArgs a = make_score_args(p, K_SAMPLE);
+    a.NL = p.NLs;        // sampled lists: one per (layer, query head)
+    a.head_mode = 0;
     int64_t tiles = 0;   // sample tiles of every (stream, layer, KV head)
     for (int s = 0; s < p.S; ++s) {
       a.tile_base[s] = tiles;
@@ -3388,13 +3987,15 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
     if (fused) {
       hipLaunchKernelGGL(k_prep_sample<D>, dim3(ps_blocks), dim3(8 * D), 0, st, pa_fused, a, ps);
     } else if (tiles > 0) {
-      const int grid = (int)std::min<int64_t>(stream_grid<D, false>(), std::max<int64_t>(1, tiles / 4));
+      const int grid = (int)std::min<int64_t>(stream_grid<D, 0>(), std::max<int64_t>(1, tiles / 4));
       hipLaunchKernelGGL(k_sample<D>, dim3(grid), dim3(256), 0, st, a);
     }
   } else {
     launch_score<D, K_SAMPLE>(make_score_args(p, K_SAMPLE), p.head_mode, 4096, st);
   }
-  if (lists > 2 * cus)
+  if (p.hm_prob)
+    hipLaunchKernelGGL(k_thresh_hp, dim3(lists), dim3(1024), 0, st, la);
+  else if (lists > 2 * cus)
     hipLaunchKernelGGL(k_thresh_dense, dim3(lists), dim3(1024), 0, st, la);
   else
     hipLaunchKernelGGL(k_thresh, dim3(lists), dim3(1024), 0, st, la);
@@ -3402,9 +4003,11 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   if (p.ev_start) (void)hipEventRecord(p.ev_start, st);
   if (p.head_mode == 0) {
     ScoreArgs a = make_score_args(p, K_STREAM);
+    a.score_mode = p.score_mode;
+    a.below = p.below;
     const int64_t tiles = a.tile_base[p.S];
     if (tiles > 0) {
-      const int grid = (int)std::min<int64_t>(stream_grid<D, false>(), std::max<int64_t>(1, tiles / 16));
+      const int grid = (int)std::min<int64_t>(stream_grid<D, 0>(), std::max<int64_t>(1, tiles / 16));
       int nseg = 0;   // (stream, layer, KV head) segments with rows
       for (int s = 0; s < p.S; ++s) nseg += a.ntile[s] > 0 ? p.L * p.Hk : 0;
       a.sgroup = stream_group(grid, nseg);
@@ -3420,8 +4023,15 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
       tiles += (int64_t)p.L * a.ntile[s];
     }
     a.tile_base[p.S] = tiles;
-    if (tiles > 0) {
-      const int grid = (int)std::min<int64_t>(stream_grid<D, true>(), std::max<int64_t>(1, tiles / 16));
+    if (tiles > 0 && p.hm_prob) {
+      a.score_mode = 1;
+      a.below = p.below;
+      a.lhat = p.lhat;
+      a.left_max = p.left_max;
+      const hipError_t e = launch_stream_hp<D>(a, p, tiles, cus, st);
+      if (e != hipSuccess) return e;
+    } else if (tiles > 0) {
+      const int grid = (int)std::min<int64_t>(stream_grid<D, 1>(), std::max<int64_t>(1, tiles / 16));
       int nseg = 0;   // (stream, layer) segments with rows
       for (int s = 0; s < p.S; ++s) nseg += a.ntile[s] > 0 ? p.L : 0;
       a.sgroup = stream_group(grid, nseg);
@@ -3446,7 +4056,8 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   va.pool_n = p.pool_n;
   va.dbg_vote_hist = p.dbg_vote_hist; va.dbg_mass_hist = p.dbg_mass_hist;
   va.dbg_pool = p.dbg_pool; va.dbg_pool_n = p.dbg_pool_n;
-  hipLaunchKernelGGL(k_select<D>, dim3(lists), dim3(1024), 0, st, la);
+  if (p.hm_prob) hipLaunchKernelGGL(k_select_hp<D>, dim3(lists), dim3(1024), 0, st, la);
+  else hipLaunchKernelGGL(k_select<D>, dim3(lists), dim3(1024), 0, st, la);
   hipLaunchKernelGGL(k_votes_pool, dim3(p.S), dim3(1024), 0, st, va);
   // 8. Gram matrix, 9. max-min
   GramArgs ga{};
@@ -3655,7 +4266,11 @@ size_t carve_workspace(RetrievePlan& p, void* ws) {
   p.qB = static_cast<uint32_t*>(take((size_t)p.S * p.L * p.Hk * 2 * (p.D / 32) * 64 * 16));
   p.tau = static_cast<uint32_t*>(take(lists * 4));
   p.cnt = static_cast<uint32_t*>(take(lists * 4));
-  p.samp = static_cast<float*>(take(lists * (size_t)p.m_max * 4));
+  p.samp = static_cast<float*>(take((size_t)p.S * p.NLs * (size_t)p.m_max * 4));
+  p.below = p.score_mode == 1 ? static_cast<uint64_t*>(take((size_t)p.S * p.NLs * 8)) : nullptr;
+  p.lhat = p.hm_prob ? static_cast<float*>(take((size_t)p.S * p.NLs * 4)) : nullptr;
+  p.cand_sc = p.hm_prob ? static_cast<float*>(take(lists * (size_t)p.cap * p.Hq * 4)) : nullptr;
+  p.left_max = p.hm_prob ? static_cast<uint32_t*>(take(lists * 4)) : nullptr;
   p.cand = static_cast<uint64_t*>(take(lists * (size_t)p.cap * 8));
   p.qcol = static_cast<float*>(take((size_t)p.S * p.L * p.Hk * 16 * 4));
   p.sexp = static_cast<int32_t*>(take((size_t)p.S * 4));

@@ -171,9 +171,10 @@ class Retriever:
     calls allocate nothing once sizes are stable.
     """
 
-    def __init__(self, indices, top_k: int, n_select: int, pool_mult: int = 4, head_mode: int = 0):
+    def __init__(self, indices, top_k: int, n_select: int, pool_mult: int = 4, head_mode: int = 0,
+                 score_mode: int = 0):
         self.indices = list(indices)
-        self.params = L.RetrieveParams(top_k, n_select, pool_mult, head_mode)
+        self.params = L.RetrieveParams(top_k, n_select, pool_mult, head_mode, score_mode)
         self._ws = None
         dev = self.indices[0].arena.device
         S = len(self.indices)

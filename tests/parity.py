@@ -54,6 +54,26 @@ def score_scale(oidx: O.Index, queries, head_mode: int = 0):
     return out
 
 
+def value_scale(oidx: O.Index, queries, head_mode: int = 0, score_mode: int = 0):
+    """The scale of each list value's error under the logit tolerance: the logit
+    scale of ``score_scale`` for scaled logits; for attention probabilities a
+    logit error of 1e-3 D moves ``p = exp(s - lse)`` by at most
+    ``p (1e-3 D_row + 1e-3 max_rows D)`` (the row's own logit and the
+    log-sum-exp, which moves by at most the largest row error), so the scale of
+    a per-head probability is ``p (D_row + max D)``, averaged over heads in
+    head mode 1."""
+    if score_mode == 0:
+        return score_scale(oidx, queries, head_mode)
+    P = O.score_lists(oidx, queries, 0, 1)
+    D = score_scale(oidx, queries, 0)
+    # plus 0.01 p: a floor of 1e-5 relative for the fp32 exp and log of the
+    # probability itself (all-zero queries make every D zero)
+    per_head = [p * (d + d.max() + 0.01) if d.size else d for p, d in zip(P, D)]
+    if head_mode == 0:
+        return per_head
+    return [np.mean(per_head[l * oidx.Hq:(l + 1) * oidx.Hq], axis=0) for l in range(oidx.L)]
+
+
 def check_topk_list(so, dscale, pos, gscore, kk, report, name=""):
     """Stage 2 for one list; returns the oracle-exact top-k positions."""
     assert pos.shape == (kk,), name
@@ -135,12 +155,12 @@ def check_maxmin(pool, desc, K, selected, report):
 
 
 def staged_check(oidx: O.Index, queries, gpu: dict, s: int, top_k: int, n_select: int,
-                 pool_mult: int = 4, head_mode: int = 0):
+                 pool_mult: int = 4, head_mode: int = 0, score_mode: int = 0):
     """Run stages 2-5 for stream ``s`` of a ``Retriever.debug`` result; returns a
     report with the swap and exemption counts."""
     report = {}
-    S_or = O.score_lists(oidx, queries, head_mode)
-    Dsc = score_scale(oidx, queries, head_mode)
+    S_or = O.score_lists(oidx, queries, head_mode, score_mode)
+    Dsc = value_scale(oidx, queries, head_mode, score_mode)
     N = oidx.candidate_rows() - oidx.first_candidate_row()     # positions are window-relative
     kk = min(top_k, N)
     NL = len(S_or)
@@ -179,7 +199,7 @@ def staged_check(oidx: O.Index, queries, gpu: dict, s: int, top_k: int, n_select
     assert np.array_equal(gpu["votes"][s, :n_out], gv[sel])
     np.testing.assert_allclose(gpu["mass"][s, :n_out], gm[sel], rtol=1e-6, atol=1e-6)
     # end to end against the pure oracle
-    ids, v, m, n = O.retrieve(oidx, queries, top_k, n_select, pool_mult, head_mode)
+    ids, v, m, n = O.retrieve(oidx, queries, top_k, n_select, pool_mult, head_mode, score_mode=score_mode)
     report["lists"] = NL
     report["end_to_end_equal"] = bool(np.array_equal(ids[:n], sel) and n == n_out)
     clean = not any(report.get(k, 0) for k in ("swaps", "pool_exempt", "pool_differs", "maxmin_exempt"))

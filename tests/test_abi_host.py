@@ -137,6 +137,16 @@ def test_retrieve_validation(L):
     assert call(prm_=L.RetrieveParams(256, 16, 0, 0)) == L.SS_ERR_INVALID_ARGUMENT
     assert call(prm_=L.RetrieveParams(256, 64, 8, 0)) == L.SS_ERR_UNSUPPORTED
     assert call(prm_=L.RetrieveParams(256, 16, 4, 2)) == L.SS_ERR_INVALID_ARGUMENT
+    assert call(prm_=L.RetrieveParams(256, 16, 4, 0, 2)) == L.SS_ERR_INVALID_ARGUMENT   # score_mode
+    assert b"score_mode" in lib.ss_last_error()
+    # head mode 1 with probabilities keeps every KV head's B tiles in registers
+    h8 = create(L, n_q_heads=32, n_kv_heads=8)
+    idx8 = L.ptr_array([h8.value])
+    assert lib.ss_retrieve(idx8, 1, q, nq, C.byref(L.RetrieveParams(256, 16, 4, 1, 1)), FAKE, ws, None,
+                           *outs) == L.SS_ERR_UNSUPPORTED
+    assert lib.ss_retrieve_workspace_bytes(idx8, 1, nq, C.byref(L.RetrieveParams(256, 16, 4, 1, 0))) > 0
+    assert lib.ss_retrieve_workspace_bytes(idx, 1, nq, C.byref(L.RetrieveParams(256, 16, 4, 1, 1))) > 0
+    lib.ss_index_destroy(h8)
     assert call(nq_=(C.c_int32 * 1)(0)) == L.SS_ERR_INVALID_ARGUMENT
     assert call(q_=L.ptr_array([FAKE, FAKE, FAKE + 4, FAKE])) == L.SS_ERR_INVALID_ARGUMENT
     assert call(n=0) == L.SS_ERR_INVALID_ARGUMENT

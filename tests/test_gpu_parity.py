@@ -713,6 +713,14 @@ def test_p4_paper_settings_full_size_staged():
     log("P4", rep)
     assert rep["lists"] == cfg.n_layers
     assert out["frame_ids"][0, 0] in set(spec.planted)
+    # the paper's rule proper: head-averaged attention probabilities
+    rp = P.Retriever([gidx], cfg.top_k, cfg.n_select, cfg.pool_mult, 1, 1)
+    outp = rp.debug(qd)
+    log("P4 probabilities: candidates per list", outp["list_stats"][0, :, 0].tolist(), "fallbacks",
+        outp["list_stats"][0, :, 1].tolist())
+    repp = staged_check(oidx, q, outp, 0, cfg.top_k, cfg.n_select, cfg.pool_mult, head_mode=1, score_mode=1)
+    log("P4 probabilities", repp)
+    assert outp["frame_ids"][0, 0] in set(spec.planted)
 
 
 def test_c5_full_size_staged():
