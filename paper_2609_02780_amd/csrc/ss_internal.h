@@ -99,8 +99,9 @@ struct RetrievePlan {
   uint64_t* below;       // score_mode 1: fixed-point sums of exp over the rows below each cut-off,
                          // [S*NL] (head mode 0) or [S*L*H_q] (hm_prob)
   float* lhat;           // hm_prob: [S*L*H_q] sample estimates of each head's log-sum-exp
-  float* cand_sc;        // hm_prob: [S*NL][cap][H_q] per-head scores of the candidates
+  float* cand_sc;        // hm_prob: [S*NL][H_q][cap] per-head logits of the candidates
   uint32_t* left_max;    // hm_prob: [S*NL] largest estimate among the rows the streaming pass left out
+  float* alpha;          // hm_prob: [S*NL][m_max] estimated attention of the sampled rows
   uint64_t* cand;        // [S*NL][cap]
   float* qcol;           // [S][L][H_kv][16] L1 norms of the scaled query columns
   int32_t* sexp;         // [S] fixed-point exponent of each stream's attention mass

@@ -1605,7 +1605,7 @@ __device__ __forceinline__ void thresh_list(const ListArgs& a) {
   const int list = blockIdx.x, s = list / a.NL, ll = list - s * a.NL;
   const int m = a.m[s], r = a.r[s];
   if (threadIdx.x == 0) a.cnt[list] = 0;
-  if (a.below && threadIdx.x == 0) a.below[list] = 0;
+  if (a.below && !a.hm_prob && threadIdx.x == 0) a.below[list] = 0;   // hm_prob: per head, in k_lhat
   if (list == 0 && threadIdx.x < kDynCtr) a.dyn_ctr[threadIdx.x * kDynStride] = 0;
   {
     int32_t* vg = a.votes_g + (size_t)s * a.f_max;
@@ -1663,85 +1663,96 @@ __device__ __forceinline__ float wave_max_f32(float v) {
 
 constexpr int kMaxHeadsHp = 128;   // query heads of a layer in head mode 1 (H_kv <= 8, G <= 16)
 
-// Head mode 1 with attention probabilities: the cut-off of a layer's list from
-// its sample.  Each head h gets an estimate of its log-sum-exp over the list,
-// Lhat_h = log((n / m) sum over the sample of exp(s_h)) (one wave per head:
-// the sample maximum first, then the shifted sum in a fixed order); then each
-// sampled row's estimated attention alpha_hat = mean_h exp(s_h - Lhat_h) and
-// the cut-off tau_hat = the r-th largest alpha_hat.  The streaming pass keeps
-// the rows with alpha_hat >= tau_hat, and k_select proves from the exact
-// normalisers that no other row can reach its top k (else it recomputes the
-// list).  The block also clears the list's exp sums and the stream's frame
-// accumulators.
-__global__ __launch_bounds__(1024) void k_thresh_hp(ListArgs a) {
-  __shared__ uint32_t hist[kSelHist];
-  __shared__ uint32_t res[4];
-  __shared__ uint32_t mm[32];
-  __shared__ float lh[kMaxHeadsHp];
-  const int list = blockIdx.x, s = list / a.NL, l = list - s * a.NL;
-  const int m = a.m[s], r = a.r[s], Hq = a.Hq;
-  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  const size_t hbase = (size_t)s * a.NLs + (size_t)l * Hq;   // sampled list of head 0 of the layer
+// Head mode 1 with attention probabilities: the cut-off of a layer's list
+// comes from its sample in three launches.  k_lhat (one block per (list,
+// head)) estimates the head's log-sum-exp over the list, Lhat_h =
+// max + log(sum exp(s_h - max)) + log(n / m) over the head's sampled logits
+// (block reductions in a fixed order), and clears the head's exp sum below
+// the cut-off and the list's largest left-out estimate; k_alpha (one thread
+// per sampled row) forms the row's estimated attention alpha_hat =
+// mean_h exp(s_h - Lhat_h); k_thresh then takes the r-th largest alpha_hat
+// as the cut-off tau_hat, as it does for logits.  The streaming pass keeps the
+// rows with alpha_hat >= tau_hat, and k_select_hp proves from the exact
+// normalisers that no other row can reach the top k (else it recomputes the
+// list).
+__global__ __launch_bounds__(256) void k_lhat(ListArgs a) {
+  __shared__ float redf[4];
+  __shared__ double redd[4];
+  const int list = blockIdx.x / a.Hq, h = blockIdx.x - list * a.Hq;
+  const int s = list / a.NL, l = list - s * a.NL;
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
+  const size_t hb = (size_t)s * a.NLs + (size_t)l * a.Hq + h;   // the head's sampled list
   if (threadIdx.x == 0) {
-    a.cnt[list] = 0;
-    a.left_max[list] = 0;
+    a.below[hb] = 0;
+    if (h == 0) a.left_max[list] = 0;
   }
-  for (int h = threadIdx.x; h < Hq; h += blockDim.x) a.below[hbase + h] = 0;
-  if (list == 0 && threadIdx.x < kDynCtr) a.dyn_ctr[threadIdx.x * kDynStride] = 0;
-  {
-    int32_t* vg = a.votes_g + (size_t)s * a.f_max;
-    int64_t* mg = a.massfx_g + (size_t)s * a.f_max;
-    for (int f = l * 1024 + threadIdx.x; f < a.f[s]; f += a.NL * 1024) {
-      vg[f] = 0;
-      mg[f] = 0;
-    }
-  }
-  if (l == 0) stream_exponent(a, s);
-  if (m == 0 || r == 0) {
-    if (threadIdx.x == 0) a.tau[list] = 0xFFFFFFFFu;
-    return;
-  }
-  const float log_nm = logf((float)a.n[s] / (float)m);
-  for (int h = wave; h < Hq; h += nw) {
-    const float* v = a.samp + (hbase + h) * a.samp_stride;
-    float mx = -INFINITY;
-    for (int u = lane; u < m; u += kWave) mx = fmaxf(mx, v[u]);
-    mx = wave_max_f32(mx);
-    double sm = 0.0;
-    for (int u = lane; u < m; u += kWave) sm += (double)__expf(v[u] - mx);
-    sm = wave_sum_f64(sm);
-    if (lane == 0) {
-      lh[h] = mx + (float)log(sm) + log_nm;
-      a.lhat[hbase + h] = lh[h];
-    }
-  }
+  const int m = a.m[s];
+  if (m == 0) return;
+  const float* v = a.samp + hb * a.samp_stride;
+  float mx = -INFINITY;
+  for (int u = threadIdx.x; u < m; u += blockDim.x) mx = fmaxf(mx, v[u]);
+  mx = wave_max_f32(mx);
+  if (lane == 0) redf[wave] = mx;
   __syncthreads();
-  float al[kThrItems];
+  const float M = fmaxf(fmaxf(redf[0], redf[1]), fmaxf(redf[2], redf[3]));
+  double sm = 0.0;
+  for (int u = threadIdx.x; u < m; u += blockDim.x) sm += (double)__expf(v[u] - M);
+  sm = wave_sum_f64(sm);
+  if (lane == 0) redd[wave] = sm;
+  __syncthreads();
+  if (threadIdx.x == 0)
+    a.lhat[hb] = M + (float)log(((redd[0] + redd[1]) + redd[2]) + redd[3]) + logf((float)a.n[s] / (float)m);
+}
+
+__global__ __launch_bounds__(256) void k_alpha(ListArgs a, float* alpha) {
+  const int list = blockIdx.x, s = list / a.NL, l = list - s * a.NL;
+  const int u = blockIdx.y * blockDim.x + threadIdx.x;
+  if (u >= a.m[s]) return;
+  const size_t hb = (size_t)s * a.NLs + (size_t)l * a.Hq;
+  float al = 0.f;
+  for (int h = 0; h < a.Hq; ++h) al += __expf(a.samp[(hb + h) * a.samp_stride + u] - a.lhat[hb + h]);
+  alpha[(size_t)list * a.samp_stride + u] = al * (1.0f / (float)a.Hq) + 0.0f;
+}
+
+// Head mode 1, attention probabilities: every candidate's per-head logits with
+// the streaming pass's arithmetic, 16 candidates per wave (each KV head's rows
+// against head mode 0's B tiles), into cand_sc [list][head][cap]; lists that
+// take the exact fallback are skipped.
+template <int D>
+__global__ __launch_bounds__(256) void k_cand_logits(ListArgs a) {
+  constexpr int KS = D / 32;
+  const int list = blockIdx.x, s = list / a.NL, l = list - s * a.NL;
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
+  const int kg = lane >> 4, rl = lane & 15, col = lane & 15;
+  const uint32_t c = a.cnt[list];
+  if (c < (uint32_t)a.kk[s] || c > (uint32_t)a.cap) return;
+  const int n = (int)c, i0 = (blockIdx.y * (blockDim.x / kWave) + wave) * kTile;
+  if (i0 >= n) return;   // uniform per wave
+  const int Hq = a.Hq, G = a.G, Hk = a.Hk;
+  const uint64_t* src = a.cand + (size_t)list * a.cap;
+  float* cs = a.cand_sc + (size_t)list * Hq * a.cap;
+  const size_t gstride = (size_t)a.stride[s] * D;
+  const int i = i0 + rl;
+  const uint32_t row = i < n ? key_row(src[i]) : 0u;
+  for (int g = 0; g < Hk; ++g) {
+    const u32x4* qb = a.qB + ((size_t)(s * a.L + l) * Hk + g) * (2 * KS * kWave);
+    const uint16_t* p = a.keys[s] + ((size_t)l * Hk + g) * gstride + (size_t)row * D + 8 * kg;
+    u32x4 bh[KS], bl[KS], A[KS];
 #pragma unroll
-  for (int it = 0; it < kThrItems; ++it) al[it] = 0.f;
-  for (int h = 0; h < Hq; ++h) {
-    const float* v = a.samp + (hbase + h) * a.samp_stride;
-    const float L = lh[h];
+    for (int ii = 0; ii < KS; ++ii) {
+      bh[ii] = qb[ii * kWave + lane];
+      bl[ii] = qb[(KS + ii) * kWave + lane];
+      A[ii] = i < n ? ld_nt(p + 32 * ii) : u32x4{0, 0, 0, 0};
+    }
+    const f32x4 acc = score_hilo<KS>(A, bh, bl);
+    if (col < G) {
 #pragma unroll
-    for (int it = 0; it < kThrItems; ++it) {
-      const int u = (int)threadIdx.x + it * 1024;
-      if (u < m) al[it] += __expf(v[u] - L);
+      for (int j = 0; j < 4; ++j) {
+        const int ic = i0 + 4 * kg + j;
+        if (ic < n) cs[(size_t)(g * G + col) * a.cap + ic] = acc[j] + 0.0f;
+      }
     }
   }
-  uint32_t x[kThrItems];
-  bool ok[kThrItems];
-  uint32_t mn = 0xFFFFFFFFu, mx = 0;
-  const float inv_h = 1.0f / (float)Hq;
-#pragma unroll
-  for (int it = 0; it < kThrItems; ++it) {
-    ok[it] = (int)threadIdx.x + it * 1024 < m;
-    x[it] = ok[it] ? ord_u32(al[it] * inv_h + 0.0f) : 0u;
-    if (ok[it]) { mn = min(mn, x[it]); mx = max(mx, x[it]); }
-  }
-  block_minmax_u32(mn, mx, mm);
-  uint32_t ng, ne;
-  const uint32_t t = block_select_range<kThrItems, true>(x, ok, mn, mx, (uint32_t)r, hist, res, ng, ne);
-  if (threadIdx.x == 0) a.tau[list] = t;
 }
 
 // ---------------------------------------------------------------------------
@@ -1927,7 +1938,7 @@ __device__ void fallback_list(const ListArgs& a, int list, uint64_t* sel, int32_
   }
   // chunk[r - c0] = score of row r for rows [c0, c0 + kFbRows) below n
   auto score_chunk = [&](int c0) {
-#pragma unroll
+#pragma unroll 1
     for (int q = 0; q < kFbTilesPerWave; ++q) {
       const int tl = wave * kFbTilesPerWave + q;        // tile of the chunk
       const int row = c0 + tl * kTile + rl;
@@ -2002,64 +2013,36 @@ __device__ float lse_from_candidates(const ListArgs& a, int list, const uint64_t
   return M + (float)log(z);
 }
 
-// Head mode 1, attention probabilities.  Every candidate's per-head logits,
-// recomputed with the streaming pass's arithmetic (16 candidate rows per wave
-// step, each KV head's rows against the head-mode-0 B tiles), into cand_sc;
-// each head's exact log-sum-exp lse_h over the list: the candidates summed
-// here in fixed point against M_h = max(Lhat_h, their largest logit), plus the
-// streaming pass's sum over the rows it left out (each of those added
-// exp(s - Lhat_h) / (H_q tau_hat)); then each candidate's exact alpha =
-// mean_h exp(s_h - lse_h), written into its composite key.  Returns rho =
-// max_h exp(Lhat_h - lse_h): a left-out row's alpha is at most rho times its
-// estimate.  Ends with a barrier.
+// Head mode 1, attention probabilities.  With every candidate's per-head
+// logits in cand_sc (k_cand_logits), each head's exact log-sum-exp lse_h over
+// the list: the candidates summed here in fixed point against M_h =
+// max(Lhat_h, their largest logit), plus the streaming pass's sum over the rows
+// it left out (each of those added exp(s - Lhat_h) / (H_q tau_hat)); then each
+// candidate's exact alpha = mean_h exp(s_h - lse_h), written into its
+// composite key.  Returns rho = max_h exp(Lhat_h - lse_h): a left-out row's
+// alpha is at most rho times its estimate.  Ends with a barrier.
 template <int D>
 __device__ float hp_candidate_values(const ListArgs& a, int list, int n) {
-  constexpr int KS = D / 32;
   __shared__ float lse_sh[kMaxHeadsHp];
   __shared__ uint32_t rho_sh;
   const int s = list / a.NL, l = list - s * a.NL;
-  const int Hq = a.Hq, G = a.G, Hk = a.Hk;
+  const int Hq = a.Hq;
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  const int kg = lane >> 4, rl = lane & 15, col = lane & 15;
   uint64_t* src = a.cand + (size_t)list * a.cap;
-  float* cs = a.cand_sc + (size_t)list * a.cap * Hq;
-  const size_t gstride = (size_t)a.stride[s] * D;
-  const size_t hb = (size_t)(s * a.L + l) * Hq;
-  for (int i0 = wave * kTile; i0 < n; i0 += nw * kTile) {
-    const int i = i0 + rl;
-    const uint32_t row = i < n ? key_row(src[i]) : 0u;
-    for (int g = 0; g < Hk; ++g) {
-      const u32x4* qb = a.qB + ((size_t)(s * a.L + l) * Hk + g) * (2 * KS * kWave);
-      const uint16_t* p = a.keys[s] + ((size_t)l * Hk + g) * gstride + (size_t)row * D + 8 * kg;
-      u32x4 bh[KS], bl[KS], A[KS];
-#pragma unroll
-      for (int ii = 0; ii < KS; ++ii) {
-        bh[ii] = qb[ii * kWave + lane];
-        bl[ii] = qb[(KS + ii) * kWave + lane];
-        A[ii] = i < n ? ld_nt(p + 32 * ii) : u32x4{0, 0, 0, 0};
-      }
-      const f32x4 acc = score_hilo<KS>(A, bh, bl);
-      if (col < G) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int ic = i0 + 4 * kg + j;
-          if (ic < n) cs[(size_t)ic * Hq + g * G + col] = acc[j] + 0.0f;
-        }
-      }
-    }
-  }
+  const float* cs = a.cand_sc + (size_t)list * Hq * a.cap;
+  const size_t hb = (size_t)s * a.NLs + (size_t)l * Hq;
   if (threadIdx.x == 0) rho_sh = 0;
-  __threadfence_block();
   __syncthreads();
   const float tau = ord_f32(a.tau[list]);
   for (int h = wave; h < Hq; h += nw) {
+    const float* ch = cs + (size_t)h * a.cap;
     const float Lh = a.lhat[hb + h];
     float mx = -INFINITY;
-    for (int i = lane; i < n; i += kWave) mx = fmaxf(mx, cs[(size_t)i * Hq + h]);
+    for (int i = lane; i < n; i += kWave) mx = fmaxf(mx, ch[i]);
     const float M = fmaxf(wave_max_f32(mx), Lh);
     unsigned long long fx = 0;
     for (int i = lane; i < n; i += kWave)
-      fx += (unsigned long long)llrint(ldexp((double)__expf(cs[(size_t)i * Hq + h] - M), kBelowExp));
+      fx += (unsigned long long)llrint(ldexp((double)__expf(ch[i] - M), kBelowExp));
     fx = wave_sum_u64(fx);
     if (lane == 0) {
       const double left_out = ldexp((double)a.below[hb + h], -kBelowExp) * (double)Hq * (double)tau;
@@ -2073,7 +2056,7 @@ __device__ float hp_candidate_values(const ListArgs& a, int list, int n) {
   const float inv_h = 1.0f / (float)Hq;
   for (int i = threadIdx.x; i < n; i += blockDim.x) {
     float al = 0.f;
-    for (int h = 0; h < Hq; ++h) al += __expf(cs[(size_t)i * Hq + h] - lse_sh[h]);
+    for (int h = 0; h < Hq; ++h) al += __expf(cs[(size_t)h * a.cap + i] - lse_sh[h]);
     src[i] = mk_key(ord_u32(al * inv_h + 0.0f), key_row(src[i]));
   }
   __threadfence_block();
@@ -3993,9 +3976,13 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   } else {
     launch_score<D, K_SAMPLE>(make_score_args(p, K_SAMPLE), p.head_mode, 4096, st);
   }
-  if (p.hm_prob)
-    hipLaunchKernelGGL(k_thresh_hp, dim3(lists), dim3(1024), 0, st, la);
-  else if (lists > 2 * cus)
+  if (p.hm_prob) {
+    hipLaunchKernelGGL(k_lhat, dim3(lists * p.Hq), dim3(256), 0, st, la);
+    hipLaunchKernelGGL(k_alpha, dim3(lists, cdiv(p.m_max, 256)), dim3(256), 0, st, la, p.alpha);
+    ListArgs lt = la;   // the cut-off over the estimated attention of the sample
+    lt.samp = p.alpha;
+    hipLaunchKernelGGL(k_thresh, dim3(lists), dim3(1024), 0, st, lt);
+  } else if (lists > 2 * cus)
     hipLaunchKernelGGL(k_thresh_dense, dim3(lists), dim3(1024), 0, st, la);
   else
     hipLaunchKernelGGL(k_thresh, dim3(lists), dim3(1024), 0, st, la);
@@ -4056,7 +4043,10 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   va.pool_n = p.pool_n;
   va.dbg_vote_hist = p.dbg_vote_hist; va.dbg_mass_hist = p.dbg_mass_hist;
   va.dbg_pool = p.dbg_pool; va.dbg_pool_n = p.dbg_pool_n;
-  if (p.hm_prob) hipLaunchKernelGGL(k_select_hp<D>, dim3(lists), dim3(1024), 0, st, la);
+  if (p.hm_prob) {
+    hipLaunchKernelGGL(k_cand_logits<D>, dim3(lists, cdiv(p.cap, 64)), dim3(256), 0, st, la);
+    hipLaunchKernelGGL(k_select_hp<D>, dim3(lists), dim3(1024), 0, st, la);
+  }
   else hipLaunchKernelGGL(k_select<D>, dim3(lists), dim3(1024), 0, st, la);
   hipLaunchKernelGGL(k_votes_pool, dim3(p.S), dim3(1024), 0, st, va);
   // 8. Gram matrix, 9. max-min
@@ -4271,6 +4261,7 @@ size_t carve_workspace(RetrievePlan& p, void* ws) {
   p.lhat = p.hm_prob ? static_cast<float*>(take((size_t)p.S * p.NLs * 4)) : nullptr;
   p.cand_sc = p.hm_prob ? static_cast<float*>(take(lists * (size_t)p.cap * p.Hq * 4)) : nullptr;
   p.left_max = p.hm_prob ? static_cast<uint32_t*>(take(lists * 4)) : nullptr;
+  p.alpha = p.hm_prob ? static_cast<float*>(take(lists * (size_t)p.m_max * 4)) : nullptr;
   p.cand = static_cast<uint64_t*>(take(lists * (size_t)p.cap * 8));
   p.qcol = static_cast<float*>(take((size_t)p.S * p.L * p.Hk * 16 * 4));
   p.sexp = static_cast<int32_t*>(take((size_t)p.S * 4));
