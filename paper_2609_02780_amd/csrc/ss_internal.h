@@ -102,6 +102,7 @@ struct RetrievePlan {
   float* cand_sc;        // hm_prob: [S*NL][H_q][cap] per-head logits of the candidates
   uint32_t* left_max;    // hm_prob: [S*NL] largest estimate among the rows the streaming pass left out
   float* alpha;          // hm_prob: [S*NL][m_max] estimated attention of the sampled rows
+  float* cand_lse;       // hm_prob: [S*NL][H_q] exact log-sum-exp of each head's list
   uint64_t* cand;        // [S*NL][cap]
   float* qcol;           // [S][L][H_kv][16] L1 norms of the scaled query columns
   int32_t* sexp;         // [S] fixed-point exponent of each stream's attention mass

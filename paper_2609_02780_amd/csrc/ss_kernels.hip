@@ -249,16 +249,24 @@ __device__ void find_digit(const uint32_t* hist, uint32_t need, uint32_t* res) {
   __syncthreads();
 }
 
+// Place of bin b in a histogram padded with one word after every 32 bins, so
+// that the 64 lanes reading their own 32 consecutive bins start in 32
+// different banks.
+__device__ __forceinline__ uint32_t pad32(uint32_t b) { return b + (b >> 5); }
+
 // Wave 0 finds, in an NB-bin histogram (NB = 64 * BPL) scanned from the top
 // bin down, the bin holding the `need`-th element: res[0..2] = bin, count
-// above it, bin count.  Ends with a barrier.
-template <int BPL>
+// above it, bin count.  PAD: the histogram is laid out by pad32 (BPL = 32).
+// Ends with a barrier.
+template <int BPL, bool PAD = false>
 __device__ void find_digit_wide(const uint32_t* hist, uint32_t need, uint32_t* res) {
+  static_assert(!PAD || BPL == 32, "padded histograms hold 32 bins per lane");
   if (threadIdx.x < kWave) {
     const int lane = threadIdx.x;
+    const uint32_t* hl = hist + (PAD ? (BPL + 1) : BPL) * lane;
     uint32_t hs[BPL], mine = 0;
 #pragma unroll
-    for (int j = 0; j < BPL; ++j) { hs[j] = hist[BPL * lane + j]; mine += hs[j]; }
+    for (int j = 0; j < BPL; ++j) { hs[j] = hl[j]; mine += hs[j]; }
     uint32_t x = mine;  // inclusive suffix sum over lanes >= lane
     for (int o = 1; o < kWave; o <<= 1) {
       const uint32_t y = __shfl_down(x, o);
@@ -1400,8 +1408,9 @@ __device__ void block_minmax_u32(uint32_t& mn, uint32_t& mx, uint32_t* sh) {
 // band.  WIDE: the first round takes 11 bits (2048 bins spread the bulk of many
 // values, which keeps same-bin LDS atomics rare, and saves a round).  Returns
 // the value; `n_greater` and `n_equal` count the valid values above it and
-// equal to it.  `hist` holds 512 words, kSelHist when WIDE.
-constexpr int kSelHist = 2048 + 512;
+// equal to it.  `hist` holds 512 words, kSelHist when WIDE (the wide
+// histogram padded by pad32).
+constexpr int kSelHist = 2048 + 64 + 512;
 
 // Ends a radix selection whose current bin [lo, hi] holds eq <= 64 values: they
 // are gathered into `vals` (64 words, no longer read as a histogram) and wave 0
@@ -1422,8 +1431,10 @@ __device__ void finish_bin_by_counting(const uint32_t (&v)[N], const bool (&ok)[
     const int lane = threadIdx.x;
     const uint32_t mine = lane < (int)eq ? vals[lane] : 0u;
     uint32_t gt = 0, ge = 0;
+    // the other values from the lanes' registers (j is uniform)
+#pragma unroll 8
     for (uint32_t j = 0; j < eq; ++j) {
-      const uint32_t o = vals[j];
+      const uint32_t o = (uint32_t)__builtin_amdgcn_readlane((int)mine, (int)j);
       gt += o > mine;
       ge += o >= mine;
     }
@@ -1453,9 +1464,9 @@ __device__ uint32_t block_select_range(const uint32_t (&v)[N], const bool (&ok)[
     const int shift = bits > 11 ? bits - 11 : 0;
 #pragma unroll
     for (int i = 0; i < N; ++i)
-      if (ok[i] && v[i] >= lo && v[i] <= hi) atomicAdd(&wide[(v[i] - lo) >> shift], 1u);
+      if (ok[i] && v[i] >= lo && v[i] <= hi) atomicAdd(&wide[pad32((v[i] - lo) >> shift)], 1u);
     __syncthreads();
-    find_digit_wide<32>(wide, need, res);
+    find_digit_wide<32, true>(wide, need, res);
     need -= res[1];
     eq = res[2];
     lo += res[0] << shift;
@@ -1511,7 +1522,8 @@ struct ListArgs {
   int NLs;                                 // sampled lists per stream (L * H_q when hm_prob)
   uint64_t* below;                         // score_mode 1: fixed-point exp sums below each cut-off
   float* lhat;                             // hm_prob: sample log-sum-exp estimate of each (layer, head)
-  float* cand_sc;                          // hm_prob: [S*NL][cap][H_q] per-head candidate scores
+  float* cand_sc;                          // hm_prob: [S*NL][H_q][cap] per-head candidate logits
+  float* cand_lse;                         // hm_prob: [S*NL][H_q] exact log-sum-exp of each head's list
   uint32_t* left_max;                      // hm_prob: [S*NL] largest alpha_hat left out (ordered bits)
   int32_t m[kMaxStreams], r[kMaxStreams], kk[kMaxStreams], n[kMaxStreams];
   int32_t f[kMaxStreams], rpf[kMaxStreams];
@@ -1568,8 +1580,10 @@ __device__ void stream_exponent(const ListArgs& a, int s) {
   }
   const int L = a.L, Hk = a.Hk;
   const float* qc = a.qcol + (size_t)s * L * Hk * 16;
+  const float km = __uint_as_float(*a.kmax[s]);   // issued with the column loads
   float b = 0.f;
   if (a.head_mode == 0) {
+#pragma unroll 4
     for (int i = threadIdx.x; i < L * Hk * 16; i += kWave) b = fmaxf(b, qc[i]);
   } else {
     for (int l = threadIdx.x; l < L; l += kWave) {
@@ -1580,7 +1594,7 @@ __device__ void stream_exponent(const ListArgs& a, int s) {
   }
   b = __uint_as_float(wave_max_u32(__float_as_uint(b)));   // non-negative: ordered as integers
   if (threadIdx.x == 0) {
-    const float bound = b * __uint_as_float(*a.kmax[s]) * 1.02f;
+    const float bound = b * km * 1.02f;
     const int E = a.NL * a.kk[s];
     int x = 120;                          // all scores are zero
     if (!(bound <= 3.0e38f)) {
@@ -1615,8 +1629,8 @@ __device__ __forceinline__ void thresh_list(const ListArgs& a) {
       mg[f] = 0;
     }
   }
-  if (ll == 0) stream_exponent(a, s);
   if (m == 0 || r == 0) {
+    if (ll == 0) stream_exponent(a, s);
     if (threadIdx.x == 0) a.tau[list] = 0xFFFFFFFFu;
     return;
   }
@@ -1624,9 +1638,11 @@ __device__ __forceinline__ void thresh_list(const ListArgs& a) {
   uint32_t x[kThrItems];
   bool ok[kThrItems];
   uint32_t mn = 0xFFFFFFFFu, mx = 0;
-  // every load issued at once, from clamped in-bounds indices (m >= 1)
+  // every load issued at once, from clamped in-bounds indices (m >= 1); the
+  // stream's mass exponent (first block) while they are in flight
 #pragma unroll
   for (int it = 0; it < kThrItems; ++it) x[it] = __float_as_uint(v[min((int)threadIdx.x + it * 1024, m - 1)]);
+  if (ll == 0) stream_exponent(a, s);
 #pragma unroll
   for (int it = 0; it < kThrItems; ++it) {
     ok[it] = (int)threadIdx.x + it * 1024 < m;
@@ -1675,9 +1691,9 @@ constexpr int kMaxHeadsHp = 128;   // query heads of a layer in head mode 1 (H_k
 // rows with alpha_hat >= tau_hat, and k_select_hp proves from the exact
 // normalisers that no other row can reach the top k (else it recomputes the
 // list).
-__global__ __launch_bounds__(256) void k_lhat(ListArgs a) {
-  __shared__ float redf[4];
-  __shared__ double redd[4];
+__global__ __launch_bounds__(1024) void k_lhat(ListArgs a) {
+  __shared__ float redf[16];
+  __shared__ double redd[16];
   const int list = blockIdx.x / a.Hq, h = blockIdx.x - list * a.Hq;
   const int s = list / a.NL, l = list - s * a.NL;
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
@@ -1689,19 +1705,32 @@ __global__ __launch_bounds__(256) void k_lhat(ListArgs a) {
   const int m = a.m[s];
   if (m == 0) return;
   const float* v = a.samp + hb * a.samp_stride;
+  float x[kThrItems];   // the sample (at most 16,384 rows) in registers, all loads in flight
+#pragma unroll
+  for (int it = 0; it < kThrItems; ++it) {
+    const int u = (int)threadIdx.x + it * 1024;
+    x[it] = u < m ? v[u] : -INFINITY;
+  }
   float mx = -INFINITY;
-  for (int u = threadIdx.x; u < m; u += blockDim.x) mx = fmaxf(mx, v[u]);
+#pragma unroll
+  for (int it = 0; it < kThrItems; ++it) mx = fmaxf(mx, x[it]);
   mx = wave_max_f32(mx);
   if (lane == 0) redf[wave] = mx;
   __syncthreads();
-  const float M = fmaxf(fmaxf(redf[0], redf[1]), fmaxf(redf[2], redf[3]));
+  float M = redf[0];
+  for (int w = 1; w < 16; ++w) M = fmaxf(M, redf[w]);
   double sm = 0.0;
-  for (int u = threadIdx.x; u < m; u += blockDim.x) sm += (double)__expf(v[u] - M);
+#pragma unroll
+  for (int it = 0; it < kThrItems; ++it)
+    if ((int)threadIdx.x + it * 1024 < m) sm += (double)__expf(x[it] - M);
   sm = wave_sum_f64(sm);
   if (lane == 0) redd[wave] = sm;
   __syncthreads();
-  if (threadIdx.x == 0)
-    a.lhat[hb] = M + (float)log(((redd[0] + redd[1]) + redd[2]) + redd[3]) + logf((float)a.n[s] / (float)m);
+  if (threadIdx.x == 0) {
+    double z = 0.0;
+    for (int w = 0; w < 16; ++w) z += redd[w];
+    a.lhat[hb] = M + (float)log(z) + logf((float)a.n[s] / (float)m);
+  }
 }
 
 __global__ __launch_bounds__(256) void k_alpha(ListArgs a, float* alpha) {
@@ -1709,16 +1738,19 @@ __global__ __launch_bounds__(256) void k_alpha(ListArgs a, float* alpha) {
   const int u = blockIdx.y * blockDim.x + threadIdx.x;
   if (u >= a.m[s]) return;
   const size_t hb = (size_t)s * a.NLs + (size_t)l * a.Hq;
+  const float* v = a.samp + hb * a.samp_stride + u;
   float al = 0.f;
-  for (int h = 0; h < a.Hq; ++h) al += __expf(a.samp[(hb + h) * a.samp_stride + u] - a.lhat[hb + h]);
+#pragma unroll 8
+  for (int h = 0; h < a.Hq; ++h) al += __expf(v[(size_t)h * a.samp_stride] - a.lhat[hb + h]);
   alpha[(size_t)list * a.samp_stride + u] = al * (1.0f / (float)a.Hq) + 0.0f;
 }
 
 // Head mode 1, attention probabilities: every candidate's per-head logits with
 // the streaming pass's arithmetic, 16 candidates per wave (each KV head's rows
-// against head mode 0's B tiles), into cand_sc [list][head][cap]; lists that
-// take the exact fallback are skipped.
-template <int D>
+// against head mode 0's B tiles, every head's key loads in flight at once),
+// into cand_sc [list][head][cap]; lists that take the exact fallback are
+// skipped.
+template <int D, int HK>
 __global__ __launch_bounds__(256) void k_cand_logits(ListArgs a) {
   constexpr int KS = D / 32;
   const int list = blockIdx.x, s = list / a.NL, l = list - s * a.NL;
@@ -1728,23 +1760,29 @@ __global__ __launch_bounds__(256) void k_cand_logits(ListArgs a) {
   if (c < (uint32_t)a.kk[s] || c > (uint32_t)a.cap) return;
   const int n = (int)c, i0 = (blockIdx.y * (blockDim.x / kWave) + wave) * kTile;
   if (i0 >= n) return;   // uniform per wave
-  const int Hq = a.Hq, G = a.G, Hk = a.Hk;
+  const int G = a.G;
   const uint64_t* src = a.cand + (size_t)list * a.cap;
-  float* cs = a.cand_sc + (size_t)list * Hq * a.cap;
+  float* cs = a.cand_sc + (size_t)list * a.Hq * a.cap;
   const size_t gstride = (size_t)a.stride[s] * D;
   const int i = i0 + rl;
   const uint32_t row = i < n ? key_row(src[i]) : 0u;
-  for (int g = 0; g < Hk; ++g) {
-    const u32x4* qb = a.qB + ((size_t)(s * a.L + l) * Hk + g) * (2 * KS * kWave);
-    const uint16_t* p = a.keys[s] + ((size_t)l * Hk + g) * gstride + (size_t)row * D + 8 * kg;
-    u32x4 bh[KS], bl[KS], A[KS];
+  u32x4 A[HK][KS];
+#pragma unroll
+  for (int g = 0; g < HK; ++g) {
+    const uint16_t* p = a.keys[s] + ((size_t)l * HK + g) * gstride + (size_t)row * D + 8 * kg;
+#pragma unroll
+    for (int ii = 0; ii < KS; ++ii) A[g][ii] = i < n ? ld_nt(p + 32 * ii) : u32x4{0, 0, 0, 0};
+  }
+#pragma unroll
+  for (int g = 0; g < HK; ++g) {
+    const u32x4* qb = a.qB + ((size_t)(s * a.L + l) * HK + g) * (2 * KS * kWave);
+    u32x4 bh[KS], bl[KS];
 #pragma unroll
     for (int ii = 0; ii < KS; ++ii) {
       bh[ii] = qb[ii * kWave + lane];
       bl[ii] = qb[(KS + ii) * kWave + lane];
-      A[ii] = i < n ? ld_nt(p + 32 * ii) : u32x4{0, 0, 0, 0};
     }
-    const f32x4 acc = score_hilo<KS>(A, bh, bl);
+    const f32x4 acc = score_hilo<KS>(A[g], bh, bl);
     if (col < G) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
@@ -2013,49 +2051,88 @@ __device__ float lse_from_candidates(const ListArgs& a, int list, const uint64_t
   return M + (float)log(z);
 }
 
-// Head mode 1, attention probabilities.  With every candidate's per-head
-// logits in cand_sc (k_cand_logits), each head's exact log-sum-exp lse_h over
-// the list: the candidates summed here in fixed point against M_h =
-// max(Lhat_h, their largest logit), plus the streaming pass's sum over the rows
-// it left out (each of those added exp(s - Lhat_h) / (H_q tau_hat)); then each
-// candidate's exact alpha = mean_h exp(s_h - lse_h), written into its
-// composite key.  Returns rho = max_h exp(Lhat_h - lse_h): a left-out row's
-// alpha is at most rho times its estimate.  Ends with a barrier.
-template <int D>
-__device__ float hp_candidate_values(const ListArgs& a, int list, int n) {
+// Head mode 1, attention probabilities: each head's exact log-sum-exp lse_h
+// over the list, one wave per (list, head), from the candidates' logits in
+// cand_sc summed in fixed point against M_h = max(Lhat_h, their largest logit)
+// (so the order of the additions does not matter), plus the streaming pass's
+// sum over the rows it left out (each of those added exp(s - Lhat_h) /
+// (H_q tau_hat)).  Lists that take the exact fallback are skipped.
+__global__ __launch_bounds__(256) void k_cand_lse(ListArgs a) {
+  constexpr int kIt = 8;   // loads in flight per thread
+  __shared__ float redf[4];
+  __shared__ unsigned long long redu[4];
+  const int list = blockIdx.x / a.Hq, h = blockIdx.x - list * a.Hq;
+  const int s = list / a.NL, l = list - s * a.NL;
+  const uint32_t c = a.cnt[list];
+  if (c < (uint32_t)a.kk[s] || c > (uint32_t)a.cap) return;
+  const int n = (int)c;
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
+  const float* ch = a.cand_sc + ((size_t)list * a.Hq + h) * a.cap;
+  const size_t hb = (size_t)s * a.NLs + (size_t)l * a.Hq + h;
+  const float Lh = a.lhat[hb];
+  float mx = -INFINITY;
+  for (int b = 0; b < n; b += 256 * kIt) {
+    float x[kIt];
+#pragma unroll
+    for (int it = 0; it < kIt; ++it) {
+      const int i = b + it * 256 + (int)threadIdx.x;
+      x[it] = i < n ? ch[i] : -INFINITY;
+    }
+#pragma unroll
+    for (int it = 0; it < kIt; ++it) mx = fmaxf(mx, x[it]);
+  }
+  mx = wave_max_f32(mx);
+  if (lane == 0) redf[wave] = mx;
+  __syncthreads();
+  const float M = fmaxf(fmaxf(fmaxf(redf[0], redf[1]), fmaxf(redf[2], redf[3])), Lh);
+  unsigned long long fx = 0;
+  for (int b = 0; b < n; b += 256 * kIt) {
+    float x[kIt];
+#pragma unroll
+    for (int it = 0; it < kIt; ++it) {
+      const int i = b + it * 256 + (int)threadIdx.x;
+      x[it] = i < n ? ch[i] : -INFINITY;
+    }
+#pragma unroll
+    for (int it = 0; it < kIt; ++it)
+      if (b + it * 256 + (int)threadIdx.x < n) fx += (unsigned long long)llrint(ldexp((double)__expf(x[it] - M), kBelowExp));
+  }
+  fx = wave_sum_u64(fx);
+  if (lane == 0) redu[wave] = fx;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const unsigned long long tot = redu[0] + redu[1] + redu[2] + redu[3];
+    const double tau = (double)ord_f32(a.tau[list]);
+    const double left_out = ldexp((double)a.below[hb], -kBelowExp) * (double)a.Hq * tau;
+    const double z = ldexp((double)tot, -kBelowExp) + left_out * exp((double)Lh - (double)M);
+    a.cand_lse[(size_t)list * a.Hq + h] = M + (float)log(z);
+  }
+}
+
+// Head mode 1, attention probabilities: each candidate's exact alpha =
+// mean_h exp(s_h - lse_h), written into its composite key.  Returns rho =
+// max_h exp(Lhat_h - lse_h): a left-out row's alpha is at most rho times its
+// estimate.  Ends with a barrier.
+__device__ __forceinline__ float hp_candidate_values(const ListArgs& a, int list, int n) {
   __shared__ float lse_sh[kMaxHeadsHp];
   __shared__ uint32_t rho_sh;
   const int s = list / a.NL, l = list - s * a.NL;
   const int Hq = a.Hq;
-  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   uint64_t* src = a.cand + (size_t)list * a.cap;
   const float* cs = a.cand_sc + (size_t)list * Hq * a.cap;
   const size_t hb = (size_t)s * a.NLs + (size_t)l * Hq;
   if (threadIdx.x == 0) rho_sh = 0;
   __syncthreads();
-  const float tau = ord_f32(a.tau[list]);
-  for (int h = wave; h < Hq; h += nw) {
-    const float* ch = cs + (size_t)h * a.cap;
-    const float Lh = a.lhat[hb + h];
-    float mx = -INFINITY;
-    for (int i = lane; i < n; i += kWave) mx = fmaxf(mx, ch[i]);
-    const float M = fmaxf(wave_max_f32(mx), Lh);
-    unsigned long long fx = 0;
-    for (int i = lane; i < n; i += kWave)
-      fx += (unsigned long long)llrint(ldexp((double)__expf(ch[i] - M), kBelowExp));
-    fx = wave_sum_u64(fx);
-    if (lane == 0) {
-      const double left_out = ldexp((double)a.below[hb + h], -kBelowExp) * (double)Hq * (double)tau;
-      const double z = ldexp((double)fx, -kBelowExp) + left_out * exp((double)Lh - (double)M);
-      const float lse = M + (float)log(z);
-      lse_sh[h] = lse;
-      atomicMax(&rho_sh, ord_u32(expf(Lh - lse)));   // positive values: the order of the floats
-    }
+  for (int h = threadIdx.x; h < Hq; h += blockDim.x) {
+    const float lse = a.cand_lse[(size_t)list * Hq + h];
+    lse_sh[h] = lse;
+    atomicMax(&rho_sh, ord_u32(expf(a.lhat[hb + h] - lse)));   // positive values: the order of the floats
   }
   __syncthreads();
   const float inv_h = 1.0f / (float)Hq;
   for (int i = threadIdx.x; i < n; i += blockDim.x) {
     float al = 0.f;
+#pragma unroll 8
     for (int h = 0; h < Hq; ++h) al += __expf(cs[(size_t)h * a.cap + i] - lse_sh[h]);
     src[i] = mk_key(ord_u32(al * inv_h + 0.0f), key_row(src[i]));
   }
@@ -2197,8 +2274,8 @@ struct SelectShared {
 // `sel`, in any order: the values (high halves) and inverted rows in
 // registers for up to 8,192 candidates, else a radix selection over the keys
 // in global memory.  Ends with a barrier.
-__device__ void select_candidates(const uint64_t* src, int n, int kk, uint64_t* sel, uint32_t* hist,
-                                  uint32_t* res, uint32_t& ngather, uint32_t* mm) {
+__device__ __forceinline__ void select_candidates(const uint64_t* src, int n, int kk, uint64_t* sel, uint32_t* hist,
+                                                  uint32_t* res, uint32_t& ngather, uint32_t* mm) {
   if (threadIdx.x == 0) ngather = 0;
   if (n <= 1024 * kSelItems) {
     // scores (high halves) and inverted rows in registers: the k-th score, then
@@ -2272,7 +2349,7 @@ __device__ void select_list(const ListArgs& a, int list, SelectShared& sh, uint3
   int fallback = (c < (uint32_t)kk || c > (uint32_t)a.cap) ? 1 : 0;
   uint64_t* src = a.cand + (size_t)list * a.cap;
   float rho = 0.f;
-  if (HP && !fallback) rho = hp_candidate_values<D>(a, list, (int)c);
+  if (HP && !fallback) rho = hp_candidate_values(a, list, (int)c);
   if (!fallback) {
     select_candidates(src, (int)c, kk, sel, hist, res, ngather, mm);
     // head mode 1, attention probabilities: the selection is exact when its
@@ -3954,6 +4031,7 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   la.dyn_ctr = p.dyn_ctr;
   la.score_mode = p.score_mode; la.hm_prob = p.hm_prob ? 1 : 0; la.NLs = p.NLs;
   la.below = p.below; la.lhat = p.lhat; la.cand_sc = p.cand_sc; la.left_max = p.left_max;
+  la.cand_lse = p.cand_lse;
   const int lists = p.S * p.NL;
   // 2. sample scores, 3. thresholds
   if (prep_hm == 0) {
@@ -3977,7 +4055,7 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
     launch_score<D, K_SAMPLE>(make_score_args(p, K_SAMPLE), p.head_mode, 4096, st);
   }
   if (p.hm_prob) {
-    hipLaunchKernelGGL(k_lhat, dim3(lists * p.Hq), dim3(256), 0, st, la);
+    hipLaunchKernelGGL(k_lhat, dim3(lists * p.Hq), dim3(1024), 0, st, la);
     hipLaunchKernelGGL(k_alpha, dim3(lists, cdiv(p.m_max, 256)), dim3(256), 0, st, la, p.alpha);
     ListArgs lt = la;   // the cut-off over the estimated attention of the sample
     lt.samp = p.alpha;
@@ -4044,7 +4122,17 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   va.dbg_vote_hist = p.dbg_vote_hist; va.dbg_mass_hist = p.dbg_mass_hist;
   va.dbg_pool = p.dbg_pool; va.dbg_pool_n = p.dbg_pool_n;
   if (p.hm_prob) {
-    hipLaunchKernelGGL(k_cand_logits<D>, dim3(lists, cdiv(p.cap, 64)), dim3(256), 0, st, la);
+    const dim3 cg(lists, cdiv(p.cap, 64));
+    switch (p.Hk) {   // the streaming pass's KV-head counts
+      case 1: hipLaunchKernelGGL((k_cand_logits<D, 1>), cg, dim3(256), 0, st, la); break;
+      case 2: hipLaunchKernelGGL((k_cand_logits<D, 2>), cg, dim3(256), 0, st, la); break;
+      case 4: hipLaunchKernelGGL((k_cand_logits<D, 4>), cg, dim3(256), 0, st, la); break;
+      case 8:   // as the streaming pass: H_kv = 8 only at head dimension 64
+        if (D * 8 <= 512) hipLaunchKernelGGL((k_cand_logits<D, (D * 8 <= 512 ? 8 : 4)>), cg, dim3(256), 0, st, la);
+        break;
+      default: break;
+    }
+    hipLaunchKernelGGL(k_cand_lse, dim3(lists * p.Hq), dim3(256), 0, st, la);
     hipLaunchKernelGGL(k_select_hp<D>, dim3(lists), dim3(1024), 0, st, la);
   }
   else hipLaunchKernelGGL(k_select<D>, dim3(lists), dim3(1024), 0, st, la);
@@ -4262,6 +4350,7 @@ size_t carve_workspace(RetrievePlan& p, void* ws) {
   p.cand_sc = p.hm_prob ? static_cast<float*>(take(lists * (size_t)p.cap * p.Hq * 4)) : nullptr;
   p.left_max = p.hm_prob ? static_cast<uint32_t*>(take(lists * 4)) : nullptr;
   p.alpha = p.hm_prob ? static_cast<float*>(take(lists * (size_t)p.m_max * 4)) : nullptr;
+  p.cand_lse = p.hm_prob ? static_cast<float*>(take(lists * (size_t)p.Hq * 4)) : nullptr;
   p.cand = static_cast<uint64_t*>(take(lists * (size_t)p.cap * 8));
   p.qcol = static_cast<float*>(take((size_t)p.S * p.L * p.Hk * 16 * 4));
   p.sexp = static_cast<int32_t*>(take((size_t)p.S * 4));
