@@ -305,8 +305,11 @@ def hot_kernel(cfg, score_mode: int) -> str:
 
 def cpu_baseline(cfg, host0, score_mode: int = 0):
     """The oracle's retrieval over stream 0 of the workload, with its queries and
-    retrieval parameters.  A raw stream is taken whole; a compressed one is cut to
-    its first 40 frames, since the float64 k-means of the oracle's append is slow."""
+    retrieval parameters, every frame of the stream.  A compressed stream keeps,
+    per frame, its first n_centroids token rows as the stored rows: the same
+    number of rows the centroids would fill, so the same retrieval work, without
+    the oracle's float64 k-means (append work, outside the timed retrieval).
+    Runs of under 3 s are repeated and the median of three is reported."""
     from oracle import oracle as O
     q, blocks, comp = host0
     try:
@@ -315,25 +318,34 @@ def cpu_baseline(cfg, host0, score_mode: int = 0):
     except Exception:
         cores = 1
     oi = O.Index(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim)
+    T = cfg.tokens_per_frame
     if comp is None:
         for kb, nf in blocks:
-            oi.append(kb, nf, cfg.tokens_per_frame)
+            oi.append(kb, nf, T)
         what = f"all {oi.n_frames} frames"
     else:
-        kb, nf = blocks[0]
-        nf = min(nf, 40)
-        oi.append([np.ascontiguousarray(k[:, :nf * cfg.tokens_per_frame, :]) for k in kb], nf,
-                  cfg.tokens_per_frame, comp)
-        what = f"the first {nf} frames"
-    t0 = time.perf_counter()
-    O.retrieve(oi, q, cfg.top_k, cfg.n_select, cfg.pool_mult, cfg.head_mode, score_mode=score_mode)
-    dt = time.perf_counter() - t0
+        rpf = min(comp[0], T)
+        for kb, nf in blocks:
+            rows = [np.concatenate([k[:, f * T:f * T + rpf, :] for f in range(nf)], axis=1) for k in kb]
+            descs = [O.descriptor(O.decode_bf16(kb[-1][:, f * T:(f + 1) * T, :])) for f in range(nf)]
+            oi.append_stored(rows, [rpf] * nf, descs)
+        what = (f"all {oi.n_frames} frames, {rpf} stored rows each (the frame's first {rpf} token rows "
+                f"in place of its k-means centroids)")
+    times = []
+    while True:
+        t0 = time.perf_counter()
+        O.retrieve(oi, q, cfg.top_k, cfg.n_select, cfg.pool_mult, cfg.head_mode, score_mode=score_mode)
+        times.append(time.perf_counter() - t0)
+        if times[0] >= 3.0 or len(times) == 3:
+            break
+    dt = float(np.median(times))
     keys = oi.n_rows * cfg.n_layers * cfg.n_kv_heads
     return {"value": keys / dt, "unit": "keys/s", "cores": int(cores), "kind": "oracle",
             "cpu": cpu_model(),
             "sample": f"float64 oracle retrieval (scores, top-k, votes, pool, max-min) over {what} "
                       f"({oi.n_rows} rows per (layer, KV head)) of stream 0 of {cfg.name} with its queries "
-                      f"and parameters: {keys} key vectors in {dt:.2f} s"}
+                      f"and parameters: {keys} key vectors in {dt:.2f} s "
+                      f"({'median of ' + str(len(times)) + ' runs' if len(times) > 1 else 'one run'})"}
 
 
 def main():

@@ -2132,8 +2132,14 @@ __device__ __forceinline__ float hp_candidate_values(const ListArgs& a, int list
   const float inv_h = 1.0f / (float)Hq;
   for (int i = threadIdx.x; i < n; i += blockDim.x) {
     float al = 0.f;
-#pragma unroll 8
-    for (int h = 0; h < Hq; ++h) al += __expf(cs[(size_t)h * a.cap + i] - lse_sh[h]);
+    for (int h0 = 0; h0 < Hq; h0 += 32) {   // 32 heads' loads in flight, summed in head order
+      float x[32];
+#pragma unroll
+      for (int j = 0; j < 32; ++j) x[j] = h0 + j < Hq ? cs[(size_t)(h0 + j) * a.cap + i] : 0.f;
+#pragma unroll
+      for (int j = 0; j < 32; ++j)
+        if (h0 + j < Hq) al += __expf(x[j] - lse_sh[h0 + j]);
+    }
     src[i] = mk_key(ord_u32(al * inv_h + 0.0f), key_row(src[i]));
   }
   __threadfence_block();
@@ -2167,7 +2173,6 @@ template <int D>
 __device__ void fallback_list_hp(const ListArgs& a, int list, uint64_t* sel, int32_t* lv, long long* lm,
                                  uint32_t* res) {
   constexpr int KS = D / 32;
-  constexpr int kHkMax = 8;
   __shared__ float chunk[kFbRows];
   __shared__ uint32_t hmax[kMaxHeadsHp];
   __shared__ unsigned long long hsum[kMaxHeadsHp];
@@ -2193,46 +2198,37 @@ __device__ void fallback_list_hp(const ListArgs& a, int list, uint64_t* sel, int
   };
   for (int h = threadIdx.x; h < Hq; h += blockDim.x) { hmax[h] = 0; hsum[h] = 0; }
   __syncthreads();
-  // pass 1: every head's largest logit
-  float mx[kHkMax];
-  double sm[kHkMax];
-#pragma unroll
-  for (int g = 0; g < kHkMax; ++g) { mx[g] = -INFINITY; sm[g] = 0.0; }
+  // pass 1: every head's largest logit (one KV head at a time, which keeps
+  // the registers of one head's running values)
   const int ntile = (n + kTile - 1) / kTile;
-  for (int t = wave; t < ntile; t += blockDim.x / kWave) {
+#pragma unroll 1
+  for (int g = 0; g < Hk; ++g) {
+    float mx = -INFINITY;
+    for (int t = wave; t < ntile; t += blockDim.x / kWave) {
+      const f32x4 acc = tile_logits(t, g);
 #pragma unroll
-    for (int g = 0; g < kHkMax; ++g) {
-      if (g < Hk) {
-        const f32x4 acc = tile_logits(t, g);
+      for (int j = 0; j < 4; ++j)
+        if (t * kTile + 4 * kg + j < n) mx = fmaxf(mx, acc[j]);
+    }
+    if (col < G && mx > -INFINITY) atomicMax(&hmax[g * G + col], ord_u32(mx));
+  }
+  __syncthreads();
+  // pass 2: every head's exp sum against its maximum (a wave's sum over its
+  // tiles in fp64, then added in fixed point)
+#pragma unroll 1
+  for (int g = 0; g < Hk; ++g) {
+    double sm = 0.0;
+    const float M = col < G ? ord_f32(hmax[g * G + col]) : 0.f;
+    for (int t = wave; t < ntile; t += blockDim.x / kWave) {
+      const f32x4 acc = tile_logits(t, g);   // uniform: the whole wave issues the loads and MFMAs
+      if (col < G) {
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          if (t * kTile + 4 * kg + j < n) mx[g] = fmaxf(mx[g], acc[j]);
+          if (t * kTile + 4 * kg + j < n) sm += (double)__expf(acc[j] - M);
       }
     }
+    if (col < G && sm > 0.0) atomicAdd(&hsum[g * G + col], (unsigned long long)llrint(ldexp(sm, kBelowExp)));
   }
-#pragma unroll
-  for (int g = 0; g < kHkMax; ++g)
-    if (g < Hk && col < G && mx[g] > -INFINITY) atomicMax(&hmax[g * G + col], ord_u32(mx[g]));
-  __syncthreads();
-  // pass 2: every head's exp sum against its maximum
-  for (int t = wave; t < ntile; t += blockDim.x / kWave) {
-#pragma unroll
-    for (int g = 0; g < kHkMax; ++g) {
-      if (g < Hk) {   // uniform: the whole wave issues the loads and MFMAs
-        const f32x4 acc = tile_logits(t, g);
-        if (col < G) {
-          const float M = ord_f32(hmax[g * G + col]);
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            if (t * kTile + 4 * kg + j < n) sm[g] += (double)__expf(acc[j] - M);
-        }
-      }
-    }
-  }
-#pragma unroll
-  for (int g = 0; g < kHkMax; ++g)
-    if (g < Hk && col < G && sm[g] > 0.0)
-      atomicAdd(&hsum[g * G + col], (unsigned long long)llrint(ldexp(sm[g], kBelowExp)));
   __syncthreads();
   for (int h = threadIdx.x; h < Hq; h += blockDim.x)
     lse_sh[h] = ord_f32(hmax[h]) + (float)log(ldexp((double)hsum[h], -kBelowExp));
