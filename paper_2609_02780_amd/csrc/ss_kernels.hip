@@ -2132,14 +2132,8 @@ __device__ __forceinline__ float hp_candidate_values(const ListArgs& a, int list
   const float inv_h = 1.0f / (float)Hq;
   for (int i = threadIdx.x; i < n; i += blockDim.x) {
     float al = 0.f;
-    for (int h0 = 0; h0 < Hq; h0 += 32) {   // 32 heads' loads in flight, summed in head order
-      float x[32];
-#pragma unroll
-      for (int j = 0; j < 32; ++j) x[j] = h0 + j < Hq ? cs[(size_t)(h0 + j) * a.cap + i] : 0.f;
-#pragma unroll
-      for (int j = 0; j < 32; ++j)
-        if (h0 + j < Hq) al += __expf(x[j] - lse_sh[h0 + j]);
-    }
+#pragma unroll 8
+    for (int h = 0; h < Hq; ++h) al += __expf(cs[(size_t)h * a.cap + i] - lse_sh[h]);
     src[i] = mk_key(ord_u32(al * inv_h + 0.0f), key_row(src[i]));
   }
   __threadfence_block();
