@@ -32,7 +32,9 @@ import workloads as W  # noqa: E402
 HBM_PEAK_GBS = 8000.0
 METRIC = "index keys scored/sec + % HBM roofline; p50 ss_retrieve latency, 1-hour index"
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_02780_amd", "csrc", "ss_kernels.hip")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_stream_c4_traffic.md")
+# committed PMC summaries of the streaming kernel per (workload, score mode)
+TRAFFIC_FILES = {("C4", 0): "k_stream_c4_traffic.md", ("C5", 0): "k_stream_c5_traffic.md",
+                 ("P4", 0): "k_stream_hm_p4_traffic.md", ("P4", 1): "k_stream_hp_p4_traffic.md"}
 HOT_KERNEL = "k_stream<128>"
 
 
@@ -45,12 +47,15 @@ def kernel_hash() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def stored_traffic(per_launch_bytes_alg: float):
-    """HBM bytes per launch of the hot kernel from the committed PMC summary, if it
-    was taken on the current kernel source; else None."""
-    if not os.path.exists(TRAFFIC_FILE):
+def stored_traffic(cfg_name: str, score_mode: int):
+    """HBM bytes per launch of the hot kernel from the committed PMC summary of
+    this workload, if there is one and it was taken on the current kernel
+    source; else None."""
+    name = TRAFFIC_FILES.get((cfg_name, score_mode))
+    path = os.path.join(ROOT, "profiles", name) if name else None
+    if path is None or not os.path.exists(path):
         return None
-    text = open(TRAFFIC_FILE).read()
+    text = open(path).read()
     m_hash = re.search(r"kernel source sha256\[:16\]:\s*([0-9a-f]{16})", text)
     m_bytes = re.search(r"HBM bytes per launch:\s*([0-9.eE+]+)", text)
     if not m_hash or not m_bytes or m_hash.group(1) != kernel_hash():
@@ -434,7 +439,7 @@ def main():
     ms_per_step = (t1 - t0) * 1e3 / K
     value = key_vectors / (ms_per_step / 1e3)
     achieved = key_bytes / (hot.mean() / 1e3) / 1e9
-    traffic = stored_traffic(key_bytes) if cfg.name == "C4" else None  # the PMC summary covers C4
+    traffic = stored_traffic(cfg.name, args.score_mode)
     out = {
         "metric": METRIC,
         "value": value,
