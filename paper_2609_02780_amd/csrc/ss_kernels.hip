@@ -1609,9 +1609,10 @@ __device__ void stream_exponent(const ListArgs& a, int s) {
   }
 }
 
-// The sample (m <= kThrItems * 1024 scores) sits in registers.  The blocks of a
-// stream also clear its frame accumulators, and its first block fixes the
-// stream's mass exponent.
+// The sample (m <= N * 1024 scores, N <= kThrItems, chosen at launch from the
+// largest sample) sits in registers.  The blocks of a stream also clear its
+// frame accumulators, and its first block fixes the stream's mass exponent.
+template <int N>
 __device__ __forceinline__ void thresh_list(const ListArgs& a) {
   __shared__ uint32_t hist[kSelHist];
   __shared__ uint32_t res[4];
@@ -1635,23 +1636,23 @@ __device__ __forceinline__ void thresh_list(const ListArgs& a) {
     return;
   }
   const float* v = a.samp + (size_t)list * a.samp_stride;
-  uint32_t x[kThrItems];
-  bool ok[kThrItems];
+  uint32_t x[N];
+  bool ok[N];
   uint32_t mn = 0xFFFFFFFFu, mx = 0;
   // every load issued at once, from clamped in-bounds indices (m >= 1); the
   // stream's mass exponent (first block) while they are in flight
 #pragma unroll
-  for (int it = 0; it < kThrItems; ++it) x[it] = __float_as_uint(v[min((int)threadIdx.x + it * 1024, m - 1)]);
+  for (int it = 0; it < N; ++it) x[it] = __float_as_uint(v[min((int)threadIdx.x + it * 1024, m - 1)]);
   if (ll == 0) stream_exponent(a, s);
 #pragma unroll
-  for (int it = 0; it < kThrItems; ++it) {
+  for (int it = 0; it < N; ++it) {
     ok[it] = (int)threadIdx.x + it * 1024 < m;
     x[it] = ok[it] ? ord_u32(__uint_as_float(x[it]) + 0.0f) : 0u;
     if (ok[it]) { mn = min(mn, x[it]); mx = max(mx, x[it]); }
   }
   block_minmax_u32(mn, mx, mm);
   uint32_t ng, ne;
-  const uint32_t t = block_select_range<kThrItems, true>(x, ok, mn, mx, (uint32_t)r, hist, res, ng, ne);
+  const uint32_t t = block_select_range<N, true>(x, ok, mn, mx, (uint32_t)r, hist, res, ng, ne);
   if (threadIdx.x == 0) a.tau[list] = t;
 }
 
@@ -1660,11 +1661,29 @@ __device__ __forceinline__ void thresh_list(const ListArgs& a) {
 // 16-stream batch: 1,536) the dense variant fits two blocks per CU in 64 VGPRs
 // with a few spills, three rounds of blocks instead of six (41 -> 32 us on that
 // batch).
+template <int N>
 __global__ __launch_bounds__(1024) void k_thresh(ListArgs a) {
-  thresh_list(a);
+  thresh_list<N>(a);
 }
+template <int N>
 __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(8, 8))) void k_thresh_dense(ListArgs a) {
-  thresh_list(a);
+  thresh_list<N>(a);
+}
+
+// Launches the cut-off kernel with the fewest sample slots per thread that
+// hold the largest sample.
+void launch_thresh(const ListArgs& la, int lists, int m_max, bool dense, hipStream_t st) {
+  const dim3 g(lists), b(1024);
+  if (m_max <= 4096) {
+    if (dense) hipLaunchKernelGGL(k_thresh_dense<4>, g, b, 0, st, la);
+    else hipLaunchKernelGGL(k_thresh<4>, g, b, 0, st, la);
+  } else if (m_max <= 8192) {
+    if (dense) hipLaunchKernelGGL(k_thresh_dense<8>, g, b, 0, st, la);
+    else hipLaunchKernelGGL(k_thresh<8>, g, b, 0, st, la);
+  } else {
+    if (dense) hipLaunchKernelGGL(k_thresh_dense<kThrItems>, g, b, 0, st, la);
+    else hipLaunchKernelGGL(k_thresh<kThrItems>, g, b, 0, st, la);
+  }
 }
 
 // Sum of a wave's doubles in a fixed butterfly (every lane gets the total).
@@ -2260,51 +2279,61 @@ struct SelectShared {
   long long lm[kVoteLds];
 };
 
+// The register path of select_candidates: N candidates per thread (of 1024);
+// the values (high halves) and inverted rows in registers: the k-th value,
+// then the cut among the ties at that value by row.
+template <int N>
+__device__ __forceinline__ void select_in_registers(const uint64_t* src, int n, int kk, uint64_t* sel,
+                                                    uint32_t* hist, uint32_t* res, uint32_t& ngather,
+                                                    uint32_t* mm) {
+  uint32_t u[N], w[N];
+  bool ok[N], tie[N];
+  uint32_t mn = 0xFFFFFFFFu, mx = 0;
+#pragma unroll
+  for (int it = 0; it < N; ++it) {
+    const int i = threadIdx.x + it * 1024;
+    ok[it] = i < n;
+    const uint64_t k = ok[it] ? src[i] : 0;
+    u[it] = (uint32_t)(k >> 32);
+    w[it] = (uint32_t)k;  // 0xFFFFFFFF - row: larger for lower rows
+    if (ok[it]) { mn = min(mn, u[it]); mx = max(mx, u[it]); }
+  }
+  block_minmax_u32(mn, mx, mm);
+  uint32_t n_gt, n_eq;
+  const uint32_t vstar = block_select_range<N, false>(u, ok, mn, mx, (uint32_t)kk, hist, res, n_gt, n_eq);
+  const uint32_t need = (uint32_t)kk - n_gt;
+  uint32_t wcut = 0;  // ties with w >= wcut (the `need` lowest rows) are taken
+  if (n_eq > need) {
+    uint32_t wmin = 0xFFFFFFFFu, wmax = 0;
+#pragma unroll
+    for (int it = 0; it < N; ++it) {
+      tie[it] = ok[it] && u[it] == vstar;
+      if (tie[it]) { wmin = min(wmin, w[it]); wmax = max(wmax, w[it]); }
+    }
+    block_minmax_u32(wmin, wmax, mm);
+    uint32_t g2, e2;
+    wcut = block_select_range<N, false>(w, tie, wmin, wmax, need, hist, res, g2, e2);
+  }
+#pragma unroll
+  for (int it = 0; it < N; ++it) {
+    if (ok[it] && (u[it] > vstar || (u[it] == vstar && w[it] >= wcut))) {
+      const uint32_t slot = atomicAdd(&ngather, 1u);
+      if (slot < (uint32_t)kMaxTopK) sel[slot] = ((uint64_t)u[it] << 32) | w[it];
+    }
+  }
+}
+
 // Exact top-kk of a list's n candidate keys (composite: value, then row) into
-// `sel`, in any order: the values (high halves) and inverted rows in
-// registers for up to 8,192 candidates, else a radix selection over the keys
-// in global memory.  Ends with a barrier.
+// `sel`, in any order: in registers for up to 8,192 candidates (4 per thread up
+// to 4,096, so that the passes over them issue no idle slots), else a radix
+// selection over the keys in global memory.  Ends with a barrier.
 __device__ __forceinline__ void select_candidates(const uint64_t* src, int n, int kk, uint64_t* sel, uint32_t* hist,
                                                   uint32_t* res, uint32_t& ngather, uint32_t* mm) {
   if (threadIdx.x == 0) ngather = 0;
-  if (n <= 1024 * kSelItems) {
-    // scores (high halves) and inverted rows in registers: the k-th score, then
-    // the cut among the ties at that score by row
-    uint32_t u[kSelItems], w[kSelItems];
-    bool ok[kSelItems], tie[kSelItems];
-    uint32_t mn = 0xFFFFFFFFu, mx = 0;
-#pragma unroll
-    for (int it = 0; it < kSelItems; ++it) {
-      const int i = threadIdx.x + it * 1024;
-      ok[it] = i < n;
-      const uint64_t k = ok[it] ? src[i] : 0;
-      u[it] = (uint32_t)(k >> 32);
-      w[it] = (uint32_t)k;  // 0xFFFFFFFF - row: larger for lower rows
-      if (ok[it]) { mn = min(mn, u[it]); mx = max(mx, u[it]); }
-    }
-    block_minmax_u32(mn, mx, mm);
-    uint32_t n_gt, n_eq;
-    const uint32_t vstar = block_select_range<kSelItems, false>(u, ok, mn, mx, (uint32_t)kk, hist, res, n_gt, n_eq);
-    const uint32_t need = (uint32_t)kk - n_gt;
-    uint32_t wcut = 0;  // ties with w >= wcut (the `need` lowest rows) are taken
-    if (n_eq > need) {
-      uint32_t wmin = 0xFFFFFFFFu, wmax = 0;
-#pragma unroll
-      for (int it = 0; it < kSelItems; ++it) {
-        tie[it] = ok[it] && u[it] == vstar;
-        if (tie[it]) { wmin = min(wmin, w[it]); wmax = max(wmax, w[it]); }
-      }
-      block_minmax_u32(wmin, wmax, mm);
-      uint32_t g2, e2;
-      wcut = block_select_range<kSelItems, false>(w, tie, wmin, wmax, need, hist, res, g2, e2);
-    }
-#pragma unroll
-    for (int it = 0; it < kSelItems; ++it) {
-      if (ok[it] && (u[it] > vstar || (u[it] == vstar && w[it] >= wcut))) {
-        const uint32_t slot = atomicAdd(&ngather, 1u);
-        if (slot < (uint32_t)kMaxTopK) sel[slot] = ((uint64_t)u[it] << 32) | w[it];
-      }
-    }
+  if (n <= 1024 * 4) {
+    select_in_registers<4>(src, n, kk, sel, hist, res, ngather, mm);
+  } else if (n <= 1024 * kSelItems) {
+    select_in_registers<kSelItems>(src, n, kk, sel, hist, res, ngather, mm);
   } else {
     // large candidate sets: radix select over the keys in global memory
     __syncthreads();
@@ -4049,11 +4078,10 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
     hipLaunchKernelGGL(k_alpha, dim3(lists, cdiv(p.m_max, 256)), dim3(256), 0, st, la, p.alpha);
     ListArgs lt = la;   // the cut-off over the estimated attention of the sample
     lt.samp = p.alpha;
-    hipLaunchKernelGGL(k_thresh, dim3(lists), dim3(1024), 0, st, lt);
-  } else if (lists > 2 * cus)
-    hipLaunchKernelGGL(k_thresh_dense, dim3(lists), dim3(1024), 0, st, la);
-  else
-    hipLaunchKernelGGL(k_thresh, dim3(lists), dim3(1024), 0, st, la);
+    launch_thresh(lt, lists, p.m_max, false, st);
+  } else {
+    launch_thresh(la, lists, p.m_max, lists > 2 * cus, st);
+  }
   // 4. streaming pass over every key row
   if (p.ev_start) (void)hipEventRecord(p.ev_start, st);
   if (p.head_mode == 0) {
