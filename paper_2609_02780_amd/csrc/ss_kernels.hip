@@ -163,15 +163,32 @@ __device__ __forceinline__ int wave_excl_count(bool p) {
   return __popcll(m & ((1ull << lane) - 1ull));
 }
 
+// Inclusive prefix sum over the lanes of a wave (lane 0 first): DPP row_shr
+// steps of 1, 2, 4 and 8 within each row of 16 lanes, then the totals of the
+// rows below, read from lanes 15, 31 and 47.
+__device__ __forceinline__ uint32_t wave_prefix_u32(uint32_t v) {
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, false);   // row_shr 1
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, false);   // row_shr 2
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, false);   // row_shr 4
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, false);   // row_shr 8
+  const uint32_t r0 = (uint32_t)__builtin_amdgcn_readlane((int)v, 15);
+  const uint32_t r1 = (uint32_t)__builtin_amdgcn_readlane((int)v, 31);
+  const uint32_t r2 = (uint32_t)__builtin_amdgcn_readlane((int)v, 47);
+  const int row = (int)(threadIdx.x & (kWave - 1)) >> 4;
+  return v + (row > 0 ? r0 : 0u) + (row > 1 ? r1 : 0u) + (row > 2 ? r2 : 0u);
+}
+
+// Inclusive suffix sum over the lanes of a wave (the lane and every higher one).
+__device__ __forceinline__ uint32_t wave_suffix_u32(uint32_t v) {
+  const uint32_t p = wave_prefix_u32(v);
+  return (uint32_t)__builtin_amdgcn_readlane((int)p, kWave - 1) - p + v;
+}
+
 // Block-wide exclusive scan of `v`; `sh` needs blockDim/64 + 1 ints.  Returns the
 // thread's exclusive prefix; `total` receives the block sum.
 __device__ int block_excl_scan(int v, int* sh, int& total) {
   const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  int x = v;
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
+  const int x = (int)wave_prefix_u32((uint32_t)v);   // inclusive, wraps like int adds
   if (lane == kWave - 1) sh[w] = x;
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -226,11 +243,7 @@ __device__ void find_digit(const uint32_t* hist, uint32_t need, uint32_t* res) {
     const uint32_t h0 = hist[4 * lane], h1 = hist[4 * lane + 1], h2 = hist[4 * lane + 2],
                    h3 = hist[4 * lane + 3];
     const uint32_t mine = h0 + h1 + h2 + h3;
-    uint32_t x = mine;  // inclusive suffix sum over lanes >= lane
-    for (int o = 1; o < kWave; o <<= 1) {
-      const uint32_t y = __shfl_down(x, o);
-      if (lane + o < kWave) x += y;
-    }
+    const uint32_t x = wave_suffix_u32(mine);  // inclusive suffix sum over lanes >= lane
     const uint32_t above = x - mine;  // elements in bins of higher lanes
     if (above < need && need <= above + mine) {
       uint32_t a = above;
@@ -267,11 +280,7 @@ __device__ void find_digit_wide(const uint32_t* hist, uint32_t need, uint32_t* r
     uint32_t hs[BPL], mine = 0;
 #pragma unroll
     for (int j = 0; j < BPL; ++j) { hs[j] = hl[j]; mine += hs[j]; }
-    uint32_t x = mine;  // inclusive suffix sum over lanes >= lane
-    for (int o = 1; o < kWave; o <<= 1) {
-      const uint32_t y = __shfl_down(x, o);
-      if (lane + o < kWave) x += y;
-    }
+    const uint32_t x = wave_suffix_u32(mine);  // inclusive suffix sum over lanes >= lane
     const uint32_t above = x - mine;
     if (above < need && need <= above + mine) {
       uint32_t a = above;
@@ -1425,7 +1434,10 @@ __device__ void finish_bin_by_counting(const uint32_t (&v)[N], const bool (&ok)[
   __syncthreads();
 #pragma unroll
   for (int i = 0; i < N; ++i)
-    if (ok[i] && v[i] >= lo && v[i] <= hi) vals[atomicAdd(&res[3], 1u)] = v[i];
+    if (ok[i] && v[i] >= lo && v[i] <= hi) {
+      const uint32_t slot = atomicAdd(&res[3], 1u);
+      if (slot < (uint32_t)kWave) vals[slot] = v[i];   // the bin holds eq <= 64 values
+    }
   __syncthreads();
   if (threadIdx.x < kWave) {
     const int lane = threadIdx.x;
