@@ -352,6 +352,28 @@ def test_long_stream_global_paths():
     log("long stream", rep)
 
 
+def test_sample_of_more_than_8192_rows():
+    """A list of 2,000,000 rows with k = 16: the planner samples about 14,300
+    rows, so the cut-off holds 16 sample slots per thread (the widest
+    instantiation); both head modes staged against the oracle."""
+    import paper_2609_02780_amd as P
+    cfg = W.Config("bigsample", 1, 2, 1, 64, 500, 2, 16, 4, n_frames=4000, n_planted=2)
+    n = cfg.n_frames * cfg.tokens_per_frame
+    m = P.sample_plan(n, cfg.top_k)[0]
+    log("big sample: rows", n, "sampled", m)
+    assert 8192 < m <= 16384
+    spec = W.stream_specs(cfg)[0]
+    q, keys = W.make_stream(cfg, spec)
+    g, o = make_pair(cfg, spec, keys)
+    for hm in (0, 1):
+        out = debug_run([g], [q], cfg.top_k, cfg.n_select, head_mode=hm)
+        stats = out["list_stats"][0]
+        log("big sample, head mode", hm, "candidates", stats[:, 0].tolist(), "fallbacks", stats[:, 1].tolist())
+        assert stats[:, 1].sum() == 0
+        rep = staged_check(o, q, out, 0, cfg.top_k, cfg.n_select, head_mode=hm)
+        log("big sample, head mode", hm, rep)
+
+
 def test_group_of_16_query_heads():
     """G = 16 query heads per KV head (the largest group: 16 MFMA columns for
     the hi chain and 16 for the lo chain), d = 64 and d = 128."""
