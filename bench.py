@@ -127,6 +127,29 @@ def time_append(torch, P, cfg, frames=64):
             "batch_frames_per_s": frames / (batch_ms / 1e3)}
 
 
+def timed_calls(torch, r, queries, calls, kernel=None):
+    """Per-call times in ms from HIP events: around each whole call, or (with
+    `kernel`, the package) around its streaming kernel, recorded by the library
+    on the call's stream.  The calls are queued back to back."""
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(calls)]
+    for e2 in ev:   # torch reads elapsed times only of events it has recorded once
+        for e in e2:
+            e.record()
+    torch.cuda.synchronize()
+    for a, b in ev:
+        if kernel is not None:
+            kernel.set_profile_events(a, b)
+            r(queries)
+        else:
+            a.record()
+            r(queries)
+            b.record()
+    if kernel is not None:
+        kernel.set_profile_events(None, None)
+    torch.cuda.synchronize()
+    return np.array([a.elapsed_time(b) for a, b in ev])
+
+
 def time_cold(torch, P, r, queries, key_bytes, calls=20, scratch_bytes=512 << 20):
     """Cold-cache retrieval: before each call a 512 MB scratch buffer is written,
     which evicts the index from L2 and the 256 MB Infinity Cache; the call and its
@@ -357,8 +380,8 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=40)
-    ap.add_argument("--events-every", type=int, default=4,
-                    help="record the latency and streaming-kernel events on every N-th timed step")
+    ap.add_argument("--samples", type=int, default=20,
+                    help="calls timed one by one with HIP events (latency percentiles, streaming kernel)")
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="C4", choices=sorted(W.CONFIGS))
     ap.add_argument("--score-mode", type=int, default=0, choices=(0, 1),
@@ -407,31 +430,19 @@ def main():
         r(queries)
     torch.cuda.synchronize()
 
-    # HIP events cost about 5 us each on the stream, so only every `every`-th timed
-    # step records them (call latency and the streaming kernel); the other steps
-    # run back to back as a serving loop would
-    K, every = args.steps, max(1, args.events_every)
-    sampled = list(range(0, K, every))
-    ev = {i: [torch.cuda.Event(enable_timing=True) for _ in range(4)] for i in sampled}
-    for e4 in ev.values():
-        for e in e4:
-            e.record()
+    # the timed steps run back to back with no event between them, as a serving
+    # loop would (a HIP event costs about 5 us of stream time); the latency
+    # percentiles and the streaming kernel's time come from separate passes of
+    # `samples` calls, each bracketed by its own events
+    K = args.steps
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(K):
-        e4 = ev.get(i)
-        if e4 is None:
-            r(queries)
-            continue
-        P.set_profile_events(e4[2], e4[3])
-        e4[0].record()
+    for _ in range(K):
         r(queries)
-        e4[1].record()
-        P.set_profile_events(None, None)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    lat = np.array([e[0].elapsed_time(e[1]) for e in ev.values()])
-    hot = np.array([e[2].elapsed_time(e[3]) for e in ev.values()])
+    lat = timed_calls(torch, r, queries, args.samples)
+    hot = timed_calls(torch, r, queries, args.samples, kernel=P)
 
     rows = [x.n_rows for x in idxs]
     key_vectors = sum(x.n_rows for x in idxs) * cfg.n_layers * cfg.n_kv_heads

@@ -1581,15 +1581,12 @@ __device__ __forceinline__ int frame_of_row(const ListArgs& a, int s, uint32_t r
 // mode 1 sums the KV heads' columns); with 2% headroom for fp32 rounding this
 // bounds all E = NL * kk selected scores of the stream, and at scale 2^x with
 // x = 61 - e - c (bound < 2^e, E <= 2^c) any sum of them stays below 2^61.
-// Run by wave 0 of the block alone (no block barrier).
-__device__ void stream_exponent(const ListArgs& a, int s) {
-  if (threadIdx.x >= kWave) return;
-  if (a.score_mode == 1) {
-    // attention probabilities: a list's selected values add up to at most 1,
-    // so a frame's mass is below NL <= 2^12 and 2^50 keeps every sum below 2^62
-    if (threadIdx.x == 0) a.sexp[s] = kProbMassExp;
-    return;
-  }
+// Computed by every lane of wave 0 (no block barrier); every selection block
+// of the stream gets the same value.
+__device__ int stream_exponent(const ListArgs& a, int s) {
+  // attention probabilities: a list's selected values add up to at most 1, so
+  // a frame's mass is below NL <= 2^12 and 2^50 keeps every sum below 2^62
+  if (a.score_mode == 1) return kProbMassExp;
   const int L = a.L, Hk = a.Hk;
   const float* qc = a.qcol + (size_t)s * L * Hk * 16;
   const float km = __uint_as_float(*a.kmax[s]);   // issued with the column loads
@@ -1605,25 +1602,29 @@ __device__ void stream_exponent(const ListArgs& a, int s) {
     }
   }
   b = __uint_as_float(wave_max_u32(__float_as_uint(b)));   // non-negative: ordered as integers
-  if (threadIdx.x == 0) {
-    const float bound = b * km * 1.02f;
-    const int E = a.NL * a.kk[s];
-    int x = 120;                          // all scores are zero
-    if (!(bound <= 3.0e38f)) {
-      x = -120;                           // non-finite keys or queries
-    } else if (bound > 0.f) {
-      int e;
-      frexpf(bound, &e);                  // bound < 2^e
-      const int c = (E > 1) ? 32 - __clz(E - 1) : 0;
-      x = min(120, max(-120, 61 - e - c));
-    }
-    a.sexp[s] = x;
+  const float bound = b * km * 1.02f;
+  const int E = a.NL * a.kk[s];
+  int x = 120;                          // all scores are zero
+  if (!(bound <= 3.0e38f)) {
+    x = -120;                           // non-finite keys or queries
+  } else if (bound > 0.f) {
+    int e;
+    frexpf(bound, &e);                  // bound < 2^e
+    const int c = (E > 1) ? 32 - __clz(E - 1) : 0;
+    x = min(120, max(-120, 61 - e - c));
   }
+  return x;
+}
+
+// The stream's mass exponent in the selection block (LDS).
+__device__ __forceinline__ int& list_mass_exponent() {
+  __shared__ int xs;
+  return xs;
 }
 
 // The sample (m <= N * 1024 scores, N <= kThrItems, chosen at launch from the
 // largest sample) sits in registers.  The blocks of a stream also clear its
-// frame accumulators, and its first block fixes the stream's mass exponent.
+// frame accumulators.
 template <int N>
 __device__ __forceinline__ void thresh_list(const ListArgs& a) {
   __shared__ uint32_t hist[kSelHist];
@@ -1643,7 +1644,6 @@ __device__ __forceinline__ void thresh_list(const ListArgs& a) {
     }
   }
   if (m == 0 || r == 0) {
-    if (ll == 0) stream_exponent(a, s);
     if (threadIdx.x == 0) a.tau[list] = 0xFFFFFFFFu;
     return;
   }
@@ -1651,11 +1651,9 @@ __device__ __forceinline__ void thresh_list(const ListArgs& a) {
   uint32_t x[N];
   bool ok[N];
   uint32_t mn = 0xFFFFFFFFu, mx = 0;
-  // every load issued at once, from clamped in-bounds indices (m >= 1); the
-  // stream's mass exponent (first block) while they are in flight
+  // every load issued at once, from clamped in-bounds indices (m >= 1)
 #pragma unroll
   for (int it = 0; it < N; ++it) x[it] = __float_as_uint(v[min((int)threadIdx.x + it * 1024, m - 1)]);
-  if (ll == 0) stream_exponent(a, s);
 #pragma unroll
   for (int it = 0; it < N; ++it) {
     ok[it] = (int)threadIdx.x + it * 1024 < m;
@@ -1680,6 +1678,149 @@ __global__ __launch_bounds__(1024) void k_thresh(ListArgs a) {
 template <int N>
 __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(8, 8))) void k_thresh_dense(ListArgs a) {
   thresh_list<N>(a);
+}
+
+// k_prep_thresh: query prep, sample scores and the cut-off of one list per
+// block in a single launch (head mode 0, d = 128, when every list's block fits
+// one round and the sample fits N slots per thread; used for short samples).  The block forms its list
+// group's B tile with the prep's exact sums (the group's first list publishes
+// it for the streaming pass), scores every sampled row of the group against it
+// with the sample pass's arithmetic (so a row gets the streaming pass's bits),
+// keeps its own column in LDS and takes the r-th largest by the cut-off
+// kernel's radix selection: the sample never goes through global memory and
+// the cut-off needs no second launch.  The group's blocks read the same sampled
+// rows; on a 256-CU device (block b on XCD b mod 8) each XCD takes whole list
+// groups, so those rows come from its L2 after the first read.
+struct PtArgs {
+  int NL, L, Hq, Hk, G, f_max;
+  int xcd_map;                          // lists (b mod 8) * (lists / 8) + b / 8
+  const uint16_t* keys[kMaxStreams];
+  int32_t stride[kMaxStreams];          // rows per (layer, KV head) in the arena
+  int32_t n[kMaxStreams];               // candidate rows
+  int32_t m[kMaxStreams];               // sampled rows per list group
+  int32_t r[kMaxStreams];               // rank of the cut-off in the sample
+  int32_t f[kMaxStreams];               // candidate frames
+  int64_t samp_step[kMaxStreams];
+  uint32_t* tau;
+  uint32_t* cnt;
+  uint64_t* below;                      // score mode 1, else null
+  uint32_t* dyn_ctr;
+  int32_t* votes_g;
+  int64_t* massfx_g;
+};
+
+constexpr int kPtDepth = 2;   // sample tiles in flight per wave
+
+template <int N>
+__global__ __launch_bounds__(1024) void k_prep_thresh(PrepArgs pa, PtArgs a) {
+  constexpr int D = 128, CPR = D / 8, TCH = 16 * CPR, NI = TCH / kWave, KS = D / 32, NW = 1024 / kWave;
+  union PtShared {
+    float part[kPrepGroups][2 * D][8];
+    u32x4 tiles[NW][TCH];
+  };
+  __shared__ PtShared sh;
+  __shared__ u32x4 bsh[2 * KS * kWave];
+  __shared__ float sv[N * 1024];
+  __shared__ uint32_t hist[kSelHist];
+  __shared__ uint32_t res[4];
+  __shared__ uint32_t mm[32];
+  const int list = a.xcd_map ? (int)(blockIdx.x % 8) * (int)(gridDim.x / 8) + (int)(blockIdx.x / 8) : (int)blockIdx.x;
+  const int s = list / a.NL, ll = list - s * a.NL;
+  const int l = ll / a.Hq, h = ll - l * a.Hq, g = h / a.G, mycol = h - g * a.G;
+  const int m = a.m[s], r = a.r[s];
+  // the list's candidate count and exp sum, the streaming pass's chunk
+  // counters and a slice of the stream's frame accumulators start at zero
+  if (threadIdx.x == 0) a.cnt[list] = 0;
+  if (a.below && threadIdx.x == 0) a.below[list] = 0;
+  if (list == 0 && threadIdx.x < kDynCtr) a.dyn_ctr[threadIdx.x * kDynStride] = 0;
+  {
+    int32_t* vg = a.votes_g + (size_t)s * a.f_max;
+    int64_t* mg = a.massfx_g + (size_t)s * a.f_max;
+    for (int f = ll * 1024 + threadIdx.x; f < a.f[s]; f += a.NL * 1024) {
+      vg[f] = 0;
+      mg[f] = 0;
+    }
+  }
+  prep_b<D>(pa, s * a.L + l, g, sh.part, bsh, mycol == 0);
+  if (m == 0 || r == 0) {
+    if (threadIdx.x == 0) a.tau[list] = 0xFFFFFFFFu;
+    return;
+  }
+  __syncthreads();   // the B tile is in LDS and the partial sums are read no more
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
+  u32x4 bh[KS], bl[KS];
+#pragma unroll
+  for (int i = 0; i < KS; ++i) {
+    bh[i] = bsh[i * kWave + lane];
+    bl[i] = bsh[(KS + i) * kWave + lane];
+  }
+  const int n = a.n[s], nt = (m + kTile - 1) / kTile;
+  const int64_t step = a.samp_step[s];
+  const uint16_t* seg = a.keys[s] + ((size_t)l * a.Hk + g) * (size_t)a.stride[s] * D;
+  const __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(seg), (short)0, n * D * 2, 0x00020000);
+  // chunk q = 64 i + lane of tile t is chunk q mod CPR of sample t 16 + q / CPR;
+  // past the samples the loads read zeros without touching memory
+  auto issue = [&](int t, u32x4 (&V)[NI]) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int q = i * kWave + lane, u = t * kTile + q / CPR;
+      const uint32_t off = (t < nt && u < m) ? (uint32_t)sample_row(step, u) * (CPR * 16) + (q % CPR) * 16
+                                             : 0x80000000u;
+      V[i] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, kAuxNT);
+    }
+  };
+  u32x4* lt_ = sh.tiles[wave];
+  // wave w scores tiles w, w + NW, ...; kPtDepth of them in flight
+  u32x4 V[kPtDepth][NI];
+#pragma unroll
+  for (int d = 0; d < kPtDepth; ++d) issue(wave + d * NW, V[d]);
+  for (int t0 = wave; t0 < nt; t0 += kPtDepth * NW) {
+#pragma unroll
+    for (int d = 0; d < kPtDepth; ++d) {
+      const int t = t0 + d * NW;
+      if (t >= nt) break;
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const int q = i * kWave + lane, R = q >> 4, C = q & 15;
+        lt_[R * 16 + (C ^ (R & 15))] = V[d][i];
+      }
+      issue(t + kPtDepth * NW, V[d]);
+      __builtin_amdgcn_wave_barrier();
+      u32x4 A[KS];
+#pragma unroll
+      for (int i = 0; i < KS; ++i) {
+        const int q = rl * CPR + 4 * i + kg, R = q >> 4, C = q & 15;
+        A[i] = lt_[R * 16 + (C ^ (R & 15))];
+      }
+      __builtin_amdgcn_wave_barrier();
+      const f32x4 acc = score_hilo<KS>(A, bh, bl);
+      if (col == mycol) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int u = t * kTile + 4 * kg + j;
+          if (u < m) sv[u] = acc[j] + 0.0f;
+        }
+      }
+    }
+  }
+  __syncthreads();
+  uint32_t x[N];
+  bool ok[N];
+  uint32_t mn = 0xFFFFFFFFu, mx = 0;
+#pragma unroll
+  for (int it = 0; it < N; ++it) {
+    const int i = (int)threadIdx.x + it * 1024;
+    ok[it] = i < m;
+    x[it] = ok[it] ? ord_u32(sv[i]) : 0u;
+    if (ok[it]) { mn = min(mn, x[it]); mx = max(mx, x[it]); }
+  }
+  block_minmax_u32(mn, mx, mm);
+  uint32_t ng, ne;
+  const uint32_t t = block_select_range<N, true>(x, ok, mn, mx, (uint32_t)r, hist, res, ng, ne);
+  if (threadIdx.x == 0) a.tau[list] = t;
 }
 
 // Launches the cut-off kernel with the fewest sample slots per thread that
@@ -1837,7 +1978,7 @@ __device__ void finish_list(const ListArgs& a, int list, uint64_t* sel, int kk,
                             int32_t* lv, long long* lm) {
   const int s = list / a.NL;
   const int F = a.f[s];
-  const int xs = a.sexp[s];
+  const int xs = list_mass_exponent();
   int32_t* vg = a.votes_g + (size_t)s * a.f_max;
   unsigned long long* mg = reinterpret_cast<unsigned long long*>(a.massfx_g + (size_t)s * a.f_max);
   if (F <= kVoteLds) {
@@ -2294,10 +2435,12 @@ struct SelectShared {
 // The register path of select_candidates: N candidates per thread (of 1024);
 // the values (high halves) and inverted rows in registers: the k-th value,
 // then the cut among the ties at that value by row.
+// Exact top-kk of the n keys the block holds in registers (key it of thread t
+// is candidate t + 1024 it; keys past n are ignored) into `sel`.
 template <int N>
-__device__ __forceinline__ void select_in_registers(const uint64_t* src, int n, int kk, uint64_t* sel,
-                                                    uint32_t* hist, uint32_t* res, uint32_t& ngather,
-                                                    uint32_t* mm) {
+__device__ __forceinline__ void select_from_keys(const uint64_t (&key)[N], int n, int kk, uint64_t* sel,
+                                                 uint32_t* hist, uint32_t* res, uint32_t& ngather,
+                                                 uint32_t* mm) {
   uint32_t u[N], w[N];
   bool ok[N], tie[N];
   uint32_t mn = 0xFFFFFFFFu, mx = 0;
@@ -2305,7 +2448,7 @@ __device__ __forceinline__ void select_in_registers(const uint64_t* src, int n, 
   for (int it = 0; it < N; ++it) {
     const int i = threadIdx.x + it * 1024;
     ok[it] = i < n;
-    const uint64_t k = ok[it] ? src[i] : 0;
+    const uint64_t k = ok[it] ? key[it] : 0;
     u[it] = (uint32_t)(k >> 32);
     w[it] = (uint32_t)k;  // 0xFFFFFFFF - row: larger for lower rows
     if (ok[it]) { mn = min(mn, u[it]); mx = max(mx, u[it]); }
@@ -2333,6 +2476,19 @@ __device__ __forceinline__ void select_in_registers(const uint64_t* src, int n, 
       if (slot < (uint32_t)kMaxTopK) sel[slot] = ((uint64_t)u[it] << 32) | w[it];
     }
   }
+}
+
+template <int N>
+__device__ __forceinline__ void select_in_registers(const uint64_t* src, int n, int kk, uint64_t* sel,
+                                                    uint32_t* hist, uint32_t* res, uint32_t& ngather,
+                                                    uint32_t* mm) {
+  uint64_t key[N];
+#pragma unroll
+  for (int it = 0; it < N; ++it) {
+    const int i = threadIdx.x + it * 1024;
+    key[it] = i < n ? src[i] : 0;
+  }
+  select_from_keys<N>(key, n, kk, sel, hist, res, ngather, mm);
 }
 
 // Exact top-kk of a list's n candidate keys (composite: value, then row) into
@@ -2372,17 +2528,42 @@ __device__ void select_list(const ListArgs& a, int list, SelectShared& sh, uint3
   long long* lm = sh.lm;
   const int s = list / a.NL;
   const int kk = a.kk[s];
-  if (kk == 0) {
+  if (kk == 0) {   // no rows: nothing is voted, the exponent only has to be finite
+    if (threadIdx.x == 0 && list == s * a.NL) a.sexp[s] = 0;
     finish_list(a, list, sel, 0, lv, lm);
     return;
   }
   const uint32_t c = a.cnt[list];
-  int fallback = (c < (uint32_t)kk || c > (uint32_t)a.cap) ? 1 : 0;
   uint64_t* src = a.cand + (size_t)list * a.cap;
+  // the first 4,096 candidate slots are read together with the count (from
+  // clamped in-bounds slots; slots past the count are ignored): one round trip
+  // instead of two for the usual list
+  uint64_t pre[4];
+  if (!HP) {
+#pragma unroll
+    for (int it = 0; it < 4; ++it) pre[it] = src[min((int)threadIdx.x + it * 1024, a.cap - 1)];
+  }
+  // the stream's mass exponent, by wave 0 while the candidates load (every
+  // path below passes block barriers before finish_list reads it); the
+  // stream's first list publishes it for the pool
+  if (threadIdx.x < kWave) {
+    const int xs = stream_exponent(a, s);
+    if (threadIdx.x == 0) {
+      list_mass_exponent() = xs;
+      if (list == s * a.NL) a.sexp[s] = xs;
+    }
+  }
+  int fallback = (c < (uint32_t)kk || c > (uint32_t)a.cap) ? 1 : 0;
   float rho = 0.f;
   if (HP && !fallback) rho = hp_candidate_values(a, list, (int)c);
   if (!fallback) {
-    select_candidates(src, (int)c, kk, sel, hist, res, ngather, mm);
+    if (!HP && c <= 4096u) {
+      if (threadIdx.x == 0) ngather = 0;
+      select_from_keys<4>(pre, (int)c, kk, sel, hist, res, ngather, mm);
+      __syncthreads();
+    } else {
+      select_candidates(src, (int)c, kk, sel, hist, res, ngather, mm);
+    }
     // head mode 1, attention probabilities: the selection is exact when its
     // k-th value beats every row the streaming pass left out (fallback 2)
     if (HP && !hp_selection_proven(a, list, sel, kk, rho, mm)) fallback = 2;
@@ -2458,7 +2639,13 @@ struct PoolShared {
   int vstar, above, inb;
 };
 
-__device__ int pool_select(const VoteArgs& a, int s, PoolShared& sh) {
+// `lds_ids` (optional, kMaxPool entries) receives the ordered pool's frame ids
+// for the caller's block; with `write_out` false the block writes nothing to
+// global memory (several blocks of a stream may rank the same pool, and then
+// only one publishes it; its records must then fit in LDS: at most kPoolSort
+// candidate frames).
+__device__ int pool_select(const VoteArgs& a, int s, PoolShared& sh, int* lds_ids = nullptr,
+                           bool write_out = true) {
   const int F = a.f[s];
   const int32_t* votes = a.votes_g + (size_t)s * a.f_max;
   const int64_t* massfx = a.massfx_g + (size_t)s * a.f_max;
@@ -2483,7 +2670,7 @@ __device__ int pool_select(const VoteArgs& a, int s, PoolShared& sh) {
       const int f = f0 + u * (int)blockDim.x + (int)threadIdx.x;
       const int v = vv[u];
       const int64_t mf = mm[u];
-      if (a.dbg_vote_hist && f < F) {
+      if (write_out && a.dbg_vote_hist && f < F) {
         a.dbg_vote_hist[(size_t)s * a.hist_stride + a.hist0[s] + f] = v;
         a.dbg_mass_hist[(size_t)s * a.hist_stride + a.hist0[s] + f] = (float)((double)mf * inv);
       }
@@ -2504,7 +2691,7 @@ __device__ int pool_select(const VoteArgs& a, int s, PoolShared& sh) {
       }
     }
   }
-  if (a.dbg_vote_hist) {
+  if (write_out && a.dbg_vote_hist) {
     for (int f = threadIdx.x; f < a.hist_stride; f += blockDim.x) {
       if (f >= a.hist0[s] && f < a.hist0[s] + F) continue;
       a.dbg_vote_hist[(size_t)s * a.hist_stride + f] = 0;
@@ -2610,13 +2797,15 @@ __device__ int pool_select(const VoteArgs& a, int s, PoolShared& sh) {
       v = (int)(sh.shi[i] >> 32);
       const uint64_t mb = (sh.shi[i] << 32) | (sh.slo[i] >> 32);
       m = (float)((double)(int64_t)(mb ^ 0x8000000000000000ull) * inv);
+      if (lds_ids) lds_ids[i] = id;
     }
+    if (!write_out) continue;
     a.pool_ids[(size_t)s * P + i] = id;
     a.pool_votes[(size_t)s * P + i] = v;
     a.pool_mass[(size_t)s * P + i] = m;
     if (a.dbg_pool) a.dbg_pool[(size_t)s * P + i] = id >= 0 ? (int32_t)(id + a.frame0[s]) : -1;
   }
-  if (threadIdx.x == 0) {
+  if (write_out && threadIdx.x == 0) {
     a.pool_n[s] = pn;
     if (a.dbg_pool_n) a.dbg_pool_n[s] = pn;
   }
@@ -2677,12 +2866,74 @@ struct MaxminArgs {
 // operations on the same fp32 values).
 struct MaxminShared {
   uint32_t d_lds[kGramLdsPool * kGramLdsPool];
+  int32_t pid[kGramLdsPool];
+  int32_t pvotes[kGramLdsPool];
+  float pmass[kGramLdsPool];
   float mind[kMaxPool];
   int taken[kMaxPool];
   int sel[kMaxSelect];
   float shv[16];
   int shi[16];
 };
+
+// Wave maximum left in every lane: DPP within rows of 16 lanes, then gfx950's
+// row swaps (the max of a value and its swapped partner needs no lane select),
+// all on the vector unit.
+__device__ __forceinline__ uint32_t wave_max_all_u32(uint32_t v) {
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x124, 0xF, 0xF, false));  // row_ror 4
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x128, 0xF, 0xF, false));  // row_ror 8
+  auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  v = max(v, max((uint32_t)r[0], (uint32_t)r[1]));
+  r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return max(v, max((uint32_t)r[0], (uint32_t)r[1]));
+}
+
+// The greedy over distance words d_lds[r * kGramLdsPool + c] = ord(1 - g_rc)
+// of a pool of pn <= kGramLdsPool frames, with d_lds[r * kGramLdsPool + r] = 0
+// (entries of columns >= pn are never used): the first K picks into sel.  Run
+// by wave 0 of the block.  Lane l holds pool ranks l and l + 64; picked and
+// absent ranks hold 0 (a pick's own row zeroes it), below every distance
+// word, so min() keeps them out of every later argmax; argmax by a wave max,
+// ties to the lowest rank through ballots; lane i keeps the i-th pick.
+__device__ __forceinline__ void maxmin_greedy_lds(const uint32_t* d_lds, int pn, int K, int* sel) {
+  if (threadIdx.x >= kWave) return;
+  const int lane = threadIdx.x;
+  uint32_t m0 = (lane > 0 && lane < pn) ? d_lds[lane] : 0u;
+  uint32_t m1 = lane + kWave < pn ? d_lds[lane + kWave] : 0u;
+  int pick = 0;
+  for (int it = 1; it < K; ++it) {
+    const uint32_t best = wave_max_all_u32(max(m0, m1));
+    const uint64_t b0 = __ballot(m0 == best), b1 = __ballot(m1 == best);
+    const int bi = b0 ? __builtin_ctzll(b0) : kWave + __builtin_ctzll(b1);
+    const uint32_t* row = d_lds + bi * kGramLdsPool;
+    m0 = min(m0, row[lane]);
+    m1 = min(m1, row[lane + kWave]);
+    pick = lane == it ? bi : pick;
+  }
+  if (lane < K) sel[lane] = pick;
+}
+
+// The K picks in selection order (pool ranks in sel), -1 padded to n_select;
+// ids, votes and mass of the stream's pool by rank.
+__device__ __forceinline__ void maxmin_write(const MaxminArgs& a, int s, int K, const int* sel, const int32_t* ids,
+                                             const int32_t* votes, const float* mass) {
+  for (int i = threadIdx.x; i < a.n_select; i += blockDim.x) {
+    const size_t o = (size_t)s * a.n_select + i;
+    if (i < K) {
+      const int p = sel[i];
+      a.out_ids[o] = ids[p] + a.frame0[s];
+      a.out_votes[o] = votes[p];
+      a.out_mass[o] = mass[p];
+    } else {
+      a.out_ids[o] = -1;
+      a.out_votes[o] = 0;
+      a.out_mass[o] = 0.f;
+    }
+  }
+  if (threadIdx.x == 0) a.out_n[s] = K;
+}
 
 __device__ void maxmin_block(const MaxminArgs& a, int s, MaxminShared& sh) {
   uint32_t* d_lds = sh.d_lds;
@@ -2691,61 +2942,55 @@ __device__ void maxmin_block(const MaxminArgs& a, int s, MaxminShared& sh) {
   int* sel = sh.sel;
   float* shv = sh.shv;
   int* shi = sh.shi;
+  const float* G = a.gram + (size_t)s * a.pool * a.ld;
+  if (a.pool <= kGramLdsPool) {
+    // row r, column c < 128: ord(1 - g_rc) for c < pn, c != r, else 0 (below
+    // every distance word, like a frame already picked).  Every row of the
+    // pool's capacity is read at once, with the pool size, as float4 from
+    // clamped in-bounds addresses (ld % 4 == 0, ld >= pool); what a clamped
+    // read or a row past the pool returns is never used.
+    constexpr int C4 = kGramLdsPool / 4;
+    const int nq = a.pool * C4;   // <= 4 float4 per thread
+    const int pn = a.pool_n[s];
+    const int t = threadIdx.x;    // the pool by rank, loaded with the matrix
+    int32_t pid = 0, pv = 0;
+    float pm = 0.f;
+    if (t < a.pool) {
+      pid = a.pool_ids[(size_t)s * a.pool + t];
+      pv = a.pool_votes[(size_t)s * a.pool + t];
+      pm = a.pool_mass[(size_t)s * a.pool + t];
+    }
+    float4 x[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = min(u * (int)blockDim.x + (int)threadIdx.x, nq - 1);
+      const int r = i / C4, c = min(4 * (i - r * C4), a.ld - 4);
+      x[u] = *reinterpret_cast<const float4*>(G + (size_t)r * a.ld + c);
+    }
+    const int K = min(a.n_select, pn);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = u * blockDim.x + threadIdx.x;
+      if (i < nq) {
+        const int r = i / C4, c = 4 * (i - r * C4);
+        const float xv[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
+        uint4 o;
+        uint32_t* ov = reinterpret_cast<uint32_t*>(&o);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) ov[q] = (c + q < pn && c + q != r) ? ord_u32(1.0f - xv[q]) : 0u;
+        *reinterpret_cast<uint4*>(d_lds + r * kGramLdsPool + c) = o;
+      }
+    }
+    if (t < a.pool) { sh.pid[t] = pid; sh.pvotes[t] = pv; sh.pmass[t] = pm; }
+    __syncthreads();
+    maxmin_greedy_lds(d_lds, pn, K, sel);
+    __syncthreads();
+    maxmin_write(a, s, K, sel, sh.pid, sh.pvotes, sh.pmass);
+    return;
+  }
   const int pn = a.pool_n[s];
   const int K = min(a.n_select, pn);
-  const float* G = a.gram + (size_t)s * a.pool * a.ld;
-  if (pn <= kGramLdsPool) {
-    // row r, column c < 128: ord(1 - g_rc) for c < pn, else 0 (below every
-    // distance word, like a frame already picked).  Rows are read as float4 from
-    // clamped in-bounds addresses (ld % 4 == 0 and ld >= pool >= pn); what a
-    // clamped read returns is never used.
-    constexpr int C4 = kGramLdsPool / 4;
-    for (int b = 0; b < pn * C4; b += 4 * blockDim.x) {
-      float4 x[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int i = min(b + u * (int)blockDim.x + (int)threadIdx.x, pn * C4 - 1);
-        const int r = i / C4, c = min(4 * (i - r * C4), a.ld - 4);
-        x[u] = *reinterpret_cast<const float4*>(G + (size_t)r * a.ld + c);
-      }
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int i = b + u * blockDim.x + threadIdx.x;
-        if (i < pn * C4) {
-          const int r = i / C4, c = 4 * (i - r * C4);
-          const float xv[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
-          uint4 o;
-          uint32_t* ov = reinterpret_cast<uint32_t*>(&o);
-#pragma unroll
-          for (int q = 0; q < 4; ++q) ov[q] = c + q < pn ? ord_u32(1.0f - xv[q]) : 0u;
-          *reinterpret_cast<uint4*>(d_lds + r * kGramLdsPool + c) = o;
-        }
-      }
-    }
-    __syncthreads();
-    if (threadIdx.x < kWave) {
-      // lane l holds pool ranks l and l + 64; picked and absent ranks hold 0, so
-      // min() keeps them out of every later argmax; argmax by a DPP max, ties
-      // to the lowest rank through ballots
-      const int lane = threadIdx.x;
-      uint32_t m0 = lane == 0 ? 0u : d_lds[lane];
-      uint32_t m1 = d_lds[lane + kWave];
-      if (lane == 0 && K > 0) sel[0] = 0;
-      for (int it = 1; it < K; ++it) {
-        const uint32_t best = wave_max_u32(max(m0, m1));
-        const uint64_t b0 = __ballot(m0 == best), b1 = __ballot(m1 == best);
-        const int bi = b0 ? __builtin_ctzll(b0) : kWave + __builtin_ctzll(b1);
-        const uint32_t* row = d_lds + bi * kGramLdsPool;
-        const uint32_t r0 = row[lane], r1 = row[lane + kWave];
-        m0 = min(m0, r0);
-        m1 = min(m1, r1);
-        m0 = lane == bi ? 0u : m0;
-        m1 = lane + kWave == bi ? 0u : m1;
-        if (lane == 0) sel[it] = bi;
-      }
-    }
-    __syncthreads();
-  } else {
+  {
     for (int u = threadIdx.x; u < pn; u += blockDim.x) {
       mind[u] = 1.0f - G[u];          // distance to pool rank 0
       taken[u] = (u == 0);
@@ -2767,20 +3012,8 @@ __device__ void maxmin_block(const MaxminArgs& a, int s, MaxminShared& sh) {
       __syncthreads();
     }
   }
-  for (int i = threadIdx.x; i < a.n_select; i += blockDim.x) {
-    const size_t o = (size_t)s * a.n_select + i;
-    if (i < K) {
-      const int p = sel[i];
-      a.out_ids[o] = a.pool_ids[(size_t)s * a.pool + p] + a.frame0[s];
-      a.out_votes[o] = a.pool_votes[(size_t)s * a.pool + p];
-      a.out_mass[o] = a.pool_mass[(size_t)s * a.pool + p];
-    } else {
-      a.out_ids[o] = -1;
-      a.out_votes[o] = 0;
-      a.out_mass[o] = 0.f;
-    }
-  }
-  if (threadIdx.x == 0) a.out_n[s] = K;
+  maxmin_write(a, s, K, sel, a.pool_ids + (size_t)s * a.pool, a.pool_votes + (size_t)s * a.pool,
+               a.pool_mass + (size_t)s * a.pool);
 }
 
 __global__ __launch_bounds__(1024) void k_maxmin(MaxminArgs a) {
@@ -2803,7 +3036,51 @@ struct GramArgs {
   float* gram;          // [S][pool][ld]
 };
 
+// Tile (ti, tj) of stream s from the pool's frame ids `ids` (pn of them);
+// called by the whole block, waves 0..3 compute, `part` is 4 KiB of LDS.
 template <int NST>   // 16-dimension steps per wave: dim / 64
+__device__ __forceinline__ void gram_tile(const GramArgs& a, int s, int ti, int tj, int pn,
+                                          const int32_t* ids, float (*part)[256]) {
+  const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x >> 6;
+  constexpr int dim = 64 * NST;
+  if (w < 4) {
+    // rows past the pool repeat its last row: they only feed tile entries that
+    // are never stored
+    const int ri = min(ti * 16 + (lane & 15), pn - 1), rj = min(tj * 16 + (lane & 15), pn - 1);
+    const float* xi = a.desc[s] + (size_t)ids[ri] * dim + w * (dim / 4) + 4 * (lane >> 4);
+    const float* xj = a.desc[s] + (size_t)ids[rj] * dim + w * (dim / 4) + 4 * (lane >> 4);
+    float4 va[NST], vb[NST];
+#pragma unroll
+    for (int u = 0; u < NST; ++u) {
+      va[u] = *reinterpret_cast<const float4*>(xi + 16 * u);
+      vb[u] = *reinterpret_cast<const float4*>(xj + 16 * u);
+    }
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int u = 0; u < NST; ++u) {
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(va[u].x, vb[u].x, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(va[u].y, vb[u].y, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(va[u].z, vb[u].z, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(va[u].w, vb[u].w, acc, 0, 0, 0);
+    }
+    // lane l holds tile rows 4 (l >> 4) + j, column l & 15
+#pragma unroll
+    for (int j = 0; j < 4; ++j) part[w][(4 * (lane >> 4) + j) * 16 + (lane & 15)] = acc[j];
+  }
+  __syncthreads();
+  if (threadIdx.x < 256) {
+    const int r = threadIdx.x >> 4, c = threadIdx.x & 15;
+    const float v = ((part[0][threadIdx.x] + part[1][threadIdx.x]) + part[2][threadIdx.x]) + part[3][threadIdx.x];
+    const int pi = ti * 16 + r, pj = tj * 16 + c;
+    if (pi < pn && pj < pn) {
+      float* G = a.gram + (size_t)s * a.pool * a.ld;
+      G[(size_t)pi * a.ld + pj] = v;
+      G[(size_t)pj * a.ld + pi] = v;
+    }
+  }
+}
+
+template <int NST>
 __global__ __launch_bounds__(256) void k_gram(GramArgs a) {
   __shared__ float part[4][256];
   const int s = blockIdx.x / (a.tiles * a.tiles);
@@ -2811,47 +3088,36 @@ __global__ __launch_bounds__(256) void k_gram(GramArgs a) {
   const int ti = t / a.tiles, tj = t % a.tiles;
   const int pn = a.pool_n[s];
   if (tj < ti || ti * 16 >= pn || tj * 16 >= pn) return;
-  const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x >> 6;
-  constexpr int dim = 64 * NST;
-  const int32_t* ids = a.pool_ids + (size_t)s * a.pool;
-  // rows past the pool repeat its last row: they only feed tile entries that
-  // are never stored
-  const int ri = min(ti * 16 + (lane & 15), pn - 1), rj = min(tj * 16 + (lane & 15), pn - 1);
-  const float* xi = a.desc[s] + (size_t)ids[ri] * dim + w * (dim / 4) + 4 * (lane >> 4);
-  const float* xj = a.desc[s] + (size_t)ids[rj] * dim + w * (dim / 4) + 4 * (lane >> 4);
-  float4 va[NST], vb[NST];
-#pragma unroll
-  for (int u = 0; u < NST; ++u) {
-    va[u] = *reinterpret_cast<const float4*>(xi + 16 * u);
-    vb[u] = *reinterpret_cast<const float4*>(xj + 16 * u);
-  }
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int u = 0; u < NST; ++u) {
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(va[u].x, vb[u].x, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(va[u].y, vb[u].y, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(va[u].z, vb[u].z, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(va[u].w, vb[u].w, acc, 0, 0, 0);
-  }
-  // lane l holds tile rows 4 (l >> 4) + j, column l & 15
-#pragma unroll
-  for (int j = 0; j < 4; ++j) part[w][(4 * (lane >> 4) + j) * 16 + (lane & 15)] = acc[j];
-  __syncthreads();
-  const int r = threadIdx.x >> 4, c = threadIdx.x & 15;
-  const float v = ((part[0][threadIdx.x] + part[1][threadIdx.x]) + part[2][threadIdx.x]) + part[3][threadIdx.x];
-  const int pi = ti * 16 + r, pj = tj * 16 + c;
-  if (pi < pn && pj < pn) {
-    float* G = a.gram + (size_t)s * a.pool * a.ld;
-    G[(size_t)pi * a.ld + pj] = v;
-    G[(size_t)pj * a.ld + pi] = v;
-  }
+  gram_tile<NST>(a, s, ti, tj, pn, a.pool_ids + (size_t)s * a.pool, part);
 }
 
-// k_gram<1..N> launchers indexed by dim / 64 - 1
-using GramLaunch = void (*)(dim3, const GramArgs&, hipStream_t);
+// The pool and its Gram matrix in one launch, for streams of at most kPoolSort
+// candidate frames: every block of the upper triangle ranks the stream's pool
+// itself (the same records, so the same pool) and computes its tile from the
+// ids in LDS; tile (0, 0) publishes the pool.  This saves the pool kernel's
+// launch and the Gram blocks' read of the pool ids.
 template <int NST>
-void launch_gram_n(dim3 g, const GramArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(k_gram<NST>, g, dim3(256), 0, st, a);
+__global__ __launch_bounds__(1024) void k_pool_gram(VoteArgs va, GramArgs a) {
+  __shared__ PoolShared psh;
+  __shared__ int32_t ids[kMaxPool];
+  __shared__ float part[4][256];
+  const int s = blockIdx.x / (a.tiles * a.tiles);
+  const int t = blockIdx.x % (a.tiles * a.tiles);
+  const int ti = t / a.tiles, tj = t % a.tiles;
+  if (tj < ti) return;
+  const int pn = pool_select(va, s, psh, ids, t == 0);
+  __syncthreads();
+  if (ti * 16 >= pn || tj * 16 >= pn) return;
+  gram_tile<NST>(a, s, ti, tj, pn, ids, part);
+}
+
+// k_gram<1..N> (pool from the pool kernel: va null) and k_pool_gram<1..N>
+// launchers indexed by dim / 64 - 1
+using GramLaunch = void (*)(dim3, const VoteArgs*, const GramArgs&, hipStream_t);
+template <int NST>
+void launch_gram_n(dim3 g, const VoteArgs* va, const GramArgs& a, hipStream_t st) {
+  if (va) hipLaunchKernelGGL(k_pool_gram<NST>, g, dim3(1024), 0, st, *va, a);
+  else hipLaunchKernelGGL(k_gram<NST>, g, dim3(256), 0, st, a);
 }
 template <int... I>
 const GramLaunch* gram_table(std::integer_sequence<int, I...>) {
@@ -4026,7 +4292,15 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   // head mode 1 with attention probabilities keeps every head's logits: its
   // prep and sample are head mode 0's (one sampled list per head)
   const int prep_hm = p.hm_prob ? 0 : p.head_mode;
-  const bool fused = prep_hm == 0 && pairs <= 128 && ps_blocks <= cus;
+  const int lists = p.S * p.NL;
+  // prep, sample and cut-off in one launch (k_prep_thresh) when every list's
+  // block fits one round and the sample is at most 2,048 rows: every block
+  // gathers its group's whole sample, which pays while that is short (A/B on
+  // one box: 10-minute index 110.9 -> 110.2 us per call, m = 1,072; compressed
+  // 58.5 -> 56.3 us, m = 262) but not at the 1-hour index's 3,216 rows
+  // (450.2 -> 456.3 us)
+  const bool pt = D == 128 && p.head_mode == 0 && !p.hm_prob && pairs <= 128 && lists <= cus && p.m_max <= 2048;
+  const bool fused = !pt && prep_hm == 0 && pairs <= 128 && ps_blocks <= cus;
   PrepArgs pa_fused{};
   for (int first = 0; first < pairs; first += 128) {
     PrepArgs a{};
@@ -4039,7 +4313,7 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
     for (int s = 0; s < p.S; ++s) { a.nq[s] = p.st[s].nq; a.qscale[s] = p.st[s].qscale; }
     a.qB = reinterpret_cast<u32x4*>(p.qB);
     a.qcol = p.qcol;
-    if (fused)
+    if (fused || pt)
       pa_fused = a;
     else
       hipLaunchKernelGGL(k_prep<D>, dim3(cnt * p.Hk), dim3(8 * D), 0, st, a);
@@ -4063,9 +4337,24 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   la.score_mode = p.score_mode; la.hm_prob = p.hm_prob ? 1 : 0; la.NLs = p.NLs;
   la.below = p.below; la.lhat = p.lhat; la.cand_sc = p.cand_sc; la.left_max = p.left_max;
   la.cand_lse = p.cand_lse;
-  const int lists = p.S * p.NL;
   // 2. sample scores, 3. thresholds
-  if (prep_hm == 0) {
+  if (pt) {
+    PtArgs t{};
+    t.NL = p.NL; t.L = p.L; t.Hq = p.Hq; t.Hk = p.Hk; t.G = p.G; t.f_max = p.f_max;
+    t.xcd_map = cus == 256 && lists % 8 == 0 && (lists / 8) % p.G == 0;
+    for (int s = 0; s < p.S; ++s) {
+      t.keys[s] = p.st[s].keys;
+      t.stride[s] = p.st[s].row_stride;
+      t.n[s] = p.st[s].n;
+      t.m[s] = p.st[s].m;
+      t.r[s] = p.st[s].r;
+      t.f[s] = p.st[s].f;
+      t.samp_step[s] = p.st[s].m > 0 ? (int64_t)(((unsigned __int128)p.st[s].n << 32) / (unsigned)p.st[s].m) : 0;
+    }
+    t.tau = p.tau; t.cnt = p.cnt; t.below = p.below; t.dyn_ctr = p.dyn_ctr;
+    t.votes_g = p.votes; t.massfx_g = p.massfx;
+    hipLaunchKernelGGL(k_prep_thresh<2>, dim3(lists), dim3(1024), 0, st, pa_fused, t);
+  } else if (prep_hm == 0) {
     ScoreArgs a = make_score_args(p, K_SAMPLE);
     a.NL = p.NLs;        // sampled lists: one per (layer, query head)
     a.head_mode = 0;
@@ -4091,7 +4380,7 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
     ListArgs lt = la;   // the cut-off over the estimated attention of the sample
     lt.samp = p.alpha;
     launch_thresh(lt, lists, p.m_max, false, st);
-  } else {
+  } else if (!pt) {
     launch_thresh(la, lists, p.m_max, lists > 2 * cus, st);
   }
   // 4. streaming pass over every key row
@@ -4166,7 +4455,6 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
     hipLaunchKernelGGL(k_select_hp<D>, dim3(lists), dim3(1024), 0, st, la);
   }
   else hipLaunchKernelGGL(k_select<D>, dim3(lists), dim3(1024), 0, st, la);
-  hipLaunchKernelGGL(k_votes_pool, dim3(p.S), dim3(1024), 0, st, va);
   // 8. Gram matrix, 9. max-min
   GramArgs ga{};
   ga.pool = p.pool; ga.ld = (p.pool + 3) & ~3; ga.dim = p.Hk * D; ga.tiles = cdiv(p.pool, 16);
@@ -4179,7 +4467,11 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   for (int s = 0; s < p.S; ++s) ma.frame0[s] = p.st[s].frame0;
   ma.out_ids = p.out_ids; ma.out_votes = p.out_votes; ma.out_mass = p.out_mass; ma.out_n = p.out_n;
   if (ga.dim % 64 != 0 || ga.dim < 64 || ga.dim > kMaxDescDim) return hipErrorInvalidValue;
-  gram_launchers<kMaxDescDim / 64>()[ga.dim / 64 - 1](dim3(p.S * ga.tiles * ga.tiles), ga, st);
+  // pool and Gram matrix in one launch when every record fits in LDS
+  const bool pool_gram = p.f_max <= kPoolSort;
+  if (!pool_gram) hipLaunchKernelGGL(k_votes_pool, dim3(p.S), dim3(1024), 0, st, va);
+  gram_launchers<kMaxDescDim / 64>()[ga.dim / 64 - 1](dim3(p.S * ga.tiles * ga.tiles), pool_gram ? &va : nullptr,
+                                                      ga, st);
   hipLaunchKernelGGL(k_maxmin, dim3(p.S), dim3(1024), 0, st, ma);
   return hipGetLastError();
 }
