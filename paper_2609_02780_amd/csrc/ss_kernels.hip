@@ -1087,6 +1087,7 @@ __global__ __launch_bounds__(8 * D) void k_prep_sample(PrepArgs pa, ScoreArgs a,
   };
   __shared__ PsShared sh;
   __shared__ u32x4 bsh[2 * KS * kWave];
+  __shared__ float sout[kMaxGroup][kPsTiles * kTile];   // the block's scores, written out by whole lines
   int s = 0;
   while ((int)blockIdx.x >= ps.blk_base[s + 1]) ++s;
   const int rem = (int)blockIdx.x - ps.blk_base[s];
@@ -1100,8 +1101,6 @@ __global__ __launch_bounds__(8 * D) void k_prep_sample(PrepArgs pa, ScoreArgs a,
   u32x4* lt_ = sh.tiles[wave];
   const int n = a.n[s], m = a.units[s], nt = a.ntile[s];
   const int64_t step = a.samp_step[s];
-  const bool colv = col < a.G;
-  const int list = s * a.NL + l * a.Hq + g * a.G + col;
   u32x4 bh[KS], bl[KS];
 #pragma unroll
   for (int i = 0; i < KS; ++i) {
@@ -1144,10 +1143,16 @@ __global__ __launch_bounds__(8 * D) void k_prep_sample(PrepArgs pa, ScoreArgs a,
     __builtin_amdgcn_wave_barrier();
     const f32x4 acc = score_hilo<KS>(A, bh, bl);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int u = t * kTile + 4 * kg + j;
-      if (colv && t < nt && u < m) a.samp[(size_t)list * a.samp_stride + u] = acc[j] + 0.0f;
-    }
+    for (int j = 0; j < 4; ++j) sout[col][(wave + NW * p) * kTile + 4 * kg + j] = acc[j] + 0.0f;
+  }
+  __syncthreads();
+  // column c's kPsTiles * 16 scores are consecutive samples of list c of the
+  // group: contiguous in the sample buffer
+  const int u0 = slice * kPsTiles * kTile, nu = min(kPsTiles * kTile, m - u0);
+  const int list0 = s * a.NL + l * a.Hq + g * a.G;
+  for (int i = threadIdx.x; i < a.G * kPsTiles * kTile; i += blockDim.x) {
+    const int c = i / (kPsTiles * kTile), u = i - c * (kPsTiles * kTile);
+    if (u < nu) a.samp[(size_t)(list0 + c) * a.samp_stride + u0 + u] = sout[c][u];
   }
 }
 
