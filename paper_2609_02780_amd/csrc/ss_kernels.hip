@@ -2828,6 +2828,17 @@ __global__ __launch_bounds__(1024) void k_select(ListArgs a) {
   __shared__ uint32_t mm[32];
   select_list<D, false>(a, blockIdx.x, sh, hist, res, ngather, mm);
 }
+// The same at two blocks per CU (64 VGPRs), for batches with more lists than
+// two per CU.
+template <int D>
+__global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(8, 8))) void k_select_dense(ListArgs a) {
+  __shared__ SelectShared sh;
+  __shared__ uint32_t hist[512];
+  __shared__ uint32_t res[4];
+  __shared__ uint32_t ngather;
+  __shared__ uint32_t mm[32];
+  select_list<D, false>(a, blockIdx.x, sh, hist, res, ngather, mm);
+}
 
 // The same for head mode 1 with attention probabilities.
 template <int D>
@@ -4459,6 +4470,7 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
     hipLaunchKernelGGL(k_cand_lse, dim3(lists * p.Hq), dim3(256), 0, st, la);
     hipLaunchKernelGGL(k_select_hp<D>, dim3(lists), dim3(1024), 0, st, la);
   }
+  else if (lists > 2 * cus) hipLaunchKernelGGL(k_select_dense<D>, dim3(lists), dim3(1024), 0, st, la);
   else hipLaunchKernelGGL(k_select<D>, dim3(lists), dim3(1024), 0, st, la);
   // 8. Gram matrix, 9. max-min
   GramArgs ga{};
