@@ -379,7 +379,7 @@ def cpu_baseline(cfg, host0, score_mode: int = 0):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=40)
+    ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--samples", type=int, default=20,
                     help="calls timed one by one with HIP events (latency percentiles, streaming kernel)")
     ap.add_argument("--warmup", type=int, default=5)
