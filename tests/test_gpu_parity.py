@@ -412,6 +412,30 @@ def test_more_streams_than_one_launch():
     log("40 streams staged")
 
 
+def test_largest_pool_and_selection():
+    """The largest frame budget the boundary takes (K = 64) with the pool
+    multiplier 4: a pool of 256 frames, beyond the 128 whose distances max-min
+    keeps in LDS (its block-wide greedy over the Gram matrix in global memory)
+    and a 16 x 16 grid of Gram tiles; 10-minute head shape (G = 7, d = 128) on
+    300 frames, of which more than 128 get votes.  Staged against the oracle
+    (the greedy property of the selection checked on the oracle's
+    descriptors)."""
+    base = W.CONFIGS["C2"]
+    cfg = W.Config("pool256", base.n_layers, base.n_q_heads, base.n_kv_heads, base.head_dim, 196, base.n_q,
+                   base.top_k, 64, n_frames=300, n_planted=4)
+    spec = W.stream_specs(cfg)[0]
+    q, keys = W.make_stream(cfg, spec)
+    gidx, oidx = make_pair(cfg, spec, keys)
+    out = debug_run([gidx], [q], cfg.top_k, 64, 4)
+    pn = int(out["pool_n"][0])
+    log("voted frames in the pool:", pn)
+    assert 128 < pn <= 256          # more than the LDS-resident distances hold
+    assert int(out["n_out"][0]) == 64
+    rep = staged_check(oidx, q, out, 0, cfg.top_k, 64, 4)
+    log("K = 64, pool 256:", rep)
+    assert rep["lists"] == cfg.n_layers * cfg.n_q_heads
+
+
 def test_deterministic_repeat():
     cfg, spec, q, keys = c1()
     gidx, _ = make_pair(cfg, spec, keys)
