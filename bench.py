@@ -150,6 +150,30 @@ def timed_calls(torch, r, queries, calls, kernel=None):
     return np.array([a.elapsed_time(b) for a, b in ev])
 
 
+def time_serving(torch, P, idxs, queries, cfg, score_mode, key_vectors, key_bytes, want_ids, calls=100):
+    """Two queries in flight, as a serving loop may keep them: two retrievers
+    (each its own workspace and outputs) take the calls in turn on two HIP
+    streams of default priority, so one call's small kernels can run beside the
+    other's streaming pass.  Whole-loop wall time per call; every call's frame
+    ids must equal the single-stream call's."""
+    rs = [P.Retriever(idxs, cfg.top_k, cfg.n_select, cfg.pool_mult, cfg.head_mode, score_mode) for _ in range(2)]
+    sts = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for i in range(4):
+        rs[i % 2](queries, stream=sts[i % 2])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(calls):
+        rs[i % 2](queries, stream=sts[i % 2])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for r2 in rs:
+        if not torch.equal(r2.frame_ids, want_ids):
+            raise RuntimeError("a two-stream call's frame ids differ from the single-stream call's")
+    ms = (t1 - t0) * 1e3 / calls
+    return {"streams": 2, "calls": calls, "ms_per_call": ms, "keys_per_s": key_vectors / (ms / 1e3),
+            "hbm_frac": key_bytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS}
+
+
 def time_cold(torch, P, r, queries, key_bytes, calls=20, scratch_bytes=512 << 20):
     """Cold-cache retrieval: before each call a 512 MB scratch buffer is written,
     which evicts the index from L2 and the 256 MB Infinity Cache; the call and its
@@ -482,6 +506,8 @@ def main():
                      "avg_kernel_ms": float(hot.mean()), "bytes_per_launch": key_bytes,
                      "event_samples": len(hot)},
     }
+    out["serving_two_streams"] = time_serving(torch, P, idxs, queries, cfg, args.score_mode, key_vectors,
+                                              key_bytes, r.frame_ids.clone())
     out["evidence"] = time_evidence(torch, P, idxs, r.frame_ids)
     if args.cold or key_bytes <= (1 << 30):   # indices that a warm Infinity Cache could hold
         out["cold"] = time_cold(torch, P, r, queries, key_bytes)

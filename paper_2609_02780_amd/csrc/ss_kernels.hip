@@ -8,6 +8,8 @@
 //               (k_score<SAMPLE> in head mode 1).  k_prep_sample does both
 //               steps in one launch when its blocks fit one round.
 //   k_thresh    per list, the r-th largest sample score: the streaming cut-off.
+//               k_prep_thresh does prep, sample and cut-off in one launch for
+//               short samples (one block per list).
 //   k_stream    THE HOT KERNEL: streams every bf16 key row from HBM once.
 //               The 16-row tiles of all lists form one sequence, cut into
 //               XCD-weighted group ranges (plus a handed-out tail on
@@ -24,11 +26,14 @@
 //               candidate count left [k, capacity] recomputes all of its scores
 //               and selects exactly from them instead.  Each list then adds its
 //               selected rows up per frame (count, fixed-point score sum).
+//               k_select_dense runs two blocks per CU for many lists.
 //   k_votes_pool  per stream, the vote-ranked pool from the frames' votes and
 //               fixed-point attention mass: a vote histogram fixes the cut,
 //               frames tied at it are ranked by counting (a radix cut over the
 //               128-bit records when many tie), the pool is ranked by counting.
-//   k_gram      fp32 Gram matrix of the pool descriptors.
+//   k_gram      fp32 Gram matrix of the pool descriptors.  k_pool_gram does
+//               both in one launch (every Gram block ranks the pool itself)
+//               when a stream's records fit in LDS.
 //   k_maxmin    greedy max-min diversity over the Gram matrix.
 //
 // Append: k_unit_means (pooled keys and the Eq. memory_key descriptor), k_copy (raw rows) or k_kmeans
