@@ -411,6 +411,8 @@ def main():
     ap.add_argument("--score-mode", type=int, default=0, choices=(0, 1),
                     help="list values: 0 scaled logits (the workloads' default), 1 attention probabilities")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--serving", action="store_true",
+                    help="also time two queries in flight on two streams (serving_two_streams)")
     ap.add_argument("--cold", action="store_true",
                     help="also time cold-cache calls (on by default for indices of at most 1 GiB)")
     ap.add_argument("--sweep", action="store_true",
@@ -506,8 +508,9 @@ def main():
                      "avg_kernel_ms": float(hot.mean()), "bytes_per_launch": key_bytes,
                      "event_samples": len(hot)},
     }
-    out["serving_two_streams"] = time_serving(torch, P, idxs, queries, cfg, args.score_mode, key_vectors,
-                                              key_bytes, r.frame_ids.clone())
+    if args.serving:
+        out["serving_two_streams"] = time_serving(torch, P, idxs, queries, cfg, args.score_mode, key_vectors,
+                                                  key_bytes, r.frame_ids.clone())
     out["evidence"] = time_evidence(torch, P, idxs, r.frame_ids)
     if args.cold or key_bytes <= (1 << 30):   # indices that a warm Infinity Cache could hold
         out["cold"] = time_cold(torch, P, r, queries, key_bytes)
