@@ -633,7 +633,9 @@ __device__ __forceinline__ int lane_xor32(int x) {
 
 // Candidates of the streaming pass wait in LDS, kStage per (wave, column), and
 // go to the list's global buffer in one flush: one global atomic per (wave,
-// column, flush) keeps returning atomics out of the tile loop.  `lc` is the
+// column, flush) keeps returning atomics out of the tile loop (a full stage
+// flushes here; at a segment end k_stream flushes a whole block at once,
+// block_flush below).  `lc` is the
 // staged count of the lane's column, the same in the column's four lanes.
 // The waves whose range crosses a frame where most rows pass (the frames that
 // collect the votes) flush most and finish last; 64 keys per column instead of
@@ -706,6 +708,59 @@ __device__ __forceinline__ void below_flush(uint64_t* dst, bool colv, int kg, do
   if (kg == 0 && colv && x > 0.0)
     atomicAdd(reinterpret_cast<unsigned long long*>(dst), (unsigned long long)llrint(ldexp(x * scale, kBelowExp)));
   v = 0.0;
+}
+
+// The end of a segment visit for a whole block of k_stream: every wave calls
+// it at the same segment end (the waves of a group walk the same segments).
+// The waves of a group end a segment together, and their atomics on a list's
+// counter queue one behind the other at the memory side (returning or not:
+// with one per wave, C3's pass took 6 us and C4's 5 us longer than with none).
+// One per (block, column) shortens that queue fourfold: per call, C3 56.4 ->
+// 51.6 us, C2 110.9 -> 109.2 us, C4 449.8 -> 446.2 us, C5 2,000 -> 1,995 us;
+// the head-mode-1 passes, with one list per layer, did not gain.  Each wave's
+// keys go to the block's slot range after those of the lower waves.  With `prob`, each wave's exp sum below the cut-off is rounded
+// to fixed point as in below_flush and the block adds the integers, so the
+// total does not depend on how the sums are grouped.
+template <int NW>
+struct FlushShared {
+  uint32_t cnt[NW][16];          // staged keys per (wave, column)
+  uint32_t base[16];             // the column's first slot
+  unsigned long long below[16];  // the column's fixed-point exp sum (zero between flushes)
+};
+
+template <int NW>
+__device__ __forceinline__ void block_flush(const ScoreArgs& a, int list, bool colv, int col, int kg, int wave,
+                                            const uint64_t* st, int& lc, bool prob, double& bsum,
+                                            FlushShared<NW>& fl) {
+  if (kg == 0) fl.cnt[wave][col] = colv ? (uint32_t)lc : 0u;
+  if (prob) {
+    double x = bsum;
+    x += __shfl_xor(x, 16);
+    x += __shfl_xor(x, 32);
+    if (kg == 0 && colv && x > 0.0) atomicAdd(&fl.below[col], (unsigned long long)llrint(ldexp(x, kBelowExp)));
+    bsum = 0.0;
+  }
+  __syncthreads();
+  if (wave == 0 && kg == 0 && colv) {
+    uint32_t tot = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) tot += fl.cnt[w][col];
+    fl.base[col] = tot ? atomicAdd(&a.cnt[list], tot) : 0u;
+    if (prob) {
+      const unsigned long long b = fl.below[col];
+      if (b) atomicAdd(reinterpret_cast<unsigned long long*>(&a.below[list]), b);
+      fl.below[col] = 0;
+    }
+  }
+  __syncthreads();
+  uint32_t base = fl.base[col];
+  for (int w = 0; w < wave; ++w) base += fl.cnt[w][col];
+  for (int e = kg; e < lc; e += 4) {
+    const uint32_t slot = base + (uint32_t)e;
+    if (slot < (uint32_t)a.cap) a.cand[(size_t)list * a.cap + slot] = st[col * kStage + e];
+  }
+  lc = 0;
+  __syncthreads();   // the tables are rewritten at the next segment end
 }
 
 // Head-mode 0: one KV head per item, its G query heads in the MFMA columns, the
@@ -877,6 +932,9 @@ __global__ __launch_bounds__(256) void k_stream(ScoreArgs a) {
   constexpr int PF = 128 / D;       // tiles in flight per wave
   __shared__ u32x4 tiles[4][TCH];
   __shared__ uint64_t stage[4 * kMaxGroup * kStage];
+  __shared__ FlushShared<4> fl;
+  if (threadIdx.x < 16) fl.below[threadIdx.x] = 0;
+  __syncthreads();
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: segment state in SGPRs
   const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
@@ -887,7 +945,9 @@ __global__ __launch_bounds__(256) void k_stream(ScoreArgs a) {
   // the last dyn_tiles handed out by the chunk counters to whichever waves are
   // free (the waves that visit many segments flush more and fall behind).
   const int64_t total = a.tile_base[a.S], static_end = total - a.dyn_tiles;
-  auto run_range = [&](const WaveRange& wr) {
+  // bsync: every wave of the block walks the same segments (a group range),
+  // so each segment visit ends in one flush for the whole block
+  auto run_range = [&](const WaveRange& wr, bool bsync) {
     const int SW = wr.sw;
     for (int64_t T = wr.b0; T < wr.b1;) {
       int s = 0;
@@ -899,7 +959,7 @@ __global__ __launch_bounds__(256) void k_stream(ScoreArgs a) {
       const int t1 = (int)min<int64_t>(nt, tb + (wr.b1 - T));
       const int t0 = first_tile(wr, T, tb);
       T += t1 - tb;
-      if (t0 >= t1) continue;
+      if (t0 >= t1 && !bsync) continue;   // (in a block flush the wave takes part with no keys)
       const int g = lg % a.Hk, l = lg / a.Hk;
       const int n = a.n[s];
       const bool colv = col < a.G;
@@ -957,11 +1017,15 @@ __global__ __launch_bounds__(256) void k_stream(ScoreArgs a) {
           if (tt < t1) stream_emit(a, list, colv, col, tau_f, tt * kTile, n, acc, kg, st, lc, bsum, prob);
         }
       }
-      if (__any(lc > 0)) stage_flush(a, list, colv, col, kg, st, lc);
-      if (prob) below_flush(&a.below[list], colv, kg, bsum, 1.0);
+      if (bsync) {
+        block_flush<4>(a, list, colv, col, kg, wave, st, lc, prob, bsum, fl);
+      } else {
+        if (__any(lc > 0)) stage_flush(a, list, colv, col, kg, st, lc);
+        if (prob) below_flush(&a.below[list], colv, kg, bsum, 1.0);
+      }
     }
   };
-  run_range(wave_range(static_end, wave, a.sgroup, a.xcd_weights != 0));
+  run_range(wave_range(static_end, wave, a.sgroup, a.xcd_weights != 0), true);
   if (a.dyn_tiles > 0) {
     // K = min(kDynCtr, grid / 8) counters (at least one); counter k serves the
     // chunks k, k + K, ..., and block b uses counter (b / 8) mod K, so every
@@ -982,7 +1046,7 @@ __global__ __launch_bounds__(256) void k_stream(ScoreArgs a) {
       d.b1 = min<int64_t>(d.b0 + a.dyn_chunk, total);
       d.sw = 1;
       d.wg = 0;
-      run_range(d);
+      run_range(d, false);
     }
   }
 }
