@@ -1162,29 +1162,21 @@ __global__ __launch_bounds__(8 * D) void k_prep_sample(PrepArgs pa, ScoreArgs a,
   const int rem = (int)blockIdx.x - ps.blk_base[s];
   const int lg = rem / ps.spg[s], slice = rem - lg * ps.spg[s];
   const int l = lg / a.Hk, g = lg - l * a.Hk;
-  prep_b<D>(pa, s * a.L + l, g, sh.part, bsh, slice == 0);
-  __syncthreads();   // the B tile is in LDS and the partial sums are read no more
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
-  u32x4* lt_ = sh.tiles[wave];
   const int n = a.n[s], m = a.units[s], nt = a.ntile[s];
   const int64_t step = a.samp_step[s];
-  u32x4 bh[KS], bl[KS];
-#pragma unroll
-  for (int i = 0; i < KS; ++i) {
-    bh[i] = bsh[i * kWave + lane];
-    bl[i] = bsh[(KS + i) * kWave + lane];
-  }
   const uint16_t* seg = a.keys[s] + ((size_t)l * a.Hk + g) * (size_t)a.stride[s] * D;
   const __amdgpu_buffer_rsrc_t rsrc =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(seg), (short)0, n * D * 2, 0x00020000);
   // wave w scores tiles slice kPsTiles + w + NW p (p < PF); chunk q = 64 i +
   // lane of tile t is chunk q mod CPR of sample t 16 + q / CPR; past the
-  // group's tiles or samples the loads read zeros without touching memory
+  // group's tiles or samples the loads read zeros without touching memory.
+  // The first tile's loads go out before the query prep (they need no B
+  // tile), the others after it (all of them before would spill).
   u32x4 V[PF][NI];
-#pragma unroll
-  for (int p = 0; p < PF; ++p) {
+  auto issue = [&](int p) {
     const int t = slice * kPsTiles + wave + NW * p;
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
@@ -1193,7 +1185,19 @@ __global__ __launch_bounds__(8 * D) void k_prep_sample(PrepArgs pa, ScoreArgs a,
                                              : 0x80000000u;
       V[p][i] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, kAuxNT);
     }
+  };
+  issue(0);
+  prep_b<D>(pa, s * a.L + l, g, sh.part, bsh, slice == 0);
+  __syncthreads();   // the B tile is in LDS and the partial sums are read no more
+  u32x4* lt_ = sh.tiles[wave];
+  u32x4 bh[KS], bl[KS];
+#pragma unroll
+  for (int i = 0; i < KS; ++i) {
+    bh[i] = bsh[i * kWave + lane];
+    bl[i] = bsh[(KS + i) * kWave + lane];
   }
+#pragma unroll
+  for (int p = 1; p < PF; ++p) issue(p);
 #pragma unroll
   for (int p = 0; p < PF; ++p) {
     const int t = slice * kPsTiles + wave + NW * p;
@@ -1815,21 +1819,9 @@ __global__ __launch_bounds__(1024) void k_prep_thresh(PrepArgs pa, PtArgs a) {
       mg[f] = 0;
     }
   }
-  prep_b<D>(pa, s * a.L + l, g, sh.part, bsh, mycol == 0);
-  if (m == 0 || r == 0) {
-    if (threadIdx.x == 0) a.tau[list] = 0xFFFFFFFFu;
-    return;
-  }
-  __syncthreads();   // the B tile is in LDS and the partial sums are read no more
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
-  u32x4 bh[KS], bl[KS];
-#pragma unroll
-  for (int i = 0; i < KS; ++i) {
-    bh[i] = bsh[i * kWave + lane];
-    bl[i] = bsh[(KS + i) * kWave + lane];
-  }
   const int n = a.n[s], nt = (m + kTile - 1) / kTile;
   const int64_t step = a.samp_step[s];
   const uint16_t* seg = a.keys[s] + ((size_t)l * a.Hk + g) * (size_t)a.stride[s] * D;
@@ -1846,11 +1838,26 @@ __global__ __launch_bounds__(1024) void k_prep_thresh(PrepArgs pa, PtArgs a) {
       V[i] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, kAuxNT);
     }
   };
-  u32x4* lt_ = sh.tiles[wave];
-  // wave w scores tiles w, w + NW, ...; kPtDepth of them in flight
+  // wave w scores tiles w, w + NW, ...; kPtDepth of them in flight, the
+  // first issued before the query prep (it needs no B tile), so that its
+  // round trip overlaps the prep's
   u32x4 V[kPtDepth][NI];
+  issue(wave, V[0]);
+  prep_b<D>(pa, s * a.L + l, g, sh.part, bsh, mycol == 0);
 #pragma unroll
-  for (int d = 0; d < kPtDepth; ++d) issue(wave + d * NW, V[d]);
+  for (int d = 1; d < kPtDepth; ++d) issue(wave + d * NW, V[d]);
+  if (m == 0 || r == 0) {
+    if (threadIdx.x == 0) a.tau[list] = 0xFFFFFFFFu;
+    return;
+  }
+  __syncthreads();   // the B tile is in LDS and the partial sums are read no more
+  u32x4 bh[KS], bl[KS];
+#pragma unroll
+  for (int i = 0; i < KS; ++i) {
+    bh[i] = bsh[i * kWave + lane];
+    bl[i] = bsh[(KS + i) * kWave + lane];
+  }
+  u32x4* lt_ = sh.tiles[wave];
   for (int t0 = wave; t0 < nt; t0 += kPtDepth * NW) {
 #pragma unroll
     for (int d = 0; d < kPtDepth; ++d) {
