@@ -1,0 +1,76 @@
+"""GPU parity over seeded random small batches: each case draws a head shape
+(layers, KV heads, group size, head dimension), a ragged batch of one to three
+streams (frames, tokens per frame, query tokens, recent window each their
+own), the retrieval parameters (k, frame budget, pool multiplier) and both
+readings of the scores, and every stream is staged against the oracle."""
+import sys
+
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import oracle as O
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_02780_amd  # noqa: F401  (fails loudly without the built library)
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda()
+
+
+def _case(rng, i):
+    L = int(rng.choice([1, 2, 3]))
+    Hk = int(rng.choice([1, 2, 4]))
+    G = int(rng.choice([1, 2, 3, 4, 7, 8]))
+    d = int(rng.choice([64, 128]))
+    streams = []
+    for s in range(int(rng.integers(1, 4))):
+        F = int(rng.integers(3, 250))
+        streams.append(dict(F=F, T=int(rng.integers(2, 40)), nq=int(rng.integers(1, 12)),
+                            recent=int(rng.integers(0, min(4, F))), seed=1000 * i + s))
+    return dict(L=L, Hk=Hk, G=G, d=d, streams=streams, top_k=int(rng.integers(1, 200)),
+                n_select=int(rng.integers(1, 12)), pool_mult=int(rng.choice([1, 2, 4])),
+                head_mode=int(rng.integers(0, 2)), score_mode=int(rng.integers(0, 2)))
+
+
+@pytest.mark.parametrize("i", range(24))
+def test_random_small_batch_staged(i):
+    import paper_2609_02780_amd as P
+    from parity import staged_check
+    c = _case(np.random.default_rng([2609, i]), i)
+    log("case", i, {k: v for k, v in c.items() if k != "streams"}, "streams",
+        [(x["F"], x["T"], x["nq"], x["recent"]) for x in c["streams"]])
+    gs, os_, qs = [], [], []
+    for x in c["streams"]:
+        cfg = W.Config(f"rand{i}", c["L"], c["Hk"] * c["G"], c["Hk"], c["d"], x["T"], x["nq"], c["top_k"],
+                       c["n_select"], n_frames=x["F"], n_planted=min(2, x["F"] // 4))
+        spec = W.stream_specs(cfg)[0]
+        q, keys = W.make_stream(cfg, spec, seed=x["seed"])
+        g = P.ShallowIndex(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, x["F"], x["F"] * x["T"],
+                           x["recent"])
+        g.append([_dev(k) for k in keys], x["F"], x["T"])
+        o = O.Index(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, x["recent"])
+        o.append(keys, x["F"], x["T"])
+        gs.append(g)
+        os_.append(o)
+        qs.append(q)
+    r = P.Retriever(gs, c["top_k"], c["n_select"], c["pool_mult"], c["head_mode"], c["score_mode"])
+    out = r.debug([[_dev(a) for a in q] for q in qs])
+    for s in range(len(gs)):
+        rep = staged_check(os_[s], qs[s], out, s, c["top_k"], c["n_select"], c["pool_mult"],
+                           head_mode=c["head_mode"], score_mode=c["score_mode"])
+        log("  stream", s, "fallbacks", out["list_stats"][s, :, 1].tolist(), rep)
