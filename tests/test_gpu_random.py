@@ -74,3 +74,49 @@ def test_random_small_batch_staged(i):
         rep = staged_check(os_[s], qs[s], out, s, c["top_k"], c["n_select"], c["pool_mult"],
                            head_mode=c["head_mode"], score_mode=c["score_mode"])
         log("  stream", s, "fallbacks", out["list_stats"][s, :, 1].tolist(), rep)
+
+
+def _medium_case(rng, i):
+    G = int(rng.choice([1, 2, 4, 7, 8, 16]))
+    Hk = int(rng.choice([1, 2] if G == 16 else [1, 2, 4]))
+    c = dict(L=int(rng.choice([1, 2])), Hk=Hk, G=G, d=int(rng.choice([64, 128])), streams=[],
+             top_k=int(rng.integers(16, 1025)), n_select=int(rng.integers(1, 33)), pool_mult=int(rng.choice([1, 2, 4])),
+             head_mode=int(rng.integers(0, 2)), score_mode=int(rng.integers(0, 2)))
+    for s in range(int(rng.integers(1, 5))):
+        c["streams"].append(dict(F=int(rng.integers(300, 3001)), T=int(rng.integers(2, 13)),
+                                 nq=int(rng.integers(1, 17)), recent=int(rng.integers(0, 6)), seed=50000 + 100 * i + s))
+    return c
+
+
+@pytest.mark.parametrize("i", range(8))
+def test_random_medium_batch_staged(i):
+    """Longer streams (300 to 3,000 frames, up to four of them), k up to 1,024
+    (candidate lists beyond the 4,096 slots the selection holds in registers),
+    frame budgets up to 32 and groups up to 16 query heads."""
+    import paper_2609_02780_amd as P
+    from parity import staged_check
+    c = _medium_case(np.random.default_rng([2609, 7, i]), i)
+    log("medium case", i, {k: v for k, v in c.items() if k != "streams"}, "streams",
+        [(x["F"], x["T"], x["nq"], x["recent"]) for x in c["streams"]])
+    gs, os_, qs = [], [], []
+    for x in c["streams"]:
+        cfg = W.Config(f"randm{i}", c["L"], c["Hk"] * c["G"], c["Hk"], c["d"], x["T"], x["nq"], c["top_k"],
+                       c["n_select"], n_frames=x["F"], n_planted=4)
+        spec = W.stream_specs(cfg)[0]
+        q, keys = W.make_stream(cfg, spec, seed=x["seed"])
+        g = P.ShallowIndex(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, x["F"], x["F"] * x["T"],
+                           x["recent"])
+        g.append([_dev(k) for k in keys], x["F"], x["T"])
+        o = O.Index(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, x["recent"])
+        o.append(keys, x["F"], x["T"])
+        gs.append(g)
+        os_.append(o)
+        qs.append(q)
+    r = P.Retriever(gs, c["top_k"], c["n_select"], c["pool_mult"], c["head_mode"], c["score_mode"])
+    out = r.debug([[_dev(a) for a in q] for q in qs])
+    for s in range(len(gs)):
+        rep = staged_check(os_[s], qs[s], out, s, c["top_k"], c["n_select"], c["pool_mult"],
+                           head_mode=c["head_mode"], score_mode=c["score_mode"])
+        st = out["list_stats"][s]
+        log("  stream", s, "candidates", int(st[:, 0].min()), "..", int(st[:, 0].max()),
+            "fallbacks", np.bincount(st[:, 1], minlength=3).tolist(), rep)
