@@ -643,6 +643,10 @@ __device__ __forceinline__ int lane_xor32(int x) {
 // blocks per CU).
 constexpr int kStage = 64;
 
+// Query heads a probability streaming pass can hold (H_kv * d <= 512 and
+// G <= 16: H_q <= 128).
+constexpr int kHpHeads = 128;
+
 __device__ __forceinline__ void stage_flush(const ScoreArgs& a, int list, bool colv, int col, int kg,
                                             const uint64_t* st, int& lc) {
   __builtin_amdgcn_wave_barrier();
@@ -1360,6 +1364,11 @@ __global__ __launch_bounds__(256) void k_stream_hp(ScoreArgs a) {
   constexpr int CPR = D / 8, TCH = 16 * CPR, NI = TCH / kWave, KS = D / 32;
   __shared__ u32x4 tiles[4][TCH];
   __shared__ uint64_t stage[4 * kStage];   // column 0 only
+  __shared__ unsigned long long fl_below[kHpHeads];   // the block's fixed-point sums per head
+  __shared__ uint32_t fl_lmax;
+  for (int h = threadIdx.x; h < kHpHeads; h += blockDim.x) fl_below[h] = 0;
+  if (threadIdx.x == 0) fl_lmax = 0;
+  __syncthreads();
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
@@ -1378,7 +1387,8 @@ __global__ __launch_bounds__(256) void k_stream_hp(ScoreArgs a) {
     const int t1 = (int)min<int64_t>(nt, tb + (wr.b1 - T));
     const int t0 = first_tile(wr, T, tb);
     T += t1 - tb;
-    if (t0 >= t1) continue;
+    // (every wave of the block takes part in the segment's sums, with or
+    // without tiles of its own)
     const int n = a.n[s];
     const bool colv = col == 0;
     const int list = s * a.NL + l;
@@ -1456,11 +1466,33 @@ __global__ __launch_bounds__(256) void k_stream_hp(ScoreArgs a) {
       }
     }
     if (__any(lc > 0)) stage_flush(a, list, colv, col, kg, st, lc);
+    // The waves of a group end a segment together: each wave rounds its
+    // per-head sums to fixed point as below_flush does, the block adds the
+    // integers in LDS and makes one atomic per head (and one for the
+    // largest estimate left out), not one per wave.
 #pragma unroll
-    for (int g = 0; g < HK; ++g)
-      below_flush(&a.below[hb + min(g * a.G + col, a.Hq - 1)], col < a.G, kg, bsum[g], bscale);
+    for (int g = 0; g < HK; ++g) {
+      double x = bsum[g];
+      x += __shfl_xor(x, 16);
+      x += __shfl_xor(x, 32);
+      if (kg == 0 && col < a.G && x > 0.0)
+        atomicAdd(&fl_below[g * a.G + col], (unsigned long long)llrint(ldexp(x * bscale, kBelowExp)));
+    }
     for (int o = 32; o > 0; o >>= 1) lmax = max(lmax, (uint32_t)__shfl_xor((int)lmax, o));
-    if (lane == 0 && lmax > 0) atomicMax(&a.left_max[list], lmax);
+    if (lane == 0 && lmax > 0) atomicMax(&fl_lmax, lmax);
+    __syncthreads();
+    if (wave == 0) {
+      for (int h = lane; h < a.Hq; h += kWave) {
+        const unsigned long long b = fl_below[h];
+        if (b) atomicAdd(reinterpret_cast<unsigned long long*>(&a.below[hb + h]), b);
+        fl_below[h] = 0;
+      }
+      if (lane == 0) {
+        if (fl_lmax > 0) atomicMax(&a.left_max[list], fl_lmax);
+        fl_lmax = 0;
+      }
+    }
+    __syncthreads();
   }
 }
 
