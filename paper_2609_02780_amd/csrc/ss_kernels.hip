@@ -720,11 +720,13 @@ __device__ __forceinline__ void below_flush(uint64_t* dst, bool colv, int kg, do
 // counter queue one behind the other at the memory side (returning or not:
 // with one per wave, C3's pass took 6 us and C4's 5 us longer than with none).
 // One per (block, column) shortens that queue fourfold: per call, C3 56.4 ->
-// 51.6 us, C2 110.9 -> 109.2 us, C4 449.8 -> 446.2 us, C5 2,000 -> 1,995 us;
-// the head-mode-1 passes, with one list per layer, did not gain.  Each wave's
-// keys go to the block's slot range after those of the lower waves.  With `prob`, each wave's exp sum below the cut-off is rounded
-// to fixed point as in below_flush and the block adds the integers, so the
-// total does not depend on how the sums are grouped.
+// 51.6 us, C2 110.9 -> 109.2 us, C4 449.8 -> 446.2 us, C5 2,000 -> 1,995 us
+// (the head-mean pass, with one list per layer and few keys per wave, did not
+// gain; the probability pass groups its per-head sums the same way).  Each
+// wave's keys go to the block's slot range after those of the lower waves.
+// With `prob`, each wave's exp sum below the cut-off is rounded to fixed point
+// as in below_flush and the block adds the integers, so the total does not
+// depend on how the sums are grouped.
 template <int NW>
 struct FlushShared {
   uint32_t cnt[NW][16];          // staged keys per (wave, column)
