@@ -1149,6 +1149,7 @@ constexpr int kPsTiles = 32;   // sample tiles per block
 struct PsArgs {
   int blk_base[kMaxStreams + 1];   // first block of each stream
   int spg[kMaxStreams];            // blocks per (layer, KV head) group of each stream
+  int xcd_map;                     // block b plays (b mod 8) * (blocks / 8) + b / 8
 };
 
 template <int D>
@@ -1164,8 +1165,13 @@ __global__ __launch_bounds__(8 * D) void k_prep_sample(PrepArgs pa, ScoreArgs a,
   __shared__ u32x4 bsh[2 * KS * kWave];
   __shared__ float sout[kMaxGroup][kPsTiles * kTile];   // the block's scores, written out by whole lines
   int s = 0;
-  while ((int)blockIdx.x >= ps.blk_base[s + 1]) ++s;
-  const int rem = (int)blockIdx.x - ps.blk_base[s];
+  // On a 256-CU device block b runs on XCD b mod 8: with xcd_map each XCD
+  // takes a contiguous run of the group-major block order, so the slices of
+  // a group mostly share one XCD and its L2 serves their query reads after
+  // the first.
+  const int vb = ps.xcd_map ? (int)(blockIdx.x % 8) * (int)(gridDim.x / 8) + (int)(blockIdx.x / 8) : (int)blockIdx.x;
+  while (vb >= ps.blk_base[s + 1]) ++s;
+  const int rem = vb - ps.blk_base[s];
   const int lg = rem / ps.spg[s], slice = rem - lg * ps.spg[s];
   const int l = lg / a.Hk, g = lg - l * a.Hk;
   const int lane = threadIdx.x & (kWave - 1);
@@ -4426,6 +4432,7 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   // 58.5 -> 56.3 us, m = 262) but not at the 1-hour index's 3,216 rows
   // (450.2 -> 456.3 us)
   const bool pt = D == 128 && p.head_mode == 0 && !p.hm_prob && pairs <= 128 && lists <= cus && p.m_max <= 2048;
+  ps.xcd_map = cus == 256 && ps_blocks % 8 == 0;
   const bool fused = !pt && prep_hm == 0 && pairs <= 128 && ps_blocks <= cus;
   PrepArgs pa_fused{};
   for (int first = 0; first < pairs; first += 128) {
