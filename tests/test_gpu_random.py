@@ -120,3 +120,46 @@ def test_random_medium_batch_staged(i):
         st = out["list_stats"][s]
         log("  stream", s, "candidates", int(st[:, 0].min()), "..", int(st[:, 0].max()),
             "fallbacks", np.bincount(st[:, 1], minlength=3).tolist(), rep)
+
+
+@pytest.mark.parametrize("i", range(8))
+def test_random_compressed_batch_staged(i):
+    """Ragged batches that mix streams appended with per-frame k-means (random
+    centroid counts and rounds) and plain streams: retrieval staged against the
+    oracle over the stored centroids, with descriptors from the raw keys."""
+    import paper_2609_02780_amd as P
+    from parity import staged_check
+    rng = np.random.default_rng([2609, 11, i])
+    c = _case(rng, 2000 + i)
+    comp = [bool(rng.integers(0, 2)) for _ in c["streams"]]
+    log("compressed case", i, {k: v for k, v in c.items() if k != "streams"}, "streams",
+        [(x["F"], x["T"], x["nq"], x["recent"], cp) for x, cp in zip(c["streams"], comp)])
+    gs, os_, qs = [], [], []
+    for x, cp in zip(c["streams"], comp):
+        F, T = x["F"], x["T"]
+        cfg = W.Config(f"randc{i}", c["L"], c["Hk"] * c["G"], c["Hk"], c["d"], T, x["nq"], c["top_k"],
+                       c["n_select"], n_frames=F, n_planted=min(2, F // 4))
+        spec = W.stream_specs(cfg)[0]
+        q, keys = W.make_stream(cfg, spec, seed=x["seed"])
+        o = O.Index(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, x["recent"])
+        if cp:
+            nc = int(rng.integers(1, T + 1))
+            compress = (nc, int(rng.integers(1, 6)))
+            g = P.ShallowIndex(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, F, F * nc, x["recent"])
+            g.append([_dev(k) for k in keys], F, T, compress)
+            ex = g.export()
+            desc = [O.descriptor(O.decode_bf16(keys[-1][:, f * T:(f + 1) * T, :])) for f in range(F)]
+            o.append_stored([ex["rows"][l] for l in range(cfg.n_layers)], [nc] * F, desc)
+        else:
+            g = P.ShallowIndex(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, F, F * T, x["recent"])
+            g.append([_dev(k) for k in keys], F, T)
+            o.append(keys, F, T)
+        gs.append(g)
+        os_.append(o)
+        qs.append(q)
+    r = P.Retriever(gs, c["top_k"], c["n_select"], c["pool_mult"], c["head_mode"], c["score_mode"])
+    out = r.debug([[_dev(a) for a in q] for q in qs])
+    for s in range(len(gs)):
+        rep = staged_check(os_[s], qs[s], out, s, c["top_k"], c["n_select"], c["pool_mult"],
+                           head_mode=c["head_mode"], score_mode=c["score_mode"])
+        log("  stream", s, "fallbacks", out["list_stats"][s, :, 1].tolist(), rep)
