@@ -163,3 +163,39 @@ def test_random_compressed_batch_staged(i):
         rep = staged_check(os_[s], qs[s], out, s, c["top_k"], c["n_select"], c["pool_mult"],
                            head_mode=c["head_mode"], score_mode=c["score_mode"])
         log("  stream", s, "fallbacks", out["list_stats"][s, :, 1].tolist(), rep)
+
+
+@pytest.mark.parametrize("i", range(8))
+def test_random_pooled_ranker(i):
+    """The pooled Q-K ranker over seeded random ragged batches (the head shapes
+    and per-stream lengths, tokens, query tokens and recent windows of the
+    cases above; K from 1 to 64), each stream checked as in
+    tests/test_gpu_pooled.py."""
+    import paper_2609_02780_amd as P
+    from test_gpu_pooled import check
+    rng = np.random.default_rng([2609, 13, i])
+    c = _case(rng, 3000 + i)
+    K = int(rng.integers(1, 65))
+    log("pooled case", i, {k: v for k, v in c.items() if k != "streams"}, "K", K, "streams",
+        [(x["F"], x["T"], x["nq"], x["recent"]) for x in c["streams"]])
+    gs, os_, qs = [], [], []
+    for x in c["streams"]:
+        cfg = W.Config(f"randp{i}", c["L"], c["Hk"] * c["G"], c["Hk"], c["d"], x["T"], x["nq"], c["top_k"],
+                       c["n_select"], n_frames=x["F"], n_planted=min(2, x["F"] // 4))
+        spec = W.stream_specs(cfg)[0]
+        q, keys = W.make_stream(cfg, spec, seed=x["seed"])
+        g = P.ShallowIndex(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, x["F"], x["F"] * x["T"],
+                           x["recent"])
+        g.append([_dev(k) for k in keys], x["F"], x["T"])
+        o = O.Index(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, x["recent"])
+        o.append(keys, x["F"], x["T"])
+        gs.append(g)
+        os_.append(o)
+        qs.append(q)
+    r = P.PooledRanker(gs, K)
+    ids, sc, n = r([[_dev(a) for a in q] for q in qs])
+    torch.cuda.synchronize()
+    ids, sc, n = ids.cpu().numpy(), sc.cpu().numpy(), n.cpu().numpy()
+    for s in range(len(gs)):
+        near = check(os_[s], qs[s], ids[s], sc[s], int(n[s]), K)
+        log("  stream", s, "near ties", near)
