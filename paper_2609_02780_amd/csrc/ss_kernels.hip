@@ -1243,12 +1243,40 @@ __global__ __launch_bounds__(8 * D) void k_prep_sample(PrepArgs pa, ScoreArgs a,
 
 // Head mode 1, sample and exact-recompute roles: one layer per item; every
 // tile's rows are read for each KV head in the MFMA A layout.
+// One item (stream, layer, chunk of units) of k_score_hm with the layer's B
+// operand b in registers.  Called by whole waves of a block.
+template <int D, int KIND>
+__device__ __forceinline__ void score_hm_item(const ScoreArgs& a, int s, int l, int u0, int u1, bool wr,
+                                              const u32x4 (&b)[D / 32]) {
+  constexpr int KS = D / 32;
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
+  const bool colv = col == 0;
+  const int list = s * a.NL + l;
+  const size_t gstride = (size_t)a.stride[s] * D;
+  const uint16_t* base = a.keys[s] + (size_t)l * a.Hk * gstride + 8 * kg;
+  const int ntiles = (u1 - u0 + kTile - 1) / kTile;
+  for (int t = wave; t < ntiles; t += nw) {
+    const int u = u0 + t * kTile + rl;
+    const bool ok = u < u1;
+    const int64_t row = ok ? unit_row<KIND>(a, s, u) : 0;
+    f32x4 v = {0.f, 0.f, 0.f, 0.f};
+    for (int g = 0; g < a.Hk; ++g) {
+      const uint16_t* p = base + g * gstride + row * D;
+      u32x4 A[KS];
+#pragma unroll
+      for (int i = 0; i < KS; ++i) A[i] = ok ? ld_nt(p + 32 * i) : u32x4{0, 0, 0, 0};
+      hm_accumulate<KS>(A, b, g, v);
+    }
+    emit<KIND>(a, s, list, colv, wr, u0 + t * kTile, u1, hm_finish(v), kg);
+  }
+}
+
 template <int D, int KIND>
 __global__ __launch_bounds__(256) void k_score_hm(ScoreArgs a) {
   static_assert(KIND != K_STREAM, "head-mode-1 streaming runs in k_stream_hm");
   constexpr int KS = D / 32;
-  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  const int col = lane & 15, kg = lane >> 4, rl = lane & 15;
+  const int lane = threadIdx.x & (kWave - 1), col = lane & 15;
   for (int item = blockIdx.x; item < a.total_items; item += gridDim.x) {
     int s = 0;
     while (item >= a.item_base[s + 1]) ++s;
@@ -1257,32 +1285,129 @@ __global__ __launch_bounds__(256) void k_score_hm(ScoreArgs a) {
     const int nch = (units + a.chunk - 1) / a.chunk;
     const int chunk = rem % nch, l = rem / nch;
     const int u0 = chunk * a.chunk, u1 = min(units, u0 + a.chunk);
-    const bool colv = col == 0;
-    const int list = s * a.NL + l;
     bool wr = false;
     if (KIND == K_FULL) {
-      wr = colv && l == a.only_list;
+      wr = col == 0 && l == a.only_list;
       if (!__any(wr)) continue;
     }
     u32x4 b[KS];
     hm_load_b<KS>(a.qB + (size_t)(s * a.L + l) * a.Hk * (2 * KS * kWave), a.Hk, b);
-    const size_t gstride = (size_t)a.stride[s] * D;
-    const uint16_t* base = a.keys[s] + (size_t)l * a.Hk * gstride + 8 * kg;
-    const int ntiles = (u1 - u0 + kTile - 1) / kTile;
-    for (int t = wave; t < ntiles; t += nw) {
-      const int u = u0 + t * kTile + rl;
-      const bool ok = u < u1;
-      const int64_t row = ok ? unit_row<KIND>(a, s, u) : 0;
-      f32x4 v = {0.f, 0.f, 0.f, 0.f};
-      for (int g = 0; g < a.Hk; ++g) {
-        const uint16_t* p = base + g * gstride + row * D;
-        u32x4 A[KS];
+    score_hm_item<D, KIND>(a, s, l, u0, u1, wr, b);
+  }
+}
+
+// Head mode 1, the query prep fused into the sample pass (k_score_hm_prep),
+// for batches whose query-head groups are small (G * n_q <= kHmPrepTerms):
+// every item's block forms its layer's head-mean B columns itself, the same
+// sums in k_prep's order (token groups j mod 4, heads outer, tokens inner, the
+// four groups added in order; the column's L1 norm by the same butterfly);
+// the block of the layer's first chunk also writes the B tiles and the column
+// norms for the later kernels, which read the same bits as the sample.
+// At the paper's settings (one query token) this takes a kernel and its
+// boundary off the chain before the streaming pass.
+constexpr int kHmPrepTerms = 64;
+
+template <int D>
+__device__ __forceinline__ void hm_prep_block(const PrepArgs& pa, int s, int l, int Hk, int G,
+                                              u32x4 (*colB)[2][D / 32][4], float (*l1p)[16], bool publish) {
+  constexpr int KS = D / 32, NE = D / 8;
+  const int pair = s * pa.L + l;
+  const uint16_t* q = pa.q[pair];
+  const int nq = pa.nq[s];
+  const float scale = pa.qscale[s];
+  // thread (g, ec): dims 8 ec .. 8 ec + 7 of KV head g's column
+  for (int c = threadIdx.x; c < Hk * NE; c += blockDim.x) {
+    const int g = c / NE, ec = c - g * NE;
+    float acc[4][8];
 #pragma unroll
-        for (int i = 0; i < KS; ++i) A[i] = ok ? ld_nt(p + 32 * i) : u32x4{0, 0, 0, 0};
-        hm_accumulate<KS>(A, b, g, v);
+    for (int tg = 0; tg < 4; ++tg)
+#pragma unroll
+      for (int w = 0; w < 8; ++w) acc[tg][w] = 0.f;
+#pragma unroll
+    for (int tg = 0; tg < 4; ++tg) {
+      for (int h = g * G; h < g * G + G; ++h) {
+        for (int j = tg; j < nq; j += 4) {
+          const u32x4 v = *reinterpret_cast<const u32x4*>(q + ((size_t)h * nq + j) * D + 8 * ec);
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            acc[tg][2 * w] += bf16_lo(v[w]);
+            acc[tg][2 * w + 1] += bf16_hi(v[w]);
+          }
+        }
       }
-      emit<KIND>(a, s, list, colv, wr, u0 + t * kTile, u1, hm_finish(v), kg);
     }
+    u32x4 hi, lo;
+    float l1 = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      float y0 = acc[0][2 * w], y1 = acc[0][2 * w + 1];
+#pragma unroll
+      for (int tg = 1; tg < 4; ++tg) { y0 += acc[tg][2 * w]; y1 += acc[tg][2 * w + 1]; }
+      const float x0 = y0 * scale, x1 = y1 * scale;
+      l1 += fabsf(x0) + fabsf(x1);
+      const uint16_t a0 = bf16_rne(x0), a1 = bf16_rne(x1);
+      const uint16_t b0 = bf16_rne(x0 - __uint_as_float((uint32_t)a0 << 16));
+      const uint16_t b1 = bf16_rne(x1 - __uint_as_float((uint32_t)a1 << 16));
+      hi[w] = (uint32_t)a0 | ((uint32_t)a1 << 16);
+      lo[w] = (uint32_t)b0 | ((uint32_t)b1 << 16);
+    }
+    const int i = ec >> 2, kg = ec & 3;
+    colB[g][0][i][kg] = hi;
+    colB[g][1][i][kg] = lo;
+    l1p[g][ec] = l1;
+  }
+  __syncthreads();
+  if (!publish) return;
+  // the whole B tiles (columns 1..15 zero, as k_prep leaves them in head mode 1)
+  u32x4* out = pa.qB + (size_t)pair * Hk * (2 * KS * kWave);
+  for (int e = threadIdx.x; e < Hk * 2 * KS * kWave; e += blockDim.x) {
+    const int g = e / (2 * KS * kWave), r = e - g * (2 * KS * kWave);
+    const int part = r / (KS * kWave), r2 = r - part * (KS * kWave), i = r2 / kWave, ln = r2 - i * kWave;
+    out[e] = (ln & 15) == 0 ? colB[g][part][i][ln >> 4] : u32x4{0, 0, 0, 0};
+  }
+  // the column norm: k_prep's butterfly over the NE chunks (o = NE / 2 .. 1)
+  if (pa.qcol)
+    for (int e = threadIdx.x; e < Hk * 16; e += blockDim.x) {
+      const int g = e >> 4, cl = e & 15;
+      float nrm = 0.f;
+      if (cl == 0) {
+        float v[NE];
+#pragma unroll
+        for (int k = 0; k < NE; ++k) v[k] = l1p[g][k];
+#pragma unroll
+        for (int o = NE / 2; o > 0; o >>= 1) {
+          float w[NE];
+#pragma unroll
+          for (int k = 0; k < NE; ++k) w[k] = v[k] + v[k ^ o];
+#pragma unroll
+          for (int k = 0; k < NE; ++k) v[k] = w[k];
+        }
+        nrm = v[0];
+      }
+      pa.qcol[((size_t)pair * Hk + g) * 16 + cl] = nrm;
+    }
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void k_score_hm_prep(PrepArgs pa, ScoreArgs a) {
+  constexpr int KS = D / 32;
+  __shared__ u32x4 colB[8][2][KS][4];
+  __shared__ float l1p[8][16];
+  const int lane = threadIdx.x & (kWave - 1), c = lane & 15, kg = lane >> 4, g = c & 7;
+  for (int item = blockIdx.x; item < a.total_items; item += gridDim.x) {
+    int s = 0;
+    while (item >= a.item_base[s + 1]) ++s;
+    const int rem = item - a.item_base[s];
+    const int units = a.units[s];
+    const int nch = (units + a.chunk - 1) / a.chunk;
+    const int chunk = rem % nch, l = rem / nch;
+    const int u0 = chunk * a.chunk, u1 = min(units, u0 + a.chunk);
+    __syncthreads();   // the previous item's B columns are read no more
+    hm_prep_block<D>(pa, s, l, a.Hk, a.G, colB, l1p, chunk == 0);
+    u32x4 b[KS];
+#pragma unroll
+    for (int i = 0; i < KS; ++i) b[i] = g < a.Hk ? colB[g][c < 8 ? 0 : 1][i][kg] : u32x4{0, 0, 0, 0};
+    score_hm_item<D, K_SAMPLE>(a, s, l, u0, u1, false, b);
   }
 }
 
@@ -4434,6 +4559,9 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
   const bool pt = D == 128 && p.head_mode == 0 && !p.hm_prob && pairs <= 128 && lists <= cus && p.m_max <= 2048;
   ps.xcd_map = cus == 256 && ps_blocks % 8 == 0;
   const bool fused = !pt && prep_hm == 0 && pairs <= 128 && ps_blocks <= cus;
+  int nq_max = 0;
+  for (int s = 0; s < p.S; ++s) nq_max = std::max(nq_max, p.st[s].nq);
+  const bool hm_prep = prep_hm == 1 && pairs <= 128 && p.Hk <= 8 && p.G * nq_max <= kHmPrepTerms;
   PrepArgs pa_fused{};
   for (int first = 0; first < pairs; first += 128) {
     PrepArgs a{};
@@ -4446,7 +4574,7 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
     for (int s = 0; s < p.S; ++s) { a.nq[s] = p.st[s].nq; a.qscale[s] = p.st[s].qscale; }
     a.qB = reinterpret_cast<u32x4*>(p.qB);
     a.qcol = p.qcol;
-    if (fused || pt)
+    if (fused || pt || hm_prep)
       pa_fused = a;
     else
       hipLaunchKernelGGL(k_prep<D>, dim3(cnt * p.Hk), dim3(8 * D), 0, st, a);
@@ -4504,6 +4632,10 @@ hipError_t retrieve_impl(RetrievePlan& p, hipStream_t st) {
       const int grid = (int)std::min<int64_t>(stream_grid<D, 0>(), std::max<int64_t>(1, tiles / 4));
       hipLaunchKernelGGL(k_sample<D>, dim3(grid), dim3(256), 0, st, a);
     }
+  } else if (hm_prep) {
+    ScoreArgs a = make_score_args(p, K_SAMPLE);
+    if (a.total_items > 0)
+      hipLaunchKernelGGL(k_score_hm_prep<D>, dim3(std::min(a.total_items, 4096)), dim3(256), 0, st, pa_fused, a);
   } else {
     launch_score<D, K_SAMPLE>(make_score_args(p, K_SAMPLE), p.head_mode, 4096, st);
   }
