@@ -199,3 +199,27 @@ def test_random_pooled_ranker(i):
     for s in range(len(gs)):
         near = check(os_[s], qs[s], ids[s], sc[s], int(n[s]), K)
         log("  stream", s, "near ties", near)
+
+
+@pytest.mark.parametrize("head_mode,score_mode", [(0, 0), (0, 1), (1, 0), (1, 1)])
+def test_repeat_bitwise_equal_all_modes(head_mode, score_mode):
+    """Three calls on the same inputs return bitwise-identical outputs in both
+    head modes and both readings: a two-layer, 2,000-frame stream (392,000 rows
+    per (layer, KV head), hundreds of streaming blocks), where the integer
+    atomics of the candidate counts, the sums below the cut-off and the
+    per-frame votes and mass land in a different order on every call."""
+    import paper_2609_02780_amd as P
+    F, T = 2000, 196
+    cfg = W.Config("repeat", 2, 28, 4, 128, T, 8, 256, 16, n_frames=F, n_planted=8)
+    spec = W.stream_specs(cfg)[0]
+    q, keys = W.make_stream(cfg, spec, seed=77)
+    g = P.ShallowIndex(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, F, F * T, 0)
+    g.append([_dev(k) for k in keys], F, T)
+    r = P.Retriever([g], cfg.top_k, cfg.n_select, 4, head_mode, score_mode)
+    qd = [[_dev(a) for a in q]]
+    outs = [r.debug(qd) for _ in range(3)]
+    for o in outs[1:]:
+        assert set(o) == set(outs[0])
+        for k in outs[0]:
+            np.testing.assert_array_equal(np.asarray(outs[0][k]), np.asarray(o[k]), err_msg=k)
+    log("modes", head_mode, score_mode, "fallbacks", np.bincount(outs[0]["list_stats"][0, :, 1], minlength=3).tolist())
